@@ -1,0 +1,327 @@
+"""fp64 CPU oracle for the Hessian-free curvature path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this module: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it.  It shares no code with the HIP
+library (no kernels, headers, helpers, tables or pre/post-processing); the
+only thing both sides consume is the seeded input generator, which holds none
+of the method's arithmetic.
+
+What is computed, and where it comes from
+-----------------------------------------
+Paper: He, Mudigere, Smelyanskiy, Takac, "Distributed Hessian-Free
+Optimization for Deep Neural Network" (arXiv 1606.00511).
+
+* The objective f(theta) and its gradient g_k = grad f(theta_k) (Alg. 1,
+  first step; Alg. 2, gradient and reduce steps): a fully connected network
+  with sigmoid / tanh / ReLU hidden units and a softmax cross-entropy output,
+  averaged over the minibatch.  The paper gives the network only by its
+  shapes and class counts (Sec. 3); the softmax cross-entropy objective and
+  mean-over-batch are the readings recorded in the design notes.
+* The exact Hessian-vector product H(theta) v.  The paper (Sec. 2.1, the
+  paragraph after Alg. 1) says it is obtained by a forward-backward pass with
+  the R-operator at about twice the cost of a gradient, without writing the
+  equations.  Here it is the directional derivative of the gradient,
+  R{grad f} = d/de grad f(theta + e v) at e = 0, carried through every step
+  of backpropagation (forward-mode differentiation of the gradient program).
+* The Gauss-Newton product G v (same paragraph): G = J^T H_L J, where J is
+  the Jacobian of the logits with respect to theta and H_L the Hessian of the
+  batch-mean cross-entropy with respect to the logits.  It is positive
+  semi-definite.
+* CG-Minimize on the damped operator B_k(d) = H d + lambda d (Alg. 1, steps
+  3-4) minimising the quadratic model m_k (Sec. 2.1, eq. (1)), stopping when a
+  conjugate direction p has p^T B_k p < 0 and returning the current iterate,
+  or -g_k when that happens at the first iteration (Sec. 2.1, text after
+  eq. (1)); the negative-curvature direction is oriented as
+  d~ = -sgn(g^T d) d with sgn(0) = +1 (Sec. 2.2); the iteration count is a
+  fixed budget (Sec. 2.2).  The CG recurrences are the textbook linear CG
+  (Nocedal & Wright, cited in Sec. 1 for line-search Newton-CG).
+
+Readings where the paper is silent (each also listed in the design notes):
+mean over the batch; biases present; ReLU'(0) = 0; detection on B_k with
+kappa <= 0 (the paper writes "< 0"); x_0 = 0; a relative-residual stop that
+is off by default.
+
+Parity pins
+-----------
+Every function here is pinned by ``tests/test_oracle_pins.py`` against things
+other than itself: ln C at zero weights, finite differences of the loss,
+brute-force Hessians from second differences, symmetry, PSD-ness, the L = 1
+multinomial-logistic closed form, label independence of G v, hand-computed
+CG cases, and exact n-step convergence of CG against ``numpy.linalg.solve``.
+"""
+
+import numpy as np
+
+ACTIVATIONS = ("sigmoid", "tanh", "relu")
+
+
+# ---------------------------------------------------------------- parameters
+def layer_sizes(dims):
+    """(d_out, d_in) for every weight layer l = 1..L."""
+    return [(int(dims[l]), int(dims[l - 1])) for l in range(1, len(dims))]
+
+
+def num_params(dims):
+    """n = sum_l d_l (d_{l-1} + 1): W_l then b_l for every layer."""
+    return sum(o * i + o for o, i in layer_sizes(dims))
+
+
+def unpack(theta, dims):
+    """Split the flat parameter vector into [(W_l, b_l)].
+
+    Layout: for l = 1..L, W_l row-major (d_l x d_{l-1}) followed by b_l (d_l).
+    """
+    theta = np.asarray(theta, dtype=np.float64)
+    out, off = [], 0
+    for o, i in layer_sizes(dims):
+        W = theta[off:off + o * i].reshape(o, i)
+        off += o * i
+        b = theta[off:off + o]
+        off += o
+        out.append((W, b))
+    assert off == theta.size, "theta length does not match dims"
+    return out
+
+
+def pack(layers):
+    """Inverse of ``unpack``."""
+    parts = []
+    for W, b in layers:
+        parts.append(np.asarray(W, dtype=np.float64).ravel())
+        parts.append(np.asarray(b, dtype=np.float64).ravel())
+    return np.concatenate(parts)
+
+
+# --------------------------------------------------------------- activations
+def phi(act, z):
+    """Hidden activation a = phi(z)."""
+    if act == "sigmoid":
+        return 1.0 / (1.0 + np.exp(-z))
+    if act == "tanh":
+        return np.tanh(z)
+    if act == "relu":
+        return np.maximum(z, 0.0)
+    raise ValueError(act)
+
+
+def dphi(act, z):
+    """phi'(z), written directly from the definition of each activation."""
+    if act == "sigmoid":
+        s = 1.0 / (1.0 + np.exp(-z))
+        return s * (1.0 - s)
+    if act == "tanh":
+        t = np.tanh(z)
+        return 1.0 - t * t
+    if act == "relu":
+        return (z > 0.0).astype(np.float64)     # reading: ReLU'(0) = 0
+    raise ValueError(act)
+
+
+def d2phi(act, z):
+    """phi''(z)."""
+    if act == "sigmoid":
+        s = 1.0 / (1.0 + np.exp(-z))
+        return s * (1.0 - s) * (1.0 - 2.0 * s)
+    if act == "tanh":
+        t = np.tanh(z)
+        return -2.0 * t * (1.0 - t * t)
+    if act == "relu":
+        return np.zeros_like(z)
+    raise ValueError(act)
+
+
+# ---------------------------------------------------------------- the network
+def forward(dims, act, theta, X):
+    """Pre-activations Z_l and activations A_l (A_0 = X, A_L unused).
+
+    Z_l = A_{l-1} W_l^T + b_l;  A_l = phi(Z_l) for hidden layers; Z_L are the
+    logits of the softmax output.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    layers = unpack(theta, dims)
+    A = [X]
+    Z = []
+    for l, (W, b) in enumerate(layers, start=1):
+        z = A[-1] @ W.T + b
+        Z.append(z)
+        if l < len(layers):
+            A.append(phi(act, z))
+    return Z, A
+
+
+def softmax(z):
+    """Row softmax with the usual max shift."""
+    m = z.max(axis=1, keepdims=True)
+    e = np.exp(z - m)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def loss(dims, act, theta, X, y):
+    """f(theta) = (1/B) sum_i [logsumexp(z_i) - z_{i, y_i}]."""
+    Z, _ = forward(dims, act, theta, X)
+    z = Z[-1]
+    y = np.asarray(y, dtype=np.int64)
+    m = z.max(axis=1)
+    lse = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+    return float(np.mean(lse - z[np.arange(z.shape[0]), y]))
+
+
+def loss_grad(dims, act, theta, X, y):
+    """(f, g) with g = grad f by backpropagation (Alg. 1 step 1; Alg. 2)."""
+    layers = unpack(theta, dims)
+    Z, A = forward(dims, act, theta, X)
+    B = Z[-1].shape[0]
+    y = np.asarray(y, dtype=np.int64)
+    P = softmax(Z[-1])
+    Y = np.zeros_like(P)
+    Y[np.arange(B), y] = 1.0
+    f = loss(dims, act, theta, X, y)
+    delta = (P - Y) / B                               # df/dZ_L
+    grads = [None] * len(layers)
+    for l in range(len(layers), 0, -1):               # l = L .. 1
+        W, _ = layers[l - 1]
+        grads[l - 1] = (delta.T @ A[l - 1], delta.sum(axis=0))
+        if l > 1:
+            delta = (delta @ W) * dphi(act, Z[l - 2])  # df/dZ_{l-1}
+    return f, pack(grads)
+
+
+def _r_forward(dims, act, theta, v, X):
+    """Directional derivatives RZ_l = d Z_l / de along theta + e v."""
+    layers = unpack(theta, dims)
+    vlayers = unpack(v, dims)
+    Z, A = forward(dims, act, theta, X)
+    RZ, RA = [], [np.zeros_like(A[0])]
+    for l in range(1, len(layers) + 1):
+        W, _ = layers[l - 1]
+        V, c = vlayers[l - 1]
+        rz = A[l - 1] @ V.T + c + RA[l - 1] @ W.T
+        RZ.append(rz)
+        if l < len(layers):
+            RA.append(dphi(act, Z[l - 1]) * rz)
+    return layers, vlayers, Z, A, RZ, RA
+
+
+def hvp(dims, act, theta, X, y, v):
+    """Exact H v by the R-operator: the directional derivative of the
+    backpropagation program of ``loss_grad`` (Sec. 2.1, paragraph after
+    Alg. 1)."""
+    layers, vlayers, Z, A, RZ, RA = _r_forward(dims, act, theta, v, X)
+    B = Z[-1].shape[0]
+    y = np.asarray(y, dtype=np.int64)
+    P = softmax(Z[-1])
+    Y = np.zeros_like(P)
+    Y[np.arange(B), y] = 1.0
+    delta = (P - Y) / B
+    # R{P} = P * (RZ - rowsum(P * RZ)); R{delta_L} = R{P} / B
+    rdelta = P * (RZ[-1] - (P * RZ[-1]).sum(axis=1, keepdims=True)) / B
+    out = [None] * len(layers)
+    for l in range(len(layers), 0, -1):
+        W, _ = layers[l - 1]
+        V, _ = vlayers[l - 1]
+        out[l - 1] = (rdelta.T @ A[l - 1] + delta.T @ RA[l - 1],
+                      rdelta.sum(axis=0))
+        if l > 1:
+            e = delta @ W
+            re = rdelta @ W + delta @ V
+            zp = Z[l - 2]
+            new_delta = e * dphi(act, zp)
+            rdelta = re * dphi(act, zp) + e * d2phi(act, zp) * RZ[l - 2]
+            delta = new_delta
+    return pack(out)
+
+
+def gvp(dims, act, theta, X, v):
+    """Gauss-Newton G v = J^T H_L J v (Sec. 2.1, paragraph after Alg. 1).
+
+    J v is the R-forward pass; H_L is the Hessian of the batch-mean softmax
+    cross-entropy with respect to the logits, (diag p_i - p_i p_i^T) / B per
+    row; J^T is ordinary backpropagation of that vector.  No labels enter.
+    """
+    layers, vlayers, Z, A, RZ, RA = _r_forward(dims, act, theta, v, X)
+    B = Z[-1].shape[0]
+    P = softmax(Z[-1])
+    u = P * (RZ[-1] - (P * RZ[-1]).sum(axis=1, keepdims=True)) / B
+    out = [None] * len(layers)
+    for l in range(len(layers), 0, -1):
+        W, _ = layers[l - 1]
+        out[l - 1] = (u.T @ A[l - 1], u.sum(axis=0))
+        if l > 1:
+            u = (u @ W) * dphi(act, Z[l - 2])
+    return pack(out)
+
+
+def curvature(dims, act, theta, X, y, v, mode):
+    """H v for mode 'hessian', G v for mode 'gauss_newton'."""
+    if mode == "hessian":
+        return hvp(dims, act, theta, X, y, v)
+    if mode == "gauss_newton":
+        return gvp(dims, act, theta, X, v)
+    raise ValueError(mode)
+
+
+# ------------------------------------------------------------------------ CG
+def sgn(x):
+    """sgn(x) = 1 for x >= 0, -1 otherwise (Sec. 2.2)."""
+    return 1.0 if x >= 0.0 else -1.0
+
+
+def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
+    """CG-Minimize(B_k, -g_k) with B_k(d) = A d + lam d (Alg. 1 steps 3-4).
+
+    Minimises m_k(d) = f + g^T d + d^T B_k d / 2 (Sec. 2.1, eq. (1)) from
+    d = 0.  A conjugate direction p with p^T B_k p <= 0 stops the solve: the
+    current iterate is returned, or -g if it happened at the first iteration
+    (Sec. 2.1, after eq. (1)), together with d~ = -sgn(g^T p) p (Sec. 2.2).
+    ``max_iters`` is the fixed iteration budget (Sec. 2.2).
+
+    Returns a dict with step, neg_dir (None if no detection), iters (completed
+    updates of the iterate), products (curvature products evaluated),
+    neg_curv, neg_iter, pBp, pHp, gTd, rr0, rr_final and, if ``record``,
+    the list of per-iteration kappa values and directions.
+    """
+    g = np.asarray(g, dtype=np.float64)
+    x = np.zeros_like(g)
+    r = g.copy()                 # residual of B x + g
+    p = -g
+    rr = float(r @ r)
+    res = dict(step=x, neg_dir=None, iters=0, products=0, neg_curv=0,
+               neg_iter=-1, pBp=0.0, pHp=0.0, gTd=0.0, rr0=rr, rr_final=rr,
+               kappas=[], dirs=[])
+    if rr == 0.0:
+        return res
+    for j in range(max_iters):
+        q = apply_A(p) + lam * p
+        kappa = float(p @ q)
+        if record:
+            res["kappas"].append(kappa)
+            res["dirs"].append(p.copy())
+        res["products"] = j + 1
+        if kappa <= 0.0:
+            d = -sgn(float(g @ p)) * p
+            res.update(step=(-g.copy() if j == 0 else x), neg_dir=d,
+                       iters=j, neg_curv=1, neg_iter=j, pBp=kappa,
+                       pHp=kappa - lam * float(p @ p), gTd=float(g @ d),
+                       rr_final=rr)
+            return res
+        alpha = rr / kappa
+        x = x + alpha * p
+        r = r + alpha * q
+        rr_new = float(r @ r)
+        res.update(step=x, iters=j + 1, rr_final=rr_new)
+        if rel_tol > 0.0 and rr_new <= rel_tol * rel_tol * res["rr0"]:
+            return res
+        beta = rr_new / rr
+        rr = rr_new
+        p = -r + beta * p
+    return res
+
+
+def cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
+               rel_tol=0.0, record=False):
+    """CG-Minimize with the curvature operator of the network on the fixed
+    curvature batch (Xc, yc) (Alg. 2: the product on one minibatch)."""
+    def apply_A(p):
+        return curvature(dims, act, theta, Xc, yc, p, mode)
+    return cg_minimize(apply_A, g, lam, max_iters, rel_tol, record)

@@ -1,0 +1,438 @@
+"""Pins of the fp64 oracle against things other than itself.
+
+Each test checks the oracle against mathematics that does not reuse its
+formulas: closed forms, finite differences of the loss, brute-force
+Hessians, symmetry, PSD-ness, the L = 1 textbook Hessian, hand-computed CG
+cases (tests/golden/) and exact CG convergence against numpy.linalg.solve.
+The mutation tests at the end plant plausible mistakes in the oracle and
+check that a pin catches each one.
+"""
+
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import hf_oracle as O
+from paper_1606_00511_amd import workloads as WL
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+ACTS = ("sigmoid", "tanh", "relu")
+
+
+def read_golden(name):
+    out = {}
+    with open(os.path.join(GOLDEN, name)) as fh:
+        for line in fh:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            k, v = (s.strip() for s in line.split("=", 1))
+            vals = [float(t) for t in v.split()]
+            out[k] = vals if len(vals) > 1 else vals[0]
+    return out
+
+
+def tiny(act, dims=(5, 4, 3, 4), B=7, seed=11):
+    p = WL.make_small(dims, act, B, seed, x_dist="normal", bias_std=0.5)
+    th = p["theta"].astype(np.float64)
+    return p, th
+
+
+def rel(a, b):
+    return float(np.linalg.norm(np.asarray(a) - np.asarray(b)) /
+                 max(np.linalg.norm(np.asarray(b)), 1e-300))
+
+
+# ------------------------------------------------------------------- loss
+@pytest.mark.parametrize("C", [10, 1973])
+def test_loss_at_zero_weights_is_lnC(C):
+    g = read_golden("loss_at_zero_weights.txt")
+    dims = (6, 8, C)
+    p = WL.make_small(dims, "sigmoid", 23, 5)
+    theta = np.zeros(O.num_params(dims))
+    f, grad = O.loss_grad(dims, "sigmoid", theta, p["X"], p["y"])
+    assert f == pytest.approx(g["lnC.%d" % C], rel=0, abs=1e-13)
+    freq = np.bincount(p["y"], minlength=C) / 23.0
+    gb = O.unpack(grad, dims)[-1][1]
+    np.testing.assert_allclose(gb, 1.0 / C - freq, rtol=0, atol=1e-15)
+
+
+def test_loss_single_row_by_hand():
+    # One linear layer, one row: logits z = W x + b, loss = lse(z) - z_y.
+    dims = (2, 3)
+    W = np.array([[1.0, 0.0], [0.0, 2.0], [-1.0, 1.0]])
+    b = np.array([0.5, 0.0, -0.5])
+    theta = O.pack([(W, b)])
+    X = np.array([[1.0, 1.0]])
+    z = np.array([1.5, 2.0, -0.5])
+    expect = math.log(math.exp(1.5) + math.exp(2.0) + math.exp(-0.5)) - 2.0
+    assert O.loss(dims, "relu", theta, X, np.array([1])) == pytest.approx(
+        expect, abs=1e-15)
+    del z
+
+
+# --------------------------------------------------------------- gradient
+@pytest.mark.parametrize("act", ACTS)
+def test_gradient_directional_fd(act):
+    p, th = tiny(act)
+    dims = p["dims"]
+    f, g = O.loss_grad(dims, act, th, p["X"], p["y"])
+    v = p["v"].astype(np.float64)
+    eps = 1e-6
+    fd = (O.loss(dims, act, th + eps * v, p["X"], p["y"]) -
+          O.loss(dims, act, th - eps * v, p["X"], p["y"])) / (2 * eps)
+    assert g @ v == pytest.approx(fd, rel=1e-7)
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_gradient_bruteforce_every_coordinate(act):
+    p, th = tiny(act, dims=(3, 4, 3), B=5)
+    dims = p["dims"]
+    _, g = O.loss_grad(dims, act, th, p["X"], p["y"])
+    eps = 1e-6
+    fd = np.empty_like(th)
+    for i in range(th.size):
+        e = np.zeros_like(th)
+        e[i] = eps
+        fd[i] = (O.loss(dims, act, th + e, p["X"], p["y"]) -
+                 O.loss(dims, act, th - e, p["X"], p["y"])) / (2 * eps)
+    np.testing.assert_allclose(g, fd, rtol=0, atol=1e-8)
+
+
+# --------------------------------------------------------------------- Hv
+@pytest.mark.parametrize("act", ACTS)
+def test_hvp_central_difference_of_gradient(act):
+    p, th = tiny(act, dims=(6, 8, 8, 4), B=20)
+    dims = p["dims"]
+    v = p["v"].astype(np.float64)
+    hv = O.hvp(dims, act, th, p["X"], p["y"], v)
+    eps = 1e-5
+    gp = O.loss_grad(dims, act, th + eps * v, p["X"], p["y"])[1]
+    gm = O.loss_grad(dims, act, th - eps * v, p["X"], p["y"])[1]
+    assert rel(hv, (gp - gm) / (2 * eps)) <= 1e-7
+
+
+def bruteforce_hessian(dims, act, th, X, y, eps=1e-4):
+    """H_ij from second differences of the loss alone."""
+    n = th.size
+    H = np.empty((n, n))
+    f = lambda t: O.loss(dims, act, t, X, y)
+    E = np.eye(n) * eps
+    for i in range(n):
+        for j in range(i, n):
+            h = (f(th + E[i] + E[j]) - f(th + E[i] - E[j]) -
+                 f(th - E[i] + E[j]) + f(th - E[i] - E[j])) / (4 * eps * eps)
+            H[i, j] = H[j, i] = h
+    return H
+
+
+@pytest.mark.parametrize("act", ("sigmoid", "tanh"))
+def test_hvp_columns_match_bruteforce_hessian(act):
+    p, th = tiny(act, dims=(3, 3, 2), B=4, seed=3)
+    dims = p["dims"]
+    n = th.size
+    H = bruteforce_hessian(dims, act, th, p["X"], p["y"])
+    cols = np.stack([O.hvp(dims, act, th, p["X"], p["y"], e)
+                     for e in np.eye(n)], axis=1)
+    assert np.max(np.abs(cols - H)) <= 2e-7
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_hvp_symmetry_and_linearity(act):
+    p, th = tiny(act, dims=(6, 8, 8, 4), B=20)
+    dims = p["dims"]
+    u = p["u"].astype(np.float64)
+    v = p["v"].astype(np.float64)
+    hv = O.hvp(dims, act, th, p["X"], p["y"], v)
+    hu = O.hvp(dims, act, th, p["X"], p["y"], u)
+    assert abs(u @ hv - v @ hu) <= 1e-12 * np.linalg.norm(u) * np.linalg.norm(hv)
+    h2 = O.hvp(dims, act, th, p["X"], p["y"], 2.0 * v - 3.0 * u)
+    assert rel(h2, 2.0 * hv - 3.0 * hu) <= 1e-12
+    assert np.all(O.hvp(dims, act, th, p["X"], p["y"], 0 * v) == 0)
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_vHv_second_difference(act):
+    p, th = tiny(act, dims=(6, 8, 8, 4), B=20)
+    dims = p["dims"]
+    v = p["v"].astype(np.float64)
+    v /= np.linalg.norm(v)
+    f = lambda t: O.loss(dims, act, t, p["X"], p["y"])
+    eps = 1e-3
+    sd = (f(th + eps * v) - 2 * f(th) + f(th - eps * v)) / eps ** 2
+    vhv = v @ O.hvp(dims, act, th, p["X"], p["y"], v)
+    assert vhv == pytest.approx(sd, rel=1e-5, abs=1e-7)
+
+
+# --------------------------------------------------------------------- Gv
+def full_matrix(fn, n):
+    return np.stack([fn(e) for e in np.eye(n)], axis=1)
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_gvp_symmetric_psd(act):
+    p, th = tiny(act, dims=(4, 5, 3), B=9)
+    dims = p["dims"]
+    n = th.size
+    G = full_matrix(lambda e: O.gvp(dims, act, th, p["X"], e), n)
+    assert np.max(np.abs(G - G.T)) <= 1e-14 * np.max(np.abs(G))
+    lam = np.linalg.eigvalsh(0.5 * (G + G.T))
+    assert lam.min() >= -1e-12 * np.abs(lam).max()
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_gvp_equals_JT_HL_J_with_fd_jacobian(act):
+    p, th = tiny(act, dims=(4, 5, 3), B=6)
+    dims = p["dims"]
+    X = p["X"]
+    n = th.size
+    eps = 1e-6
+    logits = lambda t: O.forward(dims, act, t, X)[0][-1].ravel()
+    J = np.stack([(logits(th + eps * e) - logits(th - eps * e)) / (2 * eps)
+                  for e in np.eye(n)], axis=1)            # (B*C) x n
+    Z = O.forward(dims, act, th, X)[0][-1]
+    B, C = Z.shape
+    HL = np.zeros((B * C, B * C))
+    for i in range(B):
+        e = np.exp(Z[i] - Z[i].max())
+        pr = e / e.sum()
+        HL[i * C:(i + 1) * C, i * C:(i + 1) * C] = (np.diag(pr) - np.outer(pr, pr)) / B
+    v = p["v"].astype(np.float64)
+    assert rel(O.gvp(dims, act, th, X, v), J.T @ HL @ J @ v) <= 1e-8
+
+
+# ------------------------------------------------------------ Hv and Gv
+@pytest.mark.parametrize("act", ACTS)
+def test_single_layer_hessian_is_multinomial_logistic(act):
+    """L = 1: H = G = (1/B) sum_i (diag p_i - p_i p_i^T) kron x~_i x~_i^T,
+    reordered from [W | b] rows into the W-then-b parameter layout."""
+    dims = (4, 3)
+    p = WL.make_small(dims, act, 8, 21, x_dist="normal")
+    th = p["theta"].astype(np.float64)
+    X = p["X"].astype(np.float64)
+    d0, C = dims
+    W, b = O.unpack(th, dims)[0]
+    Hk = np.zeros((C * (d0 + 1), C * (d0 + 1)))
+    for x in X:
+        z = W @ x + b
+        e = np.exp(z - z.max())
+        pr = e / e.sum()
+        xt = np.append(x, 1.0)
+        Hk += np.kron(np.diag(pr) - np.outer(pr, pr), np.outer(xt, xt))
+    Hk /= X.shape[0]
+    # kron index (c, k) with k = d0 meaning the bias -> theta index
+    perm = [c * d0 + k if k < d0 else C * d0 + c
+            for c in range(C) for k in range(d0 + 1)]
+    Ht = np.zeros_like(Hk)
+    Ht[np.ix_(perm, perm)] = Hk
+    n = th.size
+    Hs = full_matrix(lambda e: O.hvp(dims, act, th, X, p["y"], e), n)
+    Gs = full_matrix(lambda e: O.gvp(dims, act, th, X, e), n)
+    assert np.max(np.abs(Hs - Ht)) <= 1e-14
+    assert np.max(np.abs(Gs - Ht)) <= 1e-14
+
+
+@pytest.mark.parametrize("mode", ("hessian", "gauss_newton"))
+def test_shard_average(mode):
+    """A product on a batch is the row-weighted mean of the products on its
+    shards (Alg. 2, the reduce of per-node products with equal shares)."""
+    act = "tanh"
+    p, th = tiny(act, dims=(6, 8, 8, 4), B=24)
+    dims = p["dims"]
+    v = p["v"].astype(np.float64)
+    X, y = p["X"], p["y"]
+    full = O.curvature(dims, act, th, X, y, v, mode)
+    parts = [(0, 5), (5, 16), (16, 24)]
+    avg = sum((e - s) / 24.0 * O.curvature(dims, act, th, X[s:e], y[s:e], v, mode)
+              for s, e in parts)
+    assert rel(avg, full) <= 1e-13
+
+
+def test_relu_hessian_and_gn_differ_only_by_output_term():
+    """For ReLU, phi'' = 0 so H - G comes only from the label-dependent
+    delta V backward term; they must differ on a 2-hidden-layer net, and
+    H must be indefinite while G is PSD."""
+    p, th = tiny("relu", dims=(6, 8, 8, 4), B=20)
+    dims = p["dims"]
+    n = th.size
+    H = full_matrix(lambda e: O.hvp(dims, "relu", th, p["X"], p["y"], e), n)
+    G = full_matrix(lambda e: O.gvp(dims, "relu", th, p["X"], e), n)
+    assert np.max(np.abs(H - G)) > 1e-3
+    assert np.linalg.eigvalsh(0.5 * (H + H.T)).min() < -1e-6
+
+
+# --------------------------------------------------------------------- CG
+def diag_op(d):
+    d = np.asarray(d, dtype=np.float64)
+    return lambda p: d * p
+
+
+@pytest.mark.parametrize("case", ["case1", "case2"])
+def test_cg_hand_computed_negative_curvature(case):
+    gd = read_golden("cg_hand_cases.txt")
+    r = O.cg_minimize(diag_op(gd[case + ".A_diag"]), np.array(gd[case + ".g"]),
+                      gd[case + ".lambda"], 10)
+    assert r["neg_curv"] == 1
+    assert r["neg_iter"] == gd[case + ".neg_iter"]
+    assert r["iters"] == gd[case + ".iters"]
+    assert r["products"] == gd[case + ".products"]
+    assert r["pBp"] == pytest.approx(gd[case + ".pBp"], abs=1e-14)
+    np.testing.assert_allclose(r["step"], gd[case + ".step"], atol=1e-14)
+    np.testing.assert_allclose(r["neg_dir"], gd[case + ".neg_dir"], atol=1e-14)
+    assert r["gTd"] == pytest.approx(gd[case + ".gTd"], abs=1e-14)
+    assert r["rr0"] == pytest.approx(gd[case + ".rr0"], abs=1e-14)
+
+
+def test_cg_hand_computed_damped_exact():
+    gd = read_golden("cg_hand_cases.txt")
+    r = O.cg_minimize(diag_op(gd["case3.A_diag"]), np.array(gd["case3.g"]),
+                      gd["case3.lambda"], 2, record=True)
+    assert r["neg_curv"] == 0 and r["iters"] == 2 and r["products"] == 2
+    np.testing.assert_allclose(r["step"], gd["case3.step"], atol=1e-14)
+    np.testing.assert_allclose(r["kappas"], gd["case3.kappas"], atol=1e-14)
+
+
+@pytest.mark.parametrize("n,seed", [(5, 0), (12, 1), (20, 2)])
+def test_cg_exact_in_n_steps_on_spd(n, seed):
+    """Exact arithmetic CG solves an n x n SPD system in n steps; in fp64
+    that holds to rounding for a well-conditioned operator (condition 10).
+    At condition 1e3 the loss of conjugacy delays convergence, so there the
+    pin is 2n steps."""
+    for cond, steps, tol in ((10.0, n, 1e-12), (1e3, 2 * n, 1e-10)):
+        rng = np.random.default_rng(seed)
+        Q, _ = np.linalg.qr(rng.standard_normal((n, n)))
+        A = (Q * np.geomspace(1.0, cond, n)) @ Q.T
+        A = 0.5 * (A + A.T)
+        g = rng.standard_normal(n)
+        lam = 0.1
+        r = O.cg_minimize(lambda p: A @ p, g, lam, steps)
+        x = np.linalg.solve(A + lam * np.eye(n), -g)
+        assert r["neg_curv"] == 0 and r["iters"] == steps
+        assert rel(r["step"], x) <= tol
+    # first iterate: x_1 = -(g.g / g.Bg) g
+    r1 = O.cg_minimize(lambda p: A @ p, g, lam, 1)
+    Bg = A @ g + lam * g
+    np.testing.assert_allclose(r1["step"], -(g @ g) / (g @ Bg) * g, rtol=1e-13)
+
+
+def test_cg_invariants_and_model_decrease():
+    rng = np.random.default_rng(7)
+    n = 15
+    M = rng.standard_normal((n, n))
+    A = M @ M.T / n
+    g = rng.standard_normal(n)
+    lam = 0.05
+    Bm = A + lam * np.eye(n)
+    prev = 0.0
+    for k in range(1, 7):
+        r = O.cg_minimize(lambda p: A @ p, g, lam, k, record=True)
+        x = r["step"]
+        m = g @ x + 0.5 * x @ Bm @ x
+        assert m < prev                       # the model decreases
+        prev = m
+    r = O.cg_minimize(lambda p: A @ p, g, lam, 6, record=True)
+    P = np.stack(r["dirs"], axis=1)
+    C = P.T @ Bm @ P
+    off = C - np.diag(np.diag(C))
+    assert np.max(np.abs(off)) <= 1e-9 * np.max(np.abs(np.diag(C)))
+    # g.p_j = -||r_j||^2, and the first direction is -g
+    np.testing.assert_allclose(r["dirs"][0], -g)
+    # model value = -1/2 sum rr_i^2 / kappa_i for the recorded iterations
+    x = r["step"]
+    rrs = [g @ g]
+    xx, rr_ = np.zeros(n), g.copy()
+    for p_, kap in zip(r["dirs"], r["kappas"]):
+        assert g @ p_ == pytest.approx(-(rr_ @ rr_), rel=1e-9)
+        a = (rr_ @ rr_) / kap
+        xx = xx + a * p_
+        rr_ = rr_ + a * (Bm @ p_)
+        rrs.append(rr_ @ rr_)
+    mval = g @ x + 0.5 * x @ Bm @ x
+    assert mval == pytest.approx(
+        -0.5 * sum(rrs[i] ** 2 / r["kappas"][i] for i in range(6)), rel=1e-9)
+
+
+def test_cg_zero_gradient_and_tolerance():
+    r = O.cg_minimize(lambda p: p, np.zeros(4), 0.1, 5)
+    assert r["iters"] == 0 and r["products"] == 0 and np.all(r["step"] == 0)
+    A = np.diag([1.0, 2.0, 3.0, 4.0])
+    r = O.cg_minimize(lambda p: A @ p, np.ones(4), 0.0, 50, rel_tol=1e-6)
+    assert r["iters"] == 4 and r["rr_final"] <= 1e-12 * 4
+
+
+def test_cg_network_damped_single_layer_is_exact():
+    """L = 1 with damping: B = G + lam I is SPD and explicitly formable, so
+    n CG steps give -B^{-1} g (the GPU uses the same test)."""
+    dims = (3, 3)
+    p = WL.make_small(dims, "sigmoid", 10, 4, x_dist="normal")
+    th = p["theta"].astype(np.float64)
+    n = th.size
+    _, g = O.loss_grad(dims, "sigmoid", th, p["X"], p["y"])
+    G = full_matrix(lambda e: O.gvp(dims, "sigmoid", th, p["X"], e), n)
+    lam = 0.05
+    r = O.cg_network(dims, "sigmoid", th, p["X"], p["y"], g, lam, n,
+                     "gauss_newton")
+    x = np.linalg.solve(G + lam * np.eye(n), -g)
+    assert r["neg_curv"] == 0
+    assert rel(r["step"], x) <= 1e-8
+
+
+# --------------------------------------------------------- planted mistakes
+def _fd_hv_error(act):
+    p, th = tiny(act, dims=(6, 8, 8, 4), B=20)
+    dims = p["dims"]
+    v = p["v"].astype(np.float64)
+    hv = O.hvp(dims, act, th, p["X"], p["y"], v)
+    eps = 1e-5
+    gp = O.loss_grad(dims, act, th + eps * v, p["X"], p["y"])[1]
+    gm = O.loss_grad(dims, act, th - eps * v, p["X"], p["y"])[1]
+    return rel(hv, (gp - gm) / (2 * eps))
+
+
+def test_planted_dropped_second_derivative_is_caught(monkeypatch):
+    monkeypatch.setattr(O, "d2phi", lambda act, z: np.zeros_like(z))
+    assert _fd_hv_error("sigmoid") > 1e-4
+
+
+def test_planted_wrong_sign_in_output_hessian_is_caught(monkeypatch):
+    real = O.softmax
+    calls = {"n": 0}
+
+    def bad_softmax(z):
+        calls["n"] += 1
+        return real(z)
+    monkeypatch.setattr(O, "softmax", bad_softmax)
+    # the gradient program and Hv must agree with finite differences only if
+    # every term is right; flip the sign of the R-forward bias term
+    orig = O._r_forward
+
+    def bad_rf(dims, act, theta, v, X):
+        vv = v.copy()
+        layers = O.unpack(vv, dims)
+        for W, b in layers:
+            b *= -1.0
+        return orig(dims, act, theta, vv, X)
+    monkeypatch.setattr(O, "_r_forward", bad_rf)
+    assert _fd_hv_error("tanh") > 1e-4
+
+
+def test_planted_wrong_activation_derivative_is_caught(monkeypatch):
+    monkeypatch.setattr(O, "dphi", lambda act, z: 1.0 - np.tanh(z))
+    p, th = tiny("tanh")
+    dims = p["dims"]
+    _, g = O.loss_grad(dims, "tanh", th, p["X"], p["y"])
+    v = p["v"].astype(np.float64)
+    eps = 1e-6
+    fd = (O.loss(dims, "tanh", th + eps * v, p["X"], p["y"]) -
+          O.loss(dims, "tanh", th - eps * v, p["X"], p["y"])) / (2 * eps)
+    assert abs(g @ v - fd) > 1e-6 * abs(fd)
+
+
+def test_planted_unoriented_direction_is_caught(monkeypatch):
+    # a dropped minus in d~ = -sgn(g^T d) d
+    monkeypatch.setattr(O, "sgn", lambda x: -1.0 if x >= 0.0 else 1.0)
+    gd = read_golden("cg_hand_cases.txt")
+    r = O.cg_minimize(diag_op(gd["case1.A_diag"]), np.array(gd["case1.g"]), 0.0, 10)
+    assert not np.allclose(r["neg_dir"], gd["case1.neg_dir"])
