@@ -1,0 +1,184 @@
+/*
+ * hf.h - C ABI of the MI355X (gfx950) Hessian-free curvature library.
+ *
+ * The library computes, for a fully connected network with sigmoid, tanh or
+ * ReLU hidden units and a softmax cross-entropy output averaged over the
+ * minibatch:
+ *   - the objective f and gradient g_k = grad f(theta_k)       (Alg. 1, step 1)
+ *   - curvature-vector products: the exact Hessian H v by the R-operator and
+ *     the Gauss-Newton G v                       (Sec. 2.1, after Alg. 1)
+ *   - CG-Minimize of the quadratic model m_k(d) = f + g^T d + d^T B_k d / 2
+ *     with B_k(d) = A d + lambda d, A = H or G   (Alg. 1 steps 3-4, eq. (1)),
+ *     stopping at the first conjugate direction with p^T B_k p <= 0 and
+ *     returning the current iterate (or -g at the first iteration) and the
+ *     oriented direction d~ = -sgn(g^T p) p      (Sec. 2.1 after eq. (1); Sec. 2.2)
+ * on one GPU's share of a data-parallel minibatch (Alg. 2).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Parameter layout (theta, v, g, H v, step, neg_dir): for l = 1..L the
+ *   weight matrix W_l (d_l x d_{l-1}, row-major) followed by the bias b_l
+ *   (d_l); n = sum_l d_l (d_{l-1} + 1) fp32 values.
+ * X: B x d_0 row-major fp32.  y: B int32 labels in [0, d_L).
+ * Every array argument is a device pointer, 16-byte aligned, owned by the
+ *   caller; the library never allocates or frees device memory.  Scratch
+ *   space comes from one caller-provided workspace (hf_set_workspace).
+ * All device work is enqueued on the stream set with hf_set_stream (the
+ *   null stream by default).  hf_loss_grad and hf_hvp are asynchronous;
+ *   hf_cg returns after its solve has finished (it synchronises the stream).
+ * Return value: HF_OK or a negative HF_E* code; hf_last_error() gives the
+ *   message.  Arguments are validated before any device call, so a bad
+ *   argument never reaches the GPU.  No exception or abort crosses the ABI.
+ * A context is not thread-safe; calls on one context must not overlap.
+ */
+#ifndef HF_H
+#define HF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct hf_ctx hf_ctx;
+
+/* Hidden-layer activation; the output layer is always softmax. */
+enum { HF_SIGMOID = 0, HF_TANH = 1, HF_RELU = 2 };
+/* Curvature matrix for hf_hvp / hf_cg. */
+enum { HF_HESSIAN = 0, HF_GAUSS_NEWTON = 1 };
+/* Arithmetic: fp32 storage, fp32 MFMA, fp32 accumulation. */
+enum { HF_FP32 = 0 };
+
+enum {
+  HF_OK = 0,
+  HF_EINVAL = -1,     /* bad argument (null, misaligned, out of range)      */
+  HF_ENOMEM = -2,     /* host allocation failed                            */
+  HF_EHIP = -3,       /* a HIP runtime call failed                         */
+  HF_ELABEL = -4,     /* a label outside [0, d_L) was seen (device check)  */
+  HF_ENUMERIC = -5,   /* NaN or Inf in a CG scalar                         */
+  HF_EWORKSPACE = -6  /* no workspace set, or it is too small              */
+};
+
+/* Limits checked by hf_create. */
+#define HF_MAX_LAYERS 16
+#define HF_MAX_CLASSES 4096
+
+/*
+ * hf_create: build a context for the network d_0-d_1-...-d_L.
+ *   dims      host array of n_dims = L + 1 >= 2 positive sizes; d_L is the
+ *             number of classes (<= HF_MAX_CLASSES); L <= HF_MAX_LAYERS.
+ *   act       HF_SIGMOID | HF_TANH | HF_RELU for hidden layers.
+ *   prec      HF_FP32.
+ *   max_batch largest B any later call may use (>= 1); every B x d_l
+ *             buffer and n must stay below 2^31 elements.
+ *   out       receives the context.  Returns HF_EINVAL on bad arguments.
+ * No device call is made; the context holds no device memory.
+ */
+int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
+              int64_t max_batch, hf_ctx** out);
+
+/* Free a context (host memory, events, pinned host staging).  NULL is ok. */
+int hf_destroy(hf_ctx* ctx);
+
+/* Stream (a hipStream_t) for all later device work; NULL = null stream. */
+int hf_set_stream(hf_ctx* ctx, void* hip_stream);
+
+/* n = sum_l d_l (d_{l-1} + 1), or -1 for a NULL context. */
+int64_t hf_num_params(const hf_ctx* ctx);
+
+/* Bytes of device workspace needed for max_batch rows (0 for NULL). */
+size_t hf_workspace_bytes(const hf_ctx* ctx);
+
+/* Hand the context a device workspace of at least hf_workspace_bytes()
+ * bytes, 256-byte aligned.  The caller keeps ownership and must keep it
+ * alive while the context uses it.  Contents need no initialisation. */
+int hf_set_workspace(hf_ctx* ctx, void* dev_ptr, size_t bytes);
+
+/*
+ * hf_loss_grad: f and g = grad f at theta = W on the batch (X, y) of B rows
+ * (Alg. 1 step 1; the per-node gradient of Alg. 2).
+ *   W     device, n fp32 (parameter layout above)
+ *   X, y  device, B x d_0 fp32 and B int32
+ *   loss  device, 1 fp32: f = (1/B) sum_i [logsumexp(z_i) - z_{i,y_i}]
+ *   grad  device, n fp32
+ * Asynchronous.  A label outside [0, d_L) raises a device flag reported as
+ * HF_ELABEL by the next hf_check or hf_cg.
+ */
+int hf_loss_grad(hf_ctx* ctx, const float* W, const float* X,
+                 const int32_t* y, int64_t B, float* loss, float* grad);
+
+/*
+ * hf_hvp: one curvature-vector product on the batch (X, y) of B rows,
+ * without damping (Sec. 2.1, paragraph after Alg. 1; the per-node product of
+ * Alg. 2):
+ *   mode HF_HESSIAN      out = H v, exact Hessian of f by the R-operator
+ *   mode HF_GAUSS_NEWTON out = G v = J^T H_L J v (labels unused; y may be NULL)
+ *   v, out device, n fp32.  Asynchronous.
+ */
+int hf_hvp(hf_ctx* ctx, const float* W, const float* X, const int32_t* y,
+           int64_t B, const float* v, int32_t mode, float* out);
+
+/* Result of hf_cg (host struct). */
+typedef struct hf_cg_info {
+  int32_t iters;      /* completed updates of the iterate                   */
+  int32_t products;   /* curvature products evaluated                       */
+  int32_t neg_curv;   /* 1 if the solve stopped on p^T B_k p <= 0           */
+  int32_t neg_iter;   /* CG iteration j of the detection, else -1           */
+  double pBp;         /* p^T B_k p at the detection (kappa)                 */
+  double pHp;         /* p^T A p = kappa - lambda ||p||^2 at the detection  */
+  double gTd;         /* g^T d~ for the returned direction (<= 0)           */
+  double rr0;         /* ||g||^2                                            */
+  double rr_final;    /* ||r||^2 at exit                                    */
+  int32_t status;     /* HF_OK, HF_ENUMERIC or HF_ELABEL                    */
+  int32_t reserved;
+} hf_cg_info;
+
+/*
+ * hf_cg: CG-Minimize(B_k, -g) with B_k = A + lambda I, A = H or G on the
+ * fixed curvature batch (Xc, yc) of Bc rows at theta = W (Alg. 1 steps 3-4;
+ * Alg. 2 builds the operator from one minibatch).
+ *   g          device, n fp32: the gradient (may come from a larger batch)
+ *   damping    lambda >= 0
+ *   max_iters  fixed iteration budget >= 0 (Sec. 2.2)
+ *   rel_tol    stop when ||r||^2 <= rel_tol^2 ||g||^2; 0 disables
+ *   step       device, n fp32: the iterate at exit; -g when negative
+ *              curvature is met at the first iteration (Sec. 2.1)
+ *   neg_dir    device, n fp32: d~ = -sgn(g^T p) p for the detected p
+ *              (Sec. 2.2), zeros when there was no detection
+ *   info       host struct, filled on return
+ * Starts from x_0 = 0.  The loop runs on the device with device-resident
+ * scalars; the call synchronises the stream before it returns.
+ */
+int hf_cg(hf_ctx* ctx, const float* W, const float* Xc, const int32_t* yc,
+          int64_t Bc, const float* g, float damping, int32_t max_iters,
+          float rel_tol, int32_t mode, float* step, float* neg_dir,
+          hf_cg_info* info);
+
+/* Synchronise the stream and report a device-detected error (HF_ELABEL)
+ * raised since the last hf_check; clears the flag. */
+int hf_check(hf_ctx* ctx);
+
+/* Message for the last failed call on ctx ("" if none); static text for a
+ * NULL context. */
+const char* hf_last_error(const hf_ctx* ctx);
+
+/* Static name of an HF_* code. */
+const char* hf_strerror(int32_t code);
+
+/*
+ * Kernel timing.  When enabled, every kernel launch is bracketed by HIP
+ * events on the context's stream and its algorithmic work (flops for the
+ * contractions, bytes for memory-bound kernels) is accumulated per kernel
+ * name.  hf_prof_get synchronises the stream.
+ */
+int hf_prof_enable(hf_ctx* ctx, int32_t on);
+int hf_prof_reset(hf_ctx* ctx);
+int32_t hf_prof_count(hf_ctx* ctx);
+int hf_prof_get(hf_ctx* ctx, int32_t i, const char** name, int64_t* launches,
+                double* total_ms, double* flops, double* bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HF_H */

@@ -1,0 +1,725 @@
+// Host side of the C ABI declared in include/hf.h: context, argument
+// validation, workspace carve-up, the order of the passes for the gradient,
+// the curvature products and CG-Minimize, and the kernel profiler.
+//
+// Pass order (B = rows, L = weight layers, A_0 = X):
+//   gradient (Alg. 1 step 1):
+//     forward   Z_l = A_{l-1} W_l^T + b_l,  A_l = phi(Z_l)          (l < L)
+//     output    p = softmax(Z_L), f, delta_L = (p - e_y) / B
+//     backward  grad W_l = delta_l^T A_{l-1},  grad b_l = sum_rows delta_l,
+//               delta_{l-1} = (delta_l W_l) * phi'(A_{l-1})
+//   curvature product (Sec. 2.1, after Alg. 1), v = (V_l, c_l):
+//     R-forward RZ_l = A_{l-1} V_l^T + RA_{l-1} W_l^T + c_l,
+//               RA_l = phi'(A_l) RZ_l   (fused with the forward GEMM)
+//     output    Rdelta_L = p * (RZ_L - rowsum(p * RZ_L)) / B
+//     Hessian   (Hv)_{W_l} = Rdelta_l^T A_{l-1} + delta_l^T RA_{l-1},
+//               (Hv)_{b_l} = sum_rows Rdelta_l,
+//               Rdelta_{l-1} = (Rdelta_l W_l + delta_l V_l) phi'(A_{l-1})
+//                              + (delta_l W_l) phi''(A_{l-1}) RZ_{l-1}
+//     Gauss-Newton (Gv)_{W_l} = Rdelta_l^T A_{l-1}, (Gv)_{b_l} = sum Rdelta_l,
+//               Rdelta_{l-1} = (Rdelta_l W_l) phi'(A_{l-1})
+//   CG-Minimize (Alg. 1 steps 3-4): the forward pass, p, delta_l and
+//     (delta_l W_l) phi''(A_{l-1}) are computed once on the curvature batch and
+//     reused by every product inside the solve.
+#include "hf.h"
+#include "hf_internal.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace hfk;
+
+// ------------------------------------------------------------------ profiler
+namespace hfk {
+
+struct ProfRec {
+  std::string name;
+  int64_t launches = 0;
+  double ms = 0.0, flops = 0.0, bytes = 0.0;
+};
+
+struct Profiler {
+  std::vector<ProfRec> recs;
+  std::map<std::string, int> index;
+  struct Pending { hipEvent_t a, b; int rec; };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t open = nullptr;
+
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  int rec_of(const char* name) {
+    auto it = index.find(name);
+    if (it != index.end()) return it->second;
+    ProfRec r;
+    r.name = name;
+    recs.push_back(r);
+    index[name] = (int)recs.size() - 1;
+    return (int)recs.size() - 1;
+  }
+  void collect() {
+    for (auto& p : pending) {
+      hipEventSynchronize(p.b);
+      float ms = 0.0f;
+      if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) recs[p.rec].ms += ms;
+      pool.push_back(p.a);
+      pool.push_back(p.b);
+    }
+    pending.clear();
+  }
+  ~Profiler() {
+    collect();
+    for (auto e : pool) hipEventDestroy(e);
+  }
+};
+
+void prof_begin(const Launch& L, const char* name) {
+  (void)name;
+  if (!L.prof) return;
+  L.prof->open = L.prof->get();
+  if (L.prof->open) hipEventRecord(L.prof->open, L.stream);
+}
+
+void prof_end(const Launch& L, const char* name, double flops, double bytes) {
+  if (!L.prof) return;
+  Profiler& P = *L.prof;
+  const int r = P.rec_of(name);
+  P.recs[r].launches += 1;
+  P.recs[r].flops += flops;
+  P.recs[r].bytes += bytes;
+  hipEvent_t b = P.get();
+  if (P.open && b) {
+    hipEventRecord(b, L.stream);
+    P.pending.push_back({P.open, b, r});
+  }
+  P.open = nullptr;
+  if (P.pending.size() > (1u << 16)) P.collect();
+}
+
+}  // namespace hfk
+
+// ------------------------------------------------------------------- context
+struct hf_ctx {
+  int L = 0;                   // weight layers
+  std::vector<int> d;          // d_0 .. d_L
+  std::vector<int> ld;         // padded leading dimensions (multiple of 4)
+  int act = 0, prec = 0;
+  int64_t Bmax = 0;
+  int64_t n = 0;
+  std::vector<int64_t> offW, offB;   // 1-based, parameter offsets
+  hipStream_t stream = nullptr;
+
+  // workspace carve-up (byte offsets), 1-based per layer where it applies
+  std::vector<size_t> oA, oD, oE2, oRZ, oRA, oRD;
+  size_t oZ = 0, oP = 0, oSplit = 0, oCol = 0, oR = 0, oPv = 0, oQ = 0,
+         oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
+  int max_splits = 8;
+  size_t split_elems = 0;
+
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+
+  std::string err;
+  Profiler* prof = nullptr;
+  CgState* pinned = nullptr;       // 2 host-pinned copies of the CG state
+  hipEvent_t ev[2] = {nullptr, nullptr};
+
+  float* F(size_t off) const { return reinterpret_cast<float*>(ws + off); }
+  double* Dp(size_t off) const { return reinterpret_cast<double*>(ws + off); }
+  Launch launch() const { return Launch{stream, prof}; }
+};
+
+namespace {
+
+int fail(hf_ctx* c, int code, const char* fmt, ...) __attribute__((format(printf, 3, 4)));
+int fail(hf_ctx* c, int code, const char* fmt, ...) {
+  if (c) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    c->err = buf;
+  }
+  return code;
+}
+
+#define HIP_TRY(ctx, expr)                                                     \
+  do {                                                                         \
+    hipError_t e_ = (expr);                                                    \
+    if (e_ != hipSuccess)                                                      \
+      return fail(ctx, HF_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+inline size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
+inline bool a16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+inline int round4(int x) { return (x + 3) & ~3; }
+
+void plan(hf_ctx* c) {
+  const int L = c->L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += up256(bytes);
+    return o;
+  };
+  const size_t B = (size_t)c->Bmax;
+  c->oA.assign(L + 1, 0);
+  c->oD.assign(L + 1, 0);
+  c->oE2.assign(L + 1, 0);
+  c->oRZ.assign(L + 1, 0);
+  c->oRA.assign(L + 1, 0);
+  c->oRD.assign(L + 1, 0);
+  for (int l = 1; l <= L; ++l) {
+    const size_t sz = B * c->ld[l] * sizeof(float);
+    if (l < L) {
+      c->oA[l] = take(sz);
+      c->oE2[l] = take(sz);
+      c->oRA[l] = take(sz);
+    }
+    c->oD[l] = take(sz);
+    c->oRZ[l] = take(sz);
+    c->oRD[l] = take(sz);
+  }
+  c->oZ = take(B * c->ld[L] * sizeof(float));
+  c->oP = take(B * c->ld[L] * sizeof(float));
+  size_t mn = 0;
+  int dmax = 0;
+  for (int l = 1; l <= L; ++l) {
+    mn = std::max(mn, (size_t)c->d[l] * c->d[l - 1]);
+    dmax = std::max(dmax, c->d[l]);
+  }
+  c->split_elems = mn;
+  c->oSplit = take((size_t)c->max_splits * mn * sizeof(float));
+  c->oCol = take((size_t)colsum_chunks((int)B) * dmax * sizeof(double));
+  const size_t nv = ((size_t)c->n + 63) & ~size_t(63);
+  c->oR = take(nv * sizeof(float));
+  c->oPv = take(nv * sizeof(float));
+  c->oQ = take(nv * sizeof(float));
+  c->oRed = take(4 * 1024 * sizeof(double));
+  c->oLoss = take(((B + 3) / 4) * sizeof(double));
+  c->oState = take(sizeof(CgState));
+  c->oErr = take(sizeof(int));
+  c->need = off;
+}
+
+bool valid_act(int a) { return a == HF_SIGMOID || a == HF_TANH || a == HF_RELU; }
+
+int check_ready(hf_ctx* c) {
+  if (!c) return HF_EINVAL;
+  if (!c->ws) return fail(c, HF_EWORKSPACE, "no workspace set (hf_set_workspace)");
+  return HF_OK;
+}
+
+int check_ptr(hf_ctx* c, const void* p, const char* what) {
+  if (!p) return fail(c, HF_EINVAL, "%s is NULL", what);
+  if (!a16(p)) return fail(c, HF_EINVAL, "%s is not 16-byte aligned", what);
+  return HF_OK;
+}
+
+int check_batch(hf_ctx* c, int64_t B) {
+  if (B < 1 || B > c->Bmax)
+    return fail(c, HF_EINVAL, "batch %lld outside [1, %lld]", (long long)B,
+                (long long)c->Bmax);
+  return HF_OK;
+}
+
+// split-K factor for a weight-gradient GEMM with the given tile count and
+// reduction length: enough workgroups to cover the 256 compute units twice,
+// while every split keeps at least 256 rows of the reduction.
+int choose_splits(const hf_ctx* c, int M, int N, int Ktot) {
+  const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  int s = 1;
+  while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 256) s *= 2;
+  return s;
+}
+
+GemmShape shape(int M, int N, int K, const float* x0, const float* x1,
+                const float* y0, const float* y1, int ldx, int ldy, int nseg,
+                const int* skip) {
+  GemmShape s;
+  s.M = M; s.N = N; s.K = K;
+  s.X[0] = x0; s.X[1] = x1;
+  s.Y[0] = y0; s.Y[1] = y1;
+  s.ldx = ldx; s.ldy = ldy;
+  s.nseg = nseg;
+  s.splits = 1;
+  s.skip = skip;
+  return s;
+}
+
+EpiArgs epi(const hf_ctx* c, int hidden) {
+  EpiArgs e;
+  std::memset(&e, 0, sizeof e);
+  e.act = c->act;
+  e.hidden = hidden;
+  return e;
+}
+
+// Weight-gradient GEMM into the parameter layout: out_W (d_l x d_{l-1}) =
+// sum_seg Xs^T Ys over the rows, then the bias part from colsum(bias_src).
+void wgrad(hf_ctx* c, int l, int B, const float* x0, const float* y0,
+           const float* x1, const float* y1, int ldy, const float* bias_src,
+           float* out, const int* skip) {
+  const Launch Lc = c->launch();
+  const int M = c->d[l], N = c->d[l - 1];
+  const int nseg = x1 ? 2 : 1;
+  GemmShape s = shape(M, N, B, x0, x1, y0, y1, c->ld[l], ldy, nseg, skip);
+  s.splits = choose_splits(c, M, N, B * nseg);
+  EpiArgs e = epi(c, 0);
+  if (s.splits > 1) {
+    e.out0 = c->F(c->oSplit);
+    e.ldo = N;
+    e.split_stride = (long long)M * N;
+    gemm_wgrad(Lc, s, e);
+    splitk_reduce(Lc, c->F(c->oSplit), s.splits, M, N, out + c->offW[l], N, skip);
+  } else {
+    e.out0 = out + c->offW[l];
+    e.ldo = N;
+    gemm_wgrad(Lc, s, e);
+  }
+  colsum(Lc, bias_src, B, M, c->ld[l], c->Dp(c->oCol), out + c->offB[l], skip);
+}
+
+// Forward pass (activations only) on B rows of X; logits into Z, then the
+// softmax / cross-entropy kernel (labels optional).
+void forward_plain(hf_ctx* c, const float* W, const float* X, int B,
+                   const int32_t* y, bool want_delta) {
+  const Launch Lc = c->launch();
+  for (int l = 1; l <= c->L; ++l) {
+    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
+    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
+    GemmShape s = shape(B, c->d[l], c->d[l - 1], Ain, nullptr, W + c->offW[l],
+                        nullptr, ldin, c->d[l - 1], 1, nullptr);
+    EpiArgs e = epi(c, l < c->L);
+    e.bias = W + c->offB[l];
+    e.out0 = (l < c->L) ? c->F(c->oA[l]) : c->F(c->oZ);
+    e.ldo = c->ld[l];
+    gemm_fwd(Lc, s, e);
+  }
+  softmax_xent(Lc, c->F(c->oZ), y, B, c->d[c->L], c->ld[c->L], c->F(c->oP),
+               want_delta ? c->F(c->oD[c->L]) : nullptr, c->Dp(c->oLoss),
+               reinterpret_cast<int*>(c->ws + c->oErr));
+}
+
+// Backward data pass delta_{l-1} = (delta_l W_l) phi'(A_{l-1}); optionally
+// caches (delta_l W_l) phi''(A_{l-1}) for the Hessian product.
+void backward_data(hf_ctx* c, const float* W, int l, int B, bool cache_e2) {
+  GemmShape s = shape(B, c->d[l - 1], c->d[l], c->F(c->oD[l]), nullptr,
+                      W + c->offW[l], nullptr, c->ld[l], c->d[l - 1], 1, nullptr);
+  EpiArgs e = epi(c, 1);
+  e.out0 = c->F(c->oD[l - 1]);
+  e.out2 = cache_e2 ? c->F(c->oE2[l - 1]) : nullptr;
+  e.ldo = c->ld[l - 1];
+  e.aux0 = c->F(c->oA[l - 1]);
+  e.lda = c->ld[l - 1];
+  gemm_bwd(c->launch(), s, e);
+}
+
+// One curvature product out = A v on B rows of X with the forward cache
+// (A_l, p, delta_l, E2_l) already computed; skip = device flag or null.
+void product_cached(hf_ctx* c, const float* W, const float* X, int B,
+                    const float* v, int mode, float* out, const int* skip) {
+  const Launch Lc = c->launch();
+  const int L = c->L;
+  for (int l = 1; l <= L; ++l) {
+    GemmShape s;
+    if (l == 1) {
+      s = shape(B, c->d[1], c->d[0], X, nullptr, v + c->offW[1], nullptr,
+                c->d[0], c->d[0], 1, skip);
+    } else {
+      s = shape(B, c->d[l], c->d[l - 1], c->F(c->oRA[l - 1]), c->F(c->oA[l - 1]),
+                W + c->offW[l], v + c->offW[l], c->ld[l - 1], c->d[l - 1], 2, skip);
+    }
+    EpiArgs e = epi(c, l < L);
+    e.rbias = v + c->offB[l];
+    e.out1 = c->F(c->oRZ[l]);
+    e.out2 = (l < L) ? c->F(c->oRA[l]) : nullptr;
+    e.ldo = c->ld[l];
+    e.aux0 = (l < L) ? c->F(c->oA[l]) : nullptr;
+    e.lda = c->ld[l];
+    gemm_rfwd(Lc, s, e);
+  }
+  softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), B, c->d[L], c->ld[L],
+              c->F(c->oRD[L]), skip);
+  for (int l = L; l >= 1; --l) {
+    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
+    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
+    if (mode == HF_HESSIAN && l > 1) {
+      wgrad(c, l, B, c->F(c->oRD[l]), Ain, c->F(c->oD[l]), c->F(c->oRA[l - 1]),
+            ldin, c->F(c->oRD[l]), out, skip);
+    } else {
+      wgrad(c, l, B, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin,
+            c->F(c->oRD[l]), out, skip);
+    }
+    if (l == 1) break;
+    EpiArgs e = epi(c, 1);
+    e.out1 = c->F(c->oRD[l - 1]);
+    e.ldo = c->ld[l - 1];
+    e.aux0 = c->F(c->oA[l - 1]);
+    e.lda = c->ld[l - 1];
+    if (mode == HF_HESSIAN) {
+      GemmShape s = shape(B, c->d[l - 1], c->d[l], c->F(c->oRD[l]), c->F(c->oD[l]),
+                          W + c->offW[l], v + c->offW[l], c->ld[l], c->d[l - 1],
+                          2, skip);
+      e.aux1 = c->F(c->oRZ[l - 1]);
+      e.aux2 = c->F(c->oE2[l - 1]);
+      gemm_rbwd(Lc, s, e);
+    } else {
+      GemmShape s = shape(B, c->d[l - 1], c->d[l], c->F(c->oRD[l]), nullptr,
+                          W + c->offW[l], nullptr, c->ld[l], c->d[l - 1], 1, skip);
+      gemm_gnbwd(Lc, s, e);
+    }
+  }
+}
+
+}  // namespace
+
+// ==================================================================== C ABI
+extern "C" {
+
+int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
+              int64_t max_batch, hf_ctx** out) {
+  if (!out) return HF_EINVAL;
+  *out = nullptr;
+  if (!dims || n_dims < 2 || n_dims > HF_MAX_LAYERS + 1) return HF_EINVAL;
+  if (!valid_act(act) || prec != HF_FP32 || max_batch < 1) return HF_EINVAL;
+  for (int i = 0; i < n_dims; ++i)
+    if (dims[i] < 1) return HF_EINVAL;
+  if (dims[n_dims - 1] > HF_MAX_CLASSES) return HF_EINVAL;
+  const int64_t lim = (int64_t(1) << 31) - 1;
+  int64_t n = 0;
+  for (int i = 0; i < n_dims; ++i)
+    if (max_batch * (int64_t)round4(dims[i]) > lim) return HF_EINVAL;
+  for (int l = 1; l < n_dims; ++l) n += (int64_t)dims[l] * (dims[l - 1] + 1);
+  if (n > lim - 64) return HF_EINVAL;
+  hf_ctx* c = new (std::nothrow) hf_ctx();
+  if (!c) return HF_ENOMEM;
+  c->L = n_dims - 1;
+  c->d.assign(dims, dims + n_dims);
+  c->ld.resize(n_dims);
+  for (int i = 0; i < n_dims; ++i) c->ld[i] = round4(dims[i]);
+  c->act = act;
+  c->prec = prec;
+  c->Bmax = max_batch;
+  c->n = n;
+  c->offW.assign(n_dims, 0);
+  c->offB.assign(n_dims, 0);
+  int64_t off = 0;
+  for (int l = 1; l < n_dims; ++l) {
+    c->offW[l] = off;
+    off += (int64_t)dims[l] * dims[l - 1];
+    c->offB[l] = off;
+    off += dims[l];
+  }
+  plan(c);
+  *out = c;
+  return HF_OK;
+}
+
+int hf_destroy(hf_ctx* c) {
+  if (!c) return HF_OK;
+  delete c->prof;
+  if (c->pinned) hipHostFree(c->pinned);
+  for (auto& e : c->ev)
+    if (e) hipEventDestroy(e);
+  delete c;
+  return HF_OK;
+}
+
+int hf_set_stream(hf_ctx* c, void* s) {
+  if (!c) return HF_EINVAL;
+  c->stream = reinterpret_cast<hipStream_t>(s);
+  return HF_OK;
+}
+
+int64_t hf_num_params(const hf_ctx* c) { return c ? c->n : -1; }
+
+size_t hf_workspace_bytes(const hf_ctx* c) { return c ? c->need : 0; }
+
+int hf_set_workspace(hf_ctx* c, void* p, size_t bytes) {
+  if (!c) return HF_EINVAL;
+  if (!p) return fail(c, HF_EINVAL, "workspace pointer is NULL");
+  if ((uintptr_t)p & 255u) return fail(c, HF_EINVAL, "workspace is not 256-byte aligned");
+  if (bytes < c->need)
+    return fail(c, HF_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed",
+                bytes, c->need);
+  c->ws = reinterpret_cast<char*>(p);
+  c->ws_bytes = bytes;
+  HIP_TRY(c, hipMemset(c->ws + c->oErr, 0, sizeof(int)));
+  return HF_OK;
+}
+
+int hf_loss_grad(hf_ctx* c, const float* W, const float* X, const int32_t* y,
+                 int64_t B, float* loss, float* grad) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, X, "X")) ||
+      (rc = check_ptr(c, grad, "grad")) || (rc = check_batch(c, B)))
+    return rc;
+  if (!y) return fail(c, HF_EINVAL, "y is NULL");
+  if (!loss) return fail(c, HF_EINVAL, "loss is NULL");
+  const Launch Lc = c->launch();
+  const int b = (int)B;
+  forward_plain(c, W, X, b, y, true);
+  loss_finalize(Lc, c->Dp(c->oLoss), (b + 3) / 4, b, loss);
+  for (int l = c->L; l >= 1; --l) {
+    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
+    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
+    wgrad(c, l, b, c->F(c->oD[l]), Ain, nullptr, nullptr, ldin, c->F(c->oD[l]),
+          grad, nullptr);
+    if (l > 1) backward_data(c, W, l, b, false);
+  }
+  HIP_TRY(c, hipGetLastError());
+  return HF_OK;
+}
+
+int hf_hvp(hf_ctx* c, const float* W, const float* X, const int32_t* y,
+           int64_t B, const float* v, int32_t mode, float* out) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, X, "X")) ||
+      (rc = check_ptr(c, v, "v")) || (rc = check_ptr(c, out, "out")) ||
+      (rc = check_batch(c, B)))
+    return rc;
+  if (mode != HF_HESSIAN && mode != HF_GAUSS_NEWTON)
+    return fail(c, HF_EINVAL, "unknown mode %d", mode);
+  if (mode == HF_HESSIAN && !y) return fail(c, HF_EINVAL, "y is NULL");
+  const Launch Lc = c->launch();
+  const int b = (int)B, L = c->L;
+  // forward fused with R-forward
+  for (int l = 1; l <= L; ++l) {
+    GemmShape s;
+    if (l == 1) {
+      s = shape(b, c->d[1], c->d[0], X, nullptr, W + c->offW[1], v + c->offW[1],
+                c->d[0], c->d[0], 1, nullptr);
+    } else {
+      s = shape(b, c->d[l], c->d[l - 1], c->F(c->oA[l - 1]), c->F(c->oRA[l - 1]),
+                W + c->offW[l], v + c->offW[l], c->ld[l - 1], c->d[l - 1], 1,
+                nullptr);
+    }
+    EpiArgs e = epi(c, l < L);
+    e.bias = W + c->offB[l];
+    e.rbias = v + c->offB[l];
+    e.out0 = (l < L) ? c->F(c->oA[l]) : c->F(c->oZ);
+    e.out1 = c->F(c->oRZ[l]);
+    e.out2 = (l < L) ? c->F(c->oRA[l]) : nullptr;
+    e.ldo = c->ld[l];
+    gemm_fwd_rfwd(Lc, s, e);
+  }
+  const bool hess = mode == HF_HESSIAN;
+  softmax_xent(Lc, c->F(c->oZ), hess ? y : nullptr, b, c->d[L], c->ld[L],
+               c->F(c->oP), hess ? c->F(c->oD[L]) : nullptr, c->Dp(c->oLoss),
+               reinterpret_cast<int*>(c->ws + c->oErr));
+  softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), b, c->d[L], c->ld[L],
+              c->F(c->oRD[L]), nullptr);
+  for (int l = L; l >= 1; --l) {
+    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
+    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
+    if (hess && l > 1) {
+      wgrad(c, l, b, c->F(c->oRD[l]), Ain, c->F(c->oD[l]), c->F(c->oRA[l - 1]),
+            ldin, c->F(c->oRD[l]), out, nullptr);
+    } else {
+      wgrad(c, l, b, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin,
+            c->F(c->oRD[l]), out, nullptr);
+    }
+    if (l == 1) break;
+    EpiArgs e = epi(c, 1);
+    e.ldo = c->ld[l - 1];
+    e.aux0 = c->F(c->oA[l - 1]);
+    e.lda = c->ld[l - 1];
+    if (hess) {
+      // (E, RE) = (delta W, Rdelta W + delta V) in one pass
+      GemmShape s = shape(b, c->d[l - 1], c->d[l], c->F(c->oD[l]), c->F(c->oRD[l]),
+                          W + c->offW[l], v + c->offW[l], c->ld[l], c->d[l - 1],
+                          1, nullptr);
+      e.out0 = c->F(c->oD[l - 1]);
+      e.out1 = c->F(c->oRD[l - 1]);
+      e.aux1 = c->F(c->oRZ[l - 1]);
+      gemm_bwd_rbwd(Lc, s, e);
+    } else {
+      GemmShape s = shape(b, c->d[l - 1], c->d[l], c->F(c->oRD[l]), nullptr,
+                          W + c->offW[l], nullptr, c->ld[l], c->d[l - 1], 1,
+                          nullptr);
+      e.out1 = c->F(c->oRD[l - 1]);
+      gemm_gnbwd(Lc, s, e);
+    }
+  }
+  HIP_TRY(c, hipGetLastError());
+  return HF_OK;
+}
+
+int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
+          int64_t Bc, const float* g, float damping, int32_t max_iters,
+          float rel_tol, int32_t mode, float* step, float* neg_dir,
+          hf_cg_info* info) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, Xc, "Xc")) ||
+      (rc = check_ptr(c, g, "g")) || (rc = check_ptr(c, step, "step")) ||
+      (rc = check_ptr(c, neg_dir, "neg_dir")) || (rc = check_batch(c, Bc)))
+    return rc;
+  if (!info) return fail(c, HF_EINVAL, "info is NULL");
+  if (mode != HF_HESSIAN && mode != HF_GAUSS_NEWTON)
+    return fail(c, HF_EINVAL, "unknown mode %d", mode);
+  if (mode == HF_HESSIAN && !yc) return fail(c, HF_EINVAL, "yc is NULL");
+  if (!(damping >= 0.0f) || !std::isfinite(damping))
+    return fail(c, HF_EINVAL, "damping must be finite and >= 0");
+  if (max_iters < 0) return fail(c, HF_EINVAL, "max_iters < 0");
+  if (!(rel_tol >= 0.0f) || !std::isfinite(rel_tol))
+    return fail(c, HF_EINVAL, "rel_tol must be finite and >= 0");
+  std::memset(info, 0, sizeof *info);
+  if (!c->pinned) {
+    HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
+  }
+  const Launch Lc = c->launch();
+  const int b = (int)Bc;
+  const long long n = c->n;
+  const bool hess = mode == HF_HESSIAN;
+  CgState* st = reinterpret_cast<CgState*>(c->ws + c->oState);
+  const int* skip = &st->done;
+  double* part = c->Dp(c->oRed);
+  float* r = c->F(c->oR);
+  float* p = c->F(c->oPv);
+  float* q = c->F(c->oQ);
+
+  // cache of the curvature batch: activations, p, delta_l, E2_l
+  forward_plain(c, W, Xc, b, hess ? yc : nullptr, hess);
+  if (hess)
+    for (int l = c->L; l >= 2; --l) backward_data(c, W, l, b, true);
+  cg_init(Lc, g, step, r, p, neg_dir, n, (double)damping,
+          (double)rel_tol * (double)rel_tol, part, st);
+  for (int j = 0; j < max_iters; ++j) {
+    product_cached(c, W, Xc, b, p, mode, q, skip);
+    cg_curv_dot(Lc, p, q, n, j, part, st);
+    cg_neg(Lc, g, p, step, neg_dir, n, part, st);
+    cg_update(Lc, step, r, p, q, n, part, st);
+    cg_dir(Lc, r, p, n, st);
+    // Stop enqueueing once the device reports `done` for the previous
+    // iteration; the work already queued for this one returns at once.
+    HIP_TRY(c, hipMemcpyAsync(&c->pinned[j & 1], st, sizeof(CgState),
+                              hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
+    if (j >= 1) {
+      HIP_TRY(c, hipEventSynchronize(c->ev[(j - 1) & 1]));
+      if (c->pinned[(j - 1) & 1].done) break;
+    }
+  }
+  HIP_TRY(c, hipGetLastError());
+  HIP_TRY(c, hipMemcpyAsync(&c->pinned[0], st, sizeof(CgState),
+                            hipMemcpyDeviceToHost, c->stream));
+  int errflag = 0;
+  HIP_TRY(c, hipMemcpyAsync(&errflag, c->ws + c->oErr, sizeof(int),
+                            hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const CgState& s = c->pinned[0];
+  info->iters = s.iters;
+  info->products = s.products;
+  info->neg_curv = s.neg;
+  info->neg_iter = s.neg ? s.neg_iter : -1;
+  info->pBp = s.neg ? s.kappa : 0.0;
+  info->pHp = s.neg ? s.pq : 0.0;
+  info->gTd = s.neg ? (s.gp >= 0.0 ? -s.gp : s.gp) : 0.0;
+  info->rr0 = s.rr0;
+  info->rr_final = s.rr;
+  info->status = s.status;
+  if (errflag) {
+    info->status = HF_ELABEL;
+    int zero = 0;
+    HIP_TRY(c, hipMemcpy(c->ws + c->oErr, &zero, sizeof(int), hipMemcpyHostToDevice));
+    return fail(c, HF_ELABEL, "a label outside [0, %d) was seen", c->d[c->L]);
+  }
+  if (s.status) return fail(c, HF_ENUMERIC, "non-finite CG scalar");
+  return HF_OK;
+}
+
+int hf_check(hf_ctx* c) {
+  if (!c) return HF_EINVAL;
+  if (!c->ws) return HF_OK;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  int flag = 0;
+  HIP_TRY(c, hipMemcpy(&flag, c->ws + c->oErr, sizeof(int), hipMemcpyDeviceToHost));
+  if (flag) {
+    int zero = 0;
+    HIP_TRY(c, hipMemcpy(c->ws + c->oErr, &zero, sizeof(int), hipMemcpyHostToDevice));
+    return fail(c, HF_ELABEL, "a label outside [0, %d) was seen", c->d[c->L]);
+  }
+  return HF_OK;
+}
+
+const char* hf_last_error(const hf_ctx* c) {
+  if (!c) return "null context";
+  return c->err.c_str();
+}
+
+const char* hf_strerror(int32_t code) {
+  switch (code) {
+    case HF_OK: return "HF_OK";
+    case HF_EINVAL: return "HF_EINVAL";
+    case HF_ENOMEM: return "HF_ENOMEM";
+    case HF_EHIP: return "HF_EHIP";
+    case HF_ELABEL: return "HF_ELABEL";
+    case HF_ENUMERIC: return "HF_ENUMERIC";
+    case HF_EWORKSPACE: return "HF_EWORKSPACE";
+    default: return "HF_UNKNOWN";
+  }
+}
+
+int hf_prof_enable(hf_ctx* c, int32_t on) {
+  if (!c) return HF_EINVAL;
+  if (on && !c->prof) c->prof = new (std::nothrow) Profiler();
+  if (on && !c->prof) return HF_ENOMEM;
+  if (!on && c->prof) {
+    delete c->prof;
+    c->prof = nullptr;
+  }
+  return HF_OK;
+}
+
+int hf_prof_reset(hf_ctx* c) {
+  if (!c) return HF_EINVAL;
+  if (c->prof) {
+    c->prof->collect();
+    c->prof->recs.clear();
+    c->prof->index.clear();
+  }
+  return HF_OK;
+}
+
+int32_t hf_prof_count(hf_ctx* c) {
+  if (!c || !c->prof) return 0;
+  c->prof->collect();
+  return (int32_t)c->prof->recs.size();
+}
+
+int hf_prof_get(hf_ctx* c, int32_t i, const char** name, int64_t* launches,
+                double* total_ms, double* flops, double* bytes) {
+  if (!c || !c->prof) return HF_EINVAL;
+  c->prof->collect();
+  if (i < 0 || i >= (int32_t)c->prof->recs.size()) return HF_EINVAL;
+  const ProfRec& r = c->prof->recs[i];
+  if (name) *name = r.name.c_str();
+  if (launches) *launches = r.launches;
+  if (total_ms) *total_ms = r.ms;
+  if (flops) *flops = r.flops;
+  if (bytes) *bytes = r.bytes;
+  return HF_OK;
+}
+
+}  // extern "C"

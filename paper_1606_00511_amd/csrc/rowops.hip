@@ -1,0 +1,255 @@
+// Output-layer and reduction kernels that sit between the GEMMs.
+//
+// softmax_xent: the softmax cross-entropy objective averaged over the batch
+//   (the f whose gradient Alg. 1 takes), its output-layer error
+//   delta_L = (p - e_y) / B and the probabilities p kept for the curvature
+//   products.
+// softmax_rop:  the output-layer factor of both curvature products, the
+//   Hessian of the batch-mean cross-entropy with respect to the logits applied
+//   to R{z}: (diag p - p p^T) R{z} / B per row (Sec. 2.1, after Alg. 1).
+// colsum / splitk_reduce: deterministic fixed-order reductions for the bias
+//   parts of the gradient and of the curvature products, and for split-K
+//   weight-gradient partials.
+//
+// One wave64 per row; the row is staged in LDS once and reused from there for
+// every pass, row reductions use wave shuffles.  Every sum runs in a fixed
+// order, so repeated calls give bit-identical results.
+#include "hf_internal.h"
+
+#include <mutex>
+
+namespace hfk {
+namespace {
+
+constexpr int ROWS_PER_BLOCK = 4;   // 4 waves, one row each
+constexpr int COLSUM_ROWS = 128;    // rows per partial in colsum
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace
+
+extern "C" __global__ __launch_bounds__(256) void hf_softmax_xent(
+    const float* __restrict__ Z, const int32_t* __restrict__ y, int B, int C,
+    int ld, float invB, float* __restrict__ P, float* __restrict__ D,
+    double* __restrict__ loss_part, int* __restrict__ err);
+extern "C" __global__ __launch_bounds__(256) void hf_softmax_rop(
+    const float* __restrict__ P, const float* __restrict__ RZ, int B, int C,
+    int ld, float invB, float* __restrict__ RD, const int* __restrict__ skip);
+
+namespace {
+// Rows of up to HF_MAX_CLASSES (4096) classes are staged in LDS: 64 KiB per
+// block for softmax_xent and 128 KiB for softmax_rop, above the default
+// dynamic-LDS limit, so the limit is raised once per process.
+void raise_lds_limits() {
+  static std::once_flag once;
+  std::call_once(once, [] {
+    (void)hipFuncSetAttribute((const void*)hf_softmax_xent,
+                        hipFuncAttributeMaxDynamicSharedMemorySize,
+                        ROWS_PER_BLOCK * 4096 * (int)sizeof(float));
+    (void)hipFuncSetAttribute((const void*)hf_softmax_rop,
+                        hipFuncAttributeMaxDynamicSharedMemorySize,
+                        ROWS_PER_BLOCK * 2 * 4096 * (int)sizeof(float));
+  });
+}
+}  // namespace
+
+extern "C" __global__ __launch_bounds__(256) void hf_softmax_xent(
+    const float* __restrict__ Z, const int32_t* __restrict__ y, int B, int C,
+    int ld, float invB, float* __restrict__ P, float* __restrict__ D,
+    double* __restrict__ loss_part, int* __restrict__ err) {
+  extern __shared__ float sm[];
+  __shared__ float wl[ROWS_PER_BLOCK];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * ROWS_PER_BLOCK + wave;
+  float* zs = sm + wave * C;
+  float li = 0.0f;
+  if (row < B) {
+    const float* z = Z + (size_t)row * ld;
+    float m = -INFINITY;
+    for (int c = lane; c < C; c += 64) {
+      const float t = z[c];
+      zs[c] = t;
+      m = fmaxf(m, t);
+    }
+    m = wave_max(m);
+    float sum = 0.0f;
+    for (int c = lane; c < C; c += 64) {
+      const float e = expf(zs[c] - m);
+      zs[c] = e;
+      sum += e;
+    }
+    sum = wave_sum(sum);
+    const float inv = 1.0f / sum;
+    int yi = -1;
+    if (y) {
+      yi = y[row];
+      if (yi < 0 || yi >= C) {
+        if (lane == 0) *err = 1;
+        yi = -1;
+      }
+    }
+    float* prow = P + (size_t)row * ld;
+    float* drow = D ? D + (size_t)row * ld : nullptr;
+    for (int c = lane; c < C; c += 64) {
+      const float p = zs[c] * inv;
+      prow[c] = p;
+      if (drow) drow[c] = (c == yi ? p - 1.0f : p) * invB;
+    }
+    if (yi >= 0) li = (m + logf(sum)) - z[yi];
+  }
+  if (lane == 0) wl[wave] = li;
+  __syncthreads();
+  if (threadIdx.x == 0 && loss_part)
+    loss_part[blockIdx.x] = ((double)wl[0] + (double)wl[1]) +
+                            ((double)wl[2] + (double)wl[3]);
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_loss_finalize(
+    const double* __restrict__ part, int nparts, double invB,
+    float* __restrict__ loss) {
+  __shared__ double ws[4];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < nparts; i += 256) s += part[i];
+  s = wave_sum_d(s);
+  if ((threadIdx.x & 63) == 0) ws[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) *loss = (float)(((ws[0] + ws[1]) + (ws[2] + ws[3])) * invB);
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_softmax_rop(
+    const float* __restrict__ P, const float* __restrict__ RZ, int B, int C,
+    int ld, float invB, float* __restrict__ RD, const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  extern __shared__ float sm[];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * ROWS_PER_BLOCK + wave;
+  if (row >= B) return;
+  float* ps = sm + wave * 2 * C;
+  float* rs = ps + C;
+  const float* prow = P + (size_t)row * ld;
+  const float* rrow = RZ + (size_t)row * ld;
+  float dot = 0.0f;
+  for (int c = lane; c < C; c += 64) {
+    const float p = prow[c], r = rrow[c];
+    ps[c] = p;
+    rs[c] = r;
+    dot += p * r;
+  }
+  dot = wave_sum(dot);
+  float* out = RD + (size_t)row * ld;
+  for (int c = lane; c < C; c += 64) out[c] = ps[c] * (rs[c] - dot) * invB;
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_colsum_part(
+    const float* __restrict__ D, int rows, int cols, int ld,
+    double* __restrict__ part, const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  const int r0 = blockIdx.y * COLSUM_ROWS;
+  const int r1 = min(rows, r0 + COLSUM_ROWS);
+  double s = 0.0;
+  for (int r = r0; r < r1; ++r) s += D[(size_t)r * ld + c];
+  part[(size_t)blockIdx.y * cols + c] = s;
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_colsum_final(
+    const double* __restrict__ part, int chunks, int cols,
+    float* __restrict__ out, const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  double s = 0.0;
+  for (int z = 0; z < chunks; ++z) s += part[(size_t)z * cols + c];
+  out[c] = (float)s;
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce(
+    const float* __restrict__ part, int splits, int M, int N,
+    float* __restrict__ out, int ldo, const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  const size_t mn = (size_t)M * N;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < mn;
+       i += (size_t)gridDim.x * 256) {
+    float s = 0.0f;
+    for (int z = 0; z < splits; ++z) s += part[(size_t)z * mn + i];
+    const size_t m = i / N, n = i - m * N;
+    out[m * ldo + n] = s;
+  }
+}
+
+// ------------------------------------------------------------- launchers
+void softmax_xent(const Launch& L, const float* Z, const int32_t* y, int B,
+                  int C, int ld, float* P, float* D, double* loss_part,
+                  int* err_flag) {
+  const int blocks = (B + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK;
+  const size_t lds = (size_t)ROWS_PER_BLOCK * C * sizeof(float);
+  raise_lds_limits();
+  prof_begin(L, "hf_softmax_xent");
+  hipLaunchKernelGGL(hf_softmax_xent, dim3(blocks), dim3(256), lds, L.stream,
+                     Z, y, B, C, ld, 1.0f / (float)B, P, D, loss_part, err_flag);
+  prof_end(L, "hf_softmax_xent", 0.0,
+           4.0 * B * C * (D ? 3.0 : 2.0) + (y ? 4.0 * B : 0.0));
+}
+
+void loss_finalize(const Launch& L, const double* loss_part, int nparts,
+                   int B, float* loss) {
+  prof_begin(L, "hf_loss_finalize");
+  hipLaunchKernelGGL(hf_loss_finalize, dim3(1), dim3(256), 0, L.stream,
+                     loss_part, nparts, 1.0 / (double)B, loss);
+  prof_end(L, "hf_loss_finalize", 0.0, 8.0 * nparts);
+}
+
+void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
+                 int C, int ld, float* RD, const int* skip) {
+  const int blocks = (B + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK;
+  const size_t lds = (size_t)ROWS_PER_BLOCK * 2 * C * sizeof(float);
+  raise_lds_limits();
+  prof_begin(L, "hf_softmax_rop");
+  hipLaunchKernelGGL(hf_softmax_rop, dim3(blocks), dim3(256), lds, L.stream,
+                     P, RZ, B, C, ld, 1.0f / (float)B, RD, skip);
+  prof_end(L, "hf_softmax_rop", 0.0, 12.0 * B * C);
+}
+
+int colsum_chunks(int rows) { return (rows + COLSUM_ROWS - 1) / COLSUM_ROWS; }
+
+void colsum(const Launch& L, const float* D, int rows, int cols, int ld,
+            double* part, float* out, const int* skip) {
+  const int chunks = colsum_chunks(rows);
+  const int cb = (cols + 255) / 256;
+  prof_begin(L, "hf_colsum_part");
+  hipLaunchKernelGGL(hf_colsum_part, dim3(cb, chunks), dim3(256), 0, L.stream,
+                     D, rows, cols, ld, part, skip);
+  prof_end(L, "hf_colsum_part", 0.0, 4.0 * rows * cols + 8.0 * chunks * cols);
+  prof_begin(L, "hf_colsum_final");
+  hipLaunchKernelGGL(hf_colsum_final, dim3(cb), dim3(256), 0, L.stream, part,
+                     chunks, cols, out, skip);
+  prof_end(L, "hf_colsum_final", 0.0, 8.0 * chunks * cols + 4.0 * cols);
+}
+
+void splitk_reduce(const Launch& L, const float* part, int splits, int M,
+                   int N, float* out, int ldo, const int* skip) {
+  const long long mn = (long long)M * N;
+  long long blocks = (mn + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  prof_begin(L, "hf_splitk_reduce");
+  hipLaunchKernelGGL(hf_splitk_reduce, dim3((unsigned)blocks), dim3(256), 0,
+                     L.stream, part, splits, M, N, out, ldo, skip);
+  prof_end(L, "hf_splitk_reduce", 0.0, 4.0 * mn * (splits + 1));
+}
+
+}  // namespace hfk

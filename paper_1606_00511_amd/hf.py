@@ -1,0 +1,244 @@
+"""Thin ctypes binding of the C ABI in ``include/hf.h``.
+
+Argument marshalling only: every step of the gradient, the curvature products
+and CG runs in the HIP kernels of ``libhf.so``.  PyTorch provides the device
+memory (the tensors and the workspace) and the stream.  There is no other
+backend: without the built library every call raises.
+"""
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhf.so")
+
+HF_SIGMOID, HF_TANH, HF_RELU = 0, 1, 2
+HF_HESSIAN, HF_GAUSS_NEWTON = 0, 1
+HF_FP32 = 0
+HF_OK, HF_EINVAL, HF_ENOMEM, HF_EHIP, HF_ELABEL, HF_ENUMERIC, HF_EWORKSPACE = \
+    0, -1, -2, -3, -4, -5, -6
+
+ACTS = {"sigmoid": HF_SIGMOID, "tanh": HF_TANH, "relu": HF_RELU}
+MODES = {"hessian": HF_HESSIAN, "gauss_newton": HF_GAUSS_NEWTON}
+
+# Every function declared in include/hf.h.
+EXPORTS = (
+    "hf_create", "hf_destroy", "hf_set_stream", "hf_num_params",
+    "hf_workspace_bytes", "hf_set_workspace", "hf_loss_grad", "hf_hvp",
+    "hf_cg", "hf_check", "hf_last_error", "hf_strerror", "hf_prof_enable",
+    "hf_prof_reset", "hf_prof_count", "hf_prof_get",
+)
+
+
+class hf_cg_info(ctypes.Structure):
+    _fields_ = [
+        ("iters", ctypes.c_int32), ("products", ctypes.c_int32),
+        ("neg_curv", ctypes.c_int32), ("neg_iter", ctypes.c_int32),
+        ("pBp", ctypes.c_double), ("pHp", ctypes.c_double),
+        ("gTd", ctypes.c_double), ("rr0", ctypes.c_double),
+        ("rr_final", ctypes.c_double), ("status", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+
+
+class HFError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("%s: %s" % (strerror(code), msg))
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """Load libhf.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            "libhf.so is not built (%s); run python -m paper_1606_00511_amd.build"
+            % LIB_PATH)
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    F32, D = ctypes.c_float, ctypes.c_double
+    sig = {
+        "hf_create": (ctypes.c_int, [ctypes.POINTER(I32), I32, I32, I32, I64,
+                                     ctypes.POINTER(P)]),
+        "hf_destroy": (ctypes.c_int, [P]),
+        "hf_set_stream": (ctypes.c_int, [P, P]),
+        "hf_num_params": (I64, [P]),
+        "hf_workspace_bytes": (SZ, [P]),
+        "hf_set_workspace": (ctypes.c_int, [P, P, SZ]),
+        "hf_loss_grad": (ctypes.c_int, [P, P, P, P, I64, P, P]),
+        "hf_hvp": (ctypes.c_int, [P, P, P, P, I64, P, I32, P]),
+        "hf_cg": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P, P,
+                                 ctypes.POINTER(hf_cg_info)]),
+        "hf_check": (ctypes.c_int, [P]),
+        "hf_last_error": (ctypes.c_char_p, [P]),
+        "hf_strerror": (ctypes.c_char_p, [I32]),
+        "hf_prof_enable": (ctypes.c_int, [P, I32]),
+        "hf_prof_reset": (ctypes.c_int, [P]),
+        "hf_prof_count": (I32, [P]),
+        "hf_prof_get": (ctypes.c_int, [P, I32, ctypes.POINTER(ctypes.c_char_p),
+                                       ctypes.POINTER(I64), ctypes.POINTER(D),
+                                       ctypes.POINTER(D), ctypes.POINTER(D)]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def strerror(code):
+    return lib().hf_strerror(code).decode()
+
+
+def _ptr(t, dtype, numel, what):
+    """Device pointer of a contiguous CUDA tensor, after checking it."""
+    import torch
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError("%s must be a CUDA tensor" % what)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (what, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % what)
+    if numel is not None and t.numel() != numel:
+        raise ValueError("%s has %d elements, expected %d" % (what, t.numel(), numel))
+    return t.data_ptr()
+
+
+class HFNet:
+    """One context of the C library plus its torch-allocated workspace.
+
+    dims: (d_0, ..., d_L); act: "sigmoid" | "tanh" | "relu"; max_batch: the
+    largest batch any call will use.  Calls run on torch's current stream.
+    """
+
+    def __init__(self, dims, act, max_batch, device="cuda"):
+        import torch
+        self.dims = tuple(int(d) for d in dims)
+        self.act = act
+        self.max_batch = int(max_batch)
+        L = lib()
+        arr = (ctypes.c_int32 * len(self.dims))(*self.dims)
+        h = ctypes.c_void_p()
+        rc = L.hf_create(arr, len(self.dims), ACTS[act], HF_FP32, self.max_batch,
+                         ctypes.byref(h))
+        if rc != HF_OK:
+            raise HFError(rc, "hf_create rejected dims=%s act=%s max_batch=%d"
+                          % (self.dims, act, self.max_batch))
+        self._h = h
+        self.n = int(L.hf_num_params(h))
+        nbytes = int(L.hf_workspace_bytes(h))
+        self.device = torch.device(device)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self._check(L.hf_set_workspace(h, self.workspace.data_ptr(), nbytes))
+
+    # ------------------------------------------------------------- plumbing
+    def _check(self, rc):
+        if rc != HF_OK:
+            raise HFError(rc, lib().hf_last_error(self._h).decode())
+        return rc
+
+    def _stream(self):
+        import torch
+        self._check(lib().hf_set_stream(self._h, torch.cuda.current_stream(
+            self.device).cuda_stream))
+
+    def close(self):
+        if getattr(self, "_h", None) is not None:
+            lib().hf_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _rows(self, X):
+        if X.dim() != 2 or X.shape[1] != self.dims[0]:
+            raise ValueError("X must be B x %d" % self.dims[0])
+        return int(X.shape[0])
+
+    # -------------------------------------------------------------- the ABI
+    def hf_loss_grad(self, W, X, y, loss=None, grad=None):
+        import torch
+        B = self._rows(X)
+        if loss is None:
+            loss = torch.empty(1, dtype=torch.float32, device=self.device)
+        if grad is None:
+            grad = torch.empty(self.n, dtype=torch.float32, device=self.device)
+        self._stream()
+        self._check(lib().hf_loss_grad(
+            self._h, _ptr(W, torch.float32, self.n, "W"),
+            _ptr(X, torch.float32, None, "X"), _ptr(y, torch.int32, B, "y"), B,
+            _ptr(loss, torch.float32, 1, "loss"),
+            _ptr(grad, torch.float32, self.n, "grad")))
+        return loss, grad
+
+    def hf_hvp(self, W, X, y, v, mode="hessian", out=None):
+        import torch
+        B = self._rows(X)
+        if out is None:
+            out = torch.empty(self.n, dtype=torch.float32, device=self.device)
+        self._stream()
+        self._check(lib().hf_hvp(
+            self._h, _ptr(W, torch.float32, self.n, "W"),
+            _ptr(X, torch.float32, None, "X"),
+            _ptr(y, torch.int32, B, "y") if y is not None else None, B,
+            _ptr(v, torch.float32, self.n, "v"), MODES[mode],
+            _ptr(out, torch.float32, self.n, "out")))
+        return out
+
+    def hf_cg(self, W, Xc, yc, g, damping, max_iters, mode="hessian",
+              rel_tol=0.0, step=None, neg_dir=None):
+        import torch
+        B = self._rows(Xc)
+        if step is None:
+            step = torch.empty(self.n, dtype=torch.float32, device=self.device)
+        if neg_dir is None:
+            neg_dir = torch.empty(self.n, dtype=torch.float32, device=self.device)
+        info = hf_cg_info()
+        self._stream()
+        rc = lib().hf_cg(
+            self._h, _ptr(W, torch.float32, self.n, "W"),
+            _ptr(Xc, torch.float32, None, "Xc"),
+            _ptr(yc, torch.int32, B, "yc") if yc is not None else None, B,
+            _ptr(g, torch.float32, self.n, "g"), float(damping), int(max_iters),
+            float(rel_tol), MODES[mode], _ptr(step, torch.float32, self.n, "step"),
+            _ptr(neg_dir, torch.float32, self.n, "neg_dir"), ctypes.byref(info))
+        self._check(rc)
+        return step, neg_dir, info.as_dict()
+
+    def hf_check(self):
+        self._check(lib().hf_check(self._h))
+
+    # ------------------------------------------------------------ profiling
+    def prof_enable(self, on=True):
+        self._check(lib().hf_prof_enable(self._h, 1 if on else 0))
+
+    def prof_reset(self):
+        self._check(lib().hf_prof_reset(self._h))
+
+    def prof_stats(self):
+        L = lib()
+        out = {}
+        for i in range(int(L.hf_prof_count(self._h))):
+            name = ctypes.c_char_p()
+            launches = ctypes.c_int64()
+            ms, fl, by = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+            self._check(L.hf_prof_get(self._h, i, ctypes.byref(name),
+                                      ctypes.byref(launches), ctypes.byref(ms),
+                                      ctypes.byref(fl), ctypes.byref(by)))
+            out[name.value.decode()] = dict(launches=launches.value, ms=ms.value,
+                                            flops=fl.value, bytes=by.value)
+        return out

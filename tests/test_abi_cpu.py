@@ -1,0 +1,100 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, every
+symbol include/hf.h declares is exported, and argument validation rejects
+bad input before any device call."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1606_00511_amd import hf as H
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(H.LIB_PATH):
+        from paper_1606_00511_amd.build import build_library
+        build_library()
+    return H.lib()
+
+
+def declared_functions():
+    txt = open(os.path.join(ROOT, "include", "hf.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    names = re.findall(r"\b(hf_[a-z_]+)\s*\(", txt)
+    return sorted(set(names))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(H.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def create(L, dims, act=H.HF_SIGMOID, prec=H.HF_FP32, max_batch=16):
+    arr = (ctypes.c_int32 * len(dims))(*dims)
+    h = ctypes.c_void_p()
+    rc = L.hf_create(arr, len(dims), act, prec, max_batch, ctypes.byref(h))
+    return rc, h
+
+
+def test_create_validates(L):
+    assert create(L, [4])[0] == H.HF_EINVAL                 # need L >= 1
+    assert create(L, [4, 0, 3])[0] == H.HF_EINVAL           # zero width
+    assert create(L, [4, -2, 3])[0] == H.HF_EINVAL
+    assert create(L, [4, 3], act=7)[0] == H.HF_EINVAL       # unknown act
+    assert create(L, [4, 3], prec=3)[0] == H.HF_EINVAL      # unknown precision
+    assert create(L, [4, 3], max_batch=0)[0] == H.HF_EINVAL
+    assert create(L, [4, 5000])[0] == H.HF_EINVAL           # > HF_MAX_CLASSES
+    assert create(L, [2] * 18)[0] == H.HF_EINVAL            # > HF_MAX_LAYERS
+    assert create(L, [1 << 20, 4096], max_batch=4096)[0] == H.HF_EINVAL  # 2^31
+    assert L.hf_create(None, 2, 0, 0, 4, None) == H.HF_EINVAL
+
+
+@pytest.mark.parametrize("dims", [(784, 100, 10), (784, 500, 500, 500, 10),
+                                  (440, 2048, 2048, 2048, 2048, 1973), (3, 1)])
+def test_num_params_and_workspace(L, dims):
+    rc, h = create(L, list(dims), max_batch=64)
+    assert rc == H.HF_OK
+    n = sum(dims[l] * (dims[l - 1] + 1) for l in range(1, len(dims)))
+    assert L.hf_num_params(h) == n
+    ws = L.hf_workspace_bytes(h)
+    assert ws > 4 * 3 * n  # at least the CG vectors
+    assert L.hf_destroy(h) == H.HF_OK
+
+
+def test_calls_without_workspace_or_with_bad_args(L):
+    rc, h = create(L, [8, 6, 4])
+    assert rc == H.HF_OK
+    n = L.hf_num_params(h)
+    fake = ctypes.c_void_p(1 << 20)   # never dereferenced: validation fails first
+    rc = L.hf_loss_grad(h, fake, fake, fake, 4, fake, fake)
+    assert rc == H.HF_EWORKSPACE
+    assert b"workspace" in L.hf_last_error(h)
+    # workspace argument checks happen before any device call
+    assert L.hf_set_workspace(h, None, 1 << 30) == H.HF_EINVAL
+    assert L.hf_set_workspace(h, ctypes.c_void_p(4096 + 16), 1 << 30) == H.HF_EINVAL
+    assert b"256-byte" in L.hf_last_error(h)
+    assert L.hf_set_workspace(h, ctypes.c_void_p(4096), 16) == H.HF_EWORKSPACE
+    info = H.hf_cg_info()
+    assert L.hf_cg(h, fake, fake, fake, 4, fake, 0.01, 5, 0.0, 0, fake, fake,
+                   ctypes.byref(info)) == H.HF_EWORKSPACE
+    assert L.hf_destroy(h) == H.HF_OK
+    assert n == 6 * 9 + 4 * 7
+
+
+def test_null_context(L):
+    assert L.hf_num_params(None) == -1
+    assert L.hf_workspace_bytes(None) == 0
+    assert L.hf_destroy(None) == H.HF_OK
+    assert L.hf_last_error(None) == b"null context"
+    assert L.hf_strerror(H.HF_ELABEL) == b"HF_ELABEL"
+    assert L.hf_set_stream(None, None) == H.HF_EINVAL
+    assert L.hf_check(None) == H.HF_EINVAL
+    assert L.hf_prof_count(None) == 0
