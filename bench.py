@@ -1,0 +1,218 @@
+"""Benchmark of the Hessian-free curvature path on one MI355X.
+
+One step is one pass of the whole hot path over the speech-frame-shaped
+workload (440-2048x4-1973 sigmoid network, batch 16,384, Zipf(1.1) labels
+over 1,973 classes, fp32):
+  1. loss + gradient on the batch                      (Alg. 1 step 1)
+  2. one exact Hessian-vector product H v              (Sec. 2.1)
+  3. one Gauss-Newton product G v                      (Sec. 2.1)
+  4. CG-Minimize on G + lambda I, 50 iterations        (Alg. 1 steps 3-4)
+  5. CG-Minimize on H + lambda I, up to 50 iterations, stopping at the first
+     negative-curvature direction                      (Sec. 2.1, 2.2)
+with lambda = 1e-2 and all inputs resident in HBM before timing starts.
+
+value = curvature-vector products per second over the timed steps (the
+stateless H v and G v plus every product inside both CG solves).
+
+Prints one JSON line (rank 0; there is only one GPU).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("curvature-vector products/sec (Hv & Gv) at batch B; "
+          "CG iteration ms; % MFMA peak")
+PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 matrix peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+DEFAULT_WORKLOAD = "speech_440_2048x4_1973_sigmoid_b16384"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=0,
+                    help="rows of the curvature batch the oracle sample uses "
+                         "(0 = all of them)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="before timing, copy a buffer of this many MiB with a "
+                         "plain device copy (reference point for HBM counters)")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, inp, rows):
+    """The fp64 oracle timed on this host's cores on a bounded sample: one
+    H v and one G v on the first `rows` rows, scaled to the full batch."""
+    from oracle import hf_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    rows = w.curv_batch if rows <= 0 else min(rows, w.curv_batch)
+    X, y = inp["X"][:rows], inp["y"][:rows]
+    th, v = inp["theta"], inp["v"]
+    t0 = time.perf_counter()
+    O.hvp(w.dims, w.act, th, X, y, v)
+    t1 = time.perf_counter()
+    O.gvp(w.dims, w.act, th, X, v)
+    t2 = time.perf_counter()
+    scale = w.curv_batch / float(rows)
+    per_product = 0.5 * ((t1 - t0) + (t2 - t1)) * scale
+    what = ("the full %d-row batch" % rows if rows == w.curv_batch else
+            "the first %d of %d rows, time scaled by %.0fx to the full batch"
+            % (rows, w.curv_batch, scale))
+    return {"value": 1.0 / per_product, "unit": "curvature-vector products/s",
+            "cores": cores, "kind": "oracle",
+            "sample": "fp64 NumPy oracle, one Hv and one Gv on %s (%.1f s measured)"
+                      % (what, t2 - t0)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU "
+              "path (asked for --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_1606_00511_amd import workloads as WL
+    from paper_1606_00511_amd.hf import HFNet
+
+    w = WL.WORKLOADS[args.workload]
+    inp = WL.make(w)
+    dev = torch.device("cuda:0")
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    W, X, y, v = d(inp["theta"]), d(inp["X"]), d(inp["y"]), d(inp["v"])
+    Xc, yc = X[:w.curv_batch].contiguous(), y[:w.curv_batch].contiguous()
+    net = HFNet(w.dims, w.act, max(w.batch, w.curv_batch))
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    grad = torch.empty(net.n, dtype=torch.float32, device=dev)
+    hv = torch.empty_like(grad)
+    gv = torch.empty_like(grad)
+    step_g, nd_g = torch.empty_like(grad), torch.empty_like(grad)
+    step_h, nd_h = torch.empty_like(grad), torch.empty_like(grad)
+    lam = w.damping
+
+    names = ["loss_grad", "hv", "gv", "cg_gn", "cg_hess"]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+
+    def step():
+        ev[0].record()
+        net.hf_loss_grad(W, X, y, loss, grad)
+        ev[1].record()
+        net.hf_hvp(W, Xc, yc, v, "hessian", hv)
+        ev[2].record()
+        net.hf_hvp(W, Xc, yc, v, "gauss_newton", gv)
+        ev[3].record()
+        _, _, ig = net.hf_cg(W, Xc, yc, grad, lam, w.cg_iters, "gauss_newton",
+                             step=step_g, neg_dir=nd_g)
+        ev[4].record()
+        _, _, ih = net.hf_cg(W, Xc, yc, grad, lam, w.cg_iters, "hessian",
+                             step=step_h, neg_dir=nd_h)
+        ev[5].record()
+        return ig, ih
+
+    if args.copy_probe_mib > 0:
+        nel = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(nel, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    net.prof_enable(True)
+    net.prof_reset()
+    comp = {k: 0.0 for k in names}
+    products = 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ig, ih = step()
+        products += 2 + ig["products"] + ih["products"]
+        torch.cuda.synchronize()
+        for i, k in enumerate(names):
+            comp[k] += ev[i].elapsed_time(ev[i + 1])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stats = net.prof_stats()
+    net.prof_enable(False)
+    elapsed = t1 - t0
+    K = args.steps
+
+    gemms = {k: s for k, s in stats.items() if k.startswith("hf_gemm")}
+    dom = max(gemms, key=lambda k: gemms[k]["ms"])
+    ds = gemms[dom]
+    achieved = ds["flops"] / (ds["ms"] * 1e-3) / 1e12
+    gemm_ms = sum(s["ms"] for s in gemms.values())
+    gemm_fl = sum(s["flops"] for s in gemms.values())
+    vec = {k: s for k, s in stats.items() if k in (
+        "hf_cg_curv_dot", "hf_cg_update", "hf_cg_dir")}
+    vec_ms = sum(s["ms"] for s in vec.values())
+    vec_b = sum(s["bytes"] for s in vec.values())
+
+    out = {
+        "metric": METRIC,
+        "value": products / elapsed,
+        "unit": "curvature-vector products/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * elapsed / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "dims": list(w.dims), "act": w.act,
+            "batch": w.batch, "curv_batch": w.curv_batch,
+            "cg_iters": w.cg_iters, "damping": lam,
+            "parallelism": "single GPU (one worker's share)",
+        },
+        "roofline": {
+            "bound": "mfma", "kernel": dom,
+            "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
+            "launches": ds["launches"], "avg_launch_ms": ds["ms"] / ds["launches"],
+            "flops_per_launch": ds["flops"] / ds["launches"],
+        },
+        "gemm_all": {"tflops": gemm_fl / (gemm_ms * 1e-3) / 1e12,
+                     "frac": gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_FP32_TFLOPS,
+                     "ms_per_step": gemm_ms / K},
+        "cg_vector": {"GB/s": vec_b / (vec_ms * 1e-3) / 1e9 if vec_ms else None,
+                      "frac_hbm": (vec_b / (vec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS)
+                      if vec_ms else None, "ms_per_step": vec_ms / K},
+        "components_ms": {k: comp[k] / K for k in names},
+        "cg_gn": {"iters": ig["iters"], "products": ig["products"],
+                  "ms_per_iter": comp["cg_gn"] / K / max(ig["products"], 1)},
+        "cg_hess": {"iters": ih["iters"], "products": ih["products"],
+                    "neg_curv": ih["neg_curv"], "neg_iter": ih["neg_iter"]},
+        "hv_per_s_stateless": 1e3 * K / comp["hv"],
+        "gv_per_s_stateless": 1e3 * K / comp["gv"],
+        "loss": float(loss.item()),
+        "kernels": {k: {"launches": s["launches"], "ms_per_step": s["ms"] / K,
+                        "avg_us": 1e3 * s["ms"] / max(s["launches"], 1),
+                        "tflops": s["flops"] / max(s["ms"], 1e-9) / 1e9,
+                        "gbs": s["bytes"] / max(s["ms"], 1e-9) / 1e6}
+                    for k, s in sorted(stats.items(), key=lambda kv: -kv[1]["ms"])},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -47,10 +47,11 @@ struct ProfRec {
 struct Profiler {
   std::vector<ProfRec> recs;
   std::map<std::string, int> index;
-  struct Pending { hipEvent_t a, b; int rec; };
+  struct Pending { hipEvent_t a, b; int rec; int tag; double flops, bytes; };
   std::vector<Pending> pending;
   std::vector<hipEvent_t> pool;
   hipEvent_t open = nullptr;
+  int tag = -1;   // CG iteration of the launches being recorded, -1 outside CG
 
   hipEvent_t get() {
     if (!pool.empty()) {
@@ -81,6 +82,41 @@ struct Profiler {
     }
     pending.clear();
   }
+  // Drop the launches of a CG solve that the device `done` flag turned into
+  // no-ops, so that only launches that did their work are counted.
+  // last = the last iteration that evaluated a product; stop_in_dot: the solve
+  // stopped in the curvature-dot kernel of that iteration (negative
+  // curvature or a non-finite kappa), so its update and direction kernels
+  // were no-ops; stop_in_update: the tolerance stopped it in the update
+  // kernel, so its direction kernel was a no-op; neg_iter: iteration whose
+  // negative-curvature kernels ran (-1: none).
+  void retract(int last, bool stop_in_dot, bool stop_in_update, int neg_iter) {
+    std::vector<Pending> keep;
+    keep.reserve(pending.size());
+    for (auto& p : pending) {
+      bool drop = false;
+      if (p.tag >= 0) {
+        const std::string& nm = recs[p.rec].name;
+        const bool is_neg = nm == "hf_cg_neg_dot" || nm == "hf_cg_neg_write";
+        if (p.tag > last) drop = true;
+        else if (is_neg) drop = p.tag != neg_iter;
+        else if (p.tag == last && stop_in_dot)
+          drop = nm == "hf_cg_update" || nm == "hf_cg_dir";
+        else if (p.tag == last && stop_in_update)
+          drop = nm == "hf_cg_dir";
+      }
+      if (drop) {
+        recs[p.rec].launches -= 1;
+        recs[p.rec].flops -= p.flops;
+        recs[p.rec].bytes -= p.bytes;
+        pool.push_back(p.a);
+        pool.push_back(p.b);
+      } else {
+        keep.push_back(p);
+      }
+    }
+    pending.swap(keep);
+  }
   ~Profiler() {
     collect();
     for (auto e : pool) hipEventDestroy(e);
@@ -104,7 +140,7 @@ void prof_end(const Launch& L, const char* name, double flops, double bytes) {
   hipEvent_t b = P.get();
   if (P.open && b) {
     hipEventRecord(b, L.stream);
-    P.pending.push_back({P.open, b, r});
+    P.pending.push_back({P.open, b, r, P.tag, flops, bytes});
   }
   P.open = nullptr;
   if (P.pending.size() > (1u << 16)) P.collect();
@@ -606,6 +642,7 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   cg_init(Lc, g, step, r, p, neg_dir, n, (double)damping,
           (double)rel_tol * (double)rel_tol, part, st);
   for (int j = 0; j < max_iters; ++j) {
+    if (c->prof) c->prof->tag = j;
     product_cached(c, W, Xc, b, p, mode, q, skip);
     cg_curv_dot(Lc, p, q, n, j, part, st);
     cg_neg(Lc, g, p, step, neg_dir, n, part, st);
@@ -621,6 +658,7 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
       if (c->pinned[(j - 1) & 1].done) break;
     }
   }
+  if (c->prof) c->prof->tag = -1;
   HIP_TRY(c, hipGetLastError());
   HIP_TRY(c, hipMemcpyAsync(&c->pinned[0], st, sizeof(CgState),
                             hipMemcpyDeviceToHost, c->stream));
@@ -629,6 +667,11 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
                             hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   const CgState& s = c->pinned[0];
+  if (c->prof) {
+    const bool stop_dot = s.neg || (s.status && s.iters < s.products);
+    const bool stop_upd = !stop_dot && s.done && s.iters == s.products;
+    c->prof->retract(s.products - 1, stop_dot, stop_upd, s.neg ? s.neg_iter : -1);
+  }
   info->iters = s.iters;
   info->products = s.products;
   info->neg_curv = s.neg;

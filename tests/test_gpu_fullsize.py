@@ -1,0 +1,136 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark uses (same context sizes, same batch, same kernels).
+
+The fp64 oracle is affordable on full batches for single products, so loss,
+gradient, H v and G v are compared over whole vectors (rel-L2 <= 1e-4).  For
+CG the oracle's cost grows with the iteration count, so each solve is
+compared up to a per-workload cap of iterations (identical counts, identical
+negative-curvature decision and sign); the full-budget GPU solve must then
+agree with the capped one on everything up to the cap.
+"""
+
+import gc
+
+import numpy as np
+import pytest
+
+from oracle import hf_oracle as O
+from paper_1606_00511_amd import workloads as WL
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+NAMES = list(WL.WORKLOADS)
+# CG iterations compared against the oracle: (hessian, gauss_newton)
+CAPS = {
+    "mnist_784_100_10_sigmoid_b1000": (10, 10),
+    "mnist_784_500x3_10_tanh_b10000": (50, 8),
+    "mnist_784_500x3_10_relu_b60000_c6000": (12, 6),
+    "speech_440_2048x4_1973_sigmoid_b16384": (4, 3),
+    "speech_440_2048x4_1973_sigmoid_b4096_c1024": (6, 5),
+}
+_cache = {}
+
+
+def rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def setup(name):
+    """Inputs (numpy and device) plus a context sized like the benchmark's."""
+    import torch
+    from paper_1606_00511_amd.hf import HFNet
+    if name in _cache:
+        return _cache[name]
+    for k in list(_cache):          # one workload resident at a time
+        _cache.pop(k)["net"].close()
+    gc.collect()
+    torch.cuda.empty_cache()
+    w = WL.WORKLOADS[name]
+    inp = WL.make(w)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+    st = dict(w=w, inp=inp, W=d(inp["theta"]), X=d(inp["X"]), y=d(inp["y"]),
+              v=d(inp["v"]), Xc=d(inp["X"][:w.curv_batch]),
+              yc=d(inp["y"][:w.curv_batch]),
+              net=HFNet(w.dims, w.act, max(w.batch, w.curv_batch)))
+    _cache[name] = st
+    return st
+
+
+def host(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_full_loss_grad(name):
+    s = setup(name)
+    w, inp = s["w"], s["inp"]
+    loss, grad = s["net"].hf_loss_grad(s["W"], s["X"], s["y"])
+    s["net"].hf_check()
+    f_o, g_o = O.loss_grad(w.dims, w.act, inp["theta"], inp["X"], inp["y"])
+    s["grad"] = grad
+    s["g_np"] = host(grad)
+    print("%s loss %.6f vs %.6f, grad rel %.2e" % (
+        name, float(host(loss)[0]), f_o, rel(s["g_np"], g_o)))
+    assert abs(float(host(loss)[0]) - f_o) <= TOL * abs(f_o)
+    assert rel(s["g_np"], g_o) <= TOL
+
+
+@pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
+@pytest.mark.parametrize("name", NAMES)
+def test_full_product(name, mode):
+    s = setup(name)
+    w, inp = s["w"], s["inp"]
+    out = host(s["net"].hf_hvp(s["W"], s["Xc"], s["yc"], s["v"], mode))
+    Xc, yc = inp["X"][:w.curv_batch], inp["y"][:w.curv_batch]
+    ref = O.curvature(w.dims, w.act, inp["theta"], Xc, yc, inp["v"], mode)
+    e = rel(out, ref)
+    print("%s %s rel %.2e" % (name, mode, e))
+    assert e <= TOL
+
+
+@pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
+@pytest.mark.parametrize("name", NAMES)
+def test_full_cg(name, mode):
+    s = setup(name)
+    w, inp = s["w"], s["inp"]
+    if "grad" not in s:
+        s["grad"] = s["net"].hf_loss_grad(s["W"], s["X"], s["y"])[1]
+        s["g_np"] = host(s["grad"])
+    cap = CAPS[name][0 if mode == "hessian" else 1]
+    lam = w.damping
+    Xc, yc = inp["X"][:w.curv_batch], inp["y"][:w.curv_batch]
+    oi = O.cg_network(w.dims, w.act, inp["theta"], Xc, yc,
+                      s["g_np"].astype(np.float64), lam, cap, mode)
+    step, nd, gi = s["net"].hf_cg(s["W"], s["Xc"], s["yc"], s["grad"], lam,
+                                  cap, mode)
+    step = host(step)
+    print("%s %s cap %d: gpu %s | oracle iters %d products %d neg %d pBp %.4g"
+          % (name, mode, cap, {k: gi[k] for k in ("iters", "products", "neg_curv",
+                                                   "neg_iter", "pBp")},
+             oi["iters"], oi["products"], oi["neg_curv"], oi["pBp"]))
+    assert gi["iters"] == oi["iters"]
+    assert gi["products"] == oi["products"]
+    assert gi["neg_curv"] == oi["neg_curv"]
+    assert gi["neg_iter"] == oi["neg_iter"]
+    if oi["neg_curv"]:
+        assert np.sign(gi["pBp"]) == np.sign(oi["pBp"])
+        assert gi["pBp"] == pytest.approx(oi["pBp"], rel=1e-3)
+        assert gi["gTd"] <= 0.0
+        assert rel(host(nd), oi["neg_dir"]) <= 1e-3
+    assert rel(step, oi["step"]) <= 1e-3
+    # the full-budget solve agrees with the capped one
+    step2, nd2, g2 = s["net"].hf_cg(s["W"], s["Xc"], s["yc"], s["grad"], lam,
+                                    w.cg_iters, mode)
+    if oi["neg_curv"]:
+        assert (g2["iters"], g2["products"], g2["neg_iter"]) == \
+            (gi["iters"], gi["products"], gi["neg_iter"])
+        assert np.array_equal(host(step2), step)
+    else:
+        assert g2["products"] >= gi["products"]
+        if mode == "gauss_newton":
+            assert g2["neg_curv"] == 0 and g2["iters"] == w.cg_iters
