@@ -105,8 +105,12 @@ def phi(act, z):
     raise ValueError(act)
 
 
-def dphi(act, z):
-    """phi'(z), written directly from the definition of each activation."""
+def dphi(act, z, kink=0.0):
+    """phi'(z), written directly from the definition of each activation.
+
+    ``kink`` moves ReLU's step: phi'(z) = 1[z > kink].  The method uses
+    kink = 0 (ReLU'(0) = 0); tests evaluate kink = -tau and +tau to bound
+    the effect of pre-activations that lie within fp32 rounding of 0."""
     if act == "sigmoid":
         s = 1.0 / (1.0 + np.exp(-z))
         return s * (1.0 - s)
@@ -114,7 +118,7 @@ def dphi(act, z):
         t = np.tanh(z)
         return 1.0 - t * t
     if act == "relu":
-        return (z > 0.0).astype(np.float64)     # reading: ReLU'(0) = 0
+        return (z > kink).astype(np.float64)    # reading: ReLU'(0) = 0
     raise ValueError(act)
 
 
@@ -167,7 +171,7 @@ def loss(dims, act, theta, X, y):
     return float(np.mean(lse - z[np.arange(z.shape[0]), y]))
 
 
-def loss_grad(dims, act, theta, X, y):
+def loss_grad(dims, act, theta, X, y, kink=0.0):
     """(f, g) with g = grad f by backpropagation (Alg. 1 step 1; Alg. 2)."""
     layers = unpack(theta, dims)
     Z, A = forward(dims, act, theta, X)
@@ -183,11 +187,11 @@ def loss_grad(dims, act, theta, X, y):
         W, _ = layers[l - 1]
         grads[l - 1] = (delta.T @ A[l - 1], delta.sum(axis=0))
         if l > 1:
-            delta = (delta @ W) * dphi(act, Z[l - 2])  # df/dZ_{l-1}
+            delta = (delta @ W) * dphi(act, Z[l - 2], kink)  # df/dZ_{l-1}
     return f, pack(grads)
 
 
-def _r_forward(dims, act, theta, v, X):
+def _r_forward(dims, act, theta, v, X, kink=0.0):
     """Directional derivatives RZ_l = d Z_l / de along theta + e v."""
     layers = unpack(theta, dims)
     vlayers = unpack(v, dims)
@@ -199,15 +203,15 @@ def _r_forward(dims, act, theta, v, X):
         rz = A[l - 1] @ V.T + c + RA[l - 1] @ W.T
         RZ.append(rz)
         if l < len(layers):
-            RA.append(dphi(act, Z[l - 1]) * rz)
+            RA.append(dphi(act, Z[l - 1], kink) * rz)
     return layers, vlayers, Z, A, RZ, RA
 
 
-def hvp(dims, act, theta, X, y, v):
+def hvp(dims, act, theta, X, y, v, kink=0.0):
     """Exact H v by the R-operator: the directional derivative of the
     backpropagation program of ``loss_grad`` (Sec. 2.1, paragraph after
     Alg. 1)."""
-    layers, vlayers, Z, A, RZ, RA = _r_forward(dims, act, theta, v, X)
+    layers, vlayers, Z, A, RZ, RA = _r_forward(dims, act, theta, v, X, kink)
     B = Z[-1].shape[0]
     y = np.asarray(y, dtype=np.int64)
     P = softmax(Z[-1])
@@ -226,20 +230,20 @@ def hvp(dims, act, theta, X, y, v):
             e = delta @ W
             re = rdelta @ W + delta @ V
             zp = Z[l - 2]
-            new_delta = e * dphi(act, zp)
-            rdelta = re * dphi(act, zp) + e * d2phi(act, zp) * RZ[l - 2]
+            new_delta = e * dphi(act, zp, kink)
+            rdelta = re * dphi(act, zp, kink) + e * d2phi(act, zp) * RZ[l - 2]
             delta = new_delta
     return pack(out)
 
 
-def gvp(dims, act, theta, X, v):
+def gvp(dims, act, theta, X, v, kink=0.0):
     """Gauss-Newton G v = J^T H_L J v (Sec. 2.1, paragraph after Alg. 1).
 
     J v is the R-forward pass; H_L is the Hessian of the batch-mean softmax
     cross-entropy with respect to the logits, (diag p_i - p_i p_i^T) / B per
     row; J^T is ordinary backpropagation of that vector.  No labels enter.
     """
-    layers, vlayers, Z, A, RZ, RA = _r_forward(dims, act, theta, v, X)
+    layers, vlayers, Z, A, RZ, RA = _r_forward(dims, act, theta, v, X, kink)
     B = Z[-1].shape[0]
     P = softmax(Z[-1])
     u = P * (RZ[-1] - (P * RZ[-1]).sum(axis=1, keepdims=True)) / B
@@ -248,16 +252,16 @@ def gvp(dims, act, theta, X, v):
         W, _ = layers[l - 1]
         out[l - 1] = (u.T @ A[l - 1], u.sum(axis=0))
         if l > 1:
-            u = (u @ W) * dphi(act, Z[l - 2])
+            u = (u @ W) * dphi(act, Z[l - 2], kink)
     return pack(out)
 
 
-def curvature(dims, act, theta, X, y, v, mode):
+def curvature(dims, act, theta, X, y, v, mode, kink=0.0):
     """H v for mode 'hessian', G v for mode 'gauss_newton'."""
     if mode == "hessian":
-        return hvp(dims, act, theta, X, y, v)
+        return hvp(dims, act, theta, X, y, v, kink)
     if mode == "gauss_newton":
-        return gvp(dims, act, theta, X, v)
+        return gvp(dims, act, theta, X, v, kink)
     raise ValueError(mode)
 
 

@@ -74,7 +74,7 @@ struct Profiler {
   }
   void collect() {
     for (auto& p : pending) {
-      hipEventSynchronize(p.b);
+      (void)hipEventSynchronize(p.b);
       float ms = 0.0f;
       if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) recs[p.rec].ms += ms;
       pool.push_back(p.a);
@@ -119,7 +119,7 @@ struct Profiler {
   }
   ~Profiler() {
     collect();
-    for (auto e : pool) hipEventDestroy(e);
+    for (auto e : pool) (void)hipEventDestroy(e);
   }
 };
 
@@ -127,7 +127,7 @@ void prof_begin(const Launch& L, const char* name) {
   (void)name;
   if (!L.prof) return;
   L.prof->open = L.prof->get();
-  if (L.prof->open) hipEventRecord(L.prof->open, L.stream);
+  if (L.prof->open) (void)hipEventRecord(L.prof->open, L.stream);
 }
 
 void prof_end(const Launch& L, const char* name, double flops, double bytes) {
@@ -139,7 +139,7 @@ void prof_end(const Launch& L, const char* name, double flops, double bytes) {
   P.recs[r].bytes += bytes;
   hipEvent_t b = P.get();
   if (P.open && b) {
-    hipEventRecord(b, L.stream);
+    (void)hipEventRecord(b, L.stream);
     P.pending.push_back({P.open, b, r, P.tag, flops, bytes});
   }
   P.open = nullptr;
@@ -470,9 +470,9 @@ int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
 int hf_destroy(hf_ctx* c) {
   if (!c) return HF_OK;
   delete c->prof;
-  if (c->pinned) hipHostFree(c->pinned);
+  if (c->pinned) (void)hipHostFree(c->pinned);
   for (auto& e : c->ev)
-    if (e) hipEventDestroy(e);
+    if (e) (void)hipEventDestroy(e);
   delete c;
   return HF_OK;
 }

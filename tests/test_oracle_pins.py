@@ -408,18 +408,18 @@ def test_planted_wrong_sign_in_output_hessian_is_caught(monkeypatch):
     # every term is right; flip the sign of the R-forward bias term
     orig = O._r_forward
 
-    def bad_rf(dims, act, theta, v, X):
+    def bad_rf(dims, act, theta, v, X, kink=0.0):
         vv = v.copy()
         layers = O.unpack(vv, dims)
         for W, b in layers:
             b *= -1.0
-        return orig(dims, act, theta, vv, X)
+        return orig(dims, act, theta, vv, X, kink)
     monkeypatch.setattr(O, "_r_forward", bad_rf)
     assert _fd_hv_error("tanh") > 1e-4
 
 
 def test_planted_wrong_activation_derivative_is_caught(monkeypatch):
-    monkeypatch.setattr(O, "dphi", lambda act, z: 1.0 - np.tanh(z))
+    monkeypatch.setattr(O, "dphi", lambda act, z, kink=0.0: 1.0 - np.tanh(z))
     p, th = tiny("tanh")
     dims = p["dims"]
     _, g = O.loss_grad(dims, "tanh", th, p["X"], p["y"])
@@ -436,3 +436,20 @@ def test_planted_unoriented_direction_is_caught(monkeypatch):
     gd = read_golden("cg_hand_cases.txt")
     r = O.cg_minimize(diag_op(gd["case1.A_diag"]), np.array(gd["case1.g"]), 0.0, 10)
     assert not np.allclose(r["neg_dir"], gd["case1.neg_dir"])
+
+
+def test_relu_kink_threshold_only_moves_the_step():
+    """kink = 0 is the method's ReLU'(0) = 0; a shifted kink changes only
+    the units whose pre-activation lies between 0 and the shift."""
+    p, th = tiny("relu", dims=(6, 8, 8, 4), B=20)
+    dims = p["dims"]
+    v = p["v"].astype(np.float64)
+    base = O.hvp(dims, "relu", th, p["X"], p["y"], v)
+    assert np.array_equal(base, O.hvp(dims, "relu", th, p["X"], p["y"], v, kink=0.0))
+    Z, _ = O.forward(dims, "relu", th, p["X"])
+    zmin = min(np.abs(z).min() for z in Z[:-1])
+    # a shift smaller than every |z| changes nothing
+    assert np.array_equal(base, O.hvp(dims, "relu", th, p["X"], p["y"], v,
+                                      kink=0.5 * zmin))
+    assert np.array_equal(O.gvp(dims, "relu", th, p["X"], v),
+                          O.gvp(dims, "relu", th, p["X"], v, kink=-0.5 * zmin))
