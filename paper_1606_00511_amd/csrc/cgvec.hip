@@ -7,13 +7,19 @@
 //   alpha = rr / kappa;  x += alpha p;  r += alpha (A p + lambda p)
 //   rr' = r.r;  beta = rr' / rr;  p = -r + beta p
 //
-// The scalars live in a CgState in device memory and never travel to the
-// host inside the loop.  Each dot product is a grid of blocks that reduce
-// float data in double precision (wave shuffles, then LDS across the 4
-// waves); the last block to finish (atomic ticket) sums the per-block
-// partials in block order and updates the state, so every sum has a fixed
-// order and repeated solves are bit-identical.  After a stop every kernel
-// reads `done` and returns at once.
+// Kernel schedule of iteration j (all on one stream):
+//   dot     per-block partials of p.q and p.p
+//   update  every block sums the dot partials in block order (so all blocks
+//           hold the same kappa), takes the stop decision, and if it goes on
+//           updates x and r and writes per-block partials of r.r
+//   neg_dot / neg_write  only at a detection: g.p, then d~ and the step
+//   dir     every block sums the r.r partials in block order, forms beta
+//           and updates p
+// Block 0 of update and dir records the scalars in a CgState in device
+// memory; rr is kept in two slots indexed by the iteration's parity so that
+// no block reads a slot that another block of the same kernel writes.  No
+// fences or atomics are needed, every sum has a fixed order, and repeated
+// solves are bit-identical.  Once `done` is set every kernel returns at once.
 #include "hf_internal.h"
 
 namespace hfk {
@@ -30,48 +36,29 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
-// Sum over the block in a fixed order; the result is valid in thread 0.
+// Fixed-order block sum; the result is returned to every thread.
 __device__ __forceinline__ double block_sum(double v, double* sh) {
   v = wave_sum(v);
   const int w = threadIdx.x >> 6;
+  __syncthreads();
   if ((threadIdx.x & 63) == 0) sh[w] = v;
   __syncthreads();
-  double r = 0.0;
-  if (threadIdx.x == 0) r = (sh[0] + sh[1]) + (sh[2] + sh[3]);
-  __syncthreads();
-  return r;
+  return (sh[0] + sh[1]) + (sh[2] + sh[3]);
 }
 
-// Publish this block's partials, then report whether it is the last block.
-template <int K>
-__device__ __forceinline__ bool publish(const double (&v)[K], double* part,
-                                        unsigned int* counter, double* sh) {
-  __shared__ bool last;
-  double r[K];
-#pragma unroll
-  for (int k = 0; k < K; ++k) r[k] = block_sum(v[k], sh);
-  if (threadIdx.x == 0) {
-#pragma unroll
-    for (int k = 0; k < K; ++k) part[(size_t)k * MAX_GRID + blockIdx.x] = r[k];
-    __threadfence();
-    const unsigned int t = atomicAdd(counter, 1u);
-    last = (t == gridDim.x - 1);
-  }
-  __syncthreads();
-  if (last) __threadfence();
-  return last;
-}
-
-// In the last block: the fixed-order total of partial k over all blocks.
-__device__ __forceinline__ double gather(const double* part, int k,
-                                         double* sh) {
+// Fixed-order total of nb per-block partials (same value in every block).
+__device__ __forceinline__ double total(const double* part, int nb, double* sh) {
   double s = 0.0;
-  for (int b = threadIdx.x; b < (int)gridDim.x; b += NT)
-    s += part[(size_t)k * MAX_GRID + b];
+  for (int b = threadIdx.x; b < nb; b += NT) s += part[b];
   return block_sum(s, sh);
 }
 
 __device__ __forceinline__ bool is_fin(double x) { return isfinite(x); }
+
+__device__ __forceinline__ double dot4(f32x4 a, f32x4 b) {
+  return ((double)a[0] * b[0] + (double)a[1] * b[1]) +
+         ((double)a[2] * b[2] + (double)a[3] * b[3]);
+}
 
 }  // namespace
 
@@ -82,212 +69,217 @@ extern "C" __global__ void hf_cg_reset(CgState* __restrict__ st) {
   }
 }
 
+// x = 0, r = g, p = -g, d~ = 0, partials of g.g
 extern "C" __global__ __launch_bounds__(256) void hf_cg_init(
     const float* __restrict__ g, float* __restrict__ x, float* __restrict__ r,
-    float* __restrict__ p, float* __restrict__ nd, long long n, double lambda,
-    double tol2, double* __restrict__ part, CgState* __restrict__ st) {
+    float* __restrict__ p, float* __restrict__ nd, long long n,
+    double* __restrict__ part) {
   __shared__ double sh[4];
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
   double s = 0.0;
   const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n4; i += stride) {
+  for (long long i = t0; i < n4; i += stride) {
     const f32x4 gv = ((const f32x4*)g)[i];
     ((f32x4*)x)[i] = z4;
     ((f32x4*)r)[i] = gv;
     ((f32x4*)p)[i] = -gv;
     ((f32x4*)nd)[i] = z4;
-    s += (double)gv[0] * gv[0] + (double)gv[1] * gv[1] +
-         (double)gv[2] * gv[2] + (double)gv[3] * gv[3];
+    s += dot4(gv, gv);
   }
-  for (long long i = n4 * 4 + (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride) {
+  for (long long i = n4 * 4 + t0; i < n; i += stride) {
     const float gv = g[i];
     x[i] = 0.f; r[i] = gv; p[i] = -gv; nd[i] = 0.f;
     s += (double)gv * gv;
   }
-  const double v[1] = {s};
-  if (!publish<1>(v, part, &st->counter[0], sh)) return;
-  const double rr = gather(part, 0, sh);
+  s = block_sum(s, sh);
+  if (threadIdx.x == 0) part[blockIdx.x] = s;
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_cg_init_fin(
+    const double* __restrict__ part, int nb, double lambda, double tol2,
+    CgState* __restrict__ st) {
+  __shared__ double sh[4];
+  const double rr = total(part, nb, sh);
   if (threadIdx.x == 0) {
-    st->rr = rr;
+    st->rr[0] = rr;
+    st->rr[1] = rr;
     st->rr0 = rr;
     st->lambda = lambda;
     st->tol2 = tol2;
-    st->kappa = st->alpha = st->beta = st->pp = st->pq = st->gp = 0.0;
-    st->neg = 0;
-    st->neg_pending = 0;
     st->neg_iter = -1;
-    st->iters = 0;
-    st->products = 0;
-    st->j = 0;
     st->status = is_fin(rr) ? 0 : -5;
     st->done = (rr == 0.0 || !is_fin(rr)) ? 1 : 0;
-    st->counter[0] = 0;
   }
 }
 
-extern "C" __global__ __launch_bounds__(256) void hf_cg_curv_dot(
+extern "C" __global__ __launch_bounds__(256) void hf_cg_dot(
     const float* __restrict__ p, const float* __restrict__ q, long long n,
-    int j, double* __restrict__ part, CgState* __restrict__ st) {
+    double* __restrict__ part, const CgState* __restrict__ st) {
   if (st->done) return;
   __shared__ double sh[4];
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
   double pq = 0.0, pp = 0.0;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n4; i += stride) {
-    const f32x4 a = ((const f32x4*)p)[i];
-    const f32x4 b = ((const f32x4*)q)[i];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      pq += (double)a[c] * b[c];
-      pp += (double)a[c] * a[c];
-    }
+  long long i = t0;
+  for (; i + stride < n4; i += 2 * stride) {
+    const f32x4 a0 = ((const f32x4*)p)[i], a1 = ((const f32x4*)p)[i + stride];
+    const f32x4 b0 = ((const f32x4*)q)[i], b1 = ((const f32x4*)q)[i + stride];
+    pq += dot4(a0, b0) + dot4(a1, b1);
+    pp += dot4(a0, a0) + dot4(a1, a1);
   }
-  for (long long i = n4 * 4 + (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride) {
-    pq += (double)p[i] * q[i];
-    pp += (double)p[i] * p[i];
+  for (; i < n4; i += stride) {
+    const f32x4 a = ((const f32x4*)p)[i], b = ((const f32x4*)q)[i];
+    pq += dot4(a, b);
+    pp += dot4(a, a);
   }
-  const double v[2] = {pq, pp};
-  if (!publish<2>(v, part, &st->counter[1], sh)) return;
-  const double tpq = gather(part, 0, sh);
-  const double tpp = gather(part, 1, sh);
+  for (long long e = n4 * 4 + t0; e < n; e += stride) {
+    pq += (double)p[e] * q[e];
+    pp += (double)p[e] * p[e];
+  }
+  pq = block_sum(pq, sh);
+  pp = block_sum(pp, sh);
   if (threadIdx.x == 0) {
-    const double kappa = tpq + st->lambda * tpp;
-    st->pq = tpq;
-    st->pp = tpp;
+    part[blockIdx.x] = pq;
+    part[MAX_GRID + blockIdx.x] = pp;
+  }
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
+    float* __restrict__ x, float* __restrict__ r, const float* __restrict__ p,
+    const float* __restrict__ q, long long n, int j,
+    const double* __restrict__ dpart, double* __restrict__ rpart,
+    CgState* __restrict__ st) {
+  if (st->done) return;
+  __shared__ double sh[4];
+  const int nb = gridDim.x;
+  const double pq = total(dpart, nb, sh);
+  const double pp = total(dpart + MAX_GRID, nb, sh);
+  const double lam = st->lambda;
+  const double kappa = pq + lam * pp;
+  const double rr = st->rr[j & 1];
+  const bool stop = !is_fin(kappa) || kappa <= 0.0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
     st->kappa = kappa;
+    st->pq = pq;
+    st->pp = pp;
     st->products = j + 1;
-    st->j = j;
     if (!is_fin(kappa)) {
       st->status = -5;
       st->done = 1;
     } else if (kappa <= 0.0) {
       st->neg = 1;
-      st->neg_pending = 1;
       st->neg_iter = j;
       st->done = 1;
     } else {
-      st->alpha = st->rr / kappa;
+      st->alpha = rr / kappa;
     }
-    st->counter[1] = 0;
   }
+  if (stop) return;
+  const float alpha = (float)(rr / kappa);
+  const float lamf = (float)lam;
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  double s = 0.0;
+  for (long long i = t0; i < n4; i += stride) {
+    const f32x4 pv = ((const f32x4*)p)[i];
+    const f32x4 qv = ((const f32x4*)q)[i];
+    f32x4 xv = ((f32x4*)x)[i];
+    f32x4 rv = ((f32x4*)r)[i];
+    xv += alpha * pv;
+    rv += alpha * (qv + lamf * pv);
+    ((f32x4*)x)[i] = xv;
+    ((f32x4*)r)[i] = rv;
+    s += dot4(rv, rv);
+  }
+  for (long long e = n4 * 4 + t0; e < n; e += stride) {
+    const float pv = p[e];
+    x[e] += alpha * pv;
+    const float rv = r[e] + alpha * (q[e] + lamf * pv);
+    r[e] = rv;
+    s += (double)rv * rv;
+  }
+  s = block_sum(s, sh);
+  if (threadIdx.x == 0) rpart[blockIdx.x] = s;
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_neg_dot(
     const float* __restrict__ g, const float* __restrict__ p, long long n,
-    double* __restrict__ part, CgState* __restrict__ st) {
-  if (!st->neg_pending) return;
+    int j, double* __restrict__ part, const CgState* __restrict__ st) {
+  if (!st->neg || st->neg_iter != j) return;
   __shared__ double sh[4];
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
   double gp = 0.0;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n4; i += stride) {
-    const f32x4 a = ((const f32x4*)g)[i];
-    const f32x4 b = ((const f32x4*)p)[i];
-    gp += (double)a[0] * b[0] + (double)a[1] * b[1] + (double)a[2] * b[2] +
-          (double)a[3] * b[3];
-  }
-  for (long long i = n4 * 4 + (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride)
-    gp += (double)g[i] * p[i];
-  const double v[1] = {gp};
-  if (!publish<1>(v, part, &st->counter[2], sh)) return;
-  const double t = gather(part, 0, sh);
-  if (threadIdx.x == 0) {
-    st->gp = t;
-    st->counter[2] = 0;
-  }
+  for (long long i = t0; i < n4; i += stride)
+    gp += dot4(((const f32x4*)g)[i], ((const f32x4*)p)[i]);
+  for (long long e = n4 * 4 + t0; e < n; e += stride) gp += (double)g[e] * p[e];
+  gp = block_sum(gp, sh);
+  if (threadIdx.x == 0) part[blockIdx.x] = gp;
 }
 
 // d~ = -sgn(g.p) p with sgn(0) = +1; the step is -g when the detection
 // happened at the first iteration, else the current iterate.
 extern "C" __global__ __launch_bounds__(256) void hf_cg_neg_write(
     const float* __restrict__ g, const float* __restrict__ p,
-    float* __restrict__ x, float* __restrict__ nd, long long n,
-    CgState* __restrict__ st) {
-  if (!st->neg_pending) return;
-  const float coef = st->gp >= 0.0 ? -1.0f : 1.0f;
-  const bool first = st->neg_iter == 0;
+    float* __restrict__ x, float* __restrict__ nd, long long n, int j,
+    const double* __restrict__ part, CgState* __restrict__ st) {
+  if (!st->neg || st->neg_iter != j) return;
+  __shared__ double sh[4];
+  const double gp = total(part, gridDim.x, sh);
+  if (blockIdx.x == 0 && threadIdx.x == 0) st->gp = gp;
+  const float coef = gp >= 0.0 ? -1.0f : 1.0f;
+  const bool first = j == 0;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n4; i += stride) {
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  for (long long i = t0; i < n4; i += stride) {
     ((f32x4*)nd)[i] = coef * ((const f32x4*)p)[i];
     if (first) ((f32x4*)x)[i] = -((const f32x4*)g)[i];
   }
-  for (long long i = n4 * 4 + (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride) {
-    nd[i] = coef * p[i];
-    if (first) x[i] = -g[i];
-  }
-  __shared__ bool last;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    last = atomicAdd(&st->counter[3], 1u) == gridDim.x - 1;
-  }
-  __syncthreads();
-  if (last && threadIdx.x == 0) {
-    st->neg_pending = 0;
-    st->counter[3] = 0;
-  }
-}
-
-extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
-    float* __restrict__ x, float* __restrict__ r, const float* __restrict__ p,
-    const float* __restrict__ q, long long n, double* __restrict__ part,
-    CgState* __restrict__ st) {
-  if (st->done) return;
-  __shared__ double sh[4];
-  const float alpha = (float)st->alpha;
-  const float lam = (float)st->lambda;
-  const long long n4 = n >> 2;
-  const long long stride = (long long)gridDim.x * NT;
-  double rr = 0.0;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n4; i += stride) {
-    const f32x4 pv = ((const f32x4*)p)[i];
-    const f32x4 qv = ((const f32x4*)q)[i];
-    f32x4 xv = ((f32x4*)x)[i];
-    f32x4 rv = ((f32x4*)r)[i];
-    xv += alpha * pv;
-    rv += alpha * (qv + lam * pv);
-    ((f32x4*)x)[i] = xv;
-    ((f32x4*)r)[i] = rv;
-    rr += (double)rv[0] * rv[0] + (double)rv[1] * rv[1] +
-          (double)rv[2] * rv[2] + (double)rv[3] * rv[3];
-  }
-  for (long long i = n4 * 4 + (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride) {
-    const float pv = p[i];
-    x[i] += alpha * pv;
-    const float rv = r[i] + alpha * (q[i] + lam * pv);
-    r[i] = rv;
-    rr += (double)rv * rv;
-  }
-  const double v[1] = {rr};
-  if (!publish<1>(v, part, &st->counter[0], sh)) return;
-  const double t = gather(part, 0, sh);
-  if (threadIdx.x == 0) {
-    st->iters = st->j + 1;
-    if (!is_fin(t)) {
-      st->status = -5;
-      st->done = 1;
-    } else {
-      st->beta = t / st->rr;
-      st->rr = t;
-      if (st->tol2 > 0.0 && t <= st->tol2 * st->rr0) st->done = 1;
-    }
-    st->counter[0] = 0;
+  for (long long e = n4 * 4 + t0; e < n; e += stride) {
+    nd[e] = coef * p[e];
+    if (first) x[e] = -g[e];
   }
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_dir(
-    const float* __restrict__ r, float* __restrict__ p, long long n,
-    const CgState* __restrict__ st) {
+    const float* __restrict__ r, float* __restrict__ p, long long n, int j,
+    const double* __restrict__ rpart, CgState* __restrict__ st) {
   if (st->done) return;
-  const float beta = (float)st->beta;
+  __shared__ double sh[4];
+  const double rr_new = total(rpart, gridDim.x, sh);
+  const double rr = st->rr[j & 1];
+  const double beta = rr_new / rr;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    st->rr[(j + 1) & 1] = rr_new;
+    st->iters = j + 1;
+    st->beta = beta;
+    if (!is_fin(rr_new)) {
+      st->status = -5;
+      st->done = 1;
+    } else if (st->tol2 > 0.0 && rr_new <= st->tol2 * st->rr0) {
+      st->done = 1;
+    }
+  }
+  const float b = (float)beta;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n4; i += stride)
-    ((f32x4*)p)[i] = beta * ((const f32x4*)p)[i] - ((const f32x4*)r)[i];
-  for (long long i = n4 * 4 + (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride)
-    p[i] = beta * p[i] - r[i];
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  long long i = t0;
+  for (; i + stride < n4; i += 2 * stride) {
+    const f32x4 p0 = ((const f32x4*)p)[i], p1 = ((const f32x4*)p)[i + stride];
+    const f32x4 r0 = ((const f32x4*)r)[i], r1 = ((const f32x4*)r)[i + stride];
+    ((f32x4*)p)[i] = b * p0 - r0;
+    ((f32x4*)p)[i + stride] = b * p1 - r1;
+  }
+  for (; i < n4; i += stride)
+    ((f32x4*)p)[i] = b * ((const f32x4*)p)[i] - ((const f32x4*)r)[i];
+  for (long long e = n4 * 4 + t0; e < n; e += stride) p[e] = b * p[e] - r[e];
 }
 
 // ------------------------------------------------------------- launchers
@@ -298,49 +290,47 @@ int cg_grid(long long n) {
   return (int)b;
 }
 
+int cg_part_doubles() { return 5 * MAX_GRID; }
+
 void cg_init(const Launch& L, const float* g, float* x, float* r, float* p,
              float* neg_dir, long long n, double lambda, double tol2,
              double* part, CgState* st) {
+  const int nb = cg_grid(n);
   hipLaunchKernelGGL(hf_cg_reset, dim3(1), dim3(64), 0, L.stream, st);
   prof_begin(L, "hf_cg_init");
-  hipLaunchKernelGGL(hf_cg_init, dim3(cg_grid(n)), dim3(NT), 0, L.stream, g, x,
-                     r, p, neg_dir, n, lambda, tol2, part, st);
+  hipLaunchKernelGGL(hf_cg_init, dim3(nb), dim3(NT), 0, L.stream, g, x, r, p,
+                     neg_dir, n, part + 4 * MAX_GRID);
   prof_end(L, "hf_cg_init", 0.0, 5.0 * 4.0 * n);
+  hipLaunchKernelGGL(hf_cg_init_fin, dim3(1), dim3(NT), 0, L.stream,
+                     part + 4 * MAX_GRID, nb, lambda, tol2, st);
 }
 
-void cg_curv_dot(const Launch& L, const float* p, const float* q, long long n,
-                 int j, double* part, CgState* st) {
-  prof_begin(L, "hf_cg_curv_dot");
-  hipLaunchKernelGGL(hf_cg_curv_dot, dim3(cg_grid(n)), dim3(NT), 0, L.stream,
-                     p, q, n, j, part, st);
-  prof_end(L, "hf_cg_curv_dot", 0.0, 2.0 * 4.0 * n);
-}
-
-void cg_neg(const Launch& L, const float* g, const float* p, float* x,
-            float* neg_dir, long long n, double* part, CgState* st) {
-  prof_begin(L, "hf_cg_neg_dot");
-  hipLaunchKernelGGL(hf_cg_neg_dot, dim3(cg_grid(n)), dim3(NT), 0, L.stream, g,
-                     p, n, part, st);
-  prof_end(L, "hf_cg_neg_dot", 0.0, 0.0);
-  prof_begin(L, "hf_cg_neg_write");
-  hipLaunchKernelGGL(hf_cg_neg_write, dim3(cg_grid(n)), dim3(NT), 0, L.stream,
-                     g, p, x, neg_dir, n, st);
-  prof_end(L, "hf_cg_neg_write", 0.0, 0.0);
-}
-
-void cg_update(const Launch& L, float* x, float* r, const float* p,
-               const float* q, long long n, double* part, CgState* st) {
+void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
+                  const float* g, float* neg_dir, long long n, int j,
+                  double* part, CgState* st) {
+  const int nb = cg_grid(n);
+  double* dpart = part;                  // 2 * MAX_GRID: p.q, p.p
+  double* rpart = part + 2 * MAX_GRID;   // r.r
+  double* gpart = part + 3 * MAX_GRID;   // g.p
+  prof_begin(L, "hf_cg_dot");
+  hipLaunchKernelGGL(hf_cg_dot, dim3(nb), dim3(NT), 0, L.stream, p, q, n,
+                     dpart, st);
+  prof_end(L, "hf_cg_dot", 0.0, 2.0 * 4.0 * n);
   prof_begin(L, "hf_cg_update");
-  hipLaunchKernelGGL(hf_cg_update, dim3(cg_grid(n)), dim3(NT), 0, L.stream, x,
-                     r, p, q, n, part, st);
+  hipLaunchKernelGGL(hf_cg_update, dim3(nb), dim3(NT), 0, L.stream, x, r, p, q,
+                     n, j, dpart, rpart, st);
   prof_end(L, "hf_cg_update", 0.0, 6.0 * 4.0 * n);
-}
-
-void cg_dir(const Launch& L, const float* r, float* p, long long n,
-            CgState* st) {
+  prof_begin(L, "hf_cg_neg_dot");
+  hipLaunchKernelGGL(hf_cg_neg_dot, dim3(nb), dim3(NT), 0, L.stream, g, p, n, j,
+                     gpart, st);
+  prof_end(L, "hf_cg_neg_dot", 0.0, 2.0 * 4.0 * n);
+  prof_begin(L, "hf_cg_neg_write");
+  hipLaunchKernelGGL(hf_cg_neg_write, dim3(nb), dim3(NT), 0, L.stream, g, p, x,
+                     neg_dir, n, j, gpart, st);
+  prof_end(L, "hf_cg_neg_write", 0.0, 2.0 * 4.0 * n);
   prof_begin(L, "hf_cg_dir");
-  hipLaunchKernelGGL(hf_cg_dir, dim3(cg_grid(n)), dim3(NT), 0, L.stream, r, p,
-                     n, st);
+  hipLaunchKernelGGL(hf_cg_dir, dim3(nb), dim3(NT), 0, L.stream, r, p, n, j,
+                     rpart, st);
   prof_end(L, "hf_cg_dir", 0.0, 3.0 * 4.0 * n);
 }
 

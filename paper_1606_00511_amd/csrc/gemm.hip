@@ -217,7 +217,9 @@ struct EStore {
 // MODE 0: single (nseg K-segments, optional split-K over grid z)
 // MODE 1: dual   acc0 = X0 Y0, acc1 = X1 Y0 + X0 Y1
 // MODE 2: dual0  acc0 = X0 Y0, acc1 = X0 Y1
-template <int MODE, bool XK, bool YK, int VEC, class Epi>
+// BIAS (weight gradient): blocks of the first column tile also sum their X
+// tiles of K-segment 0 over k, giving sum_k X(m, k) for their 128 rows.
+template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS = false>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) {
   if (s.skip && *s.skip) return;
   constexpr int T = MODE == 0 ? 2 : (MODE == 1 ? 4 : 3);
@@ -340,6 +342,8 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     }
   };
 
+  const bool do_bias = BIAS && blockIdx.x == 0 && (e.bias_out || e.bias_part);
+  double bsum = 0.0;
   if (vb0 < vb1) {
     gload(vb0);
     sstore(0);
@@ -349,9 +353,25 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
       const bool more = vb + 1 < vb1;
       if (more) gload(vb + 1);
       compute(buf);
+      if (BIAS && do_bias && vb < kbps) {
+        // X tile is [k][m] (XK = false): this thread sums 8 k for column m
+        const float* xs = lds[buf][0] + (tid >> 7) * 8 * LDM + (tid & 127);
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) bsum += (double)xs[kk * LDM];
+      }
       if (more) sstore(buf ^ 1);
       __syncthreads();
       buf ^= 1;
+    }
+  }
+  if (BIAS && do_bias) {
+    __shared__ double bhalf[128];
+    if (tid >= 128) bhalf[tid - 128] = bsum;
+    __syncthreads();
+    if (tid < 128 && m0 + tid < s.M) {
+      const double t = bsum + bhalf[tid];
+      if (s.splits > 1) e.bias_part[(size_t)blockIdx.z * s.M + m0 + tid] = t;
+      else e.bias_out[m0 + tid] = (float)t;
     }
   }
 
@@ -372,25 +392,25 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
 
 }  // namespace
 
-#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI)                                 \
+#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS)                           \
   extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v4(GemmShape s,   \
                                                                  EpiArgs e) {   \
-    gemm_body<MODE, XK, YK, 4, EPI>(s, e);                                      \
+    gemm_body<MODE, XK, YK, 4, EPI, BIAS>(s, e);                                \
   }                                                                             \
   extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v1(GemmShape s,   \
                                                                  EpiArgs e) {   \
-    gemm_body<MODE, XK, YK, 1, EPI>(s, e);                                      \
+    gemm_body<MODE, XK, YK, 1, EPI, BIAS>(s, e);                                \
   }
 
-HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, true, EFwd)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd)
-HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, true, ERFwd)
-HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd)
-HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd)
-HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd)
-HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd)
-HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore)
+HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, true, EFwd, false)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false)
+HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, true, ERFwd, false)
+HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false)
+HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false)
+HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false)
+HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false)
+HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true)
 
 namespace {
 

@@ -84,13 +84,12 @@ struct Profiler {
   }
   // Drop the launches of a CG solve that the device `done` flag turned into
   // no-ops, so that only launches that did their work are counted.
-  // last = the last iteration that evaluated a product; stop_in_dot: the solve
-  // stopped in the curvature-dot kernel of that iteration (negative
-  // curvature or a non-finite kappa), so its update and direction kernels
-  // were no-ops; stop_in_update: the tolerance stopped it in the update
-  // kernel, so its direction kernel was a no-op; neg_iter: iteration whose
-  // negative-curvature kernels ran (-1: none).
-  void retract(int last, bool stop_in_dot, bool stop_in_update, int neg_iter) {
+  // last = the last iteration that evaluated a product; stop_on_kappa: the
+  // update kernel of that iteration stopped on kappa (negative curvature or a
+  // non-finite value) before touching the vectors, so it and the direction
+  // kernel did no vector work; neg_iter: iteration whose negative-curvature
+  // kernels ran (-1: none).
+  void retract(int last, bool stop_on_kappa, int neg_iter) {
     std::vector<Pending> keep;
     keep.reserve(pending.size());
     for (auto& p : pending) {
@@ -100,10 +99,8 @@ struct Profiler {
         const bool is_neg = nm == "hf_cg_neg_dot" || nm == "hf_cg_neg_write";
         if (p.tag > last) drop = true;
         else if (is_neg) drop = p.tag != neg_iter;
-        else if (p.tag == last && stop_in_dot)
+        else if (p.tag == last && stop_on_kappa)
           drop = nm == "hf_cg_update" || nm == "hf_cg_dir";
-        else if (p.tag == last && stop_in_update)
-          drop = nm == "hf_cg_dir";
       }
       if (drop) {
         recs[p.rec].launches -= 1;
@@ -161,9 +158,9 @@ struct hf_ctx {
 
   // workspace carve-up (byte offsets), 1-based per layer where it applies
   std::vector<size_t> oA, oD, oE2, oRZ, oRA, oRD;
-  size_t oZ = 0, oP = 0, oSplit = 0, oCol = 0, oR = 0, oPv = 0, oQ = 0,
+  size_t oZ = 0, oP = 0, oSplit = 0, oBpart = 0, oR = 0, oPv = 0, oQ = 0,
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
-  int max_splits = 8;
+  int max_splits = 16;
   size_t split_elems = 0;
 
   char* ws = nullptr;
@@ -241,12 +238,12 @@ void plan(hf_ctx* c) {
   }
   c->split_elems = mn;
   c->oSplit = take((size_t)c->max_splits * mn * sizeof(float));
-  c->oCol = take((size_t)colsum_chunks((int)B) * dmax * sizeof(double));
+  c->oBpart = take((size_t)c->max_splits * dmax * sizeof(double));
   const size_t nv = ((size_t)c->n + 63) & ~size_t(63);
   c->oR = take(nv * sizeof(float));
   c->oPv = take(nv * sizeof(float));
   c->oQ = take(nv * sizeof(float));
-  c->oRed = take(4 * 1024 * sizeof(double));
+  c->oRed = take((size_t)cg_part_doubles() * sizeof(double));
   c->oLoss = take(((B + 3) / 4) * sizeof(double));
   c->oState = take(sizeof(CgState));
   c->oErr = take(sizeof(int));
@@ -275,11 +272,15 @@ int check_batch(hf_ctx* c, int64_t B) {
 }
 
 // split-K factor for a weight-gradient GEMM with the given tile count and
-// reduction length: enough workgroups to cover the 256 compute units twice,
-// while every split keeps at least 256 rows of the reduction.
+// reduction length.  First, no split accumulates more than 2,048 rows in
+// fp32 (the weight gradients are batch means with heavy cancellation, and the
+// splits are combined in fixed order in the reduce kernel); then, enough
+// workgroups to cover the 256 compute units twice while every split keeps
+// at least 256 rows.
 int choose_splits(const hf_ctx* c, int M, int N, int Ktot) {
   const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
   int s = 1;
+  while (s < c->max_splits && (Ktot + s - 1) / s > 2048) s *= 2;
   while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 256) s *= 2;
   return s;
 }
@@ -307,28 +308,30 @@ EpiArgs epi(const hf_ctx* c, int hidden) {
 }
 
 // Weight-gradient GEMM into the parameter layout: out_W (d_l x d_{l-1}) =
-// sum_seg Xs^T Ys over the rows, then the bias part from colsum(bias_src).
+// sum_seg Xs^T Ys over the rows, and out_b = column sums of x0 (the first
+// segment's X operand), both from the same kernel.
 void wgrad(hf_ctx* c, int l, int B, const float* x0, const float* y0,
-           const float* x1, const float* y1, int ldy, const float* bias_src,
-           float* out, const int* skip) {
+           const float* x1, const float* y1, int ldy, float* out,
+           const int* skip) {
   const Launch Lc = c->launch();
   const int M = c->d[l], N = c->d[l - 1];
   const int nseg = x1 ? 2 : 1;
   GemmShape s = shape(M, N, B, x0, x1, y0, y1, c->ld[l], ldy, nseg, skip);
   s.splits = choose_splits(c, M, N, B * nseg);
   EpiArgs e = epi(c, 0);
+  e.ldo = N;
   if (s.splits > 1) {
     e.out0 = c->F(c->oSplit);
-    e.ldo = N;
     e.split_stride = (long long)M * N;
+    e.bias_part = c->Dp(c->oBpart);
     gemm_wgrad(Lc, s, e);
-    splitk_reduce(Lc, c->F(c->oSplit), s.splits, M, N, out + c->offW[l], N, skip);
+    splitk_reduce(Lc, c->F(c->oSplit), c->Dp(c->oBpart), s.splits, M, N,
+                  out + c->offW[l], N, out + c->offB[l], skip);
   } else {
     e.out0 = out + c->offW[l];
-    e.ldo = N;
+    e.bias_out = out + c->offB[l];
     gemm_wgrad(Lc, s, e);
   }
-  colsum(Lc, bias_src, B, M, c->ld[l], c->Dp(c->oCol), out + c->offB[l], skip);
 }
 
 // Forward pass (activations only) on B rows of X; logits into Z, then the
@@ -397,10 +400,9 @@ void product_cached(hf_ctx* c, const float* W, const float* X, int B,
     const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
     if (mode == HF_HESSIAN && l > 1) {
       wgrad(c, l, B, c->F(c->oRD[l]), Ain, c->F(c->oD[l]), c->F(c->oRA[l - 1]),
-            ldin, c->F(c->oRD[l]), out, skip);
+            ldin, out, skip);
     } else {
-      wgrad(c, l, B, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin,
-            c->F(c->oRD[l]), out, skip);
+      wgrad(c, l, B, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin, out, skip);
     }
     if (l == 1) break;
     EpiArgs e = epi(c, 1);
@@ -516,8 +518,7 @@ int hf_loss_grad(hf_ctx* c, const float* W, const float* X, const int32_t* y,
   for (int l = c->L; l >= 1; --l) {
     const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
     const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
-    wgrad(c, l, b, c->F(c->oD[l]), Ain, nullptr, nullptr, ldin, c->F(c->oD[l]),
-          grad, nullptr);
+    wgrad(c, l, b, c->F(c->oD[l]), Ain, nullptr, nullptr, ldin, grad, nullptr);
     if (l > 1) backward_data(c, W, l, b, false);
   }
   HIP_TRY(c, hipGetLastError());
@@ -568,10 +569,9 @@ int hf_hvp(hf_ctx* c, const float* W, const float* X, const int32_t* y,
     const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
     if (hess && l > 1) {
       wgrad(c, l, b, c->F(c->oRD[l]), Ain, c->F(c->oD[l]), c->F(c->oRA[l - 1]),
-            ldin, c->F(c->oRD[l]), out, nullptr);
+            ldin, out, nullptr);
     } else {
-      wgrad(c, l, b, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin,
-            c->F(c->oRD[l]), out, nullptr);
+      wgrad(c, l, b, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin, out, nullptr);
     }
     if (l == 1) break;
     EpiArgs e = epi(c, 1);
@@ -644,10 +644,7 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   for (int j = 0; j < max_iters; ++j) {
     if (c->prof) c->prof->tag = j;
     product_cached(c, W, Xc, b, p, mode, q, skip);
-    cg_curv_dot(Lc, p, q, n, j, part, st);
-    cg_neg(Lc, g, p, step, neg_dir, n, part, st);
-    cg_update(Lc, step, r, p, q, n, part, st);
-    cg_dir(Lc, r, p, n, st);
+    cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st);
     // Stop enqueueing once the device reports `done` for the previous
     // iteration; the work already queued for this one returns at once.
     HIP_TRY(c, hipMemcpyAsync(&c->pinned[j & 1], st, sizeof(CgState),
@@ -667,11 +664,9 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
                             hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   const CgState& s = c->pinned[0];
-  if (c->prof) {
-    const bool stop_dot = s.neg || (s.status && s.iters < s.products);
-    const bool stop_upd = !stop_dot && s.done && s.iters == s.products;
-    c->prof->retract(s.products - 1, stop_dot, stop_upd, s.neg ? s.neg_iter : -1);
-  }
+  if (c->prof)
+    c->prof->retract(s.products - 1, s.neg || (s.status && s.iters < s.products),
+                     s.neg ? s.neg_iter : -1);
   info->iters = s.iters;
   info->products = s.products;
   info->neg_curv = s.neg;
@@ -680,7 +675,7 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   info->pHp = s.neg ? s.pq : 0.0;
   info->gTd = s.neg ? (s.gp >= 0.0 ? -s.gp : s.gp) : 0.0;
   info->rr0 = s.rr0;
-  info->rr_final = s.rr;
+  info->rr_final = s.rr[s.iters & 1];
   info->status = s.status;
   if (errflag) {
     info->status = HF_ELABEL;

@@ -57,6 +57,11 @@ struct EpiArgs {
   const float* aux2;     // E_{l-1} * phi''(A_{l-1})
   int lda;               // leading dimension of aux0..aux2
   long long split_stride;  // split-K partial stride (elements)
+  // weight gradient only: column sums of the first K-segment's X operand
+  // (the bias part of the gradient or product): written to bias_out when
+  // there is one split, else per split to bias_part[z * M + m]
+  float* bias_out;
+  double* bias_part;
 };
 
 // Forward:  out0 = phi(acc + bias) (hidden) or acc + bias (logits)
@@ -78,7 +83,8 @@ void gemm_bwd_rbwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
 void gemm_rbwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
 // Gauss-Newton backward: out1 = acc * phi'(aux0)
 void gemm_gnbwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
-// Weight gradient (XK = YK = false): out0[z * split_stride + m * ldo + n] = acc
+// Weight gradient (XK = YK = false): out0[z * split_stride + m * ldo + n] = acc,
+// plus the bias sums sum_k X[0](m, k) (see EpiArgs::bias_out / bias_part)
 void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e);
 
 // --------------------------------------------------------------- row ops
@@ -94,41 +100,32 @@ void loss_finalize(const Launch& L, const double* loss_part, int nparts,
 // Rdelta_L = P * (RZ - rowsum(P * RZ)) / B.
 void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
                  int C, int ld, float* RD, const int* skip);
-// out[c] = sum_r D[r * ld + c] for c < cols (deterministic two-pass);
-// part must hold colsum_chunks(rows) * cols doubles.
-int colsum_chunks(int rows);
-void colsum(const Launch& L, const float* D, int rows, int cols, int ld,
-            double* part, float* out, const int* skip);
-// out[m * ldo + n] = sum_z part[z * M * N + m * N + n]
-void splitk_reduce(const Launch& L, const float* part, int splits, int M,
-                   int N, float* out, int ldo, const int* skip);
+// out[m * ldo + n] = sum_z part[z * M * N + m * N + n] and
+// bout[m] = sum_z bpart[z * M + m], both in split order
+void splitk_reduce(const Launch& L, const float* part, const double* bpart,
+                   int splits, int M, int N, float* out, int ldo, float* bout,
+                   const int* skip);
 
 // ------------------------------------------------------------------- CG
 struct CgState {
-  double rr, rr0, kappa, alpha, beta, pp, pq, gp;
+  double rr[2];        // r.r, slot = iteration parity
+  double rr0, kappa, alpha, beta, pp, pq, gp;
   double lambda, tol2;
-  int done, neg, neg_pending, neg_iter;
-  int iters, products, status, j;
-  unsigned int counter[4];
-  int pad[4];
+  int done, neg, neg_iter, iters, products, status;
 };
 
 int cg_grid(long long n);
-// x = 0, r = g, p = -g, neg_dir = 0, rr = rr0 = |g|^2 (state initialised)
+int cg_part_doubles();
+// x = 0, r = g, p = -g, neg_dir = 0; state initialised (rr = rr0 = |g|^2)
 void cg_init(const Launch& L, const float* g, float* x, float* r, float* p,
              float* neg_dir, long long n, double lambda, double tol2,
              double* part, CgState* st);
-// kappa = p.q + lambda p.p; detection; alpha
-void cg_curv_dot(const Launch& L, const float* p, const float* q, long long n,
-                 int j, double* part, CgState* st);
-// on a pending detection: gp = g.p; neg_dir = -sgn(gp) p; step = -g at j = 0
-void cg_neg(const Launch& L, const float* g, const float* p, float* x,
-            float* neg_dir, long long n, double* part, CgState* st);
-// x += alpha p; r += alpha (q + lambda p); rr' = r.r; beta; tolerance
-void cg_update(const Launch& L, float* x, float* r, const float* p,
-               const float* q, long long n, double* part, CgState* st);
-// p = -r + beta p
-void cg_dir(const Launch& L, const float* r, float* p, long long n,
-            CgState* st);
+// One CG iteration j after the product q = A p has been formed:
+// kappa = p.q + lambda p.p and the stop test; x += alpha p,
+// r += alpha (q + lambda p); at a detection d~ = -sgn(g.p) p and, at j = 0,
+// x = -g; beta = rr'/rr and p = -r + beta p.
+void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
+                  const float* g, float* neg_dir, long long n, int j,
+                  double* part, CgState* st);
 
 }  // namespace hfk

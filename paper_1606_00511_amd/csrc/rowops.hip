@@ -7,9 +7,8 @@
 // softmax_rop:  the output-layer factor of both curvature products, the
 //   Hessian of the batch-mean cross-entropy with respect to the logits applied
 //   to R{z}: (diag p - p p^T) R{z} / B per row (Sec. 2.1, after Alg. 1).
-// colsum / splitk_reduce: deterministic fixed-order reductions for the bias
-//   parts of the gradient and of the curvature products, and for split-K
-//   weight-gradient partials.
+// splitk_reduce: deterministic fixed-order reduction of split-K partials of
+//   the weight gradients and of their bias sums.
 //
 // One wave64 per row; the row is staged in LDS once and reused from there for
 // every pass, row reductions use wave shuffles.  Every sum runs in a fixed
@@ -22,7 +21,6 @@ namespace hfk {
 namespace {
 
 constexpr int ROWS_PER_BLOCK = 4;   // 4 waves, one row each
-constexpr int COLSUM_ROWS = 128;    // rows per partial in colsum
 
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
@@ -154,41 +152,25 @@ extern "C" __global__ __launch_bounds__(256) void hf_softmax_rop(
   for (int c = lane; c < C; c += 64) out[c] = ps[c] * (rs[c] - dot) * invB;
 }
 
-extern "C" __global__ __launch_bounds__(256) void hf_colsum_part(
-    const float* __restrict__ D, int rows, int cols, int ld,
-    double* __restrict__ part, const int* __restrict__ skip) {
-  if (skip && *skip) return;
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= cols) return;
-  const int r0 = blockIdx.y * COLSUM_ROWS;
-  const int r1 = min(rows, r0 + COLSUM_ROWS);
-  double s = 0.0;
-  for (int r = r0; r < r1; ++r) s += D[(size_t)r * ld + c];
-  part[(size_t)blockIdx.y * cols + c] = s;
-}
-
-extern "C" __global__ __launch_bounds__(256) void hf_colsum_final(
-    const double* __restrict__ part, int chunks, int cols,
-    float* __restrict__ out, const int* __restrict__ skip) {
-  if (skip && *skip) return;
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= cols) return;
-  double s = 0.0;
-  for (int z = 0; z < chunks; ++z) s += part[(size_t)z * cols + c];
-  out[c] = (float)s;
-}
-
 extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce(
-    const float* __restrict__ part, int splits, int M, int N,
-    float* __restrict__ out, int ldo, const int* __restrict__ skip) {
+    const float* __restrict__ part, const double* __restrict__ bpart,
+    int splits, int M, int N, float* __restrict__ out, int ldo,
+    float* __restrict__ bout, const int* __restrict__ skip) {
   if (skip && *skip) return;
   const size_t mn = (size_t)M * N;
+  if (bpart) {
+    for (int m = blockIdx.x * 256 + threadIdx.x; m < M; m += gridDim.x * 256) {
+      double t = 0.0;
+      for (int z = 0; z < splits; ++z) t += bpart[(size_t)z * M + m];
+      bout[m] = (float)t;
+    }
+  }
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < mn;
        i += (size_t)gridDim.x * 256) {
-    float s = 0.0f;
+    double s = 0.0;
     for (int z = 0; z < splits; ++z) s += part[(size_t)z * mn + i];
     const size_t m = i / N, n = i - m * N;
-    out[m * ldo + n] = s;
+    out[m * ldo + n] = (float)s;
   }
 }
 
@@ -225,30 +207,15 @@ void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
   prof_end(L, "hf_softmax_rop", 0.0, 12.0 * B * C);
 }
 
-int colsum_chunks(int rows) { return (rows + COLSUM_ROWS - 1) / COLSUM_ROWS; }
-
-void colsum(const Launch& L, const float* D, int rows, int cols, int ld,
-            double* part, float* out, const int* skip) {
-  const int chunks = colsum_chunks(rows);
-  const int cb = (cols + 255) / 256;
-  prof_begin(L, "hf_colsum_part");
-  hipLaunchKernelGGL(hf_colsum_part, dim3(cb, chunks), dim3(256), 0, L.stream,
-                     D, rows, cols, ld, part, skip);
-  prof_end(L, "hf_colsum_part", 0.0, 4.0 * rows * cols + 8.0 * chunks * cols);
-  prof_begin(L, "hf_colsum_final");
-  hipLaunchKernelGGL(hf_colsum_final, dim3(cb), dim3(256), 0, L.stream, part,
-                     chunks, cols, out, skip);
-  prof_end(L, "hf_colsum_final", 0.0, 8.0 * chunks * cols + 4.0 * cols);
-}
-
-void splitk_reduce(const Launch& L, const float* part, int splits, int M,
-                   int N, float* out, int ldo, const int* skip) {
+void splitk_reduce(const Launch& L, const float* part, const double* bpart,
+                   int splits, int M, int N, float* out, int ldo, float* bout,
+                   const int* skip) {
   const long long mn = (long long)M * N;
   long long blocks = (mn + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   prof_begin(L, "hf_splitk_reduce");
   hipLaunchKernelGGL(hf_splitk_reduce, dim3((unsigned)blocks), dim3(256), 0,
-                     L.stream, part, splits, M, N, out, ldo, skip);
+                     L.stream, part, bpart, splits, M, N, out, ldo, bout, skip);
   prof_end(L, "hf_splitk_reduce", 0.0, 4.0 * mn * (splits + 1));
 }
 
