@@ -24,11 +24,11 @@ FLAGS = [
 ]
 
 
-def build_library(verbose=False):
+def build_library(verbose=False, out=LIB, extra=()):
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC] + FLAGS + ["-I", os.path.join(ROOT, "include"), "-I", CSRC,
-                             "-o", tmp] + srcs
+    tmp = out + ".tmp"
+    cmd = [HIPCC] + FLAGS + list(extra) + [
+        "-I", os.path.join(ROOT, "include"), "-I", CSRC, "-o", tmp] + srcs
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -38,8 +38,8 @@ def build_library(verbose=False):
         raise RuntimeError("hipcc failed (%d):\n%s" % (res.returncode, errs))
     if verbose and errs:
         print(errs, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -3,32 +3,36 @@
 // curvature products of Sec. 2.1; Alg. 2 evaluates them on each node's
 // minibatch).
 //
-// One workgroup of 256 threads (4 wave64) owns a 128 x 128 output tile;
-// each wave owns a 64 x 64 quadrant computed as 2 x 2 blocks of
-// v_mfma_f32_32x32x2_f32.  K advances in blocks of 16 through two LDS
-// buffers: while the MFMAs consume one buffer, the next K block is fetched
-// from global memory into registers and then written to the other buffer.
+// One workgroup of 256 threads (4 wave64 in a 2 x 2 grid) owns a 128 x 128
+// output tile; each wave owns a 64 x 64 quadrant computed as 2 x 2 blocks of
+// v_mfma_f32_32x32x2_f32 (fp32 operands, fp32 accumulation).  K advances in
+// blocks of 16 through two LDS buffers: while the MFMAs consume one buffer,
+// the next K block is fetched from global memory into registers and then
+// written to the other buffer.  Tiles that lie fully inside the operands
+// take unguarded loads; edge tiles take element-wise guarded loads.
+// (Measured on MI355X: 256 x 256 tiles with 4 x 4 blocks per wave ran
+// 5-15% slower than this shape at one wave per SIMD.)
 //
-// Operand tiles are copied to LDS without transposition: a K-contiguous
-// operand is kept as [row][k] (row stride 20 floats) and read back with two
-// 128-bit LDS loads per lane; a row-contiguous operand is kept as [k][row]
-// (row stride 132 floats) and read with 32-bit LDS loads.  Within a K block
-// each half-wave works on its own 8 consecutive k values, which permutes the
-// order of the K sum identically for both operands.
+// LDS layouts (the gfx950 LDS has 64 four-byte banks):
+//  - a row-contiguous operand is kept as [k][row] (row stride 132 floats) and
+//    read with 32-bit LDS loads;
+//  - a K-contiguous operand is kept either as [row][k] with its four 16-byte
+//    k chunks XOR-swizzled by (row >> 2) & 3 (no bank conflicts on the
+//    128-bit stores and loads), or transposed on the way in to [k][row]; the
+//    transposed form measured faster when both operands are K-contiguous
+//    (forward and R-forward), the swizzled form otherwise.
+// Within a K block each half-wave works on its own 8 consecutive k values,
+// which permutes the order of the K sum identically for both operands.
 #include "hf_internal.h"
 
 namespace hfk {
 namespace {
 
-constexpr int BM = 128;
-constexpr int BN = 128;
 constexpr int BK = 16;
+constexpr int HK = BK / 2;      // k values per half-wave per K block
 constexpr int NT = 256;
-constexpr int LDK = BK + 4;     // [row][k] tile row stride
-constexpr int LDM = BM + 4;     // [k][row] tile row stride
-constexpr int TILE = (BM * LDK > BK * LDM) ? BM * LDK : BK * LDM;
-
-static_assert(BM == BN, "one loader serves both operands");
+constexpr int LDK = BK;         // [row][k] tile row stride (swizzled chunks)
+__device__ __forceinline__ int swz(int row) { return (row >> 2) & 3; }
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -38,34 +42,44 @@ __device__ __forceinline__ float act_f(int act, float z) {
   if (act == ACT_TANH) return tanhf(z);
   return fmaxf(z, 0.0f);
 }
-// phi'(z) written in terms of a = phi(z)
+// phi'(z) written in terms of a = phi(z); selects rather than branches keep
+// the epilogue loops straight-line so the accumulators stay in registers
 __device__ __forceinline__ float act_d1(int act, float a) {
-  if (act == ACT_SIGMOID) return a * (1.0f - a);
-  if (act == ACT_TANH) return 1.0f - a * a;
-  return a > 0.0f ? 1.0f : 0.0f;
+  const float sg = a * (1.0f - a);
+  const float th = 1.0f - a * a;
+  const float rl = a > 0.0f ? 1.0f : 0.0f;
+  return act == ACT_SIGMOID ? sg : (act == ACT_TANH ? th : rl);
 }
 // phi''(z) written in terms of a = phi(z)
 __device__ __forceinline__ float act_d2(int act, float a) {
-  if (act == ACT_SIGMOID) return a * (1.0f - a) * (1.0f - 2.0f * a);
-  if (act == ACT_TANH) return -2.0f * a * (1.0f - a * a);
-  return 0.0f;
+  const float sg = a * (1.0f - a) * (1.0f - 2.0f * a);
+  const float th = -2.0f * a * (1.0f - a * a);
+  return act == ACT_SIGMOID ? sg : (act == ACT_TANH ? th : 0.0f);
 }
 
 // ------------------------------------------------------------ tile loading
-// MK: the operand is stored rows x K with K contiguous; otherwise K x rows
-// with rows contiguous.  Each thread moves 8 floats of a 128 x 16 tile.
-template <bool MK, int VEC>
+// A ROWS x BK operand tile.  MK: the operand is stored rows x K with K
+// contiguous, kept in LDS as swizzled [row][k] (stride LDK), or as [k][row]
+// when TR; otherwise K x rows with rows contiguous, kept as [k][row] (stride
+// LDM).  Each of the NT threads moves V1 floats per tile.
+template <bool MK, int VEC, int ROWS, bool TR = false>
 struct Tile {
+  static constexpr int LDM = ROWS + 4;
+  static constexpr int SIZE = (ROWS * LDK > BK * LDM) ? ROWS * LDK : BK * LDM;
+  static constexpr int V4 = ROWS * BK / 4 / NT;
+  static constexpr int V1 = ROWS * BK / NT;
+
+  // Guarded load of the tile at (r0, k0); elements outside are zero.
   __device__ static __forceinline__ void load(const float* __restrict__ base,
                                               int ld, int rows, int K, int r0,
-                                              int k0, int tid, float (&g)[8]) {
+                                              int k0, int tid, float (&g)[V1]) {
     if (VEC == 4) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < V4; ++i) {
         const int idx = tid + NT * i;
         int r, k;
-        if (MK) { r = r0 + (idx >> 2); k = k0 + (idx & 3) * 4; }
-        else    { k = k0 + (idx >> 5); r = r0 + (idx & 31) * 4; }
+        if (MK) { r = r0 + idx / (BK / 4); k = k0 + (idx % (BK / 4)) * 4; }
+        else    { k = k0 + idx / (ROWS / 4); r = r0 + (idx % (ROWS / 4)) * 4; }
         const bool full = MK ? (r < rows && k + 3 < K) : (k < K && r + 3 < rows);
         if (full) {
           const f32x4 v = MK ? *(const f32x4*)(base + (size_t)r * ld + k)
@@ -85,11 +99,11 @@ struct Tile {
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < V1; ++i) {
         const int idx = tid + NT * i;
         int r, k;
-        if (MK) { r = r0 + (idx >> 4); k = k0 + (idx & 15); }
-        else    { k = k0 + (idx >> 7); r = r0 + (idx & 127); }
+        if (MK) { r = r0 + idx / BK; k = k0 + idx % BK; }
+        else    { k = k0 + idx / ROWS; r = r0 + idx % ROWS; }
         g[i] = (r < rows && k < K)
             ? (MK ? base[(size_t)r * ld + k] : base[(size_t)k * ld + r])
             : 0.0f;
@@ -97,38 +111,100 @@ struct Tile {
     }
   }
 
+  // Offset of the thread's first element from the tile origin.
+  __device__ static __forceinline__ size_t offset(int ld, int tid) {
+    if (VEC == 4)
+      return MK ? (size_t)(tid / (BK / 4)) * ld + (tid % (BK / 4)) * 4
+                : (size_t)(tid / (ROWS / 4)) * ld + (tid % (ROWS / 4)) * 4;
+    return MK ? (size_t)(tid / BK) * ld + tid % BK
+              : (size_t)(tid / ROWS) * ld + tid % ROWS;
+  }
+
+  // Unguarded load of a tile that lies fully inside the operand; p points at
+  // the thread's first element (operand + tile origin + offset()).
+  __device__ static __forceinline__ void load_fast(const float* __restrict__ p,
+                                                   int ld, float (&g)[V1]) {
+    if (VEC == 4) {
+      const size_t step = MK ? (size_t)(NT / (BK / 4)) * ld
+                             : (size_t)(NT / (ROWS / 4)) * ld;
+#pragma unroll
+      for (int i = 0; i < V4; ++i) {
+        const f32x4 v = *(const f32x4*)(p + i * step);
+        g[4 * i + 0] = v[0]; g[4 * i + 1] = v[1];
+        g[4 * i + 2] = v[2]; g[4 * i + 3] = v[3];
+      }
+    } else {
+      const size_t step = MK ? (size_t)(NT / BK) * ld : (size_t)(NT / ROWS) * ld;
+#pragma unroll
+      for (int i = 0; i < V1; ++i) g[i] = p[i * step];
+    }
+  }
+
   __device__ static __forceinline__ void store(float* __restrict__ s, int tid,
-                                               const float (&g)[8]) {
+                                               const float (&g)[V1]) {
+    if (MK && TR) {
+      // transpose into [k][row]
+      if (VEC == 4) {
+#pragma unroll
+        for (int i = 0; i < V4; ++i) {
+          const int idx = tid + NT * i;
+          const int row = idx / (BK / 4), k = (idx % (BK / 4)) * 4;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) s[(k + j) * LDM + row] = g[4 * i + j];
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < V1; ++i) {
+          const int idx = tid + NT * i;
+          s[(idx % BK) * LDM + idx / BK] = g[i];
+        }
+      }
+      return;
+    }
     if (VEC == 4) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < V4; ++i) {
         const int idx = tid + NT * i;
-        float* d = MK ? s + (idx >> 2) * LDK + (idx & 3) * 4
-                      : s + (idx >> 5) * LDM + (idx & 31) * 4;
+        float* d;
+        if (MK) {
+          const int row = idx / (BK / 4), c = idx % (BK / 4);
+          d = s + row * LDK + ((c ^ swz(row)) * 4);
+        } else {
+          d = s + (idx / (ROWS / 4)) * LDM + (idx % (ROWS / 4)) * 4;
+        }
         f32x4 v = {g[4 * i], g[4 * i + 1], g[4 * i + 2], g[4 * i + 3]};
         *(f32x4*)d = v;
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < V1; ++i) {
         const int idx = tid + NT * i;
-        if (MK) s[(idx >> 4) * LDK + (idx & 15)] = g[i];
-        else    s[(idx >> 7) * LDM + (idx & 127)] = g[i];
+        if (MK) {
+          const int row = idx / BK, k = idx % BK;
+          s[row * LDK + (((k >> 2) ^ swz(row)) * 4) + (k & 3)] = g[i];
+        } else {
+          s[(idx / ROWS) * LDM + idx % ROWS] = g[i];
+        }
       }
     }
   }
 
-  // The 8 values lane (row, half h) feeds to MFMA steps 0..7 of a K block.
+  // The HK values lane (row, half h) feeds to MFMA steps 0..HK-1 of a K
+  // block: k = h * HK + step.  Both operands use the same k order, so the
+  // sum over k is unchanged.
   __device__ static __forceinline__ void frag(const float* __restrict__ s,
-                                              int row, int h, float (&f)[8]) {
-    if (MK) {
-      const f32x4 a = *(const f32x4*)(s + row * LDK + h * 8);
-      const f32x4 b = *(const f32x4*)(s + row * LDK + h * 8 + 4);
-      f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
-      f[4] = b[0]; f[5] = b[1]; f[6] = b[2]; f[7] = b[3];
+                                              int row, int h, float (&f)[HK]) {
+    if (MK && !TR) {
+#pragma unroll
+      for (int q = 0; q < HK / 4; ++q) {
+        const int c = (h * HK) / 4 + q;
+        const f32x4 a = *(const f32x4*)(s + row * LDK + ((c ^ swz(row)) * 4));
+        f[4 * q + 0] = a[0]; f[4 * q + 1] = a[1];
+        f[4 * q + 2] = a[2]; f[4 * q + 3] = a[3];
+      }
     } else {
 #pragma unroll
-      for (int s8 = 0; s8 < 8; ++s8) f[s8] = s[(h * 8 + s8) * LDM + row];
+      for (int q = 0; q < HK; ++q) f[q] = s[(h * HK + q) * LDM + row];
     }
   }
 };
@@ -174,10 +250,18 @@ struct ERFwd {
 struct EBwd {
   static __device__ __forceinline__ void apply(const EpiArgs& e, int r, int c,
                                                float v0, float) {
+    e.out0[(size_t)r * e.ldo + c] =
+        v0 * act_d1(e.act, e.aux0[(size_t)r * e.lda + c]);
+  }
+};
+// backward data that also caches E * phi''(A) for the Hessian product
+struct EBwdE2 {
+  static __device__ __forceinline__ void apply(const EpiArgs& e, int r, int c,
+                                               float v0, float) {
     const size_t o = (size_t)r * e.ldo + c;
     const float a = e.aux0[(size_t)r * e.lda + c];
     e.out0[o] = v0 * act_d1(e.act, a);
-    if (e.out2) e.out2[o] = v0 * act_d2(e.act, a);
+    e.out2[o] = v0 * act_d2(e.act, a);
   }
 };
 struct EBwdRBwd {
@@ -217,24 +301,28 @@ struct EStore {
 // MODE 0: single (nseg K-segments, optional split-K over grid z)
 // MODE 1: dual   acc0 = X0 Y0, acc1 = X1 Y0 + X0 Y1
 // MODE 2: dual0  acc0 = X0 Y0, acc1 = X0 Y1
+// TR: K-contiguous operands are transposed to [k][row] in LDS.
 // BIAS (weight gradient): blocks of the first column tile also sum their X
-// tiles of K-segment 0 over k, giving sum_k X(m, k) for their 128 rows.
-template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS = false>
+// tiles of K-segment 0 over k, giving sum_k X(m, k) for their rows.
+template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS, bool TR>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) {
   if (s.skip && *s.skip) return;
+  constexpr int W = 2;          // 2 x 2 MFMA blocks per wave
+  constexpr int ROWS = 64 * W;
+  using TX = Tile<XK, VEC, ROWS, TR>;
+  using TY = Tile<YK, VEC, ROWS, TR>;
   constexpr int T = MODE == 0 ? 2 : (MODE == 1 ? 4 : 3);
-  __shared__ __attribute__((aligned(16))) float lds[2][T][TILE];
-
-  using TX = Tile<XK, VEC>;
-  using TY = Tile<YK, VEC>;
+  constexpr int SZ = TX::SIZE > TY::SIZE ? TX::SIZE : TY::SIZE;
+  constexpr int V1 = TX::V1;
+  __shared__ __attribute__((aligned(16))) float lds[2][T][SZ];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int li = lane & 31, h = lane >> 5;
-  const int m0 = blockIdx.y * BM;
-  const int n0 = blockIdx.x * BN;
+  const int m0 = blockIdx.y * ROWS;
+  const int n0 = blockIdx.x * ROWS;
 
   const int kbps = (s.K + BK - 1) / BK;
   const int nvb = (MODE == 0 ? s.nseg : 1) * kbps;
@@ -245,18 +333,44 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     vb1 = min(nvb, vb0 + per);
   }
 
-  f32x16 acc0[2][2], acc1[2][2];
+  f32x16 acc0[W][W], acc1[W][W];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < W; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < W; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) { acc0[a][b][r] = 0.0f; acc1[a][b][r] = 0.0f; }
+      for (int r = 0; r < 16; ++r) {
+        acc0[a][b][r] = 0.0f;
+        if (MODE != 0) acc1[a][b][r] = 0.0f;
+      }
 
-  float g[T][8];
+  float g[T][V1];
+  // Rows of this tile lie inside both operands: every K block except a
+  // ragged last one can use unguarded loads.
+  const bool interior = m0 + ROWS <= s.M && n0 + ROWS <= s.N;
+  const size_t ox = TX::offset(s.ldx, tid) + (XK ? (size_t)m0 * s.ldx : (size_t)m0);
+  const size_t oy = TY::offset(s.ldy, tid) + (YK ? (size_t)n0 * s.ldy : (size_t)n0);
   auto gload = [&](int vb) {
     const int seg = (MODE == 0) ? vb / kbps : 0;
     const int k0 = (vb - seg * kbps) * BK;
+    if (interior && k0 + BK <= s.K) {
+      const size_t kx = XK ? (size_t)k0 : (size_t)k0 * s.ldx;
+      const size_t ky = YK ? (size_t)k0 : (size_t)k0 * s.ldy;
+      if (MODE == 0) {
+        TX::load_fast(s.X[seg] + ox + kx, s.ldx, g[0]);
+        TY::load_fast(s.Y[seg] + oy + ky, s.ldy, g[1]);
+      } else if (MODE == 1) {
+        TX::load_fast(s.X[0] + ox + kx, s.ldx, g[0]);
+        TX::load_fast(s.X[1] + ox + kx, s.ldx, g[1]);
+        TY::load_fast(s.Y[0] + oy + ky, s.ldy, g[2]);
+        TY::load_fast(s.Y[1] + oy + ky, s.ldy, g[3]);
+      } else {
+        TX::load_fast(s.X[0] + ox + kx, s.ldx, g[0]);
+        TY::load_fast(s.Y[0] + oy + ky, s.ldy, g[1]);
+        TY::load_fast(s.Y[1] + oy + ky, s.ldy, g[2]);
+      }
+      return;
+    }
     if (MODE == 0) {
       TX::load(s.X[seg], s.ldx, s.M, s.K, m0, k0, tid, g[0]);
       TY::load(s.Y[seg], s.ldy, s.N, s.K, n0, k0, tid, g[1]);
@@ -287,61 +401,63 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     }
   };
   auto compute = [&](int buf) {
-    float x0[2][8], y0[2][8];
+    float x0[W][HK], y0[W][HK];
     if (MODE == 0) {
 #pragma unroll
-      for (int a = 0; a < 2; ++a) TX::frag(lds[buf][0], wm * 64 + a * 32 + li, h, x0[a]);
+      for (int a = 0; a < W; ++a) TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
 #pragma unroll
-      for (int b = 0; b < 2; ++b) TY::frag(lds[buf][1], wn * 64 + b * 32 + li, h, y0[b]);
+      for (int b = 0; b < W; ++b) TY::frag(lds[buf][1], wn * 32 * W + b * 32 + li, h, y0[b]);
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
+      for (int k = 0; k < HK; ++k)
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int a = 0; a < W; ++a)
 #pragma unroll
-          for (int b = 0; b < 2; ++b) acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
+          for (int b = 0; b < W; ++b) acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
     } else if (MODE == 1) {
-      float x1[2][8], y1[2][8];
+      float x1[W][HK], y1[W][HK];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) {
-        TX::frag(lds[buf][0], wm * 64 + a * 32 + li, h, x0[a]);
-        TX::frag(lds[buf][1], wm * 64 + a * 32 + li, h, x1[a]);
+      for (int a = 0; a < W; ++a) {
+        TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
+        TX::frag(lds[buf][1], wm * 32 * W + a * 32 + li, h, x1[a]);
       }
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        TY::frag(lds[buf][2], wn * 64 + b * 32 + li, h, y0[b]);
-        TY::frag(lds[buf][3], wn * 64 + b * 32 + li, h, y1[b]);
+      for (int b = 0; b < W; ++b) {
+        TY::frag(lds[buf][2], wn * 32 * W + b * 32 + li, h, y0[b]);
+        TY::frag(lds[buf][3], wn * 32 * W + b * 32 + li, h, y1[b]);
       }
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
+      for (int k = 0; k < HK; ++k)
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int a = 0; a < W; ++a)
 #pragma unroll
-          for (int b = 0; b < 2; ++b) {
+          for (int b = 0; b < W; ++b) {
             acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
             acc1[a][b] = mfma(x1[a][k], y0[b][k], acc1[a][b]);
             acc1[a][b] = mfma(x0[a][k], y1[b][k], acc1[a][b]);
           }
     } else {
-      float y1[2][8];
+      float y1[W][HK];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) TX::frag(lds[buf][0], wm * 64 + a * 32 + li, h, x0[a]);
+      for (int a = 0; a < W; ++a) TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        TY::frag(lds[buf][1], wn * 64 + b * 32 + li, h, y0[b]);
-        TY::frag(lds[buf][2], wn * 64 + b * 32 + li, h, y1[b]);
+      for (int b = 0; b < W; ++b) {
+        TY::frag(lds[buf][1], wn * 32 * W + b * 32 + li, h, y0[b]);
+        TY::frag(lds[buf][2], wn * 32 * W + b * 32 + li, h, y1[b]);
       }
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
+      for (int k = 0; k < HK; ++k)
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int a = 0; a < W; ++a)
 #pragma unroll
-          for (int b = 0; b < 2; ++b) {
+          for (int b = 0; b < W; ++b) {
             acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
             acc1[a][b] = mfma(x0[a][k], y1[b][k], acc1[a][b]);
           }
     }
   };
 
+  // bias sums: thread t owns column t % ROWS and KPT consecutive k of a block
+  constexpr int KPT = BK * ROWS / NT;
   const bool do_bias = BIAS && blockIdx.x == 0 && (e.bias_out || e.bias_part);
   double bsum = 0.0;
   if (vb0 < vb1) {
@@ -354,10 +470,10 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
       if (more) gload(vb + 1);
       compute(buf);
       if (BIAS && do_bias && vb < kbps) {
-        // X tile is [k][m] (XK = false): this thread sums 8 k for column m
-        const float* xs = lds[buf][0] + (tid >> 7) * 8 * LDM + (tid & 127);
+        // X tile is [k][m] (XK = false)
+        const float* xs = lds[buf][0] + (tid / ROWS) * KPT * TX::LDM + tid % ROWS;
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) bsum += (double)xs[kk * LDM];
+        for (int kk = 0; kk < KPT; ++kk) bsum += (double)xs[kk * TX::LDM];
       }
       if (more) sstore(buf ^ 1);
       __syncthreads();
@@ -365,11 +481,12 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     }
   }
   if (BIAS && do_bias) {
-    __shared__ double bhalf[128];
-    if (tid >= 128) bhalf[tid - 128] = bsum;
+    static_assert(NT / ROWS <= 2, "bias combine handles at most two parts");
+    __shared__ double bpart2[NT];
+    if (NT / ROWS == 2 && tid >= ROWS) bpart2[tid - ROWS] = bsum;
     __syncthreads();
-    if (tid < 128 && m0 + tid < s.M) {
-      const double t = bsum + bhalf[tid];
+    if (tid < ROWS && m0 + tid < s.M) {
+      const double t = (NT / ROWS == 2) ? bsum + bpart2[tid] : bsum;
       if (s.splits > 1) e.bias_part[(size_t)blockIdx.z * s.M + m0 + tid] = t;
       else e.bias_out[m0 + tid] = (float)t;
     }
@@ -378,39 +495,47 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
   // 32x32 f32 accumulator layout: lane (li, h), register r holds
   // row 8 * (r / 4) + 4 * h + r % 4, column li of the 32 x 32 block.
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < W; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < W; ++b) {
+      const f32x16 v0 = acc0[a][b];
+      const f32x16 v1 = MODE == 0 ? v0 : acc1[a][b];
+      const int rbase = m0 + wm * 32 * W + a * 32 + 4 * h;
+      const int col = n0 + wn * 32 * W + b * 32 + li;
+      if (col < s.N) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        const int col = n0 + wn * 64 + b * 32 + li;
-        if (row < s.M && col < s.N)
-          Epi::apply(e, row, col, acc0[a][b][r], MODE == 0 ? 0.0f : acc1[a][b][r]);
+        for (int r = 0; r < 16; ++r) {
+          const int row = rbase + 8 * (r >> 2) + (r & 3);
+          if (row < s.M) Epi::apply(e, row, col, v0[r], MODE == 0 ? 0.0f : v1[r]);
+        }
       }
+      // keep the scheduler from hoisting every block's loads to the top
+      __builtin_amdgcn_sched_barrier(0);
+    }
 }
 
 }  // namespace
 
-#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS)                           \
+#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS, TR)                       \
   extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v4(GemmShape s,   \
                                                                  EpiArgs e) {   \
-    gemm_body<MODE, XK, YK, 4, EPI, BIAS>(s, e);                                \
+    gemm_body<MODE, XK, YK, 4, EPI, BIAS, TR>(s, e);                            \
   }                                                                             \
   extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v1(GemmShape s,   \
                                                                  EpiArgs e) {   \
-    gemm_body<MODE, XK, YK, 1, EPI, BIAS>(s, e);                                \
+    gemm_body<MODE, XK, YK, 1, EPI, BIAS, TR>(s, e);                            \
   }
 
-HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, true, EFwd, false)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false)
-HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, true, ERFwd, false)
-HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false)
-HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false)
-HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false)
-HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false)
-HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true)
+HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, true, EFwd, false, true)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, true, ERFwd, false, true)
+HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false, false)
+HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, false)
 
 namespace {
 
@@ -427,16 +552,21 @@ int pick_vec(const GemmShape& s, int mode) {
   return 4;
 }
 
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
 void launch(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1,
-            int mode, const GemmShape& s, const EpiArgs& e, double flops,
-            double bytes) {
+            int rows, int mode, const GemmShape& s, const EpiArgs& e,
+            double flops, double bytes) {
   const int vec = pick_vec(s, mode);
-  dim3 grid((s.N + BN - 1) / BN, (s.M + BM - 1) / BM,
+  dim3 grid(cdiv(s.N, rows), cdiv(s.M, rows),
             (mode == 0 && s.splits > 1) ? s.splits : 1);
   prof_begin(L, name);
   hipLaunchKernelGGL(vec == 4 ? k4 : k1, grid, dim3(NT), 0, L.stream, s, e);
   prof_end(L, name, flops, bytes);
 }
+
+#define HF_LAUNCH_SINGLE(NAME, L, s, e, fl, by) \
+  launch(L, #NAME, NAME##_v4, NAME##_v1, 128, 0, s, e, fl, by)
 
 inline double mnk(const GemmShape& s) { return 2.0 * s.M * s.N * (double)s.K; }
 inline double io(const GemmShape& s, int nx, int ny, int nout) {
@@ -447,41 +577,42 @@ inline double io(const GemmShape& s, int nx, int ny, int nout) {
 }  // namespace
 
 void gemm_fwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  launch(L, "hf_gemm_fwd", hf_gemm_fwd_v4, hf_gemm_fwd_v1, 0, s, e,
-         mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 1));
+  HF_LAUNCH_SINGLE(hf_gemm_fwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 1));
 }
 void gemm_fwd_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   if (s.X[1]) {
-    launch(L, "hf_gemm_fwd_rfwd", hf_gemm_fwd_rfwd_v4, hf_gemm_fwd_rfwd_v1, 1,
-           s, e, 3 * mnk(s), io(s, 2, 2, e.hidden ? 3 : 2));
+    launch(L, "hf_gemm_fwd_rfwd", hf_gemm_fwd_rfwd_v4, hf_gemm_fwd_rfwd_v1,
+           128, 1, s, e, 3 * mnk(s), io(s, 2, 2, e.hidden ? 3 : 2));
   } else {
     launch(L, "hf_gemm_fwd_rfwd0", hf_gemm_fwd_rfwd0_v4, hf_gemm_fwd_rfwd0_v1,
-           2, s, e, 2 * mnk(s), io(s, 1, 2, e.hidden ? 3 : 2));
+           128, 2, s, e, 2 * mnk(s), io(s, 1, 2, e.hidden ? 3 : 2));
   }
 }
 void gemm_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  launch(L, "hf_gemm_rfwd", hf_gemm_rfwd_v4, hf_gemm_rfwd_v1, 0, s, e,
-         mnk(s) * s.nseg, io(s, s.nseg, s.nseg, e.hidden ? 3 : 1));
+  HF_LAUNCH_SINGLE(hf_gemm_rfwd, L, s, e, mnk(s) * s.nseg,
+                   io(s, s.nseg, s.nseg, e.hidden ? 3 : 1));
 }
 void gemm_bwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  launch(L, "hf_gemm_bwd", hf_gemm_bwd_v4, hf_gemm_bwd_v1, 0, s, e,
-         mnk(s) * s.nseg, io(s, s.nseg, s.nseg, e.out2 ? 3 : 2));
+  if (e.out2)
+    HF_LAUNCH_SINGLE(hf_gemm_bwd_e2, L, s, e, mnk(s) * s.nseg,
+                     io(s, s.nseg, s.nseg, 3));
+  else
+    HF_LAUNCH_SINGLE(hf_gemm_bwd, L, s, e, mnk(s) * s.nseg,
+                     io(s, s.nseg, s.nseg, 2));
 }
 void gemm_bwd_rbwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  launch(L, "hf_gemm_bwd_rbwd", hf_gemm_bwd_rbwd_v4, hf_gemm_bwd_rbwd_v1, 1, s,
-         e, 3 * mnk(s), io(s, 2, 2, 4));
+  launch(L, "hf_gemm_bwd_rbwd", hf_gemm_bwd_rbwd_v4, hf_gemm_bwd_rbwd_v1, 128,
+         1, s, e, 3 * mnk(s), io(s, 2, 2, 4));
 }
 void gemm_rbwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  launch(L, "hf_gemm_rbwd", hf_gemm_rbwd_v4, hf_gemm_rbwd_v1, 0, s, e,
-         mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 4));
+  HF_LAUNCH_SINGLE(hf_gemm_rbwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 4));
 }
 void gemm_gnbwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  launch(L, "hf_gemm_gnbwd", hf_gemm_gnbwd_v4, hf_gemm_gnbwd_v1, 0, s, e,
-         mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 2));
+  HF_LAUNCH_SINGLE(hf_gemm_gnbwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 2));
 }
 void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  launch(L, "hf_gemm_wgrad", hf_gemm_wgrad_v4, hf_gemm_wgrad_v1, 0, s, e,
-         mnk(s) * s.nseg, io(s, s.nseg, s.nseg, s.splits > 1 ? s.splits : 1));
+  HF_LAUNCH_SINGLE(hf_gemm_wgrad, L, s, e, mnk(s) * s.nseg,
+                   io(s, s.nseg, s.nseg, s.splits > 1 ? s.splits : 1));
 }
 
 }  // namespace hfk

@@ -51,7 +51,8 @@ struct Profiler {
   std::vector<Pending> pending;
   std::vector<hipEvent_t> pool;
   hipEvent_t open = nullptr;
-  int tag = -1;   // CG iteration of the launches being recorded, -1 outside CG
+  int tag = -1;          // CG iteration of the launches being recorded, -1 outside CG
+  size_t solve_begin = 0;  // first pending entry of the CG solve in progress
 
   hipEvent_t get() {
     if (!pool.empty()) {
@@ -90,9 +91,10 @@ struct Profiler {
   // kernel did no vector work; neg_iter: iteration whose negative-curvature
   // kernels ran (-1: none).
   void retract(int last, bool stop_on_kappa, int neg_iter) {
-    std::vector<Pending> keep;
+    std::vector<Pending> keep(pending.begin(), pending.begin() + solve_begin);
     keep.reserve(pending.size());
-    for (auto& p : pending) {
+    for (size_t i = solve_begin; i < pending.size(); ++i) {
+      Pending& p = pending[i];
       bool drop = false;
       if (p.tag >= 0) {
         const std::string& nm = recs[p.rec].name;
@@ -140,7 +142,7 @@ void prof_end(const Launch& L, const char* name, double flops, double bytes) {
     P.pending.push_back({P.open, b, r, P.tag, flops, bytes});
   }
   P.open = nullptr;
-  if (P.pending.size() > (1u << 16)) P.collect();
+  if (P.tag < 0 && P.pending.size() > (1u << 16)) P.collect();
 }
 
 }  // namespace hfk
@@ -624,6 +626,7 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
     HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
     HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
   }
+  if (c->prof) c->prof->solve_begin = c->prof->pending.size();
   const Launch Lc = c->launch();
   const int b = (int)Bc;
   const long long n = c->n;

@@ -62,6 +62,10 @@ SMALL = [
     ((784, 100, 10), "sigmoid", 1000),
     # wide output layer, like the speech workload
     ((40, 96, 1973), "sigmoid", 200),
+    # enough rows for the 256 x 256 tiles, with ragged tile edges ...
+    ((64, 1100, 10), "tanh", 15000),
+    # ... and with unaligned widths (scalar global loads)
+    ((63, 1101, 10), "sigmoid", 15000),
 ]
 
 
