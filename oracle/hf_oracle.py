@@ -329,3 +329,82 @@ def cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
     def apply_A(p):
         return curvature(dims, act, theta, Xc, yc, p, mode)
     return cg_minimize(apply_A, g, lam, max_iters, rel_tol, record)
+
+
+# ----------------------------------------------------------------- Bi-CG-STAB
+def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
+    """Bi-CG-STAB (Alg. 3) for B_k d = -g_k, B_k = A + lam I, from d = 0
+    (Alg. 2: the Newton system is solved by Bi-CG-STAB from 0).
+
+    Each iteration follows the listing's steps in order: alpha from
+    (r_j, r0*) / (A p_j, r0*), the half step s_j, the stabilisation
+    coefficient gamma_j = (s_j, A s_j) / (A s_j, A s_j), the new iterate and
+    residual, beta_j = (r_{j+1}, r0*) / (r_j, r0*) * alpha_j / gamma_j and the
+    new direction.  Every iterate x_{j+1} is a candidate direction (Sec. 2.2):
+    its curvature x^T A x (undamped operator, computed here with an explicit
+    product) classifies it as a Newton-type (> 0) or negative-curvature (< 0)
+    direction; the first negative-curvature candidate is returned oriented as
+    d~ = -sgn(g^T x) x.
+
+    Readings of the listing (each also in the design notes): the "IF" is a
+    loop over the fixed budget ``max_iters`` (Sec. 2.2) with an optional
+    relative-residual stop; r0* = r0; gamma_j is the usual omega_j; a zero
+    (A p_j, r0*) or (r_{j+1}, r0*) ends the solve; A s_j = 0 gives gamma_j = 0
+    (then s_j = 0 for a nonsingular operator and x_{j+1} = x_j + alpha_j p_j).
+    """
+    g = np.asarray(g, dtype=np.float64)
+
+    def B(v):
+        return apply_A(v) + lam * v
+
+    x = np.zeros_like(g)
+    r = -g.copy()
+    rs = r.copy()            # r0*
+    p = r.copy()
+    rho = float(r @ rs)
+    rr0 = float(r @ r)
+    res = dict(step=x, neg_dir=None, iters=0, products=0, neg_curv=0,
+               neg_iter=-1, dBd=0.0, dHd=0.0, gTd=0.0, rr0=rr0, rr_final=rr0,
+               curvatures=[])
+    if rr0 == 0.0:
+        return res
+    for j in range(max_iters):
+        Ap = B(p)
+        res["products"] += 1
+        den = float(Ap @ rs)
+        if den == 0.0 or not np.isfinite(den):
+            break
+        alpha = rho / den
+        s = r - alpha * Ap
+        t = B(s)
+        res["products"] += 1
+        tt = float(t @ t)
+        gamma = float(s @ t) / tt if tt != 0.0 else 0.0
+        x = x + alpha * p + gamma * s
+        r = s - gamma * t
+        rr = float(r @ r)
+        res.update(step=x, iters=j + 1, rr_final=rr)
+        dHd = float(x @ apply_A(x))
+        if record:
+            res["curvatures"].append(dHd)
+        if dHd < 0.0 and not res["neg_curv"]:
+            d = -sgn(float(g @ x)) * x
+            res.update(neg_dir=d, neg_curv=1, neg_iter=j, dHd=dHd,
+                       dBd=dHd + lam * float(x @ x), gTd=float(g @ d))
+        if rel_tol > 0.0 and rr <= rel_tol * rel_tol * rr0:
+            break
+        rho_new = float(r @ rs)
+        if rho_new == 0.0 or gamma == 0.0:
+            break
+        beta = (rho_new / rho) * (alpha / gamma)
+        p = r + beta * (p - gamma * Ap)
+        rho = rho_new
+    return res
+
+
+def bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
+                     rel_tol=0.0, record=False):
+    """Bi-CG-STAB with the network's curvature operator on (Xc, yc)."""
+    def apply_A(p):
+        return curvature(dims, act, theta, Xc, yc, p, mode)
+    return bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol, record)

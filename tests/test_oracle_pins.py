@@ -453,3 +453,75 @@ def test_relu_kink_threshold_only_moves_the_step():
                                       kink=0.5 * zmin))
     assert np.array_equal(O.gvp(dims, "relu", th, p["X"], v),
                           O.gvp(dims, "relu", th, p["X"], v, kink=-0.5 * zmin))
+
+
+# ------------------------------------------------------------- Bi-CG-STAB
+def test_bicgstab_hand_computed_indefinite():
+    gd = read_golden("cg_hand_cases.txt")
+    r = O.bicgstab_minimize(diag_op(gd["bicg1.A_diag"]), np.array(gd["bicg1.g"]),
+                            gd["bicg1.lambda"], 10)
+    assert r["iters"] == gd["bicg1.iters"] and r["products"] == gd["bicg1.products"]
+    assert r["neg_curv"] == 1 and r["neg_iter"] == gd["bicg1.neg_iter"]
+    assert r["dHd"] == pytest.approx(gd["bicg1.dHd"], abs=1e-14)
+    np.testing.assert_allclose(r["neg_dir"], gd["bicg1.neg_dir"], atol=1e-14)
+    assert r["gTd"] == pytest.approx(gd["bicg1.gTd"], abs=1e-14)
+    np.testing.assert_allclose(r["step"], gd["bicg1.step"], atol=1e-14)
+
+
+@pytest.mark.parametrize("n,seed,sym", [(6, 0, True), (12, 1, True),
+                                        (8, 2, False), (15, 3, False)])
+def test_bicgstab_solves_well_conditioned_systems(n, seed, sym):
+    """Bi-CG-STAB solves symmetric and nonsymmetric nonsingular systems; the
+    result is pinned by numpy.linalg.solve."""
+    rng = np.random.default_rng(seed)
+    Q, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    A = (Q * np.geomspace(1.0, 10.0, n)) @ Q.T
+    if not sym:
+        A = A + 0.3 * rng.standard_normal((n, n)) / np.sqrt(n)
+    g = rng.standard_normal(n)
+    lam = 0.05
+    r = O.bicgstab_minimize(lambda p: A @ p, g, lam, 4 * n, rel_tol=1e-13)
+    x = np.linalg.solve(A + lam * np.eye(n), -g)
+    assert rel(r["step"], x) <= 1e-9
+    assert r["products"] == 2 * r["iters"]
+
+
+def test_bicgstab_residual_recurrence_and_candidates():
+    """The recurrence residual equals b - B x, and every candidate's
+    curvature equals x^T (A x) (pinned against the explicit matrix)."""
+    rng = np.random.default_rng(5)
+    n = 10
+    M = rng.standard_normal((n, n))
+    A = 0.5 * (M + M.T)                 # symmetric indefinite
+    g = rng.standard_normal(n)
+    lam = 0.1
+    for k in range(1, 6):
+        r = O.bicgstab_minimize(lambda p: A @ p, g, lam, k, record=True)
+        x = r["step"]
+        res = -g - (A + lam * np.eye(n)) @ x
+        assert r["rr_final"] == pytest.approx(res @ res, rel=1e-8)
+        assert r["curvatures"][-1] == pytest.approx(x @ A @ x, rel=1e-10)
+        if r["neg_curv"]:
+            d = r["neg_dir"]
+            assert g @ d < 0 and d @ A @ d < 0
+
+
+def test_planted_wrong_beta_sign_is_caught(monkeypatch):
+    real = O.bicgstab_minimize
+    n = 8
+    rng = np.random.default_rng(2)
+    Q, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    A = (Q * np.geomspace(1.0, 10.0, n)) @ Q.T
+    g = rng.standard_normal(n)
+    x = np.linalg.solve(A + 0.05 * np.eye(n), -g)
+    good = real(lambda p: A @ p, g, 0.05, 4 * n, rel_tol=1e-13)
+    assert rel(good["step"], x) <= 1e-9
+    # the same recurrences with beta's sign flipped no longer converge
+    src = __import__("inspect").getsource(real)
+    bad_src = src.replace("beta = (rho_new / rho) * (alpha / gamma)",
+                          "beta = -(rho_new / rho) * (alpha / gamma)")
+    assert bad_src != src
+    ns = dict(O.__dict__)
+    exec(compile(bad_src, "bad", "exec"), ns)
+    bad = ns["bicgstab_minimize"](lambda p: A @ p, g, 0.05, 4 * n, rel_tol=1e-13)
+    assert rel(bad["step"], x) > 1e-3
