@@ -16,11 +16,12 @@
 // LDS layouts (the gfx950 LDS has 64 four-byte banks):
 //  - a row-contiguous operand is kept as [k][row] (row stride 132 floats) and
 //    read with 32-bit LDS loads;
-//  - a K-contiguous operand is kept either as [row][k] with its four 16-byte
-//    k chunks XOR-swizzled by (row >> 2) & 3 (no bank conflicts on the
-//    128-bit stores and loads), or transposed on the way in to [k][row]; the
-//    transposed form measured faster when both operands are K-contiguous
-//    (forward and R-forward), the swizzled form otherwise.
+//  - a K-contiguous operand is kept as [row][k] with its four 16-byte k
+//    chunks XOR-swizzled by (row >> 2) & 3: no bank conflicts on the 128-bit
+//    stores and loads.
+// Every single-product GEMM pairs a K-contiguous left operand with a
+// row-contiguous right one (the forward passes take transposed weights),
+// the pairing that measured fastest on MI355X.
 // Within a K block each half-wave works on its own 8 consecutive k values,
 // which permutes the order of the K sum identically for both operands.
 #include "hf_internal.h"
@@ -59,10 +60,10 @@ __device__ __forceinline__ float act_d2(int act, float a) {
 
 // ------------------------------------------------------------ tile loading
 // A ROWS x BK operand tile.  MK: the operand is stored rows x K with K
-// contiguous, kept in LDS as swizzled [row][k] (stride LDK), or as [k][row]
-// when TR; otherwise K x rows with rows contiguous, kept as [k][row] (stride
-// LDM).  Each of the NT threads moves V1 floats per tile.
-template <bool MK, int VEC, int ROWS, bool TR = false>
+// contiguous, kept in LDS as swizzled [row][k] (stride LDK); otherwise
+// K x rows with rows contiguous, kept as [k][row] (stride LDM).  Each of the
+// NT threads moves V1 floats per tile.
+template <bool MK, int VEC, int ROWS>
 struct Tile {
   static constexpr int LDM = ROWS + 4;
   static constexpr int SIZE = (ROWS * LDK > BK * LDM) ? ROWS * LDK : BK * LDM;
@@ -142,25 +143,6 @@ struct Tile {
 
   __device__ static __forceinline__ void store(float* __restrict__ s, int tid,
                                                const float (&g)[V1]) {
-    if (MK && TR) {
-      // transpose into [k][row]
-      if (VEC == 4) {
-#pragma unroll
-        for (int i = 0; i < V4; ++i) {
-          const int idx = tid + NT * i;
-          const int row = idx / (BK / 4), k = (idx % (BK / 4)) * 4;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) s[(k + j) * LDM + row] = g[4 * i + j];
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < V1; ++i) {
-          const int idx = tid + NT * i;
-          s[(idx % BK) * LDM + idx / BK] = g[i];
-        }
-      }
-      return;
-    }
     if (VEC == 4) {
 #pragma unroll
       for (int i = 0; i < V4; ++i) {
@@ -194,7 +176,7 @@ struct Tile {
   // sum over k is unchanged.
   __device__ static __forceinline__ void frag(const float* __restrict__ s,
                                               int row, int h, float (&f)[HK]) {
-    if (MK && !TR) {
+    if (MK) {
 #pragma unroll
       for (int q = 0; q < HK / 4; ++q) {
         const int c = (h * HK) / 4 + q;
@@ -301,16 +283,15 @@ struct EStore {
 // MODE 0: single (nseg K-segments, optional split-K over grid z)
 // MODE 1: dual   acc0 = X0 Y0, acc1 = X1 Y0 + X0 Y1
 // MODE 2: dual0  acc0 = X0 Y0, acc1 = X0 Y1
-// TR: K-contiguous operands are transposed to [k][row] in LDS.
 // BIAS (weight gradient): blocks of the first column tile also sum their X
 // tiles of K-segment 0 over k, giving sum_k X(m, k) for their rows.
-template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS, bool TR>
+template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) {
   if (s.skip && *s.skip) return;
   constexpr int W = 2;          // 2 x 2 MFMA blocks per wave
   constexpr int ROWS = 64 * W;
-  using TX = Tile<XK, VEC, ROWS, TR>;
-  using TY = Tile<YK, VEC, ROWS, TR>;
+  using TX = Tile<XK, VEC, ROWS>;
+  using TY = Tile<YK, VEC, ROWS>;
   constexpr int T = MODE == 0 ? 2 : (MODE == 1 ? 4 : 3);
   constexpr int SZ = TX::SIZE > TY::SIZE ? TX::SIZE : TY::SIZE;
   constexpr int V1 = TX::V1;
@@ -345,44 +326,40 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
       }
 
   float g[T][V1];
-  // Rows of this tile lie inside both operands: every K block except a
-  // ragged last one can use unguarded loads.
-  const bool interior = m0 + ROWS <= s.M && n0 + ROWS <= s.N;
+  // Whether this tile's rows lie inside each operand: full K blocks of such
+  // an operand take unguarded loads, the rest (a ragged last K block, or an
+  // operand whose tile runs past its edge) take guarded ones.
+  const bool in_x = m0 + ROWS <= s.M;
+  const bool in_y = n0 + ROWS <= s.N;
   const size_t ox = TX::offset(s.ldx, tid) + (XK ? (size_t)m0 * s.ldx : (size_t)m0);
   const size_t oy = TY::offset(s.ldy, tid) + (YK ? (size_t)n0 * s.ldy : (size_t)n0);
+  auto ldx = [&](const float* base, int k0, float (&r)[V1]) {
+    if (in_x && k0 + BK <= s.K)
+      TX::load_fast(base + ox + (XK ? (size_t)k0 : (size_t)k0 * s.ldx), s.ldx, r);
+    else
+      TX::load(base, s.ldx, s.M, s.K, m0, k0, tid, r);
+  };
+  auto ldy = [&](const float* base, int k0, float (&r)[V1]) {
+    if (in_y && k0 + BK <= s.K)
+      TY::load_fast(base + oy + (YK ? (size_t)k0 : (size_t)k0 * s.ldy), s.ldy, r);
+    else
+      TY::load(base, s.ldy, s.N, s.K, n0, k0, tid, r);
+  };
   auto gload = [&](int vb) {
     const int seg = (MODE == 0) ? vb / kbps : 0;
     const int k0 = (vb - seg * kbps) * BK;
-    if (interior && k0 + BK <= s.K) {
-      const size_t kx = XK ? (size_t)k0 : (size_t)k0 * s.ldx;
-      const size_t ky = YK ? (size_t)k0 : (size_t)k0 * s.ldy;
-      if (MODE == 0) {
-        TX::load_fast(s.X[seg] + ox + kx, s.ldx, g[0]);
-        TY::load_fast(s.Y[seg] + oy + ky, s.ldy, g[1]);
-      } else if (MODE == 1) {
-        TX::load_fast(s.X[0] + ox + kx, s.ldx, g[0]);
-        TX::load_fast(s.X[1] + ox + kx, s.ldx, g[1]);
-        TY::load_fast(s.Y[0] + oy + ky, s.ldy, g[2]);
-        TY::load_fast(s.Y[1] + oy + ky, s.ldy, g[3]);
-      } else {
-        TX::load_fast(s.X[0] + ox + kx, s.ldx, g[0]);
-        TY::load_fast(s.Y[0] + oy + ky, s.ldy, g[1]);
-        TY::load_fast(s.Y[1] + oy + ky, s.ldy, g[2]);
-      }
-      return;
-    }
     if (MODE == 0) {
-      TX::load(s.X[seg], s.ldx, s.M, s.K, m0, k0, tid, g[0]);
-      TY::load(s.Y[seg], s.ldy, s.N, s.K, n0, k0, tid, g[1]);
+      ldx(s.X[seg], k0, g[0]);
+      ldy(s.Y[seg], k0, g[1]);
     } else if (MODE == 1) {
-      TX::load(s.X[0], s.ldx, s.M, s.K, m0, k0, tid, g[0]);
-      TX::load(s.X[1], s.ldx, s.M, s.K, m0, k0, tid, g[1]);
-      TY::load(s.Y[0], s.ldy, s.N, s.K, n0, k0, tid, g[2]);
-      TY::load(s.Y[1], s.ldy, s.N, s.K, n0, k0, tid, g[3]);
+      ldx(s.X[0], k0, g[0]);
+      ldx(s.X[1], k0, g[1]);
+      ldy(s.Y[0], k0, g[2]);
+      ldy(s.Y[1], k0, g[3]);
     } else {
-      TX::load(s.X[0], s.ldx, s.M, s.K, m0, k0, tid, g[0]);
-      TY::load(s.Y[0], s.ldy, s.N, s.K, n0, k0, tid, g[1]);
-      TY::load(s.Y[1], s.ldy, s.N, s.K, n0, k0, tid, g[2]);
+      ldx(s.X[0], k0, g[0]);
+      ldy(s.Y[0], k0, g[1]);
+      ldy(s.Y[1], k0, g[2]);
     }
   };
   auto sstore = [&](int buf) {
@@ -516,26 +493,26 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
 
 }  // namespace
 
-#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS, TR)                       \
+#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS)                           \
   extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v4(GemmShape s,   \
                                                                  EpiArgs e) {   \
-    gemm_body<MODE, XK, YK, 4, EPI, BIAS, TR>(s, e);                            \
+    gemm_body<MODE, XK, YK, 4, EPI, BIAS>(s, e);                                \
   }                                                                             \
   extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v1(GemmShape s,   \
                                                                  EpiArgs e) {   \
-    gemm_body<MODE, XK, YK, 1, EPI, BIAS, TR>(s, e);                            \
+    gemm_body<MODE, XK, YK, 1, EPI, BIAS>(s, e);                                \
   }
 
-HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, true, EFwd, false, true)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, true, ERFwd, false, true)
-HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false, false)
-HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, false)
+HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, false, EFwd, false)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false)
+HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false)
+HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false)
+HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false)
+HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false)
+HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false)
+HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false)
+HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true)
 
 namespace {
 

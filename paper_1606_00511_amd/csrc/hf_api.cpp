@@ -159,7 +159,7 @@ struct hf_ctx {
   hipStream_t stream = nullptr;
 
   // workspace carve-up (byte offsets), 1-based per layer where it applies
-  std::vector<size_t> oA, oD, oE2, oRZ, oRA, oRD;
+  std::vector<size_t> oA, oD, oE2, oRZ, oRA, oRD, oWT, oVT;
   size_t oZ = 0, oP = 0, oSplit = 0, oBpart = 0, oR = 0, oPv = 0, oQ = 0,
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
   int max_splits = 16;
@@ -219,6 +219,13 @@ void plan(hf_ctx* c) {
   c->oRZ.assign(L + 1, 0);
   c->oRA.assign(L + 1, 0);
   c->oRD.assign(L + 1, 0);
+  c->oWT.assign(L + 1, 0);
+  c->oVT.assign(L + 1, 0);
+  for (int l = 1; l <= L; ++l) {
+    // W_l and V_l transposed: d_{l-1} rows of ld_l floats
+    c->oWT[l] = take((size_t)c->d[l - 1] * c->ld[l] * sizeof(float));
+    c->oVT[l] = take((size_t)c->d[l - 1] * c->ld[l] * sizeof(float));
+  }
   for (int l = 1; l <= L; ++l) {
     const size_t sz = B * c->ld[l] * sizeof(float);
     if (l < L) {
@@ -336,16 +343,26 @@ void wgrad(hf_ctx* c, int l, int B, const float* x0, const float* y0,
   }
 }
 
+// Weight blocks of a parameter-layout vector, transposed to [d_{l-1}][ld_l]
+// (the row-contiguous right operand of the forward GEMMs).
+void transpose_weights(hf_ctx* c, const float* v, const std::vector<size_t>& dst,
+                       const int* skip) {
+  for (int l = 1; l <= c->L; ++l)
+    transpose(c->launch(), v + c->offW[l], c->d[l], c->d[l - 1], c->d[l - 1],
+              c->F(dst[l]), c->ld[l], skip);
+}
+
 // Forward pass (activations only) on B rows of X; logits into Z, then the
 // softmax / cross-entropy kernel (labels optional).
 void forward_plain(hf_ctx* c, const float* W, const float* X, int B,
                    const int32_t* y, bool want_delta) {
   const Launch Lc = c->launch();
+  transpose_weights(c, W, c->oWT, nullptr);
   for (int l = 1; l <= c->L; ++l) {
     const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
     const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
-    GemmShape s = shape(B, c->d[l], c->d[l - 1], Ain, nullptr, W + c->offW[l],
-                        nullptr, ldin, c->d[l - 1], 1, nullptr);
+    GemmShape s = shape(B, c->d[l], c->d[l - 1], Ain, nullptr, c->F(c->oWT[l]),
+                        nullptr, ldin, c->ld[l], 1, nullptr);
     EpiArgs e = epi(c, l < c->L);
     e.bias = W + c->offB[l];
     e.out0 = (l < c->L) ? c->F(c->oA[l]) : c->F(c->oZ);
@@ -372,19 +389,21 @@ void backward_data(hf_ctx* c, const float* W, int l, int B, bool cache_e2) {
 }
 
 // One curvature product out = A v on B rows of X with the forward cache
-// (A_l, p, delta_l, E2_l) already computed; skip = device flag or null.
+// (A_l, p, delta_l, E2_l and the transposed weights) already computed;
+// skip = device flag or null.
 void product_cached(hf_ctx* c, const float* W, const float* X, int B,
                     const float* v, int mode, float* out, const int* skip) {
   const Launch Lc = c->launch();
   const int L = c->L;
+  transpose_weights(c, v, c->oVT, skip);
   for (int l = 1; l <= L; ++l) {
     GemmShape s;
     if (l == 1) {
-      s = shape(B, c->d[1], c->d[0], X, nullptr, v + c->offW[1], nullptr,
-                c->d[0], c->d[0], 1, skip);
+      s = shape(B, c->d[1], c->d[0], X, nullptr, c->F(c->oVT[1]), nullptr,
+                c->d[0], c->ld[1], 1, skip);
     } else {
       s = shape(B, c->d[l], c->d[l - 1], c->F(c->oRA[l - 1]), c->F(c->oA[l - 1]),
-                W + c->offW[l], v + c->offW[l], c->ld[l - 1], c->d[l - 1], 2, skip);
+                c->F(c->oWT[l]), c->F(c->oVT[l]), c->ld[l - 1], c->ld[l], 2, skip);
     }
     EpiArgs e = epi(c, l < L);
     e.rbias = v + c->offB[l];

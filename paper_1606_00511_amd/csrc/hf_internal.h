@@ -64,13 +64,15 @@ struct EpiArgs {
   double* bias_part;
 };
 
-// Forward:  out0 = phi(acc + bias) (hidden) or acc + bias (logits)
+// Forward:  out0 = phi(acc + bias) (hidden) or acc + bias (logits);
+// the weights come transposed (Y row-contiguous: Y[k * ldy + n])
 void gemm_fwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
 // Forward + R-forward (dual / dual0):
 //   hidden: out0 = A = phi(acc0 + b), out1 = RZ = acc1 + c,
 //           out2 = RA = phi'(A) RZ;   output: out0 = acc0 + b, out1 = acc1 + c
 void gemm_fwd_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
-// R-forward on cached activations aux0 = A_l:
+// R-forward on cached activations aux0 = A_l, weights and direction
+// transposed (Y row-contiguous):
 //   out1 = RZ = acc + c; hidden: out2 = RA = phi'(A) RZ
 void gemm_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
 // Backward data for the gradient: out0 = delta = acc * phi'(aux0);
@@ -100,6 +102,9 @@ void loss_finalize(const Launch& L, const double* loss_part, int nparts,
 // Rdelta_L = P * (RZ - rowsum(P * RZ)) / B.
 void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
                  int C, int ld, float* RD, const int* skip);
+// out[c * ldo + r] = in[r * ldi + c] (R x C -> C x R)
+void transpose(const Launch& L, const float* in, int R, int C, int ldi,
+               float* out, int ldo, const int* skip);
 // out[m * ldo + n] = sum_z part[z * M * N + m * N + n] and
 // bout[m] = sum_z bpart[z * M + m], both in split order
 void splitk_reduce(const Launch& L, const float* part, const double* bpart,

@@ -174,6 +174,28 @@ extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce(
   }
 }
 
+// out[c * ldo + r] = in[r * ldi + c] for r < R, c < C, through a padded
+// 32 x 32 LDS tile so both the reads and the writes are coalesced.
+extern "C" __global__ __launch_bounds__(256) void hf_transpose(
+    const float* __restrict__ in, int R, int C, int ldi,
+    float* __restrict__ out, int ldo, const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  __shared__ float t[32][33];
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = r0 + ty + 8 * j, c = c0 + tx;
+    if (r < R && c < C) t[ty + 8 * j][tx] = in[(size_t)r * ldi + c];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = c0 + ty + 8 * j, r = r0 + tx;
+    if (r < R && c < C) out[(size_t)c * ldo + r] = t[tx][ty + 8 * j];
+  }
+}
+
 // ------------------------------------------------------------- launchers
 void softmax_xent(const Launch& L, const float* Z, const int32_t* y, int B,
                   int C, int ld, float* P, float* D, double* loss_part,
@@ -205,6 +227,14 @@ void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
   hipLaunchKernelGGL(hf_softmax_rop, dim3(blocks), dim3(256), lds, L.stream,
                      P, RZ, B, C, ld, 1.0f / (float)B, RD, skip);
   prof_end(L, "hf_softmax_rop", 0.0, 12.0 * B * C);
+}
+
+void transpose(const Launch& L, const float* in, int R, int C, int ldi,
+               float* out, int ldo, const int* skip) {
+  prof_begin(L, "hf_transpose");
+  hipLaunchKernelGGL(hf_transpose, dim3((C + 31) / 32, (R + 31) / 32), dim3(256),
+                     0, L.stream, in, R, C, ldi, out, ldo, skip);
+  prof_end(L, "hf_transpose", 0.0, 8.0 * R * C);
 }
 
 void splitk_reduce(const Launch& L, const float* part, const double* bpart,
