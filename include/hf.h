@@ -155,6 +155,32 @@ int hf_cg(hf_ctx* ctx, const float* W, const float* Xc, const int32_t* yc,
           float rel_tol, int32_t mode, float* step, float* neg_dir,
           hf_cg_info* info);
 
+/*
+ * hf_bicgstab: Bi-CG-STAB (Alg. 3; the solver behind the paper's results,
+ * Sec. 2.1 footnote) for B_k d = -g with B_k = A + lambda I, A = H or G on
+ * the fixed curvature batch (Xc, yc) of Bc rows at theta = W, from d = 0
+ * with r0* = r0 (Alg. 2: "starting point 0").  Two curvature products per
+ * iteration.  Every iterate x is a candidate direction (Sec. 2.2): its
+ * curvature x^T A x (from x^T B x = -(g, x) - (r, x), r being the residual)
+ * marks it Newton-type (> 0) or negative-curvature (< 0).
+ *   step      device, n fp32: the final iterate (the Newton-system solution)
+ *   neg_dir   device, n fp32: the FIRST negative-curvature candidate,
+ *             oriented d~ = -sgn(g^T x) x, or zeros if none was met
+ *   info      iters = completed iterations, products = curvature products,
+ *             neg_curv / neg_iter = whether and at which iteration the first
+ *             negative-curvature candidate appeared, pBp = d~^T B d~,
+ *             pHp = d~^T A d~ (< 0), gTd = g^T d~ (< 0), rr0 = |g|^2,
+ *             rr_final = |r|^2 at exit
+ * The solve runs max_iters iterations unless the relative residual falls
+ * below rel_tol (0 disables) or a denominator of the recurrences vanishes
+ * ((A p, r0*) = 0 or (r, r0*) = 0; A s = 0 takes gamma = 0).  Arguments as
+ * for hf_cg; the call synchronises the stream before it returns.
+ */
+int hf_bicgstab(hf_ctx* ctx, const float* W, const float* Xc, const int32_t* yc,
+                int64_t Bc, const float* g, float damping, int32_t max_iters,
+                float rel_tol, int32_t mode, float* step, float* neg_dir,
+                hf_cg_info* info);
+
 /* Synchronise the stream and report a device-detected error (HF_ELABEL)
  * raised since the last hf_check; clears the flag. */
 int hf_check(hf_ctx* ctx);

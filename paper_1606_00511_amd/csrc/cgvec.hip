@@ -290,7 +290,7 @@ int cg_grid(long long n) {
   return (int)b;
 }
 
-int cg_part_doubles() { return 5 * MAX_GRID; }
+int cg_part_doubles() { return 10 * MAX_GRID; }
 
 void cg_init(const Launch& L, const float* g, float* x, float* r, float* p,
              float* neg_dir, long long n, double lambda, double tol2,
@@ -332,6 +332,338 @@ void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
   hipLaunchKernelGGL(hf_cg_dir, dim3(nb), dim3(NT), 0, L.stream, r, p, n, j,
                      rpart, st);
   prof_end(L, "hf_cg_dir", 0.0, 3.0 * 4.0 * n);
+}
+
+// ========================================================== Bi-CG-STAB
+// Alg. 3 on B_k d = -g, B_k = A + lambda I, from d = 0 with r0* = r0.
+// Iteration j, with its two curvature products (Ap = B p_j, t = B s_j):
+//   bicg_dot1    partials of (Ap, r0*)
+//   bicg_s       alpha = rho_j / (Ap, r0*) (every block sums the partials);
+//                s = r - alpha Ap
+//   bicg_dot2    partials of (s, t) and (t, t)
+//   bicg_update  gamma = (s, t) / (t, t) (0 if t = 0); x += alpha p + gamma s;
+//                r = s - gamma t; partials of (r, r0*), (r, r), (g, x),
+//                (r, x), (x, x)
+//   bicg_dir     the candidate x_{j+1}: since r = -g - B x, its curvature is
+//                x^T B x = -(g, x) - (r, x) and x^T A x = x^T B x - lambda (x, x);
+//                beta = (rho_{j+1} / rho_j)(alpha / gamma); p = r + beta (p - gamma Ap)
+//   bicg_negw    at the first negative-curvature candidate: d~ = -sgn(g, x) x
+// Scalars stay in a BicgState; as for CG, blocks that need a reduced value
+// each sum the per-block partials in block order, and block 0 records it.
+namespace {
+constexpr int PA = 0;                 // (Ap, r0*)
+constexpr int PB = 1 * MAX_GRID;      // (s, t), (t, t)
+constexpr int PC = 3 * MAX_GRID;      // five dots of bicg_update
+constexpr int PI = 8 * MAX_GRID;      // (g, g) of the init
+}  // namespace
+
+extern "C" __global__ void hf_bicg_reset(BicgState* __restrict__ st) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    BicgState z = {};
+    *st = z;
+  }
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_bicg_init(
+    const float* __restrict__ g, float* __restrict__ x, float* __restrict__ r,
+    float* __restrict__ rs, float* __restrict__ p, float* __restrict__ nd,
+    long long n, double* __restrict__ part) {
+  __shared__ double sh[4];
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  double s = 0.0;
+  const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
+  for (long long i = t0; i < n4; i += stride) {
+    const f32x4 gv = ((const f32x4*)g)[i];
+    ((f32x4*)x)[i] = z4;
+    ((f32x4*)r)[i] = -gv;
+    ((f32x4*)rs)[i] = -gv;
+    ((f32x4*)p)[i] = -gv;
+    ((f32x4*)nd)[i] = z4;
+    s += dot4(gv, gv);
+  }
+  for (long long i = n4 * 4 + t0; i < n; i += stride) {
+    const float gv = g[i];
+    x[i] = 0.f; r[i] = -gv; rs[i] = -gv; p[i] = -gv; nd[i] = 0.f;
+    s += (double)gv * gv;
+  }
+  s = block_sum(s, sh);
+  if (threadIdx.x == 0) part[PI + blockIdx.x] = s;
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_bicg_init_fin(
+    const double* __restrict__ part, int nb, double lambda, double tol2,
+    BicgState* __restrict__ st) {
+  __shared__ double sh[4];
+  const double rr = total(part + PI, nb, sh);
+  if (threadIdx.x == 0) {
+    st->rho[0] = rr;          // (r0, r0*) = |g|^2
+    st->rr0 = rr;
+    st->rr = rr;
+    st->lambda = lambda;
+    st->tol2 = tol2;
+    st->neg_iter = -1;
+    st->status = is_fin(rr) ? 0 : -5;
+    st->done = (rr == 0.0 || !is_fin(rr)) ? 1 : 0;
+  }
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_bicg_dot1(
+    const float* __restrict__ Ap, const float* __restrict__ rs, long long n,
+    double* __restrict__ part, const BicgState* __restrict__ st) {
+  if (st->done) return;
+  __shared__ double sh[4];
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  double a = 0.0;
+  for (long long i = t0; i < n4; i += stride)
+    a += dot4(((const f32x4*)Ap)[i], ((const f32x4*)rs)[i]);
+  for (long long e = n4 * 4 + t0; e < n; e += stride) a += (double)Ap[e] * rs[e];
+  a = block_sum(a, sh);
+  if (threadIdx.x == 0) part[PA + blockIdx.x] = a;
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_bicg_s(
+    const float* __restrict__ r, const float* __restrict__ Ap,
+    float* __restrict__ s, long long n, int j, const double* __restrict__ part,
+    BicgState* __restrict__ st) {
+  if (st->done) return;
+  __shared__ double sh[4];
+  const double den = total(part + PA, gridDim.x, sh);
+  const double alpha = st->rho[j & 1] / den;
+  const bool stop = den == 0.0 || !is_fin(alpha);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    st->products = 2 * j + 1;
+    st->alpha = alpha;
+    if (stop) {
+      if (!is_fin(den)) st->status = -5;
+      st->done = 1;
+    }
+  }
+  if (stop) return;
+  const float a = (float)alpha;
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  for (long long i = t0; i < n4; i += stride)
+    ((f32x4*)s)[i] = ((const f32x4*)r)[i] - a * ((const f32x4*)Ap)[i];
+  for (long long e = n4 * 4 + t0; e < n; e += stride) s[e] = r[e] - a * Ap[e];
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_bicg_dot2(
+    const float* __restrict__ s, const float* __restrict__ t, long long n,
+    double* __restrict__ part, const BicgState* __restrict__ st) {
+  if (st->done) return;
+  __shared__ double sh[4];
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  double st_ = 0.0, tt = 0.0;
+  for (long long i = t0; i < n4; i += stride) {
+    const f32x4 a = ((const f32x4*)s)[i], b = ((const f32x4*)t)[i];
+    st_ += dot4(a, b);
+    tt += dot4(b, b);
+  }
+  for (long long e = n4 * 4 + t0; e < n; e += stride) {
+    st_ += (double)s[e] * t[e];
+    tt += (double)t[e] * t[e];
+  }
+  st_ = block_sum(st_, sh);
+  tt = block_sum(tt, sh);
+  if (threadIdx.x == 0) {
+    part[PB + blockIdx.x] = st_;
+    part[PB + MAX_GRID + blockIdx.x] = tt;
+  }
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_bicg_update(
+    float* __restrict__ x, float* __restrict__ r, const float* __restrict__ rs,
+    const float* __restrict__ p, const float* __restrict__ s,
+    const float* __restrict__ t, const float* __restrict__ g, long long n,
+    int j, double* __restrict__ part, BicgState* __restrict__ st) {
+  if (st->done) return;
+  __shared__ double sh[4];
+  const double stv = total(part + PB, gridDim.x, sh);
+  const double tt = total(part + PB + MAX_GRID, gridDim.x, sh);
+  const double gamma = tt != 0.0 ? stv / tt : 0.0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    st->gamma = gamma;
+    st->products = 2 * j + 2;
+    st->iters = j + 1;
+  }
+  const float a = (float)st->alpha, c = (float)gamma;
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0, d4 = 0.0;
+  for (long long i = t0; i < n4; i += stride) {
+    const f32x4 sv = ((const f32x4*)s)[i], tv = ((const f32x4*)t)[i];
+    f32x4 xv = ((f32x4*)x)[i];
+    xv += a * ((const f32x4*)p)[i] + c * sv;
+    const f32x4 rv = sv - c * tv;
+    ((f32x4*)x)[i] = xv;
+    ((f32x4*)r)[i] = rv;
+    d0 += dot4(rv, ((const f32x4*)rs)[i]);
+    d1 += dot4(rv, rv);
+    d2 += dot4(((const f32x4*)g)[i], xv);
+    d3 += dot4(rv, xv);
+    d4 += dot4(xv, xv);
+  }
+  for (long long e = n4 * 4 + t0; e < n; e += stride) {
+    const float xv = x[e] + a * p[e] + c * s[e];
+    const float rv = s[e] - c * t[e];
+    x[e] = xv;
+    r[e] = rv;
+    d0 += (double)rv * rs[e];
+    d1 += (double)rv * rv;
+    d2 += (double)g[e] * xv;
+    d3 += (double)rv * xv;
+    d4 += (double)xv * xv;
+  }
+  d0 = block_sum(d0, sh);
+  d1 = block_sum(d1, sh);
+  d2 = block_sum(d2, sh);
+  d3 = block_sum(d3, sh);
+  d4 = block_sum(d4, sh);
+  if (threadIdx.x == 0) {
+    part[PC + blockIdx.x] = d0;
+    part[PC + MAX_GRID + blockIdx.x] = d1;
+    part[PC + 2 * MAX_GRID + blockIdx.x] = d2;
+    part[PC + 3 * MAX_GRID + blockIdx.x] = d3;
+    part[PC + 4 * MAX_GRID + blockIdx.x] = d4;
+  }
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_bicg_dir(
+    float* __restrict__ p, const float* __restrict__ r,
+    const float* __restrict__ Ap, long long n, int j,
+    const double* __restrict__ part, BicgState* __restrict__ st) {
+  if (st->done) return;
+  __shared__ double sh[4];
+  const int nb = gridDim.x;
+  const double rho1 = total(part + PC, nb, sh);
+  const double rr = total(part + PC + MAX_GRID, nb, sh);
+  const double gx = total(part + PC + 2 * MAX_GRID, nb, sh);
+  const double rx = total(part + PC + 3 * MAX_GRID, nb, sh);
+  const double xx = total(part + PC + 4 * MAX_GRID, nb, sh);
+  const double rho = st->rho[j & 1];
+  const double gamma = st->gamma;
+  const double xBx = -gx - rx;
+  const double xHx = xBx - st->lambda * xx;
+  const bool bad = !is_fin(rr) || !is_fin(rho1) || !is_fin(xBx);
+  const bool stop = bad || (st->tol2 > 0.0 && rr <= st->tol2 * st->rr0) ||
+                    rho1 == 0.0 || gamma == 0.0;
+  const double beta = stop ? 0.0 : (rho1 / rho) * (st->alpha / gamma);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    st->rr = rr;
+    st->rho[(j + 1) & 1] = rho1;
+    st->beta = beta;
+    if (xHx < 0.0 && st->neg_iter < 0) {
+      st->neg = 1;
+      st->neg_iter = j;
+      st->dHd = xHx;
+      st->dBd = xBx;
+      st->coef = gx >= 0.0 ? -1.0 : 1.0;     // d~ = -sgn(g.x) x
+      st->gTd = st->coef * gx;
+    }
+    if (bad) st->status = -5;
+    if (stop) st->done = 1;
+  }
+  if (stop) return;
+  const float b = (float)beta, c = (float)gamma;
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  for (long long i = t0; i < n4; i += stride)
+    ((f32x4*)p)[i] = ((const f32x4*)r)[i] +
+                     b * (((const f32x4*)p)[i] - c * ((const f32x4*)Ap)[i]);
+  for (long long e = n4 * 4 + t0; e < n; e += stride)
+    p[e] = r[e] + b * (p[e] - c * Ap[e]);
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_bicg_negw(
+    const float* __restrict__ x, float* __restrict__ nd, long long n, int j,
+    const BicgState* __restrict__ st) {
+  if (st->neg_iter != j) return;
+  const float c = (float)st->coef;
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  for (long long i = t0; i < n4; i += stride)
+    ((f32x4*)nd)[i] = c * ((const f32x4*)x)[i];
+  for (long long e = n4 * 4 + t0; e < n; e += stride) nd[e] = c * x[e];
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_axpy(
+    float* __restrict__ y, const float* __restrict__ x, float a, long long n,
+    const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  for (long long i = t0; i < n4; i += stride)
+    ((f32x4*)y)[i] += a * ((const f32x4*)x)[i];
+  for (long long e = n4 * 4 + t0; e < n; e += stride) y[e] += a * x[e];
+}
+
+void axpy(const Launch& L, float* y, const float* x, float a, long long n,
+          const int* skip) {
+  prof_begin(L, "hf_axpy");
+  hipLaunchKernelGGL(hf_axpy, dim3(cg_grid(n)), dim3(NT), 0, L.stream, y, x, a,
+                     n, skip);
+  prof_end(L, "hf_axpy", 0.0, 3.0 * 4.0 * n);
+}
+
+void bicg_init(const Launch& L, const float* g, float* x, float* r, float* rs,
+               float* p, float* neg_dir, long long n, double lambda,
+               double tol2, double* part, BicgState* st) {
+  const int nb = cg_grid(n);
+  hipLaunchKernelGGL(hf_bicg_reset, dim3(1), dim3(64), 0, L.stream, st);
+  prof_begin(L, "hf_bicg_init");
+  hipLaunchKernelGGL(hf_bicg_init, dim3(nb), dim3(NT), 0, L.stream, g, x, r, rs,
+                     p, neg_dir, n, part);
+  prof_end(L, "hf_bicg_init", 0.0, 6.0 * 4.0 * n);
+  hipLaunchKernelGGL(hf_bicg_init_fin, dim3(1), dim3(NT), 0, L.stream, part, nb,
+                     lambda, tol2, st);
+}
+
+void bicg_half(const Launch& L, const float* r, const float* rs,
+               const float* Ap, float* s, long long n, int j, double* part,
+               BicgState* st) {
+  const int nb = cg_grid(n);
+  prof_begin(L, "hf_bicg_dot1");
+  hipLaunchKernelGGL(hf_bicg_dot1, dim3(nb), dim3(NT), 0, L.stream, Ap, rs, n,
+                     part, st);
+  prof_end(L, "hf_bicg_dot1", 0.0, 2.0 * 4.0 * n);
+  prof_begin(L, "hf_bicg_s");
+  hipLaunchKernelGGL(hf_bicg_s, dim3(nb), dim3(NT), 0, L.stream, r, Ap, s, n, j,
+                     part, st);
+  prof_end(L, "hf_bicg_s", 0.0, 3.0 * 4.0 * n);
+}
+
+void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
+               const float* Ap, const float* s, const float* t, const float* g,
+               float* neg_dir, long long n, int j, double* part,
+               BicgState* st) {
+  const int nb = cg_grid(n);
+  prof_begin(L, "hf_bicg_dot2");
+  hipLaunchKernelGGL(hf_bicg_dot2, dim3(nb), dim3(NT), 0, L.stream, s, t, n,
+                     part, st);
+  prof_end(L, "hf_bicg_dot2", 0.0, 2.0 * 4.0 * n);
+  prof_begin(L, "hf_bicg_update");
+  hipLaunchKernelGGL(hf_bicg_update, dim3(nb), dim3(NT), 0, L.stream, x, r, rs,
+                     p, s, t, g, n, j, part, st);
+  prof_end(L, "hf_bicg_update", 0.0, 8.0 * 4.0 * n);
+  prof_begin(L, "hf_bicg_dir");
+  hipLaunchKernelGGL(hf_bicg_dir, dim3(nb), dim3(NT), 0, L.stream, p, r, Ap, n,
+                     j, part, st);
+  prof_end(L, "hf_bicg_dir", 0.0, 4.0 * 4.0 * n);
+  prof_begin(L, "hf_bicg_negw");
+  hipLaunchKernelGGL(hf_bicg_negw, dim3(nb), dim3(NT), 0, L.stream, x, neg_dir,
+                     n, j, st);
+  prof_end(L, "hf_bicg_negw", 0.0, 2.0 * 4.0 * n);
 }
 
 }  // namespace hfk

@@ -116,6 +116,30 @@ struct Profiler {
     }
     pending.swap(keep);
   }
+  // Bi-CG-STAB: launches are tagged with the index of the curvature product
+  // they belong to (2j, 2j+1); drop those past the last product evaluated and
+  // the candidate writes of iterations without a detection.
+  void retract_bicg(int products, int neg_iter) {
+    std::vector<Pending> keep(pending.begin(), pending.begin() + solve_begin);
+    for (size_t i = solve_begin; i < pending.size(); ++i) {
+      Pending& p = pending[i];
+      bool drop = false;
+      if (p.tag >= 0) {
+        if (p.tag >= products) drop = true;
+        else if (recs[p.rec].name == "hf_bicg_negw") drop = p.tag / 2 != neg_iter;
+      }
+      if (drop) {
+        recs[p.rec].launches -= 1;
+        recs[p.rec].flops -= p.flops;
+        recs[p.rec].bytes -= p.bytes;
+        pool.push_back(p.a);
+        pool.push_back(p.b);
+      } else {
+        keep.push_back(p);
+      }
+    }
+    pending.swap(keep);
+  }
   ~Profiler() {
     collect();
     for (auto e : pool) (void)hipEventDestroy(e);
@@ -160,6 +184,7 @@ struct hf_ctx {
 
   // workspace carve-up (byte offsets), 1-based per layer where it applies
   std::vector<size_t> oA, oD, oE2, oRZ, oRA, oRD, oWT, oVT;
+  size_t oS = 0, oT = 0, oRs = 0;    // Bi-CG-STAB: s, t = B s, r0*
   size_t oZ = 0, oP = 0, oSplit = 0, oBpart = 0, oR = 0, oPv = 0, oQ = 0,
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
   int max_splits = 16;
@@ -171,6 +196,7 @@ struct hf_ctx {
   std::string err;
   Profiler* prof = nullptr;
   CgState* pinned = nullptr;       // 2 host-pinned copies of the CG state
+  void* pinned_bicg = nullptr;     // 2 host-pinned copies of the Bi-CG-STAB state
   hipEvent_t ev[2] = {nullptr, nullptr};
 
   float* F(size_t off) const { return reinterpret_cast<float*>(ws + off); }
@@ -252,9 +278,13 @@ void plan(hf_ctx* c) {
   c->oR = take(nv * sizeof(float));
   c->oPv = take(nv * sizeof(float));
   c->oQ = take(nv * sizeof(float));
+  c->oS = take(nv * sizeof(float));
+  c->oT = take(nv * sizeof(float));
+  c->oRs = take(nv * sizeof(float));
   c->oRed = take((size_t)cg_part_doubles() * sizeof(double));
   c->oLoss = take(((B + 3) / 4) * sizeof(double));
-  c->oState = take(sizeof(CgState));
+  c->oState = take(sizeof(CgState) > sizeof(BicgState) ? sizeof(CgState)
+                                                        : sizeof(BicgState));
   c->oErr = take(sizeof(int));
   c->need = off;
 }
@@ -446,6 +476,12 @@ void product_cached(hf_ctx* c, const float* W, const float* X, int B,
   }
 }
 
+// q += lambda v: the damping term of B_k = A + lambda I (Alg. 1 step 3)
+void lambda_axpy(hf_ctx* c, float* q, const float* v, float lambda,
+                 const int* skip) {
+  if (lambda != 0.0f) axpy(c->launch(), q, v, lambda, c->n, skip);
+}
+
 }  // namespace
 
 // ==================================================================== C ABI
@@ -494,6 +530,7 @@ int hf_destroy(hf_ctx* c) {
   if (!c) return HF_OK;
   delete c->prof;
   if (c->pinned) (void)hipHostFree(c->pinned);
+  if (c->pinned_bicg) (void)hipHostFree(c->pinned_bicg);
   for (auto& e : c->ev)
     if (e) (void)hipEventDestroy(e);
   delete c;
@@ -706,6 +743,104 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
     return fail(c, HF_ELABEL, "a label outside [0, %d) was seen", c->d[c->L]);
   }
   if (s.status) return fail(c, HF_ENUMERIC, "non-finite CG scalar");
+  return HF_OK;
+}
+
+int hf_bicgstab(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
+                int64_t Bc, const float* g, float damping, int32_t max_iters,
+                float rel_tol, int32_t mode, float* step, float* neg_dir,
+                hf_cg_info* info) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, Xc, "Xc")) ||
+      (rc = check_ptr(c, g, "g")) || (rc = check_ptr(c, step, "step")) ||
+      (rc = check_ptr(c, neg_dir, "neg_dir")) || (rc = check_batch(c, Bc)))
+    return rc;
+  if (!info) return fail(c, HF_EINVAL, "info is NULL");
+  if (mode != HF_HESSIAN && mode != HF_GAUSS_NEWTON)
+    return fail(c, HF_EINVAL, "unknown mode %d", mode);
+  if (mode == HF_HESSIAN && !yc) return fail(c, HF_EINVAL, "yc is NULL");
+  if (!(damping >= 0.0f) || !std::isfinite(damping))
+    return fail(c, HF_EINVAL, "damping must be finite and >= 0");
+  if (max_iters < 0) return fail(c, HF_EINVAL, "max_iters < 0");
+  if (!(rel_tol >= 0.0f) || !std::isfinite(rel_tol))
+    return fail(c, HF_EINVAL, "rel_tol must be finite and >= 0");
+  std::memset(info, 0, sizeof *info);
+  if (!c->pinned) {
+    HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
+  }
+  BicgState* hostst = reinterpret_cast<BicgState*>(c->pinned_bicg);
+  if (!hostst) {
+    HIP_TRY(c, hipHostMalloc((void**)&c->pinned_bicg, 2 * sizeof(BicgState),
+                             hipHostMallocDefault));
+    hostst = reinterpret_cast<BicgState*>(c->pinned_bicg);
+  }
+  if (c->prof) c->prof->solve_begin = c->prof->pending.size();
+  const Launch Lc = c->launch();
+  const int b = (int)Bc;
+  const long long n = c->n;
+  const bool hess = mode == HF_HESSIAN;
+  BicgState* st = reinterpret_cast<BicgState*>(c->ws + c->oState);
+  const int* skip = &st->done;
+  double* part = c->Dp(c->oRed);
+  float* r = c->F(c->oR);
+  float* p = c->F(c->oPv);
+  float* Ap = c->F(c->oQ);
+  float* sv = c->F(c->oS);
+  float* t = c->F(c->oT);
+  float* rs = c->F(c->oRs);
+
+  forward_plain(c, W, Xc, b, hess ? yc : nullptr, hess);
+  if (hess)
+    for (int l = c->L; l >= 2; --l) backward_data(c, W, l, b, true);
+  bicg_init(Lc, g, step, r, rs, p, neg_dir, n, (double)damping,
+            (double)rel_tol * (double)rel_tol, part, st);
+  for (int j = 0; j < max_iters; ++j) {
+    if (c->prof) c->prof->tag = 2 * j;
+    product_cached(c, W, Xc, b, p, mode, Ap, skip);
+    lambda_axpy(c, Ap, p, damping, skip);
+    bicg_half(Lc, r, rs, Ap, sv, n, j, part, st);
+    if (c->prof) c->prof->tag = 2 * j + 1;
+    product_cached(c, W, Xc, b, sv, mode, t, skip);
+    lambda_axpy(c, t, sv, damping, skip);
+    bicg_rest(Lc, step, r, rs, p, Ap, sv, t, g, neg_dir, n, j, part, st);
+    HIP_TRY(c, hipMemcpyAsync(&hostst[j & 1], st, sizeof(BicgState),
+                              hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
+    if (j >= 1) {
+      HIP_TRY(c, hipEventSynchronize(c->ev[(j - 1) & 1]));
+      if (hostst[(j - 1) & 1].done) break;
+    }
+  }
+  if (c->prof) c->prof->tag = -1;
+  HIP_TRY(c, hipGetLastError());
+  HIP_TRY(c, hipMemcpyAsync(&hostst[0], st, sizeof(BicgState),
+                            hipMemcpyDeviceToHost, c->stream));
+  int errflag = 0;
+  HIP_TRY(c, hipMemcpyAsync(&errflag, c->ws + c->oErr, sizeof(int),
+                            hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const BicgState& s = hostst[0];
+  if (c->prof) c->prof->retract_bicg(s.products, s.neg ? s.neg_iter : -1);
+  info->iters = s.iters;
+  info->products = s.products;
+  info->neg_curv = s.neg;
+  info->neg_iter = s.neg ? s.neg_iter : -1;
+  info->pBp = s.neg ? s.dBd : 0.0;
+  info->pHp = s.neg ? s.dHd : 0.0;
+  info->gTd = s.neg ? s.gTd : 0.0;
+  info->rr0 = s.rr0;
+  info->rr_final = s.rr;
+  info->status = s.status;
+  if (errflag) {
+    info->status = HF_ELABEL;
+    int zero = 0;
+    HIP_TRY(c, hipMemcpy(c->ws + c->oErr, &zero, sizeof(int), hipMemcpyHostToDevice));
+    return fail(c, HF_ELABEL, "a label outside [0, %d) was seen", c->d[c->L]);
+  }
+  if (s.status) return fail(c, HF_ENUMERIC, "non-finite Bi-CG-STAB scalar");
   return HF_OK;
 }
 

@@ -133,4 +133,31 @@ void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
                   const float* g, float* neg_dir, long long n, int j,
                   double* part, CgState* st);
 
+// ----------------------------------------------------------- Bi-CG-STAB
+struct BicgState {
+  double rho[2];       // (r_j, r0*), slot = iteration parity
+  double rr0, rr, alpha, gamma, beta;
+  double lambda, tol2;
+  double dBd, dHd, gTd, coef;   // first negative-curvature candidate
+  int done, status, iters, products, neg, neg_iter;
+};
+
+// y += a x (the damping term of B = A + lambda I)
+void axpy(const Launch& L, float* y, const float* x, float a, long long n,
+          const int* skip);
+// x = 0, r = r0* = p = -g, neg_dir = 0; state initialised
+void bicg_init(const Launch& L, const float* g, float* x, float* r, float* rs,
+               float* p, float* neg_dir, long long n, double lambda,
+               double tol2, double* part, BicgState* st);
+// first half of iteration j, after Ap = B p: alpha and s = r - alpha Ap
+void bicg_half(const Launch& L, const float* r, const float* rs,
+               const float* Ap, float* s, long long n, int j, double* part,
+               BicgState* st);
+// second half, after t = B s: gamma, x, r, candidate curvature, beta, p,
+// and the oriented candidate at the first negative curvature
+void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
+               const float* Ap, const float* s, const float* t, const float* g,
+               float* neg_dir, long long n, int j, double* part,
+               BicgState* st);
+
 }  // namespace hfk

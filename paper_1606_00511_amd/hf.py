@@ -25,7 +25,7 @@ MODES = {"hessian": HF_HESSIAN, "gauss_newton": HF_GAUSS_NEWTON}
 EXPORTS = (
     "hf_create", "hf_destroy", "hf_set_stream", "hf_num_params",
     "hf_workspace_bytes", "hf_set_workspace", "hf_loss_grad", "hf_hvp",
-    "hf_cg", "hf_check", "hf_last_error", "hf_strerror", "hf_prof_enable",
+    "hf_cg", "hf_bicgstab", "hf_check", "hf_last_error", "hf_strerror", "hf_prof_enable",
     "hf_prof_reset", "hf_prof_count", "hf_prof_get",
 )
 
@@ -77,6 +77,8 @@ def lib():
         "hf_hvp": (ctypes.c_int, [P, P, P, P, I64, P, I32, P]),
         "hf_cg": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P, P,
                                  ctypes.POINTER(hf_cg_info)]),
+        "hf_bicgstab": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P,
+                                       P, ctypes.POINTER(hf_cg_info)]),
         "hf_check": (ctypes.c_int, [P]),
         "hf_last_error": (ctypes.c_char_p, [P]),
         "hf_strerror": (ctypes.c_char_p, [I32]),
@@ -201,6 +203,16 @@ class HFNet:
 
     def hf_cg(self, W, Xc, yc, g, damping, max_iters, mode="hessian",
               rel_tol=0.0, step=None, neg_dir=None):
+        return self._solve("hf_cg", W, Xc, yc, g, damping, max_iters, mode,
+                           rel_tol, step, neg_dir)
+
+    def hf_bicgstab(self, W, Xc, yc, g, damping, max_iters, mode="hessian",
+                    rel_tol=0.0, step=None, neg_dir=None):
+        return self._solve("hf_bicgstab", W, Xc, yc, g, damping, max_iters,
+                           mode, rel_tol, step, neg_dir)
+
+    def _solve(self, fn, W, Xc, yc, g, damping, max_iters, mode, rel_tol, step,
+               neg_dir):
         import torch
         B = self._rows(Xc)
         if step is None:
@@ -209,7 +221,7 @@ class HFNet:
             neg_dir = torch.empty(self.n, dtype=torch.float32, device=self.device)
         info = hf_cg_info()
         self._stream()
-        rc = lib().hf_cg(
+        rc = getattr(lib(), fn)(
             self._h, _ptr(W, torch.float32, self.n, "W"),
             _ptr(Xc, torch.float32, None, "Xc"),
             _ptr(yc, torch.int32, B, "yc") if yc is not None else None, B,

@@ -85,6 +85,8 @@ def test_calls_without_workspace_or_with_bad_args(L):
     info = H.hf_cg_info()
     assert L.hf_cg(h, fake, fake, fake, 4, fake, 0.01, 5, 0.0, 0, fake, fake,
                    ctypes.byref(info)) == H.HF_EWORKSPACE
+    assert L.hf_bicgstab(h, fake, fake, fake, 4, fake, 0.01, 5, 0.0, 0, fake,
+                         fake, ctypes.byref(info)) == H.HF_EWORKSPACE
     assert L.hf_destroy(h) == H.HF_OK
     assert n == 6 * 9 + 4 * 7
 
