@@ -332,7 +332,8 @@ def cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
 
 
 # ----------------------------------------------------------------- Bi-CG-STAB
-def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
+def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
+                      store=None):
     """Bi-CG-STAB (Alg. 3) for B_k d = -g_k, B_k = A + lam I, from d = 0
     (Alg. 2: the Newton system is solved by Bi-CG-STAB from 0).
 
@@ -351,7 +352,14 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
     relative-residual stop; r0* = r0; gamma_j is the usual omega_j; a zero
     (A p_j, r0*) or (r_{j+1}, r0*) ends the solve; A s_j = 0 gives gamma_j = 0
     (then s_j = 0 for a nonsingular operator and x_{j+1} = x_j + alpha_j p_j).
+
+    ``store`` (identity when None) is applied to every vector the recurrences
+    keep (s, x, r, p) as it is formed.  Tests pass a rounding to float32 to
+    measure how far storage rounding alone moves the iterates: near a
+    breakdown of the recurrences that sensitivity is large, and it sets the
+    bound for comparing a float32 implementation with this fp64 one.
     """
+    keep = store if store is not None else (lambda v: v)
     g = np.asarray(g, dtype=np.float64)
 
     def B(v):
@@ -375,13 +383,13 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
         if den == 0.0 or not np.isfinite(den):
             break
         alpha = rho / den
-        s = r - alpha * Ap
+        s = keep(r - alpha * Ap)
         t = B(s)
         res["products"] += 1
         tt = float(t @ t)
         gamma = float(s @ t) / tt if tt != 0.0 else 0.0
-        x = x + alpha * p + gamma * s
-        r = s - gamma * t
+        x = keep(x + alpha * p + gamma * s)
+        r = keep(s - gamma * t)
         rr = float(r @ r)
         res.update(step=x, iters=j + 1, rr_final=rr)
         dHd = float(x @ apply_A(x))
@@ -397,14 +405,14 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
         if rho_new == 0.0 or gamma == 0.0:
             break
         beta = (rho_new / rho) * (alpha / gamma)
-        p = r + beta * (p - gamma * Ap)
+        p = keep(r + beta * (p - gamma * Ap))
         rho = rho_new
     return res
 
 
 def bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-                     rel_tol=0.0, record=False):
+                     rel_tol=0.0, record=False, store=None):
     """Bi-CG-STAB with the network's curvature operator on (Xc, yc)."""
     def apply_A(p):
         return curvature(dims, act, theta, Xc, yc, p, mode)
-    return bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol, record)
+    return bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol, record, store)

@@ -55,6 +55,18 @@ __device__ __forceinline__ double total(const double* part, int nb, double* sh) 
 
 __device__ __forceinline__ bool is_fin(double x) { return isfinite(x); }
 
+// Vector updates apply their (fp64) scalars in fp64 and round once on the
+// store: near a breakdown of the Bi-CG-STAB recurrences, casting the scalars
+// to fp32 and updating in fp32 amplified rounding by orders of magnitude.
+struct d4 { double v[4]; };
+__device__ __forceinline__ d4 up(f32x4 a) {
+  d4 r; r.v[0] = a[0]; r.v[1] = a[1]; r.v[2] = a[2]; r.v[3] = a[3]; return r;
+}
+__device__ __forceinline__ f32x4 down(const d4& a) {
+  f32x4 r = {(float)a.v[0], (float)a.v[1], (float)a.v[2], (float)a.v[3]};
+  return r;
+}
+
 __device__ __forceinline__ double dot4(f32x4 a, f32x4 b) {
   return ((double)a[0] * b[0] + (double)a[1] * b[1]) +
          ((double)a[2] * b[2] + (double)a[3] * b[3]);
@@ -178,27 +190,30 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
     }
   }
   if (stop) return;
-  const float alpha = (float)(rr / kappa);
-  const float lamf = (float)lam;
+  const double alpha = rr / kappa;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
   double s = 0.0;
   for (long long i = t0; i < n4; i += stride) {
-    const f32x4 pv = ((const f32x4*)p)[i];
-    const f32x4 qv = ((const f32x4*)q)[i];
-    f32x4 xv = ((f32x4*)x)[i];
-    f32x4 rv = ((f32x4*)r)[i];
-    xv += alpha * pv;
-    rv += alpha * (qv + lamf * pv);
-    ((f32x4*)x)[i] = xv;
-    ((f32x4*)r)[i] = rv;
-    s += dot4(rv, rv);
+    const d4 pv = up(((const f32x4*)p)[i]);
+    const d4 qv = up(((const f32x4*)q)[i]);
+    d4 xv = up(((f32x4*)x)[i]);
+    d4 rv = up(((f32x4*)r)[i]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      xv.v[k] += alpha * pv.v[k];
+      rv.v[k] += alpha * (qv.v[k] + lam * pv.v[k]);
+    }
+    const f32x4 r4 = down(rv);
+    ((f32x4*)x)[i] = down(xv);
+    ((f32x4*)r)[i] = r4;
+    s += dot4(r4, r4);
   }
   for (long long e = n4 * 4 + t0; e < n; e += stride) {
-    const float pv = p[e];
-    x[e] += alpha * pv;
-    const float rv = r[e] + alpha * (q[e] + lamf * pv);
+    const double pv = p[e];
+    x[e] = (float)((double)x[e] + alpha * pv);
+    const float rv = (float)((double)r[e] + alpha * ((double)q[e] + lam * pv));
     r[e] = rv;
     s += (double)rv * rv;
   }
@@ -266,20 +281,18 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_dir(
       st->done = 1;
     }
   }
-  const float b = (float)beta;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  long long i = t0;
-  for (; i + stride < n4; i += 2 * stride) {
-    const f32x4 p0 = ((const f32x4*)p)[i], p1 = ((const f32x4*)p)[i + stride];
-    const f32x4 r0 = ((const f32x4*)r)[i], r1 = ((const f32x4*)r)[i + stride];
-    ((f32x4*)p)[i] = b * p0 - r0;
-    ((f32x4*)p)[i + stride] = b * p1 - r1;
+  for (long long i = t0; i < n4; i += stride) {
+    d4 pv = up(((const f32x4*)p)[i]);
+    const d4 rv = up(((const f32x4*)r)[i]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pv.v[k] = beta * pv.v[k] - rv.v[k];
+    ((f32x4*)p)[i] = down(pv);
   }
-  for (; i < n4; i += stride)
-    ((f32x4*)p)[i] = b * ((const f32x4*)p)[i] - ((const f32x4*)r)[i];
-  for (long long e = n4 * 4 + t0; e < n; e += stride) p[e] = b * p[e] - r[e];
+  for (long long e = n4 * 4 + t0; e < n; e += stride)
+    p[e] = (float)(beta * (double)p[e] - (double)r[e]);
 }
 
 // ------------------------------------------------------------- launchers
@@ -443,13 +456,18 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_s(
     }
   }
   if (stop) return;
-  const float a = (float)alpha;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  for (long long i = t0; i < n4; i += stride)
-    ((f32x4*)s)[i] = ((const f32x4*)r)[i] - a * ((const f32x4*)Ap)[i];
-  for (long long e = n4 * 4 + t0; e < n; e += stride) s[e] = r[e] - a * Ap[e];
+  for (long long i = t0; i < n4; i += stride) {
+    d4 rv = up(((const f32x4*)r)[i]);
+    const d4 av = up(((const f32x4*)Ap)[i]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) rv.v[k] -= alpha * av.v[k];
+    ((f32x4*)s)[i] = down(rv);
+  }
+  for (long long e = n4 * 4 + t0; e < n; e += stride)
+    s[e] = (float)((double)r[e] - alpha * (double)Ap[e]);
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_dot2(
@@ -493,46 +511,51 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_update(
     st->products = 2 * j + 2;
     st->iters = j + 1;
   }
-  const float a = (float)st->alpha, c = (float)gamma;
+  const double a = st->alpha, c = gamma;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0, d4 = 0.0;
+  double e0 = 0.0, e1 = 0.0, e2 = 0.0, e3 = 0.0, e4 = 0.0;
   for (long long i = t0; i < n4; i += stride) {
-    const f32x4 sv = ((const f32x4*)s)[i], tv = ((const f32x4*)t)[i];
-    f32x4 xv = ((f32x4*)x)[i];
-    xv += a * ((const f32x4*)p)[i] + c * sv;
-    const f32x4 rv = sv - c * tv;
-    ((f32x4*)x)[i] = xv;
-    ((f32x4*)r)[i] = rv;
-    d0 += dot4(rv, ((const f32x4*)rs)[i]);
-    d1 += dot4(rv, rv);
-    d2 += dot4(((const f32x4*)g)[i], xv);
-    d3 += dot4(rv, xv);
-    d4 += dot4(xv, xv);
+    const d4 sv = up(((const f32x4*)s)[i]), tv = up(((const f32x4*)t)[i]);
+    const d4 pv = up(((const f32x4*)p)[i]);
+    d4 xv = up(((f32x4*)x)[i]), rv;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      xv.v[k] += a * pv.v[k] + c * sv.v[k];
+      rv.v[k] = sv.v[k] - c * tv.v[k];
+    }
+    const f32x4 x4 = down(xv), r4 = down(rv);
+    ((f32x4*)x)[i] = x4;
+    ((f32x4*)r)[i] = r4;
+    e0 += dot4(r4, ((const f32x4*)rs)[i]);
+    e1 += dot4(r4, r4);
+    e2 += dot4(((const f32x4*)g)[i], x4);
+    e3 += dot4(r4, x4);
+    e4 += dot4(x4, x4);
   }
   for (long long e = n4 * 4 + t0; e < n; e += stride) {
-    const float xv = x[e] + a * p[e] + c * s[e];
-    const float rv = s[e] - c * t[e];
+    const float xv = (float)((double)x[e] + a * (double)p[e] + c * (double)s[e]);
+    const float rv = (float)((double)s[e] - c * (double)t[e]);
     x[e] = xv;
     r[e] = rv;
-    d0 += (double)rv * rs[e];
-    d1 += (double)rv * rv;
-    d2 += (double)g[e] * xv;
-    d3 += (double)rv * xv;
-    d4 += (double)xv * xv;
+    e0 += (double)rv * rs[e];
+    e1 += (double)rv * rv;
+    e2 += (double)g[e] * xv;
+    e3 += (double)rv * xv;
+    e4 += (double)xv * xv;
   }
-  d0 = block_sum(d0, sh);
-  d1 = block_sum(d1, sh);
-  d2 = block_sum(d2, sh);
-  d3 = block_sum(d3, sh);
-  d4 = block_sum(d4, sh);
+  const double d0 = block_sum(e0, sh);
+  const double d1 = block_sum(e1, sh);
+  const double d2 = block_sum(e2, sh);
+  const double d3 = block_sum(e3, sh);
+  const double d4s = block_sum(e4, sh);
   if (threadIdx.x == 0) {
     part[PC + blockIdx.x] = d0;
     part[PC + MAX_GRID + blockIdx.x] = d1;
     part[PC + 2 * MAX_GRID + blockIdx.x] = d2;
     part[PC + 3 * MAX_GRID + blockIdx.x] = d3;
-    part[PC + 4 * MAX_GRID + blockIdx.x] = d4;
+    part[PC + 4 * MAX_GRID + blockIdx.x] = d4s;
   }
 }
 
@@ -572,15 +595,18 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_dir(
     if (stop) st->done = 1;
   }
   if (stop) return;
-  const float b = (float)beta, c = (float)gamma;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  for (long long i = t0; i < n4; i += stride)
-    ((f32x4*)p)[i] = ((const f32x4*)r)[i] +
-                     b * (((const f32x4*)p)[i] - c * ((const f32x4*)Ap)[i]);
+  for (long long i = t0; i < n4; i += stride) {
+    d4 pv = up(((const f32x4*)p)[i]);
+    const d4 rv = up(((const f32x4*)r)[i]), av = up(((const f32x4*)Ap)[i]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pv.v[k] = rv.v[k] + beta * (pv.v[k] - gamma * av.v[k]);
+    ((f32x4*)p)[i] = down(pv);
+  }
   for (long long e = n4 * 4 + t0; e < n; e += stride)
-    p[e] = r[e] + b * (p[e] - c * Ap[e]);
+    p[e] = (float)((double)r[e] + beta * ((double)p[e] - gamma * (double)Ap[e]));
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_negw(
@@ -597,22 +623,28 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_negw(
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_axpy(
-    float* __restrict__ y, const float* __restrict__ x, float a, long long n,
+    float* __restrict__ y, const float* __restrict__ x, double a, long long n,
     const int* __restrict__ skip) {
   if (skip && *skip) return;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  for (long long i = t0; i < n4; i += stride)
-    ((f32x4*)y)[i] += a * ((const f32x4*)x)[i];
-  for (long long e = n4 * 4 + t0; e < n; e += stride) y[e] += a * x[e];
+  for (long long i = t0; i < n4; i += stride) {
+    d4 yv = up(((const f32x4*)y)[i]);
+    const d4 xv = up(((const f32x4*)x)[i]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) yv.v[k] += a * xv.v[k];
+    ((f32x4*)y)[i] = down(yv);
+  }
+  for (long long e = n4 * 4 + t0; e < n; e += stride)
+    y[e] = (float)((double)y[e] + a * (double)x[e]);
 }
 
 void axpy(const Launch& L, float* y, const float* x, float a, long long n,
           const int* skip) {
   prof_begin(L, "hf_axpy");
-  hipLaunchKernelGGL(hf_axpy, dim3(cg_grid(n)), dim3(NT), 0, L.stream, y, x, a,
-                     n, skip);
+  hipLaunchKernelGGL(hf_axpy, dim3(cg_grid(n)), dim3(NT), 0, L.stream, y, x,
+                     (double)a, n, skip);
   prof_end(L, "hf_axpy", 0.0, 3.0 * 4.0 * n);
 }
 
