@@ -51,6 +51,30 @@ def parse():
     return ap.parse_args()
 
 
+def counter_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None when the summary does not cover
+    the kernel or the GEMM source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "speech_b16384_hbm_counters.md")
+    src = os.path.join(ROOT, "paper_1606_00511_amd", "csrc", "gemm.hip")
+    try:
+        lines = open(path).read().split("\n")
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    vals = {}
+    for l in lines:
+        t = l.split()
+        if len(t) == 3 and t[0] == "traffic_bytes_per_launch":
+            vals[t[1]] = float(t[2])
+        if len(t) == 2 and t[0] == "gemm_source_sha256":
+            vals["sha"] = t[1]
+    if vals.get("sha") != sha:
+        return None
+    return vals.get(kernel)
+
+
 def cpu_baseline(w, inp, rows):
     """The fp64 oracle timed on this host's cores on a bounded sample: one
     H v and one G v on the first `rows` rows, scaled to the full batch."""
@@ -152,6 +176,16 @@ def main():
     elapsed = t1 - t0
     K = args.steps
 
+    # Bi-CG-STAB (Alg. 3) on the same curvature batch, timed on its own after
+    # the steps: 10 iterations on the Hessian, two products per iteration
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    _, _, ib = net.hf_bicgstab(W, Xc, yc, grad, lam, 10, "hessian",
+                               step=step_h, neg_dir=nd_h)
+    e1.record()
+    torch.cuda.synchronize()
+    bicg_ms = e0.elapsed_time(e1)
+
     gemms = {k: s for k, s in stats.items() if k.startswith("hf_gemm")}
     dom = max(gemms, key=lambda k: gemms[k]["ms"])
     ds = gemms[dom]
@@ -185,7 +219,8 @@ def main():
         "roofline": {
             "bound": "mfma", "kernel": dom,
             "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
+            "frac": achieved / PEAK_FP32_TFLOPS, "traffic": counter_traffic(dom),
+            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "launches": ds["launches"], "avg_launch_ms": ds["ms"] / ds["launches"],
             "flops_per_launch": ds["flops"] / ds["launches"],
         },
@@ -200,6 +235,9 @@ def main():
                   "ms_per_iter": comp["cg_gn"] / K / max(ig["products"], 1)},
         "cg_hess": {"iters": ih["iters"], "products": ih["products"],
                     "neg_curv": ih["neg_curv"], "neg_iter": ih["neg_iter"]},
+        "bicgstab_hessian": {"iters": ib["iters"], "products": ib["products"],
+                             "neg_iter": ib["neg_iter"], "ms": bicg_ms,
+                             "ms_per_product": bicg_ms / max(ib["products"], 1)},
         "hv_per_s_stateless": 1e3 * K / comp["hv"],
         "gv_per_s_stateless": 1e3 * K / comp["gv"],
         "loss": float(loss.item()),
