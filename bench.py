@@ -12,7 +12,10 @@ over 1,973 classes, fp32):
 with lambda = 1e-2 and all inputs resident in HBM before timing starts.
 
 value = curvature-vector products per second over the timed steps (the
-stateless H v and G v plus every product inside both CG solves).
+stateless H v and G v plus every product inside both CG solves), with fp32
+GEMMs.  The same step is then timed with bf16 GEMM operands and fp32
+accumulation (reported under "bf16_inputs"), and 10 Bi-CG-STAB iterations
+(Alg. 3) are timed after each leg.
 
 Prints one JSON line (rank 0; there is only one GPU).
 """
@@ -31,6 +34,7 @@ sys.path.insert(0, ROOT)
 METRIC = ("curvature-vector products/sec (Hv & Gv) at batch B; "
           "CG iteration ms; % MFMA peak")
 PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 matrix peak
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 DEFAULT_WORKLOAD = "speech_440_2048x4_1973_sigmoid_b16384"
 
@@ -42,6 +46,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bf16", action="store_true",
+                    help="skip the bf16-operand leg")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows of the curvature batch the oracle sample uses "
                          "(0 = all of them)")
@@ -103,23 +109,17 @@ def cpu_baseline(w, inp, rows):
                       % (what, t2 - t0)}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU "
-              "path (asked for --gpus %d)" % args.gpus, file=sys.stderr)
-        sys.exit(2)
+def run_leg(args, w, inp, prec):
+    """Warm up, then time args.steps steps of the hot path with the library's
+    kernel profiler on; returns the measurements of this precision."""
     import torch
-    from paper_1606_00511_amd import workloads as WL
     from paper_1606_00511_amd.hf import HFNet
 
-    w = WL.WORKLOADS[args.workload]
-    inp = WL.make(w)
     dev = torch.device("cuda:0")
     d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     W, X, y, v = d(inp["theta"]), d(inp["X"]), d(inp["y"]), d(inp["v"])
     Xc, yc = X[:w.curv_batch].contiguous(), y[:w.curv_batch].contiguous()
-    net = HFNet(w.dims, w.act, max(w.batch, w.curv_batch))
+    net = HFNet(w.dims, w.act, max(w.batch, w.curv_batch), prec=prec)
     loss = torch.empty(1, dtype=torch.float32, device=dev)
     grad = torch.empty(net.n, dtype=torch.float32, device=dev)
     hv = torch.empty_like(grad)
@@ -147,13 +147,6 @@ def main():
         ev[5].record()
         return ig, ih
 
-    if args.copy_probe_mib > 0:
-        nel = args.copy_probe_mib * (1 << 20) // 4
-        src = torch.ones(nel, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -173,8 +166,6 @@ def main():
     t1 = time.perf_counter()
     stats = net.prof_stats()
     net.prof_enable(False)
-    elapsed = t1 - t0
-    K = args.steps
 
     # Bi-CG-STAB (Alg. 3) on the same curvature batch, timed on its own after
     # the steps: 10 iterations on the Hessian, two products per iteration
@@ -184,27 +175,85 @@ def main():
                                step=step_h, neg_dir=nd_h)
     e1.record()
     torch.cuda.synchronize()
-    bicg_ms = e0.elapsed_time(e1)
+    res = dict(stats=stats, comp=comp, products=products, elapsed=t1 - t0,
+               ig=ig, ih=ih, ib=ib, bicg_ms=e0.elapsed_time(e1),
+               loss=float(loss.item()))
+    net.close()
+    del net, W, X, y, v, Xc, yc, loss, grad, hv, gv, step_g, nd_g, step_h, nd_h
+    torch.cuda.empty_cache()
+    return res
 
-    gemms = {k: s for k, s in stats.items() if k.startswith("hf_gemm")}
+
+def summary(res, K, peak):
+    """Roofline figures of one leg: the dominant GEMM kernel by time, all
+    GEMMs together, and the CG vector kernels."""
+    stats = res["stats"]
+    gemms = {k: s for k, s in stats.items() if k.startswith(("hf_gemm", "hf_hgemm"))}
     dom = max(gemms, key=lambda k: gemms[k]["ms"])
     ds = gemms[dom]
     achieved = ds["flops"] / (ds["ms"] * 1e-3) / 1e12
     gemm_ms = sum(s["ms"] for s in gemms.values())
     gemm_fl = sum(s["flops"] for s in gemms.values())
     vec = {k: s for k, s in stats.items() if k in (
-        "hf_cg_curv_dot", "hf_cg_update", "hf_cg_dir")}
+        "hf_cg_dot", "hf_cg_update", "hf_cg_dir")}
     vec_ms = sum(s["ms"] for s in vec.values())
     vec_b = sum(s["bytes"] for s in vec.values())
+    comp, ig, ih, ib = res["comp"], res["ig"], res["ih"], res["ib"]
+    return dict(
+        dom=dom, ds=ds, achieved=achieved,
+        gemm_all={"tflops": gemm_fl / (gemm_ms * 1e-3) / 1e12,
+                  "frac": gemm_fl / (gemm_ms * 1e-3) / 1e12 / peak,
+                  "ms_per_step": gemm_ms / K},
+        cg_vector={"GB/s": vec_b / (vec_ms * 1e-3) / 1e9 if vec_ms else None,
+                   "frac_hbm": (vec_b / (vec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS)
+                   if vec_ms else None, "ms_per_step": vec_ms / K},
+        components_ms={k: comp[k] / K for k in comp},
+        cg_gn={"iters": ig["iters"], "products": ig["products"],
+               "ms_per_iter": comp["cg_gn"] / K / max(ig["products"], 1)},
+        cg_hess={"iters": ih["iters"], "products": ih["products"],
+                 "neg_curv": ih["neg_curv"], "neg_iter": ih["neg_iter"]},
+        bicgstab_hessian={"iters": ib["iters"], "products": ib["products"],
+                          "neg_iter": ib["neg_iter"], "ms": res["bicg_ms"],
+                          "ms_per_product": res["bicg_ms"] / max(ib["products"], 1)},
+        hv_per_s_stateless=1e3 * K / comp["hv"],
+        gv_per_s_stateless=1e3 * K / comp["gv"],
+        kernels={k: {"launches": s["launches"], "ms_per_step": s["ms"] / K,
+                     "avg_us": 1e3 * s["ms"] / max(s["launches"], 1),
+                     "tflops": s["flops"] / max(s["ms"], 1e-9) / 1e9,
+                     "gbs": s["bytes"] / max(s["ms"], 1e-9) / 1e6}
+                 for k, s in sorted(stats.items(), key=lambda kv: -kv[1]["ms"])})
 
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU "
+              "path (asked for --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_1606_00511_amd import workloads as WL
+
+    w = WL.WORKLOADS[args.workload]
+    inp = WL.make(w)
+    if args.copy_probe_mib > 0:
+        nel = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(nel, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    K = args.steps
+    r32 = run_leg(args, w, inp, "fp32")
+    s32 = summary(r32, K, PEAK_FP32_TFLOPS)
+    ds = s32["ds"]
     out = {
         "metric": METRIC,
-        "value": products / elapsed,
+        "value": r32["products"] / r32["elapsed"],
         "unit": "curvature-vector products/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
-        "ms_per_step": 1e3 * elapsed / K,
+        "ms_per_step": 1e3 * r32["elapsed"] / K,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -213,40 +262,45 @@ def main():
         "config": {
             "workload": w.name, "dims": list(w.dims), "act": w.act,
             "batch": w.batch, "curv_batch": w.curv_batch,
-            "cg_iters": w.cg_iters, "damping": lam,
+            "cg_iters": w.cg_iters, "damping": w.damping,
             "parallelism": "single GPU (one worker's share)",
         },
         "roofline": {
-            "bound": "mfma", "kernel": dom,
-            "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_FP32_TFLOPS, "traffic": counter_traffic(dom),
+            "bound": "mfma", "kernel": s32["dom"],
+            "achieved": s32["achieved"], "peak": PEAK_FP32_TFLOPS,
+            "unit": "TFLOP/s", "frac": s32["achieved"] / PEAK_FP32_TFLOPS,
+            "traffic": counter_traffic(s32["dom"]),
             "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "launches": ds["launches"], "avg_launch_ms": ds["ms"] / ds["launches"],
             "flops_per_launch": ds["flops"] / ds["launches"],
         },
-        "gemm_all": {"tflops": gemm_fl / (gemm_ms * 1e-3) / 1e12,
-                     "frac": gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_FP32_TFLOPS,
-                     "ms_per_step": gemm_ms / K},
-        "cg_vector": {"GB/s": vec_b / (vec_ms * 1e-3) / 1e9 if vec_ms else None,
-                      "frac_hbm": (vec_b / (vec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS)
-                      if vec_ms else None, "ms_per_step": vec_ms / K},
-        "components_ms": {k: comp[k] / K for k in names},
-        "cg_gn": {"iters": ig["iters"], "products": ig["products"],
-                  "ms_per_iter": comp["cg_gn"] / K / max(ig["products"], 1)},
-        "cg_hess": {"iters": ih["iters"], "products": ih["products"],
-                    "neg_curv": ih["neg_curv"], "neg_iter": ih["neg_iter"]},
-        "bicgstab_hessian": {"iters": ib["iters"], "products": ib["products"],
-                             "neg_iter": ib["neg_iter"], "ms": bicg_ms,
-                             "ms_per_product": bicg_ms / max(ib["products"], 1)},
-        "hv_per_s_stateless": 1e3 * K / comp["hv"],
-        "gv_per_s_stateless": 1e3 * K / comp["gv"],
-        "loss": float(loss.item()),
-        "kernels": {k: {"launches": s["launches"], "ms_per_step": s["ms"] / K,
-                        "avg_us": 1e3 * s["ms"] / max(s["launches"], 1),
-                        "tflops": s["flops"] / max(s["ms"], 1e-9) / 1e9,
-                        "gbs": s["bytes"] / max(s["ms"], 1e-9) / 1e6}
-                    for k, s in sorted(stats.items(), key=lambda kv: -kv[1]["ms"])},
+        "loss": r32["loss"],
     }
+    for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
+              "bicgstab_hessian", "hv_per_s_stateless", "gv_per_s_stateless",
+              "kernels"):
+        out[k] = s32[k]
+    if not args.no_bf16:
+        # the same step with bf16 GEMM operands (fp32 accumulation)
+        r16 = run_leg(args, w, inp, "bf16")
+        s16 = summary(r16, K, PEAK_BF16_TFLOPS)
+        d16 = s16["ds"]
+        out["bf16_inputs"] = {
+            "value": r16["products"] / r16["elapsed"],
+            "ms_per_step": 1e3 * r16["elapsed"] / K,
+            "dtype": "bf16 operands, f32 accumulate",
+            "roofline": {
+                "bound": "mfma", "kernel": s16["dom"], "achieved": s16["achieved"],
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": s16["achieved"] / PEAK_BF16_TFLOPS,
+                "launches": d16["launches"],
+                "avg_launch_ms": d16["ms"] / d16["launches"],
+                "flops_per_launch": d16["flops"] / d16["launches"]},
+            "loss": r16["loss"],
+        }
+        for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
+                  "bicgstab_hessian", "kernels"):
+            out["bf16_inputs"][k] = s16[k]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_rows)
     print(json.dumps(out), flush=True)

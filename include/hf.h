@@ -47,8 +47,15 @@ typedef struct hf_ctx hf_ctx;
 enum { HF_SIGMOID = 0, HF_TANH = 1, HF_RELU = 2 };
 /* Curvature matrix for hf_hvp / hf_cg. */
 enum { HF_HESSIAN = 0, HF_GAUSS_NEWTON = 1 };
-/* Arithmetic: fp32 storage, fp32 MFMA, fp32 accumulation. */
-enum { HF_FP32 = 0 };
+/* Arithmetic of the GEMMs (every other step is fp32, reductions fp64):
+ *   HF_FP32         fp32 operands, fp32 MFMA, fp32 accumulation;
+ *   HF_BF16_INPUTS  every GEMM operand (X, W, v, the activations and deltas
+ *                   of the forward, backward, R-forward and R-backward
+ *                   passes) rounded to bf16 (nearest even), bf16 MFMA with
+ *                   fp32 accumulation; biases, epilogues (phi, phi', phi''),
+ *                   the softmax and R-softmax rows, the phi'' cache, the
+ *                   weight-gradient sums and all CG arithmetic stay fp32. */
+enum { HF_FP32 = 0, HF_BF16_INPUTS = 1 };
 
 enum {
   HF_OK = 0,
@@ -69,7 +76,7 @@ enum {
  *   dims      host array of n_dims = L + 1 >= 2 positive sizes; d_L is the
  *             number of classes (<= HF_MAX_CLASSES); L <= HF_MAX_LAYERS.
  *   act       HF_SIGMOID | HF_TANH | HF_RELU for hidden layers.
- *   prec      HF_FP32.
+ *   prec      HF_FP32 or HF_BF16_INPUTS.
  *   max_batch largest B any later call may use (>= 1); every B x d_l
  *             buffer and n must stay below 2^31 elements.
  *   out       receives the context.  Returns HF_EINVAL on bad arguments.

@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhf.so")
-SOURCES = ["hf_api.cpp", "gemm.hip", "rowops.hip", "cgvec.hip"]
+SOURCES = ["hf_api.cpp", "gemm.hip", "gemm_bf16.hip", "rowops.hip", "cgvec.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

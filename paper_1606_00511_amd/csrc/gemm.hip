@@ -24,6 +24,7 @@
 // the pairing that measured fastest on MI355X.
 // Within a K block each half-wave works on its own 8 consecutive k values,
 // which permutes the order of the K sum identically for both operands.
+#include "act.h"
 #include "hf_internal.h"
 
 namespace hfk {
@@ -37,26 +38,6 @@ __device__ __forceinline__ int swz(int row) { return (row >> 2) & 3; }
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ float act_f(int act, float z) {
-  if (act == ACT_SIGMOID) return 1.0f / (1.0f + expf(-z));
-  if (act == ACT_TANH) return tanhf(z);
-  return fmaxf(z, 0.0f);
-}
-// phi'(z) written in terms of a = phi(z); selects rather than branches keep
-// the epilogue loops straight-line so the accumulators stay in registers
-__device__ __forceinline__ float act_d1(int act, float a) {
-  const float sg = a * (1.0f - a);
-  const float th = 1.0f - a * a;
-  const float rl = a > 0.0f ? 1.0f : 0.0f;
-  return act == ACT_SIGMOID ? sg : (act == ACT_TANH ? th : rl);
-}
-// phi''(z) written in terms of a = phi(z)
-__device__ __forceinline__ float act_d2(int act, float a) {
-  const float sg = a * (1.0f - a) * (1.0f - 2.0f * a);
-  const float th = -2.0f * a * (1.0f - a * a);
-  return act == ACT_SIGMOID ? sg : (act == ACT_TANH ? th : 0.0f);
-}
 
 // ------------------------------------------------------------ tile loading
 // A ROWS x BK operand tile.  MK: the operand is stored rows x K with K

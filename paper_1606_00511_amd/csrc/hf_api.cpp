@@ -184,6 +184,12 @@ struct hf_ctx {
 
   // workspace carve-up (byte offsets), 1-based per layer where it applies
   std::vector<size_t> oA, oD, oE2, oRZ, oRA, oRD, oWT, oVT;
+  // HF_BF16_INPUTS: bf16 GEMM operands.  Row-major copies have leading
+  // dimension ldh_l; the transposed (batch-contiguous) ones *T have ldB.
+  std::vector<int> ldh;
+  int ldB = 0;
+  size_t hX = 0, hXT = 0;
+  std::vector<size_t> hW, hWT, hV, hVT, hA, hAT, hRA, hRAT, hD, hDT, hRD, hRDT;
   size_t oS = 0, oT = 0, oRs = 0;    // Bi-CG-STAB: s, t = B s, r0*
   size_t oZ = 0, oP = 0, oSplit = 0, oBpart = 0, oR = 0, oPv = 0, oQ = 0,
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
@@ -201,6 +207,8 @@ struct hf_ctx {
 
   float* F(size_t off) const { return reinterpret_cast<float*>(ws + off); }
   double* Dp(size_t off) const { return reinterpret_cast<double*>(ws + off); }
+  bf16_t* H(size_t off) const { return reinterpret_cast<bf16_t*>(ws + off); }
+  bool bf16() const { return prec == HF_BF16_INPUTS; }
   Launch launch() const { return Launch{stream, prof}; }
 };
 
@@ -229,9 +237,11 @@ int fail(hf_ctx* c, int code, const char* fmt, ...) {
 inline size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 inline bool a16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 inline int round4(int x) { return (x + 3) & ~3; }
+inline int round8(int x) { return (x + 7) & ~7; }
 
 void plan(hf_ctx* c) {
   const int L = c->L;
+  const bool h = c->bf16();
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -239,32 +249,61 @@ void plan(hf_ctx* c) {
     return o;
   };
   const size_t B = (size_t)c->Bmax;
-  c->oA.assign(L + 1, 0);
-  c->oD.assign(L + 1, 0);
-  c->oE2.assign(L + 1, 0);
-  c->oRZ.assign(L + 1, 0);
-  c->oRA.assign(L + 1, 0);
-  c->oRD.assign(L + 1, 0);
-  c->oWT.assign(L + 1, 0);
-  c->oVT.assign(L + 1, 0);
+  for (auto* v : {&c->oA, &c->oD, &c->oE2, &c->oRZ, &c->oRA, &c->oRD, &c->oWT,
+                  &c->oVT, &c->hW, &c->hWT, &c->hV, &c->hVT, &c->hA, &c->hAT,
+                  &c->hRA, &c->hRAT, &c->hD, &c->hDT, &c->hRD, &c->hRDT})
+    v->assign(L + 1, 0);
+  const size_t f4 = sizeof(float), h2 = sizeof(bf16_t);
+  const size_t LB = (size_t)c->ldB;
   for (int l = 1; l <= L; ++l) {
-    // W_l and V_l transposed: d_{l-1} rows of ld_l floats
-    c->oWT[l] = take((size_t)c->d[l - 1] * c->ld[l] * sizeof(float));
-    c->oVT[l] = take((size_t)c->d[l - 1] * c->ld[l] * sizeof(float));
-  }
-  for (int l = 1; l <= L; ++l) {
-    const size_t sz = B * c->ld[l] * sizeof(float);
-    if (l < L) {
-      c->oA[l] = take(sz);
-      c->oE2[l] = take(sz);
-      c->oRA[l] = take(sz);
+    if (!h) {
+      // W_l and V_l transposed: d_{l-1} rows of ld_l floats
+      c->oWT[l] = take((size_t)c->d[l - 1] * c->ld[l] * f4);
+      c->oVT[l] = take((size_t)c->d[l - 1] * c->ld[l] * f4);
+    } else {
+      // bf16 W_l, V_l (row-major, forward) and transposed (backward)
+      c->hW[l] = take((size_t)c->d[l] * c->ldh[l - 1] * h2);
+      c->hWT[l] = take((size_t)c->d[l - 1] * c->ldh[l] * h2);
+      c->hV[l] = take((size_t)c->d[l] * c->ldh[l - 1] * h2);
+      c->hVT[l] = take((size_t)c->d[l - 1] * c->ldh[l] * h2);
     }
-    c->oD[l] = take(sz);
-    c->oRZ[l] = take(sz);
-    c->oRD[l] = take(sz);
   }
-  c->oZ = take(B * c->ld[L] * sizeof(float));
-  c->oP = take(B * c->ld[L] * sizeof(float));
+  if (h) {
+    c->hX = take(B * c->ldh[0] * h2);
+    c->hXT = take((size_t)c->d[0] * LB * h2);
+  }
+  for (int l = 1; l <= L; ++l) {
+    const size_t sz = B * c->ld[l] * f4;
+    if (!h) {
+      if (l < L) {
+        c->oA[l] = take(sz);
+        c->oE2[l] = take(sz);
+        c->oRA[l] = take(sz);
+      }
+      c->oD[l] = take(sz);
+      c->oRZ[l] = take(sz);
+      c->oRD[l] = take(sz);
+    } else {
+      const size_t szh = B * c->ldh[l] * h2, szt = (size_t)c->d[l] * LB * h2;
+      if (l < L) {
+        c->oE2[l] = take(sz);
+        c->hA[l] = take(szh);
+        c->hAT[l] = take(szt);
+        c->hRA[l] = take(szh);
+        c->hRAT[l] = take(szt);
+      } else {
+        c->oD[l] = take(sz);     // fp32 softmax outputs, converted to bf16
+        c->oRD[l] = take(sz);
+      }
+      c->oRZ[l] = take(sz);
+      c->hD[l] = take(szh);
+      c->hDT[l] = take(szt);
+      c->hRD[l] = take(szh);
+      c->hRDT[l] = take(szt);
+    }
+  }
+  c->oZ = take(B * c->ld[L] * f4);
+  c->oP = take(B * c->ld[L] * f4);
   size_t mn = 0;
   int dmax = 0;
   for (int l = 1; l <= L; ++l) {
@@ -272,15 +311,15 @@ void plan(hf_ctx* c) {
     dmax = std::max(dmax, c->d[l]);
   }
   c->split_elems = mn;
-  c->oSplit = take((size_t)c->max_splits * mn * sizeof(float));
+  c->oSplit = take((size_t)c->max_splits * mn * f4);
   c->oBpart = take((size_t)c->max_splits * dmax * sizeof(double));
   const size_t nv = ((size_t)c->n + 63) & ~size_t(63);
-  c->oR = take(nv * sizeof(float));
-  c->oPv = take(nv * sizeof(float));
-  c->oQ = take(nv * sizeof(float));
-  c->oS = take(nv * sizeof(float));
-  c->oT = take(nv * sizeof(float));
-  c->oRs = take(nv * sizeof(float));
+  c->oR = take(nv * f4);
+  c->oPv = take(nv * f4);
+  c->oQ = take(nv * f4);
+  c->oS = take(nv * f4);
+  c->oT = take(nv * f4);
+  c->oRs = take(nv * f4);
   c->oRed = take((size_t)cg_part_doubles() * sizeof(double));
   c->oLoss = take(((B + 3) / 4) * sizeof(double));
   c->oState = take(sizeof(CgState) > sizeof(BicgState) ? sizeof(CgState)
@@ -476,6 +515,279 @@ void product_cached(hf_ctx* c, const float* W, const float* X, int B,
   }
 }
 
+// ------------------------------------------------- bf16-input passes
+// The same pass order as above with every GEMM operand a bf16 copy.  The
+// producing epilogues write each bf16 activation or delta twice: row-major
+// (the next forward or backward GEMM's operand) and transposed (the weight
+// gradient's batch-contiguous operand).  Softmax, RZ, the phi'' cache and
+// all reductions stay fp32.
+
+EpiH epih(const hf_ctx* c, int hidden) {
+  EpiH e;
+  std::memset(&e, 0, sizeof e);
+  e.act = c->act;
+  e.hidden = hidden;
+  e.ldt = c->ldB;
+  return e;
+}
+
+GemmShapeH shapeh(int M, int N, int K, const bf16_t* x0, const bf16_t* x1,
+                  const bf16_t* y0, const bf16_t* y1, int ldx, int ldy,
+                  int nseg, const int* skip) {
+  GemmShapeH s;
+  s.M = M; s.N = N; s.K = K;
+  s.X[0] = x0; s.X[1] = x1;
+  s.Y[0] = y0; s.Y[1] = y1;
+  s.ldx = ldx; s.ldy = ldy;
+  s.nseg = nseg;
+  s.splits = 1;
+  s.skip = skip;
+  return s;
+}
+
+// bf16 copies of the weight blocks of a parameter-layout vector: W_l
+// row-major [d_l][ldh_{l-1}] and transposed [d_{l-1}][ldh_l]
+void weights_h(hf_ctx* c, const float* v, const std::vector<size_t>& row,
+               const std::vector<size_t>& tr, const int* skip) {
+  for (int l = 1; l <= c->L; ++l)
+    cvt_bf16(c->launch(), v + c->offW[l], c->d[l], c->d[l - 1], c->d[l - 1],
+             c->H(row[l]), c->ldh[l - 1], c->H(tr[l]), c->ldh[l], skip);
+}
+
+// bf16 copies of the input rows: X [B][ldh_0] and X^T [d_0][ldB]
+void input_h(hf_ctx* c, const float* X, int B) {
+  cvt_bf16(c->launch(), X, B, c->d[0], c->d[0], c->H(c->hX), c->ldh[0],
+           c->H(c->hXT), c->ldB, nullptr);
+}
+
+// an fp32 output-layer delta (B x d_L, ld_L) to its two bf16 copies
+void delta_h(hf_ctx* c, const float* D, int B, size_t row, size_t tr,
+             const int* skip) {
+  const int L = c->L;
+  cvt_bf16(c->launch(), D, B, c->d[L], c->ld[L], c->H(row), c->ldh[L],
+           c->H(tr), c->ldB, skip);
+}
+
+const bf16_t* act_h(const hf_ctx* c, int l) {       // A_l, row-major
+  return c->H(l == 0 ? c->hX : c->hA[l]);
+}
+const bf16_t* act_ht(const hf_ctx* c, int l) {      // A_l, transposed
+  return c->H(l == 0 ? c->hXT : c->hAT[l]);
+}
+
+void wgrad_h(hf_ctx* c, int l, int B, const bf16_t* x0, const bf16_t* y0,
+             const bf16_t* x1, const bf16_t* y1, float* out, const int* skip) {
+  const Launch Lc = c->launch();
+  const int M = c->d[l], N = c->d[l - 1];
+  const int nseg = x1 ? 2 : 1;
+  GemmShapeH s = shapeh(M, N, B, x0, x1, y0, y1, c->ldB, c->ldB, nseg, skip);
+  s.splits = choose_splits(c, M, N, B * nseg);
+  EpiH e = epih(c, 0);
+  e.ldf = N;
+  if (s.splits > 1) {
+    e.f0 = c->F(c->oSplit);
+    e.split_stride = (long long)M * N;
+    e.bias_part = c->Dp(c->oBpart);
+    hgemm_wgrad(Lc, s, e);
+    splitk_reduce(Lc, c->F(c->oSplit), c->Dp(c->oBpart), s.splits, M, N,
+                  out + c->offW[l], N, out + c->offB[l], skip);
+  } else {
+    e.f0 = out + c->offW[l];
+    e.bias_out = out + c->offB[l];
+    hgemm_wgrad(Lc, s, e);
+  }
+}
+
+void forward_plain_h(hf_ctx* c, const float* W, const float* X, int B,
+                     const int32_t* y, bool want_delta) {
+  const Launch Lc = c->launch();
+  const int L = c->L;
+  input_h(c, X, B);
+  weights_h(c, W, c->hW, c->hWT, nullptr);
+  for (int l = 1; l <= L; ++l) {
+    GemmShapeH s = shapeh(B, c->d[l], c->d[l - 1], act_h(c, l - 1), nullptr,
+                          c->H(c->hW[l]), nullptr, c->ldh[l - 1], c->ldh[l - 1],
+                          1, nullptr);
+    EpiH e = epih(c, l < L);
+    e.bias = W + c->offB[l];
+    if (l < L) {
+      e.h0 = c->H(c->hA[l]);
+      e.t0 = c->H(c->hAT[l]);
+      e.ldo = c->ldh[l];
+    } else {
+      e.f0 = c->F(c->oZ);
+      e.ldf = c->ld[L];
+    }
+    hgemm_fwd(Lc, s, e);
+  }
+  softmax_xent(Lc, c->F(c->oZ), y, B, c->d[L], c->ld[L], c->F(c->oP),
+               want_delta ? c->F(c->oD[L]) : nullptr, c->Dp(c->oLoss),
+               reinterpret_cast<int*>(c->ws + c->oErr));
+  if (want_delta) delta_h(c, c->F(c->oD[L]), B, c->hD[L], c->hDT[L], nullptr);
+}
+
+void backward_data_h(hf_ctx* c, int l, int B, bool cache_e2) {
+  GemmShapeH s = shapeh(B, c->d[l - 1], c->d[l], c->H(c->hD[l]), nullptr,
+                        c->H(c->hWT[l]), nullptr, c->ldh[l], c->ldh[l], 1,
+                        nullptr);
+  EpiH e = epih(c, 1);
+  e.h0 = c->H(c->hD[l - 1]);
+  e.t0 = c->H(c->hDT[l - 1]);
+  e.ldo = c->ldh[l - 1];
+  e.a0 = c->H(c->hA[l - 1]);
+  e.f2 = cache_e2 ? c->F(c->oE2[l - 1]) : nullptr;
+  e.ldf = c->ld[l - 1];
+  hgemm_bwd(c->launch(), s, e);
+}
+
+// weight gradients of a curvature product at layer l (both modes) and, for
+// l > 1, the backward step to Rdelta_{l-1} (and delta_{l-1} when stateless)
+void rbackward_h(hf_ctx* c, int l, int B, int mode, bool stateless,
+                 float* out, const int* skip) {
+  const bool hess = mode == HF_HESSIAN;
+  if (hess && l > 1)
+    wgrad_h(c, l, B, c->H(c->hRDT[l]), act_ht(c, l - 1), c->H(c->hDT[l]),
+            c->H(c->hRAT[l - 1]), out, skip);
+  else
+    wgrad_h(c, l, B, c->H(c->hRDT[l]), act_ht(c, l - 1), nullptr, nullptr,
+            out, skip);
+  if (l == 1) return;
+  EpiH e = epih(c, 1);
+  e.h1 = c->H(c->hRD[l - 1]);
+  e.t1 = c->H(c->hRDT[l - 1]);
+  e.ldo = c->ldh[l - 1];
+  e.a0 = c->H(c->hA[l - 1]);
+  e.ldf = c->ld[l - 1];
+  const int ld = c->ldh[l];
+  if (hess && stateless) {
+    // (E, RE) = (delta W, Rdelta W + delta V) in one pass
+    GemmShapeH s = shapeh(B, c->d[l - 1], c->d[l], c->H(c->hD[l]),
+                          c->H(c->hRD[l]), c->H(c->hWT[l]), c->H(c->hVT[l]),
+                          ld, ld, 1, skip);
+    e.h0 = c->H(c->hD[l - 1]);
+    e.t0 = c->H(c->hDT[l - 1]);
+    e.a1 = c->F(c->oRZ[l - 1]);
+    hgemm_bwd_rbwd(c->launch(), s, e);
+  } else if (hess) {
+    GemmShapeH s = shapeh(B, c->d[l - 1], c->d[l], c->H(c->hRD[l]),
+                          c->H(c->hD[l]), c->H(c->hWT[l]), c->H(c->hVT[l]), ld,
+                          ld, 2, skip);
+    e.a1 = c->F(c->oRZ[l - 1]);
+    e.a2 = c->F(c->oE2[l - 1]);
+    hgemm_rbwd(c->launch(), s, e);
+  } else {
+    GemmShapeH s = shapeh(B, c->d[l - 1], c->d[l], c->H(c->hRD[l]), nullptr,
+                          c->H(c->hWT[l]), nullptr, ld, ld, 1, skip);
+    hgemm_gnbwd(c->launch(), s, e);
+  }
+}
+
+void product_cached_h(hf_ctx* c, int B, const float* v, int mode, float* out,
+                      const int* skip) {
+  const Launch Lc = c->launch();
+  const int L = c->L;
+  weights_h(c, v, c->hV, c->hVT, skip);
+  for (int l = 1; l <= L; ++l) {
+    GemmShapeH s;
+    if (l == 1)
+      s = shapeh(B, c->d[1], c->d[0], c->H(c->hX), nullptr, c->H(c->hV[1]),
+                 nullptr, c->ldh[0], c->ldh[0], 1, skip);
+    else
+      s = shapeh(B, c->d[l], c->d[l - 1], c->H(c->hRA[l - 1]),
+                 c->H(c->hA[l - 1]), c->H(c->hW[l]), c->H(c->hV[l]),
+                 c->ldh[l - 1], c->ldh[l - 1], 2, skip);
+    EpiH e = epih(c, l < L);
+    e.rbias = v + c->offB[l];
+    e.f1 = c->F(c->oRZ[l]);
+    e.ldf = c->ld[l];
+    if (l < L) {
+      e.h2 = c->H(c->hRA[l]);
+      e.t2 = c->H(c->hRAT[l]);
+      e.a0 = c->H(c->hA[l]);
+      e.ldo = c->ldh[l];
+    }
+    hgemm_rfwd(Lc, s, e);
+  }
+  softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), B, c->d[L], c->ld[L],
+              c->F(c->oRD[L]), skip);
+  delta_h(c, c->F(c->oRD[L]), B, c->hRD[L], c->hRDT[L], skip);
+  for (int l = L; l >= 1; --l) rbackward_h(c, l, B, mode, false, out, skip);
+}
+
+// stateless curvature product: forward fused with R-forward, then the
+// R-backward (Hv) or Gauss-Newton backward (Gv)
+void hvp_h(hf_ctx* c, const float* W, const float* X, const int32_t* y, int B,
+           const float* v, int mode, float* out) {
+  const Launch Lc = c->launch();
+  const int L = c->L;
+  const bool hess = mode == HF_HESSIAN;
+  input_h(c, X, B);
+  weights_h(c, W, c->hW, c->hWT, nullptr);
+  weights_h(c, v, c->hV, c->hVT, nullptr);
+  for (int l = 1; l <= L; ++l) {
+    const int ldk = c->ldh[l - 1];
+    GemmShapeH s = shapeh(B, c->d[l], c->d[l - 1], act_h(c, l - 1),
+                          l == 1 ? nullptr : c->H(c->hRA[l - 1]),
+                          c->H(c->hW[l]), c->H(c->hV[l]), ldk, ldk, 1, nullptr);
+    EpiH e = epih(c, l < L);
+    e.bias = W + c->offB[l];
+    e.rbias = v + c->offB[l];
+    e.f1 = c->F(c->oRZ[l]);
+    e.ldf = c->ld[l];
+    if (l < L) {
+      e.h0 = c->H(c->hA[l]);
+      e.t0 = c->H(c->hAT[l]);
+      e.h2 = c->H(c->hRA[l]);
+      e.t2 = c->H(c->hRAT[l]);
+      e.ldo = c->ldh[l];
+    } else {
+      e.f0 = c->F(c->oZ);
+    }
+    hgemm_fwd_rfwd(Lc, s, e);
+  }
+  softmax_xent(Lc, c->F(c->oZ), hess ? y : nullptr, B, c->d[L], c->ld[L],
+               c->F(c->oP), hess ? c->F(c->oD[L]) : nullptr, c->Dp(c->oLoss),
+               reinterpret_cast<int*>(c->ws + c->oErr));
+  if (hess) delta_h(c, c->F(c->oD[L]), B, c->hD[L], c->hDT[L], nullptr);
+  softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), B, c->d[L], c->ld[L],
+              c->F(c->oRD[L]), nullptr);
+  delta_h(c, c->F(c->oRD[L]), B, c->hRD[L], c->hRDT[L], nullptr);
+  for (int l = L; l >= 1; --l) rbackward_h(c, l, B, mode, true, out, nullptr);
+}
+
+void loss_grad_h(hf_ctx* c, const float* W, const float* X, const int32_t* y,
+                 int B, float* loss, float* grad) {
+  forward_plain_h(c, W, X, B, y, true);
+  loss_finalize(c->launch(), c->Dp(c->oLoss), (B + 3) / 4, B, loss);
+  for (int l = c->L; l >= 1; --l) {
+    wgrad_h(c, l, B, c->H(c->hDT[l]), act_ht(c, l - 1), nullptr, nullptr,
+            grad, nullptr);
+    if (l > 1) backward_data_h(c, l, B, false);
+  }
+}
+
+// ------------------------------------------------ precision dispatch
+// The cache of a solve on the curvature batch: forward pass, p and, for the
+// Hessian, delta_l and (delta_l W_l) phi''(A_{l-1}).
+void build_cache(hf_ctx* c, const float* W, const float* X, int B,
+                 const int32_t* y, bool hess) {
+  if (c->bf16()) {
+    forward_plain_h(c, W, X, B, hess ? y : nullptr, hess);
+    if (hess)
+      for (int l = c->L; l >= 2; --l) backward_data_h(c, l, B, true);
+  } else {
+    forward_plain(c, W, X, B, hess ? y : nullptr, hess);
+    if (hess)
+      for (int l = c->L; l >= 2; --l) backward_data(c, W, l, B, true);
+  }
+}
+
+void product(hf_ctx* c, const float* W, const float* X, int B, const float* v,
+             int mode, float* out, const int* skip) {
+  if (c->bf16()) product_cached_h(c, B, v, mode, out, skip);
+  else product_cached(c, W, X, B, v, mode, out, skip);
+}
+
 // q += lambda v: the damping term of B_k = A + lambda I (Alg. 1 step 3)
 void lambda_axpy(hf_ctx* c, float* q, const float* v, float lambda,
                  const int* skip) {
@@ -492,14 +804,17 @@ int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
   if (!out) return HF_EINVAL;
   *out = nullptr;
   if (!dims || n_dims < 2 || n_dims > HF_MAX_LAYERS + 1) return HF_EINVAL;
-  if (!valid_act(act) || prec != HF_FP32 || max_batch < 1) return HF_EINVAL;
+  if (!valid_act(act) || (prec != HF_FP32 && prec != HF_BF16_INPUTS) || max_batch < 1)
+    return HF_EINVAL;
   for (int i = 0; i < n_dims; ++i)
     if (dims[i] < 1) return HF_EINVAL;
   if (dims[n_dims - 1] > HF_MAX_CLASSES) return HF_EINVAL;
   const int64_t lim = (int64_t(1) << 31) - 1;
   int64_t n = 0;
   for (int i = 0; i < n_dims; ++i)
-    if (max_batch * (int64_t)round4(dims[i]) > lim) return HF_EINVAL;
+    if (max_batch * (int64_t)round8(dims[i]) > lim ||
+        ((max_batch + 7) & ~int64_t(7)) * dims[i] > lim)
+      return HF_EINVAL;
   for (int l = 1; l < n_dims; ++l) n += (int64_t)dims[l] * (dims[l - 1] + 1);
   if (n > lim - 64) return HF_EINVAL;
   hf_ctx* c = new (std::nothrow) hf_ctx();
@@ -508,6 +823,9 @@ int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
   c->d.assign(dims, dims + n_dims);
   c->ld.resize(n_dims);
   for (int i = 0; i < n_dims; ++i) c->ld[i] = round4(dims[i]);
+  c->ldh.resize(n_dims);
+  for (int i = 0; i < n_dims; ++i) c->ldh[i] = round8(dims[i]);
+  c->ldB = round8((int)max_batch);
   c->act = act;
   c->prec = prec;
   c->Bmax = max_batch;
@@ -571,6 +889,11 @@ int hf_loss_grad(hf_ctx* c, const float* W, const float* X, const int32_t* y,
   if (!loss) return fail(c, HF_EINVAL, "loss is NULL");
   const Launch Lc = c->launch();
   const int b = (int)B;
+  if (c->bf16()) {
+    loss_grad_h(c, W, X, y, b, loss, grad);
+    HIP_TRY(c, hipGetLastError());
+    return HF_OK;
+  }
   forward_plain(c, W, X, b, y, true);
   loss_finalize(Lc, c->Dp(c->oLoss), (b + 3) / 4, b, loss);
   for (int l = c->L; l >= 1; --l) {
@@ -596,6 +919,11 @@ int hf_hvp(hf_ctx* c, const float* W, const float* X, const int32_t* y,
   if (mode == HF_HESSIAN && !y) return fail(c, HF_EINVAL, "y is NULL");
   const Launch Lc = c->launch();
   const int b = (int)B, L = c->L;
+  if (c->bf16()) {
+    hvp_h(c, W, X, y, b, v, mode, out);
+    HIP_TRY(c, hipGetLastError());
+    return HF_OK;
+  }
   // forward fused with R-forward
   for (int l = 1; l <= L; ++l) {
     GemmShape s;
@@ -695,14 +1023,12 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   float* q = c->F(c->oQ);
 
   // cache of the curvature batch: activations, p, delta_l, E2_l
-  forward_plain(c, W, Xc, b, hess ? yc : nullptr, hess);
-  if (hess)
-    for (int l = c->L; l >= 2; --l) backward_data(c, W, l, b, true);
+  build_cache(c, W, Xc, b, yc, hess);
   cg_init(Lc, g, step, r, p, neg_dir, n, (double)damping,
           (double)rel_tol * (double)rel_tol, part, st);
   for (int j = 0; j < max_iters; ++j) {
     if (c->prof) c->prof->tag = j;
-    product_cached(c, W, Xc, b, p, mode, q, skip);
+    product(c, W, Xc, b, p, mode, q, skip);
     cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st);
     // Stop enqueueing once the device reports `done` for the previous
     // iteration; the work already queued for this one returns at once.
@@ -792,18 +1118,16 @@ int hf_bicgstab(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   float* t = c->F(c->oT);
   float* rs = c->F(c->oRs);
 
-  forward_plain(c, W, Xc, b, hess ? yc : nullptr, hess);
-  if (hess)
-    for (int l = c->L; l >= 2; --l) backward_data(c, W, l, b, true);
+  build_cache(c, W, Xc, b, yc, hess);
   bicg_init(Lc, g, step, r, rs, p, neg_dir, n, (double)damping,
             (double)rel_tol * (double)rel_tol, part, st);
   for (int j = 0; j < max_iters; ++j) {
     if (c->prof) c->prof->tag = 2 * j;
-    product_cached(c, W, Xc, b, p, mode, Ap, skip);
+    product(c, W, Xc, b, p, mode, Ap, skip);
     lambda_axpy(c, Ap, p, damping, skip);
     bicg_half(Lc, r, rs, Ap, sv, n, j, part, st);
     if (c->prof) c->prof->tag = 2 * j + 1;
-    product_cached(c, W, Xc, b, sv, mode, t, skip);
+    product(c, W, Xc, b, sv, mode, t, skip);
     lambda_axpy(c, t, sv, damping, skip);
     bicg_rest(Lc, step, r, rs, p, Ap, sv, t, g, neg_dir, n, j, part, st);
     HIP_TRY(c, hipMemcpyAsync(&hostst[j & 1], st, sizeof(BicgState),

@@ -89,6 +89,69 @@ void gemm_gnbwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
 // plus the bias sums sum_k X[0](m, k) (see EpiArgs::bias_out / bias_part)
 void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e);
 
+// --------------------------------------------------------- bf16-input GEMM
+// Precision HF_BF16_INPUTS: every GEMM operand is a bf16 copy (stored as
+// uint16_t, rounded to nearest even from fp32), the MFMAs accumulate in fp32
+// and the epilogues compute in fp32.  Every operand is K-contiguous:
+//   X(m, k) = X[m * ldx + k],  Y(n, k) = Y[n * ldy + k]
+// with ldx, ldy multiples of 8 and 16-byte aligned rows.  Modes as above.
+typedef uint16_t bf16_t;
+
+struct GemmShapeH {
+  int M, N, K;
+  const bf16_t* X[2];
+  const bf16_t* Y[2];
+  int ldx, ldy;
+  int nseg;
+  int splits;
+  const int* skip;
+};
+
+// Epilogue arguments of the bf16-input kernels.  A bf16 result is written
+// twice: row-major to h* (leading dimension ldo) and transposed to t*
+// (t[col * ldt + row]), the batch-contiguous copy the weight gradient
+// contracts over.  fp32 results (logits, RZ, the phi'' cache, weight
+// gradients) go to f* with leading dimension ldf.
+struct EpiH {
+  int act;
+  int hidden;
+  const float* bias;
+  const float* rbias;
+  bf16_t* h0; bf16_t* h1; bf16_t* h2;
+  bf16_t* t0; bf16_t* t1; bf16_t* t2;
+  float* f0; float* f1; float* f2;
+  int ldo, ldt, ldf;
+  const bf16_t* a0;      // A_{l-1} (bf16, leading dimension ldo)
+  const float* a1;       // RZ_{l-1} (fp32, ldf)
+  const float* a2;       // E_{l-1} * phi''(A_{l-1}) (fp32, ldf)
+  long long split_stride;
+  float* bias_out;
+  double* bias_part;
+};
+
+// Same contractions and epilogue formulas as the fp32 kernels above, with
+// the outputs placed as follows:
+//   fwd        hidden: A -> h0/t0; output layer: logits -> f0
+//   fwd_rfwd   RZ -> f1; hidden: A -> h0/t0, RA -> h2/t2; output: logits -> f0
+//   rfwd       RZ -> f1; hidden: RA = phi'(a0) RZ -> h2/t2
+//   bwd        delta -> h0/t0; if f2: E phi''(a0) -> f2
+//   bwd_rbwd   delta -> h0/t0, Rdelta -> h1/t1
+//   rbwd       Rdelta = acc phi'(a0) + a2 a1 -> h1/t1
+//   gnbwd      Rdelta = acc phi'(a0) -> h1/t1
+//   wgrad      acc -> f0 (+ split stride), bias sums as for gemm_wgrad
+void hgemm_fwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
+void hgemm_fwd_rfwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
+void hgemm_rfwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
+void hgemm_bwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
+void hgemm_bwd_rbwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
+void hgemm_rbwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
+void hgemm_gnbwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
+void hgemm_wgrad(const Launch& L, const GemmShapeH& s, const EpiH& e);
+// out[r * ldo + c] = bf16(in[r * ldi + c]), outT[c * ldt + r] = the same
+// (R x C; either output may be null)
+void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
+              bf16_t* out, int ldo, bf16_t* outT, int ldt, const int* skip);
+
 // --------------------------------------------------------------- row ops
 // Softmax cross-entropy over rows of Z (B x C, leading dimension ld):
 //   P = softmax(Z); if y: D = (P - onehot(y)) / B and per-block loss partials

@@ -14,12 +14,13 @@ LIB_PATH = os.path.join(HERE, "libhf.so")
 
 HF_SIGMOID, HF_TANH, HF_RELU = 0, 1, 2
 HF_HESSIAN, HF_GAUSS_NEWTON = 0, 1
-HF_FP32 = 0
+HF_FP32, HF_BF16_INPUTS = 0, 1
 HF_OK, HF_EINVAL, HF_ENOMEM, HF_EHIP, HF_ELABEL, HF_ENUMERIC, HF_EWORKSPACE = \
     0, -1, -2, -3, -4, -5, -6
 
 ACTS = {"sigmoid": HF_SIGMOID, "tanh": HF_TANH, "relu": HF_RELU}
 MODES = {"hessian": HF_HESSIAN, "gauss_newton": HF_GAUSS_NEWTON}
+PRECS = {"fp32": HF_FP32, "bf16": HF_BF16_INPUTS}
 
 # Every function declared in include/hf.h.
 EXPORTS = (
@@ -121,22 +122,24 @@ class HFNet:
     """One context of the C library plus its torch-allocated workspace.
 
     dims: (d_0, ..., d_L); act: "sigmoid" | "tanh" | "relu"; max_batch: the
-    largest batch any call will use.  Calls run on torch's current stream.
+    largest batch any call will use; prec: "fp32" or "bf16" (bf16 GEMM
+    operands, fp32 accumulation).  Calls run on torch's current stream.
     """
 
-    def __init__(self, dims, act, max_batch, device="cuda"):
+    def __init__(self, dims, act, max_batch, device="cuda", prec="fp32"):
         import torch
         self.dims = tuple(int(d) for d in dims)
         self.act = act
+        self.prec = prec
         self.max_batch = int(max_batch)
         L = lib()
         arr = (ctypes.c_int32 * len(self.dims))(*self.dims)
         h = ctypes.c_void_p()
-        rc = L.hf_create(arr, len(self.dims), ACTS[act], HF_FP32, self.max_batch,
-                         ctypes.byref(h))
+        rc = L.hf_create(arr, len(self.dims), ACTS[act], PRECS[prec],
+                         self.max_batch, ctypes.byref(h))
         if rc != HF_OK:
-            raise HFError(rc, "hf_create rejected dims=%s act=%s max_batch=%d"
-                          % (self.dims, act, self.max_batch))
+            raise HFError(rc, "hf_create rejected dims=%s act=%s max_batch=%d prec=%s"
+                          % (self.dims, act, self.max_batch, prec))
         self._h = h
         self.n = int(L.hf_num_params(h))
         nbytes = int(L.hf_workspace_bytes(h))

@@ -24,19 +24,19 @@ def rel(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
 
 
-def check(gpu, ref, act, bracket=None, tol=TOL):
+def check(gpu, ref, act, bracket=None, tol=TOL, tau=RELU_TAU):
     """Assert ||gpu - ref|| <= tol ||ref|| (+ the ReLU bracket width).
 
-    bracket(kink) must return the oracle's result with ReLU's step at kink.
-    Returns (error, bound) relative to ||ref||."""
+    bracket(kink) must return the oracle's result with ReLU's step at kink;
+    the bracket is [-tau, +tau].  Returns (error, bound) relative to ||ref||."""
     gpu = np.asarray(gpu, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     nref = max(np.linalg.norm(ref), 1e-300)
     err = np.linalg.norm(gpu - ref) / nref
     bound = tol
     if act == "relu" and bracket is not None:
-        lo = np.asarray(bracket(-RELU_TAU), dtype=np.float64)
-        hi = np.asarray(bracket(+RELU_TAU), dtype=np.float64)
+        lo = np.asarray(bracket(-tau), dtype=np.float64)
+        hi = np.asarray(bracket(+tau), dtype=np.float64)
         bound += np.linalg.norm(lo - hi) / nref
     assert err <= bound, "rel error %.3e above bound %.3e" % (err, bound)
     return err, bound

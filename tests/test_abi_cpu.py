@@ -50,6 +50,8 @@ def test_create_validates(L):
     assert create(L, [4, -2, 3])[0] == H.HF_EINVAL
     assert create(L, [4, 3], act=7)[0] == H.HF_EINVAL       # unknown act
     assert create(L, [4, 3], prec=3)[0] == H.HF_EINVAL      # unknown precision
+    rc, h = create(L, [4, 3], prec=H.HF_BF16_INPUTS)       # bf16 GEMM inputs
+    assert rc == H.HF_OK and L.hf_destroy(h) == H.HF_OK
     assert create(L, [4, 3], max_batch=0)[0] == H.HF_EINVAL
     assert create(L, [4, 5000])[0] == H.HF_EINVAL           # > HF_MAX_CLASSES
     assert create(L, [2] * 18)[0] == H.HF_EINVAL            # > HF_MAX_LAYERS
@@ -66,6 +68,10 @@ def test_num_params_and_workspace(L, dims):
     assert L.hf_num_params(h) == n
     ws = L.hf_workspace_bytes(h)
     assert ws > 4 * 3 * n  # at least the CG vectors
+    assert L.hf_destroy(h) == H.HF_OK
+    rc, h = create(L, list(dims), prec=H.HF_BF16_INPUTS, max_batch=64)
+    assert rc == H.HF_OK and L.hf_num_params(h) == n
+    assert L.hf_workspace_bytes(h) > 4 * 3 * n
     assert L.hf_destroy(h) == H.HF_OK
 
 
