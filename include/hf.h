@@ -99,7 +99,9 @@ size_t hf_workspace_bytes(const hf_ctx* ctx);
 
 /* Hand the context a device workspace of at least hf_workspace_bytes()
  * bytes, 256-byte aligned.  The caller keeps ownership and must keep it
- * alive while the context uses it.  Contents need no initialisation. */
+ * alive while the context uses it, and must not write to it meanwhile.
+ * Contents need no initialisation: the call clears what needs clearing
+ * (for HF_BF16_INPUTS, the operand padding) and synchronises the device. */
 int hf_set_workspace(hf_ctx* ctx, void* dev_ptr, size_t bytes);
 
 /*

@@ -11,13 +11,27 @@
 // activations and deltas that the producing epilogues write beside the
 // row-major ones.  One LDS layout therefore serves every operand.
 //
-// One workgroup of 256 threads (4 wave64 in a 2 x 2 grid) owns a 128 x 128
-// output tile; each wave owns a 64 x 64 quadrant as 2 x 2 blocks of 32 x 32.
-// K advances in blocks of 32 through two LDS buffers; the next block's
-// global loads are in flight while the MFMAs consume the current one.
-// LDS tiles are [row][k] with 64 bytes per row; the four 16-byte chunks of a
-// row are XOR-swizzled by (row >> 2) & 3, which keeps both the 128-bit
-// stores and the 128-bit fragment loads free of bank conflicts.
+// Operand buffers are laid out so that no load needs a bounds check: every
+// leading dimension is a multiple of 64 with zeros between K and the next
+// multiple of 64, and every operand has rows up to the next multiple of 256
+// (rows past M or N only feed outputs that are not stored).  The epilogues
+// keep the zeros: a transposed copy gets zeros in its rows M .. (M rounded
+// up to 64), which the next weight-gradient GEMM reads as K padding.
+//
+// A workgroup of GM x GN wave64s owns a (32 WM GM) x (32 WN GN) output
+// tile; each wave owns WM x WN blocks of 32 x 32.  Tiles are handed out in
+// an order that keeps neighbouring tiles on one XCD (the hardware deals
+// consecutive workgroups to the 8 XCDs in turn, each with its own L2) and,
+// within an XCD, walks groups of 8 tile rows column by column, so that the
+// workgroups resident at one time share their operand panels in L2.
+// K advances BK at a time through S stages of LDS, filled by direct
+// global-to-LDS loads (global_load_lds_dwordx4) issued S - 1 blocks ahead of
+// the block the MFMAs consume: no registers stage the operands, and each
+// wave waits only for the loads of the block it is about to read.
+// LDS tiles are [row][k]; the 16-byte chunks of a row are XOR-swizzled so
+// that the 128-bit fragment loads are free of bank conflicts.  A direct
+// load writes lane i's 16 bytes at 16 i past the wave's LDS base, so the
+// swizzle is applied by choosing which global chunk each lane fetches.
 // Lane (i, h) of an MFMA feeds the 8 consecutive k values 8h .. 8h + 7 of
 // its row for both operands, so the sum over k is exact up to its order.
 #include "act.h"
@@ -26,20 +40,11 @@
 namespace hfk {
 namespace {
 
-constexpr int BK = 32;                  // k values per K block
-constexpr int NT = 256;                 // threads per workgroup
-constexpr int ROWS = 128;               // tile rows of each operand
-constexpr int CH = BK / 8;              // 16-byte chunks per tile row
-constexpr int CPT = ROWS * CH / NT;     // chunks per thread per tile
-constexpr int TILE = ROWS * BK;         // bf16 elements per tile
-constexpr int W = 2;                    // 2 x 2 MFMA blocks per wave
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ int swz(int row) { return (row >> 2) & 3; }
 
 __device__ __forceinline__ float bf2f(bf16_t h) {
   return __uint_as_float((uint32_t)h << 16);
@@ -50,51 +55,29 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
 }
 
 // ------------------------------------------------------------ tile loading
-// The thread's CPT chunks of the ROWS x BK tile at (r0, k0) of an operand
-// stored rows x K with leading dimension ld (a multiple of 8, rows 16-byte
-// aligned).  Chunk i covers row (tid + NT i) / CH, k values 8 ((tid + NT i) %
-// CH) .. + 7.
+// A ROWS x BK tile kept in LDS as [row][k]; the CH 16-byte chunks of a row
+// are XOR-swizzled by (row / RPB) % CH, RPB being the number of rows that
+// span the 64 banks.  Chunk position P of the tile (P = row * CH + pos, 64
+// chunks per direct-load instruction) holds global chunk pos ^ swz(row).
+template <int ROWS, int BK, int NW>
 struct Tile {
-  __device__ static __forceinline__ size_t offset(int ld, int tid) {
-    return (size_t)(tid / CH) * ld + (tid % CH) * 8;
+  static constexpr int CH = BK / 8;
+  static constexpr int RPB = 128 / BK;
+  static constexpr int SIZE = ROWS * BK;             // bf16 elements
+  static constexpr int INSTR = ROWS * CH / 64 / NW;  // direct loads per wave
+  static_assert(INSTR >= 1 && ROWS * CH % (64 * NW) == 0, "tile does not split over the waves");
+
+  __device__ static __forceinline__ int swz(int row) { return (row / RPB) % CH; }
+  // element offset, within an operand of leading dimension ld, of the chunk
+  // that lane `lane` of wave `wave` fetches with its instruction j
+  __device__ static __forceinline__ uint32_t src(int ld, int wave, int lane, int j) {
+    const int P = (wave * INSTR + j) * 64 + lane;
+    const int row = P / CH, pos = P % CH;
+    return (uint32_t)row * (uint32_t)ld + 8u * (uint32_t)(pos ^ swz(row));
   }
-  // tile fully inside the operand; p = operand + tile origin + offset()
-  __device__ static __forceinline__ void load_fast(const bf16_t* __restrict__ p,
-                                                   int ld, u32x4 (&g)[CPT]) {
-    const size_t step = (size_t)(NT / CH) * ld;
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) g[i] = *(const u32x4*)(p + i * step);
-  }
-  // guarded: elements outside rows x K read as zero
-  __device__ static __forceinline__ void load(const bf16_t* __restrict__ base,
-                                              int ld, int rows, int K, int r0,
-                                              int k0, int tid, u32x4 (&g)[CPT]) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int idx = tid + NT * i;
-      const int r = r0 + idx / CH, k = k0 + (idx % CH) * 8;
-      const bf16_t* p = base + (size_t)r * ld + k;
-      if (r < rows && k + 7 < K) {
-        g[i] = *(const u32x4*)p;
-      } else {
-        uint32_t w[4] = {0u, 0u, 0u, 0u};
-        if (r < rows) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            if (k + j < K) w[j >> 1] |= (uint32_t)p[j] << (16 * (j & 1));
-        }
-        g[i] = u32x4{w[0], w[1], w[2], w[3]};
-      }
-    }
-  }
-  __device__ static __forceinline__ void store(bf16_t* __restrict__ s, int tid,
-                                               const u32x4 (&g)[CPT]) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int idx = tid + NT * i;
-      const int row = idx / CH, c = idx % CH;
-      *(u32x4*)(s + row * BK + ((c ^ swz(row)) * 8)) = g[i];
-    }
+  // LDS element offset of the 64 chunks written by instruction j of a wave
+  __device__ static __forceinline__ int dst(int wave, int j) {
+    return (wave * INSTR + j) * 512;
   }
   // operand of MFMA step q (k = 16 q .. 16 q + 15) for lane (row, h)
   __device__ static __forceinline__ bf16x8 frag(const bf16_t* __restrict__ s,
@@ -102,100 +85,255 @@ struct Tile {
     const int c = 2 * q + h;
     return *(const bf16x8*)(s + row * BK + ((c ^ swz(row)) * 8));
   }
+  // sum of the 8 k values of chunk c of a row
+  __device__ static __forceinline__ float chunk_sum(const bf16_t* __restrict__ s,
+                                                    int row, int c) {
+    const u32x4 v = *(const u32x4*)(s + row * BK + ((c ^ swz(row)) * 8));
+    float t = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      t += __uint_as_float(v[j] << 16) + __uint_as_float(v[j] & 0xffff0000u);
+    return t;
+  }
 };
+
+// 16 bytes per lane from global memory straight into LDS at dst + 16 lane.
+// Written as inline assembly: with the compiler builtin, any direct load in
+// flight makes the compiler wait for every outstanding LDS read before each
+// MFMA step, which serialises the fragment loads with the MFMAs.  The
+// kernel tracks these loads itself (wait_vm before a stage is read).  M0
+// holds the wave's LDS base and needs one wait state before the load.
+__device__ __forceinline__ void dma16(const bf16_t* src, bf16_t* dst) {
+  const uint32_t lds_addr = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)dst);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(lds_addr) : "memory");
+}
+// wait until at most N vector-memory operations of this wave are pending
+// and every LDS operation has completed
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+// workgroup barrier that neither the compiler nor the scheduler may move
+// memory operations across; unlike __syncthreads it does not drain the
+// wave's outstanding direct loads
+__device__ __forceinline__ void stage_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
 
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 // ----------------------------------------------------------------- epilogues
-// Row-major bf16 outputs h* (leading dimension ldo), their transposed copies
-// t* ([col][row], leading dimension ldt), fp32 outputs f* (ldf).  aux a0 is
-// bf16 with ldo, a1 and a2 are fp32 with ldf.
-__device__ __forceinline__ void put(const EpiH& e, bf16_t* h, bf16_t* t, int r,
-                                    int c, float v) {
-  const bf16_t b = f2bf(v);
-  h[(size_t)r * e.ldo + c] = b;
-  t[(size_t)c * e.ldt + r] = b;
+// An epilogue handles 4 consecutive rows r0 .. r0 + 3 (r0 a multiple of 4)
+// of one column c < N, with r0 below M rounded up to 64.  Row-major bf16
+// outputs h* (leading dimension ldo) and fp32 outputs f* (ldf) are stored
+// for rows below M; the transposed copy t* gets the 4 rows as one 8-byte
+// store, with zeros for rows at or past M.  aux a0 is bf16 with ldo, a1 and
+// a2 are fp32 with ldf; their rows exist up to the next multiple of 256, so
+// they are read without checks and only masked.
+struct Q {                          // 4 consecutive rows of one column
+  float v[4];
+};
+
+__device__ __forceinline__ void st_h(const EpiH& e, bf16_t* h, int r0, int c,
+                                     const Q& q, int M) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (r0 + j < M) h[(size_t)(r0 + j) * e.ldo + c] = f2bf(q.v[j]);
 }
-__device__ __forceinline__ float aux0(const EpiH& e, int r, int c) {
-  return bf2f(e.a0[(size_t)r * e.ldo + c]);
+__device__ __forceinline__ void st_t(const EpiH& e, bf16_t* t, int r0, int c,
+                                     const Q& q, int M) {
+  uint32_t w[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const uint32_t lo = r0 + 2 * j < M ? f2bf(q.v[2 * j]) : 0u;
+    const uint32_t hi = r0 + 2 * j + 1 < M ? f2bf(q.v[2 * j + 1]) : 0u;
+    w[j] = lo | (hi << 16);
+  }
+  *(u32x2*)(t + (size_t)c * e.ldt + r0) = u32x2{w[0], w[1]};
+}
+__device__ __forceinline__ void st_ht(const EpiH& e, bf16_t* h, bf16_t* t,
+                                      int r0, int c, const Q& q, int M) {
+  st_h(e, h, r0, c, q, M);
+  st_t(e, t, r0, c, q, M);
+}
+__device__ __forceinline__ void st_f(const EpiH& e, float* f, int r0, int c,
+                                     const Q& q, int M) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (r0 + j < M) f[(size_t)(r0 + j) * e.ldf + c] = q.v[j];
+}
+__device__ __forceinline__ Q ld_a0(const EpiH& e, int r0, int c) {
+  Q a;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) a.v[j] = bf2f(e.a0[(size_t)(r0 + j) * e.ldo + c]);
+  return a;
+}
+__device__ __forceinline__ Q ld_f(const EpiH& e, const float* f, int r0, int c) {
+  Q a;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) a.v[j] = f[(size_t)(r0 + j) * e.ldf + c];
+  return a;
 }
 
 struct EFwd {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float) {
-    const float z = v0 + e.bias[c];
-    if (e.hidden) put(e, e.h0, e.t0, r, c, act_f(e.act, z));
-    else e.f0[(size_t)r * e.ldf + c] = z;
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q&) {
+    Q z;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) z.v[j] = v0.v[j] + e.bias[c];
+    if (e.hidden) {
+      Q a;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) a.v[j] = act_f(e.act, z.v[j]);
+      st_ht(e, e.h0, e.t0, r0, c, a, M);
+    } else {
+      st_f(e, e.f0, r0, c, z, M);
+    }
   }
 };
 struct EFwdRFwd {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float v1) {
-    const float z = v0 + e.bias[c];
-    const float rz = v1 + e.rbias[c];
-    e.f1[(size_t)r * e.ldf + c] = rz;
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q& v1) {
+    Q z, rz;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      z.v[j] = v0.v[j] + e.bias[c];
+      rz.v[j] = v1.v[j] + e.rbias[c];
+    }
+    st_f(e, e.f1, r0, c, rz, M);
     if (e.hidden) {
-      const float a = act_f(e.act, z);
-      put(e, e.h0, e.t0, r, c, a);
-      put(e, e.h2, e.t2, r, c, act_d1(e.act, a) * rz);
+      Q a, ra;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        a.v[j] = act_f(e.act, z.v[j]);
+        ra.v[j] = act_d1(e.act, a.v[j]) * rz.v[j];
+      }
+      st_ht(e, e.h0, e.t0, r0, c, a, M);
+      st_ht(e, e.h2, e.t2, r0, c, ra, M);
     } else {
-      e.f0[(size_t)r * e.ldf + c] = z;
+      st_f(e, e.f0, r0, c, z, M);
     }
   }
 };
 struct ERFwd {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float) {
-    const float rz = v0 + e.rbias[c];
-    e.f1[(size_t)r * e.ldf + c] = rz;
-    if (e.hidden) put(e, e.h2, e.t2, r, c, act_d1(e.act, aux0(e, r, c)) * rz);
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q&) {
+    Q rz;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rz.v[j] = v0.v[j] + e.rbias[c];
+    st_f(e, e.f1, r0, c, rz, M);
+    if (e.hidden) {
+      const Q a = ld_a0(e, r0, c);
+      Q ra;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) ra.v[j] = act_d1(e.act, a.v[j]) * rz.v[j];
+      st_ht(e, e.h2, e.t2, r0, c, ra, M);
+    }
   }
 };
 struct EBwd {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float) {
-    put(e, e.h0, e.t0, r, c, v0 * act_d1(e.act, aux0(e, r, c)));
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q&) {
+    const Q a = ld_a0(e, r0, c);
+    Q d;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) d.v[j] = v0.v[j] * act_d1(e.act, a.v[j]);
+    st_ht(e, e.h0, e.t0, r0, c, d, M);
   }
 };
+// backward data that also caches E * phi''(A) for the Hessian product
 struct EBwdE2 {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float) {
-    const float a = aux0(e, r, c);
-    put(e, e.h0, e.t0, r, c, v0 * act_d1(e.act, a));
-    e.f2[(size_t)r * e.ldf + c] = v0 * act_d2(e.act, a);
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q&) {
+    const Q a = ld_a0(e, r0, c);
+    Q d, e2;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      d.v[j] = v0.v[j] * act_d1(e.act, a.v[j]);
+      e2.v[j] = v0.v[j] * act_d2(e.act, a.v[j]);
+    }
+    st_ht(e, e.h0, e.t0, r0, c, d, M);
+    st_f(e, e.f2, r0, c, e2, M);
   }
 };
 struct EBwdRBwd {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float v1) {
-    const float a = aux0(e, r, c);
-    const float d1 = act_d1(e.act, a);
-    put(e, e.h0, e.t0, r, c, v0 * d1);
-    put(e, e.h1, e.t1, r, c,
-        v1 * d1 + v0 * act_d2(e.act, a) * e.a1[(size_t)r * e.ldf + c]);
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q& v1) {
+    const Q a = ld_a0(e, r0, c);
+    const Q rz = ld_f(e, e.a1, r0, c);
+    Q d, rd;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float d1 = act_d1(e.act, a.v[j]);
+      d.v[j] = v0.v[j] * d1;
+      rd.v[j] = v1.v[j] * d1 + v0.v[j] * act_d2(e.act, a.v[j]) * rz.v[j];
+    }
+    st_ht(e, e.h0, e.t0, r0, c, d, M);
+    st_ht(e, e.h1, e.t1, r0, c, rd, M);
   }
 };
 struct ERBwd {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float) {
-    const size_t o = (size_t)r * e.ldf + c;
-    put(e, e.h1, e.t1, r, c, v0 * act_d1(e.act, aux0(e, r, c)) + e.a2[o] * e.a1[o]);
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q&) {
+    const Q a = ld_a0(e, r0, c);
+    const Q rz = ld_f(e, e.a1, r0, c);
+    const Q e2 = ld_f(e, e.a2, r0, c);
+    Q rd;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      rd.v[j] = v0.v[j] * act_d1(e.act, a.v[j]) + e2.v[j] * rz.v[j];
+    st_ht(e, e.h1, e.t1, r0, c, rd, M);
   }
 };
 struct EGNBwd {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float) {
-    put(e, e.h1, e.t1, r, c, v0 * act_d1(e.act, aux0(e, r, c)));
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q&) {
+    const Q a = ld_a0(e, r0, c);
+    Q rd;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rd.v[j] = v0.v[j] * act_d1(e.act, a.v[j]);
+    st_ht(e, e.h1, e.t1, r0, c, rd, M);
   }
 };
 struct EStore {
-  static __device__ __forceinline__ void apply(const EpiH& e, int r, int c,
-                                               float v0, float) {
-    e.f0[(size_t)blockIdx.z * e.split_stride + (size_t)r * e.ldf + c] = v0;
+  static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
+                                               const Q& v0, const Q&) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (r0 + j < M)
+        e.f0[(size_t)zs * e.split_stride + (size_t)(r0 + j) * e.ldf + c] = v0.v[j];
   }
 };
+
+// ------------------------------------------------------------- tile order
+// The tile (tn, tm) and split tz this workgroup computes.  Linear dispatch
+// index L goes to XCD L % 8; when the grid is a multiple of 8, XCD x gets
+// the x-th contiguous eighth of the logical order.  Within a split, the
+// logical order walks groups of 8 tile rows, column by column.
+__device__ __forceinline__ void tile_of(int& tn, int& tm, int& tz) {
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int T = gx * gy * gridDim.z;
+  const int L = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int Lg = (T % 8 == 0) ? (L % 8) * (T / 8) + L / 8 : L;
+  tz = Lg / (gx * gy);
+  const int r = Lg % (gx * gy);
+  constexpr int G = 8;
+  const int g = r / (G * gx);
+  const int first = g * G;
+  const int rows = min(G, gy - first);
+  const int w = r - g * G * gx;
+  tm = first + w % rows;
+  tn = w / rows;
+}
 
 // ------------------------------------------------------------------- body
 // MODE 0: single (nseg K-segments, optional split-K over grid z)
@@ -203,213 +341,281 @@ struct EStore {
 // MODE 2: dual0  acc0 = X0 Y0, acc1 = X0 Y1
 // BIAS (weight gradient): blocks of the first column tile also sum their X
 // tiles of K-segment 0 over k, giving sum_k X(m, k) for their rows.
-template <int MODE, class Epi, bool BIAS>
+template <int MODE, class Epi, bool BIAS, int WM, int WN, int GM, int GN, int BK, int S>
 __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
   if (s.skip && *s.skip) return;
-  constexpr int T = MODE == 0 ? 2 : (MODE == 1 ? 4 : 3);
-  __shared__ __attribute__((aligned(16))) bf16_t lds[2][T][TILE];
+  constexpr int NW = GM * GN, NT = 64 * NW;
+  constexpr int RM = 32 * WM * GM, RN = 32 * WN * GN;
+  using TX = Tile<RM, BK, NW>;
+  using TY = Tile<RN, BK, NW>;
+  constexpr int NX = MODE == 1 ? 2 : 1;      // X tiles per K block
+  constexpr int NY = MODE == 0 ? 1 : 2;      // Y tiles per K block
+  constexpr int STAGE = NX * TX::SIZE + NY * TY::SIZE;
+  constexpr int LPB = NX * TX::INSTR + NY * TY::INSTR;   // loads per block per wave
+  static_assert(S >= 2 && (S - 2) * LPB < 64, "pipeline depth");
+  __shared__ __attribute__((aligned(16))) bf16_t lds[S * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / GN, wn = wave % GN;
   const int li = lane & 31, h = lane >> 5;
-  const int m0 = blockIdx.y * ROWS;
-  const int n0 = blockIdx.x * ROWS;
+  int tn, tm, tz;
+  tile_of(tn, tm, tz);
+  const int m0 = tm * RM;
+  const int n0 = tn * RN;
 
   const int kbps = (s.K + BK - 1) / BK;
   const int nvb = (MODE == 0 ? s.nseg : 1) * kbps;
   int vb0 = 0, vb1 = nvb;
   if (MODE == 0 && s.splits > 1) {
     const int per = (nvb + s.splits - 1) / s.splits;
-    vb0 = blockIdx.z * per;
+    vb0 = tz * per;
     vb1 = min(nvb, vb0 + per);
   }
+  const int nblk = vb1 > vb0 ? vb1 - vb0 : 0;
 
-  f32x16 acc0[W][W], acc1[W][W];
+  f32x16 acc0[WM][WN], acc1[WM][WN];
 #pragma unroll
-  for (int a = 0; a < W; ++a)
+  for (int a = 0; a < WM; ++a)
 #pragma unroll
-    for (int b = 0; b < W; ++b)
+    for (int b = 0; b < WN; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         acc0[a][b][r] = 0.0f;
         if (MODE != 0) acc1[a][b][r] = 0.0f;
       }
 
-  u32x4 g[T][CPT];
-  const bool in_x = m0 + ROWS <= s.M;
-  const bool in_y = n0 + ROWS <= s.N;
-  const size_t ox = Tile::offset(s.ldx, tid) + (size_t)m0 * s.ldx;
-  const size_t oy = Tile::offset(s.ldy, tid) + (size_t)n0 * s.ldy;
-  auto ldx = [&](const bf16_t* base, int k0, u32x4 (&r)[CPT]) {
-    if (in_x && k0 + BK <= s.K) Tile::load_fast(base + ox + k0, s.ldx, r);
-    else Tile::load(base, s.ldx, s.M, s.K, m0, k0, tid, r);
-  };
-  auto ldy = [&](const bf16_t* base, int k0, u32x4 (&r)[CPT]) {
-    if (in_y && k0 + BK <= s.K) Tile::load_fast(base + oy + k0, s.ldy, r);
-    else Tile::load(base, s.ldy, s.N, s.K, n0, k0, tid, r);
-  };
-  auto gload = [&](int vb) {
+  // per-lane source offsets of the direct loads, relative to the tile origin
+  uint32_t offx[TX::INSTR], offy[TY::INSTR];
+#pragma unroll
+  for (int j = 0; j < TX::INSTR; ++j) offx[j] = TX::src(s.ldx, wave, lane, j);
+#pragma unroll
+  for (int j = 0; j < TY::INSTR; ++j) offy[j] = TY::src(s.ldy, wave, lane, j);
+  const size_t bx = (size_t)m0 * s.ldx, by = (size_t)n0 * s.ldy;
+
+  // operand pointers in registers: an indexed read of the argument array
+  // inside the loop would be a scalar memory load, which shares the LDS
+  // wait counter and forces every fragment wait to drain it completely
+  const bf16_t* const X0 = s.X[0];
+  const bf16_t* const X1 = s.X[1];
+  const bf16_t* const Y0 = s.Y[0];
+  const bf16_t* const Y1 = s.Y[1];
+  auto issue = [&](int vb, int st) {
     const int seg = (MODE == 0) ? vb / kbps : 0;
     const int k0 = (vb - seg * kbps) * BK;
-    if (MODE == 0) {
-      ldx(s.X[seg], k0, g[0]);
-      ldy(s.Y[seg], k0, g[1]);
-    } else if (MODE == 1) {
-      ldx(s.X[0], k0, g[0]);
-      ldx(s.X[1], k0, g[1]);
-      ldy(s.Y[0], k0, g[2]);
-      ldy(s.Y[1], k0, g[3]);
-    } else {
-      ldx(s.X[0], k0, g[0]);
-      ldy(s.Y[0], k0, g[1]);
-      ldy(s.Y[1], k0, g[2]);
+    bf16_t* base = lds + st * STAGE;
+#pragma unroll
+    for (int t = 0; t < NX; ++t) {
+      const bf16_t* x = ((MODE == 0 ? seg : t) ? X1 : X0) + bx + k0;
+#pragma unroll
+      for (int j = 0; j < TX::INSTR; ++j)
+        dma16(x + offx[j], base + t * TX::SIZE + TX::dst(wave, j));
+    }
+#pragma unroll
+    for (int t = 0; t < NY; ++t) {
+      const bf16_t* y = ((MODE == 0 ? seg : t) ? Y1 : Y0) + by + k0;
+#pragma unroll
+      for (int j = 0; j < TY::INSTR; ++j)
+        dma16(y + offy[j], base + NX * TX::SIZE + t * TY::SIZE + TY::dst(wave, j));
     }
   };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int t = 0; t < T; ++t) Tile::store(lds[buf][t], tid, g[t]);
+  const int xrow = wm * 32 * WM + li;
+  const int yrow = wn * 32 * WN + li;
+  // Fragments of one MFMA step; two sets alternate so that the LDS reads of
+  // step q + 1 are in flight while the MFMAs of step q run.
+  struct Frags {
+    bf16x8 x0[WM], x1[WM], y0[WN], y1[WN];
   };
-  const int xrow = wm * 32 * W + li;
-  const int yrow = wn * 32 * W + li;
-  auto compute = [&](int buf) {
+  auto fetch = [&](Frags& f, int st, int q) {
+    const bf16_t* lx0 = lds + st * STAGE;
+    const bf16_t* lx1 = lx0 + (NX - 1) * TX::SIZE;
+    const bf16_t* ly0 = lds + st * STAGE + NX * TX::SIZE;
+    const bf16_t* ly1 = ly0 + (NY - 1) * TY::SIZE;
 #pragma unroll
-    for (int q = 0; q < BK / 16; ++q) {
-      bf16x8 x0[W], y0[W];
+    for (int a = 0; a < WM; ++a) {
+      f.x0[a] = TX::frag(lx0, xrow + 32 * a, h, q);
+      if (MODE == 1) f.x1[a] = TX::frag(lx1, xrow + 32 * a, h, q);
+    }
 #pragma unroll
-      for (int a = 0; a < W; ++a) x0[a] = Tile::frag(lds[buf][0], xrow + 32 * a, h, q);
-      if (MODE == 0) {
+    for (int b = 0; b < WN; ++b) {
+      f.y0[b] = TY::frag(ly0, yrow + 32 * b, h, q);
+      if (MODE != 0) f.y1[b] = TY::frag(ly1, yrow + 32 * b, h, q);
+    }
+  };
+  auto mma = [&](const Frags& f) {
 #pragma unroll
-        for (int b = 0; b < W; ++b) y0[b] = Tile::frag(lds[buf][1], yrow + 32 * b, h, q);
+    for (int a = 0; a < WM; ++a)
 #pragma unroll
-        for (int a = 0; a < W; ++a)
-#pragma unroll
-          for (int b = 0; b < W; ++b) acc0[a][b] = mfma(x0[a], y0[b], acc0[a][b]);
-      } else if (MODE == 1) {
-        bf16x8 x1[W], y1[W];
-#pragma unroll
-        for (int a = 0; a < W; ++a) x1[a] = Tile::frag(lds[buf][1], xrow + 32 * a, h, q);
-#pragma unroll
-        for (int b = 0; b < W; ++b) {
-          y0[b] = Tile::frag(lds[buf][2], yrow + 32 * b, h, q);
-          y1[b] = Tile::frag(lds[buf][3], yrow + 32 * b, h, q);
+      for (int b = 0; b < WN; ++b) {
+        acc0[a][b] = mfma(f.x0[a], f.y0[b], acc0[a][b]);
+        if (MODE == 1) {
+          acc1[a][b] = mfma(f.x1[a], f.y0[b], acc1[a][b]);
+          acc1[a][b] = mfma(f.x0[a], f.y1[b], acc1[a][b]);
+        } else if (MODE == 2) {
+          acc1[a][b] = mfma(f.x0[a], f.y1[b], acc1[a][b]);
         }
-#pragma unroll
-        for (int a = 0; a < W; ++a)
-#pragma unroll
-          for (int b = 0; b < W; ++b) {
-            acc0[a][b] = mfma(x0[a], y0[b], acc0[a][b]);
-            acc1[a][b] = mfma(x1[a], y0[b], acc1[a][b]);
-            acc1[a][b] = mfma(x0[a], y1[b], acc1[a][b]);
-          }
-      } else {
-        bf16x8 y1[W];
-#pragma unroll
-        for (int b = 0; b < W; ++b) {
-          y0[b] = Tile::frag(lds[buf][1], yrow + 32 * b, h, q);
-          y1[b] = Tile::frag(lds[buf][2], yrow + 32 * b, h, q);
-        }
-#pragma unroll
-        for (int a = 0; a < W; ++a)
-#pragma unroll
-          for (int b = 0; b < W; ++b) {
-            acc0[a][b] = mfma(x0[a], y0[b], acc0[a][b]);
-            acc1[a][b] = mfma(x0[a], y1[b], acc1[a][b]);
-          }
       }
+  };
+  auto compute = [&](int st) {
+    constexpr int NQ = BK / 16;
+    Frags fa, fb;
+    fetch(fa, st, 0);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      if (q + 1 < NQ) fetch((q & 1) ? fa : fb, st, q + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      mma((q & 1) ? fb : fa);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // bias sums: thread t owns row t % ROWS of the X tile and the half
-  // t / ROWS of its k values (two 16-byte chunks)
-  static_assert(NT == 2 * ROWS && CH == 4, "bias sum layout");
-  const bool do_bias = BIAS && blockIdx.x == 0 && (e.bias_out || e.bias_part);
+  // bias sums: thread t owns row t % RM of the X tile and part t / RM of
+  // its chunks
+  constexpr int PARTS = NT / RM > 0 ? NT / RM : 1;
+  static_assert(!BIAS || (NT % RM == 0 && TX::CH % PARTS == 0), "bias sum layout");
+  const bool do_bias = BIAS && tn == 0 && (e.bias_out || e.bias_part);
   double bsum = 0.0;
-  if (vb0 < vb1) {
-    gload(vb0);
-    sstore(0);
-    __syncthreads();
-    int buf = 0;
-    for (int vb = vb0; vb < vb1; ++vb) {
-      const bool more = vb + 1 < vb1;
-      if (more) gload(vb + 1);
-      compute(buf);
-      if (BIAS && do_bias && vb < kbps) {
-        const int row = tid % ROWS, half = tid / ROWS;
+
+  // prologue: the first S - 1 blocks in flight
 #pragma unroll
-        for (int cc = 0; cc < 2; ++cc) {
-          const int c = 2 * half + cc;
-          const u32x4 v = *(const u32x4*)(lds[buf][0] + row * BK + ((c ^ swz(row)) * 8));
-          float part = 0.0f;
+  for (int i = 0; i < S - 1; ++i)
+    if (i < nblk) issue(vb0 + i, i);
+  for (int it = 0; it < nblk; ++it) {
+    // this wave's loads of block it have landed once at most
+    // min(S - 2, nblk - 1 - it) later blocks are still pending
+    // (one unconditional wait, so that the compiler sees every earlier
+    // scalar and LDS operation complete on every path)
+    const int ahead = min(S - 2, nblk - 1 - it);
+    wait_vm<(S - 2) * LPB>();
+    if (S > 3 && ahead == 1) wait_vm<(S > 3 ? LPB : 0)>();
+    if (ahead == 0) wait_vm<0>();
+    stage_barrier();     // every wave's loads landed; stage it - 1 is free
+    if (it + S - 1 < nblk) issue(vb0 + it + S - 1, (it + S - 1) % S);
+    const int st = it % S;
+    compute(st);
+    if (BIAS && do_bias && vb0 + it < kbps) {
+      const int row = tid % RM, part = tid / RM;
+      constexpr int CPP = TX::CH / PARTS;
+      const bf16_t* lx0 = lds + st * STAGE;
+      float t = 0.0f;
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            part += __uint_as_float(v[j] << 16) + __uint_as_float(v[j] & 0xffff0000u);
-          bsum += (double)part;
-        }
-      }
-      if (more) sstore(buf ^ 1);
-      __syncthreads();
-      buf ^= 1;
+      for (int cc = 0; cc < CPP; ++cc) t += TX::chunk_sum(lx0, row, part * CPP + cc);
+      bsum += (double)t;
     }
   }
   if (BIAS && do_bias) {
-    __shared__ double bpart2[ROWS];
-    if (tid >= ROWS) bpart2[tid - ROWS] = bsum;
+    __shared__ double bpart2[RM];
+    if (PARTS == 2 && tid >= RM) bpart2[tid - RM] = bsum;
     __syncthreads();
-    if (tid < ROWS && m0 + tid < s.M) {
-      const double t = bsum + bpart2[tid];
-      if (s.splits > 1) e.bias_part[(size_t)blockIdx.z * s.M + m0 + tid] = t;
+    if (tid < RM && m0 + tid < s.M) {
+      const double t = PARTS == 2 ? bsum + bpart2[tid] : bsum;
+      if (s.splits > 1) e.bias_part[(size_t)tz * s.M + m0 + tid] = t;
       else e.bias_out[m0 + tid] = (float)t;
     }
   }
 
   // 32 x 32 accumulator layout: lane (li, h), register r holds row
-  // 8 (r / 4) + 4 h + r % 4, column li of the block.
+  // 8 (r / 4) + 4 h + r % 4, column li of the block; registers 4g .. 4g + 3
+  // are 4 consecutive rows.
+  const int Mpad = (s.M + 63) & ~63;
 #pragma unroll
-  for (int a = 0; a < W; ++a)
+  for (int a = 0; a < WM; ++a)
 #pragma unroll
-    for (int b = 0; b < W; ++b) {
-      const f32x16 v0 = acc0[a][b];
-      const f32x16 v1 = MODE == 0 ? v0 : acc1[a][b];
-      const int rbase = m0 + wm * 32 * W + a * 32 + 4 * h;
-      const int col = n0 + wn * 32 * W + b * 32 + li;
+    for (int b = 0; b < WN; ++b) {
+      const int rbase = m0 + wm * 32 * WM + a * 32 + 4 * h;
+      const int col = n0 + wn * 32 * WN + b * 32 + li;
       if (col < s.N) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = rbase + 8 * (r >> 2) + (r & 3);
-          if (row < s.M) Epi::apply(e, row, col, v0[r], MODE == 0 ? 0.0f : v1[r]);
+        for (int g = 0; g < 4; ++g) {
+          const int r0 = rbase + 8 * g;
+          if (r0 < Mpad) {
+            Q v0, v1;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              v0.v[j] = acc0[a][b][4 * g + j];
+              v1.v[j] = MODE == 0 ? 0.0f : acc1[a][b][4 * g + j];
+            }
+            Epi::apply(e, r0, col, s.M, tz, v0, v1);
+          }
         }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
 }
 
+// Tile shapes (WM, WN, GM, GN, BK, stages) of the single-product kernels
+// and of the dual ones (which hold two accumulator sets and up to four
+// tiles).
+#ifndef HF_HS_WM
+#define HF_HS_WM 4
+#endif
+#ifndef HF_HS_WN
+#define HF_HS_WN 2
+#endif
+#ifndef HF_HS_GM
+#define HF_HS_GM 2
+#endif
+#ifndef HF_HS_GN
+#define HF_HS_GN 4
+#endif
+#ifndef HF_HS_BK
+#define HF_HS_BK 64
+#endif
+#ifndef HF_HS_S
+#define HF_HS_S 2
+#endif
+#ifndef HF_HD_WM
+#define HF_HD_WM 2
+#endif
+#ifndef HF_HD_WN
+#define HF_HD_WN 2
+#endif
+#ifndef HF_HD_GM
+#define HF_HD_GM 2
+#endif
+#ifndef HF_HD_GN
+#define HF_HD_GN 2
+#endif
+#ifndef HF_HD_BK
+#define HF_HD_BK 32
+#endif
+#ifndef HF_HD_S
+#define HF_HD_S 3
+#endif
+constexpr int SWM = HF_HS_WM, SWN = HF_HS_WN, SGM = HF_HS_GM, SGN = HF_HS_GN;
+constexpr int SBK = HF_HS_BK, SS = HF_HS_S;
+constexpr int DWM = HF_HD_WM, DWN = HF_HD_WN, DGM = HF_HD_GM, DGN = HF_HD_GN;
+constexpr int DBK = HF_HD_BK, DS = HF_HD_S;
+constexpr int SNT = 64 * SGM * SGN, DNT = 64 * DGM * DGN;
+
 }  // namespace
 
-#define HF_HGEMM_KERNEL(NAME, MODE, EPI, BIAS)                                 \
-  extern "C" __global__ __launch_bounds__(256, 1) void NAME(GemmShapeH s,      \
-                                                            EpiH e) {          \
-    hgemm_body<MODE, EPI, BIAS>(s, e);                                         \
+#define HF_HGEMM_KERNEL(NAME, MODE, EPI, BIAS, P)                              \
+  extern "C" __global__ __launch_bounds__(P##NT, 1) void NAME(GemmShapeH s,    \
+                                                              EpiH e) {        \
+    hgemm_body<MODE, EPI, BIAS, P##WM, P##WN, P##GM, P##GN, P##BK, P##S>(s, e);  \
   }
 
-HF_HGEMM_KERNEL(hf_hgemm_fwd, 0, EFwd, false)
-HF_HGEMM_KERNEL(hf_hgemm_fwd_rfwd, 1, EFwdRFwd, false)
-HF_HGEMM_KERNEL(hf_hgemm_fwd_rfwd0, 2, EFwdRFwd, false)
-HF_HGEMM_KERNEL(hf_hgemm_rfwd, 0, ERFwd, false)
-HF_HGEMM_KERNEL(hf_hgemm_bwd, 0, EBwd, false)
-HF_HGEMM_KERNEL(hf_hgemm_bwd_e2, 0, EBwdE2, false)
-HF_HGEMM_KERNEL(hf_hgemm_bwd_rbwd, 1, EBwdRBwd, false)
-HF_HGEMM_KERNEL(hf_hgemm_rbwd, 0, ERBwd, false)
-HF_HGEMM_KERNEL(hf_hgemm_gnbwd, 0, EGNBwd, false)
-HF_HGEMM_KERNEL(hf_hgemm_wgrad, 0, EStore, true)
+HF_HGEMM_KERNEL(hf_hgemm_fwd, 0, EFwd, false, S)
+HF_HGEMM_KERNEL(hf_hgemm_fwd_rfwd, 1, EFwdRFwd, false, D)
+HF_HGEMM_KERNEL(hf_hgemm_fwd_rfwd0, 2, EFwdRFwd, false, D)
+HF_HGEMM_KERNEL(hf_hgemm_rfwd, 0, ERFwd, false, S)
+HF_HGEMM_KERNEL(hf_hgemm_bwd, 0, EBwd, false, S)
+HF_HGEMM_KERNEL(hf_hgemm_bwd_e2, 0, EBwdE2, false, S)
+HF_HGEMM_KERNEL(hf_hgemm_bwd_rbwd, 1, EBwdRBwd, false, D)
+HF_HGEMM_KERNEL(hf_hgemm_rbwd, 0, ERBwd, false, S)
+HF_HGEMM_KERNEL(hf_hgemm_gnbwd, 0, EGNBwd, false, S)
+HF_HGEMM_KERNEL(hf_hgemm_wgrad, 0, EStore, true, S)
 
-// out[r * ldo + c] = bf16(in[r * ldi + c]) and outT[c * ldt + r] = the same
-// value, for r < R, c < C, through a padded 32 x 32 LDS tile so that the
+// out[r * ldo + c] = bf16(in[r * ldi + c]) for r < R, and outT[c * ldt + r]
+// = the same value for r < R, zero for R <= r < Rpad (the K padding a later
+// GEMM reads), for c < C; through a padded 32 x 32 LDS tile so that the
 // reads and both writes are coalesced.  Either output may be null.
 extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16(
     const float* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ out,
-    int ldo, bf16_t* __restrict__ outT, int ldt, const int* __restrict__ skip) {
+    int ldo, bf16_t* __restrict__ outT, int ldt, int Rpad,
+    const int* __restrict__ skip) {
   if (skip && *skip) return;
   __shared__ bf16_t t[32][34];
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
@@ -417,18 +623,19 @@ extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16(
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = r0 + ty + 8 * j, c = c0 + tx;
+    bf16_t b = 0;
     if (r < R && c < C) {
-      const bf16_t b = f2bf(in[(size_t)r * ldi + c]);
-      t[ty + 8 * j][tx] = b;
+      b = f2bf(in[(size_t)r * ldi + c]);
       if (out) out[(size_t)r * ldo + c] = b;
     }
+    t[ty + 8 * j][tx] = b;
   }
   if (!outT) return;
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int c = c0 + ty + 8 * j, r = r0 + tx;
-    if (r < R && c < C) outT[(size_t)c * ldt + r] = t[tx][ty + 8 * j];
+    if (r < Rpad && c < C) outT[(size_t)c * ldt + r] = t[tx][ty + 8 * j];
   }
 }
 
@@ -439,10 +646,12 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 void launch(const Launch& L, const char* name, HKernel k, int mode,
             const GemmShapeH& s, const EpiH& e, double flops, double bytes) {
-  dim3 grid(cdiv(s.N, ROWS), cdiv(s.M, ROWS),
-            (mode == 0 && s.splits > 1) ? s.splits : 1);
+  const bool sg = mode == 0;
+  const int rm = 32 * (sg ? SWM * SGM : DWM * DGM);
+  const int rn = 32 * (sg ? SWN * SGN : DWN * DGN);
+  dim3 grid(cdiv(s.N, rn), cdiv(s.M, rm), (sg && s.splits > 1) ? s.splits : 1);
   prof_begin(L, name);
-  hipLaunchKernelGGL(k, grid, dim3(NT), 0, L.stream, s, e);
+  hipLaunchKernelGGL(k, grid, dim3(sg ? SNT : DNT), 0, L.stream, s, e);
   prof_end(L, name, flops, bytes);
 }
 
@@ -496,10 +705,12 @@ void hgemm_wgrad(const Launch& L, const GemmShapeH& s, const EpiH& e) {
          io(s, s.nseg, s.nseg, 4.0 * (s.splits > 1 ? s.splits : 1)));
 }
 void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
-              bf16_t* out, int ldo, bf16_t* outT, int ldt, const int* skip) {
+              bf16_t* out, int ldo, bf16_t* outT, int ldt, int Rpad,
+              const int* skip) {
+  if (Rpad < R) Rpad = R;
   prof_begin(L, "hf_cvt_bf16");
-  hipLaunchKernelGGL(hf_cvt_bf16, dim3(cdiv(C, 32), cdiv(R, 32)), dim3(256), 0,
-                     L.stream, in, R, C, ldi, out, ldo, outT, ldt, skip);
+  hipLaunchKernelGGL(hf_cvt_bf16, dim3(cdiv(C, 32), cdiv(Rpad, 32)), dim3(256), 0,
+                     L.stream, in, R, C, ldi, out, ldo, outT, ldt, Rpad, skip);
   prof_end(L, "hf_cvt_bf16", 0.0,
            (double)R * C * (4.0 + (out ? 2.0 : 0.0) + (outT ? 2.0 : 0.0)));
 }

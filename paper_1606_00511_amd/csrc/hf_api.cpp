@@ -188,6 +188,7 @@ struct hf_ctx {
   // dimension ldh_l; the transposed (batch-contiguous) ones *T have ldB.
   std::vector<int> ldh;
   int ldB = 0;
+  size_t hbeg = 0, hend = 0;   // the bf16 region, zeroed by hf_set_workspace
   size_t hX = 0, hXT = 0;
   std::vector<size_t> hW, hWT, hV, hVT, hA, hAT, hRA, hRAT, hD, hDT, hRD, hRDT;
   size_t oS = 0, oT = 0, oRs = 0;    // Bi-CG-STAB: s, t = B s, r0*
@@ -237,7 +238,8 @@ int fail(hf_ctx* c, int code, const char* fmt, ...) {
 inline size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 inline bool a16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 inline int round4(int x) { return (x + 3) & ~3; }
-inline int round8(int x) { return (x + 7) & ~7; }
+inline int round64(int x) { return (x + 63) & ~63; }
+inline size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
 
 void plan(hf_ctx* c) {
   const int L = c->L;
@@ -255,25 +257,44 @@ void plan(hf_ctx* c) {
     v->assign(L + 1, 0);
   const size_t f4 = sizeof(float), h2 = sizeof(bf16_t);
   const size_t LB = (size_t)c->ldB;
-  for (int l = 1; l <= L; ++l) {
-    if (!h) {
+  // bf16 operands (and the fp32 rows the bf16 epilogues read) have rows up
+  // to a multiple of 256: the GEMM tiles read them without bounds checks
+  const size_t RB = h ? round256(B) : B;
+  auto R256 = [&](int d) { return round256((size_t)d); };
+  if (!h) {
+    for (int l = 1; l <= L; ++l) {
       // W_l and V_l transposed: d_{l-1} rows of ld_l floats
       c->oWT[l] = take((size_t)c->d[l - 1] * c->ld[l] * f4);
       c->oVT[l] = take((size_t)c->d[l - 1] * c->ld[l] * f4);
-    } else {
-      // bf16 W_l, V_l (row-major, forward) and transposed (backward)
-      c->hW[l] = take((size_t)c->d[l] * c->ldh[l - 1] * h2);
-      c->hWT[l] = take((size_t)c->d[l - 1] * c->ldh[l] * h2);
-      c->hV[l] = take((size_t)c->d[l] * c->ldh[l - 1] * h2);
-      c->hVT[l] = take((size_t)c->d[l - 1] * c->ldh[l] * h2);
     }
-  }
-  if (h) {
-    c->hX = take(B * c->ldh[0] * h2);
-    c->hXT = take((size_t)c->d[0] * LB * h2);
+  } else {
+    c->hbeg = off;
+    for (int l = 1; l <= L; ++l) {
+      // bf16 W_l, V_l (row-major, forward) and transposed (backward)
+      c->hW[l] = take(R256(c->d[l]) * c->ldh[l - 1] * h2);
+      c->hWT[l] = take(R256(c->d[l - 1]) * c->ldh[l] * h2);
+      c->hV[l] = take(R256(c->d[l]) * c->ldh[l - 1] * h2);
+      c->hVT[l] = take(R256(c->d[l - 1]) * c->ldh[l] * h2);
+    }
+    c->hX = take(RB * c->ldh[0] * h2);
+    c->hXT = take(R256(c->d[0]) * LB * h2);
+    for (int l = 1; l <= L; ++l) {
+      const size_t szh = RB * c->ldh[l] * h2, szt = R256(c->d[l]) * LB * h2;
+      if (l < L) {
+        c->hA[l] = take(szh);
+        c->hAT[l] = take(szt);
+        c->hRA[l] = take(szh);
+        c->hRAT[l] = take(szt);
+      }
+      c->hD[l] = take(szh);
+      c->hDT[l] = take(szt);
+      c->hRD[l] = take(szh);
+      c->hRDT[l] = take(szt);
+    }
+    c->hend = off;
   }
   for (int l = 1; l <= L; ++l) {
-    const size_t sz = B * c->ld[l] * f4;
+    const size_t sz = RB * c->ld[l] * f4;
     if (!h) {
       if (l < L) {
         c->oA[l] = take(sz);
@@ -284,26 +305,16 @@ void plan(hf_ctx* c) {
       c->oRZ[l] = take(sz);
       c->oRD[l] = take(sz);
     } else {
-      const size_t szh = B * c->ldh[l] * h2, szt = (size_t)c->d[l] * LB * h2;
-      if (l < L) {
-        c->oE2[l] = take(sz);
-        c->hA[l] = take(szh);
-        c->hAT[l] = take(szt);
-        c->hRA[l] = take(szh);
-        c->hRAT[l] = take(szt);
-      } else {
+      if (l < L) c->oE2[l] = take(sz);
+      else {
         c->oD[l] = take(sz);     // fp32 softmax outputs, converted to bf16
         c->oRD[l] = take(sz);
       }
       c->oRZ[l] = take(sz);
-      c->hD[l] = take(szh);
-      c->hDT[l] = take(szt);
-      c->hRD[l] = take(szh);
-      c->hRDT[l] = take(szt);
     }
   }
-  c->oZ = take(B * c->ld[L] * f4);
-  c->oP = take(B * c->ld[L] * f4);
+  c->oZ = take(RB * c->ld[L] * f4);
+  c->oP = take(RB * c->ld[L] * f4);
   size_t mn = 0;
   int dmax = 0;
   for (int l = 1; l <= L; ++l) {
@@ -551,13 +562,13 @@ void weights_h(hf_ctx* c, const float* v, const std::vector<size_t>& row,
                const std::vector<size_t>& tr, const int* skip) {
   for (int l = 1; l <= c->L; ++l)
     cvt_bf16(c->launch(), v + c->offW[l], c->d[l], c->d[l - 1], c->d[l - 1],
-             c->H(row[l]), c->ldh[l - 1], c->H(tr[l]), c->ldh[l], skip);
+             c->H(row[l]), c->ldh[l - 1], c->H(tr[l]), c->ldh[l], c->ldh[l], skip);
 }
 
 // bf16 copies of the input rows: X [B][ldh_0] and X^T [d_0][ldB]
 void input_h(hf_ctx* c, const float* X, int B) {
   cvt_bf16(c->launch(), X, B, c->d[0], c->d[0], c->H(c->hX), c->ldh[0],
-           c->H(c->hXT), c->ldB, nullptr);
+           c->H(c->hXT), c->ldB, round64(B), nullptr);
 }
 
 // an fp32 output-layer delta (B x d_L, ld_L) to its two bf16 copies
@@ -565,7 +576,7 @@ void delta_h(hf_ctx* c, const float* D, int B, size_t row, size_t tr,
              const int* skip) {
   const int L = c->L;
   cvt_bf16(c->launch(), D, B, c->d[L], c->ld[L], c->H(row), c->ldh[L],
-           c->H(tr), c->ldB, skip);
+           c->H(tr), c->ldB, round64(B), skip);
 }
 
 const bf16_t* act_h(const hf_ctx* c, int l) {       // A_l, row-major
@@ -812,8 +823,8 @@ int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
   const int64_t lim = (int64_t(1) << 31) - 1;
   int64_t n = 0;
   for (int i = 0; i < n_dims; ++i)
-    if (max_batch * (int64_t)round8(dims[i]) > lim ||
-        ((max_batch + 7) & ~int64_t(7)) * dims[i] > lim)
+    if (((max_batch + 255) & ~int64_t(255)) * (int64_t)round64(dims[i]) > lim ||
+        ((max_batch + 63) & ~int64_t(63)) * (int64_t)round256(dims[i]) > lim)
       return HF_EINVAL;
   for (int l = 1; l < n_dims; ++l) n += (int64_t)dims[l] * (dims[l - 1] + 1);
   if (n > lim - 64) return HF_EINVAL;
@@ -824,8 +835,8 @@ int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
   c->ld.resize(n_dims);
   for (int i = 0; i < n_dims; ++i) c->ld[i] = round4(dims[i]);
   c->ldh.resize(n_dims);
-  for (int i = 0; i < n_dims; ++i) c->ldh[i] = round8(dims[i]);
-  c->ldB = round8((int)max_batch);
+  for (int i = 0; i < n_dims; ++i) c->ldh[i] = round64(dims[i]);
+  c->ldB = round64((int)max_batch);
   c->act = act;
   c->prec = prec;
   c->Bmax = max_batch;
@@ -875,6 +886,12 @@ int hf_set_workspace(hf_ctx* c, void* p, size_t bytes) {
   c->ws = reinterpret_cast<char*>(p);
   c->ws_bytes = bytes;
   HIP_TRY(c, hipMemset(c->ws + c->oErr, 0, sizeof(int)));
+  // bf16 operands: the zeros in their padding columns are never rewritten;
+  // wait for them so that no later stream can run ahead of the fill
+  if (c->hend > c->hbeg) {
+    HIP_TRY(c, hipMemset(c->ws + c->hbeg, 0, c->hend - c->hbeg));
+    HIP_TRY(c, hipDeviceSynchronize());
+  }
   return HF_OK;
 }
 

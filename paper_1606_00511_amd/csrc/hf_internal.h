@@ -94,7 +94,10 @@ void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e);
 // uint16_t, rounded to nearest even from fp32), the MFMAs accumulate in fp32
 // and the epilogues compute in fp32.  Every operand is K-contiguous:
 //   X(m, k) = X[m * ldx + k],  Y(n, k) = Y[n * ldy + k]
-// with ldx, ldy multiples of 8 and 16-byte aligned rows.  Modes as above.
+// and the kernels read without bounds checks, so each operand buffer must
+// have: a leading dimension that is a multiple of 64, zeros in columns
+// K .. ld, 256-byte alignment, and rows up to M (or N) rounded up to 256.
+// Modes as above.
 typedef uint16_t bf16_t;
 
 struct GemmShapeH {
@@ -110,8 +113,10 @@ struct GemmShapeH {
 // Epilogue arguments of the bf16-input kernels.  A bf16 result is written
 // twice: row-major to h* (leading dimension ldo) and transposed to t*
 // (t[col * ldt + row]), the batch-contiguous copy the weight gradient
-// contracts over.  fp32 results (logits, RZ, the phi'' cache, weight
-// gradients) go to f* with leading dimension ldf.
+// contracts over; t* also gets zeros in rows M .. (M rounded up to 64).
+// fp32 results (logits, RZ, the phi'' cache, weight gradients) go to f*
+// with leading dimension ldf.  Aux buffers must have rows up to M rounded
+// up to 256 (they are read unchecked and masked).
 struct EpiH {
   int act;
   int hidden;
@@ -148,9 +153,10 @@ void hgemm_rbwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
 void hgemm_gnbwd(const Launch& L, const GemmShapeH& s, const EpiH& e);
 void hgemm_wgrad(const Launch& L, const GemmShapeH& s, const EpiH& e);
 // out[r * ldo + c] = bf16(in[r * ldi + c]), outT[c * ldt + r] = the same
-// (R x C; either output may be null)
+// for r < R and 0 for R <= r < Rpad (R x C; either output may be null)
 void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
-              bf16_t* out, int ldo, bf16_t* outT, int ldt, const int* skip);
+              bf16_t* out, int ldo, bf16_t* outT, int ldt, int Rpad,
+              const int* skip);
 
 // --------------------------------------------------------------- row ops
 // Softmax cross-entropy over rows of Z (B x C, leading dimension ld):
