@@ -37,10 +37,18 @@ Optimization for Deep Neural Network" (arXiv 1606.00511).
   fixed budget (Sec. 2.2).  The CG recurrences are the textbook linear CG
   (Nocedal & Wright, cited in Sec. 1 for line-search Newton-CG).
 
+* One outer iteration of the distributed method on one worker's share
+  (Alg. 2): gradient, solve from 0 or from the warm start eta delta_{k-1},
+  the choice between the solver's step and the negative-curvature direction,
+  Armijo backtracking, and the Hybrid-CG curvature policy (Sec. 3).
+
 Readings where the paper is silent (each also listed in the design notes):
 mean over the batch; biases present; ReLU'(0) = 0; detection on B_k with
-kappa <= 0 (the paper writes "< 0"); x_0 = 0; a relative-residual stop that
-is off by default.
+kappa <= 0 (the paper writes "< 0"); x_0 = 0 unless a warm start is given;
+a relative-residual stop that is off by default; the outer iteration's
+"best descent direction" is the candidate whose Armijo step reaches the
+lower loss, the negative-curvature candidate is rescaled to the length of
+the solver's step, and the Armijo constants are c = 1e-4, shrink 0.5.
 
 Parity pins
 -----------
@@ -271,28 +279,39 @@ def sgn(x):
     return 1.0 if x >= 0.0 else -1.0
 
 
-def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
+def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
+                x0=None):
     """CG-Minimize(B_k, -g_k) with B_k(d) = A d + lam d (Alg. 1 steps 3-4).
 
     Minimises m_k(d) = f + g^T d + d^T B_k d / 2 (Sec. 2.1, eq. (1)) from
-    d = 0.  A conjugate direction p with p^T B_k p <= 0 stops the solve: the
-    current iterate is returned, or -g if it happened at the first iteration
-    (Sec. 2.1, after eq. (1)), together with d~ = -sgn(g^T p) p (Sec. 2.2).
-    ``max_iters`` is the fixed iteration budget (Sec. 2.2).
+    d = 0, or from d = x0 (Alg. 2 allows the warm start eta delta_{k-1}; one
+    extra product forms its residual).  A conjugate direction p with
+    p^T B_k p <= 0 stops the solve: the current iterate is returned, or -g if
+    it happened at the first iteration (Sec. 2.1, after eq. (1)), together
+    with d~ = -sgn(g^T p) p (Sec. 2.2).  ``max_iters`` is the fixed iteration
+    budget (Sec. 2.2); the optional relative stop compares |r|^2 with
+    rel_tol^2 |g|^2.
 
     Returns a dict with step, neg_dir (None if no detection), iters (completed
-    updates of the iterate), products (curvature products evaluated),
-    neg_curv, neg_iter, pBp, pHp, gTd, rr0, rr_final and, if ``record``,
-    the list of per-iteration kappa values and directions.
+    updates of the iterate), products (curvature products evaluated,
+    including the warm start's), neg_curv, neg_iter, pBp, pHp, gTd,
+    rr0 (= |g|^2), rr_final and, if ``record``, the list of per-iteration
+    kappa values and directions.
     """
     g = np.asarray(g, dtype=np.float64)
-    x = np.zeros_like(g)
-    r = g.copy()                 # residual of B x + g
-    p = -g
+    nprod0 = 0
+    if x0 is None:
+        x = np.zeros_like(g)
+        r = g.copy()             # residual of B x + g
+    else:
+        x = np.asarray(x0, dtype=np.float64).copy()
+        r = g + apply_A(x) + lam * x
+        nprod0 = 1
+    p = -r
     rr = float(r @ r)
-    res = dict(step=x, neg_dir=None, iters=0, products=0, neg_curv=0,
-               neg_iter=-1, pBp=0.0, pHp=0.0, gTd=0.0, rr0=rr, rr_final=rr,
-               kappas=[], dirs=[])
+    res = dict(step=x, neg_dir=None, iters=0, products=nprod0, neg_curv=0,
+               neg_iter=-1, pBp=0.0, pHp=0.0, gTd=0.0, rr0=float(g @ g),
+               rr_final=rr, kappas=[], dirs=[])
     if rr == 0.0:
         return res
     for j in range(max_iters):
@@ -301,7 +320,7 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
         if record:
             res["kappas"].append(kappa)
             res["dirs"].append(p.copy())
-        res["products"] = j + 1
+        res["products"] = nprod0 + j + 1
         if kappa <= 0.0:
             d = -sgn(float(g @ p)) * p
             res.update(step=(-g.copy() if j == 0 else x), neg_dir=d,
@@ -323,19 +342,21 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False):
 
 
 def cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-               rel_tol=0.0, record=False):
+               rel_tol=0.0, record=False, x0=None):
     """CG-Minimize with the curvature operator of the network on the fixed
     curvature batch (Xc, yc) (Alg. 2: the product on one minibatch)."""
     def apply_A(p):
         return curvature(dims, act, theta, Xc, yc, p, mode)
-    return cg_minimize(apply_A, g, lam, max_iters, rel_tol, record)
+    return cg_minimize(apply_A, g, lam, max_iters, rel_tol, record, x0)
 
 
 # ----------------------------------------------------------------- Bi-CG-STAB
 def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
-                      store=None):
-    """Bi-CG-STAB (Alg. 3) for B_k d = -g_k, B_k = A + lam I, from d = 0
-    (Alg. 2: the Newton system is solved by Bi-CG-STAB from 0).
+                      store=None, x0=None):
+    """Bi-CG-STAB (Alg. 3) for B_k d = -g_k, B_k = A + lam I, from d = 0 or
+    from d = x0 (Alg. 2: the Newton system is solved by Bi-CG-STAB from 0 or
+    from the warm start eta delta_{k-1}; one extra product forms its
+    residual r0 = -g - B x0).
 
     Each iteration follows the listing's steps in order: alpha from
     (r_j, r0*) / (A p_j, r0*), the half step s_j, the stabilisation
@@ -365,16 +386,22 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
     def B(v):
         return apply_A(v) + lam * v
 
-    x = np.zeros_like(g)
-    r = -g.copy()
+    nprod0 = 0
+    if x0 is None:
+        x = np.zeros_like(g)
+        r = -g.copy()
+    else:
+        x = keep(np.asarray(x0, dtype=np.float64).copy())
+        r = keep(-g - B(x))
+        nprod0 = 1
     rs = r.copy()            # r0*
     p = r.copy()
     rho = float(r @ rs)
-    rr0 = float(r @ r)
-    res = dict(step=x, neg_dir=None, iters=0, products=0, neg_curv=0,
-               neg_iter=-1, dBd=0.0, dHd=0.0, gTd=0.0, rr0=rr0, rr_final=rr0,
-               curvatures=[])
-    if rr0 == 0.0:
+    rr0 = float(g @ g)       # the relative stop is against |b| = |g|
+    res = dict(step=x, neg_dir=None, iters=0, products=nprod0, neg_curv=0,
+               neg_iter=-1, dBd=0.0, dHd=0.0, gTd=0.0, rr0=rr0,
+               rr_final=float(r @ r), curvatures=[])
+    if float(r @ r) == 0.0:
         return res
     for j in range(max_iters):
         Ap = B(p)
@@ -411,8 +438,96 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
 
 
 def bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-                     rel_tol=0.0, record=False, store=None):
+                     rel_tol=0.0, record=False, store=None, x0=None):
     """Bi-CG-STAB with the network's curvature operator on (Xc, yc)."""
     def apply_A(p):
         return curvature(dims, act, theta, Xc, yc, p, mode)
-    return bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol, record, store)
+    return bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol, record, store,
+                             x0)
+
+
+# --------------------------------------------------------- outer iteration
+HESSIAN, GAUSS_NEWTON, HYBRID = "hessian", "gauss_newton", "hybrid"
+
+
+def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
+            lam=1e-2, max_iters=10, rel_tol=0.0, eta=0.0, delta_prev=None,
+            hybrid_g=False, c=1e-4, shrink=0.5, max_backtracks=20):
+    """One iteration of the distributed HF method on one worker's share
+    (Alg. 2, one k), in the paper's order:
+
+    1. f_k and g_k on the batch (X, y).
+    2. The curvature operator on the curvature batch (Xc, yc): the Hessian,
+       the Gauss-Newton matrix, or Hybrid-CG (Sec. 3): the Hessian, except
+       in the iteration right after a Hessian solve met negative curvature,
+       which uses Gauss-Newton (``hybrid_g`` carries that across calls).
+    3. The Newton system solved by CG-Minimize (Alg. 1) or Bi-CG-STAB
+       (Alg. 3) with lambda damping, from 0 or from eta delta_{k-1} (Alg. 2).
+    4. The candidate descent directions (Alg. 2, the step after the solve;
+       Sec. 2.2): the solver's step s_k if g^T s_k < 0, and the oriented
+       negative-curvature direction d~_k if one was met, rescaled to the
+       length of s_k (of g_k when s_k = 0).  Reading: "the best descent
+       direction" is the candidate whose Armijo step gives the lower f.
+    5. For each candidate, Armijo backtracking (Alg. 2): alpha = 1, then
+       alpha <- shrink alpha until f(theta + alpha delta) <= f + c alpha
+       g^T delta, at most ``max_backtracks`` reductions.  c and shrink are
+       not given in the paper (readings: 1e-4 and 0.5).
+    6. theta_{k+1} = theta_k + alpha_k delta_k, or theta_k when no candidate
+       was accepted.
+
+    Returns a dict: theta (new), delta (the chosen direction, zeros when
+    none), f0, f1, alpha, gTd, direction (0 step, 1 negative curvature,
+    -1 none), accepted, evals (loss evaluations in the line searches),
+    mode_used, hybrid_g (the state for the next call), solve (the solver's
+    result dict).
+    """
+    theta = np.asarray(theta, dtype=np.float64)
+    f0, g = loss_grad(dims, act, theta, X, y)
+    if curvature_kind == HYBRID:
+        mode = GAUSS_NEWTON if hybrid_g else HESSIAN
+    else:
+        mode = curvature_kind
+    x0 = None
+    if eta > 0.0 and delta_prev is not None:
+        x0 = eta * np.asarray(delta_prev, dtype=np.float64)
+    if solver == "cg":
+        sol = cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
+                         rel_tol, x0=x0)
+    else:
+        sol = bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters,
+                               mode, rel_tol, x0=x0)
+    s = sol["step"]
+    cands = []
+    if float(g @ s) < 0.0:
+        cands.append((0, s))
+    if sol["neg_curv"]:
+        d = sol["neg_dir"]
+        ns = float(np.linalg.norm(s))
+        target = ns if ns > 0.0 else float(np.linalg.norm(g))
+        nd = float(np.linalg.norm(d))
+        if nd > 0.0:
+            cands.append((1, d * (target / nd)))
+    best = None
+    evals = 0
+    for kind, d in cands:
+        gTd = float(g @ d)
+        alpha = 1.0
+        for b in range(max_backtracks + 1):
+            ft = loss(dims, act, theta + alpha * d, X, y)
+            evals += 1
+            if ft <= f0 + c * alpha * gTd:
+                if best is None or ft < best[3]:
+                    best = (kind, d, alpha, ft, gTd)
+                break
+            alpha *= shrink
+    res = dict(f0=f0, evals=evals, mode_used=mode, solve=sol,
+               hybrid_g=(curvature_kind == HYBRID and mode == HESSIAN
+                         and bool(sol["neg_curv"])))
+    if best is None:
+        res.update(theta=theta.copy(), delta=np.zeros_like(theta), f1=f0,
+                   alpha=0.0, gTd=0.0, direction=-1, accepted=0)
+    else:
+        kind, d, alpha, ft, gTd = best
+        res.update(theta=theta + alpha * d, delta=d, f1=ft, alpha=alpha,
+                   gTd=gTd, direction=kind, accepted=1)
+    return res

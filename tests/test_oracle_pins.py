@@ -526,3 +526,114 @@ def test_planted_wrong_beta_sign_is_caught(monkeypatch):
     exec(compile(bad_src, "bad", "exec"), ns)
     bad = ns["bicgstab_minimize"](lambda p: A @ p, g, 0.05, n)
     assert rel(bad["step"], x) > 1e-3
+
+
+# ------------------------------------------------ warm start, outer iteration
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
+@pytest.mark.parametrize("n,seed", [(6, 0), (11, 1)])
+def test_warm_started_solvers_reach_the_solution(solver, n, seed):
+    """From a random starting point both solvers still solve the damped SPD
+    system (pinned by numpy.linalg.solve), with one extra product for the
+    starting residual."""
+    rng = np.random.default_rng(seed)
+    Q, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    A = (Q * np.geomspace(1.0, 10.0, n)) @ Q.T
+    g = rng.standard_normal(n)
+    x0 = rng.standard_normal(n)
+    lam = 0.05
+    x = np.linalg.solve(A + lam * np.eye(n), -g)
+    if solver == "cg":
+        r = O.cg_minimize(lambda p: A @ p, g, lam, n, x0=x0)
+        assert r["products"] == r["iters"] + 1
+    else:
+        r = O.bicgstab_minimize(lambda p: A @ p, g, lam, 4 * n, rel_tol=1e-13,
+                                x0=x0)
+        assert r["products"] == 2 * r["iters"] + 1
+    assert rel(r["step"], x) <= 1e-9
+    assert r["rr0"] == pytest.approx(g @ g)
+
+
+def test_warm_start_at_the_solution_stays_there():
+    rng = np.random.default_rng(4)
+    n = 7
+    M = rng.standard_normal((n, n))
+    A = M @ M.T + np.eye(n)
+    g = rng.standard_normal(n)
+    x = np.linalg.solve(A + 0.1 * np.eye(n), -g)
+    r = O.cg_minimize(lambda p: A @ p, g, 0.1, 3, x0=x)
+    assert rel(r["step"], x) <= 1e-12
+    assert r["rr_final"] <= 1e-20 * (g @ g)
+
+
+def _explicit_curvature(dims, act, th, X, y, mode):
+    n = th.size
+    return np.stack([O.curvature(dims, act, th, X, y, np.eye(n)[i], mode)
+                     for i in range(n)], axis=1)
+
+
+def test_iterate_takes_the_damped_newton_step_on_a_convex_net():
+    """One weight layer: the objective is convex and H = G is PSD, CG run to
+    convergence solves (H + lambda I) d = -g, and d is what the iteration
+    tries first; the result is checked against the explicitly formed
+    Hessian and numpy.linalg.solve."""
+    dims = (6, 4)
+    p = WL.make_small(dims, "sigmoid", 40, seed=5)
+    th = p["theta"].astype(np.float64)
+    lam = 1e-3
+    n = th.size
+    Hm = _explicit_curvature(dims, "sigmoid", th, p["X"], p["y"], "hessian")
+    _, g = O.loss_grad(dims, "sigmoid", th, p["X"], p["y"])
+    newton = np.linalg.solve(Hm + lam * np.eye(n), -g)
+    r = O.iterate(dims, "sigmoid", th, p["X"], p["y"], p["X"], p["y"],
+                  solver="cg", curvature_kind="hessian", lam=lam,
+                  max_iters=3 * n, rel_tol=1e-12)
+    assert r["solve"]["neg_curv"] == 0
+    assert r["direction"] == 0 and r["accepted"] == 1
+    assert rel(r["delta"], newton) <= 1e-8
+    assert rel(r["theta"], th + r["alpha"] * newton) <= 1e-8
+
+
+@pytest.mark.parametrize("act", ["sigmoid", "tanh", "relu"])
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
+def test_iterate_armijo_descent_and_hybrid_policy(act, solver):
+    """Over several iterations: every accepted step satisfies the Armijo
+    condition with the loss recomputed at the new point, f decreases
+    monotonically, and the Hybrid policy uses Gauss-Newton exactly in the
+    iterations that follow a Hessian solve with negative curvature."""
+    dims = (20, 16, 12, 5)
+    p = WL.make_small(dims, act, 64, seed=3)
+    th = p["theta"].astype(np.float64)
+    hyb, delta, prev = False, None, None
+    for k in range(5):
+        r = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"],
+                      solver=solver, curvature_kind="hybrid", max_iters=6,
+                      eta=0.5, delta_prev=delta, hybrid_g=hyb)
+        expect = "gauss_newton" if (prev is not None and prev["mode_used"] ==
+                                    "hessian" and prev["solve"]["neg_curv"]) \
+            else "hessian"
+        assert r["mode_used"] == expect
+        if r["accepted"]:
+            f_new = O.loss(dims, act, r["theta"], p["X"], p["y"])
+            assert f_new == pytest.approx(r["f1"], rel=1e-12)
+            assert f_new <= r["f0"] + 1e-4 * r["alpha"] * r["gTd"]
+            assert r["gTd"] < 0.0 and r["f1"] < r["f0"]
+        th, delta, hyb, prev = r["theta"], r["delta"], r["hybrid_g"], r
+
+
+def test_planted_uphill_step_is_caught(monkeypatch):
+    """A sign error that walks along +g instead of the solver's step would
+    fail the Armijo test above: the planted iteration never accepts."""
+    dims = (20, 16, 12, 5)
+    p = WL.make_small(dims, "tanh", 64, seed=3)
+    th = p["theta"].astype(np.float64)
+    real_cg = O.cg_network
+
+    def uphill(*a, **k):
+        r = real_cg(*a, **k)
+        _, g = O.loss_grad(dims, "tanh", th, p["X"], p["y"])
+        r = dict(r, step=g.copy(), neg_curv=0, neg_dir=None)
+        return r
+    monkeypatch.setattr(O, "cg_network", uphill)
+    r = O.iterate(dims, "tanh", th, p["X"], p["y"], p["X"], p["y"])
+    assert r["accepted"] == 0 and r["direction"] == -1
+    assert r["f1"] == r["f0"]
