@@ -45,8 +45,11 @@ typedef struct hf_ctx hf_ctx;
 
 /* Hidden-layer activation; the output layer is always softmax. */
 enum { HF_SIGMOID = 0, HF_TANH = 1, HF_RELU = 2 };
-/* Curvature matrix for hf_hvp / hf_cg. */
-enum { HF_HESSIAN = 0, HF_GAUSS_NEWTON = 1 };
+/* Curvature matrix for hf_hvp / hf_cg / hf_bicgstab; hf_iterate also takes
+ * HF_HYBRID (the Hybrid-CG policy of Sec. 3). */
+enum { HF_HESSIAN = 0, HF_GAUSS_NEWTON = 1, HF_HYBRID = 2 };
+/* Newton-system solver of hf_iterate. */
+enum { HF_SOLVER_CG = 0, HF_SOLVER_BICGSTAB = 1 };
 /* Arithmetic of the GEMMs (every other step is fp32, reductions fp64):
  *   HF_FP32         fp32 operands, fp32 MFMA, fp32 accumulation;
  *   HF_BF16_INPUTS  every GEMM operand (X, W, v, the activations and deltas
@@ -189,6 +192,69 @@ int hf_bicgstab(hf_ctx* ctx, const float* W, const float* Xc, const int32_t* yc,
                 int64_t Bc, const float* g, float damping, int32_t max_iters,
                 float rel_tol, int32_t mode, float* step, float* neg_dir,
                 hf_cg_info* info);
+
+/*
+ * hf_loss: the objective alone, f = (1/B) sum_i [logsumexp(z_i) - z_{i,y_i}]
+ * at theta = W on the batch (X, y) of B rows (the forward pass only; the
+ * line search of Alg. 2 evaluates it at trial points).
+ *   loss  device, 1 fp32.  Asynchronous; labels checked as in hf_loss_grad.
+ */
+int hf_loss(hf_ctx* ctx, const float* W, const float* X, const int32_t* y,
+            int64_t B, float* loss);
+
+/* Parameters of hf_iterate (host struct). */
+typedef struct hf_iter_params {
+  int32_t solver;         /* HF_SOLVER_CG or HF_SOLVER_BICGSTAB              */
+  int32_t curvature;      /* HF_HESSIAN, HF_GAUSS_NEWTON or HF_HYBRID         */
+  float damping;          /* lambda >= 0                                      */
+  int32_t max_iters;      /* solver iteration budget >= 0 (Sec. 2.2)         */
+  float rel_tol;          /* relative residual stop against |g|, 0 = off     */
+  float eta;              /* warm start x0 = eta * delta; 0 starts from 0    */
+  float armijo_c;         /* c of the Armijo condition, in (0, 1)            */
+  float shrink;           /* step reduction per rejected trial, in (0, 1)    */
+  int32_t max_backtracks; /* reductions tried per candidate, >= 0            */
+} hf_iter_params;
+
+/* Result of hf_iterate (host struct). */
+typedef struct hf_iter_info {
+  hf_cg_info solve;       /* the solve; products include the warm start's   */
+  int32_t mode_used;      /* HF_HESSIAN or HF_GAUSS_NEWTON                    */
+  int32_t direction;      /* 0 the solver's step, 1 the negative-curvature
+                             direction, -1 no candidate accepted            */
+  int32_t accepted;       /* 1 if a step satisfied the Armijo condition      */
+  int32_t evals;          /* objective evaluations in the line searches      */
+  double f0, f1;          /* f before and after (f1 = f0 if none accepted)   */
+  double alpha;           /* accepted step length, 0 if none                */
+  double gTd;             /* g^T delta for the chosen direction             */
+} hf_iter_info;
+
+/*
+ * hf_iterate: one iteration of the distributed HF method on one worker's
+ * share (Alg. 2, one k; Alg. 1):
+ *   1. f and g at theta = W on the batch (X, y) of B rows;
+ *   2. the curvature on the batch (Xc, yc) of Bc rows: H, G, or HF_HYBRID:
+ *      H, except in the iteration right after a Hessian solve that met
+ *      negative curvature, which uses G (Sec. 3); *hybrid_state carries
+ *      this between calls (in/out, 0 initially; ignored otherwise);
+ *   3. the Newton system (A + lambda I) d = -g by CG-Minimize (Alg. 1) or
+ *      Bi-CG-STAB (Alg. 3), from 0 or from eta * delta (Alg. 2);
+ *   4. the candidate directions (Sec. 2.2): the solver's step if
+ *      g^T step < 0, and the oriented negative-curvature direction if one
+ *      was met, rescaled to the step's length (to |g| if the step is 0);
+ *   5. for each candidate, Armijo backtracking (Alg. 2): alpha = 1, then
+ *      alpha *= shrink until f(W + alpha d) <= f + c alpha g^T d, at most
+ *      max_backtracks reductions; the candidate reaching the lower f wins;
+ *   6. W += alpha d in place, and delta = d (zeros if none was accepted).
+ *   W      device, n fp32, in/out.  X, y / Xc, yc as for hf_loss_grad /
+ *          hf_cg (yc may be NULL only for HF_GAUSS_NEWTON).
+ *   delta  device, n fp32, in/out: delta_{k-1} in, delta_k out.
+ * The objective values that decide the line search are reduced in fp64.
+ * Synchronises the stream; uses the workspace's solver vectors.
+ */
+int hf_iterate(hf_ctx* ctx, float* W, const float* X, const int32_t* y,
+               int64_t B, const float* Xc, const int32_t* yc, int64_t Bc,
+               const hf_iter_params* params, int32_t* hybrid_state,
+               float* delta, hf_iter_info* info);
 
 /* Synchronise the stream and report a device-detected error (HF_ELABEL)
  * raised since the last hf_check; clears the flag. */

@@ -478,8 +478,8 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
     Returns a dict: theta (new), delta (the chosen direction, zeros when
     none), f0, f1, alpha, gTd, direction (0 step, 1 negative curvature,
     -1 none), accepted, evals (loss evaluations in the line searches),
-    mode_used, hybrid_g (the state for the next call), solve (the solver's
-    result dict).
+    trials (kind, alpha, f, Armijo bound) of every evaluation, mode_used,
+    hybrid_g (the state for the next call), solve (the solver's result).
     """
     theta = np.asarray(theta, dtype=np.float64)
     f0, g = loss_grad(dims, act, theta, X, y)
@@ -509,18 +509,20 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
             cands.append((1, d * (target / nd)))
     best = None
     evals = 0
+    trials = []
     for kind, d in cands:
         gTd = float(g @ d)
         alpha = 1.0
         for b in range(max_backtracks + 1):
             ft = loss(dims, act, theta + alpha * d, X, y)
             evals += 1
+            trials.append((kind, alpha, ft, f0 + c * alpha * gTd))
             if ft <= f0 + c * alpha * gTd:
                 if best is None or ft < best[3]:
                     best = (kind, d, alpha, ft, gTd)
                 break
             alpha *= shrink
-    res = dict(f0=f0, evals=evals, mode_used=mode, solve=sol,
+    res = dict(f0=f0, evals=evals, trials=trials, mode_used=mode, solve=sol,
                hybrid_g=(curvature_kind == HYBRID and mode == HESSIAN
                          and bool(sol["neg_curv"])))
     if best is None:

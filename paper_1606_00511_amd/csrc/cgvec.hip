@@ -81,43 +81,47 @@ extern "C" __global__ void hf_cg_reset(CgState* __restrict__ st) {
   }
 }
 
-// x = 0, r = g, p = -g, d~ = 0, partials of g.g
+// From x0 = 0: x = 0, r = g, p = -g.  From a warm start x0 (with q = A x0):
+// x = x0, r = g + q + lambda x0 (the gradient of the model at x0), p = -r.
+// d~ = 0.  Partials of r.r and of g.g (the relative stop is against |g|).
 extern "C" __global__ __launch_bounds__(256) void hf_cg_init(
-    const float* __restrict__ g, float* __restrict__ x, float* __restrict__ r,
-    float* __restrict__ p, float* __restrict__ nd, long long n,
-    double* __restrict__ part) {
+    const float* __restrict__ g, const float* __restrict__ x0,
+    const float* __restrict__ q, double lambda, float* __restrict__ x,
+    float* __restrict__ r, float* __restrict__ p, float* __restrict__ nd,
+    long long n, double* __restrict__ part_rr, double* __restrict__ part_gg) {
   __shared__ double sh[4];
-  const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  double s = 0.0;
-  const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
-  for (long long i = t0; i < n4; i += stride) {
-    const f32x4 gv = ((const f32x4*)g)[i];
-    ((f32x4*)x)[i] = z4;
-    ((f32x4*)r)[i] = gv;
-    ((f32x4*)p)[i] = -gv;
-    ((f32x4*)nd)[i] = z4;
-    s += dot4(gv, gv);
-  }
-  for (long long i = n4 * 4 + t0; i < n; i += stride) {
+  double srr = 0.0, sgg = 0.0;
+  for (long long i = t0; i < n; i += stride) {
     const float gv = g[i];
-    x[i] = 0.f; r[i] = gv; p[i] = -gv; nd[i] = 0.f;
-    s += (double)gv * gv;
+    float xv = 0.f, rv = gv;
+    if (x0) {
+      xv = x0[i];
+      rv = (float)((double)gv + (double)q[i] + lambda * (double)xv);
+    }
+    x[i] = xv; r[i] = rv; p[i] = -rv; nd[i] = 0.f;
+    srr += (double)rv * rv;
+    sgg += (double)gv * gv;
   }
-  s = block_sum(s, sh);
-  if (threadIdx.x == 0) part[blockIdx.x] = s;
+  srr = block_sum(srr, sh);
+  sgg = block_sum(sgg, sh);
+  if (threadIdx.x == 0) {
+    part_rr[blockIdx.x] = srr;
+    part_gg[blockIdx.x] = sgg;
+  }
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_init_fin(
-    const double* __restrict__ part, int nb, double lambda, double tol2,
-    CgState* __restrict__ st) {
+    const double* __restrict__ part_rr, const double* __restrict__ part_gg,
+    int nb, double lambda, double tol2, CgState* __restrict__ st) {
   __shared__ double sh[4];
-  const double rr = total(part, nb, sh);
+  const double rr = total(part_rr, nb, sh);
+  const double gg = total(part_gg, nb, sh);
   if (threadIdx.x == 0) {
     st->rr[0] = rr;
     st->rr[1] = rr;
-    st->rr0 = rr;
+    st->rr0 = gg;
     st->lambda = lambda;
     st->tol2 = tol2;
     st->neg_iter = -1;
@@ -305,17 +309,18 @@ int cg_grid(long long n) {
 
 int cg_part_doubles() { return 10 * MAX_GRID; }
 
-void cg_init(const Launch& L, const float* g, float* x, float* r, float* p,
-             float* neg_dir, long long n, double lambda, double tol2,
-             double* part, CgState* st) {
+void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
+             float* x, float* r, float* p, float* neg_dir, long long n,
+             double lambda, double tol2, double* part, CgState* st) {
   const int nb = cg_grid(n);
   hipLaunchKernelGGL(hf_cg_reset, dim3(1), dim3(64), 0, L.stream, st);
   prof_begin(L, "hf_cg_init");
-  hipLaunchKernelGGL(hf_cg_init, dim3(nb), dim3(NT), 0, L.stream, g, x, r, p,
-                     neg_dir, n, part + 4 * MAX_GRID);
-  prof_end(L, "hf_cg_init", 0.0, 5.0 * 4.0 * n);
+  hipLaunchKernelGGL(hf_cg_init, dim3(nb), dim3(NT), 0, L.stream, g, x0, q,
+                     lambda, x, r, p, neg_dir, n, part + 4 * MAX_GRID,
+                     part + 5 * MAX_GRID);
+  prof_end(L, "hf_cg_init", 0.0, (x0 ? 7.0 : 5.0) * 4.0 * n);
   hipLaunchKernelGGL(hf_cg_init_fin, dim3(1), dim3(NT), 0, L.stream,
-                     part + 4 * MAX_GRID, nb, lambda, tol2, st);
+                     part + 4 * MAX_GRID, part + 5 * MAX_GRID, nb, lambda, tol2, st);
 }
 
 void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
@@ -367,7 +372,7 @@ namespace {
 constexpr int PA = 0;                 // (Ap, r0*)
 constexpr int PB = 1 * MAX_GRID;      // (s, t), (t, t)
 constexpr int PC = 3 * MAX_GRID;      // five dots of bicg_update
-constexpr int PI = 8 * MAX_GRID;      // (g, g) of the init
+constexpr int PI = 8 * MAX_GRID;      // (r0, r0) and (g, g) of the init
 }  // namespace
 
 extern "C" __global__ void hf_bicg_reset(BicgState* __restrict__ st) {
@@ -377,32 +382,35 @@ extern "C" __global__ void hf_bicg_reset(BicgState* __restrict__ st) {
   }
 }
 
+// From 0: x = 0, r = r0* = p = -g.  From a warm start x0 (q = A x0):
+// x = x0, r = r0* = p = -g - (q + lambda x0).  d~ = 0.  Partials of r.r
+// (= (r0, r0*)) and of g.g (the relative stop is against |g|).
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_init(
-    const float* __restrict__ g, float* __restrict__ x, float* __restrict__ r,
-    float* __restrict__ rs, float* __restrict__ p, float* __restrict__ nd,
-    long long n, double* __restrict__ part) {
+    const float* __restrict__ g, const float* __restrict__ x0,
+    const float* __restrict__ q, double lambda, float* __restrict__ x,
+    float* __restrict__ r, float* __restrict__ rs, float* __restrict__ p,
+    float* __restrict__ nd, long long n, double* __restrict__ part) {
   __shared__ double sh[4];
-  const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  double s = 0.0;
-  const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
-  for (long long i = t0; i < n4; i += stride) {
-    const f32x4 gv = ((const f32x4*)g)[i];
-    ((f32x4*)x)[i] = z4;
-    ((f32x4*)r)[i] = -gv;
-    ((f32x4*)rs)[i] = -gv;
-    ((f32x4*)p)[i] = -gv;
-    ((f32x4*)nd)[i] = z4;
-    s += dot4(gv, gv);
-  }
-  for (long long i = n4 * 4 + t0; i < n; i += stride) {
+  double srr = 0.0, sgg = 0.0;
+  for (long long i = t0; i < n; i += stride) {
     const float gv = g[i];
-    x[i] = 0.f; r[i] = -gv; rs[i] = -gv; p[i] = -gv; nd[i] = 0.f;
-    s += (double)gv * gv;
+    float xv = 0.f, rv = -gv;
+    if (x0) {
+      xv = x0[i];
+      rv = (float)(-(double)gv - ((double)q[i] + lambda * (double)xv));
+    }
+    x[i] = xv; r[i] = rv; rs[i] = rv; p[i] = rv; nd[i] = 0.f;
+    srr += (double)rv * rv;
+    sgg += (double)gv * gv;
   }
-  s = block_sum(s, sh);
-  if (threadIdx.x == 0) part[PI + blockIdx.x] = s;
+  srr = block_sum(srr, sh);
+  sgg = block_sum(sgg, sh);
+  if (threadIdx.x == 0) {
+    part[PI + blockIdx.x] = srr;
+    part[PI + MAX_GRID + blockIdx.x] = sgg;
+  }
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_init_fin(
@@ -410,9 +418,10 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_init_fin(
     BicgState* __restrict__ st) {
   __shared__ double sh[4];
   const double rr = total(part + PI, nb, sh);
+  const double gg = total(part + PI + MAX_GRID, nb, sh);
   if (threadIdx.x == 0) {
-    st->rho[0] = rr;          // (r0, r0*) = |g|^2
-    st->rr0 = rr;
+    st->rho[0] = rr;          // (r0, r0*) = |r0|^2
+    st->rr0 = gg;
     st->rr = rr;
     st->lambda = lambda;
     st->tol2 = tol2;
@@ -648,15 +657,16 @@ void axpy(const Launch& L, float* y, const float* x, float a, long long n,
   prof_end(L, "hf_axpy", 0.0, 3.0 * 4.0 * n);
 }
 
-void bicg_init(const Launch& L, const float* g, float* x, float* r, float* rs,
-               float* p, float* neg_dir, long long n, double lambda,
-               double tol2, double* part, BicgState* st) {
+void bicg_init(const Launch& L, const float* g, const float* x0,
+               const float* q, float* x, float* r, float* rs, float* p,
+               float* neg_dir, long long n, double lambda, double tol2,
+               double* part, BicgState* st) {
   const int nb = cg_grid(n);
   hipLaunchKernelGGL(hf_bicg_reset, dim3(1), dim3(64), 0, L.stream, st);
   prof_begin(L, "hf_bicg_init");
-  hipLaunchKernelGGL(hf_bicg_init, dim3(nb), dim3(NT), 0, L.stream, g, x, r, rs,
-                     p, neg_dir, n, part);
-  prof_end(L, "hf_bicg_init", 0.0, 6.0 * 4.0 * n);
+  hipLaunchKernelGGL(hf_bicg_init, dim3(nb), dim3(NT), 0, L.stream, g, x0, q,
+                     lambda, x, r, rs, p, neg_dir, n, part);
+  prof_end(L, "hf_bicg_init", 0.0, (x0 ? 8.0 : 6.0) * 4.0 * n);
   hipLaunchKernelGGL(hf_bicg_init_fin, dim3(1), dim3(NT), 0, L.stream, part, nb,
                      lambda, tol2, st);
 }
@@ -696,6 +706,73 @@ void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
   hipLaunchKernelGGL(hf_bicg_negw, dim3(nb), dim3(NT), 0, L.stream, x, neg_dir,
                      n, j, st);
   prof_end(L, "hf_bicg_negw", 0.0, 2.0 * 4.0 * n);
+}
+
+
+// ============================================================ outer step
+// out = w + a d (w may be null: out = a d), applied in fp64
+extern "C" __global__ __launch_bounds__(256) void hf_waxpy(
+    float* __restrict__ out, const float* __restrict__ w, double a,
+    const float* __restrict__ d, long long n) {
+  const long long stride = (long long)gridDim.x * NT;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride)
+    out[i] = (float)((w ? (double)w[i] : 0.0) + a * (double)d[i]);
+}
+
+// per-block partials of the four dot products a_k . b_k
+extern "C" __global__ __launch_bounds__(256) void hf_dots4(
+    const float* __restrict__ a0, const float* __restrict__ b0,
+    const float* __restrict__ a1, const float* __restrict__ b1,
+    const float* __restrict__ a2, const float* __restrict__ b2,
+    const float* __restrict__ a3, const float* __restrict__ b3, long long n,
+    double* __restrict__ part) {
+  __shared__ double sh[4];
+  const long long stride = (long long)gridDim.x * NT;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride) {
+    s0 += (double)a0[i] * b0[i];
+    s1 += (double)a1[i] * b1[i];
+    s2 += (double)a2[i] * b2[i];
+    s3 += (double)a3[i] * b3[i];
+  }
+  s0 = block_sum(s0, sh);
+  s1 = block_sum(s1, sh);
+  s2 = block_sum(s2, sh);
+  s3 = block_sum(s3, sh);
+  if (threadIdx.x == 0) {
+    part[blockIdx.x] = s0;
+    part[MAX_GRID + blockIdx.x] = s1;
+    part[2 * MAX_GRID + blockIdx.x] = s2;
+    part[3 * MAX_GRID + blockIdx.x] = s3;
+  }
+}
+
+// out[k] = sum of the partials of dot k, in block order
+extern "C" __global__ __launch_bounds__(256) void hf_dots4_fin(
+    const double* __restrict__ part, int nb, double* __restrict__ out) {
+  __shared__ double sh[4];
+  for (int k = 0; k < 4; ++k) {
+    const double t = total(part + k * MAX_GRID, nb, sh);
+    if (threadIdx.x == 0) out[k] = t;
+  }
+}
+
+void waxpy(const Launch& L, float* out, const float* w, double a,
+           const float* d, long long n) {
+  const int nb = cg_grid(n);
+  prof_begin(L, "hf_waxpy");
+  hipLaunchKernelGGL(hf_waxpy, dim3(nb), dim3(NT), 0, L.stream, out, w, a, d, n);
+  prof_end(L, "hf_waxpy", 0.0, (w ? 3.0 : 2.0) * 4.0 * n);
+}
+
+void dots4(const Launch& L, const float* const a[4], const float* const b[4],
+           long long n, double* part, double* out) {
+  const int nb = cg_grid(n);
+  prof_begin(L, "hf_dots4");
+  hipLaunchKernelGGL(hf_dots4, dim3(nb), dim3(NT), 0, L.stream, a[0], b[0], a[1],
+                     b[1], a[2], b[2], a[3], b[3], n, part);
+  prof_end(L, "hf_dots4", 0.0, 8.0 * 4.0 * n);
+  hipLaunchKernelGGL(hf_dots4_fin, dim3(1), dim3(NT), 0, L.stream, part, nb, out);
 }
 
 }  // namespace hfk

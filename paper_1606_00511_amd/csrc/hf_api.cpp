@@ -192,6 +192,9 @@ struct hf_ctx {
   size_t hX = 0, hXT = 0;
   std::vector<size_t> hW, hWT, hV, hVT, hA, hAT, hRA, hRAT, hD, hDT, hRD, hRDT;
   size_t oS = 0, oT = 0, oRs = 0;    // Bi-CG-STAB: s, t = B s, r0*
+  // outer iteration: gradient, solver step and direction, warm start,
+  // trial weights, and device scalars (4 dot products, the fp64 loss)
+  size_t oG = 0, oStep = 0, oNd = 0, oX0 = 0, oWt = 0, oScal = 0;
   size_t oZ = 0, oP = 0, oSplit = 0, oBpart = 0, oR = 0, oPv = 0, oQ = 0,
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
   int max_splits = 16;
@@ -331,6 +334,12 @@ void plan(hf_ctx* c) {
   c->oS = take(nv * f4);
   c->oT = take(nv * f4);
   c->oRs = take(nv * f4);
+  c->oG = take(nv * f4);
+  c->oStep = take(nv * f4);
+  c->oNd = take(nv * f4);
+  c->oX0 = take(nv * f4);
+  c->oWt = take(nv * f4);
+  c->oScal = take(8 * sizeof(double));
   c->oRed = take((size_t)cg_part_doubles() * sizeof(double));
   c->oLoss = take(((B + 3) / 4) * sizeof(double));
   c->oState = take(sizeof(CgState) > sizeof(BicgState) ? sizeof(CgState)
@@ -766,17 +775,6 @@ void hvp_h(hf_ctx* c, const float* W, const float* X, const int32_t* y, int B,
   for (int l = L; l >= 1; --l) rbackward_h(c, l, B, mode, true, out, nullptr);
 }
 
-void loss_grad_h(hf_ctx* c, const float* W, const float* X, const int32_t* y,
-                 int B, float* loss, float* grad) {
-  forward_plain_h(c, W, X, B, y, true);
-  loss_finalize(c->launch(), c->Dp(c->oLoss), (B + 3) / 4, B, loss);
-  for (int l = c->L; l >= 1; --l) {
-    wgrad_h(c, l, B, c->H(c->hDT[l]), act_ht(c, l - 1), nullptr, nullptr,
-            grad, nullptr);
-    if (l > 1) backward_data_h(c, l, B, false);
-  }
-}
-
 // ------------------------------------------------ precision dispatch
 // The cache of a solve on the curvature batch: forward pass, p and, for the
 // Hessian, delta_l and (delta_l W_l) phi''(A_{l-1}).
@@ -803,6 +801,204 @@ void product(hf_ctx* c, const float* W, const float* X, int B, const float* v,
 void lambda_axpy(hf_ctx* c, float* q, const float* v, float lambda,
                  const int* skip) {
   if (lambda != 0.0f) axpy(c->launch(), q, v, lambda, c->n, skip);
+}
+
+}  // namespace
+
+namespace {
+
+// f on B rows (forward pass only) into loss (fp32) and/or loss64 (fp64)
+void loss_only(hf_ctx* c, const float* W, const float* X, const int32_t* y,
+               int B, float* loss, double* loss64) {
+  if (c->bf16()) forward_plain_h(c, W, X, B, y, false);
+  else forward_plain(c, W, X, B, y, false);
+  loss_finalize(c->launch(), c->Dp(c->oLoss), (B + 3) / 4, B, loss, loss64);
+}
+
+// f and g on B rows (arguments already checked)
+void loss_grad_any(hf_ctx* c, const float* W, const float* X, const int32_t* y,
+                   int b, float* loss, double* loss64, float* grad) {
+  if (c->bf16()) {
+    forward_plain_h(c, W, X, b, y, true);
+    loss_finalize(c->launch(), c->Dp(c->oLoss), (b + 3) / 4, b, loss, loss64);
+    for (int l = c->L; l >= 1; --l) {
+      wgrad_h(c, l, b, c->H(c->hDT[l]), act_ht(c, l - 1), nullptr, nullptr,
+              grad, nullptr);
+      if (l > 1) backward_data_h(c, l, b, false);
+    }
+    return;
+  }
+  forward_plain(c, W, X, b, y, true);
+  loss_finalize(c->launch(), c->Dp(c->oLoss), (b + 3) / 4, b, loss, loss64);
+  for (int l = c->L; l >= 1; --l) {
+    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
+    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
+    wgrad(c, l, b, c->F(c->oD[l]), Ain, nullptr, nullptr, ldin, grad, nullptr);
+    if (l > 1) backward_data(c, W, l, b, false);
+  }
+}
+
+}  // namespace
+
+namespace {
+
+// CG-Minimize after argument checks; x0 (device, may be null) is the warm
+// start of Alg. 2
+int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
+             int b, const float* g, float damping, int32_t max_iters,
+             float rel_tol, int32_t mode, const float* x0, float* step,
+             float* neg_dir, hf_cg_info* info) {
+  std::memset(info, 0, sizeof *info);
+  if (!c->pinned) {
+    HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
+  }
+  if (c->prof) c->prof->solve_begin = c->prof->pending.size();
+  const Launch Lc = c->launch();
+  const long long n = c->n;
+  const bool hess = mode == HF_HESSIAN;
+  CgState* st = reinterpret_cast<CgState*>(c->ws + c->oState);
+  const int* skip = &st->done;
+  double* part = c->Dp(c->oRed);
+  float* r = c->F(c->oR);
+  float* p = c->F(c->oPv);
+  float* q = c->F(c->oQ);
+
+  // cache of the curvature batch: activations, p, delta_l, E2_l
+  build_cache(c, W, Xc, b, yc, hess);
+  // a warm start's residual needs one product on the cache
+  if (x0) product(c, W, Xc, b, x0, mode, q, nullptr);
+  cg_init(Lc, g, x0, x0 ? q : nullptr, step, r, p, neg_dir, n, (double)damping,
+          (double)rel_tol * (double)rel_tol, part, st);
+  for (int j = 0; j < max_iters; ++j) {
+    if (c->prof) c->prof->tag = j;
+    product(c, W, Xc, b, p, mode, q, skip);
+    cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st);
+    // Stop enqueueing once the device reports `done` for the previous
+    // iteration; the work already queued for this one returns at once.
+    HIP_TRY(c, hipMemcpyAsync(&c->pinned[j & 1], st, sizeof(CgState),
+                              hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
+    if (j >= 1) {
+      HIP_TRY(c, hipEventSynchronize(c->ev[(j - 1) & 1]));
+      if (c->pinned[(j - 1) & 1].done) break;
+    }
+  }
+  if (c->prof) c->prof->tag = -1;
+  HIP_TRY(c, hipGetLastError());
+  HIP_TRY(c, hipMemcpyAsync(&c->pinned[0], st, sizeof(CgState),
+                            hipMemcpyDeviceToHost, c->stream));
+  int errflag = 0;
+  HIP_TRY(c, hipMemcpyAsync(&errflag, c->ws + c->oErr, sizeof(int),
+                            hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const CgState& s = c->pinned[0];
+  if (c->prof)
+    c->prof->retract(s.products - 1, s.neg || (s.status && s.iters < s.products),
+                     s.neg ? s.neg_iter : -1);
+  info->iters = s.iters;
+  info->products = s.products + (x0 ? 1 : 0);
+  info->neg_curv = s.neg;
+  info->neg_iter = s.neg ? s.neg_iter : -1;
+  info->pBp = s.neg ? s.kappa : 0.0;
+  info->pHp = s.neg ? s.pq : 0.0;
+  info->gTd = s.neg ? (s.gp >= 0.0 ? -s.gp : s.gp) : 0.0;
+  info->rr0 = s.rr0;
+  info->rr_final = s.rr[s.iters & 1];
+  info->status = s.status;
+  if (errflag) {
+    info->status = HF_ELABEL;
+    int zero = 0;
+    HIP_TRY(c, hipMemcpy(c->ws + c->oErr, &zero, sizeof(int), hipMemcpyHostToDevice));
+    return fail(c, HF_ELABEL, "a label outside [0, %d) was seen", c->d[c->L]);
+  }
+  if (s.status) return fail(c, HF_ENUMERIC, "non-finite CG scalar");
+  return HF_OK;
+}
+
+// Bi-CG-STAB after argument checks; x0 (device, may be null) is the warm
+// start of Alg. 2
+int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
+               int b, const float* g, float damping, int32_t max_iters,
+               float rel_tol, int32_t mode, const float* x0, float* step,
+               float* neg_dir, hf_cg_info* info) {
+  std::memset(info, 0, sizeof *info);
+  if (!c->pinned) {
+    HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
+  }
+  BicgState* hostst = reinterpret_cast<BicgState*>(c->pinned_bicg);
+  if (!hostst) {
+    HIP_TRY(c, hipHostMalloc((void**)&c->pinned_bicg, 2 * sizeof(BicgState),
+                             hipHostMallocDefault));
+    hostst = reinterpret_cast<BicgState*>(c->pinned_bicg);
+  }
+  if (c->prof) c->prof->solve_begin = c->prof->pending.size();
+  const Launch Lc = c->launch();
+  const long long n = c->n;
+  const bool hess = mode == HF_HESSIAN;
+  BicgState* st = reinterpret_cast<BicgState*>(c->ws + c->oState);
+  const int* skip = &st->done;
+  double* part = c->Dp(c->oRed);
+  float* r = c->F(c->oR);
+  float* p = c->F(c->oPv);
+  float* Ap = c->F(c->oQ);
+  float* sv = c->F(c->oS);
+  float* t = c->F(c->oT);
+  float* rs = c->F(c->oRs);
+
+  build_cache(c, W, Xc, b, yc, hess);
+  // a warm start's residual needs one product on the cache
+  if (x0) product(c, W, Xc, b, x0, mode, Ap, nullptr);
+  bicg_init(Lc, g, x0, x0 ? Ap : nullptr, step, r, rs, p, neg_dir, n,
+            (double)damping, (double)rel_tol * (double)rel_tol, part, st);
+  for (int j = 0; j < max_iters; ++j) {
+    if (c->prof) c->prof->tag = 2 * j;
+    product(c, W, Xc, b, p, mode, Ap, skip);
+    lambda_axpy(c, Ap, p, damping, skip);
+    bicg_half(Lc, r, rs, Ap, sv, n, j, part, st);
+    if (c->prof) c->prof->tag = 2 * j + 1;
+    product(c, W, Xc, b, sv, mode, t, skip);
+    lambda_axpy(c, t, sv, damping, skip);
+    bicg_rest(Lc, step, r, rs, p, Ap, sv, t, g, neg_dir, n, j, part, st);
+    HIP_TRY(c, hipMemcpyAsync(&hostst[j & 1], st, sizeof(BicgState),
+                              hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
+    if (j >= 1) {
+      HIP_TRY(c, hipEventSynchronize(c->ev[(j - 1) & 1]));
+      if (hostst[(j - 1) & 1].done) break;
+    }
+  }
+  if (c->prof) c->prof->tag = -1;
+  HIP_TRY(c, hipGetLastError());
+  HIP_TRY(c, hipMemcpyAsync(&hostst[0], st, sizeof(BicgState),
+                            hipMemcpyDeviceToHost, c->stream));
+  int errflag = 0;
+  HIP_TRY(c, hipMemcpyAsync(&errflag, c->ws + c->oErr, sizeof(int),
+                            hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const BicgState& s = hostst[0];
+  if (c->prof) c->prof->retract_bicg(s.products, s.neg ? s.neg_iter : -1);
+  info->iters = s.iters;
+  info->products = s.products + (x0 ? 1 : 0);
+  info->neg_curv = s.neg;
+  info->neg_iter = s.neg ? s.neg_iter : -1;
+  info->pBp = s.neg ? s.dBd : 0.0;
+  info->pHp = s.neg ? s.dHd : 0.0;
+  info->gTd = s.neg ? s.gTd : 0.0;
+  info->rr0 = s.rr0;
+  info->rr_final = s.rr;
+  info->status = s.status;
+  if (errflag) {
+    info->status = HF_ELABEL;
+    int zero = 0;
+    HIP_TRY(c, hipMemcpy(c->ws + c->oErr, &zero, sizeof(int), hipMemcpyHostToDevice));
+    return fail(c, HF_ELABEL, "a label outside [0, %d) was seen", c->d[c->L]);
+  }
+  if (s.status) return fail(c, HF_ENUMERIC, "non-finite Bi-CG-STAB scalar");
+  return HF_OK;
 }
 
 }  // namespace
@@ -904,21 +1100,21 @@ int hf_loss_grad(hf_ctx* c, const float* W, const float* X, const int32_t* y,
     return rc;
   if (!y) return fail(c, HF_EINVAL, "y is NULL");
   if (!loss) return fail(c, HF_EINVAL, "loss is NULL");
-  const Launch Lc = c->launch();
-  const int b = (int)B;
-  if (c->bf16()) {
-    loss_grad_h(c, W, X, y, b, loss, grad);
-    HIP_TRY(c, hipGetLastError());
-    return HF_OK;
-  }
-  forward_plain(c, W, X, b, y, true);
-  loss_finalize(Lc, c->Dp(c->oLoss), (b + 3) / 4, b, loss);
-  for (int l = c->L; l >= 1; --l) {
-    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
-    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
-    wgrad(c, l, b, c->F(c->oD[l]), Ain, nullptr, nullptr, ldin, grad, nullptr);
-    if (l > 1) backward_data(c, W, l, b, false);
-  }
+  loss_grad_any(c, W, X, y, (int)B, loss, nullptr, grad);
+  HIP_TRY(c, hipGetLastError());
+  return HF_OK;
+}
+
+int hf_loss(hf_ctx* c, const float* W, const float* X, const int32_t* y,
+            int64_t B, float* loss) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, X, "X")) ||
+      (rc = check_batch(c, B)))
+    return rc;
+  if (!y) return fail(c, HF_EINVAL, "y is NULL");
+  if (!loss) return fail(c, HF_EINVAL, "loss is NULL");
+  loss_only(c, W, X, y, (int)B, loss, nullptr);
   HIP_TRY(c, hipGetLastError());
   return HF_OK;
 }
@@ -1021,72 +1217,8 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   if (max_iters < 0) return fail(c, HF_EINVAL, "max_iters < 0");
   if (!(rel_tol >= 0.0f) || !std::isfinite(rel_tol))
     return fail(c, HF_EINVAL, "rel_tol must be finite and >= 0");
-  std::memset(info, 0, sizeof *info);
-  if (!c->pinned) {
-    HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
-  }
-  if (c->prof) c->prof->solve_begin = c->prof->pending.size();
-  const Launch Lc = c->launch();
-  const int b = (int)Bc;
-  const long long n = c->n;
-  const bool hess = mode == HF_HESSIAN;
-  CgState* st = reinterpret_cast<CgState*>(c->ws + c->oState);
-  const int* skip = &st->done;
-  double* part = c->Dp(c->oRed);
-  float* r = c->F(c->oR);
-  float* p = c->F(c->oPv);
-  float* q = c->F(c->oQ);
-
-  // cache of the curvature batch: activations, p, delta_l, E2_l
-  build_cache(c, W, Xc, b, yc, hess);
-  cg_init(Lc, g, step, r, p, neg_dir, n, (double)damping,
-          (double)rel_tol * (double)rel_tol, part, st);
-  for (int j = 0; j < max_iters; ++j) {
-    if (c->prof) c->prof->tag = j;
-    product(c, W, Xc, b, p, mode, q, skip);
-    cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st);
-    // Stop enqueueing once the device reports `done` for the previous
-    // iteration; the work already queued for this one returns at once.
-    HIP_TRY(c, hipMemcpyAsync(&c->pinned[j & 1], st, sizeof(CgState),
-                              hipMemcpyDeviceToHost, c->stream));
-    HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
-    if (j >= 1) {
-      HIP_TRY(c, hipEventSynchronize(c->ev[(j - 1) & 1]));
-      if (c->pinned[(j - 1) & 1].done) break;
-    }
-  }
-  if (c->prof) c->prof->tag = -1;
-  HIP_TRY(c, hipGetLastError());
-  HIP_TRY(c, hipMemcpyAsync(&c->pinned[0], st, sizeof(CgState),
-                            hipMemcpyDeviceToHost, c->stream));
-  int errflag = 0;
-  HIP_TRY(c, hipMemcpyAsync(&errflag, c->ws + c->oErr, sizeof(int),
-                            hipMemcpyDeviceToHost, c->stream));
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
-  const CgState& s = c->pinned[0];
-  if (c->prof)
-    c->prof->retract(s.products - 1, s.neg || (s.status && s.iters < s.products),
-                     s.neg ? s.neg_iter : -1);
-  info->iters = s.iters;
-  info->products = s.products;
-  info->neg_curv = s.neg;
-  info->neg_iter = s.neg ? s.neg_iter : -1;
-  info->pBp = s.neg ? s.kappa : 0.0;
-  info->pHp = s.neg ? s.pq : 0.0;
-  info->gTd = s.neg ? (s.gp >= 0.0 ? -s.gp : s.gp) : 0.0;
-  info->rr0 = s.rr0;
-  info->rr_final = s.rr[s.iters & 1];
-  info->status = s.status;
-  if (errflag) {
-    info->status = HF_ELABEL;
-    int zero = 0;
-    HIP_TRY(c, hipMemcpy(c->ws + c->oErr, &zero, sizeof(int), hipMemcpyHostToDevice));
-    return fail(c, HF_ELABEL, "a label outside [0, %d) was seen", c->d[c->L]);
-  }
-  if (s.status) return fail(c, HF_ENUMERIC, "non-finite CG scalar");
-  return HF_OK;
+  return solve_cg(c, W, Xc, yc, (int)Bc, g, damping, max_iters, rel_tol, mode,
+                  nullptr, step, neg_dir, info);
 }
 
 int hf_bicgstab(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
@@ -1108,80 +1240,158 @@ int hf_bicgstab(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   if (max_iters < 0) return fail(c, HF_EINVAL, "max_iters < 0");
   if (!(rel_tol >= 0.0f) || !std::isfinite(rel_tol))
     return fail(c, HF_EINVAL, "rel_tol must be finite and >= 0");
-  std::memset(info, 0, sizeof *info);
-  if (!c->pinned) {
-    HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
-  }
-  BicgState* hostst = reinterpret_cast<BicgState*>(c->pinned_bicg);
-  if (!hostst) {
-    HIP_TRY(c, hipHostMalloc((void**)&c->pinned_bicg, 2 * sizeof(BicgState),
-                             hipHostMallocDefault));
-    hostst = reinterpret_cast<BicgState*>(c->pinned_bicg);
-  }
-  if (c->prof) c->prof->solve_begin = c->prof->pending.size();
-  const Launch Lc = c->launch();
-  const int b = (int)Bc;
-  const long long n = c->n;
-  const bool hess = mode == HF_HESSIAN;
-  BicgState* st = reinterpret_cast<BicgState*>(c->ws + c->oState);
-  const int* skip = &st->done;
-  double* part = c->Dp(c->oRed);
-  float* r = c->F(c->oR);
-  float* p = c->F(c->oPv);
-  float* Ap = c->F(c->oQ);
-  float* sv = c->F(c->oS);
-  float* t = c->F(c->oT);
-  float* rs = c->F(c->oRs);
+  return solve_bicg(c, W, Xc, yc, (int)Bc, g, damping, max_iters, rel_tol,
+                    mode, nullptr, step, neg_dir, info);
+}
 
-  build_cache(c, W, Xc, b, yc, hess);
-  bicg_init(Lc, g, step, r, rs, p, neg_dir, n, (double)damping,
-            (double)rel_tol * (double)rel_tol, part, st);
-  for (int j = 0; j < max_iters; ++j) {
-    if (c->prof) c->prof->tag = 2 * j;
-    product(c, W, Xc, b, p, mode, Ap, skip);
-    lambda_axpy(c, Ap, p, damping, skip);
-    bicg_half(Lc, r, rs, Ap, sv, n, j, part, st);
-    if (c->prof) c->prof->tag = 2 * j + 1;
-    product(c, W, Xc, b, sv, mode, t, skip);
-    lambda_axpy(c, t, sv, damping, skip);
-    bicg_rest(Lc, step, r, rs, p, Ap, sv, t, g, neg_dir, n, j, part, st);
-    HIP_TRY(c, hipMemcpyAsync(&hostst[j & 1], st, sizeof(BicgState),
-                              hipMemcpyDeviceToHost, c->stream));
-    HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
-    if (j >= 1) {
-      HIP_TRY(c, hipEventSynchronize(c->ev[(j - 1) & 1]));
-      if (hostst[(j - 1) & 1].done) break;
-    }
-  }
-  if (c->prof) c->prof->tag = -1;
-  HIP_TRY(c, hipGetLastError());
-  HIP_TRY(c, hipMemcpyAsync(&hostst[0], st, sizeof(BicgState),
-                            hipMemcpyDeviceToHost, c->stream));
-  int errflag = 0;
-  HIP_TRY(c, hipMemcpyAsync(&errflag, c->ws + c->oErr, sizeof(int),
+int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
+               int64_t B, const float* Xc, const int32_t* yc, int64_t Bc,
+               const hf_iter_params* prm, int32_t* hybrid_state, float* delta,
+               hf_iter_info* info) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, X, "X")) ||
+      (rc = check_ptr(c, Xc, "Xc")) || (rc = check_ptr(c, delta, "delta")) ||
+      (rc = check_batch(c, B)) || (rc = check_batch(c, Bc)))
+    return rc;
+  if (!y) return fail(c, HF_EINVAL, "y is NULL");
+  if (!prm) return fail(c, HF_EINVAL, "params is NULL");
+  if (!info) return fail(c, HF_EINVAL, "info is NULL");
+  if (prm->solver != HF_SOLVER_CG && prm->solver != HF_SOLVER_BICGSTAB)
+    return fail(c, HF_EINVAL, "unknown solver %d", prm->solver);
+  if (prm->curvature != HF_HESSIAN && prm->curvature != HF_GAUSS_NEWTON &&
+      prm->curvature != HF_HYBRID)
+    return fail(c, HF_EINVAL, "unknown curvature %d", prm->curvature);
+  if (prm->curvature == HF_HYBRID && !hybrid_state)
+    return fail(c, HF_EINVAL, "hybrid_state is NULL");
+  if (prm->curvature != HF_GAUSS_NEWTON && !yc)
+    return fail(c, HF_EINVAL, "yc is NULL");
+  if (!(prm->damping >= 0.0f) || !std::isfinite(prm->damping))
+    return fail(c, HF_EINVAL, "damping must be finite and >= 0");
+  if (prm->max_iters < 0) return fail(c, HF_EINVAL, "max_iters < 0");
+  if (!(prm->rel_tol >= 0.0f) || !std::isfinite(prm->rel_tol))
+    return fail(c, HF_EINVAL, "rel_tol must be finite and >= 0");
+  if (!(prm->eta >= 0.0f) || !std::isfinite(prm->eta))
+    return fail(c, HF_EINVAL, "eta must be finite and >= 0");
+  if (!(prm->armijo_c > 0.0f && prm->armijo_c < 1.0f))
+    return fail(c, HF_EINVAL, "armijo_c must lie in (0, 1)");
+  if (!(prm->shrink > 0.0f && prm->shrink < 1.0f))
+    return fail(c, HF_EINVAL, "shrink must lie in (0, 1)");
+  if (prm->max_backtracks < 0) return fail(c, HF_EINVAL, "max_backtracks < 0");
+  std::memset(info, 0, sizeof *info);
+  const Launch Lc = c->launch();
+  const long long n = c->n;
+  const int b = (int)B, bc = (int)Bc;
+  float* g = c->F(c->oG);
+  float* s = c->F(c->oStep);
+  float* d = c->F(c->oNd);
+  float* x0v = c->F(c->oX0);
+  float* wt = c->F(c->oWt);
+  double* scal = c->Dp(c->oScal);       // [0..3] dots, [4] loss
+  double hs[5];
+
+  // 1. f_k and g_k on the batch (X, y)
+  loss_grad_any(c, W, X, y, b, nullptr, scal + 4, g);
+  HIP_TRY(c, hipMemcpyAsync(&hs[4], scal + 4, sizeof(double),
                             hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  const BicgState& s = hostst[0];
-  if (c->prof) c->prof->retract_bicg(s.products, s.neg ? s.neg_iter : -1);
-  info->iters = s.iters;
-  info->products = s.products;
-  info->neg_curv = s.neg;
-  info->neg_iter = s.neg ? s.neg_iter : -1;
-  info->pBp = s.neg ? s.dBd : 0.0;
-  info->pHp = s.neg ? s.dHd : 0.0;
-  info->gTd = s.neg ? s.gTd : 0.0;
-  info->rr0 = s.rr0;
-  info->rr_final = s.rr;
-  info->status = s.status;
+  const double f0 = hs[4];
+  int errflag = 0;
+  HIP_TRY(c, hipMemcpy(&errflag, c->ws + c->oErr, sizeof(int), hipMemcpyDeviceToHost));
   if (errflag) {
-    info->status = HF_ELABEL;
     int zero = 0;
     HIP_TRY(c, hipMemcpy(c->ws + c->oErr, &zero, sizeof(int), hipMemcpyHostToDevice));
     return fail(c, HF_ELABEL, "a label outside [0, %d) was seen", c->d[c->L]);
   }
-  if (s.status) return fail(c, HF_ENUMERIC, "non-finite Bi-CG-STAB scalar");
+  if (!std::isfinite(f0)) return fail(c, HF_ENUMERIC, "non-finite objective");
+
+  // 2. the curvature of this iteration (Hybrid-CG: Gauss-Newton right after
+  // a Hessian solve that met negative curvature)
+  int mode = prm->curvature;
+  if (mode == HF_HYBRID) mode = *hybrid_state ? HF_GAUSS_NEWTON : HF_HESSIAN;
+
+  // 3. the Newton system, from 0 or from eta delta_{k-1}
+  const float* x0 = nullptr;
+  if (prm->eta > 0.0f) {
+    waxpy(Lc, x0v, nullptr, (double)prm->eta, delta, n);
+    x0 = x0v;
+  }
+  rc = (prm->solver == HF_SOLVER_CG)
+           ? solve_cg(c, W, Xc, yc, bc, g, prm->damping, prm->max_iters,
+                      prm->rel_tol, mode, x0, s, d, &info->solve)
+           : solve_bicg(c, W, Xc, yc, bc, g, prm->damping, prm->max_iters,
+                        prm->rel_tol, mode, x0, s, d, &info->solve);
+  if (rc != HF_OK) return rc;
+
+  // 4. candidates: the solver's step if it descends, and the oriented
+  // negative-curvature direction rescaled to the step's length
+  const float* da[4] = {g, s, g, d};
+  const float* db[4] = {s, s, d, d};
+  dots4(Lc, da, db, n, c->Dp(c->oRed), scal);
+  HIP_TRY(c, hipMemcpyAsync(hs, scal, 4 * sizeof(double), hipMemcpyDeviceToHost,
+                            c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const double gs = hs[0], ss = hs[1], gd = hs[2], dd = hs[3];
+  const double gg = info->solve.rr0;
+  struct Cand { int kind; const float* v; double scale, gTd; };
+  Cand cand[2];
+  int nc = 0;
+  if (gs < 0.0) cand[nc++] = Cand{0, s, 1.0, gs};
+  if (info->solve.neg_curv && dd > 0.0) {
+    const double target = ss > 0.0 ? std::sqrt(ss) : std::sqrt(gg);
+    const double sc = target / std::sqrt(dd);
+    cand[nc++] = Cand{1, d, sc, gd * sc};
+  }
+
+  // 5. Armijo backtracking for each candidate; keep the lower f
+  int best = -1;
+  double best_alpha = 0.0, best_f = f0;
+  for (int k = 0; k < nc; ++k) {
+    double alpha = 1.0;
+    for (int t = 0; t <= prm->max_backtracks; ++t) {
+      waxpy(Lc, wt, W, alpha * cand[k].scale, cand[k].v, n);
+      loss_only(c, wt, X, y, b, nullptr, scal + 4);
+      HIP_TRY(c, hipMemcpyAsync(&hs[4], scal + 4, sizeof(double),
+                                hipMemcpyDeviceToHost, c->stream));
+      HIP_TRY(c, hipStreamSynchronize(c->stream));
+      info->evals += 1;
+      const double ft = hs[4];
+      if (ft <= f0 + (double)prm->armijo_c * alpha * cand[k].gTd) {
+        if (best < 0 || ft < best_f) {
+          best = k;
+          best_alpha = alpha;
+          best_f = ft;
+        }
+        break;
+      }
+      alpha *= (double)prm->shrink;
+    }
+  }
+
+  // 6. theta_{k+1} and delta_k
+  info->mode_used = mode;
+  info->f0 = f0;
+  if (best >= 0) {
+    const Cand& cb = cand[best];
+    waxpy(Lc, W, W, best_alpha * cb.scale, cb.v, n);
+    waxpy(Lc, delta, nullptr, cb.scale, cb.v, n);
+    info->direction = cb.kind;
+    info->accepted = 1;
+    info->alpha = best_alpha;
+    info->f1 = best_f;
+    info->gTd = cb.gTd;
+  } else {
+    waxpy(Lc, delta, nullptr, 0.0, g, n);
+    info->direction = -1;
+    info->accepted = 0;
+    info->alpha = 0.0;
+    info->f1 = f0;
+    info->gTd = 0.0;
+  }
+  if (prm->curvature == HF_HYBRID)
+    *hybrid_state = (mode == HF_HESSIAN && info->solve.neg_curv) ? 1 : 0;
+  HIP_TRY(c, hipGetLastError());
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
   return HF_OK;
 }
 

@@ -165,9 +165,10 @@ void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
 void softmax_xent(const Launch& L, const float* Z, const int32_t* y, int B,
                   int C, int ld, float* P, float* D, double* loss_part,
                   int* err_flag);
-// loss = sum(loss_part[0 .. nparts)) / B, in a fixed order.
+// loss = sum(loss_part[0 .. nparts)) / B, in a fixed order, to loss (fp32)
+// and loss64 (fp64); either may be null.
 void loss_finalize(const Launch& L, const double* loss_part, int nparts,
-                   int B, float* loss);
+                   int B, float* loss, double* loss64 = nullptr);
 // Rdelta_L = P * (RZ - rowsum(P * RZ)) / B.
 void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
                  int C, int ld, float* RD, const int* skip);
@@ -190,10 +191,12 @@ struct CgState {
 
 int cg_grid(long long n);
 int cg_part_doubles();
-// x = 0, r = g, p = -g, neg_dir = 0; state initialised (rr = rr0 = |g|^2)
-void cg_init(const Launch& L, const float* g, float* x, float* r, float* p,
-             float* neg_dir, long long n, double lambda, double tol2,
-             double* part, CgState* st);
+// x = 0, r = g, p = -g; or, from a warm start x0 with q = A x0, x = x0,
+// r = g + q + lambda x0, p = -r.  neg_dir = 0; state initialised with
+// rr = |r|^2 and rr0 = |g|^2.  x0 and q may be null (start from 0).
+void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
+             float* x, float* r, float* p, float* neg_dir, long long n,
+             double lambda, double tol2, double* part, CgState* st);
 // One CG iteration j after the product q = A p has been formed:
 // kappa = p.q + lambda p.p and the stop test; x += alpha p,
 // r += alpha (q + lambda p); at a detection d~ = -sgn(g.p) p and, at j = 0,
@@ -214,10 +217,13 @@ struct BicgState {
 // y += a x (the damping term of B = A + lambda I)
 void axpy(const Launch& L, float* y, const float* x, float a, long long n,
           const int* skip);
-// x = 0, r = r0* = p = -g, neg_dir = 0; state initialised
-void bicg_init(const Launch& L, const float* g, float* x, float* r, float* rs,
-               float* p, float* neg_dir, long long n, double lambda,
-               double tol2, double* part, BicgState* st);
+// x = 0, r = r0* = p = -g; or, from a warm start x0 with q = A x0,
+// x = x0, r = r0* = p = -g - (q + lambda x0).  neg_dir = 0; state
+// initialised with rho = |r0|^2 and rr0 = |g|^2.  x0, q may be null.
+void bicg_init(const Launch& L, const float* g, const float* x0,
+               const float* q, float* x, float* r, float* rs, float* p,
+               float* neg_dir, long long n, double lambda, double tol2,
+               double* part, BicgState* st);
 // first half of iteration j, after Ap = B p: alpha and s = r - alpha Ap
 void bicg_half(const Launch& L, const float* r, const float* rs,
                const float* Ap, float* s, long long n, int j, double* part,
@@ -228,5 +234,14 @@ void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
                const float* Ap, const float* s, const float* t, const float* g,
                float* neg_dir, long long n, int j, double* part,
                BicgState* st);
+
+// ------------------------------------------------------------ outer step
+// out = w + a d, in fp64 (w null: out = a d)
+void waxpy(const Launch& L, float* out, const float* w, double a,
+           const float* d, long long n);
+// out[k] = a[k] . b[k] for k < 4 (device doubles), fixed summation order;
+// uses the first 4 partial regions of part
+void dots4(const Launch& L, const float* const a[4], const float* const b[4],
+           long long n, double* part, double* out);
 
 }  // namespace hfk

@@ -118,14 +118,18 @@ extern "C" __global__ __launch_bounds__(256) void hf_softmax_xent(
 
 extern "C" __global__ __launch_bounds__(256) void hf_loss_finalize(
     const double* __restrict__ part, int nparts, double invB,
-    float* __restrict__ loss) {
+    float* __restrict__ loss, double* __restrict__ loss64) {
   __shared__ double ws[4];
   double s = 0.0;
   for (int i = threadIdx.x; i < nparts; i += 256) s += part[i];
   s = wave_sum_d(s);
   if ((threadIdx.x & 63) == 0) ws[threadIdx.x >> 6] = s;
   __syncthreads();
-  if (threadIdx.x == 0) *loss = (float)(((ws[0] + ws[1]) + (ws[2] + ws[3])) * invB);
+  if (threadIdx.x == 0) {
+    const double f = ((ws[0] + ws[1]) + (ws[2] + ws[3])) * invB;
+    if (loss) *loss = (float)f;
+    if (loss64) *loss64 = f;
+  }
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_softmax_rop(
@@ -211,10 +215,10 @@ void softmax_xent(const Launch& L, const float* Z, const int32_t* y, int B,
 }
 
 void loss_finalize(const Launch& L, const double* loss_part, int nparts,
-                   int B, float* loss) {
+                   int B, float* loss, double* loss64) {
   prof_begin(L, "hf_loss_finalize");
   hipLaunchKernelGGL(hf_loss_finalize, dim3(1), dim3(256), 0, L.stream,
-                     loss_part, nparts, 1.0 / (double)B, loss);
+                     loss_part, nparts, 1.0 / (double)B, loss, loss64);
   prof_end(L, "hf_loss_finalize", 0.0, 8.0 * nparts);
 }
 

@@ -13,20 +13,25 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libhf.so")
 
 HF_SIGMOID, HF_TANH, HF_RELU = 0, 1, 2
-HF_HESSIAN, HF_GAUSS_NEWTON = 0, 1
+HF_HESSIAN, HF_GAUSS_NEWTON, HF_HYBRID = 0, 1, 2
+HF_SOLVER_CG, HF_SOLVER_BICGSTAB = 0, 1
 HF_FP32, HF_BF16_INPUTS = 0, 1
 HF_OK, HF_EINVAL, HF_ENOMEM, HF_EHIP, HF_ELABEL, HF_ENUMERIC, HF_EWORKSPACE = \
     0, -1, -2, -3, -4, -5, -6
 
 ACTS = {"sigmoid": HF_SIGMOID, "tanh": HF_TANH, "relu": HF_RELU}
 MODES = {"hessian": HF_HESSIAN, "gauss_newton": HF_GAUSS_NEWTON}
+CURVATURES = {"hessian": HF_HESSIAN, "gauss_newton": HF_GAUSS_NEWTON,
+              "hybrid": HF_HYBRID}
+SOLVERS = {"cg": HF_SOLVER_CG, "bicgstab": HF_SOLVER_BICGSTAB}
 PRECS = {"fp32": HF_FP32, "bf16": HF_BF16_INPUTS}
 
 # Every function declared in include/hf.h.
 EXPORTS = (
     "hf_create", "hf_destroy", "hf_set_stream", "hf_num_params",
     "hf_workspace_bytes", "hf_set_workspace", "hf_loss_grad", "hf_hvp",
-    "hf_cg", "hf_bicgstab", "hf_check", "hf_last_error", "hf_strerror", "hf_prof_enable",
+    "hf_cg", "hf_bicgstab", "hf_loss", "hf_iterate", "hf_check", "hf_last_error",
+    "hf_strerror", "hf_prof_enable",
     "hf_prof_reset", "hf_prof_count", "hf_prof_get",
 )
 
@@ -43,6 +48,31 @@ class hf_cg_info(ctypes.Structure):
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+
+
+class hf_iter_params(ctypes.Structure):
+    _fields_ = [
+        ("solver", ctypes.c_int32), ("curvature", ctypes.c_int32),
+        ("damping", ctypes.c_float), ("max_iters", ctypes.c_int32),
+        ("rel_tol", ctypes.c_float), ("eta", ctypes.c_float),
+        ("armijo_c", ctypes.c_float), ("shrink", ctypes.c_float),
+        ("max_backtracks", ctypes.c_int32),
+    ]
+
+
+class hf_iter_info(ctypes.Structure):
+    _fields_ = [
+        ("solve", hf_cg_info), ("mode_used", ctypes.c_int32),
+        ("direction", ctypes.c_int32), ("accepted", ctypes.c_int32),
+        ("evals", ctypes.c_int32), ("f0", ctypes.c_double),
+        ("f1", ctypes.c_double), ("alpha", ctypes.c_double),
+        ("gTd", ctypes.c_double),
+    ]
+
+    def as_dict(self):
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "solve"}
+        d["solve"] = self.solve.as_dict()
+        return d
 
 
 class HFError(RuntimeError):
@@ -80,6 +110,11 @@ def lib():
                                  ctypes.POINTER(hf_cg_info)]),
         "hf_bicgstab": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P,
                                        P, ctypes.POINTER(hf_cg_info)]),
+        "hf_loss": (ctypes.c_int, [P, P, P, P, I64, P]),
+        "hf_iterate": (ctypes.c_int, [P, P, P, P, I64, P, P, I64,
+                                      ctypes.POINTER(hf_iter_params),
+                                      ctypes.POINTER(I32), P,
+                                      ctypes.POINTER(hf_iter_info)]),
         "hf_check": (ctypes.c_int, [P]),
         "hf_last_error": (ctypes.c_char_p, [P]),
         "hf_strerror": (ctypes.c_char_p, [I32]),
@@ -233,6 +268,43 @@ class HFNet:
             _ptr(neg_dir, torch.float32, self.n, "neg_dir"), ctypes.byref(info))
         self._check(rc)
         return step, neg_dir, info.as_dict()
+
+    def hf_loss(self, W, X, y, loss=None):
+        import torch
+        B = self._rows(X)
+        if loss is None:
+            loss = torch.empty(1, dtype=torch.float32, device=self.device)
+        self._stream()
+        self._check(lib().hf_loss(
+            self._h, _ptr(W, torch.float32, self.n, "W"),
+            _ptr(X, torch.float32, None, "X"), _ptr(y, torch.int32, B, "y"), B,
+            _ptr(loss, torch.float32, 1, "loss")))
+        return loss
+
+    def hf_iterate(self, W, X, y, Xc, yc, delta, solver="cg",
+                   curvature="hessian", damping=1e-2, max_iters=10, rel_tol=0.0,
+                   eta=0.0, armijo_c=1e-4, shrink=0.5, max_backtracks=20,
+                   hybrid_state=0):
+        """One outer HF iteration; W and delta are updated in place.
+        Returns (info dict, the new hybrid state)."""
+        import torch
+        B = self._rows(X)
+        Bc = self._rows(Xc)
+        prm = hf_iter_params(SOLVERS[solver], CURVATURES[curvature],
+                             float(damping), int(max_iters), float(rel_tol),
+                             float(eta), float(armijo_c), float(shrink),
+                             int(max_backtracks))
+        hs = ctypes.c_int32(int(hybrid_state))
+        info = hf_iter_info()
+        self._stream()
+        self._check(lib().hf_iterate(
+            self._h, _ptr(W, torch.float32, self.n, "W"),
+            _ptr(X, torch.float32, None, "X"), _ptr(y, torch.int32, B, "y"), B,
+            _ptr(Xc, torch.float32, None, "Xc"),
+            _ptr(yc, torch.int32, Bc, "yc") if yc is not None else None, Bc,
+            ctypes.byref(prm), ctypes.byref(hs),
+            _ptr(delta, torch.float32, self.n, "delta"), ctypes.byref(info)))
+        return info.as_dict(), int(hs.value)
 
     def hf_check(self):
         self._check(lib().hf_check(self._h))

@@ -93,6 +93,12 @@ def test_calls_without_workspace_or_with_bad_args(L):
                    ctypes.byref(info)) == H.HF_EWORKSPACE
     assert L.hf_bicgstab(h, fake, fake, fake, 4, fake, 0.01, 5, 0.0, 0, fake,
                          fake, ctypes.byref(info)) == H.HF_EWORKSPACE
+    assert L.hf_loss(h, fake, fake, fake, 4, fake) == H.HF_EWORKSPACE
+    prm = H.hf_iter_params(0, 0, 0.01, 5, 0.0, 0.0, 1e-4, 0.5, 10)
+    hs = ctypes.c_int32(0)
+    it = H.hf_iter_info()
+    assert L.hf_iterate(h, fake, fake, fake, 4, fake, fake, 4, ctypes.byref(prm),
+                        ctypes.byref(hs), fake, ctypes.byref(it)) == H.HF_EWORKSPACE
     assert L.hf_destroy(h) == H.HF_OK
     assert n == 6 * 9 + 4 * 7
 
