@@ -14,8 +14,10 @@ with lambda = 1e-2 and all inputs resident in HBM before timing starts.
 value = curvature-vector products per second over the timed steps (the
 stateless H v and G v plus every product inside both CG solves), with fp32
 GEMMs.  The same step is then timed with bf16 GEMM operands and fp32
-accumulation (reported under "bf16_inputs"), and 10 Bi-CG-STAB iterations
-(Alg. 3) are timed after each leg.
+accumulation (reported under "bf16_inputs").  After each leg's timed steps,
+10 Bi-CG-STAB iterations (Alg. 3) and one full outer iteration (Alg. 2:
+gradient, Hessian CG, direction choice, Armijo line search) are timed on
+their own.
 
 Prints one JSON line (rank 0; there is only one GPU).
 """
@@ -175,9 +177,24 @@ def run_leg(args, w, inp, prec):
                                step=step_h, neg_dir=nd_h)
     e1.record()
     torch.cuda.synchronize()
+    bicg_ms = e0.elapsed_time(e1)
+    # one outer iteration (Alg. 2): gradient, Hessian CG from 0, direction
+    # choice and Armijo line search, on a copy of the weights
+    Wk = W.clone()
+    dk = torch.zeros_like(grad)
+    e0.record()
+    it, _ = net.hf_iterate(Wk, X, y, Xc, yc, dk, solver="cg",
+                           curvature="hessian", damping=lam,
+                           max_iters=w.cg_iters)
+    e1.record()
+    torch.cuda.synchronize()
+    outer = {"ms": e0.elapsed_time(e1), "direction": it["direction"],
+             "alpha": it["alpha"], "evals": it["evals"], "f0": it["f0"],
+             "f1": it["f1"], "solve_products": it["solve"]["products"]}
+    del Wk, dk
     res = dict(stats=stats, comp=comp, products=products, elapsed=t1 - t0,
-               ig=ig, ih=ih, ib=ib, bicg_ms=e0.elapsed_time(e1),
-               loss=float(loss.item()))
+               ig=ig, ih=ih, ib=ib, bicg_ms=bicg_ms,
+               outer=outer, loss=float(loss.item()))
     net.close()
     del net, W, X, y, v, Xc, yc, loss, grad, hv, gv, step_g, nd_g, step_h, nd_h
     torch.cuda.empty_cache()
@@ -215,6 +232,7 @@ def summary(res, K, peak):
         bicgstab_hessian={"iters": ib["iters"], "products": ib["products"],
                           "neg_iter": ib["neg_iter"], "ms": res["bicg_ms"],
                           "ms_per_product": res["bicg_ms"] / max(ib["products"], 1)},
+        outer_iteration=res["outer"],
         hv_per_s_stateless=1e3 * K / comp["hv"],
         gv_per_s_stateless=1e3 * K / comp["gv"],
         kernels={k: {"launches": s["launches"], "ms_per_step": s["ms"] / K,
@@ -277,8 +295,8 @@ def main():
         "loss": r32["loss"],
     }
     for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
-              "bicgstab_hessian", "hv_per_s_stateless", "gv_per_s_stateless",
-              "kernels"):
+              "bicgstab_hessian", "outer_iteration", "hv_per_s_stateless",
+              "gv_per_s_stateless", "kernels"):
         out[k] = s32[k]
     if not args.no_bf16:
         # the same step with bf16 GEMM operands (fp32 accumulation)
@@ -299,7 +317,7 @@ def main():
             "loss": r16["loss"],
         }
         for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
-                  "bicgstab_hessian", "kernels"):
+                  "bicgstab_hessian", "outer_iteration", "kernels"):
             out["bf16_inputs"][k] = s16[k]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_rows)
