@@ -4,8 +4,14 @@
 // minibatch).
 //
 // One workgroup of 256 threads (4 wave64 in a 2 x 2 grid) owns a 128 x 128
-// output tile; each wave owns a 64 x 64 quadrant computed as 2 x 2 blocks of
-// v_mfma_f32_32x32x2_f32 (fp32 operands, fp32 accumulation).  K advances in
+// output tile; each wave owns a 64 x 64 quadrant computed either as 2 x 2
+// blocks of v_mfma_f32_32x32x2_f32 or as 4 x 4 blocks of
+// v_mfma_f32_16x16x4_f32 (fp32 operands, fp32 accumulation).  The 16 x 16
+// form runs 16 independent accumulation chains per wave instead of 4 (on
+// MI355X, chains of dependent 32 x 32 fp32 MFMAs sustain about 90% of the
+// issue rate with 4 accumulators and 98% with 8 or more); the 32 x 32 form
+// writes 32-column row segments in the epilogue instead of 16.  Each kernel
+// takes the form that measured faster for it.  K advances in
 // blocks of 16 through two LDS buffers: while the MFMAs consume one buffer,
 // the next K block is fetched from global memory into registers and then
 // written to the other buffer.  Tiles that lie fully inside the operands
@@ -22,8 +28,11 @@
 // Every single-product GEMM pairs a K-contiguous left operand with a
 // row-contiguous right one (the forward passes take transposed weights),
 // the pairing that measured fastest on MI355X.
-// Within a K block each half-wave works on its own 8 consecutive k values,
-// which permutes the order of the K sum identically for both operands.
+// Within a K block each half-wave (32 x 32 form) or quarter-wave (16 x 16
+// form) works on its own consecutive k values, which permutes the order of
+// the K sum identically for both operands.
+#include <type_traits>
+
 #include "act.h"
 #include "hf_internal.h"
 
@@ -152,6 +161,23 @@ struct Tile {
     }
   }
 
+  // 16 x 16 x 4 operands: lane group g (lanes 16 g .. 16 g + 15) feeds
+  // k = 4 g + step at MFMA step 0..3 of a K block, so a lane reads one
+  // 16-byte chunk of a K-contiguous row (16 lanes, 16 rows, 16 distinct
+  // bank groups under the swizzle) or, from a [k][row] tile, 16 consecutive
+  // rows of k row 4 g + step (the 132-float row stride puts the four groups
+  // on distinct banks).
+  __device__ static __forceinline__ void frag16(const float* __restrict__ s,
+                                                int row, int g, float (&f)[4]) {
+    if (MK) {
+      const f32x4 a = *(const f32x4*)(s + row * LDK + ((g ^ swz(row)) * 4));
+      f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) f[q] = s[(4 * g + q) * LDM + row];
+    }
+  }
+
   // The HK values lane (row, half h) feeds to MFMA steps 0..HK-1 of a K
   // block: k = h * HK + step.  Both operands use the same k order, so the
   // sum over k is unchanged.
@@ -172,6 +198,9 @@ struct Tile {
   }
 };
 
+__device__ __forceinline__ f32x4 mfma16(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
 __device__ __forceinline__ f32x16 mfma(float a, float b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
@@ -266,7 +295,9 @@ struct EStore {
 // MODE 2: dual0  acc0 = X0 Y0, acc1 = X0 Y1
 // BIAS (weight gradient): blocks of the first column tile also sum their X
 // tiles of K-segment 0 over k, giving sum_k X(m, k) for their rows.
-template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS>
+// M16: 4 x 4 blocks of 16 x 16 x 4 MFMAs per wave instead of 2 x 2 blocks
+// of 32 x 32 x 2.
+template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS, bool M16>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) {
   if (s.skip && *s.skip) return;
   constexpr int W = 2;          // 2 x 2 MFMA blocks per wave
@@ -295,13 +326,18 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     vb1 = min(nvb, vb0 + per);
   }
 
-  f32x16 acc0[W][W], acc1[W][W];
+  // MFMA blocks per wave and dimension, and accumulator registers per block
+  constexpr int NB = M16 ? 4 : W;
+  constexpr int AR = M16 ? 4 : 16;
+  using Acc = typename std::conditional<M16, f32x4, f32x16>::type;
+  const int r16 = lane & 15, g16 = lane >> 4;   // 16 x 16 lane coordinates
+  Acc acc0[NB][NB], acc1[NB][NB];
 #pragma unroll
-  for (int a = 0; a < W; ++a)
+  for (int a = 0; a < NB; ++a)
 #pragma unroll
-    for (int b = 0; b < W; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
+      for (int r = 0; r < AR; ++r) {
         acc0[a][b][r] = 0.0f;
         if (MODE != 0) acc1[a][b][r] = 0.0f;
       }
@@ -359,59 +395,116 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     }
   };
   auto compute = [&](int buf) {
-    float x0[W][HK], y0[W][HK];
-    if (MODE == 0) {
+    if constexpr (M16) {
+      float x0[NB][4], y0[NB][4];
+      const int rx = wm * 64 + r16, ry = wn * 64 + r16;
+      if (MODE == 0) {
 #pragma unroll
-      for (int a = 0; a < W; ++a) TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
+        for (int a = 0; a < NB; ++a) TX::frag16(lds[buf][0], rx + 16 * a, g16, x0[a]);
 #pragma unroll
-      for (int b = 0; b < W; ++b) TY::frag(lds[buf][1], wn * 32 * W + b * 32 + li, h, y0[b]);
+        for (int b = 0; b < NB; ++b) TY::frag16(lds[buf][1], ry + 16 * b, g16, y0[b]);
 #pragma unroll
-      for (int k = 0; k < HK; ++k)
+        for (int k = 0; k < 4; ++k)
 #pragma unroll
-        for (int a = 0; a < W; ++a)
+          for (int a = 0; a < NB; ++a)
 #pragma unroll
-          for (int b = 0; b < W; ++b) acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
-    } else if (MODE == 1) {
-      float x1[W][HK], y1[W][HK];
+            for (int b = 0; b < NB; ++b) acc0[a][b] = mfma16(x0[a][k], y0[b][k], acc0[a][b]);
+      } else if (MODE == 1) {
+        float x1[NB][4], y1[NB][4];
 #pragma unroll
-      for (int a = 0; a < W; ++a) {
-        TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
-        TX::frag(lds[buf][1], wm * 32 * W + a * 32 + li, h, x1[a]);
+        for (int a = 0; a < NB; ++a) {
+          TX::frag16(lds[buf][0], rx + 16 * a, g16, x0[a]);
+          TX::frag16(lds[buf][1], rx + 16 * a, g16, x1[a]);
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          TY::frag16(lds[buf][2], ry + 16 * b, g16, y0[b]);
+          TY::frag16(lds[buf][3], ry + 16 * b, g16, y1[b]);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int a = 0; a < NB; ++a)
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+              acc0[a][b] = mfma16(x0[a][k], y0[b][k], acc0[a][b]);
+              acc1[a][b] = mfma16(x1[a][k], y0[b][k], acc1[a][b]);
+              acc1[a][b] = mfma16(x0[a][k], y1[b][k], acc1[a][b]);
+            }
+      } else {
+        float y1[NB][4];
+#pragma unroll
+        for (int a = 0; a < NB; ++a) TX::frag16(lds[buf][0], rx + 16 * a, g16, x0[a]);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          TY::frag16(lds[buf][1], ry + 16 * b, g16, y0[b]);
+          TY::frag16(lds[buf][2], ry + 16 * b, g16, y1[b]);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int a = 0; a < NB; ++a)
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+              acc0[a][b] = mfma16(x0[a][k], y0[b][k], acc0[a][b]);
+              acc1[a][b] = mfma16(x0[a][k], y1[b][k], acc1[a][b]);
+            }
       }
-#pragma unroll
-      for (int b = 0; b < W; ++b) {
-        TY::frag(lds[buf][2], wn * 32 * W + b * 32 + li, h, y0[b]);
-        TY::frag(lds[buf][3], wn * 32 * W + b * 32 + li, h, y1[b]);
-      }
-#pragma unroll
-      for (int k = 0; k < HK; ++k)
-#pragma unroll
-        for (int a = 0; a < W; ++a)
-#pragma unroll
-          for (int b = 0; b < W; ++b) {
-            acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
-            acc1[a][b] = mfma(x1[a][k], y0[b][k], acc1[a][b]);
-            acc1[a][b] = mfma(x0[a][k], y1[b][k], acc1[a][b]);
-          }
     } else {
-      float y1[W][HK];
+      float x0[W][HK], y0[W][HK];
+      if (MODE == 0) {
 #pragma unroll
-      for (int a = 0; a < W; ++a) TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
+        for (int a = 0; a < W; ++a) TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
 #pragma unroll
-      for (int b = 0; b < W; ++b) {
-        TY::frag(lds[buf][1], wn * 32 * W + b * 32 + li, h, y0[b]);
-        TY::frag(lds[buf][2], wn * 32 * W + b * 32 + li, h, y1[b]);
+        for (int b = 0; b < W; ++b) TY::frag(lds[buf][1], wn * 32 * W + b * 32 + li, h, y0[b]);
+#pragma unroll
+        for (int k = 0; k < HK; ++k)
+#pragma unroll
+          for (int a = 0; a < W; ++a)
+#pragma unroll
+            for (int b = 0; b < W; ++b) acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
+      } else if (MODE == 1) {
+        float x1[W][HK], y1[W][HK];
+#pragma unroll
+        for (int a = 0; a < W; ++a) {
+          TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
+          TX::frag(lds[buf][1], wm * 32 * W + a * 32 + li, h, x1[a]);
+        }
+#pragma unroll
+        for (int b = 0; b < W; ++b) {
+          TY::frag(lds[buf][2], wn * 32 * W + b * 32 + li, h, y0[b]);
+          TY::frag(lds[buf][3], wn * 32 * W + b * 32 + li, h, y1[b]);
+        }
+#pragma unroll
+        for (int k = 0; k < HK; ++k)
+#pragma unroll
+          for (int a = 0; a < W; ++a)
+#pragma unroll
+            for (int b = 0; b < W; ++b) {
+              acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
+              acc1[a][b] = mfma(x1[a][k], y0[b][k], acc1[a][b]);
+              acc1[a][b] = mfma(x0[a][k], y1[b][k], acc1[a][b]);
+            }
+      } else {
+        float y1[W][HK];
+#pragma unroll
+        for (int a = 0; a < W; ++a) TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
+#pragma unroll
+        for (int b = 0; b < W; ++b) {
+          TY::frag(lds[buf][1], wn * 32 * W + b * 32 + li, h, y0[b]);
+          TY::frag(lds[buf][2], wn * 32 * W + b * 32 + li, h, y1[b]);
+        }
+#pragma unroll
+        for (int k = 0; k < HK; ++k)
+#pragma unroll
+          for (int a = 0; a < W; ++a)
+#pragma unroll
+            for (int b = 0; b < W; ++b) {
+              acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
+              acc1[a][b] = mfma(x0[a][k], y1[b][k], acc1[a][b]);
+            }
       }
-#pragma unroll
-      for (int k = 0; k < HK; ++k)
-#pragma unroll
-        for (int a = 0; a < W; ++a)
-#pragma unroll
-          for (int b = 0; b < W; ++b) {
-            acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
-            acc1[a][b] = mfma(x0[a][k], y1[b][k], acc1[a][b]);
-          }
-    }
+      }
   };
 
   // bias sums: thread t owns column t % ROWS and KPT consecutive k of a block
@@ -450,50 +543,75 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     }
   }
 
-  // 32x32 f32 accumulator layout: lane (li, h), register r holds
-  // row 8 * (r / 4) + 4 * h + r % 4, column li of the 32 x 32 block.
+  if constexpr (M16) {
+    // 16x16 f32 accumulator layout: lane (r16, g16), register r holds row
+    // 4 * g16 + r, column r16 of the 16 x 16 block.
 #pragma unroll
-  for (int a = 0; a < W; ++a)
+    for (int a = 0; a < NB; ++a)
 #pragma unroll
-    for (int b = 0; b < W; ++b) {
-      const f32x16 v0 = acc0[a][b];
-      const f32x16 v1 = MODE == 0 ? v0 : acc1[a][b];
-      const int rbase = m0 + wm * 32 * W + a * 32 + 4 * h;
-      const int col = n0 + wn * 32 * W + b * 32 + li;
-      if (col < s.N) {
+      for (int b = 0; b < NB; ++b) {
+        const Acc v0 = acc0[a][b];
+        const Acc v1 = MODE == 0 ? v0 : acc1[a][b];
+        const int rbase = m0 + wm * 64 + a * 16 + 4 * g16;
+        const int col = n0 + wn * 64 + b * 16 + r16;
+        if (col < s.N) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = rbase + 8 * (r >> 2) + (r & 3);
-          if (row < s.M) Epi::apply(e, row, col, v0[r], MODE == 0 ? 0.0f : v1[r]);
+          for (int r = 0; r < 4; ++r) {
+            const int row = rbase + r;
+            if (row < s.M) Epi::apply(e, row, col, v0[r], MODE == 0 ? 0.0f : v1[r]);
+          }
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
-      // keep the scheduler from hoisting every block's loads to the top
-      __builtin_amdgcn_sched_barrier(0);
-    }
+  } else {
+    // 32x32 f32 accumulator layout: lane (li, h), register r holds
+    // row 8 * (r / 4) + 4 * h + r % 4, column li of the 32 x 32 block.
+#pragma unroll
+    for (int a = 0; a < W; ++a)
+#pragma unroll
+      for (int b = 0; b < W; ++b) {
+        const Acc v0 = acc0[a][b];
+        const Acc v1 = MODE == 0 ? v0 : acc1[a][b];
+        const int rbase = m0 + wm * 32 * W + a * 32 + 4 * h;
+        const int col = n0 + wn * 32 * W + b * 32 + li;
+        if (col < s.N) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = rbase + 8 * (r >> 2) + (r & 3);
+            if (row < s.M) Epi::apply(e, row, col, v0[r], MODE == 0 ? 0.0f : v1[r]);
+          }
+        }
+        // keep the scheduler from hoisting every block's loads to the top
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  }
 }
 
 }  // namespace
 
-#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS)                           \
+#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS, M16)                      \
   extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v4(GemmShape s,   \
                                                                  EpiArgs e) {   \
-    gemm_body<MODE, XK, YK, 4, EPI, BIAS>(s, e);                                \
+    gemm_body<MODE, XK, YK, 4, EPI, BIAS, M16>(s, e);                           \
   }                                                                             \
   extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v1(GemmShape s,   \
                                                                  EpiArgs e) {   \
-    gemm_body<MODE, XK, YK, 1, EPI, BIAS>(s, e);                                \
+    gemm_body<MODE, XK, YK, 1, EPI, BIAS, M16>(s, e);                           \
   }
 
-HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, false, EFwd, false)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false)
-HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false)
-HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false)
-HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false)
-HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false)
-HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false)
-HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false)
-HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true)
+// The last argument selects the 16 x 16 form (measured on the speech-frame
+// net: bwd_rbwd +22%, bwd and gnbwd +3%, wgrad +1.5%, fwd +1%; the forward
+// R-operator kernels with their heavier epilogues ran 2% slower in it).
+HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, false, EFwd, false, true)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false, true)
+HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false, true)
+HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, true)
+HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false, true)
+HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false, true)
+HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, true)
 
 namespace {
 
