@@ -41,6 +41,8 @@ Optimization for Deep Neural Network" (arXiv 1606.00511).
   (Alg. 2): gradient, solve from 0 or from the warm start eta delta_{k-1},
   the choice between the solver's step and the negative-curvature direction,
   Armijo backtracking, and the Hybrid-CG curvature policy (Sec. 3).
+  Optionally CG-backtracking over the solver's iterates (Sec. 2.2, after
+  Martens 2010) and the damping adjustment of Alg. 1's second step.
 
 Readings where the paper is silent (each also listed in the design notes):
 mean over the batch; biases present; ReLU'(0) = 0; detection on B_k with
@@ -48,7 +50,10 @@ kappa <= 0 (the paper writes "< 0"); x_0 = 0 unless a warm start is given;
 a relative-residual stop that is off by default; the outer iteration's
 "best descent direction" is the candidate whose Armijo step reaches the
 lower loss, the negative-curvature candidate is rescaled to the length of
-the solver's step, and the Armijo constants are c = 1e-4, shrink 0.5.
+the solver's step, and the Armijo constants are c = 1e-4, shrink 0.5;
+CG-backtracking keeps iterates at a ratio-1.3 schedule and walks back from
+the final one while f decreases; the damping rule is Levenberg-Marquardt on
+the reduction ratio against the damped model m_k of eq. (1).
 
 Parity pins
 -----------
@@ -56,7 +61,9 @@ Every function here is pinned by ``tests/test_oracle_pins.py`` against things
 other than itself: ln C at zero weights, finite differences of the loss,
 brute-force Hessians from second differences, symmetry, PSD-ness, the L = 1
 multinomial-logistic closed form, label independence of G v, hand-computed
-CG cases, and exact n-step convergence of CG against ``numpy.linalg.solve``.
+CG cases, exact n-step convergence of CG against ``numpy.linalg.solve``,
+the CG-backtracking rule on a hand-made sequence, rho = 1 on an exactly
+quadratic objective and rho against finite-difference curvature.
 """
 
 import numpy as np
@@ -280,7 +287,7 @@ def sgn(x):
 
 
 def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
-                x0=None):
+                x0=None, snap_at=()):
     """CG-Minimize(B_k, -g_k) with B_k(d) = A d + lam d (Alg. 1 steps 3-4).
 
     Minimises m_k(d) = f + g^T d + d^T B_k d / 2 (Sec. 2.1, eq. (1)) from
@@ -295,8 +302,9 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
     Returns a dict with step, neg_dir (None if no detection), iters (completed
     updates of the iterate), products (curvature products evaluated,
     including the warm start's), neg_curv, neg_iter, pBp, pHp, gTd,
-    rr0 (= |g|^2), rr_final and, if ``record``, the list of per-iteration
-    kappa values and directions.
+    rr0 (= |g|^2), rr_final, kept (a copy of the iterate after j updates
+    for every j in ``snap_at`` that the solve reached) and, if ``record``,
+    the list of per-iteration kappa values and directions.
     """
     g = np.asarray(g, dtype=np.float64)
     nprod0 = 0
@@ -311,7 +319,7 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
     rr = float(r @ r)
     res = dict(step=x, neg_dir=None, iters=0, products=nprod0, neg_curv=0,
                neg_iter=-1, pBp=0.0, pHp=0.0, gTd=0.0, rr0=float(g @ g),
-               rr_final=rr, kappas=[], dirs=[])
+               rr_final=rr, kappas=[], dirs=[], kept={})
     if rr == 0.0:
         return res
     for j in range(max_iters):
@@ -333,6 +341,8 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
         r = r + alpha * q
         rr_new = float(r @ r)
         res.update(step=x, iters=j + 1, rr_final=rr_new)
+        if j + 1 in snap_at:
+            res["kept"][j + 1] = x.copy()
         if rel_tol > 0.0 and rr_new <= rel_tol * rel_tol * res["rr0"]:
             return res
         beta = rr_new / rr
@@ -342,17 +352,17 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
 
 
 def cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-               rel_tol=0.0, record=False, x0=None):
+               rel_tol=0.0, record=False, x0=None, snap_at=()):
     """CG-Minimize with the curvature operator of the network on the fixed
     curvature batch (Xc, yc) (Alg. 2: the product on one minibatch)."""
     def apply_A(p):
         return curvature(dims, act, theta, Xc, yc, p, mode)
-    return cg_minimize(apply_A, g, lam, max_iters, rel_tol, record, x0)
+    return cg_minimize(apply_A, g, lam, max_iters, rel_tol, record, x0, snap_at)
 
 
 # ----------------------------------------------------------------- Bi-CG-STAB
 def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
-                      store=None, x0=None):
+                      store=None, x0=None, snap_at=()):
     """Bi-CG-STAB (Alg. 3) for B_k d = -g_k, B_k = A + lam I, from d = 0 or
     from d = x0 (Alg. 2: the Newton system is solved by Bi-CG-STAB from 0 or
     from the warm start eta delta_{k-1}; one extra product forms its
@@ -373,6 +383,9 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
     relative-residual stop; r0* = r0; gamma_j is the usual omega_j; a zero
     (A p_j, r0*) or (r_{j+1}, r0*) ends the solve; A s_j = 0 gives gamma_j = 0
     (then s_j = 0 for a nonsingular operator and x_{j+1} = x_j + alpha_j p_j).
+
+    ``kept`` holds a copy of the iterate after j iterations for every j in
+    ``snap_at`` that the solve reached.
 
     ``store`` (identity when None) is applied to every vector the recurrences
     keep (s, x, r, p) as it is formed.  Tests pass a rounding to float32 to
@@ -400,7 +413,7 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
     rr0 = float(g @ g)       # the relative stop is against |b| = |g|
     res = dict(step=x, neg_dir=None, iters=0, products=nprod0, neg_curv=0,
                neg_iter=-1, dBd=0.0, dHd=0.0, gTd=0.0, rr0=rr0,
-               rr_final=float(r @ r), curvatures=[])
+               rr_final=float(r @ r), curvatures=[], kept={})
     if float(r @ r) == 0.0:
         return res
     for j in range(max_iters):
@@ -419,6 +432,8 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
         r = keep(s - gamma * t)
         rr = float(r @ r)
         res.update(step=x, iters=j + 1, rr_final=rr)
+        if j + 1 in snap_at:
+            res["kept"][j + 1] = x.copy()
         dHd = float(x @ apply_A(x))
         if record:
             res["curvatures"].append(dHd)
@@ -438,21 +453,81 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
 
 
 def bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-                     rel_tol=0.0, record=False, store=None, x0=None):
+                     rel_tol=0.0, record=False, store=None, x0=None, snap_at=()):
     """Bi-CG-STAB with the network's curvature operator on (Xc, yc)."""
     def apply_A(p):
         return curvature(dims, act, theta, Xc, yc, p, mode)
     return bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol, record, store,
-                             x0)
+                             x0, snap_at)
 
 
 # --------------------------------------------------------- outer iteration
 HESSIAN, GAUSS_NEWTON, HYBRID = "hessian", "gauss_newton", "hybrid"
 
 
+def backtrack_schedule(max_iters, cap):
+    """Iterations (counts of completed solver updates) whose iterates
+    CG-backtracking keeps: j = 1, then j <- max(j + 1, ceil(1.3 j)), the
+    geometric spacing with ratio 1.3 of Martens (2010, Sec. 4.6), which the
+    paper cites for CG-backtracking (Sec. 2.2).  The ceiling is taken in
+    integer arithmetic, ceil(13 j / 10).  Only j < max_iters are listed (the
+    final iterate is always a candidate), and at most ``cap`` of them, the
+    latest ones."""
+    J, j = [], 1
+    while j < max_iters:
+        J.append(j)
+        j = max(j + 1, (13 * j + 9) // 10)
+    return J[-cap:] if cap > 0 else []
+
+
+def cg_backtrack(f, chain):
+    """CG-backtracking (Martens 2010, Sec. 4.6; the paper's Sec. 2.2 takes
+    the solver's iterates as its candidates): ``chain`` lists (j, x_j) from
+    the final iterate back to the earliest kept one.  The objective f is
+    evaluated from the final iterate backwards for as long as it decreases;
+    the last iterate before it rises again is chosen.  Returns (j, x_j,
+    f(x_j), number of evaluations)."""
+    j_best, x_best = chain[0]
+    f_best = f(x_best)
+    evals = 1
+    for j, x in chain[1:]:
+        fj = f(x)
+        evals += 1
+        if fj < f_best:
+            j_best, x_best, f_best = j, x, fj
+        else:
+            break
+    return j_best, x_best, f_best, evals
+
+
+def reduction_ratio(f0, f1, g, p, Bp):
+    """rho = (f(theta + p) - f(theta)) / (m_k(p) - m_k(0)), the actual over
+    the predicted decrease, with the paper's quadratic model m_k of eq. (1)
+    (the damped B_k).  Undefined, returned as -inf, when the model predicts
+    no decrease (m_k(p) >= m_k(0))."""
+    pred = float(g @ p) + 0.5 * float(p @ Bp)
+    if not pred < 0.0:
+        return float("-inf")
+    return (f1 - f0) / pred
+
+
+def adapt_damping(lam, rho):
+    """Levenberg-Marquardt adjustment of lambda (Alg. 1, second step, leaves
+    the rule open; this is the rule of Martens 2010, Sec. 4.1, which the
+    paper cites): rho < 1/4 raises lambda by 3/2, rho > 3/4 lowers it by
+    2/3, otherwise it is kept.  An iteration that accepted no step passes
+    rho = -inf."""
+    if rho < 0.25:
+        return 1.5 * lam
+    if rho > 0.75:
+        return lam * (2.0 / 3.0)
+    return lam
+
+
 def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
             lam=1e-2, max_iters=10, rel_tol=0.0, eta=0.0, delta_prev=None,
-            hybrid_g=False, c=1e-4, shrink=0.5, max_backtracks=20):
+            hybrid_g=False, c=1e-4, shrink=0.5, max_backtracks=20,
+            damping_adapt=False, backtrack_cap=0):
     """One iteration of the distributed HF method on one worker's share
     (Alg. 2, one k), in the paper's order:
 
@@ -475,11 +550,21 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
     6. theta_{k+1} = theta_k + alpha_k delta_k, or theta_k when no candidate
        was accepted.
 
+    With ``backtrack_cap`` > 0 the solver keeps its iterates at
+    backtrack_schedule(max_iters, backtrack_cap), and the step candidate of
+    4. is the iterate cg_backtrack chooses among them and the final one; its
+    objective value is the Armijo trial at alpha = 1.  With
+    ``damping_adapt`` the iteration ends with rho of the accepted update
+    p = alpha_k delta_k (reduction_ratio, with B_k p formed by a curvature
+    product at theta_k) and the next lambda (adapt_damping).
+
     Returns a dict: theta (new), delta (the chosen direction, zeros when
     none), f0, f1, alpha, gTd, direction (0 step, 1 negative curvature,
-    -1 none), accepted, evals (loss evaluations in the line searches),
-    trials (kind, alpha, f, Armijo bound) of every evaluation, mode_used,
-    hybrid_g (the state for the next call), solve (the solver's result).
+    -1 none), accepted, evals (loss evaluations in backtracking and the line
+    searches), trials (kind, alpha, f, Armijo bound) of every line-search
+    evaluation, mode_used, hybrid_g (the state for the next call), solve
+    (the solver's result), backtrack_iter (the chosen iterate's j, -1 without
+    backtracking), rho (nan without damping adaptation) and lam_next.
     """
     theta = np.asarray(theta, dtype=np.float64)
     f0, g = loss_grad(dims, act, theta, X, y)
@@ -490,16 +575,27 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
     x0 = None
     if eta > 0.0 and delta_prev is not None:
         x0 = eta * np.asarray(delta_prev, dtype=np.float64)
+    J = backtrack_schedule(max_iters, backtrack_cap) if backtrack_cap > 0 else []
     if solver == "cg":
         sol = cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-                         rel_tol, x0=x0)
+                         rel_tol, x0=x0, snap_at=J)
     else:
         sol = bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters,
-                               mode, rel_tol, x0=x0)
+                               mode, rel_tol, x0=x0, snap_at=J)
     s = sol["step"]
+    evals = 0
+    bt_iter, f_step = -1, None
+    if backtrack_cap > 0:
+        chain = [(sol["iters"], s)] + [(j, sol["kept"][j])
+                                       for j in sorted(sol["kept"], reverse=True)
+                                       if j < sol["iters"]]
+        bt_iter, s_bt, f_step, evals = cg_backtrack(
+            lambda x: loss(dims, act, theta + x, X, y), chain)
+    else:
+        s_bt = s
     cands = []
-    if float(g @ s) < 0.0:
-        cands.append((0, s))
+    if float(g @ s_bt) < 0.0:
+        cands.append((0, s_bt))
     if sol["neg_curv"]:
         d = sol["neg_dir"]
         ns = float(np.linalg.norm(s))
@@ -508,14 +604,16 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
         if nd > 0.0:
             cands.append((1, d * (target / nd)))
     best = None
-    evals = 0
     trials = []
     for kind, d in cands:
         gTd = float(g @ d)
         alpha = 1.0
         for b in range(max_backtracks + 1):
-            ft = loss(dims, act, theta + alpha * d, X, y)
-            evals += 1
+            if kind == 0 and b == 0 and f_step is not None:
+                ft = f_step          # known from backtracking
+            else:
+                ft = loss(dims, act, theta + alpha * d, X, y)
+                evals += 1
             trials.append((kind, alpha, ft, f0 + c * alpha * gTd))
             if ft <= f0 + c * alpha * gTd:
                 if best is None or ft < best[3]:
@@ -524,12 +622,20 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
             alpha *= shrink
     res = dict(f0=f0, evals=evals, trials=trials, mode_used=mode, solve=sol,
                hybrid_g=(curvature_kind == HYBRID and mode == HESSIAN
-                         and bool(sol["neg_curv"])))
+                         and bool(sol["neg_curv"])),
+               backtrack_iter=bt_iter, rho=float("nan"), lam_next=lam)
     if best is None:
         res.update(theta=theta.copy(), delta=np.zeros_like(theta), f1=f0,
                    alpha=0.0, gTd=0.0, direction=-1, accepted=0)
+        if damping_adapt:
+            res.update(rho=float("-inf"), lam_next=adapt_damping(lam, float("-inf")))
     else:
         kind, d, alpha, ft, gTd = best
         res.update(theta=theta + alpha * d, delta=d, f1=ft, alpha=alpha,
                    gTd=gTd, direction=kind, accepted=1)
+        if damping_adapt:
+            p = alpha * d
+            Bp = curvature(dims, act, theta, Xc, yc, p, mode) + lam * p
+            rho = reduction_ratio(f0, ft, g, p, Bp)
+            res.update(rho=rho, lam_next=adapt_damping(lam, rho))
     return res

@@ -637,3 +637,146 @@ def test_planted_uphill_step_is_caught(monkeypatch):
     r = O.iterate(dims, "tanh", th, p["X"], p["y"], p["X"], p["y"])
     assert r["accepted"] == 0 and r["direction"] == -1
     assert r["f1"] == r["f0"]
+
+
+# ------------------------------------------- CG-backtracking and damping
+def test_backtrack_schedule_is_the_ratio_13_sequence():
+    """j_1 = 1, j_{i+1} = max(j_i + 1, ceil(1.3 j_i)), checked with exact
+    rational arithmetic; only j < max_iters, the latest cap of them."""
+    import math
+    from fractions import Fraction
+    seq, j = [], 1
+    while j < 50:
+        seq.append(j)
+        j = max(j + 1, math.ceil(Fraction(13, 10) * j))
+    assert seq == [1, 2, 3, 4, 6, 8, 11, 15, 20, 26, 34, 45]
+    assert O.backtrack_schedule(50, 100) == seq
+    assert O.backtrack_schedule(50, 3) == [26, 34, 45]
+    assert O.backtrack_schedule(2, 5) == [1]
+    assert O.backtrack_schedule(1, 5) == []
+    assert O.backtrack_schedule(0, 5) == []
+
+
+def test_cg_backtrack_hand_sequence():
+    """From the final iterate backwards while f decreases: with f = 3.0,
+    2.5, 2.0, 2.2, 1.0 (final first) the third is chosen after four
+    evaluations; the lower value behind the rise is never reached."""
+    fv = {"a": 3.0, "b": 2.5, "c": 2.0, "d": 2.2, "e": 1.0}
+    chain = [(5, "a"), (4, "b"), (3, "c"), (2, "d"), (1, "e")]
+    assert O.cg_backtrack(lambda x: fv[x], chain) == (3, "c", 2.0, 4)
+    # final iterate best: two evaluations
+    fv2 = {"a": 1.0, "b": 1.5, "c": 0.5}
+    assert O.cg_backtrack(lambda x: fv2[x], chain[:3]) == (5, "a", 1.0, 2)
+    # monotone: walks to the earliest kept iterate
+    fv3 = {"a": 5.0, "b": 4.0, "c": 3.0}
+    assert O.cg_backtrack(lambda x: fv3[x], chain[:3]) == (3, "c", 3.0, 3)
+    # a single candidate
+    assert O.cg_backtrack(lambda x: fv[x], chain[:1]) == (5, "a", 3.0, 1)
+
+
+def test_reduction_ratio_and_damping_rule():
+    """On an exactly quadratic objective f(t) = g^T t + t^T B t / 2 the model
+    is exact: rho = 1 for every p.  A model that predicts no decrease gives
+    rho = -inf.  The Levenberg-Marquardt rule: raise by 3/2 below 1/4, lower
+    by 2/3 above 3/4, keep in between (boundaries included)."""
+    rng = np.random.default_rng(5)
+    n = 7
+    M = rng.standard_normal((n, n))
+    B = M @ M.T + 0.5 * np.eye(n)
+    g = rng.standard_normal(n)
+    f = lambda t: float(g @ t + 0.5 * t @ B @ t)
+    for _ in range(5):
+        p = -0.3 * np.linalg.solve(B, g) + 0.05 * rng.standard_normal(n)
+        if float(g @ p + 0.5 * p @ B @ p) < 0:
+            assert O.reduction_ratio(f(np.zeros(n)), f(p), g, p, B @ p) == \
+                pytest.approx(1.0, abs=1e-12)
+    p = -np.linalg.solve(B, g) * 3.0          # overshoot: model rises
+    assert float(g @ p + 0.5 * p @ B @ p) > 0
+    assert O.reduction_ratio(0.0, -1.0, g, p, B @ p) == float("-inf")
+    lam = 0.01
+    assert O.adapt_damping(lam, 0.1) == pytest.approx(0.015)
+    assert O.adapt_damping(lam, 0.25) == lam
+    assert O.adapt_damping(lam, 0.5) == lam
+    assert O.adapt_damping(lam, 0.75) == lam
+    assert O.adapt_damping(lam, 0.9) == pytest.approx(0.01 * 2 / 3)
+    assert O.adapt_damping(lam, float("-inf")) == pytest.approx(0.015)
+
+
+@pytest.mark.parametrize("case", [((12, 10, 9, 4), 40, 21, 0.05, 6, 1),
+                                  ((10, 8, 5), 30, 24, 1e-3, 12, 0)])
+def test_iterate_rho_against_finite_difference_curvature(case):
+    """rho of an accepted Hessian-CG update (one case takes the
+    negative-curvature direction, one the solver's step) equals the ratio
+    recomputed with B_k p from central differences of the gradient (not from
+    the R-operator), and lambda moves as the rule says."""
+    dims, B, seed, lam, iters, direction = case
+    act = "tanh"
+    p = WL.make_small(dims, act, B, seed=seed)
+    th = p["theta"].astype(np.float64)
+    r = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver="cg",
+                  curvature_kind="hessian", lam=lam, max_iters=iters,
+                  damping_adapt=True)
+    assert r["accepted"] == 1 and r["direction"] == direction
+    f0, g = O.loss_grad(dims, act, th, p["X"], p["y"])
+    step = r["theta"] - th
+    eps = 1e-5
+    Hp = (O.loss_grad(dims, act, th + eps * step, p["X"], p["y"])[1] -
+          O.loss_grad(dims, act, th - eps * step, p["X"], p["y"])[1]) / (2 * eps)
+    pred = float(g @ step) + 0.5 * float(step @ (Hp + lam * step))
+    rho = (O.loss(dims, act, r["theta"], p["X"], p["y"]) - f0) / pred
+    assert r["rho"] == pytest.approx(rho, rel=1e-6)
+    assert r["lam_next"] == pytest.approx(O.adapt_damping(lam, rho))
+    # an iteration that accepts nothing raises lambda
+    z = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], max_iters=0,
+                  lam=lam, damping_adapt=True)
+    assert z["accepted"] == 0 and z["lam_next"] == pytest.approx(1.5 * lam)
+
+
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
+def test_kept_iterates_equal_truncated_solves(solver):
+    """The iterate kept after j updates is the final step of the same solve
+    truncated to j iterations (no off-by-one in the snapshot index)."""
+    dims, act = (10, 8, 5), "sigmoid"
+    p = WL.make_small(dims, act, 30, seed=23)
+    th = p["theta"].astype(np.float64)
+    _, g = O.loss_grad(dims, act, th, p["X"], p["y"])
+    run = O.cg_network if solver == "cg" else O.bicgstab_network
+    J = O.backtrack_schedule(9, 10)
+    full = run(dims, act, th, p["X"], p["y"], g, 0.1, 9, "gauss_newton", snap_at=J)
+    assert sorted(full["kept"]) == [j for j in J if j <= full["iters"]]
+    for j, x in full["kept"].items():
+        short = run(dims, act, th, p["X"], p["y"], g, 0.1, j, "gauss_newton")
+        assert np.allclose(x, short["step"], rtol=0, atol=1e-14)
+
+
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
+def test_iterate_with_backtracking(solver):
+    """With CG-backtracking the chosen iterate is the first local minimum of
+    f walking back from the final iterate over the kept ones (checked by
+    brute force over all of them), its f is never above the final
+    iterate's, and without kept iterates the iteration is unchanged."""
+    dims, act = (10, 8, 5), "tanh"
+    p = WL.make_small(dims, act, 30, seed=24)
+    th = p["theta"].astype(np.float64)
+    kw = dict(solver=solver, curvature_kind="gauss_newton", lam=1e-3,
+              max_iters=12)
+    r = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"],
+                  backtrack_cap=20, **kw)
+    sol = r["solve"]
+    f = lambda x: O.loss(dims, act, th + x, p["X"], p["y"])
+    js = [sol["iters"]] + sorted((j for j in sol["kept"] if j < sol["iters"]),
+                                 reverse=True)
+    xs = {sol["iters"]: sol["step"], **{j: sol["kept"][j] for j in js[1:]}}
+    fs = [f(xs[j]) for j in js]
+    k = 0
+    while k + 1 < len(fs) and fs[k + 1] < fs[k]:
+        k += 1
+    assert r["backtrack_iter"] == js[k]
+    assert fs[k] <= fs[0]
+    r0 = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], **kw)
+    assert r0["backtrack_iter"] == -1
+    r1 = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"],
+                   backtrack_cap=20, **dict(kw, max_iters=1))
+    assert r1["backtrack_iter"] == r1["solve"]["iters"]
+    assert np.array_equal(r1["theta"], O.iterate(
+        dims, act, th, p["X"], p["y"], p["X"], p["y"], **dict(kw, max_iters=1))["theta"])
