@@ -17,13 +17,15 @@ GEMMs.  The same step is then timed with bf16 GEMM operands and fp32
 accumulation (reported under "bf16_inputs").  After each leg's timed steps,
 10 Bi-CG-STAB iterations (Alg. 3) and one full outer iteration (Alg. 2:
 gradient, Hessian CG, direction choice, Armijo line search) are timed on
-their own.
+their own, and once more on the Gauss-Newton matrix with CG-backtracking
+over 16 kept iterates and the damping adjustment.
 
 Prints one JSON line (rank 0; there is only one GPU).
 """
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -191,10 +193,27 @@ def run_leg(args, w, inp, prec):
     outer = {"ms": e0.elapsed_time(e1), "direction": it["direction"],
              "alpha": it["alpha"], "evals": it["evals"], "f0": it["f0"],
              "f1": it["f1"], "solve_products": it["solve"]["products"]}
-    del Wk, dk
+    # the same iteration on the Gauss-Newton matrix with CG-backtracking over
+    # kept iterates (Sec. 2.2) and the damping adjustment (Alg. 1)
+    Wk.copy_(W)
+    dk.zero_()
+    keep = torch.empty((16, net.n), dtype=torch.float32, device=dev)
+    e0.record()
+    it, _ = net.hf_iterate(Wk, X, y, Xc, yc, dk, solver="cg",
+                           curvature="gauss_newton", damping=lam,
+                           max_iters=w.cg_iters, adapt_damping=True, keep=keep)
+    e1.record()
+    torch.cuda.synchronize()
+    outer_bt = {"ms": e0.elapsed_time(e1), "direction": it["direction"],
+                "alpha": it["alpha"], "evals": it["evals"], "f0": it["f0"],
+                "f1": it["f1"], "solve_products": it["solve"]["products"],
+                "backtrack_iter": it["backtrack_iter"],
+                "rho": it["rho"] if math.isfinite(it["rho"]) else None,
+                "damping_next": it["damping_next"]}
+    del Wk, dk, keep
     res = dict(stats=stats, comp=comp, products=products, elapsed=t1 - t0,
                ig=ig, ih=ih, ib=ib, bicg_ms=bicg_ms,
-               outer=outer, loss=float(loss.item()))
+               outer=outer, outer_bt=outer_bt, loss=float(loss.item()))
     net.close()
     del net, W, X, y, v, Xc, yc, loss, grad, hv, gv, step_g, nd_g, step_h, nd_h
     torch.cuda.empty_cache()
@@ -233,6 +252,7 @@ def summary(res, K, peak):
                           "neg_iter": ib["neg_iter"], "ms": res["bicg_ms"],
                           "ms_per_product": res["bicg_ms"] / max(ib["products"], 1)},
         outer_iteration=res["outer"],
+        outer_iteration_gn_backtrack=res["outer_bt"],
         hv_per_s_stateless=1e3 * K / comp["hv"],
         gv_per_s_stateless=1e3 * K / comp["gv"],
         kernels={k: {"launches": s["launches"], "ms_per_step": s["ms"] / K,
@@ -295,7 +315,8 @@ def main():
         "loss": r32["loss"],
     }
     for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
-              "bicgstab_hessian", "outer_iteration", "hv_per_s_stateless",
+              "bicgstab_hessian", "outer_iteration", "outer_iteration_gn_backtrack",
+              "hv_per_s_stateless",
               "gv_per_s_stateless", "kernels"):
         out[k] = s32[k]
     if not args.no_bf16:
@@ -317,7 +338,8 @@ def main():
             "loss": r16["loss"],
         }
         for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
-                  "bicgstab_hessian", "outer_iteration", "kernels"):
+                  "bicgstab_hessian", "outer_iteration",
+                  "outer_iteration_gn_backtrack", "kernels"):
             out["bf16_inputs"][k] = s16[k]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_rows)

@@ -213,6 +213,9 @@ typedef struct hf_iter_params {
   float armijo_c;         /* c of the Armijo condition, in (0, 1)            */
   float shrink;           /* step reduction per rejected trial, in (0, 1)    */
   int32_t max_backtracks; /* reductions tried per candidate, >= 0            */
+  int32_t adapt_damping;  /* 1: compute rho and the next lambda (LM rule)   */
+  int32_t keep_cap;       /* CG-backtracking: iterates kept, 0 = off        */
+  float* keep_buf;        /* device, keep_cap * n fp32, caller-owned         */
 } hf_iter_params;
 
 /* Result of hf_iterate (host struct). */
@@ -226,6 +229,9 @@ typedef struct hf_iter_info {
   double f0, f1;          /* f before and after (f1 = f0 if none accepted)   */
   double alpha;           /* accepted step length, 0 if none                */
   double gTd;             /* g^T delta for the chosen direction             */
+  int32_t backtrack_iter; /* solver iterate chosen by backtracking, -1 off  */
+  double rho;             /* reduction ratio (-inf: undefined; nan: off)    */
+  double damping_next;    /* lambda for the next iteration                  */
 } hf_iter_info;
 
 /*
@@ -245,6 +251,20 @@ typedef struct hf_iter_info {
  *      alpha *= shrink until f(W + alpha d) <= f + c alpha g^T d, at most
  *      max_backtracks reductions; the candidate reaching the lower f wins;
  *   6. W += alpha d in place, and delta = d (zeros if none was accepted).
+ * CG-backtracking (keep_cap > 0; Sec. 2.2 takes the solver's iterates as
+ * candidates for it, after Martens 2010): the solver keeps its iterate after
+ * j updates for j = 1, then j <- max(j + 1, ceil(13 j / 10)), j < max_iters,
+ * the latest keep_cap of them, in keep_buf (keep_cap consecutive vectors of
+ * n floats, overwritten).  f is then evaluated from the final iterate
+ * backwards while it decreases; the last iterate before it rises replaces
+ * the solver's step in 4., and its f serves as the Armijo trial at
+ * alpha = 1.  Damping (adapt_damping = 1; Alg. 1 adjusts lambda in its
+ * second step): rho = (f1 - f0) / (m(p) - m(0)) for the accepted update
+ * p = alpha d, with m the damped quadratic model of eq. (1) and B p from one
+ * stateless curvature product at the old W; damping_next = 3/2 lambda if
+ * rho < 1/4 (also when nothing was accepted or m(p) >= m(0), reported as
+ * rho = -inf), 2/3 lambda if rho > 3/4, else lambda.  Without it rho is NaN
+ * and damping_next = damping.
  *   W      device, n fp32, in/out.  X, y / Xc, yc as for hf_loss_grad /
  *          hf_cg (yc may be NULL only for HF_GAUSS_NEWTON).
  *   delta  device, n fp32, in/out: delta_{k-1} in, delta_k out.

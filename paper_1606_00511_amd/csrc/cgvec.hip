@@ -719,6 +719,17 @@ extern "C" __global__ __launch_bounds__(256) void hf_waxpy(
     out[i] = (float)((w ? (double)w[i] : 0.0) + a * (double)d[i]);
 }
 
+// dst = src, unless the solve has stopped (*skip != 0): keeps a solver
+// iterate for CG-backtracking only if the iteration that formed it ran
+extern "C" __global__ __launch_bounds__(256) void hf_keep_iterate(
+    float* __restrict__ dst, const float* __restrict__ src, long long n,
+    const int* __restrict__ skip) {
+  if (*skip) return;
+  const long long stride = (long long)gridDim.x * NT;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride)
+    dst[i] = src[i];
+}
+
 // per-block partials of the four dot products a_k . b_k
 extern "C" __global__ __launch_bounds__(256) void hf_dots4(
     const float* __restrict__ a0, const float* __restrict__ b0,
@@ -763,6 +774,15 @@ void waxpy(const Launch& L, float* out, const float* w, double a,
   prof_begin(L, "hf_waxpy");
   hipLaunchKernelGGL(hf_waxpy, dim3(nb), dim3(NT), 0, L.stream, out, w, a, d, n);
   prof_end(L, "hf_waxpy", 0.0, (w ? 3.0 : 2.0) * 4.0 * n);
+}
+
+void keep_iterate(const Launch& L, float* dst, const float* src, long long n,
+                  const int* skip) {
+  const int nb = cg_grid(n);
+  prof_begin(L, "hf_keep_iterate");
+  hipLaunchKernelGGL(hf_keep_iterate, dim3(nb), dim3(NT), 0, L.stream, dst, src,
+                     n, skip);
+  prof_end(L, "hf_keep_iterate", 0.0, 2.0 * 4.0 * n);
 }
 
 void dots4(const Launch& L, const float* const a[4], const float* const b[4],

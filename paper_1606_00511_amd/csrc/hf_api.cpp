@@ -24,6 +24,7 @@
 #include "hf.h"
 #include "hf_internal.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -842,12 +843,37 @@ void loss_grad_any(hf_ctx* c, const float* W, const float* X, const int32_t* y,
 
 namespace {
 
+// Iterates kept for CG-backtracking: after j solver updates for every j of
+// the schedule (j = 1, then j <- max(j + 1, ceil(13 j / 10)), j < max_iters,
+// the latest `cap` of them), each into its own vector of buf.  A copy
+// enqueued after the solve has stopped does nothing (device flag).
+struct KeepPlan {
+  std::vector<int> js;   // increasing
+  float* buf = nullptr;
+  KeepPlan(int max_iters, int cap, float* b) : buf(b) {
+    for (int j = 1; j < max_iters; j = std::max(j + 1, (13 * j + 9) / 10))
+      js.push_back(j);
+    if ((int)js.size() > cap) js.erase(js.begin(), js.end() - cap);
+  }
+  // slot of iteration count j, or -1
+  int slot(int j) const {
+    for (size_t i = 0; i < js.size(); ++i)
+      if (js[i] == j) return (int)i;
+    return -1;
+  }
+  void after(const Launch& L, int j, const float* x, long long n,
+             const int* skip) const {
+    const int i = slot(j);
+    if (i >= 0) keep_iterate(L, buf + (size_t)i * n, x, n, skip);
+  }
+};
+
 // CG-Minimize after argument checks; x0 (device, may be null) is the warm
 // start of Alg. 2
 int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
              int b, const float* g, float damping, int32_t max_iters,
              float rel_tol, int32_t mode, const float* x0, float* step,
-             float* neg_dir, hf_cg_info* info) {
+             float* neg_dir, hf_cg_info* info, const KeepPlan* keep = nullptr) {
   std::memset(info, 0, sizeof *info);
   if (!c->pinned) {
     HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
@@ -875,6 +901,7 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
     if (c->prof) c->prof->tag = j;
     product(c, W, Xc, b, p, mode, q, skip);
     cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st);
+    if (keep) keep->after(Lc, j + 1, step, n, skip);
     // Stop enqueueing once the device reports `done` for the previous
     // iteration; the work already queued for this one returns at once.
     HIP_TRY(c, hipMemcpyAsync(&c->pinned[j & 1], st, sizeof(CgState),
@@ -922,7 +949,7 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
 int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
                int b, const float* g, float damping, int32_t max_iters,
                float rel_tol, int32_t mode, const float* x0, float* step,
-               float* neg_dir, hf_cg_info* info) {
+               float* neg_dir, hf_cg_info* info, const KeepPlan* keep = nullptr) {
   std::memset(info, 0, sizeof *info);
   if (!c->pinned) {
     HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
@@ -963,6 +990,7 @@ int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
     product(c, W, Xc, b, sv, mode, t, skip);
     lambda_axpy(c, t, sv, damping, skip);
     bicg_rest(Lc, step, r, rs, p, Ap, sv, t, g, neg_dir, n, j, part, st);
+    if (keep) keep->after(Lc, j + 1, step, n, skip);
     HIP_TRY(c, hipMemcpyAsync(&hostst[j & 1], st, sizeof(BicgState),
                               hipMemcpyDeviceToHost, c->stream));
     HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
@@ -1278,6 +1306,11 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
   if (!(prm->shrink > 0.0f && prm->shrink < 1.0f))
     return fail(c, HF_EINVAL, "shrink must lie in (0, 1)");
   if (prm->max_backtracks < 0) return fail(c, HF_EINVAL, "max_backtracks < 0");
+  if (prm->adapt_damping != 0 && prm->adapt_damping != 1)
+    return fail(c, HF_EINVAL, "adapt_damping must be 0 or 1");
+  if (prm->keep_cap < 0) return fail(c, HF_EINVAL, "keep_cap < 0");
+  if (prm->keep_cap > 0 && (rc = check_ptr(c, prm->keep_buf, "keep_buf")))
+    return rc;
   std::memset(info, 0, sizeof *info);
   const Launch Lc = c->launch();
   const long long n = c->n;
@@ -1316,17 +1349,61 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
     waxpy(Lc, x0v, nullptr, (double)prm->eta, delta, n);
     x0 = x0v;
   }
+  const bool backtrack = prm->keep_cap > 0;
+  const KeepPlan keep(prm->max_iters, prm->keep_cap, prm->keep_buf);
   rc = (prm->solver == HF_SOLVER_CG)
            ? solve_cg(c, W, Xc, yc, bc, g, prm->damping, prm->max_iters,
-                      prm->rel_tol, mode, x0, s, d, &info->solve)
+                      prm->rel_tol, mode, x0, s, d, &info->solve,
+                      backtrack ? &keep : nullptr)
            : solve_bicg(c, W, Xc, yc, bc, g, prm->damping, prm->max_iters,
-                        prm->rel_tol, mode, x0, s, d, &info->solve);
+                        prm->rel_tol, mode, x0, s, d, &info->solve,
+                        backtrack ? &keep : nullptr);
   if (rc != HF_OK) return rc;
 
-  // 4. candidates: the solver's step if it descends, and the oriented
-  // negative-curvature direction rescaled to the step's length
+  // objective at W + a v, reduced in fp64 (one full-batch forward)
+  auto objective = [&](double a, const float* v, double* f) -> int {
+    waxpy(Lc, wt, W, a, v, n);
+    loss_only(c, wt, X, y, b, nullptr, scal + 4);
+    HIP_TRY(c, hipMemcpyAsync(f, scal + 4, sizeof(double),
+                              hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+    info->evals += 1;
+    return HF_OK;
+  };
+
+  // CG-backtracking: from the final iterate back through the kept ones
+  // (those formed before it) while f decreases
+  const float* sb = s;          // the step candidate
+  double f_sb = 0.0;
+  info->backtrack_iter = -1;
+  if (backtrack) {
+    const int iters = info->solve.iters;
+    int j_best = iters;
+    if ((rc = objective(1.0, s, &f_sb))) return rc;
+    for (int i = (int)keep.js.size() - 1; i >= 0; --i) {
+      if (keep.js[i] >= iters) continue;
+      const float* xj = keep.buf + (size_t)i * n;
+      double fj;
+      if ((rc = objective(1.0, xj, &fj))) return rc;
+      if (!(fj < f_sb)) break;
+      sb = xj;
+      f_sb = fj;
+      j_best = keep.js[i];
+    }
+    info->backtrack_iter = j_best;
+    // the kept vectors sit n floats apart, so an earlier iterate may not be
+    // 16-byte aligned: continue with an aligned copy (the warm start's
+    // vector is free once the solve has run)
+    if (sb != s) {
+      waxpy(Lc, x0v, nullptr, 1.0, sb, n);
+      sb = x0v;
+    }
+  }
+
+  // 4. candidates: the step if it descends, and the oriented
+  // negative-curvature direction rescaled to the solver's step length
   const float* da[4] = {g, s, g, d};
-  const float* db[4] = {s, s, d, d};
+  const float* db[4] = {sb, s, d, d};
   dots4(Lc, da, db, n, c->Dp(c->oRed), scal);
   HIP_TRY(c, hipMemcpyAsync(hs, scal, 4 * sizeof(double), hipMemcpyDeviceToHost,
                             c->stream));
@@ -1336,7 +1413,7 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
   struct Cand { int kind; const float* v; double scale, gTd; };
   Cand cand[2];
   int nc = 0;
-  if (gs < 0.0) cand[nc++] = Cand{0, s, 1.0, gs};
+  if (gs < 0.0) cand[nc++] = Cand{0, sb, 1.0, gs};
   if (info->solve.neg_curv && dd > 0.0) {
     const double target = ss > 0.0 ? std::sqrt(ss) : std::sqrt(gg);
     const double sc = target / std::sqrt(dd);
@@ -1349,13 +1426,12 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
   for (int k = 0; k < nc; ++k) {
     double alpha = 1.0;
     for (int t = 0; t <= prm->max_backtracks; ++t) {
-      waxpy(Lc, wt, W, alpha * cand[k].scale, cand[k].v, n);
-      loss_only(c, wt, X, y, b, nullptr, scal + 4);
-      HIP_TRY(c, hipMemcpyAsync(&hs[4], scal + 4, sizeof(double),
-                                hipMemcpyDeviceToHost, c->stream));
-      HIP_TRY(c, hipStreamSynchronize(c->stream));
-      info->evals += 1;
-      const double ft = hs[4];
+      double ft;
+      if (backtrack && cand[k].kind == 0 && t == 0) {
+        ft = f_sb;                        // known from backtracking
+      } else if ((rc = objective(alpha * cand[k].scale, cand[k].v, &ft))) {
+        return rc;
+      }
       if (ft <= f0 + (double)prm->armijo_c * alpha * cand[k].gTd) {
         if (best < 0 || ft < best_f) {
           best = k;
@@ -1366,6 +1442,33 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
       }
       alpha *= (double)prm->shrink;
     }
+  }
+
+  // damping for the next iteration (Levenberg-Marquardt on rho); B p from a
+  // stateless product at the old W (the line search has overwritten the
+  // solve's activation cache)
+  const double lam = (double)prm->damping;
+  info->rho = std::nan("");
+  info->damping_next = lam;
+  if (prm->adapt_damping) {
+    double rho = -INFINITY;
+    if (best >= 0) {
+      const Cand& cb = cand[best];
+      float* q = c->F(c->oQ);
+      if ((rc = hf_hvp(c, W, Xc, yc, Bc, cb.v, mode, q))) return rc;
+      const float* ua[4] = {cb.v, cb.v, cb.v, cb.v};
+      const float* ub[4] = {q, cb.v, q, cb.v};
+      dots4(Lc, ua, ub, n, c->Dp(c->oRed), scal);
+      HIP_TRY(c, hipMemcpyAsync(hs, scal, 2 * sizeof(double),
+                                hipMemcpyDeviceToHost, c->stream));
+      HIP_TRY(c, hipStreamSynchronize(c->stream));
+      const double a = best_alpha * cb.scale;            // p = a v
+      const double pBp = a * a * (hs[0] + lam * hs[1]);
+      const double pred = best_alpha * cb.gTd + 0.5 * pBp;
+      if (pred < 0.0) rho = (best_f - f0) / pred;
+    }
+    info->rho = rho;
+    info->damping_next = rho < 0.25 ? 1.5 * lam : (rho > 0.75 ? lam * (2.0 / 3.0) : lam);
   }
 
   // 6. theta_{k+1} and delta_k

@@ -239,6 +239,9 @@ void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
 // out = w + a d, in fp64 (w null: out = a d)
 void waxpy(const Launch& L, float* out, const float* w, double a,
            const float* d, long long n);
+// dst = src unless *skip (device flag of a solve that has stopped)
+void keep_iterate(const Launch& L, float* dst, const float* src, long long n,
+                  const int* skip);
 // out[k] = a[k] . b[k] for k < 4 (device doubles), fixed summation order;
 // uses the first 4 partial regions of part
 void dots4(const Launch& L, const float* const a[4], const float* const b[4],

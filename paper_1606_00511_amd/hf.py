@@ -56,7 +56,8 @@ class hf_iter_params(ctypes.Structure):
         ("damping", ctypes.c_float), ("max_iters", ctypes.c_int32),
         ("rel_tol", ctypes.c_float), ("eta", ctypes.c_float),
         ("armijo_c", ctypes.c_float), ("shrink", ctypes.c_float),
-        ("max_backtracks", ctypes.c_int32),
+        ("max_backtracks", ctypes.c_int32), ("adapt_damping", ctypes.c_int32),
+        ("keep_cap", ctypes.c_int32), ("keep_buf", ctypes.c_void_p),
     ]
 
 
@@ -66,7 +67,8 @@ class hf_iter_info(ctypes.Structure):
         ("direction", ctypes.c_int32), ("accepted", ctypes.c_int32),
         ("evals", ctypes.c_int32), ("f0", ctypes.c_double),
         ("f1", ctypes.c_double), ("alpha", ctypes.c_double),
-        ("gTd", ctypes.c_double),
+        ("gTd", ctypes.c_double), ("backtrack_iter", ctypes.c_int32),
+        ("rho", ctypes.c_double), ("damping_next", ctypes.c_double),
     ]
 
     def as_dict(self):
@@ -284,16 +286,26 @@ class HFNet:
     def hf_iterate(self, W, X, y, Xc, yc, delta, solver="cg",
                    curvature="hessian", damping=1e-2, max_iters=10, rel_tol=0.0,
                    eta=0.0, armijo_c=1e-4, shrink=0.5, max_backtracks=20,
-                   hybrid_state=0):
+                   hybrid_state=0, adapt_damping=False, keep=None):
         """One outer HF iteration; W and delta are updated in place.
+        keep: None, or a CUDA float32 tensor of cap x n for the iterates that
+        CG-backtracking keeps (cap = keep.shape[0]).  adapt_damping: report
+        rho and the next lambda (info["damping_next"]).
         Returns (info dict, the new hybrid state)."""
         import torch
         B = self._rows(X)
         Bc = self._rows(Xc)
+        cap, kbuf = 0, None
+        if keep is not None:
+            if keep.dim() != 2 or keep.shape[1] != self.n:
+                raise ValueError("keep must be cap x %d" % self.n)
+            cap = int(keep.shape[0])
+            kbuf = _ptr(keep, torch.float32, None, "keep")
         prm = hf_iter_params(SOLVERS[solver], CURVATURES[curvature],
                              float(damping), int(max_iters), float(rel_tol),
                              float(eta), float(armijo_c), float(shrink),
-                             int(max_backtracks))
+                             int(max_backtracks), 1 if adapt_damping else 0,
+                             cap, kbuf)
         hs = ctypes.c_int32(int(hybrid_state))
         info = hf_iter_info()
         self._stream()

@@ -214,3 +214,118 @@ def test_iterate_full_size_speech_net():
                             o, W)
     print("speech: dir %d alpha %g evals %d f %.6f -> %.6f"
           % (gi["direction"], gi["alpha"], gi["evals"], gi["f0"], gi["f1"]))
+
+
+# ---------------------------------------------- CG-backtracking and damping
+def test_kept_iterates_are_the_truncated_solves():
+    """The iterates kept for CG-backtracking are bit-identical to the steps
+    of the same GPU solve truncated at their iteration counts; slots of
+    iterations the solve never reached (it stops at negative curvature on
+    the Hessian) are left untouched."""
+    import torch
+    dims, act, B = (37, 45, 13), "tanh", 130
+    p = WL.make_small(dims, act, B, seed=61)
+    h = net(dims, act, B)
+    W0, X, y = dev(p["theta"]), dev(p["X"]), dev(p["y"])
+    for curv, iters in (("gauss_newton", 9), ("hessian", 9)):
+        J = O.backtrack_schedule(iters, 4)
+        keep = torch.full((len(J), h.n), 123.0, device="cuda")
+        gi, _ = h.hf_iterate(W0.clone(), X, y, X, y, dev(np.zeros(h.n, np.float32)),
+                             solver="cg", curvature=curv, max_iters=iters,
+                             keep=keep)
+        f, g = h.hf_loss_grad(W0, X, y)
+        reached = gi["solve"]["iters"]
+        for i, j in enumerate(J):
+            k = host(keep[i])
+            if j <= reached:
+                step, _, _ = h.hf_cg(W0, X, y, g, 1e-2, j, curv)
+                assert np.array_equal(k, host(step)), (curv, j)
+            else:
+                assert bool((k == 123.0).all()), (curv, j)
+        print(curv, "reached", reached, "kept", J)
+
+
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
+@pytest.mark.parametrize("seed", [24, 25])
+def test_iterate_backtracking_and_damping(solver, seed):
+    """CG-backtracking and the damping rule against the oracle iteration:
+    the chosen iterate, the evaluation count, the accepted update, rho and
+    the next lambda.  Backtracking compares objective values of successive
+    iterates, which can lie within fp32 rounding of each other; where the
+    oracle's compared values do, only the objective of the GPU's choice is
+    checked (equal to the oracle's choice within that rounding)."""
+    import torch
+    dims, act, B = (100, 200, 150, 37), "tanh", 300
+    p = WL.make_small(dims, act, B, seed=seed)
+    th = p["theta"].astype(np.float64)
+    lam, iters = 1e-2, 8
+    o = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver=solver,
+                  curvature_kind="gauss_newton", lam=lam, max_iters=iters,
+                  damping_adapt=True, backtrack_cap=20)
+    h = net(dims, act, B)
+    W = dev(p["theta"].copy())
+    keep = torch.zeros((len(O.backtrack_schedule(iters, 20)), h.n), device="cuda")
+    gi, _ = h.hf_iterate(W, dev(p["X"]), dev(p["y"]), dev(p["X"]), dev(p["y"]),
+                         dev(np.zeros(h.n, np.float32)), solver=solver,
+                         curvature="gauss_newton", damping=lam, max_iters=iters,
+                         adapt_damping=True, keep=keep)
+    sol = o["solve"]
+    assert (gi["solve"]["iters"], gi["solve"]["products"]) == \
+        (sol["iters"], sol["products"])
+    f = lambda x: O.loss(dims, act, th + x, p["X"], p["y"])
+    js = [sol["iters"]] + sorted((j for j in sol["kept"] if j < sol["iters"]),
+                                 reverse=True)
+    xs = {sol["iters"]: sol["step"], **{j: sol["kept"][j] for j in js[1:]}}
+    fs = {j: f(xs[j]) for j in js}
+    # pairs the walk compares, up to one past the oracle's choice
+    k = js.index(o["backtrack_iter"])
+    pairs = [(js[i], js[i + 1]) for i in range(min(k + 1, len(js) - 1))]
+    close = any(abs(fs[a] - fs[b]) <= MARGIN * abs(o["f0"]) for a, b in pairs)
+    print("%s seed %d: oracle bt %d gpu bt %d evals %d/%d rho %.4f/%.4f "
+          "lam %.4g/%.4g close %s" % (solver, seed, o["backtrack_iter"],
+                                      gi["backtrack_iter"], o["evals"], gi["evals"],
+                                      o["rho"], gi["rho"], o["lam_next"],
+                                      gi["damping_next"], close))
+    if close:
+        assert gi["backtrack_iter"] in fs
+        assert abs(fs[gi["backtrack_iter"]] - fs[o["backtrack_iter"]]) <= \
+            2 * MARGIN * abs(o["f0"])
+        return
+    assert gi["backtrack_iter"] == o["backtrack_iter"]
+    kw = dict(solver=solver, damping=lam, max_iters=iters)
+    if sensitivity(dims, act, th, p, kw, "gauss_newton", None) > 1e-4:
+        # Bi-CG-STAB near a breakdown: check the GPU's own update
+        Wn = host(W).astype(np.float64)
+        assert gi["accepted"] == 1
+        assert O.loss(dims, act, Wn, p["X"], p["y"]) <= o["f0"] + 1e-4 * \
+            gi["alpha"] * gi["gTd"] + MARGIN * abs(o["f0"])
+        assert gi["damping_next"] == pytest.approx(
+            O.adapt_damping(np.float32(lam), gi["rho"]), rel=1e-6)
+        return
+    assert gi["evals"] == o["evals"]
+    assert gi["direction"] == o["direction"] and gi["accepted"] == o["accepted"]
+    assert gi["alpha"] == o["alpha"]
+    assert gi["f1"] == pytest.approx(o["f1"], rel=TOL_F)
+    assert rel(host(W).astype(np.float64), o["theta"]) <= TOL_W
+    assert gi["rho"] == pytest.approx(o["rho"], rel=1e-2)
+    if min(abs(o["rho"] - 0.25), abs(o["rho"] - 0.75)) > 1e-2:
+        assert gi["damping_next"] == pytest.approx(o["lam_next"], rel=1e-6)
+
+
+def test_damping_without_an_accepted_step_and_when_off():
+    """Nothing accepted (zero solver budget): rho = -inf and lambda rises by
+    3/2.  Adaptation off: rho is NaN and lambda is returned unchanged."""
+    dims, act, B = (20, 16, 12, 5), "sigmoid", 64
+    p = WL.make_small(dims, act, B, seed=8)
+    h = net(dims, act, B)
+    args = (dev(p["X"]), dev(p["y"]), dev(p["X"]), dev(p["y"]))
+    gi, _ = h.hf_iterate(dev(p["theta"].copy()), *args,
+                         dev(np.zeros(h.n, np.float32)), max_iters=0,
+                         damping=0.02, adapt_damping=True)
+    assert gi["accepted"] == 0 and gi["rho"] == float("-inf")
+    assert gi["damping_next"] == pytest.approx(1.5 * np.float32(0.02), rel=1e-7)
+    gi, _ = h.hf_iterate(dev(p["theta"].copy()), *args,
+                         dev(np.zeros(h.n, np.float32)), max_iters=4,
+                         damping=0.02)
+    assert np.isnan(gi["rho"]) and gi["backtrack_iter"] == -1
+    assert gi["damping_next"] == pytest.approx(np.float32(0.02), rel=1e-7)
