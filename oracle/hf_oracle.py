@@ -53,7 +53,9 @@ lower loss, the negative-curvature candidate is rescaled to the length of
 the solver's step, and the Armijo constants are c = 1e-4, shrink 0.5;
 CG-backtracking keeps iterates at a ratio-1.3 schedule and walks back from
 the final one while f decreases; the damping rule is Levenberg-Marquardt on
-the reduction ratio against the damped model m_k of eq. (1).
+the reduction ratio against the damped model m_k of eq. (1); the
+preconditioner is M = (F + lambda)^(3/4) with F the batch-average squared
+per-example gradient (Martens' form).
 
 Parity pins
 -----------
@@ -63,7 +65,9 @@ brute-force Hessians from second differences, symmetry, PSD-ness, the L = 1
 multinomial-logistic closed form, label independence of G v, hand-computed
 CG cases, exact n-step convergence of CG against ``numpy.linalg.solve``,
 the CG-backtracking rule on a hand-made sequence, rho = 1 on an exactly
-quadratic objective and rho against finite-difference curvature.
+quadratic objective, rho against finite-difference curvature, F against the
+one-layer closed form, and preconditioned CG against plain CG on the
+transformed system.
 """
 
 import numpy as np
@@ -287,7 +291,7 @@ def sgn(x):
 
 
 def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
-                x0=None, snap_at=()):
+                x0=None, snap_at=(), minv=None):
     """CG-Minimize(B_k, -g_k) with B_k(d) = A d + lam d (Alg. 1 steps 3-4).
 
     Minimises m_k(d) = f + g^T d + d^T B_k d / 2 (Sec. 2.1, eq. (1)) from
@@ -298,6 +302,13 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
     with d~ = -sgn(g^T p) p (Sec. 2.2).  ``max_iters`` is the fixed iteration
     budget (Sec. 2.2); the optional relative stop compares |r|^2 with
     rel_tol^2 |g|^2.
+
+    With ``minv`` (the diagonal of M^-1, positive) the recurrences are those
+    of preconditioned CG (Martens 2010 precondition the HF solve; the paper
+    lists pre-conditioning among his modifications, Sec. 2.1): z = M^-1 r,
+    alpha = r.z / kappa, beta = r'.z' / r.z, p = -z + beta p.  The curvature
+    test, the returned step (-g at the first iteration) and the orientation
+    are unchanged, and the relative stop still compares |r|^2.
 
     Returns a dict with step, neg_dir (None if no detection), iters (completed
     updates of the iterate), products (curvature products evaluated,
@@ -315,8 +326,10 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
         x = np.asarray(x0, dtype=np.float64).copy()
         r = g + apply_A(x) + lam * x
         nprod0 = 1
-    p = -r
+    z = r if minv is None else minv * r
+    p = -z
     rr = float(r @ r)
+    rz = float(r @ z)
     res = dict(step=x, neg_dir=None, iters=0, products=nprod0, neg_curv=0,
                neg_iter=-1, pBp=0.0, pHp=0.0, gTd=0.0, rr0=float(g @ g),
                rr_final=rr, kappas=[], dirs=[], kept={})
@@ -336,7 +349,7 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
                        pHp=kappa - lam * float(p @ p), gTd=float(g @ d),
                        rr_final=rr)
             return res
-        alpha = rr / kappa
+        alpha = rz / kappa
         x = x + alpha * p
         r = r + alpha * q
         rr_new = float(r @ r)
@@ -345,19 +358,42 @@ def cg_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
             res["kept"][j + 1] = x.copy()
         if rel_tol > 0.0 and rr_new <= rel_tol * rel_tol * res["rr0"]:
             return res
-        beta = rr_new / rr
-        rr = rr_new
-        p = -r + beta * p
+        z = r if minv is None else minv * r
+        rz_new = float(r @ z)
+        beta = rz_new / rz
+        rz = rz_new
+        p = -z + beta * p
     return res
 
 
 def cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-               rel_tol=0.0, record=False, x0=None, snap_at=()):
+               rel_tol=0.0, record=False, x0=None, snap_at=(), minv=None):
     """CG-Minimize with the curvature operator of the network on the fixed
     curvature batch (Xc, yc) (Alg. 2: the product on one minibatch)."""
     def apply_A(p):
         return curvature(dims, act, theta, Xc, yc, p, mode)
-    return cg_minimize(apply_A, g, lam, max_iters, rel_tol, record, x0, snap_at)
+    return cg_minimize(apply_A, g, lam, max_iters, rel_tol, record, x0, snap_at,
+                       minv)
+
+
+def fisher_diag(dims, act, theta, X, y):
+    """F = (1/B) sum_b grad l_b (.) grad l_b: the average over the batch of
+    the squared per-example gradients (l_b the cross-entropy of example b),
+    each example's gradient taken on its own (a one-row batch).  Martens'
+    preconditioner (2010, Sec. 4.7) is built from this diagonal."""
+    X = np.asarray(X)
+    B = X.shape[0]
+    F = np.zeros(num_params(dims))
+    for b in range(B):
+        _, gb = loss_grad(dims, act, theta, X[b:b + 1], np.asarray(y)[b:b + 1])
+        F += gb * gb
+    return F / B
+
+
+def precond_inverse(F, lam, xi=0.75):
+    """The diagonal of M^-1 for M = (F + lam)^xi (Martens 2010, Sec. 4.7;
+    xi = 3/4 there)."""
+    return (np.asarray(F, dtype=np.float64) + lam) ** (-xi)
 
 
 # ----------------------------------------------------------------- Bi-CG-STAB
@@ -527,7 +563,7 @@ def adapt_damping(lam, rho):
 def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
             lam=1e-2, max_iters=10, rel_tol=0.0, eta=0.0, delta_prev=None,
             hybrid_g=False, c=1e-4, shrink=0.5, max_backtracks=20,
-            damping_adapt=False, backtrack_cap=0):
+            damping_adapt=False, backtrack_cap=0, precondition=False, xi=0.75):
     """One iteration of the distributed HF method on one worker's share
     (Alg. 2, one k), in the paper's order:
 
@@ -549,6 +585,9 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
        not given in the paper (readings: 1e-4 and 0.5).
     6. theta_{k+1} = theta_k + alpha_k delta_k, or theta_k when no candidate
        was accepted.
+
+    With ``precondition`` (CG only) the solve is preconditioned CG with
+    M = (F + lambda)^xi, F = fisher_diag on the batch (X, y) at theta_k.
 
     With ``backtrack_cap`` > 0 the solver keeps its iterates at
     backtrack_schedule(max_iters, backtrack_cap), and the step candidate of
@@ -577,9 +616,13 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
         x0 = eta * np.asarray(delta_prev, dtype=np.float64)
     J = backtrack_schedule(max_iters, backtrack_cap) if backtrack_cap > 0 else []
     if solver == "cg":
+        minv = None
+        if precondition:
+            minv = precond_inverse(fisher_diag(dims, act, theta, X, y), lam, xi)
         sol = cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-                         rel_tol, x0=x0, snap_at=J)
+                         rel_tol, x0=x0, snap_at=J, minv=minv)
     else:
+        assert not precondition, "preconditioning is for CG"
         sol = bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters,
                                mode, rel_tol, x0=x0, snap_at=J)
     s = sol["step"]

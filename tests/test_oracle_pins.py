@@ -780,3 +780,77 @@ def test_iterate_with_backtracking(solver):
     assert r1["backtrack_iter"] == r1["solve"]["iters"]
     assert np.array_equal(r1["theta"], O.iterate(
         dims, act, th, p["X"], p["y"], p["X"], p["y"], **dict(kw, max_iters=1))["theta"])
+
+
+# ---------------------------------------------------------- preconditioning
+def test_fisher_diag_single_layer_closed_form():
+    """L = 1: the gradient of example b's cross-entropy is (p_b - e_{y_b})
+    times [x_b; 1], so F = mean_b of its elementwise square, written out."""
+    dims, act = (5, 4), "sigmoid"
+    p = WL.make_small(dims, act, 9, seed=31)
+    th = p["theta"].astype(np.float64)
+    X, y = p["X"].astype(np.float64), p["y"]
+    W = th[:20].reshape(4, 5)
+    b = th[20:]
+    F = np.zeros(24)
+    for i in range(9):
+        z = W @ X[i] + b
+        e = np.exp(z - z.max())
+        pr = e / e.sum()
+        r = pr.copy()
+        r[y[i]] -= 1.0
+        F += np.concatenate([np.outer(r, X[i]).ravel(), r]) ** 2
+    assert np.allclose(O.fisher_diag(dims, act, th, p["X"], y), F / 9, rtol=1e-12)
+
+
+def test_fisher_diag_bounds_the_squared_gradient():
+    """F = E_b[g_b^2] >= (E_b g_b)^2 = g^2 elementwise, with equality for one
+    example."""
+    dims, act = (8, 6, 5), "tanh"
+    p = WL.make_small(dims, act, 17, seed=32)
+    th = p["theta"].astype(np.float64)
+    F = O.fisher_diag(dims, act, th, p["X"], p["y"])
+    _, g = O.loss_grad(dims, act, th, p["X"], p["y"])
+    assert np.all(F >= g * g - 1e-15)
+    F1 = O.fisher_diag(dims, act, th, p["X"][:1], p["y"][:1])
+    _, g1 = O.loss_grad(dims, act, th, p["X"][:1], p["y"][:1])
+    assert np.allclose(F1, g1 * g1, rtol=1e-14, atol=0)
+    assert np.allclose(O.precond_inverse(F, 0.1, 0.75), (F + 0.1) ** -0.75)
+
+
+@pytest.mark.parametrize("spd", [True, False])
+def test_pcg_is_cg_on_the_transformed_system(spd):
+    """Preconditioned CG with M = diag(m) produces x_j = S x'_j, where x'_j
+    are the plain CG iterates on S B S with gradient S g, S = M^(-1/2)
+    (textbook identity); detection happens at the same iteration with the
+    same kappa.  A unit preconditioner gives plain CG exactly, and on an SPD
+    system the iterates reach numpy.linalg.solve."""
+    rng = np.random.default_rng(7 if spd else 8)
+    n = 12
+    Q = rng.standard_normal((n, n))
+    A = Q @ Q.T + 0.3 * np.eye(n) if spd else Q + Q.T
+    g = rng.standard_normal(n)
+    m = rng.uniform(0.2, 5.0, n)
+    S = np.diag(m ** -0.5)
+    lam = 0.05
+    for j in range(1, 8):
+        pc = O.cg_minimize(lambda v: A @ v, g, lam, j, minv=1.0 / m)
+        Bt = S @ (A + lam * np.eye(n)) @ S
+        tr = O.cg_minimize(lambda v: Bt @ v, S @ g, 0.0, j)
+        assert (pc["iters"], pc["neg_curv"]) == (tr["iters"], tr["neg_curv"])
+        if pc["neg_curv"]:
+            assert pc["pBp"] == pytest.approx(tr["pBp"], rel=1e-9)
+            if pc["neg_iter"] > 0:
+                assert np.allclose(pc["step"], S @ tr["step"], rtol=1e-9, atol=1e-12)
+            break
+        assert np.allclose(pc["step"], S @ tr["step"], rtol=1e-9, atol=1e-12)
+    plain = O.cg_minimize(lambda v: A @ v, g, lam, 6)
+    unit = O.cg_minimize(lambda v: A @ v, g, lam, 6, minv=np.ones(n))
+    assert np.array_equal(plain["step"], unit["step"])
+    assert plain["iters"] == unit["iters"]
+    if spd:
+        # exact after n steps in exact arithmetic; in fp64 the transformed
+        # system (condition number about 170) needs a few more
+        full = O.cg_minimize(lambda v: A @ v, g, lam, 2 * n, minv=1.0 / m)
+        ex = np.linalg.solve(A + lam * np.eye(n), -g)
+        assert np.linalg.norm(full["step"] - ex) <= 1e-12 * np.linalg.norm(ex)
