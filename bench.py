@@ -18,7 +18,8 @@ accumulation (reported under "bf16_inputs").  After each leg's timed steps,
 10 Bi-CG-STAB iterations (Alg. 3) and one full outer iteration (Alg. 2:
 gradient, Hessian CG, direction choice, Armijo line search) are timed on
 their own, and once more on the Gauss-Newton matrix with CG-backtracking
-over 16 kept iterates and the damping adjustment.
+over 16 kept iterates and the damping adjustment, unpreconditioned and (fp32
+only) with Martens' diagonal preconditioner.
 
 Prints one JSON line (rank 0; there is only one GPU).
 """
@@ -210,10 +211,29 @@ def run_leg(args, w, inp, prec):
                 "backtrack_iter": it["backtrack_iter"],
                 "rho": it["rho"] if math.isfinite(it["rho"]) else None,
                 "damping_next": it["damping_next"]}
+    # and preconditioned (Martens' diagonal preconditioner; fp32 contexts)
+    outer_pc = None
+    if prec == "fp32":
+        Wk.copy_(W)
+        dk.zero_()
+        e0.record()
+        it, _ = net.hf_iterate(Wk, X, y, Xc, yc, dk, solver="cg",
+                               curvature="gauss_newton", damping=lam,
+                               max_iters=w.cg_iters, adapt_damping=True,
+                               keep=keep, precondition=True)
+        e1.record()
+        torch.cuda.synchronize()
+        outer_pc = {"ms": e0.elapsed_time(e1), "direction": it["direction"],
+                    "alpha": it["alpha"], "evals": it["evals"], "f0": it["f0"],
+                    "f1": it["f1"], "solve_products": it["solve"]["products"],
+                    "backtrack_iter": it["backtrack_iter"],
+                    "rho": it["rho"] if math.isfinite(it["rho"]) else None,
+                    "damping_next": it["damping_next"]}
     del Wk, dk, keep
     res = dict(stats=stats, comp=comp, products=products, elapsed=t1 - t0,
                ig=ig, ih=ih, ib=ib, bicg_ms=bicg_ms,
-               outer=outer, outer_bt=outer_bt, loss=float(loss.item()))
+               outer=outer, outer_bt=outer_bt, outer_pc=outer_pc,
+               loss=float(loss.item()))
     net.close()
     del net, W, X, y, v, Xc, yc, loss, grad, hv, gv, step_g, nd_g, step_h, nd_h
     torch.cuda.empty_cache()
@@ -253,6 +273,7 @@ def summary(res, K, peak):
                           "ms_per_product": res["bicg_ms"] / max(ib["products"], 1)},
         outer_iteration=res["outer"],
         outer_iteration_gn_backtrack=res["outer_bt"],
+        outer_iteration_gn_precond=res["outer_pc"],
         hv_per_s_stateless=1e3 * K / comp["hv"],
         gv_per_s_stateless=1e3 * K / comp["gv"],
         kernels={k: {"launches": s["launches"], "ms_per_step": s["ms"] / K,
@@ -316,7 +337,7 @@ def main():
     }
     for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
               "bicgstab_hessian", "outer_iteration", "outer_iteration_gn_backtrack",
-              "hv_per_s_stateless",
+              "outer_iteration_gn_precond", "hv_per_s_stateless",
               "gv_per_s_stateless", "kernels"):
         out[k] = s32[k]
     if not args.no_bf16:

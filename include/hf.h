@@ -168,6 +168,34 @@ int hf_cg(hf_ctx* ctx, const float* W, const float* Xc, const int32_t* yc,
           hf_cg_info* info);
 
 /*
+ * hf_pcg: hf_cg preconditioned by the diagonal M (the pre-conditioning of
+ * Martens' HF that Sec. 2.1 lists): z = M^-1 r, p_0 = -z_0,
+ * alpha = r.z / p^T B_k p, beta = r'.z' / r.z, p = -z' + beta p.  The
+ * detection test p^T B_k p <= 0, the returned step (-g at the first
+ * iteration), the orientation of d~ and the relative stop on |r| / |g| are
+ * those of hf_cg.
+ *   minv   device, n fp32 (parameter layout), the diagonal of M^-1, > 0;
+ *          e.g. (F + lambda)^(-3/4) with F from hf_fisher_diag
+ * Other arguments, outputs and errors as for hf_cg.
+ */
+int hf_pcg(hf_ctx* ctx, const float* W, const float* Xc, const int32_t* yc,
+           int64_t Bc, const float* g, float damping, int32_t max_iters,
+           float rel_tol, int32_t mode, const float* minv, float* step,
+           float* neg_dir, hf_cg_info* info);
+
+/*
+ * hf_fisher_diag: out = (1/B) sum_b grad l_b (.) grad l_b, the batch average
+ * of the squared per-example gradients of the cross-entropy l_b of example
+ * b (parameter layout; the diagonal Martens' preconditioner is built from).
+ * One forward and one backward pass; the weight blocks are the weight-
+ * gradient contraction of squared operands.  HF_FP32 contexts only
+ * (HF_EINVAL otherwise).  X, y, B as for hf_loss_grad; out device, n fp32.
+ * Asynchronous on the context's stream.
+ */
+int hf_fisher_diag(hf_ctx* ctx, const float* W, const float* X,
+                   const int32_t* y, int64_t B, float* out);
+
+/*
  * hf_bicgstab: Bi-CG-STAB (Alg. 3; the solver behind the paper's results,
  * Sec. 2.1 footnote) for B_k d = -g with B_k = A + lambda I, A = H or G on
  * the fixed curvature batch (Xc, yc) of Bc rows at theta = W, from d = 0
@@ -216,6 +244,8 @@ typedef struct hf_iter_params {
   int32_t adapt_damping;  /* 1: compute rho and the next lambda (LM rule)   */
   int32_t keep_cap;       /* CG-backtracking: iterates kept, 0 = off        */
   float* keep_buf;        /* device, keep_cap * n fp32, caller-owned         */
+  int32_t precondition;   /* 1: preconditioned CG, M = (F + lambda)^xi      */
+  float precond_exp;      /* xi >= 0 (Martens: 3/4)                          */
 } hf_iter_params;
 
 /* Result of hf_iterate (host struct). */
@@ -264,7 +294,10 @@ typedef struct hf_iter_info {
  * stateless curvature product at the old W; damping_next = 3/2 lambda if
  * rho < 1/4 (also when nothing was accepted or m(p) >= m(0), reported as
  * rho = -inf), 2/3 lambda if rho > 3/4, else lambda.  Without it rho is NaN
- * and damping_next = damping.
+ * and damping_next = damping.  Preconditioning (precondition = 1; CG,
+ * HF_FP32 contexts and damping > 0 only): the gradient pass of 1. also
+ * forms F as hf_fisher_diag does on (X, y), and the solve of 3. is hf_pcg
+ * with M^-1 = (F + lambda)^(-xi).
  *   W      device, n fp32, in/out.  X, y / Xc, yc as for hf_loss_grad /
  *          hf_cg (yc may be NULL only for HF_GAUSS_NEWTON).
  *   delta  device, n fp32, in/out: delta_{k-1} in, delta_k out.

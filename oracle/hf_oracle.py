@@ -376,7 +376,7 @@ def cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
                        minv)
 
 
-def fisher_diag(dims, act, theta, X, y):
+def fisher_diag(dims, act, theta, X, y, kink=0.0):
     """F = (1/B) sum_b grad l_b (.) grad l_b: the average over the batch of
     the squared per-example gradients (l_b the cross-entropy of example b),
     each example's gradient taken on its own (a one-row batch).  Martens'
@@ -385,9 +385,25 @@ def fisher_diag(dims, act, theta, X, y):
     B = X.shape[0]
     F = np.zeros(num_params(dims))
     for b in range(B):
-        _, gb = loss_grad(dims, act, theta, X[b:b + 1], np.asarray(y)[b:b + 1])
+        _, gb = loss_grad(dims, act, theta, X[b:b + 1], np.asarray(y)[b:b + 1],
+                          kink)
         F += gb * gb
     return F / B
+
+
+def fisher_diag_output_layer(dims, act, theta, X, y):
+    """The output layer's blocks of fisher_diag in closed form: the gradient
+    of example b's cross-entropy with respect to (W_L, b_L) is
+    (p_b - e_{y_b}) times [a_b; 1], a_b the last hidden activation, so the
+    weight block is (1/B) (D^2)^T (A^2) and the bias block (1/B) sum_b D_b^2,
+    D = P - E.  Needs one forward pass only.  Returns (F_W, F_b)."""
+    X = np.asarray(X, dtype=np.float64)
+    B = X.shape[0]
+    Z, A = forward(dims, act, theta, X)
+    D = softmax(Z[-1])
+    D[np.arange(B), np.asarray(y)] -= 1.0
+    Ah = A[-1]
+    return (D * D).T @ (Ah * Ah) / B, (D * D).sum(axis=0) / B
 
 
 def precond_inverse(F, lam, xi=0.75):

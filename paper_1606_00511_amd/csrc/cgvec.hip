@@ -81,6 +81,41 @@ extern "C" __global__ void hf_cg_reset(CgState* __restrict__ st) {
   }
 }
 
+// PC: preconditioned CG with z = minv r; p = -z and the partials of r.z too.
+template <bool PC>
+__device__ __forceinline__ void cg_init_body(
+    const float* __restrict__ g, const float* __restrict__ x0,
+    const float* __restrict__ q, double lambda, float* __restrict__ x,
+    float* __restrict__ r, float* __restrict__ p, float* __restrict__ nd,
+    long long n, double* __restrict__ part_rr, double* __restrict__ part_gg,
+    const float* __restrict__ minv, double* __restrict__ part_rz) {
+  __shared__ double sh[4];
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  double srr = 0.0, sgg = 0.0, srz = 0.0;
+  for (long long i = t0; i < n; i += stride) {
+    const float gv = g[i];
+    float xv = 0.f, rv = gv;
+    if (x0) {
+      xv = x0[i];
+      rv = (float)((double)gv + (double)q[i] + lambda * (double)xv);
+    }
+    const float zv = PC ? (float)((double)minv[i] * (double)rv) : rv;
+    x[i] = xv; r[i] = rv; p[i] = -zv; nd[i] = 0.f;
+    srr += (double)rv * rv;
+    sgg += (double)gv * gv;
+    if (PC) srz += (double)rv * zv;
+  }
+  srr = block_sum(srr, sh);
+  sgg = block_sum(sgg, sh);
+  if (PC) srz = block_sum(srz, sh);
+  if (threadIdx.x == 0) {
+    part_rr[blockIdx.x] = srr;
+    part_gg[blockIdx.x] = sgg;
+    if (PC) part_rz[blockIdx.x] = srz;
+  }
+}
+
 // From x0 = 0: x = 0, r = g, p = -g.  From a warm start x0 (with q = A x0):
 // x = x0, r = g + q + lambda x0 (the gradient of the model at x0), p = -r.
 // d~ = 0.  Partials of r.r and of g.g (the relative stop is against |g|).
@@ -89,45 +124,54 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_init(
     const float* __restrict__ q, double lambda, float* __restrict__ x,
     float* __restrict__ r, float* __restrict__ p, float* __restrict__ nd,
     long long n, double* __restrict__ part_rr, double* __restrict__ part_gg) {
+  cg_init_body<false>(g, x0, q, lambda, x, r, p, nd, n, part_rr, part_gg,
+                      nullptr, nullptr);
+}
+// the same for preconditioned CG: p = -minv r and partials of r.(minv r)
+extern "C" __global__ __launch_bounds__(256) void hf_pcg_init(
+    const float* __restrict__ g, const float* __restrict__ x0,
+    const float* __restrict__ q, double lambda, float* __restrict__ x,
+    float* __restrict__ r, float* __restrict__ p, float* __restrict__ nd,
+    long long n, double* __restrict__ part_rr, double* __restrict__ part_gg,
+    const float* __restrict__ minv, double* __restrict__ part_rz) {
+  cg_init_body<true>(g, x0, q, lambda, x, r, p, nd, n, part_rr, part_gg, minv,
+                     part_rz);
+}
+
+template <bool PC>
+__device__ __forceinline__ void cg_init_fin_body(
+    const double* __restrict__ part_rr, const double* __restrict__ part_gg,
+    const double* __restrict__ part_rz, int nb, double lambda, double tol2,
+    CgState* __restrict__ st) {
   __shared__ double sh[4];
-  const long long stride = (long long)gridDim.x * NT;
-  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  double srr = 0.0, sgg = 0.0;
-  for (long long i = t0; i < n; i += stride) {
-    const float gv = g[i];
-    float xv = 0.f, rv = gv;
-    if (x0) {
-      xv = x0[i];
-      rv = (float)((double)gv + (double)q[i] + lambda * (double)xv);
-    }
-    x[i] = xv; r[i] = rv; p[i] = -rv; nd[i] = 0.f;
-    srr += (double)rv * rv;
-    sgg += (double)gv * gv;
-  }
-  srr = block_sum(srr, sh);
-  sgg = block_sum(sgg, sh);
+  const double rr = total(part_rr, nb, sh);
+  const double gg = total(part_gg, nb, sh);
+  const double rz = PC ? total(part_rz, nb, sh) : rr;
   if (threadIdx.x == 0) {
-    part_rr[blockIdx.x] = srr;
-    part_gg[blockIdx.x] = sgg;
+    st->rr[0] = rr;
+    st->rr[1] = rr;
+    st->rz[0] = rz;
+    st->rz[1] = rz;
+    st->rr0 = gg;
+    st->lambda = lambda;
+    st->tol2 = tol2;
+    st->neg_iter = -1;
+    const bool fin = is_fin(rr) && is_fin(rz);
+    st->status = fin ? 0 : -5;
+    st->done = (rr == 0.0 || !fin) ? 1 : 0;
   }
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_init_fin(
     const double* __restrict__ part_rr, const double* __restrict__ part_gg,
     int nb, double lambda, double tol2, CgState* __restrict__ st) {
-  __shared__ double sh[4];
-  const double rr = total(part_rr, nb, sh);
-  const double gg = total(part_gg, nb, sh);
-  if (threadIdx.x == 0) {
-    st->rr[0] = rr;
-    st->rr[1] = rr;
-    st->rr0 = gg;
-    st->lambda = lambda;
-    st->tol2 = tol2;
-    st->neg_iter = -1;
-    st->status = is_fin(rr) ? 0 : -5;
-    st->done = (rr == 0.0 || !is_fin(rr)) ? 1 : 0;
-  }
+  cg_init_fin_body<false>(part_rr, part_gg, nullptr, nb, lambda, tol2, st);
+}
+extern "C" __global__ __launch_bounds__(256) void hf_pcg_init_fin(
+    const double* __restrict__ part_rr, const double* __restrict__ part_gg,
+    const double* __restrict__ part_rz, int nb, double lambda, double tol2,
+    CgState* __restrict__ st) {
+  cg_init_fin_body<true>(part_rr, part_gg, part_rz, nb, lambda, tol2, st);
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_dot(
@@ -163,11 +207,14 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_dot(
   }
 }
 
-extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
+// PC: alpha = r.z / kappa, and per-block partials of r'.(minv r') as well
+template <bool PC>
+__device__ __forceinline__ void cg_update_body(
     float* __restrict__ x, float* __restrict__ r, const float* __restrict__ p,
     const float* __restrict__ q, long long n, int j,
     const double* __restrict__ dpart, double* __restrict__ rpart,
-    CgState* __restrict__ st) {
+    CgState* __restrict__ st, const float* __restrict__ minv,
+    double* __restrict__ zpart) {
   if (st->done) return;
   __shared__ double sh[4];
   const int nb = gridDim.x;
@@ -175,7 +222,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
   const double pp = total(dpart + MAX_GRID, nb, sh);
   const double lam = st->lambda;
   const double kappa = pq + lam * pp;
-  const double rr = st->rr[j & 1];
+  const double rr = PC ? st->rz[j & 1] : st->rr[j & 1];
   const bool stop = !is_fin(kappa) || kappa <= 0.0;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     st->kappa = kappa;
@@ -198,7 +245,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  double s = 0.0;
+  double s = 0.0, sz = 0.0;
   for (long long i = t0; i < n4; i += stride) {
     const d4 pv = up(((const f32x4*)p)[i]);
     const d4 qv = up(((const f32x4*)q)[i]);
@@ -213,6 +260,11 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
     ((f32x4*)x)[i] = down(xv);
     ((f32x4*)r)[i] = r4;
     s += dot4(r4, r4);
+    if (PC) {
+      const f32x4 m4 = ((const f32x4*)minv)[i];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) sz += (double)r4[k] * (double)(float)((double)m4[k] * (double)r4[k]);
+    }
   }
   for (long long e = n4 * 4 + t0; e < n; e += stride) {
     const double pv = p[e];
@@ -220,9 +272,30 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
     const float rv = (float)((double)r[e] + alpha * ((double)q[e] + lam * pv));
     r[e] = rv;
     s += (double)rv * rv;
+    if (PC) sz += (double)rv * (double)(float)((double)minv[e] * (double)rv);
   }
   s = block_sum(s, sh);
-  if (threadIdx.x == 0) rpart[blockIdx.x] = s;
+  if (PC) sz = block_sum(sz, sh);
+  if (threadIdx.x == 0) {
+    rpart[blockIdx.x] = s;
+    if (PC) zpart[blockIdx.x] = sz;
+  }
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
+    float* __restrict__ x, float* __restrict__ r, const float* __restrict__ p,
+    const float* __restrict__ q, long long n, int j,
+    const double* __restrict__ dpart, double* __restrict__ rpart,
+    CgState* __restrict__ st) {
+  cg_update_body<false>(x, r, p, q, n, j, dpart, rpart, st, nullptr, nullptr);
+}
+extern "C" __global__ __launch_bounds__(256) void hf_pcg_update(
+    float* __restrict__ x, float* __restrict__ r, const float* __restrict__ p,
+    const float* __restrict__ q, long long n, int j,
+    const double* __restrict__ dpart, double* __restrict__ rpart,
+    CgState* __restrict__ st, const float* __restrict__ minv,
+    double* __restrict__ zpart) {
+  cg_update_body<true>(x, r, p, q, n, j, dpart, rpart, st, minv, zpart);
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_neg_dot(
@@ -266,19 +339,24 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_neg_write(
   }
 }
 
-extern "C" __global__ __launch_bounds__(256) void hf_cg_dir(
+// PC: beta = r'.z' / r.z and p = -minv r + beta p
+template <bool PC>
+__device__ __forceinline__ void cg_dir_body(
     const float* __restrict__ r, float* __restrict__ p, long long n, int j,
-    const double* __restrict__ rpart, CgState* __restrict__ st) {
+    const double* __restrict__ rpart, CgState* __restrict__ st,
+    const float* __restrict__ minv, const double* __restrict__ zpart) {
   if (st->done) return;
   __shared__ double sh[4];
   const double rr_new = total(rpart, gridDim.x, sh);
-  const double rr = st->rr[j & 1];
-  const double beta = rr_new / rr;
+  const double rz_new = PC ? total(zpart, gridDim.x, sh) : rr_new;
+  const double rz = PC ? st->rz[j & 1] : st->rr[j & 1];
+  const double beta = rz_new / rz;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     st->rr[(j + 1) & 1] = rr_new;
+    if (PC) st->rz[(j + 1) & 1] = rz_new;
     st->iters = j + 1;
     st->beta = beta;
-    if (!is_fin(rr_new)) {
+    if (!is_fin(rr_new) || !is_fin(rz_new)) {
       st->status = -5;
       st->done = 1;
     } else if (st->tol2 > 0.0 && rr_new <= st->tol2 * st->rr0) {
@@ -290,13 +368,32 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_dir(
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
   for (long long i = t0; i < n4; i += stride) {
     d4 pv = up(((const f32x4*)p)[i]);
-    const d4 rv = up(((const f32x4*)r)[i]);
+    d4 zv = up(((const f32x4*)r)[i]);
+    if (PC) {
+      const f32x4 m4 = ((const f32x4*)minv)[i];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) pv.v[k] = beta * pv.v[k] - rv.v[k];
+      for (int k = 0; k < 4; ++k) zv.v[k] = (double)(float)((double)m4[k] * zv.v[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pv.v[k] = beta * pv.v[k] - zv.v[k];
     ((f32x4*)p)[i] = down(pv);
   }
-  for (long long e = n4 * 4 + t0; e < n; e += stride)
-    p[e] = (float)(beta * (double)p[e] - (double)r[e]);
+  for (long long e = n4 * 4 + t0; e < n; e += stride) {
+    const double zv = PC ? (double)(float)((double)minv[e] * (double)r[e]) : (double)r[e];
+    p[e] = (float)(beta * (double)p[e] - zv);
+  }
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_cg_dir(
+    const float* __restrict__ r, float* __restrict__ p, long long n, int j,
+    const double* __restrict__ rpart, CgState* __restrict__ st) {
+  cg_dir_body<false>(r, p, n, j, rpart, st, nullptr, nullptr);
+}
+extern "C" __global__ __launch_bounds__(256) void hf_pcg_dir(
+    const float* __restrict__ r, float* __restrict__ p, long long n, int j,
+    const double* __restrict__ rpart, CgState* __restrict__ st,
+    const float* __restrict__ minv, const double* __restrict__ zpart) {
+  cg_dir_body<true>(r, p, n, j, rpart, st, minv, zpart);
 }
 
 // ------------------------------------------------------------- launchers
@@ -311,9 +408,21 @@ int cg_part_doubles() { return 10 * MAX_GRID; }
 
 void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
              float* x, float* r, float* p, float* neg_dir, long long n,
-             double lambda, double tol2, double* part, CgState* st) {
+             double lambda, double tol2, double* part, CgState* st,
+             const float* minv) {
   const int nb = cg_grid(n);
   hipLaunchKernelGGL(hf_cg_reset, dim3(1), dim3(64), 0, L.stream, st);
+  if (minv) {
+    prof_begin(L, "hf_pcg_init");
+    hipLaunchKernelGGL(hf_pcg_init, dim3(nb), dim3(NT), 0, L.stream, g, x0, q,
+                       lambda, x, r, p, neg_dir, n, part + 4 * MAX_GRID,
+                       part + 5 * MAX_GRID, minv, part + 6 * MAX_GRID);
+    prof_end(L, "hf_pcg_init", 0.0, (x0 ? 8.0 : 6.0) * 4.0 * n);
+    hipLaunchKernelGGL(hf_pcg_init_fin, dim3(1), dim3(NT), 0, L.stream,
+                       part + 4 * MAX_GRID, part + 5 * MAX_GRID,
+                       part + 6 * MAX_GRID, nb, lambda, tol2, st);
+    return;
+  }
   prof_begin(L, "hf_cg_init");
   hipLaunchKernelGGL(hf_cg_init, dim3(nb), dim3(NT), 0, L.stream, g, x0, q,
                      lambda, x, r, p, neg_dir, n, part + 4 * MAX_GRID,
@@ -325,19 +434,27 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
 
 void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
                   const float* g, float* neg_dir, long long n, int j,
-                  double* part, CgState* st) {
+                  double* part, CgState* st, const float* minv) {
   const int nb = cg_grid(n);
   double* dpart = part;                  // 2 * MAX_GRID: p.q, p.p
   double* rpart = part + 2 * MAX_GRID;   // r.r
   double* gpart = part + 3 * MAX_GRID;   // g.p
+  double* zpart = part + 6 * MAX_GRID;   // r.z (preconditioned)
   prof_begin(L, "hf_cg_dot");
   hipLaunchKernelGGL(hf_cg_dot, dim3(nb), dim3(NT), 0, L.stream, p, q, n,
                      dpart, st);
   prof_end(L, "hf_cg_dot", 0.0, 2.0 * 4.0 * n);
-  prof_begin(L, "hf_cg_update");
-  hipLaunchKernelGGL(hf_cg_update, dim3(nb), dim3(NT), 0, L.stream, x, r, p, q,
-                     n, j, dpart, rpart, st);
-  prof_end(L, "hf_cg_update", 0.0, 6.0 * 4.0 * n);
+  if (minv) {
+    prof_begin(L, "hf_pcg_update");
+    hipLaunchKernelGGL(hf_pcg_update, dim3(nb), dim3(NT), 0, L.stream, x, r, p,
+                       q, n, j, dpart, rpart, st, minv, zpart);
+    prof_end(L, "hf_pcg_update", 0.0, 7.0 * 4.0 * n);
+  } else {
+    prof_begin(L, "hf_cg_update");
+    hipLaunchKernelGGL(hf_cg_update, dim3(nb), dim3(NT), 0, L.stream, x, r, p,
+                       q, n, j, dpart, rpart, st);
+    prof_end(L, "hf_cg_update", 0.0, 6.0 * 4.0 * n);
+  }
   prof_begin(L, "hf_cg_neg_dot");
   hipLaunchKernelGGL(hf_cg_neg_dot, dim3(nb), dim3(NT), 0, L.stream, g, p, n, j,
                      gpart, st);
@@ -346,10 +463,17 @@ void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
   hipLaunchKernelGGL(hf_cg_neg_write, dim3(nb), dim3(NT), 0, L.stream, g, p, x,
                      neg_dir, n, j, gpart, st);
   prof_end(L, "hf_cg_neg_write", 0.0, 2.0 * 4.0 * n);
-  prof_begin(L, "hf_cg_dir");
-  hipLaunchKernelGGL(hf_cg_dir, dim3(nb), dim3(NT), 0, L.stream, r, p, n, j,
-                     rpart, st);
-  prof_end(L, "hf_cg_dir", 0.0, 3.0 * 4.0 * n);
+  if (minv) {
+    prof_begin(L, "hf_pcg_dir");
+    hipLaunchKernelGGL(hf_pcg_dir, dim3(nb), dim3(NT), 0, L.stream, r, p, n, j,
+                       rpart, st, minv, zpart);
+    prof_end(L, "hf_pcg_dir", 0.0, 4.0 * 4.0 * n);
+  } else {
+    prof_begin(L, "hf_cg_dir");
+    hipLaunchKernelGGL(hf_cg_dir, dim3(nb), dim3(NT), 0, L.stream, r, p, n, j,
+                       rpart, st);
+    prof_end(L, "hf_cg_dir", 0.0, 3.0 * 4.0 * n);
+  }
 }
 
 // ========================================================== Bi-CG-STAB
@@ -793,6 +917,24 @@ void dots4(const Launch& L, const float* const a[4], const float* const b[4],
                      b[1], a[2], b[2], a[3], b[3], n, part);
   prof_end(L, "hf_dots4", 0.0, 8.0 * 4.0 * n);
   hipLaunchKernelGGL(hf_dots4_fin, dim3(1), dim3(NT), 0, L.stream, part, nb, out);
+}
+
+// minv = (F + lambda)^(-xi): the diagonal of M^-1 for Martens' M = (F + lambda)^xi
+extern "C" __global__ __launch_bounds__(256) void hf_precond_inv(
+    const float* __restrict__ F, double lambda, double xi, float* __restrict__ minv,
+    long long n) {
+  const long long stride = (long long)gridDim.x * NT;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride)
+    minv[i] = (float)pow((double)F[i] + lambda, -xi);
+}
+
+void precond_inverse(const Launch& L, const float* F, double lambda, double xi,
+                     float* minv, long long n) {
+  const int nb = cg_grid(n);
+  prof_begin(L, "hf_precond_inv");
+  hipLaunchKernelGGL(hf_precond_inv, dim3(nb), dim3(NT), 0, L.stream, F, lambda,
+                     xi, minv, n);
+  prof_end(L, "hf_precond_inv", 0.0, 2.0 * 4.0 * n);
 }
 
 }  // namespace hfk

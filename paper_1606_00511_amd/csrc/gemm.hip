@@ -300,7 +300,10 @@ struct EStore {
 // tiles of K-segment 0 over k, giving sum_k X(m, k) for their rows.
 // M16: 4 x 4 blocks of 16 x 16 x 4 MFMAs per wave instead of 2 x 2 blocks
 // of 32 x 32 x 2.
-template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS, bool M16>
+// SQ: every operand element is squared on its way into LDS (so the product
+// is sum_k X(m, k)^2 Y(n, k)^2, and the bias sums are sums of squares).
+template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS, bool M16,
+          bool SQ = false>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) {
   if (s.skip && *s.skip) return;
   constexpr int W = 2;          // 2 x 2 MFMA blocks per wave
@@ -391,6 +394,12 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     }
   };
   auto sstore = [&](int buf) {
+    if (SQ) {
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int i = 0; i < V1; ++i) g[t][i] *= g[t][i];
+    }
     if (MODE == 0) {
       TX::store(lds[buf][0], tid, g[0]);
       TY::store(lds[buf][1], tid, g[1]);
@@ -624,6 +633,18 @@ HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false, true)
 HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false, true)
 HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, true)
 
+// weight gradient of squared operands: sum over the rows of delta^2 a^2 (the
+// per-example squared gradients of a weight layer, up to the batch scale),
+// bias sums of delta^2
+extern "C" __global__ __launch_bounds__(256, 1) void hf_gemm_wgrad_sq_v4(
+    GemmShape s, EpiArgs e) {
+  gemm_body<0, false, false, 4, EStore, true, true, true>(s, e);
+}
+extern "C" __global__ __launch_bounds__(256, 1) void hf_gemm_wgrad_sq_v1(
+    GemmShape s, EpiArgs e) {
+  gemm_body<0, false, false, 1, EStore, true, true, true>(s, e);
+}
+
 namespace {
 
 typedef void (*GemmKernel)(GemmShape, EpiArgs);
@@ -699,6 +720,10 @@ void gemm_gnbwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
 }
 void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   HF_LAUNCH_SINGLE(hf_gemm_wgrad, L, s, e, mnk(s) * s.nseg,
+                   io(s, s.nseg, s.nseg, s.splits > 1 ? s.splits : 1));
+}
+void gemm_wgrad_sq(const Launch& L, const GemmShape& s, const EpiArgs& e) {
+  HF_LAUNCH_SINGLE(hf_gemm_wgrad_sq, L, s, e, mnk(s) * s.nseg,
                    io(s, s.nseg, s.nseg, s.splits > 1 ? s.splits : 1));
 }
 

@@ -411,7 +411,7 @@ EpiArgs epi(const hf_ctx* c, int hidden) {
 // segment's X operand), both from the same kernel.
 void wgrad(hf_ctx* c, int l, int B, const float* x0, const float* y0,
            const float* x1, const float* y1, int ldy, float* out,
-           const int* skip) {
+           const int* skip, bool sq = false) {
   const Launch Lc = c->launch();
   const int M = c->d[l], N = c->d[l - 1];
   const int nseg = x1 ? 2 : 1;
@@ -423,13 +423,13 @@ void wgrad(hf_ctx* c, int l, int B, const float* x0, const float* y0,
     e.out0 = c->F(c->oSplit);
     e.split_stride = (long long)M * N;
     e.bias_part = c->Dp(c->oBpart);
-    gemm_wgrad(Lc, s, e);
+    (sq ? gemm_wgrad_sq : gemm_wgrad)(Lc, s, e);
     splitk_reduce(Lc, c->F(c->oSplit), c->Dp(c->oBpart), s.splits, M, N,
                   out + c->offW[l], N, out + c->offB[l], skip);
   } else {
     e.out0 = out + c->offW[l];
     e.bias_out = out + c->offB[l];
-    gemm_wgrad(Lc, s, e);
+    (sq ? gemm_wgrad_sq : gemm_wgrad)(Lc, s, e);
   }
 }
 
@@ -816,9 +816,14 @@ void loss_only(hf_ctx* c, const float* W, const float* X, const int32_t* y,
   loss_finalize(c->launch(), c->Dp(c->oLoss), (B + 3) / 4, B, loss, loss64);
 }
 
-// f and g on B rows (arguments already checked)
+// f and g on B rows (arguments already checked).  With `fisher` (fp32
+// contexts) the same backward pass also forms F = (1/B) sum_b grad l_b^2:
+// delta_l carries the 1/B of the mean, so the squared-operand weight
+// gradient B sum_b delta_l^2 a_{l-1}^2 is F's weight block, and B sum_b
+// delta_l^2 its bias block.
 void loss_grad_any(hf_ctx* c, const float* W, const float* X, const int32_t* y,
-                   int b, float* loss, double* loss64, float* grad) {
+                   int b, float* loss, double* loss64, float* grad,
+                   float* fisher = nullptr) {
   if (c->bf16()) {
     forward_plain_h(c, W, X, b, y, true);
     loss_finalize(c->launch(), c->Dp(c->oLoss), (b + 3) / 4, b, loss, loss64);
@@ -835,8 +840,12 @@ void loss_grad_any(hf_ctx* c, const float* W, const float* X, const int32_t* y,
     const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
     const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
     wgrad(c, l, b, c->F(c->oD[l]), Ain, nullptr, nullptr, ldin, grad, nullptr);
+    if (fisher)
+      wgrad(c, l, b, c->F(c->oD[l]), Ain, nullptr, nullptr, ldin, fisher,
+            nullptr, true);
     if (l > 1) backward_data(c, W, l, b, false);
   }
+  if (fisher) waxpy(c->launch(), fisher, nullptr, (double)b, fisher, c->n);
 }
 
 }  // namespace
@@ -873,7 +882,8 @@ struct KeepPlan {
 int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
              int b, const float* g, float damping, int32_t max_iters,
              float rel_tol, int32_t mode, const float* x0, float* step,
-             float* neg_dir, hf_cg_info* info, const KeepPlan* keep = nullptr) {
+             float* neg_dir, hf_cg_info* info, const KeepPlan* keep = nullptr,
+             const float* minv = nullptr) {
   std::memset(info, 0, sizeof *info);
   if (!c->pinned) {
     HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
@@ -896,11 +906,11 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   // a warm start's residual needs one product on the cache
   if (x0) product(c, W, Xc, b, x0, mode, q, nullptr);
   cg_init(Lc, g, x0, x0 ? q : nullptr, step, r, p, neg_dir, n, (double)damping,
-          (double)rel_tol * (double)rel_tol, part, st);
+          (double)rel_tol * (double)rel_tol, part, st, minv);
   for (int j = 0; j < max_iters; ++j) {
     if (c->prof) c->prof->tag = j;
     product(c, W, Xc, b, p, mode, q, skip);
-    cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st);
+    cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st, minv);
     if (keep) keep->after(Lc, j + 1, step, n, skip);
     // Stop enqueueing once the device reports `done` for the previous
     // iteration; the work already queued for this one returns at once.
@@ -1249,6 +1259,46 @@ int hf_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
                   nullptr, step, neg_dir, info);
 }
 
+int hf_pcg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
+           int64_t Bc, const float* g, float damping, int32_t max_iters,
+           float rel_tol, int32_t mode, const float* minv, float* step,
+           float* neg_dir, hf_cg_info* info) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, minv, "minv"))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, Xc, "Xc")) ||
+      (rc = check_ptr(c, g, "g")) || (rc = check_ptr(c, step, "step")) ||
+      (rc = check_ptr(c, neg_dir, "neg_dir")) || (rc = check_batch(c, Bc)))
+    return rc;
+  if (!info) return fail(c, HF_EINVAL, "info is NULL");
+  if (mode != HF_HESSIAN && mode != HF_GAUSS_NEWTON)
+    return fail(c, HF_EINVAL, "unknown mode %d", mode);
+  if (mode == HF_HESSIAN && !yc) return fail(c, HF_EINVAL, "yc is NULL");
+  if (!(damping >= 0.0f) || !std::isfinite(damping))
+    return fail(c, HF_EINVAL, "damping must be finite and >= 0");
+  if (max_iters < 0) return fail(c, HF_EINVAL, "max_iters < 0");
+  if (!(rel_tol >= 0.0f) || !std::isfinite(rel_tol))
+    return fail(c, HF_EINVAL, "rel_tol must be finite and >= 0");
+  return solve_cg(c, W, Xc, yc, (int)Bc, g, damping, max_iters, rel_tol, mode,
+                  nullptr, step, neg_dir, info, nullptr, minv);
+}
+
+int hf_fisher_diag(hf_ctx* c, const float* W, const float* X, const int32_t* y,
+                   int64_t B, float* out) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, X, "X")) ||
+      (rc = check_ptr(c, out, "out")) || (rc = check_batch(c, B)))
+    return rc;
+  if (!y) return fail(c, HF_EINVAL, "y is NULL");
+  if (c->bf16())
+    return fail(c, HF_EINVAL, "hf_fisher_diag needs an HF_FP32 context");
+  // the gradient of the same pass goes to a solver vector no call keeps
+  loss_grad_any(c, W, X, y, (int)B, nullptr, nullptr, c->F(c->oT), out);
+  HIP_TRY(c, hipGetLastError());
+  return HF_OK;
+}
+
 int hf_bicgstab(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
                 int64_t Bc, const float* g, float damping, int32_t max_iters,
                 float rel_tol, int32_t mode, float* step, float* neg_dir,
@@ -1309,6 +1359,18 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
   if (prm->adapt_damping != 0 && prm->adapt_damping != 1)
     return fail(c, HF_EINVAL, "adapt_damping must be 0 or 1");
   if (prm->keep_cap < 0) return fail(c, HF_EINVAL, "keep_cap < 0");
+  if (prm->precondition != 0 && prm->precondition != 1)
+    return fail(c, HF_EINVAL, "precondition must be 0 or 1");
+  if (prm->precondition) {
+    if (prm->solver != HF_SOLVER_CG)
+      return fail(c, HF_EINVAL, "preconditioning is for HF_SOLVER_CG");
+    if (c->bf16())
+      return fail(c, HF_EINVAL, "preconditioning needs an HF_FP32 context");
+    if (!(prm->damping > 0.0f))
+      return fail(c, HF_EINVAL, "preconditioning needs damping > 0");
+    if (!(prm->precond_exp >= 0.0f) || !std::isfinite(prm->precond_exp))
+      return fail(c, HF_EINVAL, "precond_exp must be finite and >= 0");
+  }
   if (prm->keep_cap > 0 && (rc = check_ptr(c, prm->keep_buf, "keep_buf")))
     return rc;
   std::memset(info, 0, sizeof *info);
@@ -1323,8 +1385,19 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
   double* scal = c->Dp(c->oScal);       // [0..3] dots, [4] loss
   double hs[5];
 
-  // 1. f_k and g_k on the batch (X, y)
-  loss_grad_any(c, W, X, y, b, nullptr, scal + 4, g);
+  // 1. f_k and g_k on the batch (X, y); with preconditioning the same pass
+  // forms the squared per-example gradients F (into a Bi-CG-STAB vector,
+  // free under CG), and M^-1 = (F + lambda)^-xi goes to another
+  float* minv = nullptr;
+  if (prm->precondition) {
+    float* F = c->F(c->oS);
+    minv = c->F(c->oT);
+    loss_grad_any(c, W, X, y, b, nullptr, scal + 4, g, F);
+    precond_inverse(Lc, F, (double)prm->damping, (double)prm->precond_exp,
+                    minv, n);
+  } else {
+    loss_grad_any(c, W, X, y, b, nullptr, scal + 4, g);
+  }
   HIP_TRY(c, hipMemcpyAsync(&hs[4], scal + 4, sizeof(double),
                             hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
@@ -1354,7 +1427,7 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
   rc = (prm->solver == HF_SOLVER_CG)
            ? solve_cg(c, W, Xc, yc, bc, g, prm->damping, prm->max_iters,
                       prm->rel_tol, mode, x0, s, d, &info->solve,
-                      backtrack ? &keep : nullptr)
+                      backtrack ? &keep : nullptr, minv)
            : solve_bicg(c, W, Xc, yc, bc, g, prm->damping, prm->max_iters,
                         prm->rel_tol, mode, x0, s, d, &info->solve,
                         backtrack ? &keep : nullptr);

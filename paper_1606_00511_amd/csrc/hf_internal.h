@@ -88,6 +88,9 @@ void gemm_gnbwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
 // Weight gradient (XK = YK = false): out0[z * split_stride + m * ldo + n] = acc,
 // plus the bias sums sum_k X[0](m, k) (see EpiArgs::bias_out / bias_part)
 void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e);
+// The same with every operand element squared (sum_k X^2 Y^2; bias sums of
+// X[0]^2)
+void gemm_wgrad_sq(const Launch& L, const GemmShape& s, const EpiArgs& e);
 
 // --------------------------------------------------------- bf16-input GEMM
 // Precision HF_BF16_INPUTS: every GEMM operand is a bf16 copy (stored as
@@ -184,6 +187,7 @@ void splitk_reduce(const Launch& L, const float* part, const double* bpart,
 // ------------------------------------------------------------------- CG
 struct CgState {
   double rr[2];        // r.r, slot = iteration parity
+  double rz[2];        // r.z, z = M^-1 r (preconditioned CG), same slots
   double rr0, kappa, alpha, beta, pp, pq, gp;
   double lambda, tol2;
   int done, neg, neg_iter, iters, products, status;
@@ -196,14 +200,21 @@ int cg_part_doubles();
 // rr = |r|^2 and rr0 = |g|^2.  x0 and q may be null (start from 0).
 void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
              float* x, float* r, float* p, float* neg_dir, long long n,
-             double lambda, double tol2, double* part, CgState* st);
+             double lambda, double tol2, double* part, CgState* st,
+             const float* minv = nullptr);
 // One CG iteration j after the product q = A p has been formed:
 // kappa = p.q + lambda p.p and the stop test; x += alpha p,
 // r += alpha (q + lambda p); at a detection d~ = -sgn(g.p) p and, at j = 0,
 // x = -g; beta = rr'/rr and p = -r + beta p.
 void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
                   const float* g, float* neg_dir, long long n, int j,
-                  double* part, CgState* st);
+                  double* part, CgState* st, const float* minv = nullptr);
+// With minv (device, n floats, the diagonal of M^-1) cg_init and
+// cg_iteration run preconditioned CG: z = minv r, p = -z at the start,
+// alpha = r.z / kappa, beta = r'.z' / r.z, p = -z' + beta p.
+// minv = (F + lambda)^(-xi), elementwise in fp64
+void precond_inverse(const Launch& L, const float* F, double lambda, double xi,
+                     float* minv, long long n);
 
 // ----------------------------------------------------------- Bi-CG-STAB
 struct BicgState {

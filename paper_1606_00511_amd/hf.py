@@ -30,7 +30,8 @@ PRECS = {"fp32": HF_FP32, "bf16": HF_BF16_INPUTS}
 EXPORTS = (
     "hf_create", "hf_destroy", "hf_set_stream", "hf_num_params",
     "hf_workspace_bytes", "hf_set_workspace", "hf_loss_grad", "hf_hvp",
-    "hf_cg", "hf_bicgstab", "hf_loss", "hf_iterate", "hf_check", "hf_last_error",
+    "hf_cg", "hf_pcg", "hf_fisher_diag", "hf_bicgstab", "hf_loss", "hf_iterate",
+    "hf_check", "hf_last_error",
     "hf_strerror", "hf_prof_enable",
     "hf_prof_reset", "hf_prof_count", "hf_prof_get",
 )
@@ -58,6 +59,7 @@ class hf_iter_params(ctypes.Structure):
         ("armijo_c", ctypes.c_float), ("shrink", ctypes.c_float),
         ("max_backtracks", ctypes.c_int32), ("adapt_damping", ctypes.c_int32),
         ("keep_cap", ctypes.c_int32), ("keep_buf", ctypes.c_void_p),
+        ("precondition", ctypes.c_int32), ("precond_exp", ctypes.c_float),
     ]
 
 
@@ -112,6 +114,9 @@ def lib():
                                  ctypes.POINTER(hf_cg_info)]),
         "hf_bicgstab": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P,
                                        P, ctypes.POINTER(hf_cg_info)]),
+        "hf_pcg": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P, P, P,
+                                  ctypes.POINTER(hf_cg_info)]),
+        "hf_fisher_diag": (ctypes.c_int, [P, P, P, P, I64, P]),
         "hf_loss": (ctypes.c_int, [P, P, P, P, I64, P]),
         "hf_iterate": (ctypes.c_int, [P, P, P, P, I64, P, P, I64,
                                       ctypes.POINTER(hf_iter_params),
@@ -271,6 +276,40 @@ class HFNet:
         self._check(rc)
         return step, neg_dir, info.as_dict()
 
+    def hf_pcg(self, W, Xc, yc, g, minv, damping, max_iters, mode="hessian",
+               rel_tol=0.0, step=None, neg_dir=None):
+        """CG preconditioned by diag(minv) = M^-1 (hf_pcg)."""
+        import torch
+        B = self._rows(Xc)
+        if step is None:
+            step = torch.empty(self.n, dtype=torch.float32, device=self.device)
+        if neg_dir is None:
+            neg_dir = torch.empty(self.n, dtype=torch.float32, device=self.device)
+        info = hf_cg_info()
+        self._stream()
+        self._check(lib().hf_pcg(
+            self._h, _ptr(W, torch.float32, self.n, "W"),
+            _ptr(Xc, torch.float32, None, "Xc"),
+            _ptr(yc, torch.int32, B, "yc") if yc is not None else None, B,
+            _ptr(g, torch.float32, self.n, "g"), float(damping), int(max_iters),
+            float(rel_tol), MODES[mode], _ptr(minv, torch.float32, self.n, "minv"),
+            _ptr(step, torch.float32, self.n, "step"),
+            _ptr(neg_dir, torch.float32, self.n, "neg_dir"), ctypes.byref(info)))
+        return step, neg_dir, info.as_dict()
+
+    def hf_fisher_diag(self, W, X, y, out=None):
+        """(1/B) sum_b grad l_b^2 (hf_fisher_diag)."""
+        import torch
+        B = self._rows(X)
+        if out is None:
+            out = torch.empty(self.n, dtype=torch.float32, device=self.device)
+        self._stream()
+        self._check(lib().hf_fisher_diag(
+            self._h, _ptr(W, torch.float32, self.n, "W"),
+            _ptr(X, torch.float32, None, "X"), _ptr(y, torch.int32, B, "y"), B,
+            _ptr(out, torch.float32, self.n, "out")))
+        return out
+
     def hf_loss(self, W, X, y, loss=None):
         import torch
         B = self._rows(X)
@@ -286,11 +325,13 @@ class HFNet:
     def hf_iterate(self, W, X, y, Xc, yc, delta, solver="cg",
                    curvature="hessian", damping=1e-2, max_iters=10, rel_tol=0.0,
                    eta=0.0, armijo_c=1e-4, shrink=0.5, max_backtracks=20,
-                   hybrid_state=0, adapt_damping=False, keep=None):
+                   hybrid_state=0, adapt_damping=False, keep=None,
+                   precondition=False, precond_exp=0.75):
         """One outer HF iteration; W and delta are updated in place.
         keep: None, or a CUDA float32 tensor of cap x n for the iterates that
         CG-backtracking keeps (cap = keep.shape[0]).  adapt_damping: report
-        rho and the next lambda (info["damping_next"]).
+        rho and the next lambda (info["damping_next"]).  precondition:
+        preconditioned CG with M = (F + lambda)^precond_exp.
         Returns (info dict, the new hybrid state)."""
         import torch
         B = self._rows(X)
@@ -305,7 +346,8 @@ class HFNet:
                              float(damping), int(max_iters), float(rel_tol),
                              float(eta), float(armijo_c), float(shrink),
                              int(max_backtracks), 1 if adapt_damping else 0,
-                             cap, kbuf)
+                             cap, kbuf, 1 if precondition else 0,
+                             float(precond_exp))
         hs = ctypes.c_int32(int(hybrid_state))
         info = hf_iter_info()
         self._stream()

@@ -1,0 +1,200 @@
+"""GPU parity of Martens' diagonal preconditioner (Sec. 2.1 lists it among
+the modifications of HF): the squared per-example gradient F
+(hf_fisher_diag), preconditioned CG (hf_pcg) and the preconditioned outer
+iteration, against the fp64 oracle on the same seeded inputs.
+
+Bars: F within rel-L2 1e-4 (a sum of non-negative terms, no cancellation);
+PCG with identical iterations, products, detections and sign of the
+detected curvature, and on a damped single-layer net the exact solve
+within 1e-4; the outer iteration with the bar of the other iteration tests.
+At the speech net's full size, where per-example backpropagation in fp64 is
+out of reach, the output layer's blocks of F are checked against their
+forward-only closed form, and every block against F >= g^2.
+"""
+
+import gc
+
+import numpy as np
+import pytest
+
+from oracle import hf_oracle as O
+from paper_1606_00511_amd import workloads as WL
+from tests.parity_util import check, rel
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def host(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def net(dims, act, B, prec="fp32"):
+    from paper_1606_00511_amd.hf import HFNet
+    return HFNet(dims, act, B, prec=prec)
+
+
+CASES = [((100, 200, 150, 37), "tanh", 300),
+         ((100, 200, 150, 37), "relu", 300),
+         ((37, 45, 13), "sigmoid", 130),
+         ((40, 96, 1973), "sigmoid", 200),
+         ((64, 1100, 10), "tanh", 300)]
+
+
+@pytest.mark.parametrize("case", CASES, ids=["x".join(map(str, c[0])) + "-" + c[1]
+                                             for c in CASES])
+def test_fisher_diag(case):
+    dims, act, B = case
+    p = WL.make_small(dims, act, B, seed=41 + B)
+    h = net(dims, act, B)
+    F = host(h.hf_fisher_diag(dev(p["theta"]), dev(p["X"]), dev(p["y"])))
+    h.hf_check()
+    ref = O.fisher_diag(dims, act, p["theta"], p["X"], p["y"])
+    err, bound = check(F, ref, act, lambda k: O.fisher_diag(
+        dims, act, p["theta"], p["X"], p["y"], kink=k))
+    print("F rel %.2e (bound %.2e)" % (err, bound))
+    assert np.all(F >= 0.0)
+
+
+def pcg_pair(dims, act, p, g, minv, lam, iters, mode, rel_tol=0.0):
+    h = net(dims, act, p["X"].shape[0])
+    step, nd, gi = h.hf_pcg(dev(p["theta"]), dev(p["X"]), dev(p["y"]),
+                            dev(g.astype(np.float32)), dev(minv.astype(np.float32)),
+                            lam, iters, mode, rel_tol=rel_tol)
+    oi = O.cg_network(dims, act, p["theta"], p["X"], p["y"],
+                      g.astype(np.float32).astype(np.float64), lam, iters, mode,
+                      rel_tol, minv=minv.astype(np.float32).astype(np.float64))
+    return host(step), host(nd), gi, oi
+
+
+@pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
+@pytest.mark.parametrize("act", ["sigmoid", "tanh"])
+def test_pcg_counts_and_signs(act, mode):
+    dims, B = (100, 200, 150, 37), 300
+    p = WL.make_small(dims, act, B, seed=43)
+    _, g = O.loss_grad(dims, act, p["theta"], p["X"], p["y"])
+    lam = 1e-2
+    minv = O.precond_inverse(O.fisher_diag(dims, act, p["theta"], p["X"], p["y"]),
+                             lam)
+    step, nd, gi, oi = pcg_pair(dims, act, p, g, minv, lam, 8, mode)
+    print(act, mode, {k: gi[k] for k in ("iters", "products", "neg_curv",
+                                         "neg_iter", "pBp")}, oi["pBp"])
+    assert (gi["iters"], gi["products"], gi["neg_curv"], gi["neg_iter"]) == \
+        (oi["iters"], oi["products"], oi["neg_curv"], oi["neg_iter"])
+    if oi["neg_curv"]:
+        assert np.sign(gi["pBp"]) == np.sign(oi["pBp"])
+        assert gi["pBp"] == pytest.approx(oi["pBp"], rel=1e-3)
+    assert rel(step, oi["step"]) <= 1e-3
+
+
+def test_pcg_damped_single_layer_reaches_the_solution():
+    """L = 1 with damping: B = G + lambda I is SPD and explicit; PCG with
+    the Fisher preconditioner reaches numpy.linalg.solve (stopped at a
+    relative residual of 1e-6, so the error is below cond(B) 1e-6)."""
+    dims, act, B = (5, 4), "sigmoid", 40
+    p = WL.make_small(dims, act, B, seed=44)
+    n = WL.num_params(dims)
+    lam = 0.05
+    Bm = np.stack([O.curvature(dims, act, p["theta"], p["X"], p["y"], e,
+                               "gauss_newton") for e in np.eye(n)], axis=1)
+    Bm += lam * np.eye(n)
+    _, g = O.loss_grad(dims, act, p["theta"], p["X"], p["y"])
+    g32 = g.astype(np.float32).astype(np.float64)
+    minv = O.precond_inverse(O.fisher_diag(dims, act, p["theta"], p["X"], p["y"]),
+                             lam)
+    step, _, gi, oi = pcg_pair(dims, act, p, g32, minv, lam, 2 * n, "gauss_newton",
+                               rel_tol=1e-6)
+    ex = np.linalg.solve(Bm, -g32)
+    print("cond", np.linalg.cond(Bm), "iters", gi["iters"], oi["iters"],
+          "err", rel(step, ex), rel(oi["step"], ex))
+    assert gi["neg_curv"] == 0 and gi["iters"] < 2 * n
+    assert rel(step, ex) <= 1e-4
+    assert rel(oi["step"], ex) <= 1e-4
+
+
+@pytest.mark.parametrize("curv", ["hessian", "gauss_newton"])
+def test_iterate_preconditioned(curv):
+    """One preconditioned outer iteration against the oracle: curvature,
+    solver counts and detections, chosen direction, acceptance, evaluation
+    count, step length, f and the new weights."""
+    from tests.test_gpu_iterate import MARGIN, TOL_F, TOL_W, ties
+    dims, act, B = (100, 200, 150, 37), "tanh", 300
+    p = WL.make_small(dims, act, B, seed=45)
+    th = p["theta"].astype(np.float64)
+    o = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver="cg",
+                  curvature_kind=curv, lam=1e-2, max_iters=8, precondition=True)
+    h = net(dims, act, B)
+    W = dev(p["theta"].copy())
+    gi, _ = h.hf_iterate(W, dev(p["X"]), dev(p["y"]), dev(p["X"]), dev(p["y"]),
+                         dev(np.zeros(h.n, np.float32)), solver="cg",
+                         curvature=curv, damping=1e-2, max_iters=8,
+                         precondition=True)
+    s, so = gi["solve"], o["solve"]
+    print(curv, s["iters"], so["iters"], gi["direction"], o["direction"],
+          gi["alpha"], o["alpha"], gi["f1"], o["f1"])
+    assert (s["iters"], s["products"], s["neg_curv"]) == \
+        (so["iters"], so["products"], so["neg_curv"])
+    assert gi["f0"] == pytest.approx(o["f0"], rel=TOL_F)
+    Wn = host(W).astype(np.float64)
+    if ties(o):
+        assert O.loss(dims, act, Wn, p["X"], p["y"]) <= o["f0"] + 1e-4 * \
+            gi["alpha"] * gi["gTd"] + MARGIN * abs(o["f0"])
+        return
+    assert gi["direction"] == o["direction"] and gi["accepted"] == o["accepted"]
+    assert gi["evals"] == o["evals"] and gi["alpha"] == o["alpha"]
+    assert gi["f1"] == pytest.approx(o["f1"], rel=TOL_F)
+    assert rel(Wn, o["theta"]) <= TOL_W
+
+
+def test_preconditioning_rejections():
+    """Preconditioning takes CG, an fp32 context and damping > 0; the Fisher
+    diagonal takes an fp32 context.  Rejections are HF_EINVAL."""
+    from paper_1606_00511_amd.hf import HFError, HF_EINVAL
+    dims, act, B = (20, 16, 5), "sigmoid", 32
+    p = WL.make_small(dims, act, B, seed=46)
+    args = (dev(p["X"]), dev(p["y"]), dev(p["X"]), dev(p["y"]))
+    h = net(dims, act, B)
+    for kw in (dict(solver="bicgstab"), dict(damping=0.0)):
+        with pytest.raises(HFError) as ei:
+            h.hf_iterate(dev(p["theta"].copy()), *args,
+                         dev(np.zeros(h.n, np.float32)), precondition=True, **kw)
+        assert ei.value.code == HF_EINVAL
+    hb = net(dims, act, B, "bf16")
+    with pytest.raises(HFError) as ei:
+        hb.hf_fisher_diag(dev(p["theta"]), dev(p["X"]), dev(p["y"]))
+    assert ei.value.code == HF_EINVAL
+    with pytest.raises(HFError) as ei:
+        hb.hf_iterate(dev(p["theta"].copy()), *args,
+                      dev(np.zeros(hb.n, np.float32)), precondition=True)
+    assert ei.value.code == HF_EINVAL
+
+
+def test_fisher_diag_full_size_speech_net():
+    """The speech-frame net at full batch: the output layer's blocks of F
+    against the forward-only closed form (fp64), and F >= g^2 in every
+    block with the GPU's own gradient (up to fp32 rounding)."""
+    import torch
+    w = WL.WORKLOADS["speech_440_2048x4_1973_sigmoid_b16384"]
+    inp = WL.make(w)
+    gc.collect()
+    torch.cuda.empty_cache()
+    h = net(w.dims, w.act, w.batch)
+    W, X, y = dev(inp["theta"]), dev(inp["X"]), dev(inp["y"])
+    F = host(h.hf_fisher_diag(W, X, y)).astype(np.float64)
+    _, g = h.hf_loss_grad(W, X, y)
+    g = host(g).astype(np.float64)
+    FW, Fb = O.fisher_diag_output_layer(w.dims, w.act, inp["theta"], inp["X"],
+                                        inp["y"])
+    C, d = w.dims[-1], w.dims[-2]
+    Fo = F[-(C * d + C):]
+    eW, eb = rel(Fo[:C * d], FW.ravel()), rel(Fo[C * d:], Fb)
+    print("output-layer F rel: weights %.2e bias %.2e" % (eW, eb))
+    assert eW <= 1e-4 and eb <= 1e-4
+    assert np.all(F >= g * g * (1 - 1e-4) - 1e-30)
+    h.close()

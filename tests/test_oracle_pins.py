@@ -854,3 +854,20 @@ def test_pcg_is_cg_on_the_transformed_system(spd):
         full = O.cg_minimize(lambda v: A @ v, g, lam, 2 * n, minv=1.0 / m)
         ex = np.linalg.solve(A + lam * np.eye(n), -g)
         assert np.linalg.norm(full["step"] - ex) <= 1e-12 * np.linalg.norm(ex)
+
+
+def test_fisher_output_layer_closed_form_matches_definition():
+    """The forward-only closed form of the output layer's blocks equals the
+    per-example definition on a three-layer net, and F's ReLU kink moves
+    only the hidden layers' blocks."""
+    for act in ("tanh", "relu"):
+        dims = (9, 7, 6, 5)
+        p = WL.make_small(dims, act, 23, seed=33)
+        th = p["theta"].astype(np.float64)
+        F = O.fisher_diag(dims, act, th, p["X"], p["y"])
+        FW, Fb = O.fisher_diag_output_layer(dims, act, th, p["X"], p["y"])
+        nW = 5 * 6
+        assert np.allclose(F[-(nW + 5):-5], FW.ravel(), rtol=1e-12, atol=1e-16)
+        assert np.allclose(F[-5:], Fb, rtol=1e-12, atol=1e-16)
+    Fk = O.fisher_diag(dims, "relu", th, p["X"], p["y"], kink=0.5)
+    assert np.allclose(Fk[-(nW + 5):], F[-(nW + 5):], rtol=1e-12)
