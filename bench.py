@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-share", action="store_true",
+                    help="skip the one-worker-share CG timing")
     ap.add_argument("--no-bf16", action="store_true",
                     help="skip the bf16-operand leg")
     ap.add_argument("--cpu-rows", type=int, default=0,
@@ -161,10 +163,13 @@ def run_leg(args, w, inp, prec):
     products = 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    step_ms = []
     for _ in range(args.steps):
+        ts = time.perf_counter()
         ig, ih = step()
         products += 2 + ig["products"] + ih["products"]
         torch.cuda.synchronize()
+        step_ms.append(1e3 * (time.perf_counter() - ts))
         for i, k in enumerate(names):
             comp[k] += ev[i].elapsed_time(ev[i + 1])
     torch.cuda.synchronize()
@@ -231,6 +236,7 @@ def run_leg(args, w, inp, prec):
                     "damping_next": it["damping_next"]}
     del Wk, dk, keep
     res = dict(stats=stats, comp=comp, products=products, elapsed=t1 - t0,
+               step_ms=step_ms,
                ig=ig, ih=ih, ib=ib, bicg_ms=bicg_ms,
                outer=outer, outer_bt=outer_bt, outer_pc=outer_pc,
                loss=float(loss.item()))
@@ -238,6 +244,50 @@ def run_leg(args, w, inp, prec):
     del net, W, X, y, v, Xc, yc, loss, grad, hv, gv, step_g, nd_g, step_h, nd_h
     torch.cuda.empty_cache()
     return res
+
+
+def one_worker_share(WL):
+    """The speech net at one worker's share of a 32-worker step: the gradient
+    on 4,096 rows, then CG on G + lambda I over a 1,024-row curvature batch
+    for 200 iterations, with the per-iteration time split into the
+    curvature product and the CG vector kernels."""
+    import torch
+    from paper_1606_00511_amd.hf import HFNet
+    w = WL.WORKLOADS["speech_440_2048x4_1973_sigmoid_b4096_c1024"]
+    inp = WL.make(w)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+    W, X, y = d(inp["theta"]), d(inp["X"]), d(inp["y"])
+    Xc, yc = X[:w.curv_batch].contiguous(), y[:w.curv_batch].contiguous()
+    net = HFNet(w.dims, w.act, w.batch)
+    loss, grad = net.hf_loss_grad(W, X, y)
+    net.hf_cg(W, Xc, yc, grad, w.damping, 5, "gauss_newton")       # warm-up
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    net.prof_enable(True)
+    net.prof_reset()
+    e[0].record()
+    net.hf_loss_grad(W, X, y, loss, grad)
+    e[1].record()
+    _, _, info = net.hf_cg(W, Xc, yc, grad, w.damping, w.cg_iters, "gauss_newton")
+    e[2].record()
+    torch.cuda.synchronize()
+    st = net.prof_stats()
+    net.prof_enable(False)
+    net.close()
+    vec = [k for k in st if k.startswith("hf_cg_")]
+    vec_ms = sum(st[k]["ms"] for k in vec)
+    vec_b = sum(st[k]["bytes"] for k in vec)
+    cg_ms = e[1].elapsed_time(e[2])
+    it = max(info["iters"], 1)
+    return {"workload": w.name, "grad_ms": e[0].elapsed_time(e[1]),
+            "cg_iters": info["iters"], "cg_products": info["products"],
+            "neg_curv": info["neg_curv"], "cg_ms": cg_ms,
+            "cg_ms_per_iter": cg_ms / it,
+            "vector_ms_per_iter": vec_ms / it,
+            "product_ms_per_iter": (cg_ms - vec_ms) / it,
+            "vector_GB/s": vec_b / (vec_ms * 1e-3) / 1e9 if vec_ms else None,
+            "vector_frac_hbm": vec_b / (vec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS
+            if vec_ms else None}
 
 
 def summary(res, K, peak):
@@ -264,6 +314,10 @@ def summary(res, K, peak):
                    "frac_hbm": (vec_b / (vec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS)
                    if vec_ms else None, "ms_per_step": vec_ms / K},
         components_ms={k: comp[k] / K for k in comp},
+        step_ms={"median": float(np.median(res["step_ms"])),
+                 "p10": float(np.percentile(res["step_ms"], 10)),
+                 "p90": float(np.percentile(res["step_ms"], 90)),
+                 "all": [round(t, 3) for t in res["step_ms"]]},
         cg_gn={"iters": ig["iters"], "products": ig["products"],
                "ms_per_iter": comp["cg_gn"] / K / max(ig["products"], 1)},
         cg_hess={"iters": ih["iters"], "products": ih["products"],
@@ -335,11 +389,13 @@ def main():
         },
         "loss": r32["loss"],
     }
-    for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
-              "bicgstab_hessian", "outer_iteration", "outer_iteration_gn_backtrack",
-              "outer_iteration_gn_precond", "hv_per_s_stateless",
-              "gv_per_s_stateless", "kernels"):
+    for k in ("step_ms", "gemm_all", "cg_vector", "components_ms", "cg_gn",
+              "cg_hess", "bicgstab_hessian", "outer_iteration",
+              "outer_iteration_gn_backtrack", "outer_iteration_gn_precond",
+              "hv_per_s_stateless", "gv_per_s_stateless", "kernels"):
         out[k] = s32[k]
+    if not args.no_share:
+        out["one_worker_share"] = one_worker_share(WL)
     if not args.no_bf16:
         # the same step with bf16 GEMM operands (fp32 accumulation)
         r16 = run_leg(args, w, inp, "bf16")
@@ -358,8 +414,8 @@ def main():
                 "flops_per_launch": d16["flops"] / d16["launches"]},
             "loss": r16["loss"],
         }
-        for k in ("gemm_all", "cg_vector", "components_ms", "cg_gn", "cg_hess",
-                  "bicgstab_hessian", "outer_iteration",
+        for k in ("step_ms", "gemm_all", "cg_vector", "components_ms", "cg_gn",
+                  "cg_hess", "bicgstab_hessian", "outer_iteration",
                   "outer_iteration_gn_backtrack", "kernels"):
             out["bf16_inputs"][k] = s16[k]
     if not args.no_cpu_baseline:
