@@ -632,6 +632,9 @@ HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, true)
 HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false, true)
 HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false, true)
 HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, true)
+// split-K partials of the batch-row single-product GEMMs (X K-contiguous,
+// Y row-contiguous): out0[z * split_stride + m * ldo + n]
+HF_GEMM_KERNEL(hf_gemm_part, 0, true, false, EStore, false, true)
 
 // weight gradient of squared operands: sum over the rows of delta^2 a^2 (the
 // per-example squared gradients of a weight layer, up to the batch scale),
@@ -646,6 +649,23 @@ extern "C" __global__ __launch_bounds__(256, 1) void hf_gemm_wgrad_sq_v1(
 }
 
 namespace {
+
+// Sum of the split-K partials in split order (fp64), then the kernel's own
+// epilogue on the sum: the result is that of the unsplit kernel up to the
+// rounding of the partial sums.
+template <class Epi>
+__global__ __launch_bounds__(256) void splitk_epi(EpiArgs e, const float* part,
+                                                  int M, int N, int splits,
+                                                  const int* skip) {
+  if (skip && *skip) return;
+  const long long mn = (long long)M * N;
+  const long long stride = (long long)gridDim.x * 256;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < mn; i += stride) {
+    double v = 0.0;
+    for (int z = 0; z < splits; ++z) v += (double)part[z * mn + i];
+    Epi::apply(e, (int)(i / N), (int)(i % N), (float)v, 0.0f);
+  }
+}
 
 typedef void (*GemmKernel)(GemmShape, EpiArgs);
 
@@ -676,6 +696,49 @@ void launch(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1,
 #define HF_LAUNCH_SINGLE(NAME, L, s, e, fl, by) \
   launch(L, #NAME, NAME##_v4, NAME##_v1, 128, 0, s, e, fl, by)
 
+// Split-K factor for a batch-row single-product GEMM: enough workgroups for
+// two per compute unit while every split keeps at least 512 of K, within
+// the scratch.  1 = no split (always so at the speech net's full batch).
+int row_splits(const GemmShape& s, const EpiArgs& e) {
+  if (!e.split_buf) return 1;
+  const long long tiles = (long long)cdiv(s.M, 128) * cdiv(s.N, 128);
+  const int ktot = s.K * s.nseg;
+  int sp = 1;
+  while (sp < 8 && tiles * sp < 512 && ktot / (2 * sp) >= 512) sp *= 2;
+  while (sp > 1 && (long long)sp * s.M * s.N > e.split_cap) sp /= 2;
+  return sp;
+}
+
+// A batch-row single-product GEMM: one kernel with its epilogue, or, when
+// the output has too few tiles, split-K partials into the scratch (timed
+// under the kernel's name) and the reduce that applies the epilogue.
+template <class Epi>
+void launch_rows(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1,
+                 const GemmShape& s, const EpiArgs& e, double flops, double bytes) {
+  const int sp = row_splits(s, e);
+  if (sp == 1) {
+    launch(L, name, k4, k1, 128, 0, s, e, flops, bytes);
+    return;
+  }
+  GemmShape ps = s;
+  ps.splits = sp;
+  EpiArgs pe = e;
+  pe.out0 = e.split_buf;
+  pe.ldo = s.N;
+  pe.split_stride = (long long)s.M * s.N;
+  launch(L, name, hf_gemm_part_v4, hf_gemm_part_v1, 128, 0, ps, pe, flops,
+         bytes + 4.0 * sp * s.M * (double)s.N);
+  const long long mn = (long long)s.M * s.N;
+  const int nb = (int)std::min<long long>((mn + 255) / 256, 4096);
+  prof_begin(L, "hf_splitk_epi");
+  hipLaunchKernelGGL(splitk_epi<Epi>, dim3(nb), dim3(256), 0, L.stream, e,
+                     e.split_buf, s.M, s.N, sp, s.skip);
+  prof_end(L, "hf_splitk_epi", 0.0, 4.0 * (sp + 1) * (double)mn);
+}
+
+#define HF_LAUNCH_ROWS(NAME, EPI, L, s, e, fl, by) \
+  launch_rows<EPI>(L, #NAME, NAME##_v4, NAME##_v1, s, e, fl, by)
+
 inline double mnk(const GemmShape& s) { return 2.0 * s.M * s.N * (double)s.K; }
 inline double io(const GemmShape& s, int nx, int ny, int nout) {
   return 4.0 * ((double)s.M * s.K * nx + (double)s.N * s.K * ny +
@@ -685,7 +748,7 @@ inline double io(const GemmShape& s, int nx, int ny, int nout) {
 }  // namespace
 
 void gemm_fwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  HF_LAUNCH_SINGLE(hf_gemm_fwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 1));
+  HF_LAUNCH_ROWS(hf_gemm_fwd, EFwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 1));
 }
 void gemm_fwd_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   if (s.X[1]) {
@@ -697,15 +760,15 @@ void gemm_fwd_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   }
 }
 void gemm_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  HF_LAUNCH_SINGLE(hf_gemm_rfwd, L, s, e, mnk(s) * s.nseg,
+  HF_LAUNCH_ROWS(hf_gemm_rfwd, ERFwd, L, s, e, mnk(s) * s.nseg,
                    io(s, s.nseg, s.nseg, e.hidden ? 3 : 1));
 }
 void gemm_bwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   if (e.out2)
-    HF_LAUNCH_SINGLE(hf_gemm_bwd_e2, L, s, e, mnk(s) * s.nseg,
+    HF_LAUNCH_ROWS(hf_gemm_bwd_e2, EBwdE2, L, s, e, mnk(s) * s.nseg,
                      io(s, s.nseg, s.nseg, 3));
   else
-    HF_LAUNCH_SINGLE(hf_gemm_bwd, L, s, e, mnk(s) * s.nseg,
+    HF_LAUNCH_ROWS(hf_gemm_bwd, EBwd, L, s, e, mnk(s) * s.nseg,
                      io(s, s.nseg, s.nseg, 2));
 }
 void gemm_bwd_rbwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
@@ -713,10 +776,10 @@ void gemm_bwd_rbwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
          1, s, e, 3 * mnk(s), io(s, 2, 2, 4));
 }
 void gemm_rbwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  HF_LAUNCH_SINGLE(hf_gemm_rbwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 4));
+  HF_LAUNCH_ROWS(hf_gemm_rbwd, ERBwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 4));
 }
 void gemm_gnbwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
-  HF_LAUNCH_SINGLE(hf_gemm_gnbwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 2));
+  HF_LAUNCH_ROWS(hf_gemm_gnbwd, EGNBwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 2));
 }
 void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   HF_LAUNCH_SINGLE(hf_gemm_wgrad, L, s, e, mnk(s) * s.nseg,

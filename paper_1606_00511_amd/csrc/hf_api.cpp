@@ -199,6 +199,7 @@ struct hf_ctx {
   size_t oZ = 0, oP = 0, oSplit = 0, oBpart = 0, oR = 0, oPv = 0, oQ = 0,
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
   int max_splits = 16;
+  size_t split_floats = 0;  // capacity of the split-K scratch (floats)
   size_t split_elems = 0;
 
   char* ws = nullptr;
@@ -327,6 +328,7 @@ void plan(hf_ctx* c) {
   }
   c->split_elems = mn;
   c->oSplit = take((size_t)c->max_splits * mn * f4);
+  c->split_floats = (size_t)c->max_splits * mn;
   c->oBpart = take((size_t)c->max_splits * dmax * sizeof(double));
   const size_t nv = ((size_t)c->n + 63) & ~size_t(63);
   c->oR = take(nv * f4);
@@ -403,6 +405,8 @@ EpiArgs epi(const hf_ctx* c, int hidden) {
   std::memset(&e, 0, sizeof e);
   e.act = c->act;
   e.hidden = hidden;
+  e.split_buf = c->F(c->oSplit);
+  e.split_cap = (long long)c->split_floats;
   return e;
 }
 

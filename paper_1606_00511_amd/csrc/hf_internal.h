@@ -62,6 +62,11 @@ struct EpiArgs {
   // there is one split, else per split to bias_part[z * M + m]
   float* bias_out;
   double* bias_part;
+  // scratch for split-K of the batch-row GEMMs (partials of the single-
+  // product kernels when the output has too few tiles for the chip), and
+  // its capacity in floats; null: never split
+  float* split_buf;
+  long long split_cap;
 };
 
 // Forward:  out0 = phi(acc + bias) (hidden) or acc + bias (logits);

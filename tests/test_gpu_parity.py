@@ -66,6 +66,10 @@ SMALL = [
     ((64, 1100, 10), "tanh", 15000),
     # ... and with unaligned widths (scalar global loads)
     ((63, 1101, 10), "sigmoid", 15000),
+    # few rows through wide layers: the batch-row GEMMs have too few tiles
+    # and run as split-K partials plus a reduce that applies the epilogue
+    ((256, 2048, 2048, 10), "tanh", 256),
+    ((250, 2049, 1999, 13), "relu", 200),
 ]
 
 
@@ -157,8 +161,10 @@ def assert_cg_parity(gi, oi):
 @pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
 @pytest.mark.parametrize("case", [((784, 100, 10), "sigmoid", 1000, 10),
                                   ((100, 200, 150, 37), "tanh", 300, 12),
-                                  ((100, 200, 150, 37), "relu", 300, 12)],
-                         ids=["digit-784-100-10", "tanh-ragged", "relu-ragged"])
+                                  ((100, 200, 150, 37), "relu", 300, 12),
+                                  ((256, 2048, 2048, 10), "tanh", 256, 6)],
+                         ids=["digit-784-100-10", "tanh-ragged", "relu-ragged",
+                              "split-k-rows"])
 def test_cg_counts_and_signs(case, mode):
     dims, act, B, iters = case
     p = WL.make_small(dims, act, B, seed=303, bias_std=0.0)
