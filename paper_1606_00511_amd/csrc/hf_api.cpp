@@ -377,12 +377,12 @@ int check_batch(hf_ctx* c, int64_t B) {
 // fp32 (the weight gradients are batch means with heavy cancellation, and the
 // splits are combined in fixed order in the reduce kernel); then, enough
 // workgroups to cover the 256 compute units twice while every split keeps
-// at least 256 rows.
+// at least 128 rows.
 int choose_splits(const hf_ctx* c, int M, int N, int Ktot) {
   const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
   int s = 1;
   while (s < c->max_splits && (Ktot + s - 1) / s > 2048) s *= 2;
-  while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 256) s *= 2;
+  while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 128) s *= 2;
   return s;
 }
 
