@@ -329,3 +329,74 @@ def test_damping_without_an_accepted_step_and_when_off():
                          damping=0.02)
     assert np.isnan(gi["rho"]) and gi["backtrack_iter"] == -1
     assert gi["damping_next"] == pytest.approx(np.float32(0.02), rel=1e-7)
+
+
+def test_iterate_all_features_trajectory():
+    """Three outer iterations with every option on (Hybrid-CG, warm start
+    eta = 0.5, preconditioned CG, CG-backtracking, damping adjustment), the
+    caller carrying lambda from damping_next: each step against the oracle
+    started from the GPU's weights, delta and lambda."""
+    import torch
+    dims, act, B = (20, 16, 12, 5), "tanh", 64
+    p = WL.make_small(dims, act, B, seed=5)
+    h = net(dims, act, B)
+    W = dev(p["theta"].copy())
+    delta = dev(np.zeros_like(p["theta"]))
+    iters = 6
+    keep = torch.zeros((len(O.backtrack_schedule(iters, 8)), h.n), device="cuda")
+    lam, hyb = np.float32(0.05), 0
+    for k in range(3):
+        th = host(W).astype(np.float64)
+        dprev = host(delta).astype(np.float64)
+        o = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver="cg",
+                      curvature_kind="hybrid", lam=float(lam), max_iters=iters,
+                      eta=0.5, delta_prev=dprev, hybrid_g=bool(hyb),
+                      damping_adapt=True, backtrack_cap=8, precondition=True)
+        gi, hyb_new = h.hf_iterate(W, dev(p["X"]), dev(p["y"]), dev(p["X"]),
+                                   dev(p["y"]), delta, solver="cg",
+                                   curvature="hybrid", damping=float(lam),
+                                   max_iters=iters, eta=0.5, hybrid_state=hyb,
+                                   adapt_damping=True, keep=keep, precondition=True)
+        s, so = gi["solve"], o["solve"]
+        print("step %d: mode %d/%s iters %d/%d bt %d/%d dir %d/%d alpha %g/%g rho "
+              "%.4f/%.4f lam %.4g" % (k, gi["mode_used"], o["mode_used"], s["iters"],
+                                      so["iters"], gi["backtrack_iter"],
+                                      o["backtrack_iter"], gi["direction"],
+                                      o["direction"], gi["alpha"], o["alpha"],
+                                      gi["rho"], o["rho"], gi["damping_next"]))
+        assert MODE_NAMES[gi["mode_used"]] == o["mode_used"]
+        assert (s["iters"], s["products"], s["neg_curv"]) == \
+            (so["iters"], so["products"], so["neg_curv"])
+        assert gi["f0"] == pytest.approx(o["f0"], rel=TOL_F)
+        if not ties(o):
+            assert gi["backtrack_iter"] == o["backtrack_iter"]
+            assert gi["direction"] == o["direction"] and gi["alpha"] == o["alpha"]
+            assert gi["f1"] == pytest.approx(o["f1"], rel=TOL_F)
+            assert rel(host(W).astype(np.float64), o["theta"]) <= TOL_W
+            if min(abs(o["rho"] - 0.25), abs(o["rho"] - 0.75)) > 1e-2:
+                assert gi["damping_next"] == pytest.approx(o["lam_next"], rel=1e-6)
+        assert gi["f1"] <= gi["f0"]
+        assert hyb_new == int(o["hybrid_g"]) or ties(o)
+        lam, hyb = np.float32(gi["damping_next"]), hyb_new
+
+
+def test_iterate_bf16_with_backtracking_and_damping():
+    """bf16 GEMM operands with CG-backtracking and the damping adjustment:
+    the accepted update descends the exact (fp64) objective, the chosen
+    iterate is one the solve kept (or its final one), and lambda follows the
+    rule applied to the reported rho."""
+    import torch
+    dims, act, B = (100, 200, 150, 37), "sigmoid", 300
+    p = WL.make_small(dims, act, B, seed=58)
+    h = net(dims, act, B, "bf16")
+    W = dev(p["theta"].copy())
+    keep = torch.zeros((len(O.backtrack_schedule(10, 16)), h.n), device="cuda")
+    gi, _ = h.hf_iterate(W, dev(p["X"]), dev(p["y"]), dev(p["X"]), dev(p["y"]),
+                         dev(np.zeros(h.n, np.float32)), curvature="gauss_newton",
+                         max_iters=10, adapt_damping=True, keep=keep)
+    f0 = O.loss(dims, act, p["theta"], p["X"], p["y"])
+    f1 = O.loss(dims, act, host(W).astype(np.float64), p["X"], p["y"])
+    assert gi["accepted"] == 1 and f1 < f0
+    assert gi["backtrack_iter"] in O.backtrack_schedule(10, 16) + [gi["solve"]["iters"]]
+    assert gi["damping_next"] == pytest.approx(
+        O.adapt_damping(np.float32(1e-2), gi["rho"]), rel=1e-6)
