@@ -11,20 +11,33 @@
 // MI355X, chains of dependent 32 x 32 fp32 MFMAs sustain about 90% of the
 // issue rate with 4 accumulators and 98% with 8 or more); the 32 x 32 form
 // writes 32-column row segments in the epilogue instead of 16.  Each kernel
-// takes the form that measured faster for it.  K advances in
-// blocks of 16 through two LDS buffers: while the MFMAs consume one buffer,
-// the next K block is fetched from global memory into registers and then
-// written to the other buffer.  Tiles that lie fully inside the operands
-// take unguarded loads; edge tiles take element-wise guarded loads.
-// (Measured on MI355X: 256 x 256 tiles with 4 x 4 blocks per wave ran
-// 5-15% slower than this shape at one wave per SIMD.)
+// takes the form that measured faster for it.  (Measured on MI355X:
+// 256 x 256 tiles with 4 x 4 blocks per wave ran 5-15% slower than this
+// shape at one wave per SIMD.)
+//
+// K advances in blocks of 16 through three LDS stages filled by direct
+// global-to-LDS loads (16 bytes per lane, no registers in between), issued
+// two blocks ahead of the block the MFMAs consume; each wave waits only for
+// its own loads of that block, then the workgroup meets at one barrier per
+// block.  Rows past an operand's edge are clamped to its last row (they feed
+// only outputs that are never stored); the ragged last K block of a
+// K-segment is loaded through registers with zeros past K.  Operands that
+// are not 16-byte aligned or whose leading dimension is not a multiple of 4,
+// and the squared-operand kernels, stage their loads through registers and
+// two LDS buffers instead (element-wise guarded loads at the edges).
 //
 // LDS layouts (the gfx950 LDS has 64 four-byte banks):
-//  - a row-contiguous operand is kept as [k][row] (row stride 132 floats) and
-//    read with 32-bit LDS loads;
+//  - a row-contiguous operand is kept as [k][row], 128 floats per k row,
+//    with the 16-byte row chunks XOR-swizzled by ((k >> 2) & 3) << 2 and
+//    read with 32-bit LDS loads: the k rows read at once by the four
+//    quarter-waves (16 x 16 form) or the two half-waves (32 x 32 form) fall
+//    in distinct banks, and one direct load fills two whole k rows;
 //  - a K-contiguous operand is kept as [row][k] with its four 16-byte k
 //    chunks XOR-swizzled by (row >> 2) & 3: no bank conflicts on the 128-bit
 //    stores and loads.
+// A direct load writes lane i's 16 bytes at 16 i past the wave's LDS base,
+// so both swizzles are applied by choosing which global chunk each lane
+// fetches.
 // Every single-product GEMM pairs a K-contiguous left operand with a
 // row-contiguous right one (the forward passes take transposed weights),
 // the pairing that measured fastest on MI355X.
@@ -35,6 +48,7 @@
 
 #include "act.h"
 #include "hf_internal.h"
+#include "lds_dma.h"
 
 namespace hfk {
 namespace {
@@ -51,18 +65,44 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // ------------------------------------------------------------ tile loading
 // A ROWS x BK operand tile.  MK: the operand is stored rows x K with K
 // contiguous, kept in LDS as swizzled [row][k] (stride LDK); otherwise
-// K x rows with rows contiguous, kept as [k][row] (stride LDM).  Each of the
-// NT threads moves V1 floats per tile.
+// K x rows with rows contiguous, kept as swizzled [k][row] (stride LDM).
+// Register-staged loads move V1 floats per thread and tile.
 template <bool MK, int VEC, int ROWS>
 struct Tile {
-  // [k][row] row stride: 32-bit LDS loads are served 64 lanes at a time, and
-  // k rows 4 apart (the four quarter-waves of the 16 x 16 form) then sit 16
-  // banks apart (measured: no conflicts; a stride of 136 measured 1.5
-  // conflict cycles per LDS instruction)
-  static constexpr int LDM = ROWS + 4;
+  static constexpr int LDM = ROWS;
   static constexpr int SIZE = (ROWS * LDK > BK * LDM) ? ROWS * LDK : BK * LDM;
   static constexpr int V4 = ROWS * BK / 4 / NT;
   static constexpr int V1 = ROWS * BK / NT;
+  // 16-byte direct loads per wave that fill the tile (4 waves, 1 KB each)
+  static constexpr int INSTR = ROWS * BK / 1024;
+
+  // [k][row] element (kk, row): row chunk row / 4 sits at chunk position
+  // (row / 4) ^ (((kk >> 2) & 3) << 2) of k row kk, which moves the 16-row
+  // runs that lanes read from k rows 4 apart (or 8 apart) into distinct
+  // groups of 16 (or 32) banks.
+  __device__ static __forceinline__ int kr(int kk, int row) {
+    return kk * LDM + (row ^ (((kk >> 2) & 3) << 4));
+  }
+
+  // Element offset, from the operand's K block 0, of the 16-byte chunk that
+  // lane `lane` of wave `wave` loads with its direct load j (chunk position
+  // P = 64 (wave INSTR + j) + lane of the tile).  Rows past the operand's
+  // edge are clamped to its last row: they feed only outputs that are never
+  // stored.
+  __device__ static __forceinline__ size_t dma_src(int ld, int rows, int r0,
+                                                   int wave, int lane, int j) {
+    const int P = (wave * INSTR + j) * 64 + lane;
+    if (MK) {
+      const int row = P / (BK / 4), pos = P % (BK / 4);
+      const int r = min(r0 + row, rows - 1);
+      return (size_t)r * ld + 4 * (pos ^ swz(row));
+    } else {
+      const int kk = P / (ROWS / 4), pos = P % (ROWS / 4);
+      const int c = pos ^ (((kk >> 2) & 3) << 2);
+      const int r = min(r0 + 4 * c, (rows - 1) & ~3);
+      return (size_t)kk * ld + r;
+    }
+  }
 
   // Guarded load of the tile at (r0, k0); elements outside are zero.
   __device__ static __forceinline__ void load(const float* __restrict__ base,
@@ -146,7 +186,7 @@ struct Tile {
           const int row = idx / (BK / 4), c = idx % (BK / 4);
           d = s + row * LDK + ((c ^ swz(row)) * 4);
         } else {
-          d = s + (idx / (ROWS / 4)) * LDM + (idx % (ROWS / 4)) * 4;
+          d = s + kr(idx / (ROWS / 4), (idx % (ROWS / 4)) * 4);
         }
         f32x4 v = {g[4 * i], g[4 * i + 1], g[4 * i + 2], g[4 * i + 3]};
         *(f32x4*)d = v;
@@ -159,7 +199,7 @@ struct Tile {
           const int row = idx / BK, k = idx % BK;
           s[row * LDK + (((k >> 2) ^ swz(row)) * 4) + (k & 3)] = g[i];
         } else {
-          s[(idx / ROWS) * LDM + idx % ROWS] = g[i];
+          s[kr(idx / ROWS, idx % ROWS)] = g[i];
         }
       }
     }
@@ -177,7 +217,7 @@ struct Tile {
       f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
     } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) f[q] = s[(4 * g + q) * LDM + row];
+      for (int q = 0; q < 4; ++q) f[q] = s[kr(4 * g + q, row)];
     }
   }
 
@@ -196,7 +236,7 @@ struct Tile {
       }
     } else {
 #pragma unroll
-      for (int q = 0; q < HK; ++q) f[q] = s[(h * HK + q) * LDM + row];
+      for (int q = 0; q < HK; ++q) f[q] = s[kr(h * HK + q, row)];
     }
   }
 };
@@ -313,7 +353,9 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
   constexpr int T = MODE == 0 ? 2 : (MODE == 1 ? 4 : 3);
   constexpr int SZ = TX::SIZE > TY::SIZE ? TX::SIZE : TY::SIZE;
   constexpr int V1 = TX::V1;
-  __shared__ __attribute__((aligned(16))) float lds[2][T][SZ];
+  constexpr bool DMA = VEC == 4 && !SQ;
+  constexpr int S = DMA ? 3 : 2;      // LDS stages
+  __shared__ __attribute__((aligned(16))) float lds[S][T][SZ];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -414,123 +456,138 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
       TY::store(lds[buf][2], tid, g[2]);
     }
   };
-  auto compute = [&](int buf) {
+  // Operand fragments of one K block (KF k values per lane and block), and
+  // the MFMAs that consume them.
+  constexpr int KF = M16 ? 4 : HK;
+  constexpr int NXT = MODE == 1 ? 2 : 1;     // X tiles per K block
+  struct Frags {
+    float x0[NB][KF], x1[NB][KF], y0[NB][KF], y1[NB][KF];
+  };
+  auto fetch = [&](Frags& f, int buf) {
+    const float* lx0 = lds[buf][0];
+    const float* lx1 = lds[buf][NXT - 1];
+    const float* ly0 = lds[buf][NXT];
+    const float* ly1 = lds[buf][T - 1];
     if constexpr (M16) {
-      float x0[NB][4], y0[NB][4];
       const int rx = wm * 64 + r16, ry = wn * 64 + r16;
-      if (MODE == 0) {
 #pragma unroll
-        for (int a = 0; a < NB; ++a) TX::frag16(lds[buf][0], rx + 16 * a, g16, x0[a]);
+      for (int a = 0; a < NB; ++a) {
+        TX::frag16(lx0, rx + 16 * a, g16, f.x0[a]);
+        if (MODE == 1) TX::frag16(lx1, rx + 16 * a, g16, f.x1[a]);
+      }
 #pragma unroll
-        for (int b = 0; b < NB; ++b) TY::frag16(lds[buf][1], ry + 16 * b, g16, y0[b]);
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-#pragma unroll
-          for (int a = 0; a < NB; ++a)
-#pragma unroll
-            for (int b = 0; b < NB; ++b) acc0[a][b] = mfma16(x0[a][k], y0[b][k], acc0[a][b]);
-      } else if (MODE == 1) {
-        float x1[NB][4], y1[NB][4];
-#pragma unroll
-        for (int a = 0; a < NB; ++a) {
-          TX::frag16(lds[buf][0], rx + 16 * a, g16, x0[a]);
-          TX::frag16(lds[buf][1], rx + 16 * a, g16, x1[a]);
-        }
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          TY::frag16(lds[buf][2], ry + 16 * b, g16, y0[b]);
-          TY::frag16(lds[buf][3], ry + 16 * b, g16, y1[b]);
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-#pragma unroll
-          for (int a = 0; a < NB; ++a)
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-              acc0[a][b] = mfma16(x0[a][k], y0[b][k], acc0[a][b]);
-              acc1[a][b] = mfma16(x1[a][k], y0[b][k], acc1[a][b]);
-              acc1[a][b] = mfma16(x0[a][k], y1[b][k], acc1[a][b]);
-            }
-      } else {
-        float y1[NB][4];
-#pragma unroll
-        for (int a = 0; a < NB; ++a) TX::frag16(lds[buf][0], rx + 16 * a, g16, x0[a]);
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          TY::frag16(lds[buf][1], ry + 16 * b, g16, y0[b]);
-          TY::frag16(lds[buf][2], ry + 16 * b, g16, y1[b]);
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-#pragma unroll
-          for (int a = 0; a < NB; ++a)
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-              acc0[a][b] = mfma16(x0[a][k], y0[b][k], acc0[a][b]);
-              acc1[a][b] = mfma16(x0[a][k], y1[b][k], acc1[a][b]);
-            }
+      for (int b = 0; b < NB; ++b) {
+        TY::frag16(ly0, ry + 16 * b, g16, f.y0[b]);
+        if (MODE != 0) TY::frag16(ly1, ry + 16 * b, g16, f.y1[b]);
       }
     } else {
-      float x0[W][HK], y0[W][HK];
-      if (MODE == 0) {
 #pragma unroll
-        for (int a = 0; a < W; ++a) TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
-#pragma unroll
-        for (int b = 0; b < W; ++b) TY::frag(lds[buf][1], wn * 32 * W + b * 32 + li, h, y0[b]);
-#pragma unroll
-        for (int k = 0; k < HK; ++k)
-#pragma unroll
-          for (int a = 0; a < W; ++a)
-#pragma unroll
-            for (int b = 0; b < W; ++b) acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
-      } else if (MODE == 1) {
-        float x1[W][HK], y1[W][HK];
-#pragma unroll
-        for (int a = 0; a < W; ++a) {
-          TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
-          TX::frag(lds[buf][1], wm * 32 * W + a * 32 + li, h, x1[a]);
-        }
-#pragma unroll
-        for (int b = 0; b < W; ++b) {
-          TY::frag(lds[buf][2], wn * 32 * W + b * 32 + li, h, y0[b]);
-          TY::frag(lds[buf][3], wn * 32 * W + b * 32 + li, h, y1[b]);
-        }
-#pragma unroll
-        for (int k = 0; k < HK; ++k)
-#pragma unroll
-          for (int a = 0; a < W; ++a)
-#pragma unroll
-            for (int b = 0; b < W; ++b) {
-              acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
-              acc1[a][b] = mfma(x1[a][k], y0[b][k], acc1[a][b]);
-              acc1[a][b] = mfma(x0[a][k], y1[b][k], acc1[a][b]);
-            }
-      } else {
-        float y1[W][HK];
-#pragma unroll
-        for (int a = 0; a < W; ++a) TX::frag(lds[buf][0], wm * 32 * W + a * 32 + li, h, x0[a]);
-#pragma unroll
-        for (int b = 0; b < W; ++b) {
-          TY::frag(lds[buf][1], wn * 32 * W + b * 32 + li, h, y0[b]);
-          TY::frag(lds[buf][2], wn * 32 * W + b * 32 + li, h, y1[b]);
-        }
-#pragma unroll
-        for (int k = 0; k < HK; ++k)
-#pragma unroll
-          for (int a = 0; a < W; ++a)
-#pragma unroll
-            for (int b = 0; b < W; ++b) {
-              acc0[a][b] = mfma(x0[a][k], y0[b][k], acc0[a][b]);
-              acc1[a][b] = mfma(x0[a][k], y1[b][k], acc1[a][b]);
-            }
+      for (int a = 0; a < NB; ++a) {
+        TX::frag(lx0, wm * 32 * W + a * 32 + li, h, f.x0[a]);
+        if (MODE == 1) TX::frag(lx1, wm * 32 * W + a * 32 + li, h, f.x1[a]);
       }
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        TY::frag(ly0, wn * 32 * W + b * 32 + li, h, f.y0[b]);
+        if (MODE != 0) TY::frag(ly1, wn * 32 * W + b * 32 + li, h, f.y1[b]);
       }
+    }
+  };
+  auto mma = [&](const Frags& f) {
+#pragma unroll
+    for (int k = 0; k < KF; ++k)
+#pragma unroll
+      for (int a = 0; a < NB; ++a)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          if constexpr (M16) {
+            acc0[a][b] = mfma16(f.x0[a][k], f.y0[b][k], acc0[a][b]);
+            if (MODE == 1) {
+              acc1[a][b] = mfma16(f.x1[a][k], f.y0[b][k], acc1[a][b]);
+              acc1[a][b] = mfma16(f.x0[a][k], f.y1[b][k], acc1[a][b]);
+            } else if (MODE == 2) {
+              acc1[a][b] = mfma16(f.x0[a][k], f.y1[b][k], acc1[a][b]);
+            }
+          } else {
+            acc0[a][b] = mfma(f.x0[a][k], f.y0[b][k], acc0[a][b]);
+            if (MODE == 1) {
+              acc1[a][b] = mfma(f.x1[a][k], f.y0[b][k], acc1[a][b]);
+              acc1[a][b] = mfma(f.x0[a][k], f.y1[b][k], acc1[a][b]);
+            } else if (MODE == 2) {
+              acc1[a][b] = mfma(f.x0[a][k], f.y1[b][k], acc1[a][b]);
+            }
+          }
+        }
+  };
+  auto compute = [&](int buf) {
+    Frags f;
+    fetch(f, buf);
+    mma(f);
   };
 
   // bias sums: thread t owns column t % ROWS and KPT consecutive k of a block
   constexpr int KPT = BK * ROWS / NT;
   const bool do_bias = BIAS && blockIdx.x == 0 && (e.bias_out || e.bias_part);
   double bsum = 0.0;
+  if constexpr (DMA) {
+    constexpr int NYT = T - NXT;               // Y tiles per K block
+    constexpr int LPB = NXT * TX::INSTR + NYT * TY::INSTR;
+    static_assert(S >= 3 && S <= 4 && (S - 2) * LPB < 64, "pipeline depth");
+    size_t offx[TX::INSTR], offy[TY::INSTR];
+#pragma unroll
+    for (int j = 0; j < TX::INSTR; ++j) offx[j] = TX::dma_src(s.ldx, s.M, m0, wave, lane, j);
+#pragma unroll
+    for (int j = 0; j < TY::INSTR; ++j) offy[j] = TY::dma_src(s.ldy, s.N, n0, wave, lane, j);
+    const int nblk = vb1 > vb0 ? vb1 - vb0 : 0;
+    // K block vb into stage st: direct loads for a full block; a ragged last
+    // block takes guarded register loads (zeros past K), whose wait also
+    // drains every direct load issued before them
+    auto issue = [&](int vb, int st) {
+      const int seg = (MODE == 0) ? vb / kbps : 0;
+      const int k0 = (vb - seg * kbps) * BK;
+      if (k0 + BK <= s.K) {
+        const size_t kx = XK ? (size_t)k0 : (size_t)k0 * s.ldx;
+        const size_t ky = YK ? (size_t)k0 : (size_t)k0 * s.ldy;
+#pragma unroll
+        for (int t = 0; t < NXT; ++t) {
+          const float* x = ((MODE == 0 ? seg : t) ? X1 : X0) + kx;
+#pragma unroll
+          for (int j = 0; j < TX::INSTR; ++j)
+            dma16(x + offx[j], lds[st][t] + (wave * TX::INSTR + j) * 256);
+        }
+#pragma unroll
+        for (int t = 0; t < NYT; ++t) {
+          const float* y = ((MODE == 0 ? seg : t) ? Y1 : Y0) + ky;
+#pragma unroll
+          for (int j = 0; j < TY::INSTR; ++j)
+            dma16(y + offy[j], lds[st][NXT + t] + (wave * TY::INSTR + j) * 256);
+        }
+      } else {
+        gload(vb);
+        sstore(st);
+      }
+    };
+#pragma unroll
+    for (int i = 0; i < S - 1; ++i)
+      if (i < nblk) issue(vb0 + i, i);
+    for (int it = 0; it < nblk; ++it) {
+      // this wave's loads of block it have landed once at most
+      // min(S - 2, nblk - 1 - it) later blocks are still pending
+      const int ahead = min(S - 2, nblk - 1 - it);
+      wait_vm<(S - 2) * LPB>();
+      if (S > 3 && ahead == 1) wait_vm<(S > 3 ? LPB : 0)>();
+      if (ahead == 0) wait_vm<0>();
+      stage_barrier();     // every wave's loads landed; stage it - 1 is free
+      if (it + S - 1 < nblk) issue(vb0 + it + S - 1, (it + S - 1) % S);
+      const int st = it % S;
+      compute(st);
+      if (BIAS && do_bias && vb0 + it < kbps) {
+#pragma unroll
+        for (int kk = 0; kk < KPT; ++kk)
+          bsum += (double)lds[st][0][TX::kr((tid / ROWS) * KPT + kk, tid % ROWS)];
+      }
+    }
+  } else
   if (vb0 < vb1) {
     gload(vb0);
     sstore(0);
@@ -542,9 +599,9 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
       compute(buf);
       if (BIAS && do_bias && vb < kbps) {
         // X tile is [k][m] (XK = false)
-        const float* xs = lds[buf][0] + (tid / ROWS) * KPT * TX::LDM + tid % ROWS;
 #pragma unroll
-        for (int kk = 0; kk < KPT; ++kk) bsum += (double)xs[kk * TX::LDM];
+        for (int kk = 0; kk < KPT; ++kk)
+          bsum += (double)lds[buf][0][TX::kr((tid / ROWS) * KPT + kk, tid % ROWS)];
       }
       if (more) sstore(buf ^ 1);
       __syncthreads();

@@ -36,10 +36,10 @@
 // its row for both operands, so the sum over k is exact up to its order.
 #include "act.h"
 #include "hf_internal.h"
+#include "lds_dma.h"
 
 namespace hfk {
 namespace {
-
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -96,36 +96,6 @@ struct Tile {
     return t;
   }
 };
-
-// 16 bytes per lane from global memory straight into LDS at dst + 16 lane.
-// Written as inline assembly: with the compiler builtin, any direct load in
-// flight makes the compiler wait for every outstanding LDS read before each
-// MFMA step, which serialises the fragment loads with the MFMAs.  The
-// kernel tracks these loads itself (wait_vm before a stage is read).  M0
-// holds the wave's LDS base and needs one wait state before the load.
-__device__ __forceinline__ void dma16(const bf16_t* src, bf16_t* dst) {
-  const uint32_t lds_addr = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)dst);
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(lds_addr) : "memory");
-}
-// wait until at most N vector-memory operations of this wave are pending
-// and every LDS operation has completed
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
-}
-// workgroup barrier that neither the compiler nor the scheduler may move
-// memory operations across; unlike __syncthreads it does not drain the
-// wave's outstanding direct loads
-__device__ __forceinline__ void stage_barrier() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_sched_barrier(0);
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_sched_barrier(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
 
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
