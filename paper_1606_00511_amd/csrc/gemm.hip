@@ -677,12 +677,13 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
   }
 
 // The last argument selects the 16 x 16 form (measured on the speech-frame
-// net: bwd_rbwd +22%, bwd and gnbwd +3%, wgrad +1.5%, fwd +1%; the forward
-// R-operator kernels with their heavier epilogues ran 2% slower in it).
+// net: bwd_rbwd +22%, bwd and gnbwd +3%, wgrad +1.5%, fwd +1%; with direct
+// loads, rfwd +2.6%; the fused forward + R-forward kernels, which write
+// three row-major outputs, ran 2.6% slower in it).
 HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, false, EFwd, false, true)
 HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false)
 HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false, false)
+HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false, true)
 HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false, true)
 HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false, true)
 HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, true)
