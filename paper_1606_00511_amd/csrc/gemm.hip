@@ -15,11 +15,13 @@
 // 256 x 256 tiles with 4 x 4 blocks per wave ran 5-15% slower than this
 // shape at one wave per SIMD.)
 //
-// K advances in blocks of 16 through three LDS stages filled by direct
-// global-to-LDS loads (16 bytes per lane, no registers in between), issued
-// two blocks ahead of the block the MFMAs consume; each wave waits only for
-// its own loads of that block, then the workgroup meets at one barrier per
-// block.  Rows past an operand's edge are clamped to its last row (they feed
+// K advances in blocks of 16 through two LDS stages filled by direct
+// global-to-LDS loads (16 bytes per lane, no registers in between): after
+// the barrier of a block, the next block's loads are issued into the other
+// stage and land while this block's MFMAs run; each wave waits only for its
+// own loads, then the workgroup meets at one barrier per block.  (Measured
+// on MI355X: three stages, two blocks ahead, ran 2% slower at the same
+// occupancy.)  Rows past an operand's edge are clamped to its last row (they feed
 // only outputs that are never stored); the ragged last K block of a
 // K-segment is loaded through registers with zeros past K.  Operands that
 // are not 16-byte aligned or whose leading dimension is not a multiple of 4,
@@ -354,7 +356,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
   constexpr int SZ = TX::SIZE > TY::SIZE ? TX::SIZE : TY::SIZE;
   constexpr int V1 = TX::V1;
   constexpr bool DMA = VEC == 4 && !SQ;
-  constexpr int S = DMA ? 3 : 2;      // LDS stages
+  constexpr int S = 2;      // LDS stages
   __shared__ __attribute__((aligned(16))) float lds[S][T][SZ];
 
   const int tid = threadIdx.x;
@@ -532,7 +534,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
   if constexpr (DMA) {
     constexpr int NYT = T - NXT;               // Y tiles per K block
     constexpr int LPB = NXT * TX::INSTR + NYT * TY::INSTR;
-    static_assert(S >= 3 && S <= 4 && (S - 2) * LPB < 64, "pipeline depth");
+    static_assert(S >= 2 && S <= 4 && (S - 2) * LPB < 64, "pipeline depth");
     size_t offx[TX::INSTR], offy[TY::INSTR];
 #pragma unroll
     for (int j = 0; j < TX::INSTR; ++j) offx[j] = TX::dma_src(s.ldx, s.M, m0, wave, lane, j);
@@ -666,8 +668,8 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
 
 }  // namespace
 
-#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS, M16)                      \
-  extern "C" __global__ __launch_bounds__(256, 1) void NAME##_v4(GemmShape s,   \
+#define HF_GEMM_KERNEL(NAME, MODE, XK, YK, EPI, BIAS, M16, WAVES)               \
+  extern "C" __global__ __launch_bounds__(256, WAVES) void NAME##_v4(GemmShape s,   \
                                                                  EpiArgs e) {   \
     gemm_body<MODE, XK, YK, 4, EPI, BIAS, M16>(s, e);                           \
   }                                                                             \
@@ -676,23 +678,26 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     gemm_body<MODE, XK, YK, 1, EPI, BIAS, M16>(s, e);                           \
   }
 
-// The last argument selects the 16 x 16 form (measured on the speech-frame
-// net: bwd_rbwd +22%, bwd and gnbwd +3%, wgrad +1.5%, fwd +1%; with direct
-// loads, rfwd +2.6%; the fused forward + R-forward kernels, which write
-// three row-major outputs, ran 2.6% slower in it).
-HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, false, EFwd, false, true)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false)
-HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false, true)
-HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false, true)
-HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false, true)
-HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, true)
-HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false, true)
-HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false, true)
-HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, true)
+// M16 selects the 16 x 16 form (measured on the speech-frame net: bwd_rbwd
+// +22%, bwd and gnbwd +3%, wgrad +1.5%, fwd +1%; with direct loads, rfwd
+// +2.6%; the fused forward + R-forward kernels, which write three row-major
+// outputs, ran 2.6% slower in it).  WAVES is the occupancy the register
+// allocation is held to: four waves per SIMD (128 registers) made the
+// batch-row kernels 1-3% faster than three; the weight gradient spills at
+// four and keeps three.
+HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, false, EFwd, false, true, 4)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false, 1)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false, 1)
+HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false, true, 4)
+HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false, true, 4)
+HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false, true, 4)
+HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, true, 1)
+HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false, true, 4)
+HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false, true, 4)
+HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, true, 3)
 // split-K partials of the batch-row single-product GEMMs (X K-contiguous,
 // Y row-contiguous): out0[z * split_stride + m * ldo + n]
-HF_GEMM_KERNEL(hf_gemm_part, 0, true, false, EStore, false, true)
+HF_GEMM_KERNEL(hf_gemm_part, 0, true, false, EStore, false, true, 4)
 
 // weight gradient of squared operands: sum over the rows of delta^2 a^2 (the
 // per-example squared gradients of a weight layer, up to the batch scale),
