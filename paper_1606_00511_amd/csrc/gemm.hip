@@ -280,7 +280,7 @@ struct ERFwd {
                                                float v0, float) {
     const size_t o = (size_t)r * e.ldo + c;
     const float rz = v0 + e.rbias[c];
-    e.out1[o] = rz;
+    if (e.out1) e.out1[o] = rz;      // null: RZ not needed downstream
     if (e.hidden) e.out2[o] = act_d1(e.act, e.aux0[(size_t)r * e.lda + c]) * rz;
   }
 };
@@ -825,7 +825,7 @@ void gemm_fwd_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
 }
 void gemm_rfwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   HF_LAUNCH_ROWS(hf_gemm_rfwd, ERFwd, L, s, e, mnk(s) * s.nseg,
-                   io(s, s.nseg, s.nseg, e.hidden ? 3 : 1));
+                   io(s, s.nseg, s.nseg, e.hidden ? (e.out1 ? 3 : 2) : 1));
 }
 void gemm_bwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   if (e.out2)

@@ -501,7 +501,9 @@ void product_cached(hf_ctx* c, const float* W, const float* X, int B,
     }
     EpiArgs e = epi(c, l < L);
     e.rbias = v + c->offB[l];
-    e.out1 = c->F(c->oRZ[l]);
+    // RZ_l is read by the softmax R-op (l = L) and by the Hessian's
+    // R-backward; the Gauss-Newton product needs only RA_l of a hidden layer
+    e.out1 = (l == L || mode == HF_HESSIAN) ? c->F(c->oRZ[l]) : nullptr;
     e.out2 = (l < L) ? c->F(c->oRA[l]) : nullptr;
     e.ldo = c->ld[l];
     e.aux0 = (l < L) ? c->F(c->oA[l]) : nullptr;
