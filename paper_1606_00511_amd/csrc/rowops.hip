@@ -10,12 +10,11 @@
 // splitk_reduce: deterministic fixed-order reduction of split-K partials of
 //   the weight gradients and of their bias sums.
 //
-// One wave64 per row; the row is staged in LDS once and reused from there for
-// every pass, row reductions use wave shuffles.  Every sum runs in a fixed
-// order, so repeated calls give bit-identical results.
+// One wave64 per row, held in registers (the values of columns lane, lane +
+// 64, ...); row reductions use wave shuffles.  Every sum runs in a fixed order, so repeated calls give
+// bit-identical results.
 #include "hf_internal.h"
 
-#include <mutex>
 
 namespace hfk {
 namespace {
@@ -40,55 +39,37 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 
 }  // namespace
 
-extern "C" __global__ __launch_bounds__(256) void hf_softmax_xent(
-    const float* __restrict__ Z, const int32_t* __restrict__ y, int B, int C,
-    int ld, float invB, float* __restrict__ P, float* __restrict__ D,
-    double* __restrict__ loss_part, int* __restrict__ err);
-extern "C" __global__ __launch_bounds__(256) void hf_softmax_rop(
-    const float* __restrict__ P, const float* __restrict__ RZ, int B, int C,
-    int ld, float invB, float* __restrict__ RD, const int* __restrict__ skip);
 
-namespace {
-// Rows of up to HF_MAX_CLASSES (4096) classes are staged in LDS: 64 KiB per
-// block for softmax_xent and 128 KiB for softmax_rop, above the default
-// dynamic-LDS limit, so the limit is raised once per process.
-void raise_lds_limits() {
-  static std::once_flag once;
-  std::call_once(once, [] {
-    (void)hipFuncSetAttribute((const void*)hf_softmax_xent,
-                        hipFuncAttributeMaxDynamicSharedMemorySize,
-                        ROWS_PER_BLOCK * 4096 * (int)sizeof(float));
-    (void)hipFuncSetAttribute((const void*)hf_softmax_rop,
-                        hipFuncAttributeMaxDynamicSharedMemorySize,
-                        ROWS_PER_BLOCK * 2 * 4096 * (int)sizeof(float));
-  });
-}
-}  // namespace
-
-extern "C" __global__ __launch_bounds__(256) void hf_softmax_xent(
+// softmax_xent keeps its row of logits in registers (KMAX per lane,
+// C <= 64 KMAX), as softmax_rop does; the sums run in the same order as a
+// column-order pass per lane followed by the wave reduction.
+template <int KMAX>
+__device__ __forceinline__ void softmax_xent_body(
     const float* __restrict__ Z, const int32_t* __restrict__ y, int B, int C,
     int ld, float invB, float* __restrict__ P, float* __restrict__ D,
     double* __restrict__ loss_part, int* __restrict__ err) {
-  extern __shared__ float sm[];
   __shared__ float wl[ROWS_PER_BLOCK];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = blockIdx.x * ROWS_PER_BLOCK + wave;
-  float* zs = sm + wave * C;
   float li = 0.0f;
   if (row < B) {
     const float* z = Z + (size_t)row * ld;
+    float v[KMAX];
     float m = -INFINITY;
-    for (int c = lane; c < C; c += 64) {
-      const float t = z[c];
-      zs[c] = t;
-      m = fmaxf(m, t);
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      const int c = lane + 64 * k;
+      v[k] = c < C ? z[c] : -INFINITY;
+      m = fmaxf(m, v[k]);
     }
     m = wave_max(m);
     float sum = 0.0f;
-    for (int c = lane; c < C; c += 64) {
-      const float e = expf(zs[c] - m);
-      zs[c] = e;
-      sum += e;
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      if (lane + 64 * k < C) {
+        v[k] = expf(v[k] - m);
+        sum += v[k];
+      }
     }
     sum = wave_sum(sum);
     const float inv = 1.0f / sum;
@@ -102,10 +83,14 @@ extern "C" __global__ __launch_bounds__(256) void hf_softmax_xent(
     }
     float* prow = P + (size_t)row * ld;
     float* drow = D ? D + (size_t)row * ld : nullptr;
-    for (int c = lane; c < C; c += 64) {
-      const float p = zs[c] * inv;
-      prow[c] = p;
-      if (drow) drow[c] = (c == yi ? p - 1.0f : p) * invB;
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      const int c = lane + 64 * k;
+      if (c < C) {
+        const float p = v[k] * inv;
+        prow[c] = p;
+        if (drow) drow[c] = (c == yi ? p - 1.0f : p) * invB;
+      }
     }
     if (yi >= 0) li = (m + logf(sum)) - z[yi];
   }
@@ -115,6 +100,19 @@ extern "C" __global__ __launch_bounds__(256) void hf_softmax_xent(
     loss_part[blockIdx.x] = ((double)wl[0] + (double)wl[1]) +
                             ((double)wl[2] + (double)wl[3]);
 }
+
+#define HF_SOFTMAX_XENT(K)                                                      \
+  extern "C" __global__ __launch_bounds__(256) void hf_softmax_xent_k##K(       \
+      const float* __restrict__ Z, const int32_t* __restrict__ y, int B, int C, \
+      int ld, float invB, float* __restrict__ P, float* __restrict__ D,         \
+      double* __restrict__ loss_part, int* __restrict__ err) {                  \
+    softmax_xent_body<K>(Z, y, B, C, ld, invB, P, D, loss_part, err);           \
+  }
+HF_SOFTMAX_XENT(4)
+HF_SOFTMAX_XENT(8)
+HF_SOFTMAX_XENT(16)
+HF_SOFTMAX_XENT(32)
+HF_SOFTMAX_XENT(64)
 
 extern "C" __global__ __launch_bounds__(256) void hf_loss_finalize(
     const double* __restrict__ part, int nparts, double invB,
@@ -132,34 +130,58 @@ extern "C" __global__ __launch_bounds__(256) void hf_loss_finalize(
   }
 }
 
-extern "C" __global__ __launch_bounds__(256) void hf_softmax_rop(
+// softmax_rop keeps its row in registers, KMAX values of P and of RZ per
+// lane (C <= 64 KMAX), instead of staging it in LDS: the LDS rows of four
+// waves (2 x 4 x C floats) allowed only two blocks per compute unit, too few
+// waves in flight to cover the memory latency of this HBM-bound pass.  The
+// row sum runs in the same order as before (each lane's values in column
+// order, then the wave reduction).
+template <int KMAX>
+__device__ __forceinline__ void softmax_rop_body(
     const float* __restrict__ P, const float* __restrict__ RZ, int B, int C,
-    int ld, float invB, float* __restrict__ RD, const int* __restrict__ skip) {
-  if (skip && *skip) return;
-  extern __shared__ float sm[];
+    int ld, float invB, float* __restrict__ RD) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = blockIdx.x * ROWS_PER_BLOCK + wave;
   if (row >= B) return;
-  float* ps = sm + wave * 2 * C;
-  float* rs = ps + C;
   const float* prow = P + (size_t)row * ld;
   const float* rrow = RZ + (size_t)row * ld;
-  float dot = 0.0f;
-  for (int c = lane; c < C; c += 64) {
-    const float p = prow[c], r = rrow[c];
-    ps[c] = p;
-    rs[c] = r;
-    dot += p * r;
+  float p[KMAX], r[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    const int c = lane + 64 * k;
+    p[k] = c < C ? prow[c] : 0.0f;
+    r[k] = c < C ? rrow[c] : 0.0f;
   }
+  float dot = 0.0f;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k)
+    if (lane + 64 * k < C) dot += p[k] * r[k];
   dot = wave_sum(dot);
   float* out = RD + (size_t)row * ld;
-  for (int c = lane; c < C; c += 64) out[c] = ps[c] * (rs[c] - dot) * invB;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    const int c = lane + 64 * k;
+    if (c < C) out[c] = p[k] * (r[k] - dot) * invB;
+  }
 }
+
+#define HF_SOFTMAX_ROP(K)                                                       \
+  extern "C" __global__ __launch_bounds__(256) void hf_softmax_rop_k##K(        \
+      const float* __restrict__ P, const float* __restrict__ RZ, int B, int C,  \
+      int ld, float invB, float* __restrict__ RD, const int* __restrict__ skip) { \
+    if (skip && *skip) return;                                                  \
+    softmax_rop_body<K>(P, RZ, B, C, ld, invB, RD);                             \
+  }
+HF_SOFTMAX_ROP(4)
+HF_SOFTMAX_ROP(8)
+HF_SOFTMAX_ROP(16)
+HF_SOFTMAX_ROP(32)
+HF_SOFTMAX_ROP(64)
 
 extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce(
     const float* __restrict__ part, const double* __restrict__ bpart,
     int splits, int M, int N, float* __restrict__ out, int ldo,
-    float* __restrict__ bout, const int* __restrict__ skip) {
+    float* __restrict__ bout, int vec4, const int* __restrict__ skip) {
   if (skip && *skip) return;
   const size_t mn = (size_t)M * N;
   if (bpart) {
@@ -168,6 +190,24 @@ extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce(
       for (int z = 0; z < splits; ++z) t += bpart[(size_t)z * M + m];
       bout[m] = (float)t;
     }
+  }
+  if (vec4) {
+    // four consecutive elements of one row per thread: 16-byte loads of
+    // every partial and one 16-byte store (N, ldo multiples of 4, out
+    // 16-byte aligned)
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const size_t mn4 = mn / 4;
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < mn4;
+         i += (size_t)gridDim.x * 256) {
+      double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+      for (int z = 0; z < splits; ++z) {
+        const f4 v = ((const f4*)part)[(size_t)z * mn4 + i];
+        s0 += v[0]; s1 += v[1]; s2 += v[2]; s3 += v[3];
+      }
+      const size_t m = 4 * i / N, n = 4 * i - m * N;
+      *(f4*)(out + m * ldo + n) = f4{(float)s0, (float)s1, (float)s2, (float)s3};
+    }
+    return;
   }
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < mn;
        i += (size_t)gridDim.x * 256) {
@@ -205,10 +245,14 @@ void softmax_xent(const Launch& L, const float* Z, const int32_t* y, int B,
                   int C, int ld, float* P, float* D, double* loss_part,
                   int* err_flag) {
   const int blocks = (B + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK;
-  const size_t lds = (size_t)ROWS_PER_BLOCK * C * sizeof(float);
-  raise_lds_limits();
+  typedef void (*K)(const float*, const int32_t*, int, int, int, float, float*,
+                    float*, double*, int*);
+  // C <= HF_MAX_CLASSES = 64 x 64 (checked by hf_create)
+  const K k = C <= 256 ? hf_softmax_xent_k4 : C <= 512 ? hf_softmax_xent_k8
+            : C <= 1024 ? hf_softmax_xent_k16 : C <= 2048 ? hf_softmax_xent_k32
+            : hf_softmax_xent_k64;
   prof_begin(L, "hf_softmax_xent");
-  hipLaunchKernelGGL(hf_softmax_xent, dim3(blocks), dim3(256), lds, L.stream,
+  hipLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, L.stream,
                      Z, y, B, C, ld, 1.0f / (float)B, P, D, loss_part, err_flag);
   prof_end(L, "hf_softmax_xent", 0.0,
            4.0 * B * C * (D ? 3.0 : 2.0) + (y ? 4.0 * B : 0.0));
@@ -225,11 +269,15 @@ void loss_finalize(const Launch& L, const double* loss_part, int nparts,
 void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
                  int C, int ld, float* RD, const int* skip) {
   const int blocks = (B + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK;
-  const size_t lds = (size_t)ROWS_PER_BLOCK * 2 * C * sizeof(float);
-  raise_lds_limits();
+  typedef void (*K)(const float*, const float*, int, int, int, float, float*,
+                    const int*);
+  // C <= HF_MAX_CLASSES = 64 x 64 (checked by hf_create)
+  const K k = C <= 256 ? hf_softmax_rop_k4 : C <= 512 ? hf_softmax_rop_k8
+            : C <= 1024 ? hf_softmax_rop_k16 : C <= 2048 ? hf_softmax_rop_k32
+            : hf_softmax_rop_k64;
   prof_begin(L, "hf_softmax_rop");
-  hipLaunchKernelGGL(hf_softmax_rop, dim3(blocks), dim3(256), lds, L.stream,
-                     P, RZ, B, C, ld, 1.0f / (float)B, RD, skip);
+  hipLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, L.stream, P, RZ, B, C, ld,
+                     1.0f / (float)B, RD, skip);
   prof_end(L, "hf_softmax_rop", 0.0, 12.0 * B * C);
 }
 
@@ -245,11 +293,16 @@ void splitk_reduce(const Launch& L, const float* part, const double* bpart,
                    int splits, int M, int N, float* out, int ldo, float* bout,
                    const int* skip) {
   const long long mn = (long long)M * N;
-  long long blocks = (mn + 255) / 256;
+  // the split scratch is 256-byte aligned, so every partial starts 16-byte
+  // aligned when N is a multiple of 4
+  const int vec4 = (N % 4 == 0) && (ldo % 4 == 0) && (((uintptr_t)out & 15) == 0) &&
+                   (((uintptr_t)part & 15) == 0);
+  long long blocks = ((vec4 ? mn / 4 : mn) + 255) / 256;
   if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
   prof_begin(L, "hf_splitk_reduce");
   hipLaunchKernelGGL(hf_splitk_reduce, dim3((unsigned)blocks), dim3(256), 0,
-                     L.stream, part, bpart, splits, M, N, out, ldo, bout, skip);
+                     L.stream, part, bpart, splits, M, N, out, ldo, bout, vec4, skip);
   prof_end(L, "hf_splitk_reduce", 0.0, 4.0 * mn * (splits + 1));
 }
 
