@@ -414,7 +414,7 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
   hipLaunchKernelGGL(hf_cg_reset, dim3(1), dim3(64), 0, L.stream, st);
   if (minv) {
     prof_begin(L, "hf_pcg_init");
-    hipLaunchKernelGGL(hf_pcg_init, dim3(nb), dim3(NT), 0, L.stream, g, x0, q,
+    hipExtLaunchKernelGGL(hf_pcg_init, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, g, x0, q,
                        lambda, x, r, p, neg_dir, n, part + 4 * MAX_GRID,
                        part + 5 * MAX_GRID, minv, part + 6 * MAX_GRID);
     prof_end(L, "hf_pcg_init", 0.0, (x0 ? 8.0 : 6.0) * 4.0 * n);
@@ -424,7 +424,7 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
     return;
   }
   prof_begin(L, "hf_cg_init");
-  hipLaunchKernelGGL(hf_cg_init, dim3(nb), dim3(NT), 0, L.stream, g, x0, q,
+  hipExtLaunchKernelGGL(hf_cg_init, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, g, x0, q,
                      lambda, x, r, p, neg_dir, n, part + 4 * MAX_GRID,
                      part + 5 * MAX_GRID);
   prof_end(L, "hf_cg_init", 0.0, (x0 ? 7.0 : 5.0) * 4.0 * n);
@@ -441,36 +441,36 @@ void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
   double* gpart = part + 3 * MAX_GRID;   // g.p
   double* zpart = part + 6 * MAX_GRID;   // r.z (preconditioned)
   prof_begin(L, "hf_cg_dot");
-  hipLaunchKernelGGL(hf_cg_dot, dim3(nb), dim3(NT), 0, L.stream, p, q, n,
+  hipExtLaunchKernelGGL(hf_cg_dot, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, p, q, n,
                      dpart, st);
   prof_end(L, "hf_cg_dot", 0.0, 2.0 * 4.0 * n);
   if (minv) {
     prof_begin(L, "hf_pcg_update");
-    hipLaunchKernelGGL(hf_pcg_update, dim3(nb), dim3(NT), 0, L.stream, x, r, p,
+    hipExtLaunchKernelGGL(hf_pcg_update, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, r, p,
                        q, n, j, dpart, rpart, st, minv, zpart);
     prof_end(L, "hf_pcg_update", 0.0, 7.0 * 4.0 * n);
   } else {
     prof_begin(L, "hf_cg_update");
-    hipLaunchKernelGGL(hf_cg_update, dim3(nb), dim3(NT), 0, L.stream, x, r, p,
+    hipExtLaunchKernelGGL(hf_cg_update, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, r, p,
                        q, n, j, dpart, rpart, st);
     prof_end(L, "hf_cg_update", 0.0, 6.0 * 4.0 * n);
   }
   prof_begin(L, "hf_cg_neg_dot");
-  hipLaunchKernelGGL(hf_cg_neg_dot, dim3(nb), dim3(NT), 0, L.stream, g, p, n, j,
+  hipExtLaunchKernelGGL(hf_cg_neg_dot, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, g, p, n, j,
                      gpart, st);
   prof_end(L, "hf_cg_neg_dot", 0.0, 2.0 * 4.0 * n);
   prof_begin(L, "hf_cg_neg_write");
-  hipLaunchKernelGGL(hf_cg_neg_write, dim3(nb), dim3(NT), 0, L.stream, g, p, x,
+  hipExtLaunchKernelGGL(hf_cg_neg_write, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, g, p, x,
                      neg_dir, n, j, gpart, st);
   prof_end(L, "hf_cg_neg_write", 0.0, 2.0 * 4.0 * n);
   if (minv) {
     prof_begin(L, "hf_pcg_dir");
-    hipLaunchKernelGGL(hf_pcg_dir, dim3(nb), dim3(NT), 0, L.stream, r, p, n, j,
+    hipExtLaunchKernelGGL(hf_pcg_dir, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, r, p, n, j,
                        rpart, st, minv, zpart);
     prof_end(L, "hf_pcg_dir", 0.0, 4.0 * 4.0 * n);
   } else {
     prof_begin(L, "hf_cg_dir");
-    hipLaunchKernelGGL(hf_cg_dir, dim3(nb), dim3(NT), 0, L.stream, r, p, n, j,
+    hipExtLaunchKernelGGL(hf_cg_dir, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, r, p, n, j,
                        rpart, st);
     prof_end(L, "hf_cg_dir", 0.0, 3.0 * 4.0 * n);
   }
@@ -776,7 +776,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_axpy(
 void axpy(const Launch& L, float* y, const float* x, float a, long long n,
           const int* skip) {
   prof_begin(L, "hf_axpy");
-  hipLaunchKernelGGL(hf_axpy, dim3(cg_grid(n)), dim3(NT), 0, L.stream, y, x,
+  hipExtLaunchKernelGGL(hf_axpy, dim3(cg_grid(n)), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, y, x,
                      (double)a, n, skip);
   prof_end(L, "hf_axpy", 0.0, 3.0 * 4.0 * n);
 }
@@ -788,7 +788,7 @@ void bicg_init(const Launch& L, const float* g, const float* x0,
   const int nb = cg_grid(n);
   hipLaunchKernelGGL(hf_bicg_reset, dim3(1), dim3(64), 0, L.stream, st);
   prof_begin(L, "hf_bicg_init");
-  hipLaunchKernelGGL(hf_bicg_init, dim3(nb), dim3(NT), 0, L.stream, g, x0, q,
+  hipExtLaunchKernelGGL(hf_bicg_init, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, g, x0, q,
                      lambda, x, r, rs, p, neg_dir, n, part);
   prof_end(L, "hf_bicg_init", 0.0, (x0 ? 8.0 : 6.0) * 4.0 * n);
   hipLaunchKernelGGL(hf_bicg_init_fin, dim3(1), dim3(NT), 0, L.stream, part, nb,
@@ -800,11 +800,11 @@ void bicg_half(const Launch& L, const float* r, const float* rs,
                BicgState* st) {
   const int nb = cg_grid(n);
   prof_begin(L, "hf_bicg_dot1");
-  hipLaunchKernelGGL(hf_bicg_dot1, dim3(nb), dim3(NT), 0, L.stream, Ap, rs, n,
+  hipExtLaunchKernelGGL(hf_bicg_dot1, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, Ap, rs, n,
                      part, st);
   prof_end(L, "hf_bicg_dot1", 0.0, 2.0 * 4.0 * n);
   prof_begin(L, "hf_bicg_s");
-  hipLaunchKernelGGL(hf_bicg_s, dim3(nb), dim3(NT), 0, L.stream, r, Ap, s, n, j,
+  hipExtLaunchKernelGGL(hf_bicg_s, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, r, Ap, s, n, j,
                      part, st);
   prof_end(L, "hf_bicg_s", 0.0, 3.0 * 4.0 * n);
 }
@@ -815,19 +815,19 @@ void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
                BicgState* st) {
   const int nb = cg_grid(n);
   prof_begin(L, "hf_bicg_dot2");
-  hipLaunchKernelGGL(hf_bicg_dot2, dim3(nb), dim3(NT), 0, L.stream, s, t, n,
+  hipExtLaunchKernelGGL(hf_bicg_dot2, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, s, t, n,
                      part, st);
   prof_end(L, "hf_bicg_dot2", 0.0, 2.0 * 4.0 * n);
   prof_begin(L, "hf_bicg_update");
-  hipLaunchKernelGGL(hf_bicg_update, dim3(nb), dim3(NT), 0, L.stream, x, r, rs,
+  hipExtLaunchKernelGGL(hf_bicg_update, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, r, rs,
                      p, s, t, g, n, j, part, st);
   prof_end(L, "hf_bicg_update", 0.0, 8.0 * 4.0 * n);
   prof_begin(L, "hf_bicg_dir");
-  hipLaunchKernelGGL(hf_bicg_dir, dim3(nb), dim3(NT), 0, L.stream, p, r, Ap, n,
+  hipExtLaunchKernelGGL(hf_bicg_dir, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, p, r, Ap, n,
                      j, part, st);
   prof_end(L, "hf_bicg_dir", 0.0, 4.0 * 4.0 * n);
   prof_begin(L, "hf_bicg_negw");
-  hipLaunchKernelGGL(hf_bicg_negw, dim3(nb), dim3(NT), 0, L.stream, x, neg_dir,
+  hipExtLaunchKernelGGL(hf_bicg_negw, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, neg_dir,
                      n, j, st);
   prof_end(L, "hf_bicg_negw", 0.0, 2.0 * 4.0 * n);
 }
@@ -896,7 +896,7 @@ void waxpy(const Launch& L, float* out, const float* w, double a,
            const float* d, long long n) {
   const int nb = cg_grid(n);
   prof_begin(L, "hf_waxpy");
-  hipLaunchKernelGGL(hf_waxpy, dim3(nb), dim3(NT), 0, L.stream, out, w, a, d, n);
+  hipExtLaunchKernelGGL(hf_waxpy, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, out, w, a, d, n);
   prof_end(L, "hf_waxpy", 0.0, (w ? 3.0 : 2.0) * 4.0 * n);
 }
 
@@ -904,7 +904,7 @@ void keep_iterate(const Launch& L, float* dst, const float* src, long long n,
                   const int* skip) {
   const int nb = cg_grid(n);
   prof_begin(L, "hf_keep_iterate");
-  hipLaunchKernelGGL(hf_keep_iterate, dim3(nb), dim3(NT), 0, L.stream, dst, src,
+  hipExtLaunchKernelGGL(hf_keep_iterate, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, dst, src,
                      n, skip);
   prof_end(L, "hf_keep_iterate", 0.0, 2.0 * 4.0 * n);
 }
@@ -913,7 +913,7 @@ void dots4(const Launch& L, const float* const a[4], const float* const b[4],
            long long n, double* part, double* out) {
   const int nb = cg_grid(n);
   prof_begin(L, "hf_dots4");
-  hipLaunchKernelGGL(hf_dots4, dim3(nb), dim3(NT), 0, L.stream, a[0], b[0], a[1],
+  hipExtLaunchKernelGGL(hf_dots4, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, a[0], b[0], a[1],
                      b[1], a[2], b[2], a[3], b[3], n, part);
   prof_end(L, "hf_dots4", 0.0, 8.0 * 4.0 * n);
   hipLaunchKernelGGL(hf_dots4_fin, dim3(1), dim3(NT), 0, L.stream, part, nb, out);
@@ -932,7 +932,7 @@ void precond_inverse(const Launch& L, const float* F, double lambda, double xi,
                      float* minv, long long n) {
   const int nb = cg_grid(n);
   prof_begin(L, "hf_precond_inv");
-  hipLaunchKernelGGL(hf_precond_inv, dim3(nb), dim3(NT), 0, L.stream, F, lambda,
+  hipExtLaunchKernelGGL(hf_precond_inv, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, F, lambda,
                      xi, minv, n);
   prof_end(L, "hf_precond_inv", 0.0, 2.0 * 4.0 * n);
 }

@@ -752,7 +752,7 @@ void launch(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1,
   dim3 grid(cdiv(s.N, rows), cdiv(s.M, rows),
             (mode == 0 && s.splits > 1) ? s.splits : 1);
   prof_begin(L, name);
-  hipLaunchKernelGGL(vec == 4 ? k4 : k1, grid, dim3(NT), 0, L.stream, s, e);
+  hipExtLaunchKernelGGL(vec == 4 ? k4 : k1, grid, dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, s, e);
   prof_end(L, name, flops, bytes);
 }
 
@@ -795,7 +795,7 @@ void launch_rows(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1
   const long long mn = (long long)s.M * s.N;
   const int nb = (int)std::min<long long>((mn + 255) / 256, 4096);
   prof_begin(L, "hf_splitk_epi");
-  hipLaunchKernelGGL(splitk_epi<Epi>, dim3(nb), dim3(256), 0, L.stream, e,
+  hipExtLaunchKernelGGL(splitk_epi<Epi>, dim3(nb), dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0, e,
                      e.split_buf, s.M, s.N, sp, s.skip);
   prof_end(L, "hf_splitk_epi", 0.0, 4.0 * (sp + 1) * (double)mn);
 }

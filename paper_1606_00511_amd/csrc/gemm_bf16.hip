@@ -621,7 +621,7 @@ void launch(const Launch& L, const char* name, HKernel k, int mode,
   const int rn = 32 * (sg ? SWN * SGN : DWN * DGN);
   dim3 grid(cdiv(s.N, rn), cdiv(s.M, rm), (sg && s.splits > 1) ? s.splits : 1);
   prof_begin(L, name);
-  hipLaunchKernelGGL(k, grid, dim3(sg ? SNT : DNT), 0, L.stream, s, e);
+  hipExtLaunchKernelGGL(k, grid, dim3(sg ? SNT : DNT), 0, L.stream, prof_a(L), prof_b(L), 0, s, e);
   prof_end(L, name, flops, bytes);
 }
 
@@ -679,8 +679,8 @@ void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
               const int* skip) {
   if (Rpad < R) Rpad = R;
   prof_begin(L, "hf_cvt_bf16");
-  hipLaunchKernelGGL(hf_cvt_bf16, dim3(cdiv(C, 32), cdiv(Rpad, 32)), dim3(256), 0,
-                     L.stream, in, R, C, ldi, out, ldo, outT, ldt, Rpad, skip);
+  hipExtLaunchKernelGGL(hf_cvt_bf16, dim3(cdiv(C, 32), cdiv(Rpad, 32)), dim3(256), 0,
+                     L.stream, prof_a(L), prof_b(L), 0, in, R, C, ldi, out, ldo, outT, ldt, Rpad, skip);
   prof_end(L, "hf_cvt_bf16", 0.0,
            (double)R * C * (4.0 + (out ? 2.0 : 0.0) + (outT ? 2.0 : 0.0)));
 }

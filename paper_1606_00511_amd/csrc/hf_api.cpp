@@ -51,7 +51,7 @@ struct Profiler {
   struct Pending { hipEvent_t a, b; int rec; int tag; double flops, bytes; };
   std::vector<Pending> pending;
   std::vector<hipEvent_t> pool;
-  hipEvent_t open = nullptr;
+  hipEvent_t open = nullptr, close = nullptr;   // the pair of the next launch
   int tag = -1;          // CG iteration of the launches being recorded, -1 outside CG
   size_t solve_begin = 0;  // first pending entry of the CG solve in progress
 
@@ -150,9 +150,18 @@ struct Profiler {
 void prof_begin(const Launch& L, const char* name) {
   (void)name;
   if (!L.prof) return;
-  L.prof->open = L.prof->get();
-  if (L.prof->open) (void)hipEventRecord(L.prof->open, L.stream);
+  Profiler& P = *L.prof;
+  P.open = P.get();
+  P.close = P.get();
+  if (!P.open || !P.close) {
+    if (P.open) P.pool.push_back(P.open);
+    if (P.close) P.pool.push_back(P.close);
+    P.open = P.close = nullptr;
+  }
 }
+
+hipEvent_t prof_a(const Launch& L) { return L.prof ? L.prof->open : nullptr; }
+hipEvent_t prof_b(const Launch& L) { return L.prof ? L.prof->close : nullptr; }
 
 void prof_end(const Launch& L, const char* name, double flops, double bytes) {
   if (!L.prof) return;
@@ -161,12 +170,8 @@ void prof_end(const Launch& L, const char* name, double flops, double bytes) {
   P.recs[r].launches += 1;
   P.recs[r].flops += flops;
   P.recs[r].bytes += bytes;
-  hipEvent_t b = P.get();
-  if (P.open && b) {
-    (void)hipEventRecord(b, L.stream);
-    P.pending.push_back({P.open, b, r, P.tag, flops, bytes});
-  }
-  P.open = nullptr;
+  if (P.open && P.close) P.pending.push_back({P.open, P.close, r, P.tag, flops, bytes});
+  P.open = P.close = nullptr;
   if (P.tag < 0 && P.pending.size() > (1u << 16)) P.collect();
 }
 

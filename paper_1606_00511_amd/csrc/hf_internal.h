@@ -1,6 +1,7 @@
 // Internal declarations shared by the host driver and the gfx950 kernels.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -19,7 +20,14 @@ struct Launch {
   Profiler* prof;   // null when profiling is off
 };
 
+// Kernel timing: prof_begin takes a start/stop event pair for the next
+// launch, which passes prof_a(L) and prof_b(L) to hipExtLaunchKernelGGL (the
+// events are bound to the kernel's own dispatch, with no marker packets of
+// their own); prof_end files the pair for collection.  Null events when
+// profiling is off.
 void prof_begin(const Launch& L, const char* name);
+hipEvent_t prof_a(const Launch& L);
+hipEvent_t prof_b(const Launch& L);
 void prof_end(const Launch& L, const char* name, double flops, double bytes);
 
 // ------------------------------------------------------------------- GEMM

@@ -252,7 +252,7 @@ void softmax_xent(const Launch& L, const float* Z, const int32_t* y, int B,
             : C <= 1024 ? hf_softmax_xent_k16 : C <= 2048 ? hf_softmax_xent_k32
             : hf_softmax_xent_k64;
   prof_begin(L, "hf_softmax_xent");
-  hipLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, L.stream,
+  hipExtLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0,
                      Z, y, B, C, ld, 1.0f / (float)B, P, D, loss_part, err_flag);
   prof_end(L, "hf_softmax_xent", 0.0,
            4.0 * B * C * (D ? 3.0 : 2.0) + (y ? 4.0 * B : 0.0));
@@ -261,7 +261,7 @@ void softmax_xent(const Launch& L, const float* Z, const int32_t* y, int B,
 void loss_finalize(const Launch& L, const double* loss_part, int nparts,
                    int B, float* loss, double* loss64) {
   prof_begin(L, "hf_loss_finalize");
-  hipLaunchKernelGGL(hf_loss_finalize, dim3(1), dim3(256), 0, L.stream,
+  hipExtLaunchKernelGGL(hf_loss_finalize, dim3(1), dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0,
                      loss_part, nparts, 1.0 / (double)B, loss, loss64);
   prof_end(L, "hf_loss_finalize", 0.0, 8.0 * nparts);
 }
@@ -276,7 +276,7 @@ void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
             : C <= 1024 ? hf_softmax_rop_k16 : C <= 2048 ? hf_softmax_rop_k32
             : hf_softmax_rop_k64;
   prof_begin(L, "hf_softmax_rop");
-  hipLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, L.stream, P, RZ, B, C, ld,
+  hipExtLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0, P, RZ, B, C, ld,
                      1.0f / (float)B, RD, skip);
   prof_end(L, "hf_softmax_rop", 0.0, 12.0 * B * C);
 }
@@ -284,8 +284,8 @@ void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
 void transpose(const Launch& L, const float* in, int R, int C, int ldi,
                float* out, int ldo, const int* skip) {
   prof_begin(L, "hf_transpose");
-  hipLaunchKernelGGL(hf_transpose, dim3((C + 31) / 32, (R + 31) / 32), dim3(256),
-                     0, L.stream, in, R, C, ldi, out, ldo, skip);
+  hipExtLaunchKernelGGL(hf_transpose, dim3((C + 31) / 32, (R + 31) / 32), dim3(256),
+                     0, L.stream, prof_a(L), prof_b(L), 0, in, R, C, ldi, out, ldo, skip);
   prof_end(L, "hf_transpose", 0.0, 8.0 * R * C);
 }
 
@@ -301,8 +301,8 @@ void splitk_reduce(const Launch& L, const float* part, const double* bpart,
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
   prof_begin(L, "hf_splitk_reduce");
-  hipLaunchKernelGGL(hf_splitk_reduce, dim3((unsigned)blocks), dim3(256), 0,
-                     L.stream, part, bpart, splits, M, N, out, ldo, bout, vec4, skip);
+  hipExtLaunchKernelGGL(hf_splitk_reduce, dim3((unsigned)blocks), dim3(256), 0,
+                     L.stream, prof_a(L), prof_b(L), 0, part, bpart, splits, M, N, out, ldo, bout, vec4, skip);
   prof_end(L, "hf_splitk_reduce", 0.0, 4.0 * mn * (splits + 1));
 }
 
