@@ -321,12 +321,18 @@ const char* hf_last_error(const hf_ctx* ctx);
 const char* hf_strerror(int32_t code);
 
 /*
- * Kernel timing.  When enabled, every kernel launch is bracketed by HIP
- * events on the context's stream and its algorithmic work (flops for the
- * contractions, bytes for memory-bound kernels) is accumulated per kernel
- * name.  hf_prof_get synchronises the stream.
+ * Kernel timing.  When enabled, every kernel launch carries a start/stop HIP
+ * event pair bound to its dispatch on the context's stream, and its
+ * algorithmic work (flops for the contractions, bytes for memory-bound
+ * kernels) is accumulated per kernel name.  hf_prof_get synchronises the
+ * stream.  hf_prof_only restricts the events to the launches of one kernel
+ * name (NULL or "": every kernel; HF_EINVAL while timing is off); launches
+ * and work are still counted for every name, the others' times stay 0.
+ * Events cost time of their own (a few microseconds per launch), which
+ * matters for small kernels.
  */
 int hf_prof_enable(hf_ctx* ctx, int32_t on);
+int hf_prof_only(hf_ctx* ctx, const char* name);
 int hf_prof_reset(hf_ctx* ctx);
 int32_t hf_prof_count(hf_ctx* ctx);
 int hf_prof_get(hf_ctx* ctx, int32_t i, const char** name, int64_t* launches,

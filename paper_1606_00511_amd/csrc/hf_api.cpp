@@ -52,6 +52,7 @@ struct Profiler {
   std::vector<Pending> pending;
   std::vector<hipEvent_t> pool;
   hipEvent_t open = nullptr, close = nullptr;   // the pair of the next launch
+  std::string only;        // time only launches of this name ("" = all)
   int tag = -1;          // CG iteration of the launches being recorded, -1 outside CG
   size_t solve_begin = 0;  // first pending entry of the CG solve in progress
 
@@ -74,8 +75,11 @@ struct Profiler {
     index[name] = (int)recs.size() - 1;
     return (int)recs.size() - 1;
   }
+  // Launches outside the hf_prof_only filter have null events: counted, not
+  // timed.
   void collect() {
     for (auto& p : pending) {
+      if (!p.a) continue;
       (void)hipEventSynchronize(p.b);
       float ms = 0.0f;
       if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) recs[p.rec].ms += ms;
@@ -83,6 +87,11 @@ struct Profiler {
       pool.push_back(p.b);
     }
     pending.clear();
+  }
+  void release(const Pending& p) {
+    if (!p.a) return;
+    pool.push_back(p.a);
+    pool.push_back(p.b);
   }
   // Drop the launches of a CG solve that the device `done` flag turned into
   // no-ops, so that only launches that did their work are counted.
@@ -109,8 +118,7 @@ struct Profiler {
         recs[p.rec].launches -= 1;
         recs[p.rec].flops -= p.flops;
         recs[p.rec].bytes -= p.bytes;
-        pool.push_back(p.a);
-        pool.push_back(p.b);
+        release(p);
       } else {
         keep.push_back(p);
       }
@@ -133,8 +141,7 @@ struct Profiler {
         recs[p.rec].launches -= 1;
         recs[p.rec].flops -= p.flops;
         recs[p.rec].bytes -= p.bytes;
-        pool.push_back(p.a);
-        pool.push_back(p.b);
+        release(p);
       } else {
         keep.push_back(p);
       }
@@ -151,6 +158,10 @@ void prof_begin(const Launch& L, const char* name) {
   (void)name;
   if (!L.prof) return;
   Profiler& P = *L.prof;
+  if (!P.only.empty() && P.only != name) {
+    P.open = P.close = nullptr;
+    return;
+  }
   P.open = P.get();
   P.close = P.get();
   if (!P.open || !P.close) {
@@ -170,7 +181,9 @@ void prof_end(const Launch& L, const char* name, double flops, double bytes) {
   P.recs[r].launches += 1;
   P.recs[r].flops += flops;
   P.recs[r].bytes += bytes;
-  if (P.open && P.close) P.pending.push_back({P.open, P.close, r, P.tag, flops, bytes});
+  // every launch gets an entry (null events when it is not timed), so that
+  // the no-op launches of a stopped solve are retracted for every name
+  P.pending.push_back({P.open, P.close, r, P.tag, flops, bytes});
   P.open = P.close = nullptr;
   if (P.tag < 0 && P.pending.size() > (1u << 16)) P.collect();
 }
@@ -1622,6 +1635,12 @@ int hf_prof_enable(hf_ctx* c, int32_t on) {
     delete c->prof;
     c->prof = nullptr;
   }
+  return HF_OK;
+}
+
+int hf_prof_only(hf_ctx* c, const char* name) {
+  if (!c || !c->prof) return HF_EINVAL;
+  c->prof->only = name ? name : "";
   return HF_OK;
 }
 

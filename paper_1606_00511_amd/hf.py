@@ -32,7 +32,7 @@ EXPORTS = (
     "hf_workspace_bytes", "hf_set_workspace", "hf_loss_grad", "hf_hvp",
     "hf_cg", "hf_pcg", "hf_fisher_diag", "hf_bicgstab", "hf_loss", "hf_iterate",
     "hf_check", "hf_last_error",
-    "hf_strerror", "hf_prof_enable",
+    "hf_strerror", "hf_prof_enable", "hf_prof_only",
     "hf_prof_reset", "hf_prof_count", "hf_prof_get",
 )
 
@@ -126,6 +126,7 @@ def lib():
         "hf_last_error": (ctypes.c_char_p, [P]),
         "hf_strerror": (ctypes.c_char_p, [I32]),
         "hf_prof_enable": (ctypes.c_int, [P, I32]),
+        "hf_prof_only": (ctypes.c_int, [P, ctypes.c_char_p]),
         "hf_prof_reset": (ctypes.c_int, [P]),
         "hf_prof_count": (I32, [P]),
         "hf_prof_get": (ctypes.c_int, [P, I32, ctypes.POINTER(ctypes.c_char_p),
@@ -366,6 +367,10 @@ class HFNet:
     # ------------------------------------------------------------ profiling
     def prof_enable(self, on=True):
         self._check(lib().hf_prof_enable(self._h, 1 if on else 0))
+
+    def prof_only(self, name=None):
+        """Time only the launches of kernel `name` (None: every kernel)."""
+        self._check(lib().hf_prof_only(self._h, name.encode() if name else None))
 
     def prof_reset(self):
         self._check(lib().hf_prof_reset(self._h))
