@@ -684,14 +684,15 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
 // outputs, ran 2.6% slower in it).  WAVES is the occupancy the register
 // allocation is held to: four waves per SIMD (128 registers) made the
 // batch-row kernels 1-3% faster than three; the weight gradient spills at
-// four and keeps three.
+// four and keeps three; the dual kernels at two waves (202-228 registers,
+// no spills) ran 6-20% faster than at one.
 HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, false, EFwd, false, true, 4)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false, 1)
-HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false, 1)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false, 2)
+HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false, 2)
 HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false, true, 4)
 HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false, true, 4)
 HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false, true, 4)
-HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, true, 1)
+HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, true, 2)
 HF_GEMM_KERNEL(hf_gemm_rbwd, 0, true, false, ERBwd, false, true, 4)
 HF_GEMM_KERNEL(hf_gemm_gnbwd, 0, true, false, EGNBwd, false, true, 4)
 HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, true, 3)
