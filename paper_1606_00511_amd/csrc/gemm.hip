@@ -55,12 +55,6 @@
 namespace hfk {
 namespace {
 
-#ifndef HF_RF16
-#define HF_RF16 true
-#endif
-#ifndef HF_RFW
-#define HF_RFW 4
-#endif
 constexpr int BK = 16;
 constexpr int HK = BK / 2;      // k values per half-wave per K block
 constexpr int NT = 256;
@@ -695,7 +689,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
 HF_GEMM_KERNEL(hf_gemm_fwd, 0, true, false, EFwd, false, true, 4)
 HF_GEMM_KERNEL(hf_gemm_fwd_rfwd, 1, true, true, EFwdRFwd, false, false, 2)
 HF_GEMM_KERNEL(hf_gemm_fwd_rfwd0, 2, true, true, EFwdRFwd, false, false, 2)
-HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false, HF_RF16, HF_RFW)
+HF_GEMM_KERNEL(hf_gemm_rfwd, 0, true, false, ERFwd, false, true, 4)
 HF_GEMM_KERNEL(hf_gemm_bwd, 0, true, false, EBwd, false, true, 4)
 HF_GEMM_KERNEL(hf_gemm_bwd_e2, 0, true, false, EBwdE2, false, true, 4)
 HF_GEMM_KERNEL(hf_gemm_bwd_rbwd, 1, true, false, EBwdRBwd, false, true, 2)
