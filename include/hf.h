@@ -326,8 +326,10 @@ const char* hf_strerror(int32_t code);
  * algorithmic work (flops for the contractions, bytes for memory-bound
  * kernels) is accumulated per kernel name.  hf_prof_get synchronises the
  * stream.  hf_prof_only restricts the events to the launches of one kernel
- * name (NULL or "": every kernel; HF_EINVAL while timing is off); launches
- * and work are still counted for every name, the others' times stay 0.
+ * name (NULL or "": every kernel; HF_EINVAL while timing is off) until it
+ * is called again or timing is turned off (hf_prof_reset keeps it);
+ * launches and work are still counted for every name, the others' times
+ * stay 0.
  * Events cost time of their own (a few microseconds per launch), which
  * matters for small kernels.
  */
