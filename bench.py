@@ -88,9 +88,11 @@ def counter_traffic(kernel):
     return vals.get(kernel)
 
 
-def cpu_baseline(w, inp, rows):
-    """The fp64 oracle timed on this host's cores on a bounded sample: one
-    H v and one G v on the first `rows` rows, scaled to the full batch."""
+def cpu_baseline(w, inp, rows, min_s=12.0, max_pairs=3):
+    """The fp64 oracle timed on this host's cores on a bounded sample: pairs
+    of one H v and one G v on the first `rows` rows, repeated until at least
+    min_s seconds have passed (at most max_pairs pairs), scaled to the full
+    batch."""
     from oracle import hf_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -100,20 +102,24 @@ def cpu_baseline(w, inp, rows):
     rows = w.curv_batch if rows <= 0 else min(rows, w.curv_batch)
     X, y = inp["X"][:rows], inp["y"][:rows]
     th, v = inp["theta"], inp["v"]
+    pairs = 0
     t0 = time.perf_counter()
-    O.hvp(w.dims, w.act, th, X, y, v)
-    t1 = time.perf_counter()
-    O.gvp(w.dims, w.act, th, X, v)
-    t2 = time.perf_counter()
+    while True:
+        O.hvp(w.dims, w.act, th, X, y, v)
+        O.gvp(w.dims, w.act, th, X, v)
+        pairs += 1
+        elapsed = time.perf_counter() - t0
+        if elapsed >= min_s or pairs >= max_pairs:
+            break
     scale = w.curv_batch / float(rows)
-    per_product = 0.5 * ((t1 - t0) + (t2 - t1)) * scale
+    per_product = elapsed / (2 * pairs) * scale
     what = ("the full %d-row batch" % rows if rows == w.curv_batch else
             "the first %d of %d rows, time scaled by %.0fx to the full batch"
             % (rows, w.curv_batch, scale))
     return {"value": 1.0 / per_product, "unit": "curvature-vector products/s",
             "cores": cores, "kind": "oracle",
-            "sample": "fp64 NumPy oracle, one Hv and one Gv on %s (%.1f s measured)"
-                      % (what, t2 - t0)}
+            "sample": "fp64 NumPy oracle, %d x (one Hv and one Gv) on %s (%.1f s measured)"
+                      % (pairs, what, elapsed)}
 
 
 def run_leg(args, w, inp, prec):
