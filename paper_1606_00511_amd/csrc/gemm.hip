@@ -716,19 +716,31 @@ namespace {
 
 // Sum of the split-K partials in split order (fp64), then the kernel's own
 // epilogue on the sum: the result is that of the unsplit kernel up to the
-// rounding of the partial sums.
-template <class Epi>
+// rounding of the partial sums.  One thread per output element: its SP
+// partial loads and the epilogue's own loads are independent, so they are
+// all in flight at once.
+template <class Epi, int SP>
 __global__ __launch_bounds__(256) void splitk_epi(EpiArgs e, const float* part,
-                                                  int M, int N, int splits,
-                                                  const int* skip) {
+                                                  int M, int N, const int* skip) {
   if (skip && *skip) return;
-  const long long mn = (long long)M * N;
-  const long long stride = (long long)gridDim.x * 256;
-  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < mn; i += stride) {
-    double v = 0.0;
-    for (int z = 0; z < splits; ++z) v += (double)part[z * mn + i];
-    Epi::apply(e, (int)(i / N), (int)(i % N), (float)v, 0.0f);
+  const size_t mn = (size_t)M * N;
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= mn) return;
+  float p[SP];
+#pragma unroll
+  for (int z = 0; z < SP; ++z) p[z] = part[z * mn + i];
+  double v = 0.0;
+#pragma unroll
+  for (int z = 0; z < SP; ++z) v += (double)p[z];
+  int r, c;
+  if (mn <= 0xffffffffu) {
+    r = (int)((uint32_t)i / (uint32_t)N);
+    c = (int)((uint32_t)i - (uint32_t)r * (uint32_t)N);
+  } else {
+    r = (int)(i / (size_t)N);
+    c = (int)(i - (size_t)r * N);
   }
+  Epi::apply(e, r, c, (float)v, 0.0f);
 }
 
 typedef void (*GemmKernel)(GemmShape, EpiArgs);
@@ -794,10 +806,14 @@ void launch_rows(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1
   launch(L, name, hf_gemm_part_v4, hf_gemm_part_v1, 128, 0, ps, pe, flops,
          bytes + 4.0 * sp * s.M * (double)s.N);
   const long long mn = (long long)s.M * s.N;
-  const int nb = (int)std::min<long long>((mn + 255) / 256, 4096);
+  const dim3 grid((unsigned)((mn + 255) / 256));
+  // sp is a power of two from 2 to 16 (row_splits doubles from 1)
+  void (*k)(EpiArgs, const float*, int, int, const int*) =
+      sp == 2 ? splitk_epi<Epi, 2> : sp == 4 ? splitk_epi<Epi, 4>
+      : sp == 8 ? splitk_epi<Epi, 8> : splitk_epi<Epi, 16>;
   prof_begin(L, "hf_splitk_epi");
-  hipExtLaunchKernelGGL(splitk_epi<Epi>, dim3(nb), dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0, e,
-                     e.split_buf, s.M, s.N, sp, s.skip);
+  hipExtLaunchKernelGGL(k, grid, dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0, e,
+                        (const float*)e.split_buf, s.M, s.N, s.skip);
   prof_end(L, "hf_splitk_epi", 0.0, 4.0 * (sp + 1) * (double)mn);
 }
 
