@@ -218,7 +218,6 @@ struct hf_ctx {
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
   int max_splits = 16;
   size_t split_floats = 0;  // capacity of the split-K scratch (floats)
-  size_t split_elems = 0;
 
   char* ws = nullptr;
   size_t ws_bytes = 0;
@@ -344,9 +343,16 @@ void plan(hf_ctx* c) {
     mn = std::max(mn, (size_t)c->d[l] * c->d[l - 1]);
     dmax = std::max(dmax, c->d[l]);
   }
-  c->split_elems = mn;
-  c->oSplit = take((size_t)c->max_splits * mn * f4);
-  c->split_floats = (size_t)c->max_splits * mn;
+  // The weight gradients need up to max_splits x (d_l x d_{l-1}) partials.
+  // A batch-row GEMM splits only while its grid holds fewer than 512 tiles
+  // of 128 x 128, so its splits x M x N stays below 1,024 tiles' worth (and
+  // below max_splits x Bmax x the widest layer): with that much scratch the
+  // batch-row split is never cut short.  (The bf16 batch-row GEMMs do not
+  // split.)
+  const size_t rows = h ? 0 : std::min((size_t)1024 * 128 * 128,
+                                       (size_t)c->max_splits * B * (size_t)dmax);
+  c->split_floats = std::max((size_t)c->max_splits * mn, rows);
+  c->oSplit = take(c->split_floats * f4);
   c->oBpart = take((size_t)c->max_splits * dmax * sizeof(double));
   const size_t nv = ((size_t)c->n + 63) & ~size_t(63);
   c->oR = take(nv * f4);
