@@ -216,7 +216,7 @@ struct hf_ctx {
   size_t oG = 0, oStep = 0, oNd = 0, oX0 = 0, oWt = 0, oScal = 0;
   size_t oZ = 0, oP = 0, oSplit = 0, oBpart = 0, oR = 0, oPv = 0, oQ = 0,
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
-  int max_splits = 16;
+  int max_splits = 32;
   size_t split_floats = 0;  // capacity of the split-K scratch (floats)
 
   char* ws = nullptr;
@@ -337,21 +337,27 @@ void plan(hf_ctx* c) {
   }
   c->oZ = take(RB * c->ld[L] * f4);
   c->oP = take(RB * c->ld[L] * f4);
-  size_t mn = 0;
+  // Split-K scratch.  A weight gradient (d_l x d_{l-1}, K up to 2 Bmax rows
+  // over two segments) takes at most the splits that keep every split within
+  // 2,048 rows at that K, or, if the tile rule asked for more, fewer than
+  // 1,024 tiles of 128 x 128 worth of partials.  A batch-row GEMM splits only
+  // while its grid holds fewer than 512 tiles, so it too stays below 1,024
+  // tiles' worth (and below max_splits x Bmax x the widest layer).  With this
+  // much scratch no split is cut short.  (The bf16 batch-row GEMMs do not
+  // split.)
+  constexpr size_t TILES_1024 = (size_t)1024 * 128 * 128;
   int dmax = 0;
+  size_t wg = 0;
   for (int l = 1; l <= L; ++l) {
-    mn = std::max(mn, (size_t)c->d[l] * c->d[l - 1]);
+    const size_t mn = (size_t)c->d[l] * c->d[l - 1];
+    int s1 = 1;
+    while (s1 < c->max_splits && (2 * B + s1 - 1) / s1 > 2048) s1 *= 2;
+    wg = std::max(wg, std::min((size_t)c->max_splits * mn,
+                               std::max((size_t)s1 * mn, TILES_1024)));
     dmax = std::max(dmax, c->d[l]);
   }
-  // The weight gradients need up to max_splits x (d_l x d_{l-1}) partials.
-  // A batch-row GEMM splits only while its grid holds fewer than 512 tiles
-  // of 128 x 128, so its splits x M x N stays below 1,024 tiles' worth (and
-  // below max_splits x Bmax x the widest layer): with that much scratch the
-  // batch-row split is never cut short.  (The bf16 batch-row GEMMs do not
-  // split.)
-  const size_t rows = h ? 0 : std::min((size_t)1024 * 128 * 128,
-                                       (size_t)c->max_splits * B * (size_t)dmax);
-  c->split_floats = std::max((size_t)c->max_splits * mn, rows);
+  const size_t rows = h ? 0 : std::min(TILES_1024, (size_t)c->max_splits * B * (size_t)dmax);
+  c->split_floats = std::max(wg, rows);
   c->oSplit = take(c->split_floats * f4);
   c->oBpart = take((size_t)c->max_splits * dmax * sizeof(double));
   const size_t nv = ((size_t)c->n + 63) & ~size_t(63);
@@ -407,6 +413,9 @@ int choose_splits(const hf_ctx* c, int M, int N, int Ktot) {
   int s = 1;
   while (s < c->max_splits && (Ktot + s - 1) / s > 2048) s *= 2;
   while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 128) s *= 2;
+  // the scratch is sized so that this never applies; it keeps the partials
+  // in bounds regardless
+  while (s > 1 && (size_t)s * M * N > c->split_floats) s /= 2;
   return s;
 }
 

@@ -8,7 +8,7 @@
 //   Hessian of the batch-mean cross-entropy with respect to the logits applied
 //   to R{z}: (diag p - p p^T) R{z} / B per row (Sec. 2.1, after Alg. 1).
 // splitk_reduce: deterministic fixed-order reduction of split-K partials of
-//   the weight gradients and of their bias sums.
+//   the weight gradients and of their bias sums (one kernel per split count).
 //
 // One wave64 per row, held in registers (the values of columns lane, lane +
 // 64, ...); row reductions use wave shuffles.  Every sum runs in a fixed order, so repeated calls give
@@ -178,16 +178,24 @@ HF_SOFTMAX_ROP(16)
 HF_SOFTMAX_ROP(32)
 HF_SOFTMAX_ROP(64)
 
-extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce(
-    const float* __restrict__ part, const double* __restrict__ bpart,
-    int splits, int M, int N, float* __restrict__ out, int ldo,
-    float* __restrict__ bout, int vec4, const int* __restrict__ skip) {
+// Split-K partials of a weight gradient summed in split order (fp64), and
+// the bias partials likewise.  SP is a template constant so that every
+// partial load of an element is issued before the first add.
+template <int SP>
+__device__ __forceinline__ void splitk_reduce_body(
+    const float* __restrict__ part, const double* __restrict__ bpart, int M,
+    int N, float* __restrict__ out, int ldo, float* __restrict__ bout, int vec4,
+    const int* __restrict__ skip) {
   if (skip && *skip) return;
   const size_t mn = (size_t)M * N;
   if (bpart) {
     for (int m = blockIdx.x * 256 + threadIdx.x; m < M; m += gridDim.x * 256) {
+      double b[SP];
+#pragma unroll
+      for (int z = 0; z < SP; ++z) b[z] = bpart[(size_t)z * M + m];
       double t = 0.0;
-      for (int z = 0; z < splits; ++z) t += bpart[(size_t)z * M + m];
+#pragma unroll
+      for (int z = 0; z < SP; ++z) t += b[z];
       bout[m] = (float)t;
     }
   }
@@ -199,10 +207,13 @@ extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce(
     const size_t mn4 = mn / 4;
     for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < mn4;
          i += (size_t)gridDim.x * 256) {
+      f4 v[SP];
+#pragma unroll
+      for (int z = 0; z < SP; ++z) v[z] = ((const f4*)part)[(size_t)z * mn4 + i];
       double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-      for (int z = 0; z < splits; ++z) {
-        const f4 v = ((const f4*)part)[(size_t)z * mn4 + i];
-        s0 += v[0]; s1 += v[1]; s2 += v[2]; s3 += v[3];
+#pragma unroll
+      for (int z = 0; z < SP; ++z) {
+        s0 += v[z][0]; s1 += v[z][1]; s2 += v[z][2]; s3 += v[z][3];
       }
       const size_t m = 4 * i / N, n = 4 * i - m * N;
       *(f4*)(out + m * ldo + n) = f4{(float)s0, (float)s1, (float)s2, (float)s3};
@@ -211,12 +222,29 @@ extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce(
   }
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < mn;
        i += (size_t)gridDim.x * 256) {
+    float v[SP];
+#pragma unroll
+    for (int z = 0; z < SP; ++z) v[z] = part[(size_t)z * mn + i];
     double s = 0.0;
-    for (int z = 0; z < splits; ++z) s += part[(size_t)z * mn + i];
+#pragma unroll
+    for (int z = 0; z < SP; ++z) s += v[z];
     const size_t m = i / N, n = i - m * N;
     out[m * ldo + n] = (float)s;
   }
 }
+
+#define HF_SPLITK_REDUCE(SP)                                                  \
+  extern "C" __global__ __launch_bounds__(256) void hf_splitk_reduce_##SP(    \
+      const float* __restrict__ part, const double* __restrict__ bpart,      \
+      int M, int N, float* __restrict__ out, int ldo,                        \
+      float* __restrict__ bout, int vec4, const int* __restrict__ skip) {    \
+    splitk_reduce_body<SP>(part, bpart, M, N, out, ldo, bout, vec4, skip);   \
+  }
+HF_SPLITK_REDUCE(2)
+HF_SPLITK_REDUCE(4)
+HF_SPLITK_REDUCE(8)
+HF_SPLITK_REDUCE(16)
+HF_SPLITK_REDUCE(32)
 
 // out[c * ldo + r] = in[r * ldi + c] for r < R, c < C, through a padded
 // 32 x 32 LDS tile so both the reads and the writes are coalesced.
@@ -300,9 +328,14 @@ void splitk_reduce(const Launch& L, const float* part, const double* bpart,
   long long blocks = ((vec4 ? mn / 4 : mn) + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
+  // splits is a power of two from 2 to 32 (the split rules double from 1)
+  void (*k)(const float*, const double*, int, int, float*, int, float*, int, const int*) =
+      splits == 2 ? hf_splitk_reduce_2 : splits == 4 ? hf_splitk_reduce_4
+      : splits == 8 ? hf_splitk_reduce_8 : splits == 16 ? hf_splitk_reduce_16
+      : hf_splitk_reduce_32;
   prof_begin(L, "hf_splitk_reduce");
-  hipExtLaunchKernelGGL(hf_splitk_reduce, dim3((unsigned)blocks), dim3(256), 0,
-                     L.stream, prof_a(L), prof_b(L), 0, part, bpart, splits, M, N, out, ldo, bout, vec4, skip);
+  hipExtLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(256), 0,
+                        L.stream, prof_a(L), prof_b(L), 0, part, bpart, M, N, out, ldo, bout, vec4, skip);
   prof_end(L, "hf_splitk_reduce", 0.0, 4.0 * mn * (splits + 1));
 }
 
