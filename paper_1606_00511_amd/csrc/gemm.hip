@@ -344,6 +344,31 @@ struct EStore {
 // of 32 x 32 x 2.
 // SQ: every operand element is squared on its way into LDS (so the product
 // is sum_k X(m, k)^2 Y(n, k)^2, and the bias sums are sums of squares).
+// The output tile (tn, tm) of this workgroup within its split.  Linear
+// dispatch index L goes to XCD L % 8 (each XCD has its own L2).  When a
+// split's grid is a multiple of 8 tiles, XCD x gets the x-th contiguous
+// eighth of the logical order, which walks groups of 8 tile rows column by
+// column: the workgroups resident on one XCD then share their row panels of
+// X and column panels of Y in its L2, instead of every XCD fetching every
+// panel.  Otherwise the order is the dispatch order.
+__device__ __forceinline__ void tile_of(int& tn, int& tm) {
+  const int gx = gridDim.x, gy = gridDim.y, T = gx * gy;
+  if (T % 8) {
+    tn = blockIdx.x;
+    tm = blockIdx.y;
+    return;
+  }
+  const int L = blockIdx.x + gx * blockIdx.y;
+  const int Lg = (L % 8) * (T / 8) + L / 8;
+  constexpr int G = 8;
+  const int g = Lg / (G * gx);
+  const int first = g * G;
+  const int rows = min(G, gy - first);
+  const int w = Lg - g * G * gx;
+  tm = first + w % rows;
+  tn = w / rows;
+}
+
 template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS, bool M16,
           bool SQ = false>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) {
@@ -364,8 +389,10 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int li = lane & 31, h = lane >> 5;
-  const int m0 = blockIdx.y * ROWS;
-  const int n0 = blockIdx.x * ROWS;
+  int tn, tm;
+  tile_of(tn, tm);
+  const int m0 = tm * ROWS;
+  const int n0 = tn * ROWS;
 
   const int kbps = (s.K + BK - 1) / BK;
   const int nvb = (MODE == 0 ? s.nseg : 1) * kbps;
@@ -529,7 +556,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
 
   // bias sums: thread t owns column t % ROWS and KPT consecutive k of a block
   constexpr int KPT = BK * ROWS / NT;
-  const bool do_bias = BIAS && blockIdx.x == 0 && (e.bias_out || e.bias_part);
+  const bool do_bias = BIAS && tn == 0 && (e.bias_out || e.bias_part);
   double bsum = 0.0;
   if constexpr (DMA) {
     constexpr int NYT = T - NXT;               // Y tiles per K block
