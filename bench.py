@@ -364,7 +364,7 @@ def summary(res, K, peak):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU "
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU "
               "path (asked for --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
