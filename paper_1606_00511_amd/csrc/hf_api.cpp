@@ -474,9 +474,19 @@ void wgrad(hf_ctx* c, int l, int B, const float* x0, const float* y0,
 // (the row-contiguous right operand of the forward GEMMs).
 void transpose_weights(hf_ctx* c, const float* v, const std::vector<size_t>& dst,
                        const int* skip) {
-  for (int l = 1; l <= c->L; ++l)
-    transpose(c->launch(), v + c->offW[l], c->d[l], c->d[l - 1], c->d[l - 1],
-              c->F(dst[l]), c->ld[l], skip);
+  TransposeBatch b;
+  static_assert(TransposeBatch::MAX >= HF_MAX_LAYERS, "one block per layer");
+  b.n = c->L;
+  for (int l = 1; l <= c->L; ++l) {
+    const int i = l - 1;
+    b.in[i] = v + c->offW[l];
+    b.R[i] = c->d[l];
+    b.C[i] = c->d[l - 1];
+    b.ldi[i] = c->d[l - 1];
+    b.out[i] = c->F(dst[l]);
+    b.ldo[i] = c->ld[l];
+  }
+  transpose_batch(c->launch(), b, skip);
 }
 
 // Forward pass (activations only) on B rows of X; logits into Z, then the

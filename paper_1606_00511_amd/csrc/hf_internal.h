@@ -188,9 +188,16 @@ void loss_finalize(const Launch& L, const double* loss_part, int nparts,
 // Rdelta_L = P * (RZ - rowsum(P * RZ)) / B.
 void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
                  int C, int ld, float* RD, const int* skip);
-// out[c * ldo + r] = in[r * ldi + c] (R x C -> C x R)
-void transpose(const Launch& L, const float* in, int R, int C, int ldi,
-               float* out, int ldo, const int* skip);
+// Up to 16 row-major blocks transposed in one launch:
+// out[i][c * ldo[i] + r] = in[i][r * ldi[i] + c] (R[i] x C[i] -> C[i] x R[i]).
+struct TransposeBatch {
+  static constexpr int MAX = 16;
+  const float* in[MAX];
+  float* out[MAX];
+  int R[MAX], C[MAX], ldi[MAX], ldo[MAX];
+  int n;
+};
+void transpose_batch(const Launch& L, const TransposeBatch& b, const int* skip);
 // out[m * ldo + n] = sum_z part[z * M * N + m * N + n] and
 // bout[m] = sum_z bpart[z * M + m], both in split order
 void splitk_reduce(const Launch& L, const float* part, const double* bpart,

@@ -13,6 +13,8 @@
 // One wave64 per row, held in registers (the values of columns lane, lane +
 // 64, ...); row reductions use wave shuffles.  Every sum runs in a fixed order, so repeated calls give
 // bit-identical results.
+#include <algorithm>
+
 #include "hf_internal.h"
 
 
@@ -246,15 +248,22 @@ HF_SPLITK_REDUCE(8)
 HF_SPLITK_REDUCE(16)
 HF_SPLITK_REDUCE(32)
 
-// out[c * ldo + r] = in[r * ldi + c] for r < R, c < C, through a padded
-// 32 x 32 LDS tile so both the reads and the writes are coalesced.
+// Block z of the batch: out[c * ldo + r] = in[r * ldi + c] for r < R,
+// c < C, through a padded 32 x 32 LDS tile so both the reads and the writes
+// are coalesced.  The grid covers the largest block; workgroups past a
+// smaller block's edge return at once.
 extern "C" __global__ __launch_bounds__(256) void hf_transpose(
-    const float* __restrict__ in, int R, int C, int ldi,
-    float* __restrict__ out, int ldo, const int* __restrict__ skip) {
+    TransposeBatch b, const int* __restrict__ skip) {
   if (skip && *skip) return;
+  const int z = blockIdx.z;
+  const int R = b.R[z], C = b.C[z];
+  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+  if (r0 >= R || c0 >= C) return;
+  const float* __restrict__ in = b.in[z];
+  float* __restrict__ out = b.out[z];
+  const int ldi = b.ldi[z], ldo = b.ldo[z];
   __shared__ float t[32][33];
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = r0 + ty + 8 * j, c = c0 + tx;
@@ -309,12 +318,19 @@ void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
   prof_end(L, "hf_softmax_rop", 0.0, 12.0 * B * C);
 }
 
-void transpose(const Launch& L, const float* in, int R, int C, int ldi,
-               float* out, int ldo, const int* skip) {
+void transpose_batch(const Launch& L, const TransposeBatch& b, const int* skip) {
+  int gx = 0, gy = 0;
+  double bytes = 0.0;
+  for (int i = 0; i < b.n; ++i) {
+    gx = std::max(gx, (b.C[i] + 31) / 32);
+    gy = std::max(gy, (b.R[i] + 31) / 32);
+    bytes += 8.0 * b.R[i] * (double)b.C[i];
+  }
+  if (b.n < 1 || gx < 1 || gy < 1) return;
   prof_begin(L, "hf_transpose");
-  hipExtLaunchKernelGGL(hf_transpose, dim3((C + 31) / 32, (R + 31) / 32), dim3(256),
-                     0, L.stream, prof_a(L), prof_b(L), 0, in, R, C, ldi, out, ldo, skip);
-  prof_end(L, "hf_transpose", 0.0, 8.0 * R * C);
+  hipExtLaunchKernelGGL(hf_transpose, dim3(gx, gy, b.n), dim3(256), 0, L.stream,
+                        prof_a(L), prof_b(L), 0, b, skip);
+  prof_end(L, "hf_transpose", 0.0, bytes);
 }
 
 void splitk_reduce(const Launch& L, const float* part, const double* bpart,
