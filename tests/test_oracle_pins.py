@@ -815,7 +815,71 @@ def test_fisher_diag_bounds_the_squared_gradient():
     F1 = O.fisher_diag(dims, act, th, p["X"][:1], p["y"][:1])
     _, g1 = O.loss_grad(dims, act, th, p["X"][:1], p["y"][:1])
     assert np.allclose(F1, g1 * g1, rtol=1e-14, atol=0)
-    assert np.allclose(O.precond_inverse(F, 0.1, 0.75), (F + 0.1) ** -0.75)
+
+
+def test_precond_inverse_hand_values():
+    """M^-1 = (F + lambda)^(-xi) at hand-worked points where F + lambda is a
+    perfect power (tests/golden/precond_hand_values.txt): a wrong exponent
+    sign, a dropped lambda or an exponent of xi/2 misses every one."""
+    gd = read_golden("precond_hand_values.txt")
+    assert len(gd) >= 8
+    for k, (F, lam, xi, want) in sorted(gd.items()):
+        got = O.precond_inverse(np.array([F, F]), lam, xi)
+        assert got.shape == (2,)
+        assert got == pytest.approx([want, want], rel=1e-13), k
+
+
+def test_precond_inverse_structure():
+    """xi = 0 gives ones (and then preconditioned CG is plain CG, bit for
+    bit); xi = 1 gives the reciprocal 1 / (F + lambda) computed by division;
+    the result is positive and decreasing in F for xi > 0."""
+    rng = np.random.default_rng(35)
+    F = rng.uniform(0.0, 3.0, 40)
+    assert np.array_equal(O.precond_inverse(F, 0.1, 0.0), np.ones(40))
+    assert np.allclose(O.precond_inverse(F, 0.1, 1.0), 1.0 / (F + 0.1),
+                       rtol=1e-15, atol=0)
+    m = O.precond_inverse(np.sort(F), 0.1, 0.75)
+    assert np.all(m > 0) and np.all(np.diff(m) < 0)
+    n = 12
+    Q = rng.standard_normal((n, n))
+    A = Q + Q.T
+    g = rng.standard_normal(n)
+    Fs = rng.uniform(0.0, 2.0, n)
+    plain = O.cg_minimize(lambda v: A @ v, g, 0.05, 8)
+    xi0 = O.cg_minimize(lambda v: A @ v, g, 0.05, 8,
+                        minv=O.precond_inverse(Fs, 0.05, 0.0))
+    for k in ("iters", "products", "neg_curv", "neg_iter", "pBp"):
+        assert plain[k] == xi0[k], k
+    assert np.array_equal(plain["step"], xi0["step"])
+
+
+@pytest.mark.parametrize("spd", [True, False])
+def test_pcg_half_power_is_cg_on_the_scaled_system(spd):
+    """With xi = 1/2, M = (F + lambda)^(1/2), so preconditioned CG is plain CG
+    on S B S with gradient S g for S = M^(-1/2) = diag((F + lambda)^(-1/4)).
+    S is formed here by two square roots and a division, without
+    precond_inverse; the iterates satisfy x_j = S x'_j and the detection
+    (iteration and kappa) is the same."""
+    rng = np.random.default_rng(36 if spd else 37)
+    n, lam = 14, 0.03
+    Q = rng.standard_normal((n, n))
+    A = Q @ Q.T + 0.2 * np.eye(n) if spd else Q + Q.T
+    g = rng.standard_normal(n)
+    F = rng.uniform(0.0, 4.0, n)
+    S = np.diag(1.0 / np.sqrt(np.sqrt(F + lam)))
+    Bt = S @ (A + lam * np.eye(n)) @ S
+    minv = O.precond_inverse(F, lam, 0.5)
+    for j in range(1, 9):
+        pc = O.cg_minimize(lambda v: A @ v, g, lam, j, minv=minv)
+        tr = O.cg_minimize(lambda v: Bt @ v, S @ g, 0.0, j)
+        assert (pc["iters"], pc["neg_curv"], pc["neg_iter"]) == \
+            (tr["iters"], tr["neg_curv"], tr["neg_iter"])
+        if pc["neg_curv"]:
+            assert pc["pBp"] == pytest.approx(tr["pBp"], rel=1e-9)
+            break
+        assert np.allclose(pc["step"], S @ tr["step"], rtol=1e-9, atol=1e-12)
+    if not spd:
+        assert pc["neg_curv"] == 1, "the indefinite case must reach a detection"
 
 
 @pytest.mark.parametrize("spd", [True, False])
@@ -871,3 +935,18 @@ def test_fisher_output_layer_closed_form_matches_definition():
         assert np.allclose(F[-5:], Fb, rtol=1e-12, atol=1e-16)
     Fk = O.fisher_diag(dims, "relu", th, p["X"], p["y"], kink=0.5)
     assert np.allclose(Fk[-(nW + 5):], F[-(nW + 5):], rtol=1e-12)
+
+
+@pytest.mark.parametrize("bad", ["sign", "no_lambda", "half_exponent"])
+def test_planted_preconditioner_mistakes_are_caught(monkeypatch, bad):
+    """A flipped exponent sign, a dropped lambda or a halved exponent in
+    M^-1 = (F + lambda)^(-xi) each miss a hand-worked value."""
+    forms = {
+        "sign": lambda F, lam, xi=0.75: (np.asarray(F, dtype=np.float64) + lam) ** xi,
+        "no_lambda": lambda F, lam, xi=0.75: np.asarray(F, dtype=np.float64) ** (-xi),
+        "half_exponent": lambda F, lam, xi=0.75:
+            (np.asarray(F, dtype=np.float64) + lam) ** (-0.5 * xi),
+    }
+    monkeypatch.setattr(O, "precond_inverse", forms[bad])
+    with pytest.raises(AssertionError):
+        test_precond_inverse_hand_values()
