@@ -23,9 +23,10 @@
  * Every array argument is a device pointer, 16-byte aligned, owned by the
  *   caller; the library never allocates or frees device memory.  Scratch
  *   space comes from one caller-provided workspace (hf_set_workspace).
- * All device work is enqueued on the stream set with hf_set_stream (the
- *   null stream by default).  hf_loss_grad and hf_hvp are asynchronous;
- *   hf_cg returns after its solve has finished (it synchronises the stream).
+ * All device work is enqueued on the context's stream (hf_create's
+ *   hip_stream, changed later with hf_set_stream; NULL = the null stream).
+ *   hf_loss_grad and hf_hvp are asynchronous; hf_cg returns after its solve
+ *   has finished (it synchronises the stream).
  * Return value: HF_OK or a negative HF_E* code; hf_last_error() gives the
  *   message.  Arguments are validated before any device call, so a bad
  *   argument never reaches the GPU.  No exception or abort crosses the ABI.
@@ -82,11 +83,13 @@ enum {
  *   prec      HF_FP32 or HF_BF16_INPUTS.
  *   max_batch largest B any later call may use (>= 1); every B x d_l
  *             buffer and n must stay below 2^31 elements.
+ *   hip_stream a hipStream_t for all device work of the context (NULL: the
+ *             null stream); hf_set_stream changes it later.
  *   out       receives the context.  Returns HF_EINVAL on bad arguments.
  * No device call is made; the context holds no device memory.
  */
 int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
-              int64_t max_batch, hf_ctx** out);
+              int64_t max_batch, void* hip_stream, hf_ctx** out);
 
 /* Free a context (host memory, events, pinned host staging).  NULL is ok. */
 int hf_destroy(hf_ctx* ctx);
@@ -97,14 +100,20 @@ int hf_set_stream(hf_ctx* ctx, void* hip_stream);
 /* n = sum_l d_l (d_{l-1} + 1), or -1 for a NULL context. */
 int64_t hf_num_params(const hf_ctx* ctx);
 
-/* Bytes of device workspace needed for max_batch rows (0 for NULL). */
-size_t hf_workspace_bytes(const hf_ctx* ctx);
+/* Bytes of device workspace for calls of up to `batch` rows (batch <= 0:
+ * max_batch).  0 for a NULL context or batch > max_batch.  Grows with
+ * batch. */
+size_t hf_workspace_bytes(const hf_ctx* ctx, int64_t batch);
 
-/* Hand the context a device workspace of at least hf_workspace_bytes()
- * bytes, 256-byte aligned.  The caller keeps ownership and must keep it
- * alive while the context uses it, and must not write to it meanwhile.
- * Contents need no initialisation: the call clears what needs clearing
- * (for HF_BF16_INPUTS, the operand padding) and synchronises the device. */
+/* Hand the context a device workspace, 256-byte aligned, of `bytes` bytes.
+ * The context lays it out for the largest batch b <= max_batch with
+ * hf_workspace_bytes(ctx, b) <= bytes; later calls with more than b rows
+ * return HF_EWORKSPACE (as does a workspace too small for one row).  The
+ * caller keeps ownership and must keep it alive while the context uses it,
+ * and must not write to it meanwhile.  Contents need no initialisation: the
+ * call clears what needs clearing (for HF_BF16_INPUTS, the operand padding)
+ * and synchronises the device.  A new workspace discards the old one's
+ * contents (such as the cache of a solve). */
 int hf_set_workspace(hf_ctx* ctx, void* dev_ptr, size_t bytes);
 
 /*
@@ -308,6 +317,27 @@ int hf_iterate(hf_ctx* ctx, float* W, const float* X, const int32_t* y,
                int64_t B, const float* Xc, const int32_t* yc, int64_t Bc,
                const hf_iter_params* params, int32_t* hybrid_state,
                float* delta, hf_iter_info* info);
+
+/*
+ * hf_set_trace: lock-step diagnostic of the solvers' curvature products.
+ * Every later solve on ctx (hf_cg, hf_pcg, hf_bicgstab and the solve inside
+ * hf_iterate) copies the operand v and the undamped result A v of each of
+ * its first `cap` curvature products k into buf: slot 2k (n floats at
+ * buf + 2k n) gets v, slot 2k + 1 gets A v (A = H or G of the solve, on its
+ * cached curvature batch; the product B_k v of Alg. 1 step 3 is A v +
+ * lambda v).  Products are numbered in the order the solve evaluates them:
+ * a warm start's product is k = 0; CG's iteration j is k = j (+1 after a
+ * warm start); Bi-CG-STAB's iteration j is k = 2j (on p) and 2j + 1 (on s).
+ * Slots of products the solve did not evaluate are left untouched.
+ *   buf  device, 2 cap n fp32, 16-byte aligned, caller-owned; it must stay
+ *        alive while tracing is on.  cap = 0 (buf ignored) turns it off.
+ * Returns HF_EINVAL for cap < 0 or a NULL / misaligned buffer with cap > 0.
+ * Costs two vector copies per traced product.
+ */
+int hf_set_trace(hf_ctx* ctx, float* buf, int32_t cap);
+
+/* SHA-256 (hex) of the sources the library was built from. */
+const char* hf_build_id(void);
 
 /* Synchronise the stream and report a device-detected error (HF_ELABEL)
  * raised since the last hf_check; clears the flag. */

@@ -34,6 +34,10 @@
 #include <string>
 #include <vector>
 
+#ifndef HF_BUILD_ID
+#define HF_BUILD_ID "unknown"
+#endif
+
 using namespace hfk;
 
 // ------------------------------------------------------------------ profiler
@@ -197,6 +201,7 @@ struct hf_ctx {
   std::vector<int> ld;         // padded leading dimensions (multiple of 4)
   int act = 0, prec = 0;
   int64_t Bmax = 0;
+  int64_t Bws = 0;             // rows the workspace layout serves (<= Bmax)
   int64_t n = 0;
   std::vector<int64_t> offW, offB;   // 1-based, parameter offsets
   hipStream_t stream = nullptr;
@@ -227,6 +232,10 @@ struct hf_ctx {
   CgState* pinned = nullptr;       // 2 host-pinned copies of the CG state
   void* pinned_bicg = nullptr;     // 2 host-pinned copies of the Bi-CG-STAB state
   hipEvent_t ev[2] = {nullptr, nullptr};
+  // lock-step diagnostic (hf_set_trace): operand and result of the first
+  // trace_cap curvature products of every solve
+  float* trace_buf = nullptr;
+  int trace_cap = 0;
 
   float* F(size_t off) const { return reinterpret_cast<float*>(ws + off); }
   double* Dp(size_t off) const { return reinterpret_cast<double*>(ws + off); }
@@ -263,7 +272,10 @@ inline int round4(int x) { return (x + 3) & ~3; }
 inline int round64(int x) { return (x + 63) & ~63; }
 inline size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
 
-void plan(hf_ctx* c) {
+// Carve the workspace for calls of up to B rows (B <= Bmax).
+void plan(hf_ctx* c, int64_t Bplan) {
+  c->Bws = Bplan;
+  c->ldB = round64((int)Bplan);
   const int L = c->L;
   const bool h = c->bf16();
   size_t off = 0;
@@ -272,7 +284,7 @@ void plan(hf_ctx* c) {
     off += up256(bytes);
     return o;
   };
-  const size_t B = (size_t)c->Bmax;
+  const size_t B = (size_t)Bplan;
   for (auto* v : {&c->oA, &c->oD, &c->oE2, &c->oRZ, &c->oRA, &c->oRD, &c->oWT,
                   &c->oVT, &c->hW, &c->hWT, &c->hV, &c->hVT, &c->hA, &c->hAT,
                   &c->hRA, &c->hRAT, &c->hD, &c->hDT, &c->hRD, &c->hRDT})
@@ -337,12 +349,12 @@ void plan(hf_ctx* c) {
   }
   c->oZ = take(RB * c->ld[L] * f4);
   c->oP = take(RB * c->ld[L] * f4);
-  // Split-K scratch.  A weight gradient (d_l x d_{l-1}, K up to 2 Bmax rows
+  // Split-K scratch.  A weight gradient (d_l x d_{l-1}, K up to 2 B rows
   // over two segments) takes at most the splits that keep every split within
   // 2,048 rows at that K, or, if the tile rule asked for more, fewer than
   // 1,024 tiles of 128 x 128 worth of partials.  A batch-row GEMM splits only
   // while its grid holds fewer than 512 tiles, so it too stays below 1,024
-  // tiles' worth (and below max_splits x Bmax x the widest layer).  With this
+  // tiles' worth (and below max_splits x B x the widest layer).  With this
   // much scratch no split is cut short.  (The bf16 batch-row GEMMs do not
   // split.)
   constexpr size_t TILES_1024 = (size_t)1024 * 128 * 128;
@@ -399,7 +411,37 @@ int check_batch(hf_ctx* c, int64_t B) {
   if (B < 1 || B > c->Bmax)
     return fail(c, HF_EINVAL, "batch %lld outside [1, %lld]", (long long)B,
                 (long long)c->Bmax);
+  if (B > c->Bws)
+    return fail(c, HF_EWORKSPACE, "batch %lld above the %lld rows the workspace serves",
+                (long long)B, (long long)c->Bws);
   return HF_OK;
+}
+
+// Bytes of workspace for calls of up to B rows.
+size_t plan_bytes(const hf_ctx* c, int64_t B) {
+  hf_ctx t;
+  t.L = c->L;
+  t.d = c->d;
+  t.ld = c->ld;
+  t.ldh = c->ldh;
+  t.act = c->act;
+  t.prec = c->prec;
+  t.Bmax = c->Bmax;
+  t.n = c->n;
+  t.max_splits = c->max_splits;
+  plan(&t, B);
+  return t.need;
+}
+
+// Operand and result of the k-th curvature product of a solve into the
+// trace buffer (hf_set_trace), unless the solve has stopped (skip).
+void trace_product(hf_ctx* c, int k, const float* v, const float* out,
+                   const int* skip) {
+  if (!c->trace_buf || k >= c->trace_cap) return;
+  const size_t n = (size_t)c->n;
+  keep_iterate(c->launch(), c->trace_buf + (2 * (size_t)k) * n, v, (long long)n, skip);
+  keep_iterate(c->launch(), c->trace_buf + (2 * (size_t)k + 1) * n, out, (long long)n,
+               skip);
 }
 
 // split-K factor for a weight-gradient GEMM with the given tile count and
@@ -953,12 +995,17 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   // cache of the curvature batch: activations, p, delta_l, E2_l
   build_cache(c, W, Xc, b, yc, hess);
   // a warm start's residual needs one product on the cache
-  if (x0) product(c, W, Xc, b, x0, mode, q, nullptr);
+  const int k0 = x0 ? 1 : 0;
+  if (x0) {
+    product(c, W, Xc, b, x0, mode, q, nullptr);
+    trace_product(c, 0, x0, q, nullptr);
+  }
   cg_init(Lc, g, x0, x0 ? q : nullptr, step, r, p, neg_dir, n, (double)damping,
           (double)rel_tol * (double)rel_tol, part, st, minv);
   for (int j = 0; j < max_iters; ++j) {
     if (c->prof) c->prof->tag = j;
     product(c, W, Xc, b, p, mode, q, skip);
+    trace_product(c, k0 + j, p, q, skip);
     cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st, minv);
     if (keep) keep->after(Lc, j + 1, step, n, skip);
     // Stop enqueueing once the device reports `done` for the previous
@@ -1037,16 +1084,22 @@ int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
 
   build_cache(c, W, Xc, b, yc, hess);
   // a warm start's residual needs one product on the cache
-  if (x0) product(c, W, Xc, b, x0, mode, Ap, nullptr);
+  const int k0 = x0 ? 1 : 0;
+  if (x0) {
+    product(c, W, Xc, b, x0, mode, Ap, nullptr);
+    trace_product(c, 0, x0, Ap, nullptr);
+  }
   bicg_init(Lc, g, x0, x0 ? Ap : nullptr, step, r, rs, p, neg_dir, n,
             (double)damping, (double)rel_tol * (double)rel_tol, part, st);
   for (int j = 0; j < max_iters; ++j) {
     if (c->prof) c->prof->tag = 2 * j;
     product(c, W, Xc, b, p, mode, Ap, skip);
+    trace_product(c, k0 + 2 * j, p, Ap, skip);
     lambda_axpy(c, Ap, p, damping, skip);
     bicg_half(Lc, r, rs, Ap, sv, n, j, part, st);
     if (c->prof) c->prof->tag = 2 * j + 1;
     product(c, W, Xc, b, sv, mode, t, skip);
+    trace_product(c, k0 + 2 * j + 1, sv, t, skip);
     lambda_axpy(c, t, sv, damping, skip);
     bicg_rest(Lc, step, r, rs, p, Ap, sv, t, g, neg_dir, n, j, part, st);
     if (keep) keep->after(Lc, j + 1, step, n, skip);
@@ -1094,7 +1147,7 @@ int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
 extern "C" {
 
 int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
-              int64_t max_batch, hf_ctx** out) {
+              int64_t max_batch, void* hip_stream, hf_ctx** out) {
   if (!out) return HF_EINVAL;
   *out = nullptr;
   if (!dims || n_dims < 2 || n_dims > HF_MAX_LAYERS + 1) return HF_EINVAL;
@@ -1119,7 +1172,6 @@ int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
   for (int i = 0; i < n_dims; ++i) c->ld[i] = round4(dims[i]);
   c->ldh.resize(n_dims);
   for (int i = 0; i < n_dims; ++i) c->ldh[i] = round64(dims[i]);
-  c->ldB = round64((int)max_batch);
   c->act = act;
   c->prec = prec;
   c->Bmax = max_batch;
@@ -1133,7 +1185,8 @@ int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
     c->offB[l] = off;
     off += dims[l];
   }
-  plan(c);
+  c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  plan(c, max_batch);
   *out = c;
   return HF_OK;
 }
@@ -1157,15 +1210,30 @@ int hf_set_stream(hf_ctx* c, void* s) {
 
 int64_t hf_num_params(const hf_ctx* c) { return c ? c->n : -1; }
 
-size_t hf_workspace_bytes(const hf_ctx* c) { return c ? c->need : 0; }
+size_t hf_workspace_bytes(const hf_ctx* c, int64_t batch) {
+  if (!c) return 0;
+  if (batch <= 0) batch = c->Bmax;
+  if (batch > c->Bmax) return 0;
+  return plan_bytes(c, batch);
+}
 
 int hf_set_workspace(hf_ctx* c, void* p, size_t bytes) {
   if (!c) return HF_EINVAL;
   if (!p) return fail(c, HF_EINVAL, "workspace pointer is NULL");
   if ((uintptr_t)p & 255u) return fail(c, HF_EINVAL, "workspace is not 256-byte aligned");
-  if (bytes < c->need)
-    return fail(c, HF_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed",
-                bytes, c->need);
+  const size_t need1 = plan_bytes(c, 1);
+  if (bytes < need1)
+    return fail(c, HF_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed "
+                "for one row", bytes, need1);
+  // the largest batch whose layout fits (the bytes needed grow with the batch)
+  int64_t lo = 1, hi = c->Bmax;
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo + 1) / 2;
+    if (plan_bytes(c, mid) <= bytes) lo = mid;
+    else hi = mid - 1;
+  }
+  c->ws = nullptr;
+  plan(c, lo);
   c->ws = reinterpret_cast<char*>(p);
   c->ws_bytes = bytes;
   HIP_TRY(c, hipMemset(c->ws + c->oErr, 0, sizeof(int)));
@@ -1637,6 +1705,18 @@ int hf_check(hf_ctx* c) {
 const char* hf_last_error(const hf_ctx* c) {
   if (!c) return "null context";
   return c->err.c_str();
+}
+
+const char* hf_build_id(void) { return HF_BUILD_ID; }
+
+int hf_set_trace(hf_ctx* c, float* buf, int32_t cap) {
+  if (!c) return HF_EINVAL;
+  if (cap < 0) return fail(c, HF_EINVAL, "trace capacity %d < 0", cap);
+  if (cap > 0 && !buf) return fail(c, HF_EINVAL, "trace buffer is NULL");
+  if (cap > 0 && !a16(buf)) return fail(c, HF_EINVAL, "trace buffer is not 16-byte aligned");
+  c->trace_buf = cap > 0 ? buf : nullptr;
+  c->trace_cap = cap > 0 ? cap : 0;
+  return HF_OK;
 }
 
 const char* hf_strerror(int32_t code) {

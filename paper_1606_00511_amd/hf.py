@@ -9,6 +9,8 @@ backend: without the built library every call raises.
 import ctypes
 import os
 
+from paper_1606_00511_amd.buildid import source_hash
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libhf.so")
 
@@ -31,7 +33,7 @@ EXPORTS = (
     "hf_create", "hf_destroy", "hf_set_stream", "hf_num_params",
     "hf_workspace_bytes", "hf_set_workspace", "hf_loss_grad", "hf_hvp",
     "hf_cg", "hf_pcg", "hf_fisher_diag", "hf_bicgstab", "hf_loss", "hf_iterate",
-    "hf_check", "hf_last_error",
+    "hf_set_trace", "hf_build_id", "hf_check", "hf_last_error",
     "hf_strerror", "hf_prof_enable", "hf_prof_only",
     "hf_prof_reset", "hf_prof_count", "hf_prof_get",
 )
@@ -89,7 +91,8 @@ _lib = None
 
 
 def lib():
-    """Load libhf.so (raises if it has not been built)."""
+    """Load libhf.so (raises if it has not been built, or if it was built
+    from sources other than those beside it)."""
     global _lib
     if _lib is not None:
         return _lib
@@ -98,15 +101,24 @@ def lib():
             "libhf.so is not built (%s); run python -m paper_1606_00511_amd.build"
             % LIB_PATH)
     L = ctypes.CDLL(LIB_PATH)
+    L.hf_build_id.restype = ctypes.c_char_p
+    L.hf_build_id.argtypes = []
+    built = L.hf_build_id().decode()
+    want = source_hash()
+    if built != want:
+        raise RuntimeError(
+            "libhf.so (%s) was built from other sources (build id %s, sources %s);"
+            " rebuild with python -m paper_1606_00511_amd.build"
+            % (LIB_PATH, built[:16], want[:16]))
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     F32, D = ctypes.c_float, ctypes.c_double
     sig = {
         "hf_create": (ctypes.c_int, [ctypes.POINTER(I32), I32, I32, I32, I64,
-                                     ctypes.POINTER(P)]),
+                                     P, ctypes.POINTER(P)]),
         "hf_destroy": (ctypes.c_int, [P]),
         "hf_set_stream": (ctypes.c_int, [P, P]),
         "hf_num_params": (I64, [P]),
-        "hf_workspace_bytes": (SZ, [P]),
+        "hf_workspace_bytes": (SZ, [P, I64]),
         "hf_set_workspace": (ctypes.c_int, [P, P, SZ]),
         "hf_loss_grad": (ctypes.c_int, [P, P, P, P, I64, P, P]),
         "hf_hvp": (ctypes.c_int, [P, P, P, P, I64, P, I32, P]),
@@ -122,6 +134,8 @@ def lib():
                                       ctypes.POINTER(hf_iter_params),
                                       ctypes.POINTER(I32), P,
                                       ctypes.POINTER(hf_iter_info)]),
+        "hf_set_trace": (ctypes.c_int, [P, P, I32]),
+        "hf_build_id": (ctypes.c_char_p, []),
         "hf_check": (ctypes.c_int, [P]),
         "hf_last_error": (ctypes.c_char_p, [P]),
         "hf_strerror": (ctypes.c_char_p, [I32]),
@@ -166,10 +180,13 @@ class HFNet:
 
     dims: (d_0, ..., d_L); act: "sigmoid" | "tanh" | "relu"; max_batch: the
     largest batch any call will use; prec: "fp32" or "bf16" (bf16 GEMM
-    operands, fp32 accumulation).  Calls run on torch's current stream.
+    operands, fp32 accumulation); ws_batch: size the workspace for calls of
+    up to this many rows only (default max_batch).  Calls run on torch's
+    current stream.
     """
 
-    def __init__(self, dims, act, max_batch, device="cuda", prec="fp32"):
+    def __init__(self, dims, act, max_batch, device="cuda", prec="fp32",
+                 ws_batch=None):
         import torch
         self.dims = tuple(int(d) for d in dims)
         self.act = act
@@ -179,13 +196,16 @@ class HFNet:
         arr = (ctypes.c_int32 * len(self.dims))(*self.dims)
         h = ctypes.c_void_p()
         rc = L.hf_create(arr, len(self.dims), ACTS[act], PRECS[prec],
-                         self.max_batch, ctypes.byref(h))
+                         self.max_batch, None, ctypes.byref(h))
         if rc != HF_OK:
             raise HFError(rc, "hf_create rejected dims=%s act=%s max_batch=%d prec=%s"
                           % (self.dims, act, self.max_batch, prec))
         self._h = h
         self.n = int(L.hf_num_params(h))
-        nbytes = int(L.hf_workspace_bytes(h))
+        nbytes = int(L.hf_workspace_bytes(
+            h, self.max_batch if ws_batch is None else int(ws_batch)))
+        if nbytes == 0:
+            raise ValueError("ws_batch %s outside [1, %d]" % (ws_batch, self.max_batch))
         self.device = torch.device(device)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
         self._check(L.hf_set_workspace(h, self.workspace.data_ptr(), nbytes))
@@ -363,6 +383,22 @@ class HFNet:
 
     def hf_check(self):
         self._check(lib().hf_check(self._h))
+
+    def set_trace(self, cap):
+        """Record the operand and result of the first `cap` curvature
+        products of every later solve (hf_set_trace); cap = 0 turns it off.
+        Returns the 2 cap x n trace tensor: row 2k the operand v of product
+        k, row 2k + 1 the undamped product A v."""
+        import torch
+        if cap <= 0:
+            self._check(lib().hf_set_trace(self._h, None, 0))
+            self._trace = None
+            return None
+        buf = torch.full((2 * int(cap), self.n), float("nan"), dtype=torch.float32,
+                         device=self.device)
+        self._check(lib().hf_set_trace(self._h, buf.data_ptr(), int(cap)))
+        self._trace = buf   # kept alive while tracing is on
+        return buf
 
     # ------------------------------------------------------------ profiling
     def prof_enable(self, on=True):

@@ -40,7 +40,7 @@ def test_every_declared_symbol_is_exported(L):
 def create(L, dims, act=H.HF_SIGMOID, prec=H.HF_FP32, max_batch=16):
     arr = (ctypes.c_int32 * len(dims))(*dims)
     h = ctypes.c_void_p()
-    rc = L.hf_create(arr, len(dims), act, prec, max_batch, ctypes.byref(h))
+    rc = L.hf_create(arr, len(dims), act, prec, max_batch, None, ctypes.byref(h))
     return rc, h
 
 
@@ -56,7 +56,9 @@ def test_create_validates(L):
     assert create(L, [4, 5000])[0] == H.HF_EINVAL           # > HF_MAX_CLASSES
     assert create(L, [2] * 18)[0] == H.HF_EINVAL            # > HF_MAX_LAYERS
     assert create(L, [1 << 20, 4096], max_batch=4096)[0] == H.HF_EINVAL  # 2^31
-    assert L.hf_create(None, 2, 0, 0, 4, None) == H.HF_EINVAL
+    assert L.hf_create(None, 2, 0, 0, 4, None, None) == H.HF_EINVAL
+    arr = (ctypes.c_int32 * 2)(4, 3)
+    assert L.hf_create(arr, 2, 0, 0, 4, None, None) == H.HF_EINVAL  # no out
 
 
 @pytest.mark.parametrize("dims", [(784, 100, 10), (784, 500, 500, 500, 10),
@@ -66,12 +68,18 @@ def test_num_params_and_workspace(L, dims):
     assert rc == H.HF_OK
     n = sum(dims[l] * (dims[l - 1] + 1) for l in range(1, len(dims)))
     assert L.hf_num_params(h) == n
-    ws = L.hf_workspace_bytes(h)
+    ws = L.hf_workspace_bytes(h, 0)
     assert ws > 4 * 3 * n  # at least the CG vectors
+    assert L.hf_workspace_bytes(h, 64) == ws
+    # the bytes grow with the batch the workspace serves
+    sizes = [L.hf_workspace_bytes(h, b) for b in (1, 2, 17, 63, 64)]
+    assert all(a <= b for a, b in zip(sizes, sizes[1:])) and sizes[0] > 4 * 3 * n
+    assert L.hf_workspace_bytes(h, 65) == 0
     assert L.hf_destroy(h) == H.HF_OK
     rc, h = create(L, list(dims), prec=H.HF_BF16_INPUTS, max_batch=64)
     assert rc == H.HF_OK and L.hf_num_params(h) == n
-    assert L.hf_workspace_bytes(h) > 4 * 3 * n
+    assert L.hf_workspace_bytes(h, 0) > 4 * 3 * n
+    assert L.hf_workspace_bytes(h, 1) <= L.hf_workspace_bytes(h, 64)
     assert L.hf_destroy(h) == H.HF_OK
 
 
@@ -105,10 +113,42 @@ def test_calls_without_workspace_or_with_bad_args(L):
 
 def test_null_context(L):
     assert L.hf_num_params(None) == -1
-    assert L.hf_workspace_bytes(None) == 0
+    assert L.hf_workspace_bytes(None, 0) == 0
+    assert L.hf_set_trace(None, None, 0) == H.HF_EINVAL
     assert L.hf_destroy(None) == H.HF_OK
     assert L.hf_last_error(None) == b"null context"
     assert L.hf_strerror(H.HF_ELABEL) == b"HF_ELABEL"
     assert L.hf_set_stream(None, None) == H.HF_EINVAL
     assert L.hf_check(None) == H.HF_EINVAL
     assert L.hf_prof_count(None) == 0
+
+
+def test_trace_arguments(L):
+    """hf_set_trace validates before any device call."""
+    rc, h = create(L, [8, 6, 4])
+    assert rc == H.HF_OK
+    assert L.hf_set_trace(h, None, -1) == H.HF_EINVAL
+    assert L.hf_set_trace(h, None, 3) == H.HF_EINVAL
+    assert L.hf_set_trace(h, ctypes.c_void_p(4096 + 4), 3) == H.HF_EINVAL
+    assert b"16-byte" in L.hf_last_error(h)
+    assert L.hf_set_trace(h, ctypes.c_void_p(4096), 3) == H.HF_OK  # not touched
+    assert L.hf_set_trace(h, None, 0) == H.HF_OK
+    assert L.hf_destroy(h) == H.HF_OK
+
+
+def test_build_id_matches_sources(L):
+    """The library reports the hash of the sources it was built from, and
+    the binding refuses a library whose hash differs from the sources on
+    disk."""
+    from paper_1606_00511_amd import buildid
+    assert L.hf_build_id().decode() == buildid.source_hash()
+    saved = H._lib
+    try:
+        H._lib = None
+        real = H.source_hash
+        H.source_hash = lambda: "0" * 64
+        with pytest.raises(RuntimeError, match="other sources"):
+            H.lib()
+    finally:
+        H.source_hash = real
+        H._lib = saved

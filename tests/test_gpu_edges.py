@@ -141,3 +141,70 @@ def test_max_layers(act):
             (oi["iters"], oi["products"], oi["neg_curv"], oi["neg_iter"])
         if oi["neg_curv"]:
             assert np.sign(gi["pBp"]) == np.sign(oi["pBp"])
+
+
+@pytest.mark.parametrize("solver", ["hf_cg", "hf_bicgstab"])
+def test_non_finite_scalars_are_reported(solver):
+    """A NaN in g makes |g|^2 non-finite: the solve stops before its first
+    product and returns HF_ENUMERIC with info.status set.  An Inf weight
+    makes the first product, hence p^T B p, non-finite: the solve stops
+    after that product with HF_ENUMERIC.  These are numeric outcomes, not
+    faults; the context then solves a clean system as before."""
+    from paper_1606_00511_amd import hf as H
+    dims, act, B = (37, 45, 13), "tanh", 40
+    p = WL.make_small(dims, act, B, seed=5)
+    h = H.HFNet(dims, act, B)
+    L = H.lib()
+    W, X, y = dev(p["theta"]), dev(p["X"]), dev(p["y"])
+    _, g = h.hf_loss_grad(W, X, y)
+    ref_step, _, ref_info = getattr(h, solver)(W, X, y, g, 1e-2, 4, "gauss_newton")
+    ref_step = host(ref_step)
+    step, nd = g.clone(), g.clone()
+
+    def call(Wt, gt):
+        info = H.hf_cg_info()
+        rc = getattr(L, solver)(h._h, Wt.data_ptr(), X.data_ptr(), y.data_ptr(), B,
+                                gt.data_ptr(), 1e-2, 4, 0.0, H.HF_GAUSS_NEWTON,
+                                step.data_ptr(), nd.data_ptr(), ctypes.byref(info))
+        return rc, info
+
+    g_nan = g.clone()
+    g_nan[7] = float("nan")
+    rc, info = call(W, g_nan)
+    assert rc == H.HF_ENUMERIC and info.status == H.HF_ENUMERIC
+    assert info.products == 0 and info.iters == 0
+    assert b"non-finite" in L.hf_last_error(h._h)
+    W_inf = W.clone()
+    W_inf[h.n - 20] = float("inf")     # a weight of the output layer
+    rc, info = call(W_inf, g)
+    assert rc == H.HF_ENUMERIC and info.status == H.HF_ENUMERIC
+    assert info.products >= 1 and info.iters == 0
+    s2, _, i2 = getattr(h, solver)(W, X, y, g, 1e-2, 4, "gauss_newton")
+    assert i2 == ref_info
+    assert np.array_equal(host(s2), ref_step)
+
+
+def test_workspace_for_fewer_rows():
+    """A workspace laid out for b < max_batch rows serves calls up to b rows
+    with the results of a full-size one, and rejects more rows with
+    HF_EWORKSPACE, leaving the output untouched."""
+    import torch
+    from paper_1606_00511_amd import hf as H
+    dims, act, B = (100, 200, 150, 37), "sigmoid", 300
+    p = WL.make_small(dims, act, B, seed=6)
+    full = H.HFNet(dims, act, B)
+    part = H.HFNet(dims, act, B, ws_batch=120)
+    assert part.workspace.numel() < full.workspace.numel()
+    W, X, y, v = dev(p["theta"]), dev(p["X"]), dev(p["y"]), dev(p["v"])
+    for mode in ("hessian", "gauss_newton"):
+        a = host(full.hf_hvp(W, X[:120], y[:120], v, mode))
+        b = host(part.hf_hvp(W, X[:120], y[:120], v, mode))
+        assert np.array_equal(a, b)
+    out = torch.full((part.n,), 7.0, device="cuda")
+    with pytest.raises(H.HFError) as e:
+        part.hf_hvp(W, X[:121], y[:121], v, "hessian", out=out)
+    assert e.value.code == H.HF_EWORKSPACE
+    assert bool((out == 7.0).all())
+    f1, g1 = full.hf_loss_grad(W, X[:120], y[:120])
+    f2, g2 = part.hf_loss_grad(W, X[:120], y[:120])
+    assert np.array_equal(host(g1), host(g2)) and float(host(f1)[0]) == float(host(f2)[0])
