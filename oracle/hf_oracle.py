@@ -127,9 +127,11 @@ def phi(act, z):
 def dphi(act, z, kink=0.0):
     """phi'(z), written directly from the definition of each activation.
 
-    ``kink`` moves ReLU's step: phi'(z) = 1[z > kink].  The method uses
-    kink = 0 (ReLU'(0) = 0); tests evaluate kink = -tau and +tau to bound
-    the effect of pre-activations that lie within fp32 rounding of 0."""
+    ``kink`` moves ReLU's step: phi'(z) = 1[z > kink], a scalar or an array
+    shaped like z (one position per unit).  The method uses kink = 0
+    (ReLU'(0) = 0); tests move it to either side of 0 by each unit's fp32
+    rounding margin to bound the effect of pre-activations that lie within
+    that margin of 0."""
     if act == "sigmoid":
         s = 1.0 / (1.0 + np.exp(-z))
         return s * (1.0 - s)
@@ -152,6 +154,13 @@ def d2phi(act, z):
     if act == "relu":
         return np.zeros_like(z)
     raise ValueError(act)
+
+
+def _kink(kink, i):
+    """ReLU step position for the pre-activations Z[i] of hidden layer i + 1:
+    ``kink`` is one scalar for every unit, or a sequence holding one array
+    per hidden layer, shaped like that layer's Z."""
+    return kink if np.isscalar(kink) else kink[i]
 
 
 # ---------------------------------------------------------------- the network
@@ -206,7 +215,7 @@ def loss_grad(dims, act, theta, X, y, kink=0.0):
         W, _ = layers[l - 1]
         grads[l - 1] = (delta.T @ A[l - 1], delta.sum(axis=0))
         if l > 1:
-            delta = (delta @ W) * dphi(act, Z[l - 2], kink)  # df/dZ_{l-1}
+            delta = (delta @ W) * dphi(act, Z[l - 2], _kink(kink, l - 2))  # df/dZ_{l-1}
     return f, pack(grads)
 
 
@@ -222,7 +231,7 @@ def _r_forward(dims, act, theta, v, X, kink=0.0):
         rz = A[l - 1] @ V.T + c + RA[l - 1] @ W.T
         RZ.append(rz)
         if l < len(layers):
-            RA.append(dphi(act, Z[l - 1], kink) * rz)
+            RA.append(dphi(act, Z[l - 1], _kink(kink, l - 1)) * rz)
     return layers, vlayers, Z, A, RZ, RA
 
 
@@ -249,8 +258,9 @@ def hvp(dims, act, theta, X, y, v, kink=0.0):
             e = delta @ W
             re = rdelta @ W + delta @ V
             zp = Z[l - 2]
-            new_delta = e * dphi(act, zp, kink)
-            rdelta = re * dphi(act, zp, kink) + e * d2phi(act, zp) * RZ[l - 2]
+            dp = dphi(act, zp, _kink(kink, l - 2))
+            new_delta = e * dp
+            rdelta = re * dp + e * d2phi(act, zp) * RZ[l - 2]
             delta = new_delta
     return pack(out)
 
@@ -271,7 +281,7 @@ def gvp(dims, act, theta, X, v, kink=0.0):
         W, _ = layers[l - 1]
         out[l - 1] = (u.T @ A[l - 1], u.sum(axis=0))
         if l > 1:
-            u = (u @ W) * dphi(act, Z[l - 2], kink)
+            u = (u @ W) * dphi(act, Z[l - 2], _kink(kink, l - 2))
     return pack(out)
 
 
@@ -385,8 +395,9 @@ def fisher_diag(dims, act, theta, X, y, kink=0.0):
     B = X.shape[0]
     F = np.zeros(num_params(dims))
     for b in range(B):
+        kb = kink if np.isscalar(kink) else [k[b:b + 1] for k in kink]
         _, gb = loss_grad(dims, act, theta, X[b:b + 1], np.asarray(y)[b:b + 1],
-                          kink)
+                          kb)
         F += gb * gb
     return F / B
 

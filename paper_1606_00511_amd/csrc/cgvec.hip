@@ -848,7 +848,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_waxpy(
 extern "C" __global__ __launch_bounds__(256) void hf_keep_iterate(
     float* __restrict__ dst, const float* __restrict__ src, long long n,
     const int* __restrict__ skip) {
-  if (*skip) return;
+  if (skip && *skip) return;
   const long long stride = (long long)gridDim.x * NT;
   for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n; i += stride)
     dst[i] = src[i];

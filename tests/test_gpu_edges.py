@@ -18,7 +18,7 @@ import pytest
 
 from oracle import hf_oracle as O
 from paper_1606_00511_amd import workloads as WL
-from tests.parity_util import check, rel
+from tests.parity_util import check, rel, relu_margins
 
 pytestmark = pytest.mark.gpu
 
@@ -125,13 +125,15 @@ def test_max_layers(act):
     f, g = h.hf_loss_grad(W, X, y)
     f_o, g_o = O.loss_grad(dims, act, p["theta"], p["X"], p["y"])
     assert abs(float(host(f)[0]) - f_o) <= 1e-4 * abs(f_o)
+    mg = relu_margins(dims, act, p["theta"], p["X"])
     check(host(g), g_o, act, lambda k: O.loss_grad(dims, act, p["theta"], p["X"],
-                                                    p["y"], kink=k)[1])
+                                                    p["y"], kink=k)[1], margins=mg)
     for mode in ("hessian", "gauss_newton"):
         out = h.hf_hvp(W, X, y, v, mode)
         ref = O.curvature(dims, act, p["theta"], p["X"], p["y"], p["v"], mode)
         check(host(out), ref, act, lambda k: O.curvature(
-            dims, act, p["theta"], p["X"], p["y"], p["v"], mode, kink=k))
+            dims, act, p["theta"], p["X"], p["y"], p["v"], mode, kink=k),
+            margins=mg)
     g32 = g_o.astype(np.float32)
     for mode in ("hessian", "gauss_newton"):
         _, _, gi = h.hf_cg(W, X, y, dev(g32), 1e-2, 6, mode)

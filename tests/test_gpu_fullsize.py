@@ -16,7 +16,7 @@ import pytest
 
 from oracle import hf_oracle as O
 from paper_1606_00511_amd import workloads as WL
-from tests.parity_util import check
+from tests.parity_util import ambiguous_units, check, relu_margins
 
 pytestmark = pytest.mark.gpu
 
@@ -76,10 +76,12 @@ def test_full_loss_grad(name):
     s["grad"] = grad
     s["g_np"] = host(grad)
     assert abs(float(host(loss)[0]) - f_o) <= TOL * abs(f_o)
+    mg = relu_margins(w.dims, w.act, inp["theta"], inp["X"])
     err, bound = check(s["g_np"], g_o, w.act, lambda k: O.loss_grad(
-        w.dims, w.act, inp["theta"], inp["X"], inp["y"], kink=k)[1])
-    print("%s loss %.6f vs %.6f, grad rel %.2e (bound %.2e)" % (
-        name, float(host(loss)[0]), f_o, err, bound))
+        w.dims, w.act, inp["theta"], inp["X"], inp["y"], kink=k)[1], margins=mg)
+    print("%s loss %.6f vs %.6f, grad rel %.2e (bound %.2e, %d ambiguous units)" % (
+        name, float(host(loss)[0]), f_o, err, bound,
+        ambiguous_units(w.dims, w.act, inp["theta"], inp["X"], mg)))
 
 
 @pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
@@ -90,9 +92,11 @@ def test_full_product(name, mode):
     out = host(s["net"].hf_hvp(s["W"], s["Xc"], s["yc"], s["v"], mode))
     Xc, yc = inp["X"][:w.curv_batch], inp["y"][:w.curv_batch]
     ref = O.curvature(w.dims, w.act, inp["theta"], Xc, yc, inp["v"], mode)
+    mg = relu_margins(w.dims, w.act, inp["theta"], Xc)
     err, bound = check(out, ref, w.act, lambda k: O.curvature(
-        w.dims, w.act, inp["theta"], Xc, yc, inp["v"], mode, kink=k))
-    print("%s %s rel %.2e (bound %.2e)" % (name, mode, err, bound))
+        w.dims, w.act, inp["theta"], Xc, yc, inp["v"], mode, kink=k), margins=mg)
+    print("%s %s rel %.2e (bound %.2e, %d ambiguous units)" % (
+        name, mode, err, bound, ambiguous_units(w.dims, w.act, inp["theta"], Xc, mg)))
 
 
 @pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])

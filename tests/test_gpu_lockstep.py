@@ -27,7 +27,7 @@ import pytest
 
 from oracle import hf_oracle as O
 from paper_1606_00511_amd import workloads as WL
-from tests.parity_util import check
+from tests.parity_util import check, relu_margins
 
 pytestmark = pytest.mark.gpu
 
@@ -52,6 +52,7 @@ def compare_trace(tr, products, dims, act, theta, Xc, yc, mode, tol, tag,
     products evaluated must still hold the NaN fill."""
     cap = tr.shape[0] // 2
     worst = 0.0
+    margins = relu_margins(dims, act, theta, Xc) if tau is None else None
     for k in range(cap):
         v, q = tr[2 * k], tr[2 * k + 1]
         if k >= products:
@@ -63,7 +64,7 @@ def compare_trace(tr, products, dims, act, theta, Xc, yc, mode, tol, tag,
             assert np.array_equal(v, -g), "%s: p_0 != -g" % tag
         v64 = v.astype(np.float64)
         ref = O.curvature(dims, act, theta, Xc, yc, v64, mode)
-        kw = {} if tau is None else {"tau": tau}
+        kw = {"tau": tau} if tau is not None else {"margins": margins}
         err, bound = check(q, ref, act, lambda kink: O.curvature(
             dims, act, theta, Xc, yc, v64, mode, kink=kink), tol=tol, **kw)
         worst = max(worst, err)

@@ -13,7 +13,7 @@ import pytest
 
 from oracle import hf_oracle as O
 from paper_1606_00511_amd import workloads as WL
-from tests.parity_util import check
+from tests.parity_util import check, relu_margins
 
 pytestmark = pytest.mark.gpu
 
@@ -87,7 +87,8 @@ def test_loss_grad(case):
     h.hf_check()
     assert abs(float(host(loss)[0]) - f_o) <= TOL * abs(f_o)
     check(host(grad), g_o, act, lambda k: O.loss_grad(
-        dims, act, p["theta"], p["X"], p["y"], kink=k)[1])
+        dims, act, p["theta"], p["X"], p["y"], kink=k)[1],
+        margins=relu_margins(dims, act, p["theta"], p["X"]))
 
 
 @pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
@@ -99,7 +100,8 @@ def test_curvature_product(case, mode):
     h = net(dims, act, B)
     out = h.hf_hvp(dev(p["theta"]), dev(p["X"]), dev(p["y"]), dev(p["v"]), mode)
     check(host(out), ref, act, lambda k: O.curvature(
-        dims, act, p["theta"], p["X"], p["y"], p["v"], mode, kink=k))
+        dims, act, p["theta"], p["X"], p["y"], p["v"], mode, kink=k),
+        margins=relu_margins(dims, act, p["theta"], p["X"]))
 
 
 def test_gauss_newton_ignores_labels_and_is_deterministic():

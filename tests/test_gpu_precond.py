@@ -57,7 +57,8 @@ def test_fisher_diag(case):
     h.hf_check()
     ref = O.fisher_diag(dims, act, p["theta"], p["X"], p["y"])
     err, bound = check(F, ref, act, lambda k: O.fisher_diag(
-        dims, act, p["theta"], p["X"], p["y"], kink=k))
+        dims, act, p["theta"], p["X"], p["y"], kink=k),
+        margins=relu_margins(dims, act, p["theta"], p["X"]))
     print("F rel %.2e (bound %.2e)" % (err, bound))
     assert np.all(F >= 0.0)
 
