@@ -12,7 +12,9 @@ import os
 from paper_1606_00511_amd.buildid import source_hash
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libhf.so")
+# HF_LIB_PATH names another build of the same sources (the host-sanitizer
+# build of the CPU tests); by default the in-tree library.
+LIB_PATH = os.environ.get("HF_LIB_PATH") or os.path.join(HERE, "libhf.so")
 
 HF_SIGMOID, HF_TANH, HF_RELU = 0, 1, 2
 HF_HESSIAN, HF_GAUSS_NEWTON, HF_HYBRID = 0, 1, 2
@@ -33,7 +35,7 @@ EXPORTS = (
     "hf_create", "hf_destroy", "hf_set_stream", "hf_num_params",
     "hf_workspace_bytes", "hf_set_workspace", "hf_loss_grad", "hf_hvp",
     "hf_cg", "hf_pcg", "hf_fisher_diag", "hf_bicgstab", "hf_loss", "hf_iterate",
-    "hf_set_trace", "hf_build_id", "hf_check", "hf_last_error",
+    "hf_set_trace", "hf_build_id", "hf_hvp_noalloc", "hf_check", "hf_last_error",
     "hf_strerror", "hf_prof_enable", "hf_prof_only",
     "hf_prof_reset", "hf_prof_count", "hf_prof_get",
 )
@@ -122,6 +124,7 @@ def lib():
         "hf_set_workspace": (ctypes.c_int, [P, P, SZ]),
         "hf_loss_grad": (ctypes.c_int, [P, P, P, P, I64, P, P]),
         "hf_hvp": (ctypes.c_int, [P, P, P, P, I64, P, I32, P]),
+        "hf_hvp_noalloc": (ctypes.c_int, [P, P, P, P, I64, P, I32, P, P]),
         "hf_cg": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P, P,
                                  ctypes.POINTER(hf_cg_info)]),
         "hf_bicgstab": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P,

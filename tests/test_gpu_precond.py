@@ -19,7 +19,7 @@ import pytest
 
 from oracle import hf_oracle as O
 from paper_1606_00511_amd import workloads as WL
-from tests.parity_util import check, rel
+from tests.parity_util import check, rel, relu_margins
 
 pytestmark = pytest.mark.gpu
 
