@@ -339,6 +339,35 @@ int hf_set_trace(hf_ctx* ctx, float* buf, int32_t cap);
 /* SHA-256 (hex) of the sources the library was built from. */
 const char* hf_build_id(void);
 
+/* Bytes of the device scratch that hf_hvp_noalloc uses in place of a
+ * workspace: one array per GPU, held until the process ends. */
+#define HF_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/*
+ * hf_hvp_noalloc: hf_hvp for callers that cannot allocate device memory or
+ * hand over a workspace (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  It computes what hf_hvp computes, with
+ * the same kernels, but its scratch is a static device array of
+ * HF_NOALLOC_SCRATCH_BYTES per GPU instead of the context's workspace
+ * (none needs to be set).  It makes no allocating call (no hipMalloc,
+ * hipFree, memset node or host-side device allocation), is asynchronous on
+ * the context's stream, and can be captured into a graph.
+ *   label_err  device int32 or NULL: set to 0 by the call, then to 1 if a
+ *              label outside [0, d_L) was seen (hf_hvp reports this through
+ *              hf_check instead; without label_err it is not reported).
+ * The scratch holds the activations, deltas and split-K partials of one
+ * product at B rows (less than hf_workspace_bytes(ctx, B), which also
+ * holds the solvers' vectors); a batch whose layout needs more than
+ * HF_NOALLOC_SCRATCH_BYTES returns HF_EWORKSPACE before any device work.  Every call on one GPU shares that GPU's scratch and leaves
+ * its contents there: calls that may overlap on one GPU (other streams,
+ * other threads, other contexts) race and must be serialised by the caller.
+ * The context's workspace, if any, is not touched.  Other arguments and
+ * errors as for hf_hvp; the context's kernel profiler does not time it.
+ */
+int hf_hvp_noalloc(hf_ctx* ctx, const float* W, const float* X,
+                   const int32_t* y, int64_t B, const float* v, int32_t mode,
+                   float* out, int32_t* label_err);
+
 /* Synchronise the stream and report a device-detected error (HF_ELABEL)
  * raised since the last hf_check; clears the flag. */
 int hf_check(hf_ctx* ctx);

@@ -236,11 +236,19 @@ struct hf_ctx {
   // trace_cap curvature products of every solve
   float* trace_buf = nullptr;
   int trace_cap = 0;
+  // the label-error flag, when it lives outside the workspace
+  int* err_override = nullptr;
+  // layout of the no-allocation entry point's device scratch (made on its
+  // first call, re-planned for each call's batch)
+  hf_ctx* na = nullptr;
 
   float* F(size_t off) const { return reinterpret_cast<float*>(ws + off); }
   double* Dp(size_t off) const { return reinterpret_cast<double*>(ws + off); }
   bf16_t* H(size_t off) const { return reinterpret_cast<bf16_t*>(ws + off); }
   bool bf16() const { return prec == HF_BF16_INPUTS; }
+  int* errp() const {
+    return err_override ? err_override : reinterpret_cast<int*>(ws + oErr);
+  }
   Launch launch() const { return Launch{stream, prof}; }
 };
 
@@ -272,8 +280,10 @@ inline int round4(int x) { return (x + 3) & ~3; }
 inline int round64(int x) { return (x + 63) & ~63; }
 inline size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Carve the workspace for calls of up to B rows (B <= Bmax).
-void plan(hf_ctx* c, int64_t Bplan) {
+// Carve the workspace for calls of up to B rows (B <= Bmax).  A
+// product-only layout holds what a stateless curvature product uses: no
+// transposed weights (fp32) and no solver vectors or state.
+void plan(hf_ctx* c, int64_t Bplan, bool product_only = false) {
   c->Bws = Bplan;
   c->ldB = round64((int)Bplan);
   const int L = c->L;
@@ -295,13 +305,13 @@ void plan(hf_ctx* c, int64_t Bplan) {
   // to a multiple of 256: the GEMM tiles read them without bounds checks
   const size_t RB = h ? round256(B) : B;
   auto R256 = [&](int d) { return round256((size_t)d); };
-  if (!h) {
+  if (!h && !product_only) {
     for (int l = 1; l <= L; ++l) {
       // W_l and V_l transposed: d_{l-1} rows of ld_l floats
       c->oWT[l] = take((size_t)c->d[l - 1] * c->ld[l] * f4);
       c->oVT[l] = take((size_t)c->d[l - 1] * c->ld[l] * f4);
     }
-  } else {
+  } else if (h) {
     c->hbeg = off;
     for (int l = 1; l <= L; ++l) {
       // bf16 W_l, V_l (row-major, forward) and transposed (backward)
@@ -372,6 +382,14 @@ void plan(hf_ctx* c, int64_t Bplan) {
   c->split_floats = std::max(wg, rows);
   c->oSplit = take(c->split_floats * f4);
   c->oBpart = take((size_t)c->max_splits * dmax * sizeof(double));
+  c->oLoss = take(((B + 3) / 4) * sizeof(double));
+  c->oErr = take(sizeof(int));
+  if (product_only) {
+    c->oR = c->oPv = c->oQ = c->oS = c->oT = c->oRs = c->oG = c->oStep = c->oNd =
+        c->oX0 = c->oWt = c->oScal = c->oRed = c->oState = 0;
+    c->need = off;
+    return;
+  }
   const size_t nv = ((size_t)c->n + 63) & ~size_t(63);
   c->oR = take(nv * f4);
   c->oPv = take(nv * f4);
@@ -386,10 +404,8 @@ void plan(hf_ctx* c, int64_t Bplan) {
   c->oWt = take(nv * f4);
   c->oScal = take(8 * sizeof(double));
   c->oRed = take((size_t)cg_part_doubles() * sizeof(double));
-  c->oLoss = take(((B + 3) / 4) * sizeof(double));
   c->oState = take(sizeof(CgState) > sizeof(BicgState) ? sizeof(CgState)
                                                         : sizeof(BicgState));
-  c->oErr = take(sizeof(int));
   c->need = off;
 }
 
@@ -417,8 +433,9 @@ int check_batch(hf_ctx* c, int64_t B) {
   return HF_OK;
 }
 
-// Bytes of workspace for calls of up to B rows.
-size_t plan_bytes(const hf_ctx* c, int64_t B) {
+// Bytes of workspace for calls of up to B rows (product_only: the layout of
+// a stateless curvature product alone).
+size_t plan_bytes(const hf_ctx* c, int64_t B, bool product_only = false) {
   hf_ctx t;
   t.L = c->L;
   t.d = c->d;
@@ -429,7 +446,7 @@ size_t plan_bytes(const hf_ctx* c, int64_t B) {
   t.Bmax = c->Bmax;
   t.n = c->n;
   t.max_splits = c->max_splits;
-  plan(&t, B);
+  plan(&t, B, product_only);
   return t.need;
 }
 
@@ -550,7 +567,7 @@ void forward_plain(hf_ctx* c, const float* W, const float* X, int B,
   }
   softmax_xent(Lc, c->F(c->oZ), y, B, c->d[c->L], c->ld[c->L], c->F(c->oP),
                want_delta ? c->F(c->oD[c->L]) : nullptr, c->Dp(c->oLoss),
-               reinterpret_cast<int*>(c->ws + c->oErr));
+               c->errp());
 }
 
 // Backward data pass delta_{l-1} = (delta_l W_l) phi'(A_{l-1}); optionally
@@ -734,7 +751,7 @@ void forward_plain_h(hf_ctx* c, const float* W, const float* X, int B,
   }
   softmax_xent(Lc, c->F(c->oZ), y, B, c->d[L], c->ld[L], c->F(c->oP),
                want_delta ? c->F(c->oD[L]) : nullptr, c->Dp(c->oLoss),
-               reinterpret_cast<int*>(c->ws + c->oErr));
+               c->errp());
   if (want_delta) delta_h(c, c->F(c->oD[L]), B, c->hD[L], c->hDT[L], nullptr);
 }
 
@@ -859,7 +876,7 @@ void hvp_h(hf_ctx* c, const float* W, const float* X, const int32_t* y, int B,
   }
   softmax_xent(Lc, c->F(c->oZ), hess ? y : nullptr, B, c->d[L], c->ld[L],
                c->F(c->oP), hess ? c->F(c->oD[L]) : nullptr, c->Dp(c->oLoss),
-               reinterpret_cast<int*>(c->ws + c->oErr));
+               c->errp());
   if (hess) delta_h(c, c->F(c->oD[L]), B, c->hD[L], c->hDT[L], nullptr);
   softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), B, c->d[L], c->ld[L],
               c->F(c->oRD[L]), nullptr);
@@ -1143,6 +1160,78 @@ int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
 
 }  // namespace
 
+namespace {
+
+// Stateless product out = A v on B rows (arguments already checked).
+void hvp_any(hf_ctx* c, const float* W, const float* X, const int32_t* y, int b,
+             const float* v, int mode, float* out) {
+  const Launch Lc = c->launch();
+  const int L = c->L;
+  if (c->bf16()) {
+    hvp_h(c, W, X, y, b, v, mode, out);
+    return;
+  }
+  // forward fused with R-forward
+  for (int l = 1; l <= L; ++l) {
+    GemmShape s;
+    if (l == 1) {
+      s = shape(b, c->d[1], c->d[0], X, nullptr, W + c->offW[1], v + c->offW[1],
+                c->d[0], c->d[0], 1, nullptr);
+    } else {
+      s = shape(b, c->d[l], c->d[l - 1], c->F(c->oA[l - 1]), c->F(c->oRA[l - 1]),
+                W + c->offW[l], v + c->offW[l], c->ld[l - 1], c->d[l - 1], 1,
+                nullptr);
+    }
+    EpiArgs e = epi(c, l < L);
+    e.bias = W + c->offB[l];
+    e.rbias = v + c->offB[l];
+    e.out0 = (l < L) ? c->F(c->oA[l]) : c->F(c->oZ);
+    e.out1 = c->F(c->oRZ[l]);
+    e.out2 = (l < L) ? c->F(c->oRA[l]) : nullptr;
+    e.ldo = c->ld[l];
+    gemm_fwd_rfwd(Lc, s, e);
+  }
+  const bool hess = mode == HF_HESSIAN;
+  softmax_xent(Lc, c->F(c->oZ), hess ? y : nullptr, b, c->d[L], c->ld[L],
+               c->F(c->oP), hess ? c->F(c->oD[L]) : nullptr, c->Dp(c->oLoss),
+               c->errp());
+  softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), b, c->d[L], c->ld[L],
+              c->F(c->oRD[L]), nullptr);
+  for (int l = L; l >= 1; --l) {
+    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
+    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
+    if (hess && l > 1) {
+      wgrad(c, l, b, c->F(c->oRD[l]), Ain, c->F(c->oD[l]), c->F(c->oRA[l - 1]),
+            ldin, out, nullptr);
+    } else {
+      wgrad(c, l, b, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin, out, nullptr);
+    }
+    if (l == 1) break;
+    EpiArgs e = epi(c, 1);
+    e.ldo = c->ld[l - 1];
+    e.aux0 = c->F(c->oA[l - 1]);
+    e.lda = c->ld[l - 1];
+    if (hess) {
+      // (E, RE) = (delta W, Rdelta W + delta V) in one pass
+      GemmShape s = shape(b, c->d[l - 1], c->d[l], c->F(c->oD[l]), c->F(c->oRD[l]),
+                          W + c->offW[l], v + c->offW[l], c->ld[l], c->d[l - 1],
+                          1, nullptr);
+      e.out0 = c->F(c->oD[l - 1]);
+      e.out1 = c->F(c->oRD[l - 1]);
+      e.aux1 = c->F(c->oRZ[l - 1]);
+      gemm_bwd_rbwd(Lc, s, e);
+    } else {
+      GemmShape s = shape(b, c->d[l - 1], c->d[l], c->F(c->oRD[l]), nullptr,
+                          W + c->offW[l], nullptr, c->ld[l], c->d[l - 1], 1,
+                          nullptr);
+      e.out1 = c->F(c->oRD[l - 1]);
+      gemm_gnbwd(Lc, s, e);
+    }
+  }
+}
+
+}  // namespace
+
 // ==================================================================== C ABI
 extern "C" {
 
@@ -1194,6 +1283,7 @@ int hf_create(const int32_t* dims, int32_t n_dims, int32_t act, int32_t prec,
 int hf_destroy(hf_ctx* c) {
   if (!c) return HF_OK;
   delete c->prof;
+  delete c->na;
   if (c->pinned) (void)hipHostFree(c->pinned);
   if (c->pinned_bicg) (void)hipHostFree(c->pinned_bicg);
   for (auto& e : c->ev)
@@ -1285,70 +1375,64 @@ int hf_hvp(hf_ctx* c, const float* W, const float* X, const int32_t* y,
   if (mode != HF_HESSIAN && mode != HF_GAUSS_NEWTON)
     return fail(c, HF_EINVAL, "unknown mode %d", mode);
   if (mode == HF_HESSIAN && !y) return fail(c, HF_EINVAL, "y is NULL");
-  const Launch Lc = c->launch();
-  const int b = (int)B, L = c->L;
-  if (c->bf16()) {
-    hvp_h(c, W, X, y, b, v, mode, out);
-    HIP_TRY(c, hipGetLastError());
-    return HF_OK;
+  hvp_any(c, W, X, y, (int)B, v, mode, out);
+  HIP_TRY(c, hipGetLastError());
+  return HF_OK;
+}
+
+int hf_hvp_noalloc(hf_ctx* c, const float* W, const float* X, const int32_t* y,
+                   int64_t B, const float* v, int32_t mode, float* out,
+                   int32_t* label_err) {
+  int rc;
+  if (!c) return HF_EINVAL;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, X, "X")) ||
+      (rc = check_ptr(c, v, "v")) || (rc = check_ptr(c, out, "out")))
+    return rc;
+  if (B < 1 || B > c->Bmax)
+    return fail(c, HF_EINVAL, "batch %lld outside [1, %lld]", (long long)B,
+                (long long)c->Bmax);
+  if (mode != HF_HESSIAN && mode != HF_GAUSS_NEWTON)
+    return fail(c, HF_EINVAL, "unknown mode %d", mode);
+  if (mode == HF_HESSIAN && !y) return fail(c, HF_EINVAL, "y is NULL");
+  if (label_err && ((uintptr_t)label_err & 3u))
+    return fail(c, HF_EINVAL, "label_err is not 4-byte aligned");
+  const size_t need = plan_bytes(c, B, true);
+  if (need > (size_t)HF_NOALLOC_SCRATCH_BYTES)
+    return fail(c, HF_EWORKSPACE,
+                "%lld rows need %zu bytes of scratch; the no-allocation scratch "
+                "holds %zu", (long long)B, need, (size_t)HF_NOALLOC_SCRATCH_BYTES);
+  void* base = nullptr;
+  HIP_TRY(c, noalloc_scratch(&base));
+  if (!c->na) {
+    c->na = new (std::nothrow) hf_ctx();
+    if (!c->na) return fail(c, HF_ENOMEM, "no host memory for the scratch layout");
+    hf_ctx& t = *c->na;
+    t.L = c->L;
+    t.d = c->d;
+    t.ld = c->ld;
+    t.ldh = c->ldh;
+    t.act = c->act;
+    t.prec = c->prec;
+    t.Bmax = c->Bmax;
+    t.n = c->n;
+    t.offW = c->offW;
+    t.offB = c->offB;
+    t.max_splits = c->max_splits;
   }
-  // forward fused with R-forward
-  for (int l = 1; l <= L; ++l) {
-    GemmShape s;
-    if (l == 1) {
-      s = shape(b, c->d[1], c->d[0], X, nullptr, W + c->offW[1], v + c->offW[1],
-                c->d[0], c->d[0], 1, nullptr);
-    } else {
-      s = shape(b, c->d[l], c->d[l - 1], c->F(c->oA[l - 1]), c->F(c->oRA[l - 1]),
-                W + c->offW[l], v + c->offW[l], c->ld[l - 1], c->d[l - 1], 1,
-                nullptr);
-    }
-    EpiArgs e = epi(c, l < L);
-    e.bias = W + c->offB[l];
-    e.rbias = v + c->offB[l];
-    e.out0 = (l < L) ? c->F(c->oA[l]) : c->F(c->oZ);
-    e.out1 = c->F(c->oRZ[l]);
-    e.out2 = (l < L) ? c->F(c->oRA[l]) : nullptr;
-    e.ldo = c->ld[l];
-    gemm_fwd_rfwd(Lc, s, e);
-  }
-  const bool hess = mode == HF_HESSIAN;
-  softmax_xent(Lc, c->F(c->oZ), hess ? y : nullptr, b, c->d[L], c->ld[L],
-               c->F(c->oP), hess ? c->F(c->oD[L]) : nullptr, c->Dp(c->oLoss),
-               reinterpret_cast<int*>(c->ws + c->oErr));
-  softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), b, c->d[L], c->ld[L],
-              c->F(c->oRD[L]), nullptr);
-  for (int l = L; l >= 1; --l) {
-    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
-    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
-    if (hess && l > 1) {
-      wgrad(c, l, b, c->F(c->oRD[l]), Ain, c->F(c->oD[l]), c->F(c->oRA[l - 1]),
-            ldin, out, nullptr);
-    } else {
-      wgrad(c, l, b, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin, out, nullptr);
-    }
-    if (l == 1) break;
-    EpiArgs e = epi(c, 1);
-    e.ldo = c->ld[l - 1];
-    e.aux0 = c->F(c->oA[l - 1]);
-    e.lda = c->ld[l - 1];
-    if (hess) {
-      // (E, RE) = (delta W, Rdelta W + delta V) in one pass
-      GemmShape s = shape(b, c->d[l - 1], c->d[l], c->F(c->oD[l]), c->F(c->oRD[l]),
-                          W + c->offW[l], v + c->offW[l], c->ld[l], c->d[l - 1],
-                          1, nullptr);
-      e.out0 = c->F(c->oD[l - 1]);
-      e.out1 = c->F(c->oRD[l - 1]);
-      e.aux1 = c->F(c->oRZ[l - 1]);
-      gemm_bwd_rbwd(Lc, s, e);
-    } else {
-      GemmShape s = shape(b, c->d[l - 1], c->d[l], c->F(c->oRD[l]), nullptr,
-                          W + c->offW[l], nullptr, c->ld[l], c->d[l - 1], 1,
-                          nullptr);
-      e.out1 = c->F(c->oRD[l - 1]);
-      gemm_gnbwd(Lc, s, e);
-    }
-  }
+  hf_ctx& t = *c->na;
+  t.stream = c->stream;
+  t.prof = nullptr;
+  t.ws = nullptr;
+  plan(&t, B, true);
+  t.ws = reinterpret_cast<char*>(base);
+  t.ws_bytes = HF_NOALLOC_SCRATCH_BYTES;
+  t.err_override = label_err;
+  // what must start at zero: the label flag and, for bf16 operands, their
+  // padding (another call may have left anything there)
+  const Launch Lt = t.launch();
+  fill_zero(Lt, t.errp(), sizeof(int));
+  if (t.hend > t.hbeg) fill_zero(Lt, t.ws + t.hbeg, t.hend - t.hbeg);
+  hvp_any(&t, W, X, y, (int)B, v, mode, out);
   HIP_TRY(c, hipGetLastError());
   return HF_OK;
 }

@@ -273,6 +273,13 @@ void waxpy(const Launch& L, float* out, const float* w, double a,
 // dst = src unless *skip (device flag of a solve that has stopped)
 void keep_iterate(const Launch& L, float* dst, const float* src, long long n,
                   const int* skip);
+// ------------------------------------------------ no-allocation scratch
+// Device address of this GPU's HF_NOALLOC_SCRATCH_BYTES scratch array,
+// looked up on the first call on each device (the current device).
+hipError_t noalloc_scratch(void** out);
+// Zero bytes (a multiple of 4) at p with a fill kernel on L.stream.
+void fill_zero(const Launch& L, void* p, size_t bytes);
+
 // out[k] = a[k] . b[k] for k < 4 (device doubles), fixed summation order;
 // uses the first 4 partial regions of part
 void dots4(const Launch& L, const float* const a[4], const float* const b[4],

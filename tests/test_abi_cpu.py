@@ -152,3 +152,23 @@ def test_build_id_matches_sources(L):
     finally:
         H.source_hash = real
         H._lib = saved
+
+
+def test_noalloc_rejections_before_device_work(L):
+    """hf_hvp_noalloc validates its arguments and the scratch size on the
+    host: a NULL context, a batch outside [1, max_batch], a misaligned
+    pointer, and a batch whose product layout exceeds the static scratch."""
+    fake = ctypes.c_void_p(1 << 20)
+    assert L.hf_hvp_noalloc(None, fake, fake, fake, 4, fake, 0, fake, None) == H.HF_EINVAL
+    rc, h = create(L, [440, 2048, 2048, 2048, 2048, 1973], max_batch=16384)
+    assert rc == H.HF_OK
+    assert L.hf_hvp_noalloc(h, fake, fake, fake, 0, fake, 0, fake, None) == H.HF_EINVAL
+    assert L.hf_hvp_noalloc(h, fake, fake, fake, 16385, fake, 0, fake, None) == H.HF_EINVAL
+    assert L.hf_hvp_noalloc(h, ctypes.c_void_p((1 << 20) + 4), fake, fake, 4, fake, 0,
+                            fake, None) == H.HF_EINVAL
+    assert L.hf_hvp_noalloc(h, fake, fake, fake, 4, fake, 0, fake,
+                            ctypes.c_void_p((1 << 20) + 2)) == H.HF_EINVAL
+    assert L.hf_hvp_noalloc(h, fake, fake, fake, 16384, fake, 0, fake, None) == \
+        H.HF_EWORKSPACE
+    assert b"scratch" in L.hf_last_error(h)
+    assert L.hf_destroy(h) == H.HF_OK
