@@ -28,6 +28,7 @@ import argparse
 import json
 import math
 import os
+import subprocess
 import sys
 import time
 
@@ -88,15 +89,32 @@ def counter_traffic(kernel):
     return vals.get(kernel)
 
 
+def cpu_model():
+    """The host CPU's model name (lscpu), or None."""
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    return None
+
+
 def cpu_baseline(w, inp, rows, min_s=12.0, max_pairs=3):
     """The fp64 oracle timed on this host's cores on a bounded sample: pairs
     of one H v and one G v on the first `rows` rows, repeated until at least
     min_s seconds have passed (at most max_pairs pairs), scaled to the full
     batch."""
     from oracle import hf_oracle as O
+    blas = []
     try:
         from threadpoolctl import threadpool_info
-        cores = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+        info = threadpool_info()
+        cores = max([int(i.get("num_threads", 1)) for i in info] or [1])
+        blas = [{k: i.get(k) for k in ("internal_api", "version", "num_threads",
+                                       "threading_layer", "architecture")}
+                for i in info]
     except Exception:
         cores = len(os.sched_getaffinity(0))
     rows = w.curv_batch if rows <= 0 else min(rows, w.curv_batch)
@@ -117,7 +135,8 @@ def cpu_baseline(w, inp, rows, min_s=12.0, max_pairs=3):
             "the first %d of %d rows, time scaled by %.0fx to the full batch"
             % (rows, w.curv_batch, scale))
     return {"value": 1.0 / per_product, "unit": "curvature-vector products/s",
-            "cores": cores, "kind": "oracle",
+            "cores": cores, "kind": "oracle", "cpu_model": cpu_model(),
+            "host_cpus": len(os.sched_getaffinity(0)), "blas": blas,
             "sample": "fp64 NumPy oracle, %d x (one Hv and one Gv) on %s (%.1f s measured)"
                       % (pairs, what, elapsed)}
 
