@@ -152,7 +152,9 @@ typedef struct hf_cg_info {
   double rr0;         /* ||g||^2                                            */
   double rr_final;    /* ||r||^2 at exit                                    */
   int32_t status;     /* HF_OK, HF_ENUMERIC or HF_ELABEL                    */
-  int32_t reserved;
+  int32_t replayed;   /* 1 if the iterations were replayed from one captured
+                         graph of an iteration (no kernel timing, kept
+                         iterates or trace on the context), else 0          */
 } hf_cg_info;
 
 /*

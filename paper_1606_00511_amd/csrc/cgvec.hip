@@ -176,7 +176,12 @@ extern "C" __global__ __launch_bounds__(256) void hf_pcg_init_fin(
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_dot(
     const float* __restrict__ p, const float* __restrict__ q, long long n,
-    double* __restrict__ part, const CgState* __restrict__ st) {
+    double* __restrict__ part, CgState* __restrict__ st, int j) {
+  // an iteration replayed from a graph: this is its first vector kernel, and
+  // the kernels after it read the index it publishes (no block of this
+  // kernel reads jc); -1 once the solve has stopped, so that no later
+  // kernel takes a replayed iteration for the one that stopped
+  if (j < 0 && blockIdx.x == 0 && threadIdx.x == 0) st->jc = st->done ? -1 : st->jn;
   if (st->done) return;
   __shared__ double sh[4];
   const long long n4 = n >> 2;
@@ -216,6 +221,7 @@ __device__ __forceinline__ void cg_update_body(
     CgState* __restrict__ st, const float* __restrict__ minv,
     double* __restrict__ zpart) {
   if (st->done) return;
+  if (j < 0) j = st->jc;
   __shared__ double sh[4];
   const int nb = gridDim.x;
   const double pq = total(dpart, nb, sh);
@@ -301,6 +307,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_pcg_update(
 extern "C" __global__ __launch_bounds__(256) void hf_cg_neg_dot(
     const float* __restrict__ g, const float* __restrict__ p, long long n,
     int j, double* __restrict__ part, const CgState* __restrict__ st) {
+  if (j < 0) j = st->jc;
   if (!st->neg || st->neg_iter != j) return;
   __shared__ double sh[4];
   const long long n4 = n >> 2;
@@ -320,6 +327,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_neg_write(
     const float* __restrict__ g, const float* __restrict__ p,
     float* __restrict__ x, float* __restrict__ nd, long long n, int j,
     const double* __restrict__ part, CgState* __restrict__ st) {
+  if (j < 0) j = st->jc;
   if (!st->neg || st->neg_iter != j) return;
   __shared__ double sh[4];
   const double gp = total(part, gridDim.x, sh);
@@ -344,8 +352,15 @@ template <bool PC>
 __device__ __forceinline__ void cg_dir_body(
     const float* __restrict__ r, float* __restrict__ p, long long n, int j,
     const double* __restrict__ rpart, CgState* __restrict__ st,
-    const float* __restrict__ minv, const double* __restrict__ zpart) {
-  if (st->done) return;
+    const float* __restrict__ minv, const double* __restrict__ zpart,
+    int* __restrict__ hflag) {
+  const bool lead = blockIdx.x == 0 && threadIdx.x == 0;
+  if (st->done) {
+    if (hflag && lead) *(volatile int*)hflag = 1;
+    return;
+  }
+  const bool replay = j < 0;
+  if (replay) j = st->jc;
   __shared__ double sh[4];
   const double rr_new = total(rpart, gridDim.x, sh);
   const double rz_new = PC ? total(zpart, gridDim.x, sh) : rr_new;
@@ -362,6 +377,8 @@ __device__ __forceinline__ void cg_dir_body(
     } else if (st->tol2 > 0.0 && rr_new <= st->tol2 * st->rr0) {
       st->done = 1;
     }
+    if (replay) st->jn = j + 1;
+    if (hflag) *(volatile int*)hflag = st->done;
   }
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
@@ -386,14 +403,16 @@ __device__ __forceinline__ void cg_dir_body(
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_dir(
     const float* __restrict__ r, float* __restrict__ p, long long n, int j,
-    const double* __restrict__ rpart, CgState* __restrict__ st) {
-  cg_dir_body<false>(r, p, n, j, rpart, st, nullptr, nullptr);
+    const double* __restrict__ rpart, CgState* __restrict__ st,
+    int* __restrict__ hflag) {
+  cg_dir_body<false>(r, p, n, j, rpart, st, nullptr, nullptr, hflag);
 }
 extern "C" __global__ __launch_bounds__(256) void hf_pcg_dir(
     const float* __restrict__ r, float* __restrict__ p, long long n, int j,
     const double* __restrict__ rpart, CgState* __restrict__ st,
-    const float* __restrict__ minv, const double* __restrict__ zpart) {
-  cg_dir_body<true>(r, p, n, j, rpart, st, minv, zpart);
+    const float* __restrict__ minv, const double* __restrict__ zpart,
+    int* __restrict__ hflag) {
+  cg_dir_body<true>(r, p, n, j, rpart, st, minv, zpart, hflag);
 }
 
 // ------------------------------------------------------------- launchers
@@ -434,7 +453,7 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
 
 void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
                   const float* g, float* neg_dir, long long n, int j,
-                  double* part, CgState* st, const float* minv) {
+                  double* part, CgState* st, const float* minv, int* hflag) {
   const int nb = cg_grid(n);
   double* dpart = part;                  // 2 * MAX_GRID: p.q, p.p
   double* rpart = part + 2 * MAX_GRID;   // r.r
@@ -442,7 +461,7 @@ void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
   double* zpart = part + 6 * MAX_GRID;   // r.z (preconditioned)
   prof_begin(L, "hf_cg_dot");
   hipExtLaunchKernelGGL(hf_cg_dot, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, p, q, n,
-                     dpart, st);
+                     dpart, st, j);
   prof_end(L, "hf_cg_dot", 0.0, 2.0 * 4.0 * n);
   if (minv) {
     prof_begin(L, "hf_pcg_update");
@@ -466,12 +485,12 @@ void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
   if (minv) {
     prof_begin(L, "hf_pcg_dir");
     hipExtLaunchKernelGGL(hf_pcg_dir, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, r, p, n, j,
-                       rpart, st, minv, zpart);
+                       rpart, st, minv, zpart, hflag);
     prof_end(L, "hf_pcg_dir", 0.0, 4.0 * 4.0 * n);
   } else {
     prof_begin(L, "hf_cg_dir");
     hipExtLaunchKernelGGL(hf_cg_dir, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, r, p, n, j,
-                       rpart, st);
+                       rpart, st, hflag);
     prof_end(L, "hf_cg_dir", 0.0, 3.0 * 4.0 * n);
   }
 }

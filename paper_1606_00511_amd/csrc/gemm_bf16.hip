@@ -443,7 +443,8 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
   // bias sums: thread t owns row t % RM of the X tile and part t / RM of
   // its chunks
   constexpr int PARTS = NT / RM > 0 ? NT / RM : 1;
-  static_assert(!BIAS || (NT % RM == 0 && TX::CH % PARTS == 0), "bias sum layout");
+  static_assert(!BIAS || (NT % RM == 0 && TX::CH % PARTS == 0 && PARTS <= 2),
+                "bias sum layout");
   const bool do_bias = BIAS && tn == 0 && (e.bias_out || e.bias_part);
   double bsum = 0.0;
 
@@ -553,16 +554,25 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
 #ifndef HF_HD_S
 #define HF_HD_S 3
 #endif
+// minimum waves per SIMD the register allocation must allow (workgroups
+// resident per CU = OCC * 4 / waves per workgroup)
+#ifndef HF_HS_OCC
+#define HF_HS_OCC 1
+#endif
+#ifndef HF_HD_OCC
+#define HF_HD_OCC 1
+#endif
 constexpr int SWM = HF_HS_WM, SWN = HF_HS_WN, SGM = HF_HS_GM, SGN = HF_HS_GN;
 constexpr int SBK = HF_HS_BK, SS = HF_HS_S;
 constexpr int DWM = HF_HD_WM, DWN = HF_HD_WN, DGM = HF_HD_GM, DGN = HF_HD_GN;
 constexpr int DBK = HF_HD_BK, DS = HF_HD_S;
+constexpr int SOCC = HF_HS_OCC, DOCC = HF_HD_OCC;
 constexpr int SNT = 64 * SGM * SGN, DNT = 64 * DGM * DGN;
 
 }  // namespace
 
 #define HF_HGEMM_KERNEL(NAME, MODE, EPI, BIAS, P)                              \
-  extern "C" __global__ __launch_bounds__(P##NT, 1) void NAME(GemmShapeH s,    \
+  extern "C" __global__ __launch_bounds__(P##NT, P##OCC) void NAME(GemmShapeH s, \
                                                               EpiH e) {        \
     hgemm_body<MODE, EPI, BIAS, P##WM, P##WN, P##GM, P##GN, P##BK, P##S>(s, e);  \
   }

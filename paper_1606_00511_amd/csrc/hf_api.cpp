@@ -241,6 +241,24 @@ struct hf_ctx {
   // layout of the no-allocation entry point's device scratch (made on its
   // first call, re-planned for each call's batch)
   hf_ctx* na = nullptr;
+  // one CG iteration (product and vector kernels) captured as a graph and
+  // replayed per iteration; rebuilt when an argument it captured changes
+  struct CgKey {
+    const void *W, *X, *g, *step, *nd, *minv;
+    const char* ws;
+    int64_t b, Bws;
+    int mode;
+    bool operator==(const CgKey& o) const {
+      return W == o.W && X == o.X && g == o.g && step == o.step && nd == o.nd &&
+             minv == o.minv && ws == o.ws && b == o.b && Bws == o.Bws && mode == o.mode;
+    }
+  };
+  hipGraphExec_t cg_exec = nullptr;
+  CgKey cg_key = {};
+  hipStream_t cap_stream = nullptr;
+  int* hflag = nullptr;        // host-pinned stop flag the replayed iteration writes
+  int* hflag_dev = nullptr;    // its device address
+  bool graphs_off = false;     // capture failed once: use the launch-by-launch loop
 
   float* F(size_t off) const { return reinterpret_cast<float*>(ws + off); }
   double* Dp(size_t off) const { return reinterpret_cast<double*>(ws + off); }
@@ -985,6 +1003,59 @@ struct KeepPlan {
   }
 };
 
+// Make c->cg_exec replay one CG iteration with these arguments: the cached
+// product q = A p and the vector kernels, with the iteration index kept on
+// the device and the stop flag written to host-pinned memory.  Returns
+// false (and switches graphs off for the context) if the capture fails;
+// the caller then runs the launch-by-launch loop.
+bool cg_graph(hf_ctx* c, const float* W, const float* Xc, int b, const float* g,
+              float* step, float* neg_dir, int mode, const float* minv) {
+  const hf_ctx::CgKey key = {W, Xc, g, step, neg_dir, minv, c->ws, b, c->Bws, mode};
+  if (c->cg_exec && c->cg_key == key) return true;
+  if (c->cg_exec) {
+    (void)hipGraphExecDestroy(c->cg_exec);
+    c->cg_exec = nullptr;
+  }
+  auto off = [&]() {
+    c->graphs_off = true;
+    (void)hipGetLastError();
+    return false;
+  };
+  if (!c->cap_stream &&
+      hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess)
+    return off();
+  if (!c->hflag) {
+    if (hipHostMalloc((void**)&c->hflag, 64, hipHostMallocMapped | hipHostMallocCoherent) !=
+        hipSuccess) {
+      c->hflag = nullptr;
+      return off();
+    }
+    if (hipHostGetDevicePointer((void**)&c->hflag_dev, c->hflag, 0) != hipSuccess ||
+        !c->hflag_dev)
+      return off();
+  }
+  CgState* st = reinterpret_cast<CgState*>(c->ws + c->oState);
+  const hipStream_t user = c->stream;
+  if (hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeRelaxed) != hipSuccess)
+    return off();
+  c->stream = c->cap_stream;
+  product(c, W, Xc, b, c->F(c->oPv), mode, c->F(c->oQ), &st->done);
+  cg_iteration(c->launch(), step, c->F(c->oR), c->F(c->oPv), c->F(c->oQ), g, neg_dir,
+               c->n, -1, c->Dp(c->oRed), st, minv, c->hflag_dev);
+  c->stream = user;
+  hipGraph_t graph = nullptr;
+  const hipError_t e1 = hipStreamEndCapture(c->cap_stream, &graph);
+  if (e1 != hipSuccess || !graph) return off();
+  const hipError_t e2 = hipGraphInstantiate(&c->cg_exec, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (e2 != hipSuccess) {
+    c->cg_exec = nullptr;
+    return off();
+  }
+  c->cg_key = key;
+  return true;
+}
+
 // CG-Minimize after argument checks; x0 (device, may be null) is the warm
 // start of Alg. 2
 int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
@@ -1019,7 +1090,24 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   }
   cg_init(Lc, g, x0, x0 ? q : nullptr, step, r, p, neg_dir, n, (double)damping,
           (double)rel_tol * (double)rel_tol, part, st, minv);
-  for (int j = 0; j < max_iters; ++j) {
+  // Replay a captured iteration when nothing needs per-iteration host work
+  // (kernel timing, kept iterates, the product trace): one graph launch per
+  // iteration instead of a launch per kernel.
+  const bool replay = max_iters > 0 && !c->prof && !keep && !c->trace_buf &&
+                      !c->graphs_off &&
+                      cg_graph(c, W, Xc, b, g, step, neg_dir, mode, minv);
+  if (replay) {
+    *(volatile int*)c->hflag = 0;
+    for (int j = 0; j < max_iters; ++j) {
+      HIP_TRY(c, hipGraphLaunch(c->cg_exec, c->stream));
+      HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
+      if (j >= 1) {
+        HIP_TRY(c, hipEventSynchronize(c->ev[(j - 1) & 1]));
+        if (*(volatile int*)c->hflag) break;
+      }
+    }
+  }
+  for (int j = 0; !replay && j < max_iters; ++j) {
     if (c->prof) c->prof->tag = j;
     product(c, W, Xc, b, p, mode, q, skip);
     trace_product(c, k0 + j, p, q, skip);
@@ -1057,6 +1145,7 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   info->rr0 = s.rr0;
   info->rr_final = s.rr[s.iters & 1];
   info->status = s.status;
+  info->replayed = replay ? 1 : 0;
   if (errflag) {
     info->status = HF_ELABEL;
     int zero = 0;
@@ -1284,6 +1373,9 @@ int hf_destroy(hf_ctx* c) {
   if (!c) return HF_OK;
   delete c->prof;
   delete c->na;
+  if (c->cg_exec) (void)hipGraphExecDestroy(c->cg_exec);
+  if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
+  if (c->hflag) (void)hipHostFree(c->hflag);
   if (c->pinned) (void)hipHostFree(c->pinned);
   if (c->pinned_bicg) (void)hipHostFree(c->pinned_bicg);
   for (auto& e : c->ev)

@@ -211,6 +211,10 @@ struct CgState {
   double rr0, kappa, alpha, beta, pp, pq, gp;
   double lambda, tol2;
   int done, neg, neg_iter, iters, products, status;
+  // iteration index kept on the device, for an iteration replayed from a
+  // graph (the kernels then take j = -1): the dot kernel copies jn to jc,
+  // the kernels after it read jc, and the direction kernel sets jn = jc + 1
+  int jc, jn;
 };
 
 int cg_grid(long long n);
@@ -225,10 +229,14 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
 // One CG iteration j after the product q = A p has been formed:
 // kappa = p.q + lambda p.p and the stop test; x += alpha p,
 // r += alpha (q + lambda p); at a detection d~ = -sgn(g.p) p and, at j = 0,
-// x = -g; beta = rr'/rr and p = -r + beta p.
+// x = -g; beta = rr'/rr and p = -r + beta p.  j = -1 takes the index from
+// the state (an iteration captured once and replayed); then, if hflag is
+// not null (host-visible memory), the last kernel of the iteration stores
+// st->done there.
 void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
                   const float* g, float* neg_dir, long long n, int j,
-                  double* part, CgState* st, const float* minv = nullptr);
+                  double* part, CgState* st, const float* minv = nullptr,
+                  int* hflag = nullptr);
 // With minv (device, n floats, the diagonal of M^-1) cg_init and
 // cg_iteration run preconditioned CG: z = minv r, p = -z at the start,
 // alpha = r.z / kappa, beta = r'.z' / r.z, p = -z' + beta p.

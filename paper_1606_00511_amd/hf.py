@@ -48,11 +48,11 @@ class hf_cg_info(ctypes.Structure):
         ("pBp", ctypes.c_double), ("pHp", ctypes.c_double),
         ("gTd", ctypes.c_double), ("rr0", ctypes.c_double),
         ("rr_final", ctypes.c_double), ("status", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("replayed", ctypes.c_int32),
     ]
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        return {k: getattr(self, k) for k, _ in self._fields_}
 
 
 class hf_iter_params(ctypes.Structure):

@@ -129,6 +129,9 @@ def test_lockstep_trace_is_passive():
     net.set_trace(4)
     s1, d1, i1 = net.hf_cg(W, X, y, g, 1e-2, 10, "gauss_newton")
     net.set_trace(0)
+    assert i0["replayed"] == 1 and i1["replayed"] == 0   # tracing runs launch by launch
+    i0.pop("replayed")
+    i1.pop("replayed")
     assert i0 == i1
     assert np.array_equal(s0, host(s1)) and np.array_equal(d0, host(d1))
     net.close()
