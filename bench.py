@@ -59,6 +59,12 @@ def parse():
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows of the curvature batch the oracle sample uses "
                          "(0 = all of them)")
+    ap.add_argument("--timed-events", choices=("dominant", "none"), default="dominant",
+                    help="dominant: the timed steps carry kernel events on the "
+                         "dominant GEMM (the roofline is measured over them); "
+                         "none: no events in the timed steps, so that CG replays "
+                         "its captured iteration (the roofline then comes from "
+                         "the fully profiled step)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB with a "
                          "plain device copy (reference point for HBM counters)")
@@ -193,7 +199,10 @@ def run_leg(args, w, inp, prec):
     gemms = {k: st for k, st in breakdown.items() if k.startswith(("hf_gemm", "hf_hgemm"))}
     dom = max(gemms, key=lambda k: gemms[k]["ms"])
     net.prof_reset()
-    net.prof_only(dom)
+    if args.timed_events == "none":
+        net.prof_enable(False)
+    else:
+        net.prof_only(dom)
     comp = {k: 0.0 for k in names}
     products = 0
     torch.cuda.synchronize()
@@ -209,8 +218,11 @@ def run_leg(args, w, inp, prec):
             comp[k] += ev[i].elapsed_time(ev[i + 1])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    stats = net.prof_stats()
-    net.prof_enable(False)
+    if args.timed_events == "none":
+        stats = breakdown
+    else:
+        stats = net.prof_stats()
+        net.prof_enable(False)
 
     # Bi-CG-STAB (Alg. 3) on the same curvature batch, timed on its own after
     # the steps: 10 iterations on the Hessian, two products per iteration
@@ -429,7 +441,10 @@ def main():
             "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "launches": ds["launches"], "avg_launch_ms": ds["ms"] / ds["launches"],
             "flops_per_launch": ds["flops"] / ds["launches"],
+            "measured_over": ("the timed steps" if args.timed_events == "dominant"
+                              else "the fully profiled step"),
         },
+        "cg_replayed": r32["ig"].get("replayed"),
         "loss": r32["loss"],
     }
     for k in ("step_ms", "gemm_all", "cg_vector", "components_ms", "cg_gn",

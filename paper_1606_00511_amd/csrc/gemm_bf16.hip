@@ -154,7 +154,24 @@ __device__ __forceinline__ Q ld_f(const EpiH& e, const float* f, int r0, int c) 
   return a;
 }
 
+// Epilogues with bf16 outputs also have a staged form (see stage_epilogue):
+//   NB        bf16 outputs (row-major h + transposed t pairs) when staged
+//   A0        whether it reads a0
+//   staged(e) whether this launch writes bf16 outputs
+//   stage()   fp32 outputs stored directly, bf16 output values returned in o[]
+//             (a = the a0 values of the 4 rows, when A0)
+//   hout/tout the row-major and transposed destinations of bf16 output i
 struct EFwd {
+  static constexpr int NB = 1;
+  static constexpr bool A0 = false;
+  static __device__ __forceinline__ bool staged(const EpiH& e) { return e.hidden; }
+  static __device__ __forceinline__ bf16_t* hout(const EpiH& e, int) { return e.h0; }
+  static __device__ __forceinline__ bf16_t* tout(const EpiH& e, int) { return e.t0; }
+  static __device__ __forceinline__ void stage(const EpiH& e, int r0, int c, int M,
+                                               const Q& v0, const Q&, const Q&, Q* o) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[0].v[j] = act_f(e.act, v0.v[j] + e.bias[c]);
+  }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q&) {
     Q z;
@@ -171,6 +188,24 @@ struct EFwd {
   }
 };
 struct EFwdRFwd {
+  static constexpr int NB = 2;
+  static constexpr bool A0 = false;
+  static __device__ __forceinline__ bool staged(const EpiH& e) { return e.hidden; }
+  static __device__ __forceinline__ bf16_t* hout(const EpiH& e, int i) { return i ? e.h2 : e.h0; }
+  static __device__ __forceinline__ bf16_t* tout(const EpiH& e, int i) { return i ? e.t2 : e.t0; }
+  static __device__ __forceinline__ void stage(const EpiH& e, int r0, int c, int M,
+                                               const Q& v0, const Q& v1, const Q&, Q* o) {
+    Q rz;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rz.v[j] = v1.v[j] + e.rbias[c];
+    st_f(e, e.f1, r0, c, rz, M);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float a = act_f(e.act, v0.v[j] + e.bias[c]);
+      o[0].v[j] = a;
+      o[1].v[j] = act_d1(e.act, a) * rz.v[j];
+    }
+  }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q& v1) {
     Q z, rz;
@@ -195,6 +230,20 @@ struct EFwdRFwd {
   }
 };
 struct ERFwd {
+  static constexpr int NB = 1;
+  static constexpr bool A0 = true;
+  static __device__ __forceinline__ bool staged(const EpiH& e) { return e.hidden; }
+  static __device__ __forceinline__ bf16_t* hout(const EpiH& e, int) { return e.h2; }
+  static __device__ __forceinline__ bf16_t* tout(const EpiH& e, int) { return e.t2; }
+  static __device__ __forceinline__ void stage(const EpiH& e, int r0, int c, int M,
+                                               const Q& v0, const Q&, const Q& a, Q* o) {
+    Q rz;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rz.v[j] = v0.v[j] + e.rbias[c];
+    st_f(e, e.f1, r0, c, rz, M);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[0].v[j] = act_d1(e.act, a.v[j]) * rz.v[j];
+  }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q&) {
     Q rz;
@@ -211,6 +260,16 @@ struct ERFwd {
   }
 };
 struct EBwd {
+  static constexpr int NB = 1;
+  static constexpr bool A0 = true;
+  static __device__ __forceinline__ bool staged(const EpiH&) { return true; }
+  static __device__ __forceinline__ bf16_t* hout(const EpiH& e, int) { return e.h0; }
+  static __device__ __forceinline__ bf16_t* tout(const EpiH& e, int) { return e.t0; }
+  static __device__ __forceinline__ void stage(const EpiH& e, int, int, int,
+                                               const Q& v0, const Q&, const Q& a, Q* o) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[0].v[j] = v0.v[j] * act_d1(e.act, a.v[j]);
+  }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q&) {
     const Q a = ld_a0(e, r0, c);
@@ -222,6 +281,21 @@ struct EBwd {
 };
 // backward data that also caches E * phi''(A) for the Hessian product
 struct EBwdE2 {
+  static constexpr int NB = 1;
+  static constexpr bool A0 = true;
+  static __device__ __forceinline__ bool staged(const EpiH&) { return true; }
+  static __device__ __forceinline__ bf16_t* hout(const EpiH& e, int) { return e.h0; }
+  static __device__ __forceinline__ bf16_t* tout(const EpiH& e, int) { return e.t0; }
+  static __device__ __forceinline__ void stage(const EpiH& e, int r0, int c, int M,
+                                               const Q& v0, const Q&, const Q& a, Q* o) {
+    Q e2;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      o[0].v[j] = v0.v[j] * act_d1(e.act, a.v[j]);
+      e2.v[j] = v0.v[j] * act_d2(e.act, a.v[j]);
+    }
+    st_f(e, e.f2, r0, c, e2, M);
+  }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q&) {
     const Q a = ld_a0(e, r0, c);
@@ -236,6 +310,21 @@ struct EBwdE2 {
   }
 };
 struct EBwdRBwd {
+  static constexpr int NB = 2;
+  static constexpr bool A0 = true;
+  static __device__ __forceinline__ bool staged(const EpiH&) { return true; }
+  static __device__ __forceinline__ bf16_t* hout(const EpiH& e, int i) { return i ? e.h1 : e.h0; }
+  static __device__ __forceinline__ bf16_t* tout(const EpiH& e, int i) { return i ? e.t1 : e.t0; }
+  static __device__ __forceinline__ void stage(const EpiH& e, int r0, int c, int,
+                                               const Q& v0, const Q& v1, const Q& a, Q* o) {
+    const Q rz = ld_f(e, e.a1, r0, c);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float d1 = act_d1(e.act, a.v[j]);
+      o[0].v[j] = v0.v[j] * d1;
+      o[1].v[j] = v1.v[j] * d1 + v0.v[j] * act_d2(e.act, a.v[j]) * rz.v[j];
+    }
+  }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q& v1) {
     const Q a = ld_a0(e, r0, c);
@@ -252,6 +341,19 @@ struct EBwdRBwd {
   }
 };
 struct ERBwd {
+  static constexpr int NB = 1;
+  static constexpr bool A0 = true;
+  static __device__ __forceinline__ bool staged(const EpiH&) { return true; }
+  static __device__ __forceinline__ bf16_t* hout(const EpiH& e, int) { return e.h1; }
+  static __device__ __forceinline__ bf16_t* tout(const EpiH& e, int) { return e.t1; }
+  static __device__ __forceinline__ void stage(const EpiH& e, int r0, int c, int,
+                                               const Q& v0, const Q&, const Q& a, Q* o) {
+    const Q rz = ld_f(e, e.a1, r0, c);
+    const Q e2 = ld_f(e, e.a2, r0, c);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      o[0].v[j] = v0.v[j] * act_d1(e.act, a.v[j]) + e2.v[j] * rz.v[j];
+  }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q&) {
     const Q a = ld_a0(e, r0, c);
@@ -265,6 +367,16 @@ struct ERBwd {
   }
 };
 struct EGNBwd {
+  static constexpr int NB = 1;
+  static constexpr bool A0 = true;
+  static __device__ __forceinline__ bool staged(const EpiH&) { return true; }
+  static __device__ __forceinline__ bf16_t* hout(const EpiH& e, int) { return e.h1; }
+  static __device__ __forceinline__ bf16_t* tout(const EpiH& e, int) { return e.t1; }
+  static __device__ __forceinline__ void stage(const EpiH& e, int, int, int,
+                                               const Q& v0, const Q&, const Q& a, Q* o) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[0].v[j] = v0.v[j] * act_d1(e.act, a.v[j]);
+  }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q&) {
     const Q a = ld_a0(e, r0, c);
@@ -274,7 +386,8 @@ struct EGNBwd {
     st_ht(e, e.h1, e.t1, r0, c, rd, M);
   }
 };
-struct EStore {
+struct EStore {                      // fp32 only: never staged
+  static constexpr int NB = 0;
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q&) {
 #pragma unroll
@@ -306,6 +419,10 @@ __device__ __forceinline__ void tile_of(int& tn, int& tm, int& tz) {
 }
 
 // ------------------------------------------------------------------- body
+#ifndef HF_H_STAGE
+#define HF_H_STAGE 1
+#endif
+
 // MODE 0: single (nseg K-segments, optional split-K over grid z)
 // MODE 1: dual   acc0 = X0 Y0, acc1 = X1 Y0 + X0 Y1
 // MODE 2: dual0  acc0 = X0 Y0, acc1 = X0 Y1
@@ -371,6 +488,7 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
   const bf16_t* const X1 = s.X[1];
   const bf16_t* const Y0 = s.Y[0];
   const bf16_t* const Y1 = s.Y[1];
+  // the direct loads of K block vb into stage st (X tiles, then Y tiles)
   auto issue = [&](int vb, int st) {
     const int seg = (MODE == 0) ? vb / kbps : 0;
     const int k0 = (vb - seg * kbps) * BK;
@@ -490,6 +608,110 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
   // 8 (r / 4) + 4 h + r % 4, column li of the block; registers 4g .. 4g + 3
   // are 4 consecutive rows.
   const int Mpad = (s.M + 63) & ~63;
+  if constexpr (Epi::NB > 0) {
+    if (HF_H_STAGE && Epi::staged(e)) {
+      // Staged epilogue.  The bf16 outputs pass through LDS (the operand
+      // stages are free by now), so that global memory sees 16-byte
+      // coalesced loads of a0 and 16-byte coalesced stores of both the
+      // row-major and the transposed copy, instead of 2-byte row accesses
+      // and scattered 8-byte column stores.  One [RM][RN] bf16 tile per
+      // output; the 16-byte chunks of tile row r are XOR-swizzled by
+      // (r / 8) % (RN / 8), so that the transposed pass (eight rows of one
+      // column per thread) reads without bank conflicts.  a0 is loaded into
+      // the first tile and each thread overwrites its own elements with the
+      // first output.
+      constexpr int T = RM * RN;
+      constexpr int CPR = RN / 8;
+      static_assert(Epi::NB * T <= S * STAGE, "staged tiles exceed the operand stages");
+      static_assert(RM % 64 == 0 && RN % 128 == 0, "staged tile shape");
+      auto lidx = [&](int r, int c) {
+        return r * RN + (((c >> 3) ^ ((r >> 3) % CPR)) << 3) + (c & 7);
+      };
+      __syncthreads();     // every wave is done with the operand stages
+      if (Epi::A0) {
+        // a0 rows exist up to M rounded up to 256; columns past ldo read 0
+        for (int i = tid; i < T / 8; i += NT) {
+          const int r = i / CPR, k = i % CPR;
+          u32x4 v = {0u, 0u, 0u, 0u};
+          if (n0 + 8 * k + 8 <= e.ldo)
+            v = *(const u32x4*)(e.a0 + (size_t)(m0 + r) * e.ldo + n0 + 8 * k);
+          *(u32x4*)(lds + r * RN + ((k ^ ((r >> 3) % CPR)) << 3)) = v;
+        }
+        __syncthreads();
+      }
+#pragma unroll
+      for (int a = 0; a < WM; ++a)
+#pragma unroll
+        for (int b = 0; b < WN; ++b) {
+          const int lc = wn * 32 * WN + b * 32 + li;
+          const int col = n0 + lc;
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int lr0 = wm * 32 * WM + a * 32 + 4 * h + 8 * g;
+            const int r0 = m0 + lr0;
+            if (col < s.N && r0 < Mpad) {
+              Q v0, v1, av, o[Epi::NB];
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                v0.v[j] = acc0[a][b][4 * g + j];
+                v1.v[j] = MODE == 0 ? 0.0f : acc1[a][b][4 * g + j];
+                av.v[j] = Epi::A0 ? bf2f(lds[lidx(lr0 + j, lc)]) : 0.0f;
+              }
+              Epi::stage(e, r0, col, s.M, v0, v1, av, o);
+#pragma unroll
+              for (int i = 0; i < Epi::NB; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) lds[i * T + lidx(lr0 + j, lc)] = f2bf(o[i].v[j]);
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < Epi::NB; ++i) {
+        bf16_t* hp = Epi::hout(e, i);
+        bf16_t* tp = Epi::tout(e, i);
+        const bf16_t* tile = lds + i * T;
+        // row-major copy: one 16-byte chunk per thread, rows below M,
+        // columns below N (a partial last chunk element by element)
+        for (int it = tid; it < T / 8; it += NT) {
+          const int r = it / CPR, k = it % CPR;
+          const int grow = m0 + r, gcol = n0 + 8 * k;
+          if (grow < s.M && gcol < s.N) {
+            const u32x4 v = *(const u32x4*)(tile + r * RN + ((k ^ ((r >> 3) % CPR)) << 3));
+            bf16_t* dst = hp + (size_t)grow * e.ldo + gcol;
+            if (gcol + 8 <= s.N) {
+              *(u32x4*)dst = v;
+            } else {
+#pragma unroll
+              for (int j = 0; j < 8; ++j)
+                if (gcol + j < s.N) dst[j] = (bf16_t)(v[j >> 1] >> (16 * (j & 1)));
+            }
+          }
+        }
+        // transposed copy: eight consecutive rows of one column per thread,
+        // zeros for rows from M to Mpad; a wave covers 8 columns x 64 rows,
+        // 128 contiguous bytes per column
+        for (int it = tid; it < T / 8; it += NT) {
+          const int cc = it & 7, r8 = (it >> 3) & 7, grp = it >> 6;
+          const int lc = (grp % CPR) * 8 + cc, lr = (grp / CPR) * 64 + r8 * 8;
+          const int gcol = n0 + lc, grow = m0 + lr;
+          if (gcol < s.N && grow < Mpad) {
+            uint32_t w[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const uint32_t lo = grow + 2 * j < s.M ? (uint32_t)tile[lidx(lr + 2 * j, lc)] : 0u;
+              const uint32_t hi =
+                  grow + 2 * j + 1 < s.M ? (uint32_t)tile[lidx(lr + 2 * j + 1, lc)] : 0u;
+              w[j] = lo | (hi << 16);
+            }
+            *(u32x4*)(tp + (size_t)gcol * e.ldt + grow) = u32x4{w[0], w[1], w[2], w[3]};
+          }
+        }
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int a = 0; a < WM; ++a)
 #pragma unroll
