@@ -624,18 +624,28 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
       constexpr int CPR = RN / 8;
       static_assert(Epi::NB * T <= S * STAGE, "staged tiles exceed the operand stages");
       static_assert(RM % 64 == 0 && RN % 128 == 0, "staged tile shape");
+      static_assert(T / 8 % NT == 0, "staged passes: whole 16-byte chunks per thread");
+      constexpr int PASS = T / 8 / NT;               // chunks per thread and pass
       auto lidx = [&](int r, int c) {
         return r * RN + (((c >> 3) ^ ((r >> 3) % CPR)) << 3) + (c & 7);
       };
       __syncthreads();     // every wave is done with the operand stages
       if (Epi::A0) {
         // a0 rows exist up to M rounded up to 256; columns past ldo read 0
-        for (int i = tid; i < T / 8; i += NT) {
+        u32x4 v[PASS];
+#pragma unroll
+        for (int p = 0; p < PASS; ++p) {
+          const int i = tid + p * NT;
           const int r = i / CPR, k = i % CPR;
-          u32x4 v = {0u, 0u, 0u, 0u};
+          v[p] = u32x4{0u, 0u, 0u, 0u};
           if (n0 + 8 * k + 8 <= e.ldo)
-            v = *(const u32x4*)(e.a0 + (size_t)(m0 + r) * e.ldo + n0 + 8 * k);
-          *(u32x4*)(lds + r * RN + ((k ^ ((r >> 3) % CPR)) << 3)) = v;
+            v[p] = *(const u32x4*)(e.a0 + (size_t)(m0 + r) * e.ldo + n0 + 8 * k);
+        }
+#pragma unroll
+        for (int p = 0; p < PASS; ++p) {
+          const int i = tid + p * NT;
+          const int r = i / CPR, k = i % CPR;
+          *(u32x4*)(lds + r * RN + ((k ^ ((r >> 3) % CPR)) << 3)) = v[p];
         }
         __syncthreads();
       }
@@ -674,7 +684,9 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
         const bf16_t* tile = lds + i * T;
         // row-major copy: one 16-byte chunk per thread, rows below M,
         // columns below N (a partial last chunk element by element)
-        for (int it = tid; it < T / 8; it += NT) {
+#pragma unroll
+        for (int p = 0; p < PASS; ++p) {
+          const int it = tid + p * NT;
           const int r = it / CPR, k = it % CPR;
           const int grow = m0 + r, gcol = n0 + 8 * k;
           if (grow < s.M && gcol < s.N) {
@@ -692,7 +704,9 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
         // transposed copy: eight consecutive rows of one column per thread,
         // zeros for rows from M to Mpad; a wave covers 8 columns x 64 rows,
         // 128 contiguous bytes per column
-        for (int it = tid; it < T / 8; it += NT) {
+#pragma unroll
+        for (int p = 0; p < PASS; ++p) {
+          const int it = tid + p * NT;
           const int cc = it & 7, r8 = (it >> 3) & 7, grp = it >> 6;
           const int lc = (grp % CPR) * 8 + cc, lr = (grp / CPR) * 64 + r8 * 8;
           const int gcol = n0 + lc, grow = m0 + lr;
