@@ -800,7 +800,7 @@ void launch(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1,
   launch(L, #NAME, NAME##_v4, NAME##_v1, 128, 0, s, e, fl, by)
 
 // Split-K factor for a batch-row single-product GEMM: enough workgroups for
-// two per compute unit while every split keeps at least 128 of K (8 K
+// two per compute unit while every split keeps at least 64 of K (4 K
 // blocks), within the scratch.  1 = no split (always so at the speech net's
 // full batch).
 int row_splits(const GemmShape& s, const EpiArgs& e) {
@@ -808,7 +808,7 @@ int row_splits(const GemmShape& s, const EpiArgs& e) {
   const long long tiles = (long long)cdiv(s.M, 128) * cdiv(s.N, 128);
   const int ktot = s.K * s.nseg;
   int sp = 1;
-  while (sp < 16 && tiles * sp < 512 && ktot / (2 * sp) >= 128) sp *= 2;
+  while (sp < 16 && tiles * sp < 512 && ktot / (2 * sp) >= 64) sp *= 2;
   while (sp > 1 && (long long)sp * s.M * s.N > e.split_cap) sp /= 2;
   return sp;
 }

@@ -484,12 +484,13 @@ void trace_product(hf_ctx* c, int k, const float* v, const float* out,
 // fp32 (the weight gradients are batch means with heavy cancellation, and the
 // splits are combined in fixed order in the reduce kernel); then, enough
 // workgroups to cover the 256 compute units twice while every split keeps
-// at least 128 rows.
+// at least 64 rows (4 K blocks: enough to fill the load pipeline; a few
+// workgroups with long K chains would leave most of the chip idle).
 int choose_splits(const hf_ctx* c, int M, int N, int Ktot) {
   const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
   int s = 1;
   while (s < c->max_splits && (Ktot + s - 1) / s > 2048) s *= 2;
-  while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 128) s *= 2;
+  while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 64) s *= 2;
   // the scratch is sized so that this never applies; it keeps the partials
   // in bounds regardless
   while (s > 1 && (size_t)s * M * N > c->split_floats) s /= 2;
