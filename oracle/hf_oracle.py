@@ -425,7 +425,7 @@ def precond_inverse(F, lam, xi=0.75):
 
 # ----------------------------------------------------------------- Bi-CG-STAB
 def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
-                      store=None, x0=None, snap_at=()):
+                      store=None, x0=None, snap_at=(), minv=None):
     """Bi-CG-STAB (Alg. 3) for B_k d = -g_k, B_k = A + lam I, from d = 0 or
     from d = x0 (Alg. 2: the Newton system is solved by Bi-CG-STAB from 0 or
     from the warm start eta delta_{k-1}; one extra product forms its
@@ -455,12 +455,26 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
     measure how far storage rounding alone moves the iterates: near a
     breakdown of the recurrences that sensitivity is large, and it sets the
     bound for comparing a float32 implementation with this fp64 one.
+
+    With ``minv`` (the diagonal of M^-1, positive) the solve is Bi-CG-STAB
+    preconditioned on the right (the pre-conditioning of Martens' HF, which
+    the paper lists among his modifications in Sec. 2.1, applied to Alg. 3):
+    the products are taken of p^ = M^-1 p and s^ = M^-1 s, and the iterate
+    advances along them, x += alpha p^ + gamma s^; everything else is
+    unchanged.  This is plain Bi-CG-STAB on B M^-1 y = -g with x = M^-1 y, so
+    r stays the residual -g - B x of the original system: the candidate
+    curvature, the breakdown tests and the relative stop are those of the
+    unpreconditioned solve.  (Reading: the paper gives no preconditioned
+    form of Alg. 3; right preconditioning is the one that keeps r.)
     """
     keep = store if store is not None else (lambda v: v)
     g = np.asarray(g, dtype=np.float64)
 
     def B(v):
         return apply_A(v) + lam * v
+
+    def pre(v):
+        return v if minv is None else keep(minv * v)
 
     nprod0 = 0
     if x0 is None:
@@ -480,18 +494,20 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
     if float(r @ r) == 0.0:
         return res
     for j in range(max_iters):
-        Ap = B(p)
+        ph = pre(p)
+        Ap = B(ph)
         res["products"] += 1
         den = float(Ap @ rs)
         if den == 0.0 or not np.isfinite(den):
             break
         alpha = rho / den
         s = keep(r - alpha * Ap)
-        t = B(s)
+        sh = pre(s)
+        t = B(sh)
         res["products"] += 1
         tt = float(t @ t)
         gamma = float(s @ t) / tt if tt != 0.0 else 0.0
-        x = keep(x + alpha * p + gamma * s)
+        x = keep(x + alpha * ph + gamma * sh)
         r = keep(s - gamma * t)
         rr = float(r @ r)
         res.update(step=x, iters=j + 1, rr_final=rr)
@@ -516,12 +532,13 @@ def bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol=0.0, record=False,
 
 
 def bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
-                     rel_tol=0.0, record=False, store=None, x0=None, snap_at=()):
+                     rel_tol=0.0, record=False, store=None, x0=None, snap_at=(),
+                     minv=None):
     """Bi-CG-STAB with the network's curvature operator on (Xc, yc)."""
     def apply_A(p):
         return curvature(dims, act, theta, Xc, yc, p, mode)
     return bicgstab_minimize(apply_A, g, lam, max_iters, rel_tol, record, store,
-                             x0, snap_at)
+                             x0, snap_at, minv)
 
 
 # --------------------------------------------------------- outer iteration
@@ -613,8 +630,9 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
     6. theta_{k+1} = theta_k + alpha_k delta_k, or theta_k when no candidate
        was accepted.
 
-    With ``precondition`` (CG only) the solve is preconditioned CG with
-    M = (F + lambda)^xi, F = fisher_diag on the batch (X, y) at theta_k.
+    With ``precondition`` the solve is preconditioned CG, or right-
+    preconditioned Bi-CG-STAB, with M = (F + lambda)^xi, F = fisher_diag on
+    the batch (X, y) at theta_k.
 
     With ``backtrack_cap`` > 0 the solver keeps its iterates at
     backtrack_schedule(max_iters, backtrack_cap), and the step candidate of
@@ -642,16 +660,15 @@ def iterate(dims, act, theta, X, y, Xc, yc, solver="cg", curvature_kind=HESSIAN,
     if eta > 0.0 and delta_prev is not None:
         x0 = eta * np.asarray(delta_prev, dtype=np.float64)
     J = backtrack_schedule(max_iters, backtrack_cap) if backtrack_cap > 0 else []
+    minv = None
+    if precondition:
+        minv = precond_inverse(fisher_diag(dims, act, theta, X, y), lam, xi)
     if solver == "cg":
-        minv = None
-        if precondition:
-            minv = precond_inverse(fisher_diag(dims, act, theta, X, y), lam, xi)
         sol = cg_network(dims, act, theta, Xc, yc, g, lam, max_iters, mode,
                          rel_tol, x0=x0, snap_at=J, minv=minv)
     else:
-        assert not precondition, "preconditioning is for CG"
         sol = bicgstab_network(dims, act, theta, Xc, yc, g, lam, max_iters,
-                               mode, rel_tol, x0=x0, snap_at=J)
+                               mode, rel_tol, x0=x0, snap_at=J, minv=minv)
     s = sol["step"]
     evals = 0
     bt_iter, f_step = -1, None

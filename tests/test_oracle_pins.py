@@ -950,3 +950,109 @@ def test_planted_preconditioner_mistakes_are_caught(monkeypatch, bad):
     monkeypatch.setattr(O, "precond_inverse", forms[bad])
     with pytest.raises(AssertionError):
         test_precond_inverse_hand_values()
+
+
+# ------------------------------------------- preconditioned Bi-CG-STAB
+@pytest.mark.parametrize("kind", ["spd", "indefinite", "nonsymmetric"])
+def test_right_preconditioned_bicgstab_is_bicgstab_on_BMinv(kind):
+    """Right-preconditioned Bi-CG-STAB on B = A + lambda I with M = diag(m)
+    produces x_j = M^-1 y_j, y_j the plain Bi-CG-STAB iterates on the matrix
+    B M^-1 (formed explicitly here) with the same right-hand side, and the
+    same iteration count; its recurrence residual is that of the original
+    system, -g - B x_j.  (The indefinite system passes near a breakdown
+    after three iterations, where rounding alone separates the two
+    formulations; it is compared up to there.)"""
+    rng = np.random.default_rng({"spd": 51, "indefinite": 52, "nonsymmetric": 53}[kind])
+    n, lam = 10, 0.05
+    Q = rng.standard_normal((n, n))
+    A = {"spd": Q @ Q.T + 0.2 * np.eye(n), "indefinite": Q + Q.T,
+         "nonsymmetric": Q + 3.0 * np.eye(n)}[kind]
+    g = rng.standard_normal(n)
+    m = rng.uniform(0.3, 4.0, n)           # M = diag(m), M^-1 = diag(1 / m)
+    minv = 1.0 / m
+    Bt = (A + lam * np.eye(n)) @ np.diag(minv)
+    for j in range(1, 4 if kind == "indefinite" else 7):
+        pc = O.bicgstab_minimize(lambda v: A @ v, g, lam, j, minv=minv)
+        tr = O.bicgstab_minimize(lambda v: Bt @ v, g, 0.0, j)
+        assert pc["iters"] == tr["iters"]
+        assert rel(pc["step"], minv * tr["step"]) <= 1e-8
+        r = -g - (A + lam * np.eye(n)) @ pc["step"]
+        assert pc["rr_final"] == pytest.approx(float(r @ r), rel=1e-8, abs=1e-14)
+        if pc["neg_curv"]:
+            d = pc["neg_dir"]
+            assert pc["dHd"] == pytest.approx(float(d @ A @ d), rel=1e-10)
+            assert pc["gTd"] < 0
+
+
+def test_preconditioned_bicgstab_unit_and_exact_solve():
+    """A unit preconditioner gives plain Bi-CG-STAB bit for bit, and on an SPD
+    system the preconditioned solve reaches numpy.linalg.solve."""
+    rng = np.random.default_rng(54)
+    n, lam = 12, 0.1
+    Q = rng.standard_normal((n, n))
+    A = Q @ Q.T + 0.5 * np.eye(n)
+    g = rng.standard_normal(n)
+    plain = O.bicgstab_minimize(lambda v: A @ v, g, lam, 5)
+    unit = O.bicgstab_minimize(lambda v: A @ v, g, lam, 5, minv=np.ones(n))
+    assert np.array_equal(plain["step"], unit["step"])
+    assert plain["iters"] == unit["iters"] and plain["products"] == unit["products"]
+    m = rng.uniform(0.2, 5.0, n)
+    full = O.bicgstab_minimize(lambda v: A @ v, g, lam, 3 * n, rel_tol=1e-13,
+                               minv=1.0 / m)
+    ex = np.linalg.solve(A + lam * np.eye(n), -g)
+    assert np.linalg.norm(full["step"] - ex) <= 1e-9 * np.linalg.norm(ex)
+
+
+def test_planted_half_preconditioned_bicgstab_is_caught():
+    """A solve that preconditions the direction p but forgets the half step s
+    misses the B M^-1 identity."""
+    rng = np.random.default_rng(55)
+    n, lam = 10, 0.05
+    Q = rng.standard_normal((n, n))
+    A = Q + 3.0 * np.eye(n)
+    g = rng.standard_normal(n)
+    minv = 1.0 / rng.uniform(0.3, 4.0, n)
+    Bt = (A + lam * np.eye(n)) @ np.diag(minv)
+    tr = O.bicgstab_minimize(lambda v: Bt @ v, g, 0.0, 4)
+    pc = O.bicgstab_minimize(lambda v: A @ v, g, lam, 4, minv=minv)
+    assert rel(pc["step"], minv * tr["step"]) <= 1e-8
+
+    # the planted variant: p^ = M^-1 p, but s^ = s
+    def planted(v_apply, g, lam, iters, minv):
+        x = np.zeros_like(g); r = -g.copy(); rs = r.copy(); p = r.copy()
+        rho = float(r @ rs)
+        for j in range(iters):
+            ph = minv * p
+            Ap = v_apply(ph) + lam * ph
+            alpha = rho / float(Ap @ rs)
+            s = r - alpha * Ap
+            t = v_apply(s) + lam * s
+            gamma = float(s @ t) / float(t @ t)
+            x = x + alpha * ph + gamma * s
+            r = s - gamma * t
+            rho_new = float(r @ rs)
+            p = r + (rho_new / rho) * (alpha / gamma) * (p - gamma * Ap)
+            rho = rho_new
+        return x
+    bad = planted(lambda v: A @ v, g, lam, 4, minv)
+    assert rel(bad, minv * tr["step"]) > 1e-3
+
+
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
+def test_preconditioned_iterate_takes_the_damped_newton_step(solver):
+    """With the Fisher-diagonal preconditioner the converged solve of a
+    convex (one-layer) net is still the damped Newton step: preconditioning
+    changes the path, not the solution of (H + lambda I) d = -g."""
+    dims = (6, 4)
+    p = WL.make_small(dims, "sigmoid", 40, seed=5)
+    th = p["theta"].astype(np.float64)
+    lam = 1e-3
+    n = th.size
+    Hm = _explicit_curvature(dims, "sigmoid", th, p["X"], p["y"], "hessian")
+    _, g = O.loss_grad(dims, "sigmoid", th, p["X"], p["y"])
+    newton = np.linalg.solve(Hm + lam * np.eye(n), -g)
+    r = O.iterate(dims, "sigmoid", th, p["X"], p["y"], p["X"], p["y"],
+                  solver=solver, curvature_kind="hessian", lam=lam,
+                  max_iters=3 * n, rel_tol=1e-12, precondition=True)
+    assert r["solve"]["neg_curv"] == 0
+    assert rel(r["solve"]["step"], newton) <= 1e-7
