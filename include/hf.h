@@ -199,9 +199,10 @@ int hf_pcg(hf_ctx* ctx, const float* W, const float* Xc, const int32_t* yc,
  * of the squared per-example gradients of the cross-entropy l_b of example
  * b (parameter layout; the diagonal Martens' preconditioner is built from).
  * One forward and one backward pass; the weight blocks are the weight-
- * gradient contraction of squared operands.  HF_FP32 contexts only
- * (HF_EINVAL otherwise).  X, y, B as for hf_loss_grad; out device, n fp32.
- * Asynchronous on the context's stream.
+ * gradient contraction of squared operands (HF_BF16_INPUTS: of the bf16
+ * operands squared and rounded to bf16 again, accumulated in fp32).
+ * X, y, B as for hf_loss_grad; out device, n fp32.  Asynchronous on the
+ * context's stream.
  */
 int hf_fisher_diag(hf_ctx* ctx, const float* W, const float* X,
                    const int32_t* y, int64_t B, float* out);
@@ -233,6 +234,25 @@ int hf_bicgstab(hf_ctx* ctx, const float* W, const float* Xc, const int32_t* yc,
                 hf_cg_info* info);
 
 /*
+ * hf_pbicgstab: hf_bicgstab preconditioned on the right by the diagonal M
+ * (Martens' pre-conditioning, listed in Sec. 2.1, applied to Alg. 3; the
+ * paper gives no preconditioned form, and right preconditioning is the one
+ * that keeps the residual of the original system).  It is Bi-CG-STAB on
+ * B_k M^-1 y = -g with d = M^-1 y: the two products of an iteration are
+ * taken of M^-1 p and M^-1 s, and the iterate advances along them,
+ * x += alpha M^-1 p + gamma M^-1 s.  r stays -g - B_k x, so the candidate
+ * curvature, the breakdown tests and the relative stop on |r| / |g| are
+ * those of hf_bicgstab.
+ *   minv   device, n fp32 (parameter layout), the diagonal of M^-1, > 0
+ * Other arguments, outputs and errors as for hf_bicgstab.
+ */
+int hf_pbicgstab(hf_ctx* ctx, const float* W, const float* Xc,
+                 const int32_t* yc, int64_t Bc, const float* g, float damping,
+                 int32_t max_iters, float rel_tol, int32_t mode,
+                 const float* minv, float* step, float* neg_dir,
+                 hf_cg_info* info);
+
+/*
  * hf_loss: the objective alone, f = (1/B) sum_i [logsumexp(z_i) - z_{i,y_i}]
  * at theta = W on the batch (X, y) of B rows (the forward pass only; the
  * line search of Alg. 2 evaluates it at trial points).
@@ -255,7 +275,7 @@ typedef struct hf_iter_params {
   int32_t adapt_damping;  /* 1: compute rho and the next lambda (LM rule)   */
   int32_t keep_cap;       /* CG-backtracking: iterates kept, 0 = off        */
   float* keep_buf;        /* device, keep_cap * n fp32, caller-owned         */
-  int32_t precondition;   /* 1: preconditioned CG, M = (F + lambda)^xi      */
+  int32_t precondition;   /* 1: preconditioned solve, M = (F + lambda)^xi   */
   float precond_exp;      /* xi >= 0 (Martens: 3/4)                          */
 } hf_iter_params;
 
@@ -305,10 +325,10 @@ typedef struct hf_iter_info {
  * stateless curvature product at the old W; damping_next = 3/2 lambda if
  * rho < 1/4 (also when nothing was accepted or m(p) >= m(0), reported as
  * rho = -inf), 2/3 lambda if rho > 3/4, else lambda.  Without it rho is NaN
- * and damping_next = damping.  Preconditioning (precondition = 1; CG,
- * HF_FP32 contexts and damping > 0 only): the gradient pass of 1. also
- * forms F as hf_fisher_diag does on (X, y), and the solve of 3. is hf_pcg
- * with M^-1 = (F + lambda)^(-xi).
+ * and damping_next = damping.  Preconditioning (precondition = 1;
+ * damping > 0 only): the gradient pass of 1. also forms F as hf_fisher_diag
+ * does on (X, y), and the solve of 3. is hf_pcg or hf_pbicgstab with
+ * M^-1 = (F + lambda)^(-xi).
  *   W      device, n fp32, in/out.  X, y / Xc, yc as for hf_loss_grad /
  *          hf_cg (yc may be NULL only for HF_GAUSS_NEWTON).
  *   delta  device, n fp32, in/out: delta_{k-1} in, delta_k out.
@@ -322,9 +342,10 @@ int hf_iterate(hf_ctx* ctx, float* W, const float* X, const int32_t* y,
 
 /*
  * hf_set_trace: lock-step diagnostic of the solvers' curvature products.
- * Every later solve on ctx (hf_cg, hf_pcg, hf_bicgstab and the solve inside
- * hf_iterate) copies the operand v and the undamped result A v of each of
- * its first `cap` curvature products k into buf: slot 2k (n floats at
+ * Every later solve on ctx (hf_cg, hf_pcg, hf_bicgstab, hf_pbicgstab and
+ * the solve inside hf_iterate) copies the operand v (for hf_pbicgstab
+ * M^-1 p and M^-1 s) and the undamped result A v of each of its first
+ * `cap` curvature products k into buf: slot 2k (n floats at
  * buf + 2k n) gets v, slot 2k + 1 gets A v (A = H or G of the solve, on its
  * cached curvature batch; the product B_k v of Alg. 1 step 3 is A v +
  * lambda v).  Products are numbered in the order the solve evaluates them:

@@ -509,6 +509,12 @@ void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
 //                x^T B x = -(g, x) - (r, x) and x^T A x = x^T B x - lambda (x, x);
 //                beta = (rho_{j+1} / rho_j)(alpha / gamma); p = r + beta (p - gamma Ap)
 //   bicg_negw    at the first negative-curvature candidate: d~ = -sgn(g, x) x
+// Preconditioned (minv = the diagonal of M^-1 given): Bi-CG-STAB
+// preconditioned on the right.  The products are taken of p^ = M^-1 p and
+// s^ = M^-1 s, written beside p and s by the kernels that form them, and
+// x advances along them (x += alpha p^ + gamma s^); r stays the residual of
+// the original system, so every test and the candidate curvature are
+// unchanged.
 // Scalars stay in a BicgState; as for CG, blocks that need a reduced value
 // each sum the per-block partials in block order, and block 0 records it.
 namespace {
@@ -532,7 +538,8 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_init(
     const float* __restrict__ g, const float* __restrict__ x0,
     const float* __restrict__ q, double lambda, float* __restrict__ x,
     float* __restrict__ r, float* __restrict__ rs, float* __restrict__ p,
-    float* __restrict__ nd, long long n, double* __restrict__ part) {
+    float* __restrict__ nd, long long n, double* __restrict__ part,
+    const float* __restrict__ minv, float* __restrict__ ph) {
   __shared__ double sh[4];
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
@@ -545,6 +552,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_init(
       rv = (float)(-(double)gv - ((double)q[i] + lambda * (double)xv));
     }
     x[i] = xv; r[i] = rv; rs[i] = rv; p[i] = rv; nd[i] = 0.f;
+    if (minv) ph[i] = (float)((double)minv[i] * (double)rv);
     srr += (double)rv * rv;
     sgg += (double)gv * gv;
   }
@@ -593,7 +601,8 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_dot1(
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_s(
     const float* __restrict__ r, const float* __restrict__ Ap,
     float* __restrict__ s, long long n, int j, const double* __restrict__ part,
-    BicgState* __restrict__ st) {
+    BicgState* __restrict__ st, const float* __restrict__ minv,
+    float* __restrict__ shat) {
   if (st->done) return;
   __shared__ double sh[4];
   const double den = total(part + PA, gridDim.x, sh);
@@ -616,10 +625,21 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_s(
     const d4 av = up(((const f32x4*)Ap)[i]);
 #pragma unroll
     for (int k = 0; k < 4; ++k) rv.v[k] -= alpha * av.v[k];
-    ((f32x4*)s)[i] = down(rv);
+    const f32x4 s4 = down(rv);
+    ((f32x4*)s)[i] = s4;
+    if (minv) {
+      const f32x4 m4 = ((const f32x4*)minv)[i];
+      f32x4 h4;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) h4[k] = (float)((double)m4[k] * (double)s4[k]);
+      ((f32x4*)shat)[i] = h4;
+    }
   }
-  for (long long e = n4 * 4 + t0; e < n; e += stride)
-    s[e] = (float)((double)r[e] - alpha * (double)Ap[e]);
+  for (long long e = n4 * 4 + t0; e < n; e += stride) {
+    const float sv = (float)((double)r[e] - alpha * (double)Ap[e]);
+    s[e] = sv;
+    if (minv) shat[e] = (float)((double)minv[e] * (double)sv);
+  }
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_dot2(
@@ -648,11 +668,14 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_dot2(
   }
 }
 
+// ph, shat: the vectors the products were taken of (p and s themselves
+// without a preconditioner)
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_update(
     float* __restrict__ x, float* __restrict__ r, const float* __restrict__ rs,
-    const float* __restrict__ p, const float* __restrict__ s,
-    const float* __restrict__ t, const float* __restrict__ g, long long n,
-    int j, double* __restrict__ part, BicgState* __restrict__ st) {
+    const float* __restrict__ ph, const float* __restrict__ s,
+    const float* __restrict__ shat, const float* __restrict__ t,
+    const float* __restrict__ g, long long n, int j, double* __restrict__ part,
+    BicgState* __restrict__ st) {
   if (st->done) return;
   __shared__ double sh[4];
   const double stv = total(part + PB, gridDim.x, sh);
@@ -670,11 +693,11 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_update(
   double e0 = 0.0, e1 = 0.0, e2 = 0.0, e3 = 0.0, e4 = 0.0;
   for (long long i = t0; i < n4; i += stride) {
     const d4 sv = up(((const f32x4*)s)[i]), tv = up(((const f32x4*)t)[i]);
-    const d4 pv = up(((const f32x4*)p)[i]);
+    const d4 pv = up(((const f32x4*)ph)[i]), shv = up(((const f32x4*)shat)[i]);
     d4 xv = up(((f32x4*)x)[i]), rv;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      xv.v[k] += a * pv.v[k] + c * sv.v[k];
+      xv.v[k] += a * pv.v[k] + c * shv.v[k];
       rv.v[k] = sv.v[k] - c * tv.v[k];
     }
     const f32x4 x4 = down(xv), r4 = down(rv);
@@ -687,7 +710,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_update(
     e4 += dot4(x4, x4);
   }
   for (long long e = n4 * 4 + t0; e < n; e += stride) {
-    const float xv = (float)((double)x[e] + a * (double)p[e] + c * (double)s[e]);
+    const float xv = (float)((double)x[e] + a * (double)ph[e] + c * (double)shat[e]);
     const float rv = (float)((double)s[e] - c * (double)t[e]);
     x[e] = xv;
     r[e] = rv;
@@ -714,7 +737,8 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_update(
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_dir(
     float* __restrict__ p, const float* __restrict__ r,
     const float* __restrict__ Ap, long long n, int j,
-    const double* __restrict__ part, BicgState* __restrict__ st) {
+    const double* __restrict__ part, BicgState* __restrict__ st,
+    const float* __restrict__ minv, float* __restrict__ ph) {
   if (st->done) return;
   __shared__ double sh[4];
   const int nb = gridDim.x;
@@ -755,10 +779,21 @@ extern "C" __global__ __launch_bounds__(256) void hf_bicg_dir(
     const d4 rv = up(((const f32x4*)r)[i]), av = up(((const f32x4*)Ap)[i]);
 #pragma unroll
     for (int k = 0; k < 4; ++k) pv.v[k] = rv.v[k] + beta * (pv.v[k] - gamma * av.v[k]);
-    ((f32x4*)p)[i] = down(pv);
+    const f32x4 p4 = down(pv);
+    ((f32x4*)p)[i] = p4;
+    if (minv) {
+      const f32x4 m4 = ((const f32x4*)minv)[i];
+      f32x4 h4;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) h4[k] = (float)((double)m4[k] * (double)p4[k]);
+      ((f32x4*)ph)[i] = h4;
+    }
   }
-  for (long long e = n4 * 4 + t0; e < n; e += stride)
-    p[e] = (float)((double)r[e] + beta * ((double)p[e] - gamma * (double)Ap[e]));
+  for (long long e = n4 * 4 + t0; e < n; e += stride) {
+    const float pv = (float)((double)r[e] + beta * ((double)p[e] - gamma * (double)Ap[e]));
+    p[e] = pv;
+    if (minv) ph[e] = (float)((double)minv[e] * (double)pv);
+  }
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_bicg_negw(
@@ -803,20 +838,20 @@ void axpy(const Launch& L, float* y, const float* x, float a, long long n,
 void bicg_init(const Launch& L, const float* g, const float* x0,
                const float* q, float* x, float* r, float* rs, float* p,
                float* neg_dir, long long n, double lambda, double tol2,
-               double* part, BicgState* st) {
+               double* part, BicgState* st, const float* minv, float* ph) {
   const int nb = cg_grid(n);
   hipLaunchKernelGGL(hf_bicg_reset, dim3(1), dim3(64), 0, L.stream, st);
   prof_begin(L, "hf_bicg_init");
   hipExtLaunchKernelGGL(hf_bicg_init, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, g, x0, q,
-                     lambda, x, r, rs, p, neg_dir, n, part);
-  prof_end(L, "hf_bicg_init", 0.0, (x0 ? 8.0 : 6.0) * 4.0 * n);
+                     lambda, x, r, rs, p, neg_dir, n, part, minv, ph);
+  prof_end(L, "hf_bicg_init", 0.0, ((x0 ? 8.0 : 6.0) + (minv ? 2.0 : 0.0)) * 4.0 * n);
   hipLaunchKernelGGL(hf_bicg_init_fin, dim3(1), dim3(NT), 0, L.stream, part, nb,
                      lambda, tol2, st);
 }
 
 void bicg_half(const Launch& L, const float* r, const float* rs,
                const float* Ap, float* s, long long n, int j, double* part,
-               BicgState* st) {
+               BicgState* st, const float* minv, float* sh) {
   const int nb = cg_grid(n);
   prof_begin(L, "hf_bicg_dot1");
   hipExtLaunchKernelGGL(hf_bicg_dot1, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, Ap, rs, n,
@@ -824,14 +859,18 @@ void bicg_half(const Launch& L, const float* r, const float* rs,
   prof_end(L, "hf_bicg_dot1", 0.0, 2.0 * 4.0 * n);
   prof_begin(L, "hf_bicg_s");
   hipExtLaunchKernelGGL(hf_bicg_s, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, r, Ap, s, n, j,
-                     part, st);
-  prof_end(L, "hf_bicg_s", 0.0, 3.0 * 4.0 * n);
+                     part, st, minv, sh);
+  prof_end(L, "hf_bicg_s", 0.0, (minv ? 5.0 : 3.0) * 4.0 * n);
 }
 
 void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
                const float* Ap, const float* s, const float* t, const float* g,
                float* neg_dir, long long n, int j, double* part,
-               BicgState* st) {
+               BicgState* st, const float* minv, float* ph, const float* sh) {
+  if (!minv) {
+    ph = p;
+    sh = s;
+  }
   const int nb = cg_grid(n);
   prof_begin(L, "hf_bicg_dot2");
   hipExtLaunchKernelGGL(hf_bicg_dot2, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, s, t, n,
@@ -839,12 +878,12 @@ void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
   prof_end(L, "hf_bicg_dot2", 0.0, 2.0 * 4.0 * n);
   prof_begin(L, "hf_bicg_update");
   hipExtLaunchKernelGGL(hf_bicg_update, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, r, rs,
-                     p, s, t, g, n, j, part, st);
-  prof_end(L, "hf_bicg_update", 0.0, 8.0 * 4.0 * n);
+                     ph, s, sh, t, g, n, j, part, st);
+  prof_end(L, "hf_bicg_update", 0.0, (minv ? 9.0 : 8.0) * 4.0 * n);
   prof_begin(L, "hf_bicg_dir");
   hipExtLaunchKernelGGL(hf_bicg_dir, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, p, r, Ap, n,
-                     j, part, st);
-  prof_end(L, "hf_bicg_dir", 0.0, 4.0 * 4.0 * n);
+                     j, part, st, minv, ph);
+  prof_end(L, "hf_bicg_dir", 0.0, (minv ? 6.0 : 4.0) * 4.0 * n);
   prof_begin(L, "hf_bicg_negw");
   hipExtLaunchKernelGGL(hf_bicg_negw, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, neg_dir,
                      n, j, st);

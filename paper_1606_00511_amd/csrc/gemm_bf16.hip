@@ -855,6 +855,30 @@ extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16(
   }
 }
 
+// p[i] = bf16(p[i]^2) for i < n: squares a bf16 operand in place (the
+// Fisher diagonal's squared weight-gradient operands)
+extern "C" __global__ __launch_bounds__(256) void hf_square_bf16(
+    bf16_t* __restrict__ p, long long n) {
+  const long long n8 = n >> 3;
+  const long long stride = (long long)gridDim.x * 256;
+  const long long t0 = (long long)blockIdx.x * 256 + threadIdx.x;
+  for (long long i = t0; i < n8; i += stride) {
+    uint4 v = ((const uint4*)p)[i];
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float lo = bf2f((bf16_t)(w[k] & 0xffffu));
+      const float hi = bf2f((bf16_t)(w[k] >> 16));
+      w[k] = (uint32_t)f2bf(lo * lo) | ((uint32_t)f2bf(hi * hi) << 16);
+    }
+    ((uint4*)p)[i] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  for (long long e = n8 * 8 + t0; e < n; e += stride) {
+    const float f = bf2f(p[e]);
+    p[e] = f2bf(f * f);
+  }
+}
+
 namespace {
 
 typedef void (*HKernel)(GemmShapeH, EpiH);
@@ -919,6 +943,14 @@ void hgemm_gnbwd(const Launch& L, const GemmShapeH& s, const EpiH& e) {
 void hgemm_wgrad(const Launch& L, const GemmShapeH& s, const EpiH& e) {
   launch(L, "hf_hgemm_wgrad", hf_hgemm_wgrad, 0, s, e, mnk(s) * s.nseg,
          io(s, s.nseg, s.nseg, 4.0 * (s.splits > 1 ? s.splits : 1)));
+}
+void square_bf16(const Launch& L, bf16_t* p, long long n) {
+  if (n <= 0) return;
+  const long long nb = std::min<long long>((n + 8 * 256 - 1) / (8 * 256), 2048);
+  prof_begin(L, "hf_square_bf16");
+  hipExtLaunchKernelGGL(hf_square_bf16, dim3((unsigned)nb), dim3(256), 0, L.stream,
+                        prof_a(L), prof_b(L), 0, p, n);
+  prof_end(L, "hf_square_bf16", 0.0, 4.0 * n);
 }
 void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
               bf16_t* out, int ldo, bf16_t* outT, int ldt, int Rpad,

@@ -216,6 +216,8 @@ struct hf_ctx {
   size_t hX = 0, hXT = 0;
   std::vector<size_t> hW, hWT, hV, hVT, hA, hAT, hRA, hRAT, hD, hDT, hRD, hRDT;
   size_t oS = 0, oT = 0, oRs = 0;    // Bi-CG-STAB: s, t = B s, r0*
+  size_t oPh = 0, oSh = 0;           // preconditioned: M^-1 p, M^-1 s
+  size_t oMv = 0;                    // hf_iterate's M^-1
   // outer iteration: gradient, solver step and direction, warm start,
   // trial weights, and device scalars (4 dot products, the fp64 loss)
   size_t oG = 0, oStep = 0, oNd = 0, oX0 = 0, oWt = 0, oScal = 0;
@@ -403,8 +405,9 @@ void plan(hf_ctx* c, int64_t Bplan, bool product_only = false) {
   c->oLoss = take(((B + 3) / 4) * sizeof(double));
   c->oErr = take(sizeof(int));
   if (product_only) {
-    c->oR = c->oPv = c->oQ = c->oS = c->oT = c->oRs = c->oG = c->oStep = c->oNd =
-        c->oX0 = c->oWt = c->oScal = c->oRed = c->oState = 0;
+    c->oR = c->oPv = c->oQ = c->oS = c->oT = c->oRs = c->oPh = c->oSh = c->oMv =
+        c->oG = c->oStep = c->oNd = c->oX0 = c->oWt = c->oScal = c->oRed =
+            c->oState = 0;
     c->need = off;
     return;
   }
@@ -415,6 +418,9 @@ void plan(hf_ctx* c, int64_t Bplan, bool product_only = false) {
   c->oS = take(nv * f4);
   c->oT = take(nv * f4);
   c->oRs = take(nv * f4);
+  c->oPh = take(nv * f4);
+  c->oSh = take(nv * f4);
+  c->oMv = take(nv * f4);
   c->oG = take(nv * f4);
   c->oStep = take(nv * f4);
   c->oNd = take(nv * f4);
@@ -943,11 +949,13 @@ void loss_only(hf_ctx* c, const float* W, const float* X, const int32_t* y,
   loss_finalize(c->launch(), c->Dp(c->oLoss), (B + 3) / 4, B, loss, loss64);
 }
 
-// f and g on B rows (arguments already checked).  With `fisher` (fp32
-// contexts) the same backward pass also forms F = (1/B) sum_b grad l_b^2:
-// delta_l carries the 1/B of the mean, so the squared-operand weight
-// gradient B sum_b delta_l^2 a_{l-1}^2 is F's weight block, and B sum_b
-// delta_l^2 its bias block.
+// f and g on B rows (arguments already checked).  With `fisher` the same
+// backward pass also forms F = (1/B) sum_b grad l_b^2: delta_l carries the
+// 1/B of the mean, so the squared-operand weight gradient
+// B sum_b delta_l^2 a_{l-1}^2 is F's weight block, and B sum_b delta_l^2
+// its bias block.  bf16 contexts square the two transposed operands in
+// place once the gradient has read them (the backward step reads the
+// row-major copies), then run the same weight-gradient GEMM again.
 void loss_grad_any(hf_ctx* c, const float* W, const float* X, const int32_t* y,
                    int b, float* loss, double* loss64, float* grad,
                    float* fisher = nullptr) {
@@ -955,10 +963,17 @@ void loss_grad_any(hf_ctx* c, const float* W, const float* X, const int32_t* y,
     forward_plain_h(c, W, X, b, y, true);
     loss_finalize(c->launch(), c->Dp(c->oLoss), (b + 3) / 4, b, loss, loss64);
     for (int l = c->L; l >= 1; --l) {
-      wgrad_h(c, l, b, c->H(c->hDT[l]), act_ht(c, l - 1), nullptr, nullptr,
-              grad, nullptr);
+      bf16_t* dT = c->H(c->hDT[l]);
+      bf16_t* aT = c->H(l == 1 ? c->hXT : c->hAT[l - 1]);
+      wgrad_h(c, l, b, dT, aT, nullptr, nullptr, grad, nullptr);
+      if (fisher) {
+        square_bf16(c->launch(), dT, (long long)c->d[l] * c->ldB);
+        square_bf16(c->launch(), aT, (long long)c->d[l - 1] * c->ldB);
+        wgrad_h(c, l, b, dT, aT, nullptr, nullptr, fisher, nullptr);
+      }
       if (l > 1) backward_data_h(c, l, b, false);
     }
+    if (fisher) waxpy(c->launch(), fisher, nullptr, (double)b, fisher, c->n);
     return;
   }
   forward_plain(c, W, X, b, y, true);
@@ -1158,11 +1173,13 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
 }
 
 // Bi-CG-STAB after argument checks; x0 (device, may be null) is the warm
-// start of Alg. 2
+// start of Alg. 2; minv (device, may be null) the diagonal of M^-1 of a
+// solve preconditioned on the right
 int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
                int b, const float* g, float damping, int32_t max_iters,
                float rel_tol, int32_t mode, const float* x0, float* step,
-               float* neg_dir, hf_cg_info* info, const KeepPlan* keep = nullptr) {
+               float* neg_dir, hf_cg_info* info, const KeepPlan* keep = nullptr,
+               const float* minv = nullptr) {
   std::memset(info, 0, sizeof *info);
   if (!c->pinned) {
     HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
@@ -1188,6 +1205,9 @@ int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   float* sv = c->F(c->oS);
   float* t = c->F(c->oT);
   float* rs = c->F(c->oRs);
+  // the vectors the products are taken of
+  float* ph = minv ? c->F(c->oPh) : p;
+  float* sh = minv ? c->F(c->oSh) : sv;
 
   build_cache(c, W, Xc, b, yc, hess);
   // a warm start's residual needs one product on the cache
@@ -1197,18 +1217,20 @@ int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
     trace_product(c, 0, x0, Ap, nullptr);
   }
   bicg_init(Lc, g, x0, x0 ? Ap : nullptr, step, r, rs, p, neg_dir, n,
-            (double)damping, (double)rel_tol * (double)rel_tol, part, st);
+            (double)damping, (double)rel_tol * (double)rel_tol, part, st, minv,
+            ph);
   for (int j = 0; j < max_iters; ++j) {
     if (c->prof) c->prof->tag = 2 * j;
-    product(c, W, Xc, b, p, mode, Ap, skip);
-    trace_product(c, k0 + 2 * j, p, Ap, skip);
-    lambda_axpy(c, Ap, p, damping, skip);
-    bicg_half(Lc, r, rs, Ap, sv, n, j, part, st);
+    product(c, W, Xc, b, ph, mode, Ap, skip);
+    trace_product(c, k0 + 2 * j, ph, Ap, skip);
+    lambda_axpy(c, Ap, ph, damping, skip);
+    bicg_half(Lc, r, rs, Ap, sv, n, j, part, st, minv, sh);
     if (c->prof) c->prof->tag = 2 * j + 1;
-    product(c, W, Xc, b, sv, mode, t, skip);
-    trace_product(c, k0 + 2 * j + 1, sv, t, skip);
-    lambda_axpy(c, t, sv, damping, skip);
-    bicg_rest(Lc, step, r, rs, p, Ap, sv, t, g, neg_dir, n, j, part, st);
+    product(c, W, Xc, b, sh, mode, t, skip);
+    trace_product(c, k0 + 2 * j + 1, sh, t, skip);
+    lambda_axpy(c, t, sh, damping, skip);
+    bicg_rest(Lc, step, r, rs, p, Ap, sv, t, g, neg_dir, n, j, part, st, minv,
+              ph, sh);
     if (keep) keep->after(Lc, j + 1, step, n, skip);
     HIP_TRY(c, hipMemcpyAsync(&hostst[j & 1], st, sizeof(BicgState),
                               hipMemcpyDeviceToHost, c->stream));
@@ -1585,8 +1607,6 @@ int hf_fisher_diag(hf_ctx* c, const float* W, const float* X, const int32_t* y,
       (rc = check_ptr(c, out, "out")) || (rc = check_batch(c, B)))
     return rc;
   if (!y) return fail(c, HF_EINVAL, "y is NULL");
-  if (c->bf16())
-    return fail(c, HF_EINVAL, "hf_fisher_diag needs an HF_FP32 context");
   // the gradient of the same pass goes to a solver vector no call keeps
   loss_grad_any(c, W, X, y, (int)B, nullptr, nullptr, c->F(c->oT), out);
   HIP_TRY(c, hipGetLastError());
@@ -1614,6 +1634,30 @@ int hf_bicgstab(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
     return fail(c, HF_EINVAL, "rel_tol must be finite and >= 0");
   return solve_bicg(c, W, Xc, yc, (int)Bc, g, damping, max_iters, rel_tol,
                     mode, nullptr, step, neg_dir, info);
+}
+
+int hf_pbicgstab(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
+                 int64_t Bc, const float* g, float damping, int32_t max_iters,
+                 float rel_tol, int32_t mode, const float* minv, float* step,
+                 float* neg_dir, hf_cg_info* info) {
+  int rc;
+  if ((rc = check_ready(c))) return rc;
+  if ((rc = check_ptr(c, minv, "minv"))) return rc;
+  if ((rc = check_ptr(c, W, "W")) || (rc = check_ptr(c, Xc, "Xc")) ||
+      (rc = check_ptr(c, g, "g")) || (rc = check_ptr(c, step, "step")) ||
+      (rc = check_ptr(c, neg_dir, "neg_dir")) || (rc = check_batch(c, Bc)))
+    return rc;
+  if (!info) return fail(c, HF_EINVAL, "info is NULL");
+  if (mode != HF_HESSIAN && mode != HF_GAUSS_NEWTON)
+    return fail(c, HF_EINVAL, "unknown mode %d", mode);
+  if (mode == HF_HESSIAN && !yc) return fail(c, HF_EINVAL, "yc is NULL");
+  if (!(damping >= 0.0f) || !std::isfinite(damping))
+    return fail(c, HF_EINVAL, "damping must be finite and >= 0");
+  if (max_iters < 0) return fail(c, HF_EINVAL, "max_iters < 0");
+  if (!(rel_tol >= 0.0f) || !std::isfinite(rel_tol))
+    return fail(c, HF_EINVAL, "rel_tol must be finite and >= 0");
+  return solve_bicg(c, W, Xc, yc, (int)Bc, g, damping, max_iters, rel_tol,
+                    mode, nullptr, step, neg_dir, info, nullptr, minv);
 }
 
 int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
@@ -1656,10 +1700,6 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
   if (prm->precondition != 0 && prm->precondition != 1)
     return fail(c, HF_EINVAL, "precondition must be 0 or 1");
   if (prm->precondition) {
-    if (prm->solver != HF_SOLVER_CG)
-      return fail(c, HF_EINVAL, "preconditioning is for HF_SOLVER_CG");
-    if (c->bf16())
-      return fail(c, HF_EINVAL, "preconditioning needs an HF_FP32 context");
     if (!(prm->damping > 0.0f))
       return fail(c, HF_EINVAL, "preconditioning needs damping > 0");
     if (!(prm->precond_exp >= 0.0f) || !std::isfinite(prm->precond_exp))
@@ -1680,12 +1720,12 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
   double hs[5];
 
   // 1. f_k and g_k on the batch (X, y); with preconditioning the same pass
-  // forms the squared per-example gradients F (into a Bi-CG-STAB vector,
-  // free under CG), and M^-1 = (F + lambda)^-xi goes to another
+  // forms the squared per-example gradients F (into the trial weights'
+  // vector, free until the line search), and M^-1 = (F + lambda)^-xi
   float* minv = nullptr;
   if (prm->precondition) {
-    float* F = c->F(c->oS);
-    minv = c->F(c->oT);
+    float* F = wt;
+    minv = c->F(c->oMv);
     loss_grad_any(c, W, X, y, b, nullptr, scal + 4, g, F);
     precond_inverse(Lc, F, (double)prm->damping, (double)prm->precond_exp,
                     minv, n);
@@ -1724,7 +1764,7 @@ int hf_iterate(hf_ctx* c, float* W, const float* X, const int32_t* y,
                       backtrack ? &keep : nullptr, minv)
            : solve_bicg(c, W, Xc, yc, bc, g, prm->damping, prm->max_iters,
                         prm->rel_tol, mode, x0, s, d, &info->solve,
-                        backtrack ? &keep : nullptr);
+                        backtrack ? &keep : nullptr, minv);
   if (rc != HF_OK) return rc;
 
   // objective at W + a v, reduced in fp64 (one full-batch forward)

@@ -173,6 +173,8 @@ void hgemm_wgrad(const Launch& L, const GemmShapeH& s, const EpiH& e);
 void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
               bf16_t* out, int ldo, bf16_t* outT, int ldt, int Rpad,
               const int* skip);
+// p[i] = bf16(p[i]^2), i < n, in place (p 16-byte aligned)
+void square_bf16(const Launch& L, bf16_t* p, long long n);
 
 // --------------------------------------------------------------- row ops
 // Softmax cross-entropy over rows of Z (B x C, leading dimension ld):
@@ -262,17 +264,23 @@ void axpy(const Launch& L, float* y, const float* x, float a, long long n,
 void bicg_init(const Launch& L, const float* g, const float* x0,
                const float* q, float* x, float* r, float* rs, float* p,
                float* neg_dir, long long n, double lambda, double tol2,
-               double* part, BicgState* st);
+               double* part, BicgState* st, const float* minv = nullptr,
+               float* ph = nullptr);
 // first half of iteration j, after Ap = B p: alpha and s = r - alpha Ap
 void bicg_half(const Launch& L, const float* r, const float* rs,
                const float* Ap, float* s, long long n, int j, double* part,
-               BicgState* st);
+               BicgState* st, const float* minv = nullptr, float* sh = nullptr);
 // second half, after t = B s: gamma, x, r, candidate curvature, beta, p,
 // and the oriented candidate at the first negative curvature
 void bicg_rest(const Launch& L, float* x, float* r, const float* rs, float* p,
                const float* Ap, const float* s, const float* t, const float* g,
                float* neg_dir, long long n, int j, double* part,
-               BicgState* st);
+               BicgState* st, const float* minv = nullptr, float* ph = nullptr,
+               const float* sh = nullptr);
+// With minv (device, n floats, the diagonal of M^-1) the three run
+// Bi-CG-STAB preconditioned on the right: init and rest write
+// ph = minv p and half writes sh = minv s, the vectors the curvature
+// products are taken of, and the iterate advances along them.
 
 // ------------------------------------------------------------ outer step
 // out = w + a d, in fp64 (w null: out = a d)

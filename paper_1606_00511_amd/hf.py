@@ -34,7 +34,8 @@ PRECS = {"fp32": HF_FP32, "bf16": HF_BF16_INPUTS}
 EXPORTS = (
     "hf_create", "hf_destroy", "hf_set_stream", "hf_num_params",
     "hf_workspace_bytes", "hf_set_workspace", "hf_loss_grad", "hf_hvp",
-    "hf_cg", "hf_pcg", "hf_fisher_diag", "hf_bicgstab", "hf_loss", "hf_iterate",
+    "hf_cg", "hf_pcg", "hf_fisher_diag", "hf_bicgstab", "hf_pbicgstab", "hf_loss",
+    "hf_iterate",
     "hf_set_trace", "hf_build_id", "hf_hvp_noalloc", "hf_check", "hf_last_error",
     "hf_strerror", "hf_prof_enable", "hf_prof_only",
     "hf_prof_reset", "hf_prof_count", "hf_prof_get",
@@ -131,6 +132,8 @@ def lib():
                                        P, ctypes.POINTER(hf_cg_info)]),
         "hf_pcg": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P, P, P,
                                   ctypes.POINTER(hf_cg_info)]),
+        "hf_pbicgstab": (ctypes.c_int, [P, P, P, P, I64, P, F32, I32, F32, I32, P,
+                                        P, P, ctypes.POINTER(hf_cg_info)]),
         "hf_fisher_diag": (ctypes.c_int, [P, P, P, P, I64, P]),
         "hf_loss": (ctypes.c_int, [P, P, P, P, I64, P]),
         "hf_iterate": (ctypes.c_int, [P, P, P, P, I64, P, P, I64,
@@ -303,6 +306,18 @@ class HFNet:
     def hf_pcg(self, W, Xc, yc, g, minv, damping, max_iters, mode="hessian",
                rel_tol=0.0, step=None, neg_dir=None):
         """CG preconditioned by diag(minv) = M^-1 (hf_pcg)."""
+        return self._psolve("hf_pcg", W, Xc, yc, g, minv, damping, max_iters,
+                            mode, rel_tol, step, neg_dir)
+
+    def hf_pbicgstab(self, W, Xc, yc, g, minv, damping, max_iters,
+                     mode="hessian", rel_tol=0.0, step=None, neg_dir=None):
+        """Bi-CG-STAB preconditioned on the right by diag(minv) = M^-1
+        (hf_pbicgstab)."""
+        return self._psolve("hf_pbicgstab", W, Xc, yc, g, minv, damping,
+                            max_iters, mode, rel_tol, step, neg_dir)
+
+    def _psolve(self, fn, W, Xc, yc, g, minv, damping, max_iters, mode,
+                rel_tol, step, neg_dir):
         import torch
         B = self._rows(Xc)
         if step is None:
@@ -311,7 +326,7 @@ class HFNet:
             neg_dir = torch.empty(self.n, dtype=torch.float32, device=self.device)
         info = hf_cg_info()
         self._stream()
-        self._check(lib().hf_pcg(
+        self._check(getattr(lib(), fn)(
             self._h, _ptr(W, torch.float32, self.n, "W"),
             _ptr(Xc, torch.float32, None, "Xc"),
             _ptr(yc, torch.int32, B, "yc") if yc is not None else None, B,
@@ -355,7 +370,8 @@ class HFNet:
         keep: None, or a CUDA float32 tensor of cap x n for the iterates that
         CG-backtracking keeps (cap = keep.shape[0]).  adapt_damping: report
         rho and the next lambda (info["damping_next"]).  precondition:
-        preconditioned CG with M = (F + lambda)^precond_exp.
+        the solver (PCG, or Bi-CG-STAB preconditioned on the right) with
+        M = (F + lambda)^precond_exp.
         Returns (info dict, the new hybrid state)."""
         import torch
         B = self._rows(X)

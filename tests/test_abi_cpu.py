@@ -101,6 +101,11 @@ def test_calls_without_workspace_or_with_bad_args(L):
                    ctypes.byref(info)) == H.HF_EWORKSPACE
     assert L.hf_bicgstab(h, fake, fake, fake, 4, fake, 0.01, 5, 0.0, 0, fake,
                          fake, ctypes.byref(info)) == H.HF_EWORKSPACE
+    assert L.hf_pcg(h, fake, fake, fake, 4, fake, 0.01, 5, 0.0, 0, fake, fake,
+                    fake, ctypes.byref(info)) == H.HF_EWORKSPACE
+    assert L.hf_pbicgstab(h, fake, fake, fake, 4, fake, 0.01, 5, 0.0, 0, fake,
+                          fake, fake, ctypes.byref(info)) == H.HF_EWORKSPACE
+    assert L.hf_fisher_diag(h, fake, fake, fake, 4, fake) == H.HF_EWORKSPACE
     assert L.hf_loss(h, fake, fake, fake, 4, fake) == H.HF_EWORKSPACE
     prm = H.hf_iter_params(0, 0, 0.01, 5, 0.0, 0.0, 1e-4, 0.5, 10)
     hs = ctypes.c_int32(0)

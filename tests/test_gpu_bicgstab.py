@@ -30,27 +30,40 @@ def rel(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
 
 
-def run(dims, act, p, g, lam, iters, mode, rows=None, rel_tol=0.0):
+def run(dims, act, p, g, lam, iters, mode, rows=None, rel_tol=0.0, minv=None,
+        prec="fp32", noise=1e-7):
+    """The GPU solve (hf_bicgstab, or hf_pbicgstab with minv) and the
+    oracle's, plus the oracle's sensitivity: its step rerun with fp32
+    storage and products perturbed by `noise` relative noise."""
     import torch
     from paper_1606_00511_amd.hf import HFNet
     X = p["X"] if rows is None else p["X"][:rows]
     y = p["y"] if rows is None else p["y"][:rows]
     d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
-    h = HFNet(dims, act, X.shape[0])
-    step, nd, info = h.hf_bicgstab(d(p["theta"]), d(X), d(y),
-                                   d(g.astype(np.float32)), lam, iters, mode,
-                                   rel_tol=rel_tol)
+    h = HFNet(dims, act, X.shape[0], prec=prec)
+    m64 = None
+    if minv is None:
+        step, nd, info = h.hf_bicgstab(d(p["theta"]), d(X), d(y),
+                                       d(g.astype(np.float32)), lam, iters, mode,
+                                       rel_tol=rel_tol)
+    else:
+        m32 = minv.astype(np.float32)
+        m64 = m32.astype(np.float64)
+        step, nd, info = h.hf_pbicgstab(d(p["theta"]), d(X), d(y),
+                                        d(g.astype(np.float32)), d(m32), lam,
+                                        iters, mode, rel_tol=rel_tol)
     torch.cuda.synchronize()
     g64 = g.astype(np.float32).astype(np.float64)
     oi = O.bicgstab_network(dims, act, p["theta"], X, y, g64, lam, iters, mode,
-                            rel_tol=rel_tol)
+                            rel_tol=rel_tol, minv=m64)
     rng = np.random.default_rng(12345)
     f32 = lambda v: v.astype(np.float32).astype(np.float64)
 
     def noisy(v):
         w = O.curvature(dims, act, p["theta"], X, y, v, mode)
-        return w * (1.0 + 1e-7 * rng.standard_normal(w.size))
-    on = O.bicgstab_minimize(noisy, g64, lam, iters, rel_tol, store=f32)
+        return w * (1.0 + noise * rng.standard_normal(w.size))
+    on = O.bicgstab_minimize(noisy, g64, lam, iters, rel_tol, store=f32,
+                             minv=m64)
     oi["sensitivity"] = rel(on["step"], oi["step"]) if iters else 0.0
     nd = nd.cpu().numpy()
     if info["neg_curv"]:
@@ -58,7 +71,9 @@ def run(dims, act, p, g, lam, iters, mode, rows=None, rel_tol=0.0):
         oi["gpu_dHd"] = float(d64 @ O.curvature(dims, act, p["theta"], X, y,
                                                 d64, "hessian"))
         oi["gpu_gTd"] = float(g64 @ d64)
-    return step.cpu().numpy(), nd, info, oi
+    step = step.cpu().numpy()
+    h.close()
+    return step, nd, info, oi
 
 
 def check(step, nd, gi, oi, tol=1e-3):
@@ -144,3 +159,94 @@ def test_bicgstab_full_size(name, iters):
                            rows=w.curv_batch)
     print(name, gi, "oracle", oi["iters"], oi["neg_iter"], oi["dHd"])
     check(step, nd, gi, oi)
+
+
+# --------------------------------------------- preconditioned (right) form
+def fisher_minv(dims, act, p, lam):
+    return O.precond_inverse(O.fisher_diag(dims, act, p["theta"], p["X"],
+                                           p["y"]), lam)
+
+
+PCASES = [((784, 100, 10), "sigmoid", 1000, 4),
+          ((100, 200, 150, 37), "tanh", 300, 4),
+          ((37, 45, 13), "tanh", 130, 3)]
+
+
+@pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
+@pytest.mark.parametrize("case", PCASES, ids=lambda c: "%s-%s" % (
+    "x".join(map(str, c[0])), c[1]))
+def test_pbicgstab_parity(case, mode):
+    """hf_pbicgstab with the Fisher preconditioner (F + lambda)^(-3/4)
+    against the oracle's right-preconditioned Bi-CG-STAB, with the bar of
+    the unpreconditioned solve."""
+    dims, act, B, iters = case
+    p = WL.make_small(dims, act, B, seed=406, bias_std=0.0)
+    _, g = O.loss_grad(dims, act, p["theta"], p["X"], p["y"])
+    lam = 1e-2
+    minv = fisher_minv(dims, act, p, lam)
+    step, nd, gi, oi = run(dims, act, p, g, lam, iters, mode, minv=minv)
+    print(mode, dims, act, {k: gi[k] for k in ("iters", "products", "neg_curv",
+                                               "neg_iter", "pHp")},
+          "oracle", oi["iters"], oi["products"], oi["neg_iter"], oi["dHd"])
+    check(step, nd, gi, oi)
+
+
+def test_pbicgstab_damped_single_layer_is_exact():
+    """Preconditioned on the right, the damped SPD single-layer system is
+    still solved exactly: the step reaches numpy.linalg.solve."""
+    dims, act = (3, 3), "sigmoid"
+    p = WL.make_small(dims, act, 10, seed=4, x_dist="normal")
+    th = p["theta"].astype(np.float64)
+    n = th.size
+    _, g = O.loss_grad(dims, act, p["theta"], p["X"], p["y"])
+    g32 = g.astype(np.float32)
+    G = np.stack([O.gvp(dims, act, th, p["X"], e) for e in np.eye(n)], axis=1)
+    lam = 0.05
+    x = np.linalg.solve(G + lam * np.eye(n), -g32.astype(np.float64))
+    minv = fisher_minv(dims, act, p, lam)
+    step, nd, gi, oi = run(dims, act, p, g32, lam, 3 * n, "gauss_newton",
+                           rel_tol=1e-6, minv=minv)
+    print("iters", gi["iters"], oi["iters"], "err", rel(step, x),
+          rel(oi["step"], x))
+    assert rel(step, x) <= 1e-4 and rel(oi["step"], x) <= 1e-4
+    assert gi["neg_curv"] == 0
+
+
+def test_pbicgstab_unit_preconditioner_is_bicgstab():
+    """minv = 1 multiplies by one in fp64 and rounds back exactly: the
+    preconditioned solve is bit-identical to hf_bicgstab."""
+    import torch
+    from paper_1606_00511_amd.hf import HFNet
+    dims, act, B = (100, 200, 150, 37), "tanh", 300
+    p = WL.make_small(dims, act, B, seed=407)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+    h = HFNet(dims, act, B)
+    W, X, y = d(p["theta"]), d(p["X"]), d(p["y"])
+    _, g = h.hf_loss_grad(W, X, y)
+    a = h.hf_bicgstab(W, X, y, g, 1e-2, 4, "hessian")
+    b = h.hf_pbicgstab(W, X, y, g, torch.ones_like(g), 1e-2, 4, "hessian")
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    assert a[2] == b[2]
+    h.close()
+
+
+@pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
+def test_pbicgstab_bf16(mode):
+    """bf16 GEMM operands: counts and detection as the oracle's; the step
+    within 2e-2 plus 10 times the oracle's own movement when its products
+    carry 2^-8 relative noise (the bf16 rounding of an operand)."""
+    dims, act, B, iters = (100, 200, 150, 37), "tanh", 300, 3
+    p = WL.make_small(dims, act, B, seed=408, bias_std=0.0)
+    _, g = O.loss_grad(dims, act, p["theta"], p["X"], p["y"])
+    lam = 1e-2
+    minv = fisher_minv(dims, act, p, lam)
+    step, nd, gi, oi = run(dims, act, p, g, lam, iters, mode, minv=minv,
+                           prec="bf16", noise=2.0 ** -8)
+    tol = 2e-2 + 10.0 * oi["sensitivity"]
+    print(mode, "bf16 step rel %.3e, bound %.3e" % (rel(step, oi["step"]), tol),
+          {k: gi[k] for k in ("iters", "products", "neg_curv", "neg_iter")},
+          oi["iters"], oi["neg_iter"])
+    assert gi["iters"] == oi["iters"] and gi["products"] == oi["products"]
+    assert gi["neg_curv"] == oi["neg_curv"] and gi["neg_iter"] == oi["neg_iter"]
+    assert rel(step, oi["step"]) <= tol

@@ -219,6 +219,32 @@ def test_lockstep_bicgstab(name, iters):
     assert np.array_equal(tr[0], -host(g))
 
 
+def test_lockstep_pbicgstab():
+    """Right-preconditioned Bi-CG-STAB: its products are on M^-1 p and
+    M^-1 s, each against the oracle's A at the same operand; the first
+    operand is M^-1 r_0 = minv (.) (-g), rounded once to fp32."""
+    from paper_1606_00511_amd.hf import HFNet
+    dims, act, B, iters = (100, 200, 150, 37), "tanh", 300, 4
+    p = WL.make_small(dims, act, B, seed=4250)
+    lam = 1e-2
+    minv = O.precond_inverse(O.fisher_diag(dims, act, p["theta"], p["X"],
+                                           p["y"]), lam).astype(np.float32)
+    net = HFNet(dims, act, B)
+    W, Xc, yc = dev(p["theta"]), dev(p["X"]), dev(p["y"])
+    _, g = net.hf_loss_grad(W, Xc, yc)
+    for mode in ("hessian", "gauss_newton"):
+        buf = net.set_trace(2 * iters)
+        _, _, info = net.hf_pbicgstab(W, Xc, yc, g, dev(minv), lam, iters, mode)
+        net.set_trace(0)
+        tr = host(buf)
+        compare_trace(tr, info["products"], dims, act,
+                      p["theta"].astype(np.float64), p["X"], p["y"], mode, TOL,
+                      "pbicgstab %s" % mode)
+        first = (minv.astype(np.float64) * -host(g).astype(np.float64))
+        assert np.array_equal(tr[0], first.astype(np.float32))
+    net.close()
+
+
 # -------------------------------------------------------------- warm start
 def test_lockstep_warm_start():
     """hf_iterate from eta delta: product 0 is on x_0 = eta delta (rounded

@@ -1,12 +1,15 @@
 """GPU parity of Martens' diagonal preconditioner (Sec. 2.1 lists it among
 the modifications of HF): the squared per-example gradient F
 (hf_fisher_diag), preconditioned CG (hf_pcg) and the preconditioned outer
-iteration, against the fp64 oracle on the same seeded inputs.
+iteration with either solver, against the fp64 oracle on the same seeded
+inputs; preconditioned Bi-CG-STAB (hf_pbicgstab) has its own tests beside
+the unpreconditioned ones.
 
-Bars: F within rel-L2 1e-4 (a sum of non-negative terms, no cancellation);
-PCG with identical iterations, products, detections and sign of the
-detected curvature, and on a damped single-layer net the exact solve
-within 1e-4; the outer iteration with the bar of the other iteration tests.
+Bars: F within rel-L2 1e-4 (a sum of non-negative terms, no cancellation),
+2e-2 with bf16 GEMM operands; PCG with identical iterations, products,
+detections and sign of the detected curvature, and on a damped
+single-layer net the exact solve within 1e-4; the outer iteration with the
+bar of the other iteration tests.
 At the speech net's full size, where per-example backpropagation in fp64 is
 out of reach, the output layer's blocks of F are checked against their
 forward-only closed form, and every block against F >= g^2.
@@ -119,8 +122,9 @@ def test_pcg_damped_single_layer_reaches_the_solution():
     assert rel(oi["step"], ex) <= 1e-4
 
 
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
 @pytest.mark.parametrize("curv", ["hessian", "gauss_newton"])
-def test_iterate_preconditioned(curv):
+def test_iterate_preconditioned(curv, solver):
     """One preconditioned outer iteration against the oracle: curvature,
     solver counts and detections, chosen direction, acceptance, evaluation
     count, step length, f and the new weights."""
@@ -128,16 +132,18 @@ def test_iterate_preconditioned(curv):
     dims, act, B = (100, 200, 150, 37), "tanh", 300
     p = WL.make_small(dims, act, B, seed=45)
     th = p["theta"].astype(np.float64)
-    o = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver="cg",
-                  curvature_kind=curv, lam=1e-2, max_iters=8, precondition=True)
+    iters = 8 if solver == "cg" else 3
+    o = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver=solver,
+                  curvature_kind=curv, lam=1e-2, max_iters=iters,
+                  precondition=True)
     h = net(dims, act, B)
     W = dev(p["theta"].copy())
     gi, _ = h.hf_iterate(W, dev(p["X"]), dev(p["y"]), dev(p["X"]), dev(p["y"]),
-                         dev(np.zeros(h.n, np.float32)), solver="cg",
-                         curvature=curv, damping=1e-2, max_iters=8,
+                         dev(np.zeros(h.n, np.float32)), solver=solver,
+                         curvature=curv, damping=1e-2, max_iters=iters,
                          precondition=True)
     s, so = gi["solve"], o["solve"]
-    print(curv, s["iters"], so["iters"], gi["direction"], o["direction"],
+    print(curv, solver, s["iters"], so["iters"], gi["direction"], o["direction"],
           gi["alpha"], o["alpha"], gi["f1"], o["f1"])
     assert (s["iters"], s["products"], s["neg_curv"]) == \
         (so["iters"], so["products"], so["neg_curv"])
@@ -154,26 +160,103 @@ def test_iterate_preconditioned(curv):
 
 
 def test_preconditioning_rejections():
-    """Preconditioning takes CG, an fp32 context and damping > 0; the Fisher
-    diagonal takes an fp32 context.  Rejections are HF_EINVAL."""
+    """Preconditioning, with either solver and either precision, takes
+    damping > 0 (M = (F + lambda)^xi needs a positive diagonal) and a finite
+    xi >= 0.  Rejections are HF_EINVAL and leave W untouched."""
     from paper_1606_00511_amd.hf import HFError, HF_EINVAL
     dims, act, B = (20, 16, 5), "sigmoid", 32
     p = WL.make_small(dims, act, B, seed=46)
     args = (dev(p["X"]), dev(p["y"]), dev(p["X"]), dev(p["y"]))
-    h = net(dims, act, B)
-    for kw in (dict(solver="bicgstab"), dict(damping=0.0)):
-        with pytest.raises(HFError) as ei:
-            h.hf_iterate(dev(p["theta"].copy()), *args,
-                         dev(np.zeros(h.n, np.float32)), precondition=True, **kw)
-        assert ei.value.code == HF_EINVAL
-    hb = net(dims, act, B, "bf16")
-    with pytest.raises(HFError) as ei:
-        hb.hf_fisher_diag(dev(p["theta"]), dev(p["X"]), dev(p["y"]))
-    assert ei.value.code == HF_EINVAL
-    with pytest.raises(HFError) as ei:
-        hb.hf_iterate(dev(p["theta"].copy()), *args,
-                      dev(np.zeros(hb.n, np.float32)), precondition=True)
-    assert ei.value.code == HF_EINVAL
+    for prec in ("fp32", "bf16"):
+        h = net(dims, act, B, prec)
+        for solver in ("cg", "bicgstab"):
+            for kw in (dict(damping=0.0), dict(precond_exp=-0.5),
+                       dict(precond_exp=float("nan"))):
+                W = dev(p["theta"].copy())
+                with pytest.raises(HFError) as ei:
+                    h.hf_iterate(W, *args, dev(np.zeros(h.n, np.float32)),
+                                 solver=solver, precondition=True, **kw)
+                assert ei.value.code == HF_EINVAL
+                assert np.array_equal(host(W), p["theta"])
+        h.close()
+
+
+BF16_CASES = [((100, 200, 150, 37), "tanh", 300),
+              ((37, 45, 13), "sigmoid", 130),
+              ((40, 96, 1973), "sigmoid", 200)]
+
+
+@pytest.mark.parametrize("case", BF16_CASES, ids=[
+    "x".join(map(str, c[0])) + "-" + c[1] for c in BF16_CASES])
+def test_fisher_diag_bf16(case):
+    """bf16 GEMM operands: each squared operand is rounded to bf16 again
+    before the fp32-accumulated contraction, so F carries a few 2^-8
+    relative errors per term; against the oracle at 2e-2, and F >= 0."""
+    dims, act, B = case
+    p = WL.make_small(dims, act, B, seed=51 + B)
+    h = net(dims, act, B, "bf16")
+    F = host(h.hf_fisher_diag(dev(p["theta"]), dev(p["X"]), dev(p["y"])))
+    h.hf_check()
+    ref = O.fisher_diag(dims, act, p["theta"], p["X"], p["y"])
+    err = rel(F, ref)
+    print("bf16 F rel %.2e" % err)
+    assert err <= 2e-2
+    assert np.all(F >= 0.0)
+    h.close()
+
+
+@pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
+def test_pcg_bf16(mode):
+    """bf16 GEMM operands: PCG's counts and detection as the oracle's; the
+    detected curvature within 5% and the step within 5e-2 (the bf16 CG
+    bar of the full-size tests)."""
+    dims, act, B = (100, 200, 150, 37), "tanh", 300
+    p = WL.make_small(dims, act, B, seed=52)
+    _, g = O.loss_grad(dims, act, p["theta"], p["X"], p["y"])
+    lam = 1e-2
+    minv = O.precond_inverse(O.fisher_diag(dims, act, p["theta"], p["X"], p["y"]),
+                             lam)
+    h = net(dims, act, B, "bf16")
+    step, nd, gi = h.hf_pcg(dev(p["theta"]), dev(p["X"]), dev(p["y"]),
+                            dev(g.astype(np.float32)), dev(minv.astype(np.float32)),
+                            lam, 6, mode)
+    step = host(step)
+    oi = O.cg_network(dims, act, p["theta"], p["X"], p["y"],
+                      g.astype(np.float32).astype(np.float64), lam, 6, mode,
+                      minv=minv.astype(np.float32).astype(np.float64))
+    print(mode, {k: gi[k] for k in ("iters", "products", "neg_curv", "neg_iter",
+                                    "pBp")}, oi["iters"], oi["neg_iter"],
+          oi["pBp"], "step rel %.2e" % rel(step, oi["step"]))
+    assert (gi["iters"], gi["products"], gi["neg_curv"], gi["neg_iter"]) == \
+        (oi["iters"], oi["products"], oi["neg_curv"], oi["neg_iter"])
+    if oi["neg_curv"]:
+        assert np.sign(gi["pBp"]) == np.sign(oi["pBp"])
+        assert abs(gi["pBp"] - oi["pBp"]) <= 0.05 * abs(oi["pBp"])
+    assert rel(step, oi["step"]) <= 5e-2
+    h.close()
+
+
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
+def test_iterate_preconditioned_bf16_descends(solver):
+    """bf16 GEMM operands with preconditioning: the accepted step descends
+    on the exact (fp64) objective, and the reported f0 and f1 agree with it
+    at 2e-2."""
+    dims, act, B = (100, 200, 150, 37), "sigmoid", 300
+    p = WL.make_small(dims, act, B, seed=53)
+    h = net(dims, act, B, "bf16")
+    W = dev(p["theta"].copy())
+    f0 = O.loss(dims, act, p["theta"], p["X"], p["y"])
+    gi, _ = h.hf_iterate(W, dev(p["X"]), dev(p["y"]), dev(p["X"]), dev(p["y"]),
+                         dev(np.zeros_like(p["theta"])), solver=solver,
+                         curvature="gauss_newton", damping=1e-2,
+                         max_iters=6 if solver == "cg" else 3, precondition=True)
+    f1 = O.loss(dims, act, host(W).astype(np.float64), p["X"], p["y"])
+    print(solver, gi["accepted"], gi["direction"], gi["alpha"], f0, f1)
+    assert gi["accepted"] == 1
+    assert abs(gi["f0"] - f0) <= 2e-2 * f0
+    assert f1 < f0
+    assert abs(gi["f1"] - f1) <= 2e-2 * f0
+    h.close()
 
 
 def test_fisher_diag_full_size_speech_net():
