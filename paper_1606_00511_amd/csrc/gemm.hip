@@ -342,6 +342,8 @@ struct EStore {
 // tiles of K-segment 0 over k, giving sum_k X(m, k) for their rows.
 // M16: 4 x 4 blocks of 16 x 16 x 4 MFMAs per wave instead of 2 x 2 blocks
 // of 32 x 32 x 2.
+// TS: output tile rows and columns, 128 or 64 (64: single-product M16
+// kernels only; each wave then holds 2 x 2 blocks of 16 x 16).
 // SQ: every operand element is squared on its way into LDS (so the product
 // is sum_k X(m, k)^2 Y(n, k)^2, and the bias sums are sums of squares).
 // The output tile (tn, tm) of this workgroup within its split.  Linear
@@ -370,11 +372,13 @@ __device__ __forceinline__ void tile_of(int& tn, int& tm) {
 }
 
 template <int MODE, bool XK, bool YK, int VEC, class Epi, bool BIAS, bool M16,
-          bool SQ = false>
+          bool SQ = false, int TS = 128>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) {
   if (s.skip && *s.skip) return;
-  constexpr int W = 2;          // 2 x 2 MFMA blocks per wave
-  constexpr int ROWS = 64 * W;
+  static_assert(TS == 128 || (TS == 64 && M16 && MODE == 0), "tile size");
+  constexpr int ROWS = TS;
+  constexpr int W = ROWS / 64;  // 32 x 32 blocks per wave and dimension
+  constexpr int HALF = ROWS / 2;  // rows (and columns) of a wave's quadrant
   using TX = Tile<XK, VEC, ROWS>;
   using TY = Tile<YK, VEC, ROWS>;
   constexpr int T = MODE == 0 ? 2 : (MODE == 1 ? 4 : 3);
@@ -404,7 +408,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
   }
 
   // MFMA blocks per wave and dimension, and accumulator registers per block
-  constexpr int NB = M16 ? 4 : W;
+  constexpr int NB = M16 ? HALF / 16 : W;
   constexpr int AR = M16 ? 4 : 16;
   using Acc = typename std::conditional<M16, f32x4, f32x16>::type;
   const int r16 = lane & 15, g16 = lane >> 4;   // 16 x 16 lane coordinates
@@ -498,7 +502,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     const float* ly0 = lds[buf][NXT];
     const float* ly1 = lds[buf][T - 1];
     if constexpr (M16) {
-      const int rx = wm * 64 + r16, ry = wn * 64 + r16;
+      const int rx = wm * HALF + r16, ry = wn * HALF + r16;
 #pragma unroll
       for (int a = 0; a < NB; ++a) {
         TX::frag16(lx0, rx + 16 * a, g16, f.x0[a]);
@@ -638,12 +642,16 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
     }
   }
   if (BIAS && do_bias) {
-    static_assert(NT / ROWS <= 2, "bias combine handles at most two parts");
-    __shared__ double bpart2[NT];
-    if (NT / ROWS == 2 && tid >= ROWS) bpart2[tid - ROWS] = bsum;
+    // NT / ROWS threads hold partial sums of one row, over consecutive k;
+    // they are added in k order
+    constexpr int PARTS = NT / ROWS;
+    __shared__ double bparts[NT];
+    if (PARTS > 1 && tid >= ROWS) bparts[tid - ROWS] = bsum;
     __syncthreads();
     if (tid < ROWS && m0 + tid < s.M) {
-      const double t = (NT / ROWS == 2) ? bsum + bpart2[tid] : bsum;
+      double t = bsum;
+#pragma unroll
+      for (int q = 1; q < PARTS; ++q) t += bparts[(q - 1) * ROWS + tid];
       if (s.splits > 1) e.bias_part[(size_t)blockIdx.z * s.M + m0 + tid] = t;
       else e.bias_out[m0 + tid] = (float)t;
     }
@@ -658,8 +666,8 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
       for (int b = 0; b < NB; ++b) {
         const Acc v0 = acc0[a][b];
         const Acc v1 = MODE == 0 ? v0 : acc1[a][b];
-        const int rbase = m0 + wm * 64 + a * 16 + 4 * g16;
-        const int col = n0 + wn * 64 + b * 16 + r16;
+        const int rbase = m0 + wm * HALF + a * 16 + 4 * g16;
+        const int col = n0 + wn * HALF + b * 16 + r16;
         if (col < s.N) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -726,6 +734,28 @@ HF_GEMM_KERNEL(hf_gemm_wgrad, 0, false, false, EStore, true, true, 3)
 // split-K partials of the batch-row single-product GEMMs (X K-contiguous,
 // Y row-contiguous): out0[z * split_stride + m * ldo + n]
 HF_GEMM_KERNEL(hf_gemm_part, 0, true, false, EStore, false, true, 4)
+
+// 64 x 64 output tiles for small outputs (gemm_tile): four times the
+// workgroups of the 128 x 128 form, a quarter of the MFMA chain per
+// workgroup and K block, and a quarter of the padding for a narrow output.
+#define HF_GEMM_KERNEL64(NAME, XK, YK, EPI, BIAS, SQ)                            \
+  extern "C" __global__ __launch_bounds__(256, 4) void NAME##_t64_v4(          \
+      GemmShape s, EpiArgs e) {                                                \
+    gemm_body<0, XK, YK, 4, EPI, BIAS, true, SQ, 64>(s, e);                     \
+  }                                                                             \
+  extern "C" __global__ __launch_bounds__(256, 4) void NAME##_t64_v1(          \
+      GemmShape s, EpiArgs e) {                                                \
+    gemm_body<0, XK, YK, 1, EPI, BIAS, true, SQ, 64>(s, e);                     \
+  }
+HF_GEMM_KERNEL64(hf_gemm_fwd, true, false, EFwd, false, false)
+HF_GEMM_KERNEL64(hf_gemm_rfwd, true, false, ERFwd, false, false)
+HF_GEMM_KERNEL64(hf_gemm_bwd, true, false, EBwd, false, false)
+HF_GEMM_KERNEL64(hf_gemm_bwd_e2, true, false, EBwdE2, false, false)
+HF_GEMM_KERNEL64(hf_gemm_rbwd, true, false, ERBwd, false, false)
+HF_GEMM_KERNEL64(hf_gemm_gnbwd, true, false, EGNBwd, false, false)
+HF_GEMM_KERNEL64(hf_gemm_wgrad, false, false, EStore, true, false)
+HF_GEMM_KERNEL64(hf_gemm_part, true, false, EStore, false, false)
+HF_GEMM_KERNEL64(hf_gemm_wgrad_sq, false, false, EStore, true, true)
 
 // weight gradient of squared operands: sum over the rows of delta^2 a^2 (the
 // per-example squared gradients of a weight layer, up to the batch scale),
@@ -796,8 +826,24 @@ void launch(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1,
   prof_end(L, name, flops, bytes);
 }
 
+// The four kernels of a single-product GEMM: 128 and 64 tiles, 16-byte and
+// element loads
+struct Kernels {
+  GemmKernel k4, k1, t4, t1;
+};
+#define HF_KERNELS(NAME) Kernels{NAME##_v4, NAME##_v1, NAME##_t64_v4, NAME##_t64_v1}
+
+void launch_single(const Launch& L, const char* name, const Kernels& k,
+                   const GemmShape& s, const EpiArgs& e, double flops,
+                   double bytes) {
+  if (gemm_tile(s.M, s.N) == 64)
+    launch(L, name, k.t4, k.t1, 64, 0, s, e, flops, bytes);
+  else
+    launch(L, name, k.k4, k.k1, 128, 0, s, e, flops, bytes);
+}
+
 #define HF_LAUNCH_SINGLE(NAME, L, s, e, fl, by) \
-  launch(L, #NAME, NAME##_v4, NAME##_v1, 128, 0, s, e, fl, by)
+  launch_single(L, #NAME, HF_KERNELS(NAME), s, e, fl, by)
 
 // Split-K factor for a batch-row single-product GEMM: enough workgroups for
 // two per compute unit while every split keeps at least 64 of K (4 K
@@ -805,7 +851,8 @@ void launch(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1,
 // full batch).
 int row_splits(const GemmShape& s, const EpiArgs& e) {
   if (!e.split_buf) return 1;
-  const long long tiles = (long long)cdiv(s.M, 128) * cdiv(s.N, 128);
+  const int ts = gemm_tile(s.M, s.N);
+  const long long tiles = (long long)cdiv(s.M, ts) * cdiv(s.N, ts);
   const int ktot = s.K * s.nseg;
   int sp = 1;
   while (sp < 16 && tiles * sp < 512 && ktot / (2 * sp) >= 64) sp *= 2;
@@ -817,11 +864,11 @@ int row_splits(const GemmShape& s, const EpiArgs& e) {
 // the output has too few tiles, split-K partials into the scratch (timed
 // under the kernel's name) and the reduce that applies the epilogue.
 template <class Epi>
-void launch_rows(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1,
+void launch_rows(const Launch& L, const char* name, const Kernels& k,
                  const GemmShape& s, const EpiArgs& e, double flops, double bytes) {
   const int sp = row_splits(s, e);
   if (sp == 1) {
-    launch(L, name, k4, k1, 128, 0, s, e, flops, bytes);
+    launch_single(L, name, k, s, e, flops, bytes);
     return;
   }
   GemmShape ps = s;
@@ -830,22 +877,22 @@ void launch_rows(const Launch& L, const char* name, GemmKernel k4, GemmKernel k1
   pe.out0 = e.split_buf;
   pe.ldo = s.N;
   pe.split_stride = (long long)s.M * s.N;
-  launch(L, name, hf_gemm_part_v4, hf_gemm_part_v1, 128, 0, ps, pe, flops,
-         bytes + 4.0 * sp * s.M * (double)s.N);
+  launch_single(L, name, HF_KERNELS(hf_gemm_part), ps, pe, flops,
+                bytes + 4.0 * sp * s.M * (double)s.N);
   const long long mn = (long long)s.M * s.N;
   const dim3 grid((unsigned)((mn + 255) / 256));
   // sp is a power of two from 2 to 16 (row_splits doubles from 1)
-  void (*k)(EpiArgs, const float*, int, int, const int*) =
+  void (*kr)(EpiArgs, const float*, int, int, const int*) =
       sp == 2 ? splitk_epi<Epi, 2> : sp == 4 ? splitk_epi<Epi, 4>
       : sp == 8 ? splitk_epi<Epi, 8> : splitk_epi<Epi, 16>;
   prof_begin(L, "hf_splitk_epi");
-  hipExtLaunchKernelGGL(k, grid, dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0, e,
+  hipExtLaunchKernelGGL(kr, grid, dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0, e,
                         (const float*)e.split_buf, s.M, s.N, s.skip);
   prof_end(L, "hf_splitk_epi", 0.0, 4.0 * (sp + 1) * (double)mn);
 }
 
 #define HF_LAUNCH_ROWS(NAME, EPI, L, s, e, fl, by) \
-  launch_rows<EPI>(L, #NAME, NAME##_v4, NAME##_v1, s, e, fl, by)
+  launch_rows<EPI>(L, #NAME, HF_KERNELS(NAME), s, e, fl, by)
 
 inline double mnk(const GemmShape& s) { return 2.0 * s.M * s.N * (double)s.K; }
 inline double io(const GemmShape& s, int nx, int ny, int nout) {
@@ -854,6 +901,11 @@ inline double io(const GemmShape& s, int nx, int ny, int nout) {
 }
 
 }  // namespace
+
+int gemm_tile(int M, int N) {
+  const long long t128 = (long long)cdiv(M, 128) * cdiv(N, 128);
+  return (t128 < 128 || M <= 64 || N <= 64) ? 64 : 128;
+}
 
 void gemm_fwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {
   HF_LAUNCH_ROWS(hf_gemm_fwd, EFwd, L, s, e, mnk(s) * s.nseg, io(s, s.nseg, s.nseg, 1));

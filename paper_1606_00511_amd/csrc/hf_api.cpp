@@ -493,7 +493,8 @@ void trace_product(hf_ctx* c, int k, const float* v, const float* out,
 // at least 64 rows (4 K blocks: enough to fill the load pipeline; a few
 // workgroups with long K chains would leave most of the chip idle).
 int choose_splits(const hf_ctx* c, int M, int N, int Ktot) {
-  const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  const int ts = c->bf16() ? 128 : gemm_tile(M, N);
+  const int tiles = ((M + ts - 1) / ts) * ((N + ts - 1) / ts);
   int s = 1;
   while (s < c->max_splits && (Ktot + s - 1) / s > 2048) s *= 2;
   while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 64) s *= 2;

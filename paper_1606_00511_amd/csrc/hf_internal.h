@@ -77,6 +77,12 @@ struct EpiArgs {
   long long split_cap;
 };
 
+// Output tile (128 or 64 rows and columns) of the single-product GEMMs
+// for an M x N output: 64 when 128 x 128 tiles would number fewer than 128
+// (half the compute units) or an output side is at most 64 wide.  The
+// split-K choice of the weight gradients counts tiles of this size.
+int gemm_tile(int M, int N);
+
 // Forward:  out0 = phi(acc + bias) (hidden) or acc + bias (logits);
 // the weights come transposed (Y row-contiguous: Y[k * ldy + n])
 void gemm_fwd(const Launch& L, const GemmShape& s, const EpiArgs& e);
