@@ -11,10 +11,11 @@
 //   dot     per-block partials of p.q and p.p
 //   update  every block sums the dot partials in block order (so all blocks
 //           hold the same kappa), takes the stop decision, and if it goes on
-//           updates x and r and writes per-block partials of r.r
-//   neg_dot / neg_write  only at a detection: g.p, then d~ and the step
+//           updates x and r and writes per-block partials of r.r; at a
+//           detection it writes per-block partials of g.p instead
 //   dir     every block sums the r.r partials in block order, forms beta
-//           and updates p
+//           and updates p; at a detection in this iteration it sums the g.p
+//           partials and writes d~ and the step instead
 // Block 0 of update and dir records the scalars in a CgState in device
 // memory; rr is kept in two slots indexed by the iteration's parity so that
 // no block reads a slot that another block of the same kernel writes.  No
@@ -142,7 +143,7 @@ template <bool PC>
 __device__ __forceinline__ void cg_init_fin_body(
     const double* __restrict__ part_rr, const double* __restrict__ part_gg,
     const double* __restrict__ part_rz, int nb, double lambda, double tol2,
-    CgState* __restrict__ st) {
+    int max_iters, CgState* __restrict__ st) {
   __shared__ double sh[4];
   const double rr = total(part_rr, nb, sh);
   const double gg = total(part_gg, nb, sh);
@@ -155,6 +156,7 @@ __device__ __forceinline__ void cg_init_fin_body(
     st->rr0 = gg;
     st->lambda = lambda;
     st->tol2 = tol2;
+    st->max_iters = max_iters;
     st->neg_iter = -1;
     const bool fin = is_fin(rr) && is_fin(rz);
     st->status = fin ? 0 : -5;
@@ -164,14 +166,16 @@ __device__ __forceinline__ void cg_init_fin_body(
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_init_fin(
     const double* __restrict__ part_rr, const double* __restrict__ part_gg,
-    int nb, double lambda, double tol2, CgState* __restrict__ st) {
-  cg_init_fin_body<false>(part_rr, part_gg, nullptr, nb, lambda, tol2, st);
+    int nb, double lambda, double tol2, int max_iters, CgState* __restrict__ st) {
+  cg_init_fin_body<false>(part_rr, part_gg, nullptr, nb, lambda, tol2,
+                          max_iters, st);
 }
 extern "C" __global__ __launch_bounds__(256) void hf_pcg_init_fin(
     const double* __restrict__ part_rr, const double* __restrict__ part_gg,
     const double* __restrict__ part_rz, int nb, double lambda, double tol2,
-    CgState* __restrict__ st) {
-  cg_init_fin_body<true>(part_rr, part_gg, part_rz, nb, lambda, tol2, st);
+    int max_iters, CgState* __restrict__ st) {
+  cg_init_fin_body<true>(part_rr, part_gg, part_rz, nb, lambda, tol2,
+                         max_iters, st);
 }
 
 extern "C" __global__ __launch_bounds__(256) void hf_cg_dot(
@@ -219,7 +223,8 @@ __device__ __forceinline__ void cg_update_body(
     const float* __restrict__ q, long long n, int j,
     const double* __restrict__ dpart, double* __restrict__ rpart,
     CgState* __restrict__ st, const float* __restrict__ minv,
-    double* __restrict__ zpart) {
+    double* __restrict__ zpart, const float* __restrict__ g,
+    double* __restrict__ gpart) {
   if (st->done) return;
   if (j < 0) j = st->jc;
   __shared__ double sh[4];
@@ -246,11 +251,21 @@ __device__ __forceinline__ void cg_update_body(
       st->alpha = rr / kappa;
     }
   }
-  if (stop) return;
-  const double alpha = rr / kappa;
   const long long n4 = n >> 2;
   const long long stride = (long long)gridDim.x * NT;
   const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  if (stop) {
+    if (!is_fin(kappa)) return;
+    // detection: partials of g.p for the orientation of d~
+    double gp = 0.0;
+    for (long long i = t0; i < n4; i += stride)
+      gp += dot4(((const f32x4*)g)[i], ((const f32x4*)p)[i]);
+    for (long long e = n4 * 4 + t0; e < n; e += stride) gp += (double)g[e] * p[e];
+    gp = block_sum(gp, sh);
+    if (threadIdx.x == 0) gpart[blockIdx.x] = gp;
+    return;
+  }
+  const double alpha = rr / kappa;
   double s = 0.0, sz = 0.0;
   for (long long i = t0; i < n4; i += stride) {
     const d4 pv = up(((const f32x4*)p)[i]);
@@ -292,76 +307,59 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
     float* __restrict__ x, float* __restrict__ r, const float* __restrict__ p,
     const float* __restrict__ q, long long n, int j,
     const double* __restrict__ dpart, double* __restrict__ rpart,
-    CgState* __restrict__ st) {
-  cg_update_body<false>(x, r, p, q, n, j, dpart, rpart, st, nullptr, nullptr);
+    CgState* __restrict__ st, const float* __restrict__ g,
+    double* __restrict__ gpart) {
+  cg_update_body<false>(x, r, p, q, n, j, dpart, rpart, st, nullptr, nullptr,
+                        g, gpart);
 }
 extern "C" __global__ __launch_bounds__(256) void hf_pcg_update(
     float* __restrict__ x, float* __restrict__ r, const float* __restrict__ p,
     const float* __restrict__ q, long long n, int j,
     const double* __restrict__ dpart, double* __restrict__ rpart,
     CgState* __restrict__ st, const float* __restrict__ minv,
-    double* __restrict__ zpart) {
-  cg_update_body<true>(x, r, p, q, n, j, dpart, rpart, st, minv, zpart);
+    double* __restrict__ zpart, const float* __restrict__ g,
+    double* __restrict__ gpart) {
+  cg_update_body<true>(x, r, p, q, n, j, dpart, rpart, st, minv, zpart, g,
+                       gpart);
 }
 
-extern "C" __global__ __launch_bounds__(256) void hf_cg_neg_dot(
-    const float* __restrict__ g, const float* __restrict__ p, long long n,
-    int j, double* __restrict__ part, const CgState* __restrict__ st) {
-  if (j < 0) j = st->jc;
-  if (!st->neg || st->neg_iter != j) return;
-  __shared__ double sh[4];
-  const long long n4 = n >> 2;
-  const long long stride = (long long)gridDim.x * NT;
-  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  double gp = 0.0;
-  for (long long i = t0; i < n4; i += stride)
-    gp += dot4(((const f32x4*)g)[i], ((const f32x4*)p)[i]);
-  for (long long e = n4 * 4 + t0; e < n; e += stride) gp += (double)g[e] * p[e];
-  gp = block_sum(gp, sh);
-  if (threadIdx.x == 0) part[blockIdx.x] = gp;
-}
-
-// d~ = -sgn(g.p) p with sgn(0) = +1; the step is -g when the detection
-// happened at the first iteration, else the current iterate.
-extern "C" __global__ __launch_bounds__(256) void hf_cg_neg_write(
-    const float* __restrict__ g, const float* __restrict__ p,
-    float* __restrict__ x, float* __restrict__ nd, long long n, int j,
-    const double* __restrict__ part, CgState* __restrict__ st) {
-  if (j < 0) j = st->jc;
-  if (!st->neg || st->neg_iter != j) return;
-  __shared__ double sh[4];
-  const double gp = total(part, gridDim.x, sh);
-  if (blockIdx.x == 0 && threadIdx.x == 0) st->gp = gp;
-  const float coef = gp >= 0.0 ? -1.0f : 1.0f;
-  const bool first = j == 0;
-  const long long n4 = n >> 2;
-  const long long stride = (long long)gridDim.x * NT;
-  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
-  for (long long i = t0; i < n4; i += stride) {
-    ((f32x4*)nd)[i] = coef * ((const f32x4*)p)[i];
-    if (first) ((f32x4*)x)[i] = -((const f32x4*)g)[i];
-  }
-  for (long long e = n4 * 4 + t0; e < n; e += stride) {
-    nd[e] = coef * p[e];
-    if (first) x[e] = -g[e];
-  }
-}
-
-// PC: beta = r'.z' / r.z and p = -minv r + beta p
+// PC: beta = r'.z' / r.z and p = -minv r + beta p.
+// At a detection in iteration j: d~ = -sgn(g.p) p with sgn(0) = +1, and the
+// step is -g when the detection happened at the first iteration, else the
+// current iterate.
 template <bool PC>
 __device__ __forceinline__ void cg_dir_body(
     const float* __restrict__ r, float* __restrict__ p, long long n, int j,
     const double* __restrict__ rpart, CgState* __restrict__ st,
     const float* __restrict__ minv, const double* __restrict__ zpart,
-    int* __restrict__ hflag) {
+    int* __restrict__ hflag, const float* __restrict__ g,
+    float* __restrict__ x, float* __restrict__ nd,
+    const double* __restrict__ gpart) {
   const bool lead = blockIdx.x == 0 && threadIdx.x == 0;
-  if (st->done) {
-    if (hflag && lead) *(volatile int*)hflag = 1;
-    return;
-  }
   const bool replay = j < 0;
   if (replay) j = st->jc;
   __shared__ double sh[4];
+  const long long n4 = n >> 2;
+  const long long stride = (long long)gridDim.x * NT;
+  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
+  if (st->done) {
+    if (st->neg && st->neg_iter == j) {
+      const double gp = total(gpart, gridDim.x, sh);
+      if (lead) st->gp = gp;
+      const float coef = gp >= 0.0 ? -1.0f : 1.0f;
+      const bool first = j == 0;
+      for (long long i = t0; i < n4; i += stride) {
+        ((f32x4*)nd)[i] = coef * ((const f32x4*)p)[i];
+        if (first) ((f32x4*)x)[i] = -((const f32x4*)g)[i];
+      }
+      for (long long e = n4 * 4 + t0; e < n; e += stride) {
+        nd[e] = coef * p[e];
+        if (first) x[e] = -g[e];
+      }
+    }
+    if (hflag && lead) *(volatile int*)hflag = 1;
+    return;
+  }
   const double rr_new = total(rpart, gridDim.x, sh);
   const double rz_new = PC ? total(zpart, gridDim.x, sh) : rr_new;
   const double rz = PC ? st->rz[j & 1] : st->rr[j & 1];
@@ -376,13 +374,12 @@ __device__ __forceinline__ void cg_dir_body(
       st->done = 1;
     } else if (st->tol2 > 0.0 && rr_new <= st->tol2 * st->rr0) {
       st->done = 1;
+    } else if (st->max_iters > 0 && j + 1 >= st->max_iters) {
+      st->done = 1;
     }
     if (replay) st->jn = j + 1;
     if (hflag) *(volatile int*)hflag = st->done;
   }
-  const long long n4 = n >> 2;
-  const long long stride = (long long)gridDim.x * NT;
-  const long long t0 = (long long)blockIdx.x * NT + threadIdx.x;
   for (long long i = t0; i < n4; i += stride) {
     d4 pv = up(((const f32x4*)p)[i]);
     d4 zv = up(((const f32x4*)r)[i]);
@@ -404,15 +401,20 @@ __device__ __forceinline__ void cg_dir_body(
 extern "C" __global__ __launch_bounds__(256) void hf_cg_dir(
     const float* __restrict__ r, float* __restrict__ p, long long n, int j,
     const double* __restrict__ rpart, CgState* __restrict__ st,
-    int* __restrict__ hflag) {
-  cg_dir_body<false>(r, p, n, j, rpart, st, nullptr, nullptr, hflag);
+    int* __restrict__ hflag, const float* __restrict__ g,
+    float* __restrict__ x, float* __restrict__ nd,
+    const double* __restrict__ gpart) {
+  cg_dir_body<false>(r, p, n, j, rpart, st, nullptr, nullptr, hflag, g, x, nd,
+                     gpart);
 }
 extern "C" __global__ __launch_bounds__(256) void hf_pcg_dir(
     const float* __restrict__ r, float* __restrict__ p, long long n, int j,
     const double* __restrict__ rpart, CgState* __restrict__ st,
     const float* __restrict__ minv, const double* __restrict__ zpart,
-    int* __restrict__ hflag) {
-  cg_dir_body<true>(r, p, n, j, rpart, st, minv, zpart, hflag);
+    int* __restrict__ hflag, const float* __restrict__ g,
+    float* __restrict__ x, float* __restrict__ nd,
+    const double* __restrict__ gpart) {
+  cg_dir_body<true>(r, p, n, j, rpart, st, minv, zpart, hflag, g, x, nd, gpart);
 }
 
 // ------------------------------------------------------------- launchers
@@ -428,7 +430,7 @@ int cg_part_doubles() { return 10 * MAX_GRID; }
 void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
              float* x, float* r, float* p, float* neg_dir, long long n,
              double lambda, double tol2, double* part, CgState* st,
-             const float* minv) {
+             const float* minv, int max_iters) {
   const int nb = cg_grid(n);
   hipLaunchKernelGGL(hf_cg_reset, dim3(1), dim3(64), 0, L.stream, st);
   if (minv) {
@@ -439,7 +441,7 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
     prof_end(L, "hf_pcg_init", 0.0, (x0 ? 8.0 : 6.0) * 4.0 * n);
     hipLaunchKernelGGL(hf_pcg_init_fin, dim3(1), dim3(NT), 0, L.stream,
                        part + 4 * MAX_GRID, part + 5 * MAX_GRID,
-                       part + 6 * MAX_GRID, nb, lambda, tol2, st);
+                       part + 6 * MAX_GRID, nb, lambda, tol2, max_iters, st);
     return;
   }
   prof_begin(L, "hf_cg_init");
@@ -448,7 +450,8 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
                      part + 5 * MAX_GRID);
   prof_end(L, "hf_cg_init", 0.0, (x0 ? 7.0 : 5.0) * 4.0 * n);
   hipLaunchKernelGGL(hf_cg_init_fin, dim3(1), dim3(NT), 0, L.stream,
-                     part + 4 * MAX_GRID, part + 5 * MAX_GRID, nb, lambda, tol2, st);
+                     part + 4 * MAX_GRID, part + 5 * MAX_GRID, nb, lambda, tol2,
+                     max_iters, st);
 }
 
 void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
@@ -466,31 +469,23 @@ void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
   if (minv) {
     prof_begin(L, "hf_pcg_update");
     hipExtLaunchKernelGGL(hf_pcg_update, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, r, p,
-                       q, n, j, dpart, rpart, st, minv, zpart);
+                       q, n, j, dpart, rpart, st, minv, zpart, g, gpart);
     prof_end(L, "hf_pcg_update", 0.0, 7.0 * 4.0 * n);
   } else {
     prof_begin(L, "hf_cg_update");
     hipExtLaunchKernelGGL(hf_cg_update, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, r, p,
-                       q, n, j, dpart, rpart, st);
+                       q, n, j, dpart, rpart, st, g, gpart);
     prof_end(L, "hf_cg_update", 0.0, 6.0 * 4.0 * n);
   }
-  prof_begin(L, "hf_cg_neg_dot");
-  hipExtLaunchKernelGGL(hf_cg_neg_dot, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, g, p, n, j,
-                     gpart, st);
-  prof_end(L, "hf_cg_neg_dot", 0.0, 2.0 * 4.0 * n);
-  prof_begin(L, "hf_cg_neg_write");
-  hipExtLaunchKernelGGL(hf_cg_neg_write, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, g, p, x,
-                     neg_dir, n, j, gpart, st);
-  prof_end(L, "hf_cg_neg_write", 0.0, 2.0 * 4.0 * n);
   if (minv) {
     prof_begin(L, "hf_pcg_dir");
     hipExtLaunchKernelGGL(hf_pcg_dir, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, r, p, n, j,
-                       rpart, st, minv, zpart, hflag);
+                       rpart, st, minv, zpart, hflag, g, x, neg_dir, gpart);
     prof_end(L, "hf_pcg_dir", 0.0, 4.0 * 4.0 * n);
   } else {
     prof_begin(L, "hf_cg_dir");
     hipExtLaunchKernelGGL(hf_cg_dir, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, r, p, n, j,
-                       rpart, st, hflag);
+                       rpart, st, hflag, g, x, neg_dir, gpart);
     prof_end(L, "hf_cg_dir", 0.0, 3.0 * 4.0 * n);
   }
 }

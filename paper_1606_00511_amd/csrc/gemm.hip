@@ -385,7 +385,9 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
   constexpr int SZ = TX::SIZE > TY::SIZE ? TX::SIZE : TY::SIZE;
   constexpr int V1 = TX::V1;
   constexpr bool DMA = VEC == 4 && !SQ;
-  constexpr int S = 2;      // LDS stages
+  // LDS stages: 64 x 64 tiles have short K chains (split K, small grids)
+  // and a quarter of the LDS per stage, so they keep three blocks in flight
+  constexpr int S = TS == 64 ? 4 : 2;
   __shared__ __attribute__((aligned(16))) float lds[S][T][SZ];
 
   const int tid = threadIdx.x;
@@ -675,7 +677,10 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, const EpiArgs& e) 
             if (row < s.M) Epi::apply(e, row, col, v0[r], MODE == 0 ? 0.0f : v1[r]);
           }
         }
-        __builtin_amdgcn_sched_barrier(0);
+        // 128 x 128 tiles: keep the scheduler from hoisting every block's
+        // epilogue loads to the top (registers); a 64 x 64 tile's four
+        // blocks may issue theirs together
+        if constexpr (TS == 128) __builtin_amdgcn_sched_barrier(0);
       }
   } else {
     // 32x32 f32 accumulator layout: lane (li, h), register r holds

@@ -101,9 +101,9 @@ struct Profiler {
   // no-ops, so that only launches that did their work are counted.
   // last = the last iteration that evaluated a product; stop_on_kappa: the
   // update kernel of that iteration stopped on kappa (negative curvature or a
-  // non-finite value) before touching the vectors, so it and the direction
-  // kernel did no vector work; neg_iter: iteration whose negative-curvature
-  // kernels ran (-1: none).
+  // non-finite value) before touching x and r; neg_iter: the iteration of a
+  // detection (-1: none), whose update and direction kernels formed g.p and
+  // d~ (without one they did no vector work).
   void retract(int last, bool stop_on_kappa, int neg_iter) {
     std::vector<Pending> keep(pending.begin(), pending.begin() + solve_begin);
     keep.reserve(pending.size());
@@ -112,11 +112,12 @@ struct Profiler {
       bool drop = false;
       if (p.tag >= 0) {
         const std::string& nm = recs[p.rec].name;
-        const bool is_neg = nm == "hf_cg_neg_dot" || nm == "hf_cg_neg_write";
+        // at a detection the update and direction kernels form g.p and d~;
+        // at a non-finite kappa they do nothing
         if (p.tag > last) drop = true;
-        else if (is_neg) drop = p.tag != neg_iter;
-        else if (p.tag == last && stop_on_kappa)
-          drop = nm == "hf_cg_update" || nm == "hf_cg_dir";
+        else if (p.tag == last && stop_on_kappa && neg_iter != last)
+          drop = nm == "hf_cg_update" || nm == "hf_cg_dir" ||
+                 nm == "hf_pcg_update" || nm == "hf_pcg_dir";
       }
       if (drop) {
         recs[p.rec].launches -= 1;
@@ -224,6 +225,7 @@ struct hf_ctx {
   size_t oZ = 0, oP = 0, oSplit = 0, oBpart = 0, oR = 0, oPv = 0, oQ = 0,
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
   int max_splits = 32;
+  bool cached_layout = false;   // the layout holds the transposed weights
   size_t split_floats = 0;  // capacity of the split-K scratch (floats)
 
   char* ws = nullptr;
@@ -305,6 +307,7 @@ inline size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
 // transposed weights (fp32) and no solver vectors or state.
 void plan(hf_ctx* c, int64_t Bplan, bool product_only = false) {
   c->Bws = Bplan;
+  c->cached_layout = !product_only;
   c->ldB = round64((int)Bplan);
   const int L = c->L;
   const bool h = c->bf16();
@@ -401,6 +404,7 @@ void plan(hf_ctx* c, int64_t Bplan, bool product_only = false) {
   const size_t rows = h ? 0 : std::min(TILES_1024, (size_t)c->max_splits * B * (size_t)dmax);
   c->split_floats = std::max(wg, rows);
   c->oSplit = take(c->split_floats * f4);
+
   c->oBpart = take((size_t)c->max_splits * dmax * sizeof(double));
   c->oLoss = take(((B + 3) / 4) * sizeof(double));
   c->oErr = take(sizeof(int));
@@ -1106,10 +1110,11 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
     trace_product(c, 0, x0, q, nullptr);
   }
   cg_init(Lc, g, x0, x0 ? q : nullptr, step, r, p, neg_dir, n, (double)damping,
-          (double)rel_tol * (double)rel_tol, part, st, minv);
+          (double)rel_tol * (double)rel_tol, part, st, minv, max_iters);
   // Replay a captured iteration when nothing needs per-iteration host work
   // (kernel timing, kept iterates, the product trace): one graph launch per
-  // iteration instead of a launch per kernel.
+  // iteration instead of a launch per kernel.  The device also stops the
+  // solve at the budget, so that nothing replayed past it does any work.
   const bool replay = max_iters > 0 && !c->prof && !keep && !c->trace_buf &&
                       !c->graphs_off &&
                       cg_graph(c, W, Xc, b, g, step, neg_dir, mode, minv);
@@ -1282,6 +1287,16 @@ void hvp_any(hf_ctx* c, const float* W, const float* X, const int32_t* y, int b,
   const int L = c->L;
   if (c->bf16()) {
     hvp_h(c, W, X, y, b, v, mode, out);
+    return;
+  }
+  // Small batch-row GEMMs: the fused forward / R-forward and backward /
+  // R-backward kernels below have only 128 x 128 tiles and no split K, so a
+  // grid of a few workgroups would run long K chains on a few compute
+  // units.  The cached route (the forward pass of a solve, then its product)
+  // takes 64 x 64 tiles and split K there.
+  if (c->cached_layout && gemm_tile(b, c->d[1]) == 64) {
+    build_cache(c, W, X, b, y, mode == HF_HESSIAN);
+    product_cached(c, W, X, b, v, mode, out, nullptr);
     return;
   }
   // forward fused with R-forward

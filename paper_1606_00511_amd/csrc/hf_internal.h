@@ -223,6 +223,10 @@ struct CgState {
   // graph (the kernels then take j = -1): the dot kernel copies jn to jc,
   // the kernels after it read jc, and the direction kernel sets jn = jc + 1
   int jc, jn;
+  // iteration budget (> 0): the direction kernel of iteration
+  // max_iters - 1 sets done, so that iterations replayed past the budget
+  // do nothing
+  int max_iters;
 };
 
 int cg_grid(long long n);
@@ -233,7 +237,7 @@ int cg_part_doubles();
 void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
              float* x, float* r, float* p, float* neg_dir, long long n,
              double lambda, double tol2, double* part, CgState* st,
-             const float* minv = nullptr);
+             const float* minv = nullptr, int max_iters = 0);
 // One CG iteration j after the product q = A p has been formed:
 // kappa = p.q + lambda p.p and the stop test; x += alpha p,
 // r += alpha (q + lambda p); at a detection d~ = -sgn(g.p) p and, at j = 0,
