@@ -74,10 +74,14 @@ def parse():
 def counter_traffic(kernel):
     """HBM bytes per launch of `kernel` from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary, or None when the summary does not cover
-    the kernel or the GEMM source has changed since the counters were taken."""
+    the kernel or its GEMM source (gemm.hip, or gemm_bf16.hip for the bf16
+    kernels) has changed since the counters were taken."""
     import hashlib
+    bf16 = kernel.startswith("hf_hgemm")
     path = os.path.join(ROOT, "profiles", "speech_b16384_hbm_counters.md")
-    src = os.path.join(ROOT, "paper_1606_00511_amd", "csrc", "gemm.hip")
+    src = os.path.join(ROOT, "paper_1606_00511_amd", "csrc",
+                       "gemm_bf16.hip" if bf16 else "gemm.hip")
+    tag = "gemm_bf16_source_sha256" if bf16 else "gemm_source_sha256"
     try:
         lines = open(path).read().split("\n")
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
@@ -88,7 +92,7 @@ def counter_traffic(kernel):
         t = l.split()
         if len(t) == 3 and t[0] == "traffic_bytes_per_launch":
             vals[t[1]] = float(t[2])
-        if len(t) == 2 and t[0] == "gemm_source_sha256":
+        if len(t) == 2 and t[0] == tag:
             vals["sha"] = t[1]
     if vals.get("sha") != sha:
         return None
@@ -188,14 +192,19 @@ def run_leg(args, w, inp, prec):
         ev[5].record()
         return ig, ih
 
+    def progress(msg):
+        print("[bench %s] %s" % (prec, msg), file=sys.stderr, flush=True)
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    progress("warm-up done")
     net.prof_enable(True)
     net.prof_reset()
     step()
     torch.cuda.synchronize()
     breakdown = net.prof_stats()
+    progress("profiled step done")
     gemms = {k: st for k, st in breakdown.items() if k.startswith(("hf_gemm", "hf_hgemm"))}
     dom = max(gemms, key=lambda k: gemms[k]["ms"])
     net.prof_reset()
@@ -214,6 +223,7 @@ def run_leg(args, w, inp, prec):
         products += 2 + ig["products"] + ih["products"]
         torch.cuda.synchronize()
         step_ms.append(1e3 * (time.perf_counter() - ts))
+        progress("timed step %d: %.1f ms" % (len(step_ms), step_ms[-1]))
         for i, k in enumerate(names):
             comp[k] += ev[i].elapsed_time(ev[i + 1])
     torch.cuda.synchronize()
@@ -263,24 +273,23 @@ def run_leg(args, w, inp, prec):
                 "backtrack_iter": it["backtrack_iter"],
                 "rho": it["rho"] if math.isfinite(it["rho"]) else None,
                 "damping_next": it["damping_next"]}
-    # and preconditioned (Martens' diagonal preconditioner; fp32 contexts)
-    outer_pc = None
-    if prec == "fp32":
-        Wk.copy_(W)
-        dk.zero_()
-        e0.record()
-        it, _ = net.hf_iterate(Wk, X, y, Xc, yc, dk, solver="cg",
-                               curvature="gauss_newton", damping=lam,
-                               max_iters=w.cg_iters, adapt_damping=True,
-                               keep=keep, precondition=True)
-        e1.record()
-        torch.cuda.synchronize()
-        outer_pc = {"ms": e0.elapsed_time(e1), "direction": it["direction"],
-                    "alpha": it["alpha"], "evals": it["evals"], "f0": it["f0"],
-                    "f1": it["f1"], "solve_products": it["solve"]["products"],
-                    "backtrack_iter": it["backtrack_iter"],
-                    "rho": it["rho"] if math.isfinite(it["rho"]) else None,
-                    "damping_next": it["damping_next"]}
+    # and preconditioned (Martens' diagonal preconditioner)
+    Wk.copy_(W)
+    dk.zero_()
+    e0.record()
+    it, _ = net.hf_iterate(Wk, X, y, Xc, yc, dk, solver="cg",
+                           curvature="gauss_newton", damping=lam,
+                           max_iters=w.cg_iters, adapt_damping=True,
+                           keep=keep, precondition=True)
+    e1.record()
+    torch.cuda.synchronize()
+    outer_pc = {"ms": e0.elapsed_time(e1), "direction": it["direction"],
+                "alpha": it["alpha"], "evals": it["evals"], "f0": it["f0"],
+                "f1": it["f1"], "solve_products": it["solve"]["products"],
+                "backtrack_iter": it["backtrack_iter"],
+                "rho": it["rho"] if math.isfinite(it["rho"]) else None,
+                "damping_next": it["damping_next"]}
+    progress("extras done")
     del Wk, dk, keep
     res = dict(stats=stats, breakdown=breakdown, dom=dom, comp=comp,
                products=products, elapsed=t1 - t0,
@@ -467,6 +476,8 @@ def main():
                 "bound": "mfma", "kernel": s16["dom"], "achieved": s16["achieved"],
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": s16["achieved"] / PEAK_BF16_TFLOPS,
+                "traffic": counter_traffic(s16["dom"]),
+                "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "launches": d16["launches"],
                 "avg_launch_ms": d16["ms"] / d16["launches"],
                 "flops_per_launch": d16["flops"] / d16["launches"]},
@@ -474,7 +485,8 @@ def main():
         }
         for k in ("step_ms", "gemm_all", "cg_vector", "components_ms", "cg_gn",
                   "cg_hess", "bicgstab_hessian", "outer_iteration",
-                  "outer_iteration_gn_backtrack", "kernels"):
+                  "outer_iteration_gn_backtrack", "outer_iteration_gn_precond",
+                  "kernels"):
             out["bf16_inputs"][k] = s16[k]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_rows)

@@ -841,7 +841,7 @@ struct Kernels {
 void launch_single(const Launch& L, const char* name, const Kernels& k,
                    const GemmShape& s, const EpiArgs& e, double flops,
                    double bytes) {
-  if (gemm_tile(s.M, s.N) == 64)
+  if (gemm_tile(s.M, s.N, s.K * s.nseg) == 64)
     launch(L, name, k.t4, k.t1, 64, 0, s, e, flops, bytes);
   else
     launch(L, name, k.k4, k.k1, 128, 0, s, e, flops, bytes);
@@ -856,7 +856,7 @@ void launch_single(const Launch& L, const char* name, const Kernels& k,
 // full batch).
 int row_splits(const GemmShape& s, const EpiArgs& e) {
   if (!e.split_buf) return 1;
-  const int ts = gemm_tile(s.M, s.N);
+  const int ts = gemm_tile(s.M, s.N, s.K * s.nseg);
   const long long tiles = (long long)cdiv(s.M, ts) * cdiv(s.N, ts);
   const int ktot = s.K * s.nseg;
   int sp = 1;
@@ -907,9 +907,11 @@ inline double io(const GemmShape& s, int nx, int ny, int nout) {
 
 }  // namespace
 
-int gemm_tile(int M, int N) {
+int gemm_tile(int M, int N, int K) {
+  if (M <= 64 || N <= 64) return 64;
   const long long t128 = (long long)cdiv(M, 128) * cdiv(N, 128);
-  return (t128 < 128 || M <= 64 || N <= 64) ? 64 : 128;
+  const long long splits = std::max(1, std::min(32, K / 128));
+  return t128 * splits < 256 ? 64 : 128;
 }
 
 void gemm_fwd(const Launch& L, const GemmShape& s, const EpiArgs& e) {

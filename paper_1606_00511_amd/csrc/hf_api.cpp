@@ -497,7 +497,7 @@ void trace_product(hf_ctx* c, int k, const float* v, const float* out,
 // at least 64 rows (4 K blocks: enough to fill the load pipeline; a few
 // workgroups with long K chains would leave most of the chip idle).
 int choose_splits(const hf_ctx* c, int M, int N, int Ktot) {
-  const int ts = c->bf16() ? 128 : gemm_tile(M, N);
+  const int ts = c->bf16() ? 128 : gemm_tile(M, N, Ktot);
   const int tiles = ((M + ts - 1) / ts) * ((N + ts - 1) / ts);
   int s = 1;
   while (s < c->max_splits && (Ktot + s - 1) / s > 2048) s *= 2;
@@ -1291,10 +1291,11 @@ void hvp_any(hf_ctx* c, const float* W, const float* X, const int32_t* y, int b,
   }
   // Small batch-row GEMMs: the fused forward / R-forward and backward /
   // R-backward kernels below have only 128 x 128 tiles and no split K, so a
-  // grid of a few workgroups would run long K chains on a few compute
-  // units.  The cached route (the forward pass of a solve, then its product)
-  // takes 64 x 64 tiles and split K there.
-  if (c->cached_layout && gemm_tile(b, c->d[1]) == 64) {
+  // grid of fewer than 128 workgroups (half the compute units) would run
+  // long K chains on a few units.  The cached route (the forward pass of a
+  // solve, then its product) takes 64 x 64 tiles and split K there.
+  if (c->cached_layout &&
+      (long long)((b + 127) / 128) * ((c->d[1] + 127) / 128) < 128) {
     build_cache(c, W, X, b, y, mode == HF_HESSIAN);
     product_cached(c, W, X, b, v, mode, out, nullptr);
     return;

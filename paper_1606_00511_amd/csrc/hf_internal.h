@@ -78,10 +78,12 @@ struct EpiArgs {
 };
 
 // Output tile (128 or 64 rows and columns) of the single-product GEMMs
-// for an M x N output: 64 when 128 x 128 tiles would number fewer than 128
-// (half the compute units) or an output side is at most 64 wide.  The
+// for an M x N output over K (all segments): 64 when an output side is at
+// most 64 wide, or when 128 x 128 tiles could not give every compute unit a
+// workgroup even split along K (at most 32 splits of at least 128).  The
 // split-K choice of the weight gradients counts tiles of this size.
-int gemm_tile(int M, int N);
+int gemm_tile(int M, int N, int K);
+
 
 // Forward:  out0 = phi(acc + bias) (hidden) or acc + bias (logits);
 // the weights come transposed (Y row-contiguous: Y[k * ldy + n])
