@@ -364,6 +364,10 @@ def summary(res, K, peak):
     gemms = {k: s for k, s in stats.items() if k.startswith(("hf_gemm", "hf_hgemm"))}
     gemm_ms = sum(s["ms"] for s in gemms.values())
     gemm_fl = sum(s["flops"] for s in gemms.values())
+    # the separate passes that complete split-K GEMMs (epilogue of the
+    # batch-row partials, reduce of the weight-gradient partials)
+    split_ms = sum(s["ms"] for k, s in stats.items()
+                   if k in ("hf_splitk_epi", "hf_splitk_reduce"))
     vec = {k: s for k, s in stats.items() if k in (
         "hf_cg_dot", "hf_cg_update", "hf_cg_dir")}
     vec_ms = sum(s["ms"] for s in vec.values())
@@ -373,7 +377,10 @@ def summary(res, K, peak):
         dom=dom, ds=ds, achieved=achieved,
         gemm_all={"tflops": gemm_fl / (gemm_ms * 1e-3) / 1e12,
                   "frac": gemm_fl / (gemm_ms * 1e-3) / 1e12 / peak,
-                  "ms_per_step": gemm_ms},
+                  "ms_per_step": gemm_ms,
+                  "frac_with_split_passes":
+                      gemm_fl / ((gemm_ms + split_ms) * 1e-3) / 1e12 / peak,
+                  "split_pass_ms_per_step": split_ms},
         cg_vector={"GB/s": vec_b / (vec_ms * 1e-3) / 1e9 if vec_ms else None,
                    "frac_hbm": (vec_b / (vec_ms * 1e-3) / 1e9 / PEAK_HBM_GBS)
                    if vec_ms else None, "ms_per_step": vec_ms},
