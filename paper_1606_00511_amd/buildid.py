@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "hf.h")
 SOURCES = ["hf_api.cpp", "gemm.hip", "gemm_bf16.hip", "rowops.hip", "cgvec.hip",
-           "noalloc.hip"]
+           "noalloc.hip", "narrow.hip"]
 
 
 def source_files():

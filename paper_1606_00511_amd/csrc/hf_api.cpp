@@ -617,10 +617,58 @@ void backward_data(hf_ctx* c, const float* W, int l, int B, bool cache_e2) {
 // One curvature product out = A v on B rows of X with the forward cache
 // (A_l, p, delta_l, E2_l and the transposed weights) already computed;
 // skip = device flag or null.
+// The narrow-net form of product_cached: one launch up to the weight
+// gradients, where its grid of 16-row workgroups beats the GEMM path (the
+// small-output regime of the first layer's GEMM).
+bool product_narrow(hf_ctx* c, const float* W, const float* X, int B,
+                    const float* v, int mode, float* out, const int* skip) {
+  const int L = c->L;
+  if (!narrow_eligible(L, c->d.data(), X, v) || gemm_tile(B, c->d[1], c->d[0]) != 64)
+    return false;
+  const bool hess = mode == HF_HESSIAN;
+  NarrowArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.L = L;
+  a.B = B;
+  a.act = c->act;
+  a.hess = hess ? 1 : 0;
+  for (int l = 0; l <= L; ++l) {
+    a.d[l] = c->d[l];
+    a.ld[l] = l == 0 ? c->d[0] : c->ld[l];
+    a.offW[l] = l == 0 ? 0 : (long long)c->offW[l];
+    a.offB[l] = l == 0 ? 0 : (long long)c->offB[l];
+    if (l >= 1) a.RD[l] = c->F(c->oRD[l]);
+    if (l >= 1 && l < L) {
+      a.A[l] = c->F(c->oA[l]);
+      a.RA[l] = c->F(c->oRA[l]);
+      a.E2[l] = hess ? c->F(c->oE2[l]) : nullptr;
+    }
+    if (l >= 2) a.D[l] = hess ? c->F(c->oD[l]) : nullptr;
+  }
+  a.X = X;
+  a.W = W;
+  a.v = v;
+  a.P = c->F(c->oP);
+  a.invB = 1.0f / (float)B;
+  a.skip = skip;
+  narrow_product(c->launch(), a);
+  for (int l = L; l >= 1; --l) {
+    const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
+    const int ldin = (l == 1) ? c->d[0] : c->ld[l - 1];
+    if (hess && l > 1)
+      wgrad(c, l, B, c->F(c->oRD[l]), Ain, c->F(c->oD[l]), c->F(c->oRA[l - 1]),
+            ldin, out, skip);
+    else
+      wgrad(c, l, B, c->F(c->oRD[l]), Ain, nullptr, nullptr, ldin, out, skip);
+  }
+  return true;
+}
+
 void product_cached(hf_ctx* c, const float* W, const float* X, int B,
                     const float* v, int mode, float* out, const int* skip) {
   const Launch Lc = c->launch();
   const int L = c->L;
+  if (product_narrow(c, W, X, B, v, mode, out, skip)) return;
   transpose_weights(c, v, c->oVT, skip);
   for (int l = 1; l <= L; ++l) {
     GemmShape s;

@@ -113,6 +113,40 @@ void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e);
 // X[0]^2)
 void gemm_wgrad_sq(const Launch& L, const GemmShape& s, const EpiArgs& e);
 
+// ------------------------------------------------- narrow-net product
+// The cached curvature product up to the weight gradients in one launch,
+// for nets with 2 <= L <= NARROW_MAX_LAYERS, at most NARROW_MAX_INPUT inputs,
+// hidden layers at most NARROW_MAX_HIDDEN wide and at most 64 classes
+// (narrow.hip): 16 batch rows
+// per workgroup with every intermediate row in LDS.  Writes Rdelta_l
+// (l = 1..L, leading dimensions ld[l]) and, for the Hessian, RA_l
+// (l = 1..L-1), which the weight-gradient GEMMs then read.  Pointers per
+// layer index l; the cache (A_l, P, delta_l, E2_l) is that of a solve.
+constexpr int NARROW_MAX_HIDDEN = 128;
+constexpr int NARROW_MAX_LAYERS = 4;
+constexpr int NARROW_MAX_INPUT = 1024;     // d_0 (the rows of X sit in LDS)
+struct NarrowArgs {
+  int L, B, act, hess;
+  int d[NARROW_MAX_LAYERS + 1];
+  int ld[NARROW_MAX_LAYERS + 1];
+  long long offW[NARROW_MAX_LAYERS + 1], offB[NARROW_MAX_LAYERS + 1];
+  const float* X;                         // B x d_0, row-major
+  const float* W;                         // parameters
+  const float* v;                         // direction
+  const float* A[NARROW_MAX_LAYERS + 1];  // A_l, l = 1..L-1
+  const float* P;                         // softmax probabilities
+  const float* D[NARROW_MAX_LAYERS + 1];  // delta_l, l = 2..L (Hessian)
+  const float* E2[NARROW_MAX_LAYERS + 1]; // E2_l, l = 1..L-1 (Hessian)
+  float* RA[NARROW_MAX_LAYERS + 1];       // out: RA_l (Hessian)
+  float* RD[NARROW_MAX_LAYERS + 1];       // out: Rdelta_l
+  float invB;
+  const int* skip;
+};
+// Whether the layer widths and the alignment of X and v (16 bytes, d_0 a
+// multiple of 4) admit the narrow kernel.
+bool narrow_eligible(int L, const int* d, const float* X, const float* v);
+void narrow_product(const Launch& L, const NarrowArgs& a);
+
 // --------------------------------------------------------- bf16-input GEMM
 // Precision HF_BF16_INPUTS: every GEMM operand is a bf16 copy (stored as
 // uint16_t, rounded to nearest even from fp32), the MFMAs accumulate in fp32

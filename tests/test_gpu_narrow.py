@@ -1,0 +1,123 @@
+"""GPU parity of the narrow-net product (one launch up to the weight
+gradients: 16 batch rows per workgroup, every hidden unit of those rows in
+LDS), through the C ABI, against the fp64 oracle.
+
+The kernel serves nets with 2 to 4 weight layers, hidden layers at most 128
+wide and at most 64 classes, at batches where the first layer's GEMM would
+take 64 x 64 tiles.  It runs inside every cached product there: the CG
+solves and the stateless products of such nets.  Bars as for the other
+fp32 products: rel-L2 <= 1e-4 (ReLU with the per-unit bracket), CG counts,
+the detection iteration and the sign of kappa exact.  Shapes: the widest
+admitted layers (128 hidden, 64 classes), widths and batches that are not
+multiples of 16 (the kernel's row and column blocks), one row, and 2, 3 and
+4 weight layers.  The profiler confirms the kernel ran.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import hf_oracle as O
+from paper_1606_00511_amd import workloads as WL
+from tests.parity_util import check, relu_margins
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+CASES = [
+    ((784, 100, 10), "sigmoid", 1000),
+    ((64, 128, 64), "tanh", 333),
+    ((96, 40, 30, 17), "relu", 77),
+    ((32, 128, 128, 128, 64), "tanh", 50),
+    ((20, 16, 12, 5), "sigmoid", 1),
+    ((48, 100, 3), "relu", 130),
+]
+
+
+def dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def host(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def sid(c):
+    return "%s-%s-b%d" % ("x".join(map(str, c[0])), c[1], c[2])
+
+
+@pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
+@pytest.mark.parametrize("case", CASES, ids=[sid(c) for c in CASES])
+def test_narrow_product(case, mode):
+    from paper_1606_00511_amd.hf import HFNet
+    dims, act, B = case
+    p = WL.make_small(dims, act, B, seed=6100 + B + len(dims))
+    net = HFNet(dims, act, B)
+    net.prof_enable(True)
+    net.prof_reset()
+    W, X, y, v = dev(p["theta"]), dev(p["X"]), dev(p["y"]), dev(p["v"])
+    out = host(net.hf_hvp(W, X, y, v, mode))
+    stats = net.prof_stats()
+    net.prof_enable(False)
+    assert "hf_narrow_product" in stats, sorted(stats)
+    ref = O.curvature(dims, act, p["theta"], p["X"], p["y"], p["v"], mode)
+    err, bound = check(out, ref, act, lambda k: O.curvature(
+        dims, act, p["theta"], p["X"], p["y"], p["v"], mode, kink=k),
+        margins=relu_margins(dims, act, p["theta"], p["X"]))
+    print("%s %s: rel %.2e (bound %.2e)" % (sid(case), mode, err, bound))
+    net.close()
+
+
+@pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
+@pytest.mark.parametrize("case", CASES[:4], ids=[sid(c) for c in CASES[:4]])
+def test_narrow_cg(case, mode):
+    """CG on the narrow product: counts, detection and kappa's sign exact;
+    the lock-step trace compares every product with the oracle's A p_j."""
+    from paper_1606_00511_amd.hf import HFNet
+    dims, act, B = case
+    p = WL.make_small(dims, act, B, seed=6200 + B)
+    net = HFNet(dims, act, B)
+    W, X, y = dev(p["theta"]), dev(p["X"]), dev(p["y"])
+    _, g = net.hf_loss_grad(W, X, y)
+    g_np = host(g).astype(np.float64)
+    cap = 6
+    buf = net.set_trace(cap)
+    _, _, gi = net.hf_cg(W, X, y, g, 1e-2, cap, mode)
+    net.set_trace(0)
+    tr = host(buf)
+    oi = O.cg_network(dims, act, p["theta"], p["X"], p["y"], g_np, 1e-2, cap, mode)
+    print(sid(case), mode, {k: gi[k] for k in ("iters", "products", "neg_curv",
+                                               "neg_iter")},
+          oi["iters"], oi["products"], oi["neg_iter"])
+    assert (gi["iters"], gi["products"], gi["neg_curv"], gi["neg_iter"]) == \
+        (oi["iters"], oi["products"], oi["neg_curv"], oi["neg_iter"])
+    if oi["neg_curv"]:
+        assert np.sign(gi["pBp"]) == np.sign(oi["pBp"])
+    margins = relu_margins(dims, act, p["theta"], p["X"])
+    for k in range(min(cap, gi["products"])):
+        v64 = tr[2 * k].astype(np.float64)
+        ref = O.curvature(dims, act, p["theta"], p["X"], p["y"], v64, mode)
+        err, bound = check(tr[2 * k + 1], ref, act, lambda kink: O.curvature(
+            dims, act, p["theta"], p["X"], p["y"], v64, mode, kink=kink),
+            margins=margins)
+    net.close()
+
+
+def test_narrow_not_taken_outside_its_shapes():
+    """Wider hidden layers, more classes, one weight layer or a first-layer
+    width that is not a multiple of 4 keep the GEMM path."""
+    from paper_1606_00511_amd.hf import HFNet
+    for dims in ((64, 129, 10), (64, 100, 65), (64, 10), (37, 45, 13)):
+        p = WL.make_small(dims, "tanh", 40, seed=6300)
+        net = HFNet(dims, "tanh", 40)
+        net.prof_enable(True)
+        net.prof_reset()
+        out = net.hf_hvp(dev(p["theta"]), dev(p["X"]), dev(p["y"]), dev(p["v"]),
+                         "hessian")
+        host(out)
+        assert "hf_narrow_product" not in net.prof_stats(), dims
+        net.prof_enable(False)
+        net.close()
