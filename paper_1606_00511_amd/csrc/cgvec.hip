@@ -27,7 +27,7 @@ namespace hfk {
 namespace {
 
 constexpr int NT = 256;
-constexpr int MAX_GRID = 1024;
+constexpr int MAX_GRID = CG_MAX_GRID;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -224,11 +224,13 @@ __device__ __forceinline__ void cg_update_body(
     const double* __restrict__ dpart, double* __restrict__ rpart,
     CgState* __restrict__ st, const float* __restrict__ minv,
     double* __restrict__ zpart, const float* __restrict__ g,
-    double* __restrict__ gpart) {
+    double* __restrict__ gpart, int ndp) {
   if (st->done) return;
   if (j < 0) j = st->jc;
   __shared__ double sh[4];
-  const int nb = gridDim.x;
+  // the partials of p.q and p.p: one per block of the dot kernel (its grid
+  // is this one), or ndp from the product that formed them
+  const int nb = ndp > 0 ? ndp : (int)gridDim.x;
   const double pq = total(dpart, nb, sh);
   const double pp = total(dpart + MAX_GRID, nb, sh);
   const double lam = st->lambda;
@@ -308,9 +310,9 @@ extern "C" __global__ __launch_bounds__(256) void hf_cg_update(
     const float* __restrict__ q, long long n, int j,
     const double* __restrict__ dpart, double* __restrict__ rpart,
     CgState* __restrict__ st, const float* __restrict__ g,
-    double* __restrict__ gpart) {
+    double* __restrict__ gpart, int ndp) {
   cg_update_body<false>(x, r, p, q, n, j, dpart, rpart, st, nullptr, nullptr,
-                        g, gpart);
+                        g, gpart, ndp);
 }
 extern "C" __global__ __launch_bounds__(256) void hf_pcg_update(
     float* __restrict__ x, float* __restrict__ r, const float* __restrict__ p,
@@ -318,9 +320,9 @@ extern "C" __global__ __launch_bounds__(256) void hf_pcg_update(
     const double* __restrict__ dpart, double* __restrict__ rpart,
     CgState* __restrict__ st, const float* __restrict__ minv,
     double* __restrict__ zpart, const float* __restrict__ g,
-    double* __restrict__ gpart) {
+    double* __restrict__ gpart, int ndp) {
   cg_update_body<true>(x, r, p, q, n, j, dpart, rpart, st, minv, zpart, g,
-                       gpart);
+                       gpart, ndp);
 }
 
 // PC: beta = r'.z' / r.z and p = -minv r + beta p.
@@ -456,25 +458,28 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
 
 void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
                   const float* g, float* neg_dir, long long n, int j,
-                  double* part, CgState* st, const float* minv, int* hflag) {
+                  double* part, CgState* st, const float* minv, int* hflag,
+                  int dot_blocks) {
   const int nb = cg_grid(n);
   double* dpart = part;                  // 2 * MAX_GRID: p.q, p.p
   double* rpart = part + 2 * MAX_GRID;   // r.r
   double* gpart = part + 3 * MAX_GRID;   // g.p
   double* zpart = part + 6 * MAX_GRID;   // r.z (preconditioned)
-  prof_begin(L, "hf_cg_dot");
-  hipExtLaunchKernelGGL(hf_cg_dot, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, p, q, n,
-                     dpart, st, j);
-  prof_end(L, "hf_cg_dot", 0.0, 2.0 * 4.0 * n);
+  if (dot_blocks <= 0) {
+    prof_begin(L, "hf_cg_dot");
+    hipExtLaunchKernelGGL(hf_cg_dot, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, p, q,
+                          n, dpart, st, j);
+    prof_end(L, "hf_cg_dot", 0.0, 2.0 * 4.0 * n);
+  }
   if (minv) {
     prof_begin(L, "hf_pcg_update");
     hipExtLaunchKernelGGL(hf_pcg_update, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, r, p,
-                       q, n, j, dpart, rpart, st, minv, zpart, g, gpart);
+                       q, n, j, dpart, rpart, st, minv, zpart, g, gpart, dot_blocks);
     prof_end(L, "hf_pcg_update", 0.0, 7.0 * 4.0 * n);
   } else {
     prof_begin(L, "hf_cg_update");
     hipExtLaunchKernelGGL(hf_cg_update, dim3(nb), dim3(NT), 0, L.stream, prof_a(L), prof_b(L), 0, x, r, p,
-                       q, n, j, dpart, rpart, st, g, gpart);
+                       q, n, j, dpart, rpart, st, g, gpart, dot_blocks);
     prof_end(L, "hf_cg_update", 0.0, 6.0 * 4.0 * n);
   }
   if (minv) {

@@ -226,6 +226,21 @@ struct hf_ctx {
          oRed = 0, oLoss = 0, oState = 0, oErr = 0, need = 0;
   int max_splits = 32;
   bool cached_layout = false;   // the layout holds the transposed weights
+  // concatenated columns for the narrow-net weight gradients (NarrowCat):
+  // X, A_1 .. A_{L-1} (Ycat) and RA (RAcat), width ldy; Rdelta (RDcat) and
+  // delta (Dcat), width ldr.  cat_B / cat_hess: the batch and mode whose
+  // cache build filled Ycat (and Dcat), -1 if none.
+  bool narrow_cat = false;
+  int ldr_cat = 0, ldy_cat = 0;
+  int roff[NARROW_MAX_LAYERS + 1] = {}, yoff[NARROW_MAX_LAYERS + 1] = {};
+  size_t oYcat = 0, oRDcat = 0, oDcat = 0, oRAcat = 0;
+  int cat_B = -1;
+  bool cat_hess = false;
+  // a CG iteration's request that its product also form the partials of
+  // p.q and p.p (fuse.p set for that one product call); fused_blocks: how
+  // many partials it wrote, 0 if the product took a route without them
+  CgDotFuse fuse = {};
+  int fused_blocks = 0;
   size_t split_floats = 0;  // capacity of the split-K scratch (floats)
 
   char* ws = nullptr;
@@ -382,6 +397,21 @@ void plan(hf_ctx* c, int64_t Bplan, bool product_only = false) {
   }
   c->oZ = take(RB * c->ld[L] * f4);
   c->oP = take(RB * c->ld[L] * f4);
+  // narrow nets: the concatenated columns of their weight-gradient GEMM
+  c->narrow_cat = false;
+  c->cat_B = -1;
+  if (!h && !product_only && narrow_eligible(L, c->d.data(), nullptr, nullptr)) {
+    c->narrow_cat = true;
+    int r = 0, y = 0;
+    for (int l = 1; l <= L; ++l) { c->roff[l] = r; r += round4(c->d[l]); }
+    for (int l = 0; l < L; ++l) { c->yoff[l] = y; y += round4(c->d[l]); }
+    c->ldr_cat = r;
+    c->ldy_cat = y;
+    c->oYcat = take(B * (size_t)y * f4);
+    c->oRAcat = take(B * (size_t)y * f4);
+    c->oRDcat = take(B * (size_t)r * f4);
+    c->oDcat = take(B * (size_t)r * f4);
+  }
   // Split-K scratch.  A weight gradient (d_l x d_{l-1}, K up to 2 B rows
   // over two segments) takes at most the splits that keep every split within
   // 2,048 rows at that K, or, if the tile rule asked for more, fewer than
@@ -403,9 +433,15 @@ void plan(hf_ctx* c, int64_t Bplan, bool product_only = false) {
   }
   const size_t rows = h ? 0 : std::min(TILES_1024, (size_t)c->max_splits * B * (size_t)dmax);
   c->split_floats = std::max(wg, rows);
+  // the narrow nets' concatenated weight-gradient GEMM (at most max_splits
+  // partials of ldr x ldy)
+  if (c->narrow_cat)
+    c->split_floats = std::max(c->split_floats,
+                               (size_t)c->max_splits * c->ldr_cat * c->ldy_cat);
   c->oSplit = take(c->split_floats * f4);
 
-  c->oBpart = take((size_t)c->max_splits * dmax * sizeof(double));
+  c->oBpart = take((size_t)c->max_splits * std::max(dmax, c->narrow_cat ? c->ldr_cat : 0) *
+                   sizeof(double));
   c->oLoss = take(((B + 3) / 4) * sizeof(double));
   c->oErr = take(sizeof(int));
   if (product_only) {
@@ -583,6 +619,7 @@ void transpose_weights(hf_ctx* c, const float* v, const std::vector<size_t>& dst
 void forward_plain(hf_ctx* c, const float* W, const float* X, int B,
                    const int32_t* y, bool want_delta) {
   const Launch Lc = c->launch();
+  c->cat_B = -1;   // the concatenated copy no longer matches the cache
   transpose_weights(c, W, c->oWT, nullptr);
   for (int l = 1; l <= c->L; ++l) {
     const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
@@ -651,6 +688,50 @@ bool product_narrow(hf_ctx* c, const float* W, const float* X, int B,
   a.P = c->F(c->oP);
   a.invB = 1.0f / (float)B;
   a.skip = skip;
+  const bool cat = c->cat_B == B && (!hess || c->cat_hess);
+  if (cat) {
+    // every layer's Rdelta (and RA) into the concatenated columns, then one
+    // weight-gradient GEMM for all layers and the scatter of its diagonal
+    // blocks
+    a.ldRD = c->ldr_cat;
+    a.ldRA = c->ldy_cat;
+    for (int l = 1; l <= L; ++l) {
+      a.RD[l] = c->F(c->oRDcat) + c->roff[l];
+      if (l < L) a.RA[l] = c->F(c->oRAcat) + c->yoff[l];
+    }
+    narrow_product(c->launch(), a);
+    const int M = c->ldr_cat, N = c->ldy_cat;
+    GemmShape s = shape(M, N, B, c->F(c->oRDcat), hess ? c->F(c->oDcat) : nullptr,
+                        c->F(c->oYcat), hess ? c->F(c->oRAcat) : nullptr, M, N,
+                        hess ? 2 : 1, skip);
+    // always through the partials, so that the scatter has them
+    s.splits = std::max(2, choose_splits(c, M, N, B * s.nseg));
+    EpiArgs e = epi(c, 0);
+    e.out0 = c->F(c->oSplit);
+    e.ldo = N;
+    e.split_stride = (long long)M * N;
+    e.bias_part = c->Dp(c->oBpart);
+    gemm_wgrad(c->launch(), s, e);
+    NarrowCat nc;
+    std::memset(&nc, 0, sizeof nc);
+    nc.L = L;
+    nc.M = M;
+    nc.N = N;
+    for (int l = 0; l <= L; ++l) {
+      nc.d[l] = c->d[l];
+      nc.roff[l] = c->roff[l];
+      nc.yoff[l] = c->yoff[l];
+      if (l >= 1) {
+        nc.offW[l] = c->offW[l];
+        nc.offB[l] = c->offB[l];
+      }
+    }
+    nc.offW[L + 1] = c->n;
+    nc.n = c->n;
+    c->fused_blocks = narrow_scatter(c->launch(), c->F(c->oSplit), c->Dp(c->oBpart), s.splits,
+                                     nc, out, skip, c->fuse.p == v ? &c->fuse : nullptr);
+    return true;
+  }
   narrow_product(c->launch(), a);
   for (int l = L; l >= 1; --l) {
     const float* Ain = (l == 1) ? X : c->F(c->oA[l - 1]);
@@ -963,6 +1044,45 @@ void hvp_h(hf_ctx* c, const float* W, const float* X, const int32_t* y, int B,
 }
 
 // ------------------------------------------------ precision dispatch
+// Narrow nets: the solve's cache also copied into the concatenated columns of
+// the weight-gradient GEMM (X and A_1 .. A_{L-1}; for the Hessian delta_2 ..
+// delta_L), when the narrow product will serve this batch.
+void narrow_cache(hf_ctx* c, const float* X, int B, bool hess) {
+  c->cat_B = -1;
+  const int L = c->L;
+  if (!c->narrow_cat || B > c->Bws || !narrow_eligible(L, c->d.data(), X, nullptr) ||
+      gemm_tile(B, c->d[1], c->d[0]) != 64)
+    return;
+  NarrowGather g;
+  std::memset(&g, 0, sizeof g);
+  g.B = B;
+  g.ldd[0] = c->ldy_cat;
+  g.ldd[1] = c->ldr_cat;
+  int k = 0;
+  for (int l = 0; l < L; ++l) {
+    g.src[k] = l == 0 ? X : c->F(c->oA[l]);
+    g.lds[k] = l == 0 ? c->d[0] : c->ld[l];
+    g.cols[k] = c->d[l];
+    g.dst[k] = c->F(c->oYcat) + c->yoff[l];
+    g.which[k] = 0;
+    ++k;
+  }
+  if (hess) {
+    for (int l = 2; l <= L; ++l) {
+      g.src[k] = c->F(c->oD[l]);
+      g.lds[k] = c->ld[l];
+      g.cols[k] = c->d[l];
+      g.dst[k] = c->F(c->oDcat) + c->roff[l];
+      g.which[k] = 1;
+      ++k;
+    }
+  }
+  g.nblk = k;
+  narrow_gather(c->launch(), g);
+  c->cat_B = B;
+  c->cat_hess = hess;
+}
+
 // The cache of a solve on the curvature batch: forward pass, p and, for the
 // Hessian, delta_l and (delta_l W_l) phi''(A_{l-1}).
 void build_cache(hf_ctx* c, const float* W, const float* X, int B,
@@ -975,6 +1095,7 @@ void build_cache(hf_ctx* c, const float* W, const float* X, int B,
     forward_plain(c, W, X, B, hess ? y : nullptr, hess);
     if (hess)
       for (int l = c->L; l >= 2; --l) backward_data(c, W, l, B, true);
+    narrow_cache(c, X, B, hess);
   }
 }
 
@@ -982,6 +1103,21 @@ void product(hf_ctx* c, const float* W, const float* X, int B, const float* v,
              int mode, float* out, const int* skip) {
   if (c->bf16()) product_cached_h(c, B, v, mode, out, skip);
   else product_cached(c, W, X, B, v, mode, out, skip);
+}
+
+// A CG iteration's product q = A p (skipped once the solve has stopped);
+// where the product's last kernel can also form the partials of p.q and p.p
+// for the iteration's update, it does, and the count of partials is
+// returned (0: the iteration's dot kernel forms them).
+int product_cg(hf_ctx* c, const float* W, const float* X, int B, const float* p,
+               int mode, float* q, double* part, CgState* st, int j) {
+  c->fuse = {p, part, st, j};
+  c->fused_blocks = 0;
+  product(c, W, X, B, p, mode, q, &st->done);
+  c->fuse = {};
+  const int fb = c->fused_blocks;
+  c->fused_blocks = 0;
+  return fb;
 }
 
 // q += lambda v: the damping term of B_k = A + lambda I (Alg. 1 step 3)
@@ -1072,8 +1208,18 @@ struct KeepPlan {
   }
 };
 
-// Make c->cg_exec replay one CG iteration with these arguments: the cached
-// product q = A p and the vector kernels, with the iteration index kept on
+// CG iterations per captured graph.  Each graph launch costs the GPU about
+// 13 us between the last kernel of one replay and the first of the next; on
+// the 784-100-10 net (iterations of about 45 us of kernels) five
+// Gauss-Newton iterations per graph took its 10-iteration solve from 634 to
+// 563 us.  Hessian solves usually stop at a detection within a few
+// iterations, and the iterations captured past the stop would be launched
+// for nothing: one per graph.
+int cg_graph_iters(int mode) { return mode == HF_HESSIAN ? 1 : 5; }
+
+// Make c->cg_exec replay cg_graph_iters(mode) CG iterations with these
+// arguments: each the cached product q = A p and the vector kernels, with
+// the iteration index kept on
 // the device and the stop flag written to host-pinned memory.  Returns
 // false (and switches graphs off for the context) if the capture fails;
 // the caller then runs the launch-by-launch loop.
@@ -1108,9 +1254,12 @@ bool cg_graph(hf_ctx* c, const float* W, const float* Xc, int b, const float* g,
   if (hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeRelaxed) != hipSuccess)
     return off();
   c->stream = c->cap_stream;
-  product(c, W, Xc, b, c->F(c->oPv), mode, c->F(c->oQ), &st->done);
-  cg_iteration(c->launch(), step, c->F(c->oR), c->F(c->oPv), c->F(c->oQ), g, neg_dir,
-               c->n, -1, c->Dp(c->oRed), st, minv, c->hflag_dev);
+  for (int k = 0; k < cg_graph_iters(mode); ++k) {
+    const int fb = product_cg(c, W, Xc, b, c->F(c->oPv), mode, c->F(c->oQ), c->Dp(c->oRed), st,
+                              -1);
+    cg_iteration(c->launch(), step, c->F(c->oR), c->F(c->oPv), c->F(c->oQ), g, neg_dir,
+                 c->n, -1, c->Dp(c->oRed), st, minv, c->hflag_dev, fb);
+  }
   c->stream = user;
   hipGraph_t graph = nullptr;
   const hipError_t e1 = hipStreamEndCapture(c->cap_stream, &graph);
@@ -1135,8 +1284,7 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   std::memset(info, 0, sizeof *info);
   if (!c->pinned) {
     HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
+    for (auto& e : c->ev) HIP_TRY(c, hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
   if (c->prof) c->prof->solve_begin = c->prof->pending.size();
   const Launch Lc = c->launch();
@@ -1159,16 +1307,19 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   }
   cg_init(Lc, g, x0, x0 ? q : nullptr, step, r, p, neg_dir, n, (double)damping,
           (double)rel_tol * (double)rel_tol, part, st, minv, max_iters);
-  // Replay a captured iteration when nothing needs per-iteration host work
+  // Replay captured iterations when nothing needs per-iteration host work
   // (kernel timing, kept iterates, the product trace): one graph launch per
-  // iteration instead of a launch per kernel.  The device also stops the
-  // solve at the budget, so that nothing replayed past it does any work.
+  // cg_graph_iters(mode) iterations instead of a launch per kernel.  The
+  // device also stops the solve at the budget, so that nothing replayed past
+  // it does any work.
   const bool replay = max_iters > 0 && !c->prof && !keep && !c->trace_buf &&
                       !c->graphs_off &&
                       cg_graph(c, W, Xc, b, g, step, neg_dir, mode, minv);
   if (replay) {
     *(volatile int*)c->hflag = 0;
-    for (int j = 0; j < max_iters; ++j) {
+    const int K = cg_graph_iters(mode);
+    const int launches = (max_iters + K - 1) / K;
+    for (int j = 0; j < launches; ++j) {
       HIP_TRY(c, hipGraphLaunch(c->cg_exec, c->stream));
       HIP_TRY(c, hipEventRecord(c->ev[j & 1], c->stream));
       if (j >= 1) {
@@ -1179,9 +1330,9 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   }
   for (int j = 0; !replay && j < max_iters; ++j) {
     if (c->prof) c->prof->tag = j;
-    product(c, W, Xc, b, p, mode, q, skip);
+    const int fb = product_cg(c, W, Xc, b, p, mode, q, part, st, j);
     trace_product(c, k0 + j, p, q, skip);
-    cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st, minv);
+    cg_iteration(Lc, step, r, p, q, g, neg_dir, n, j, part, st, minv, nullptr, fb);
     if (keep) keep->after(Lc, j + 1, step, n, skip);
     // Stop enqueueing once the device reports `done` for the previous
     // iteration; the work already queued for this one returns at once.
@@ -1237,8 +1388,7 @@ int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   std::memset(info, 0, sizeof *info);
   if (!c->pinned) {
     HIP_TRY(c, hipHostMalloc((void**)&c->pinned, 2 * sizeof(CgState), hipHostMallocDefault));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
+    for (auto& e : c->ev) HIP_TRY(c, hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
   BicgState* hostst = reinterpret_cast<BicgState*>(c->pinned_bicg);
   if (!hostst) {
@@ -1348,6 +1498,7 @@ void hvp_any(hf_ctx* c, const float* W, const float* X, const int32_t* y, int b,
     product_cached(c, W, X, b, v, mode, out, nullptr);
     return;
   }
+  c->cat_B = -1;
   // forward fused with R-forward
   for (int l = 1; l <= L; ++l) {
     GemmShape s;
@@ -1508,11 +1659,15 @@ int hf_set_workspace(hf_ctx* c, void* p, size_t bytes) {
   c->ws_bytes = bytes;
   HIP_TRY(c, hipMemset(c->ws + c->oErr, 0, sizeof(int)));
   // bf16 operands: the zeros in their padding columns are never rewritten;
-  // wait for them so that no later stream can run ahead of the fill
-  if (c->hend > c->hbeg) {
-    HIP_TRY(c, hipMemset(c->ws + c->hbeg, 0, c->hend - c->hbeg));
-    HIP_TRY(c, hipDeviceSynchronize());
+  // nor are the zero blocks of the narrow nets' concatenated delta and RA
+  // columns (layer 1 has no second weight-gradient term); wait for the fills
+  // so that no later stream can run ahead of them
+  if (c->hend > c->hbeg) HIP_TRY(c, hipMemset(c->ws + c->hbeg, 0, c->hend - c->hbeg));
+  if (c->narrow_cat) {
+    HIP_TRY(c, hipMemset(c->ws + c->oRAcat, 0, (size_t)c->Bws * c->ldy_cat * sizeof(float)));
+    HIP_TRY(c, hipMemset(c->ws + c->oDcat, 0, (size_t)c->Bws * c->ldr_cat * sizeof(float)));
   }
+  if (c->hend > c->hbeg || c->narrow_cat) HIP_TRY(c, hipDeviceSynchronize());
   return HF_OK;
 }
 

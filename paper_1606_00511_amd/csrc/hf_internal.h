@@ -139,9 +139,53 @@ struct NarrowArgs {
   const float* E2[NARROW_MAX_LAYERS + 1]; // E2_l, l = 1..L-1 (Hessian)
   float* RA[NARROW_MAX_LAYERS + 1];       // out: RA_l (Hessian)
   float* RD[NARROW_MAX_LAYERS + 1];       // out: Rdelta_l
+  int ldRA, ldRD;                         // their leading dimensions (0: ld[l])
   float invB;
   const int* skip;
 };
+// most per-block partials of a CG vector kernel (its largest grid)
+constexpr int CG_MAX_GRID = 1024;
+// The weight gradients of every layer from one GEMM over concatenated
+// columns: Rdelta_1 .. Rdelta_L side by side (column offset roff[l], width
+// ldr) against X, A_1 .. A_{L-1} side by side (offset yoff[l - 1], width
+// ldy), and for the Hessian delta_l against RA_{l-1} likewise; layer l's
+// gradient is the diagonal block (roff[l], yoff[l - 1]).  narrow_scatter
+// sums the GEMM's split-K partials of the diagonal blocks (and the bias
+// partials of their rows) in split order and writes them in the parameter
+// layout.
+struct NarrowCat {
+  int L, M, N;                            // M = ldr, N = ldy
+  int d[NARROW_MAX_LAYERS + 1];
+  int roff[NARROW_MAX_LAYERS + 1], yoff[NARROW_MAX_LAYERS + 1];
+  long long offW[NARROW_MAX_LAYERS + 2], offB[NARROW_MAX_LAYERS + 1];
+  long long n;                            // parameters
+};
+// out[i], i < n, from `splits` partials (part: splits x M x N, bpart:
+// splits x M doubles).  With dot (a CG iteration's product q = out of the
+// direction p) the kernel also does the work of the iteration's first
+// vector kernel: the per-block partials of p.q and p.p and, for an iteration
+// replayed from a graph (j = -1), the publication of its index.  Returns
+// the number of partials written (0 without dot).
+struct CgState;
+struct CgDotFuse {
+  const float* p;
+  double* part;      // p.q partials at part[b], p.p at part[CG_MAX_GRID + b]
+  CgState* st;
+  int j;
+};
+int narrow_scatter(const Launch& L, const float* part, const double* bpart,
+                   int splits, const NarrowCat& nc, float* out, const int* skip,
+                   const CgDotFuse* dot = nullptr);
+// Copies column blocks of B rows: dst_k[r * ldd + c] = src_k[r * lds_k + c]
+// for c < cols_k (one launch for up to 2 NARROW_MAX_LAYERS blocks).
+struct NarrowGather {
+  int nblk, B, ldd[2];
+  const float* src[2 * NARROW_MAX_LAYERS];
+  int lds[2 * NARROW_MAX_LAYERS], cols[2 * NARROW_MAX_LAYERS];
+  float* dst[2 * NARROW_MAX_LAYERS];
+  int which[2 * NARROW_MAX_LAYERS];       // index into ldd
+};
+void narrow_gather(const Launch& L, const NarrowGather& g);
 // Whether the layer widths and the alignment of X and v (16 bytes, d_0 a
 // multiple of 4) admit the narrow kernel.
 bool narrow_eligible(int L, const int* d, const float* X, const float* v);
@@ -281,10 +325,12 @@ void cg_init(const Launch& L, const float* g, const float* x0, const float* q,
 // the state (an iteration captured once and replayed); then, if hflag is
 // not null (host-visible memory), the last kernel of the iteration stores
 // st->done there.
+// dot_blocks > 0: the product already wrote that many partials of p.q and
+// p.p (and published the index), so the dot kernel is not launched.
 void cg_iteration(const Launch& L, float* x, float* r, float* p, const float* q,
                   const float* g, float* neg_dir, long long n, int j,
                   double* part, CgState* st, const float* minv = nullptr,
-                  int* hflag = nullptr);
+                  int* hflag = nullptr, int dot_blocks = 0);
 // With minv (device, n floats, the diagonal of M^-1) cg_init and
 // cg_iteration run preconditioned CG: z = minv r, p = -z at the start,
 // alpha = r.z / kappa, beta = r'.z' / r.z, p = -z' + beta p.

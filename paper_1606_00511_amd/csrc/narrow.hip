@@ -47,6 +47,12 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
 }  // namespace
 
 extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g) {
@@ -172,7 +178,8 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
         sRA[0][row][n] = ra;
         if (hess) {
           sRZ[0][row][n] = nv ? rz : 0.0f;
-          if (nv && r0 + row < g.B) g.RA[1][(size_t)(r0 + row) * g.ld[1] + n] = ra;
+          if (nv && r0 + row < g.B)
+            g.RA[1][(size_t)(r0 + row) * (g.ldRA ? g.ldRA : g.ld[1]) + n] = ra;
         }
       }
     }
@@ -228,7 +235,8 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
           yo[row][n] = ra;
           if (hess) {
             sRZ[l - 1][row][n] = nv ? rz : 0.0f;
-            if (nv && r0 + row < g.B) g.RA[l][(size_t)(r0 + row) * g.ld[l] + n] = ra;
+            if (nv && r0 + row < g.B)
+              g.RA[l][(size_t)(r0 + row) * (g.ldRA ? g.ldRA : g.ld[l]) + n] = ra;
           }
         }
       } else {
@@ -253,7 +261,7 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
       const float dot = wave_sum(p * rz);
       const float rd = p * (rz - dot) * g.invB;
       sRD[1][rr][lane] = rd;
-      if (cv && rv) g.RD[L][(size_t)row * ldL + lane] = rd;
+      if (cv && rv) g.RD[L][(size_t)row * (g.ldRD ? g.ldRD : ldL) + lane] = rd;
     }
   }
   __syncthreads();
@@ -311,12 +319,115 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
                 sRZ[l - 2][row][n];
         rd = nv ? rd : 0.0f;
         yo[row][n] = rd;
-        if (nv && rv) g.RD[l - 1][(size_t)(r0 + row) * g.ld[l - 1] + n] = rd;
+        if (nv && rv)
+          g.RD[l - 1][(size_t)(r0 + row) * (g.ldRD ? g.ldRD : g.ld[l - 1]) + n] = rd;
       }
     }
     __syncthreads();
     cur ^= 1;
   }
+}
+
+// out[i] for parameter i: a weight of layer l at (m, k) is the diagonal
+// block's element (roff[l] + m, yoff[l - 1] + k), a bias of layer l its row
+// roff[l] + m; both summed over the splits in split order (fp64).  With dpart
+// (a CG iteration's product, p its direction): the block's partials of p.q
+// and p.p, q being the stored fp32 out, summed in fp64 in a fixed order.
+extern "C" __global__ __launch_bounds__(256) void hf_narrow_scatter(
+    const float* __restrict__ part, const double* __restrict__ bpart, int S,
+    NarrowCat nc, float* __restrict__ out, const int* __restrict__ skip,
+    const float* __restrict__ p, double* __restrict__ dpart,
+    CgState* __restrict__ st, int j) {
+  // an iteration replayed from a graph: publish its index for the vector
+  // kernels after this one, -1 once the solve has stopped
+  if (dpart && j < 0 && blockIdx.x == 0 && threadIdx.x == 0)
+    st->jc = st->done ? -1 : st->jn;
+  if (skip && *skip) return;
+  const size_t mn = (size_t)nc.M * nc.N;
+  double pq = 0.0, pp = 0.0;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < nc.n;
+       i += (long long)gridDim.x * 256) {
+    int l = 1;
+    while (l < nc.L && i >= nc.offW[l + 1]) ++l;
+    double t = 0.0;
+    if (i < nc.offB[l]) {
+      const long long loc = i - nc.offW[l];
+      const int dk = nc.d[l - 1];
+      const int m = (int)(loc / dk), k = (int)(loc - (long long)m * dk);
+      const float* src = part + (size_t)(nc.roff[l] + m) * nc.N + nc.yoff[l - 1] + k;
+      for (int z0 = 0; z0 < S; z0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int z = 0; z < 8; ++z) v[z] = z0 + z < S ? src[(size_t)(z0 + z) * mn] : 0.0f;
+#pragma unroll
+        for (int z = 0; z < 8; ++z)
+          if (z0 + z < S) t += (double)v[z];
+      }
+    } else {
+      const int m = (int)(i - nc.offB[l]);
+      for (int z = 0; z < S; ++z) t += bpart[(size_t)z * nc.M + nc.roff[l] + m];
+    }
+    const float q = (float)t;
+    out[i] = q;
+    if (dpart) {
+      const double pv = p[i];
+      pq += pv * (double)q;
+      pp += pv * pv;
+    }
+  }
+  if (!dpart) return;
+  __shared__ double sh[2][4];
+  pq = wave_sum_d(pq);
+  pp = wave_sum_d(pp);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sh[0][w] = pq;
+    sh[1][w] = pp;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    dpart[blockIdx.x] = (sh[0][0] + sh[0][1]) + (sh[0][2] + sh[0][3]);
+    dpart[CG_MAX_GRID + blockIdx.x] = (sh[1][0] + sh[1][1]) + (sh[1][2] + sh[1][3]);
+  }
+}
+
+extern "C" __global__ __launch_bounds__(256) void hf_narrow_gather(NarrowGather g) {
+  const int k = blockIdx.y;
+  if (k >= g.nblk) return;
+  const float* __restrict__ src = g.src[k];
+  float* __restrict__ dst = g.dst[k];
+  const int cols = g.cols[k], lds = g.lds[k], ldd = g.ldd[g.which[k]];
+  const long long tot = (long long)g.B * cols;
+  for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < tot;
+       e += (long long)gridDim.x * 256) {
+    const int r = (int)(e / cols), c = (int)(e - (long long)r * cols);
+    dst[(size_t)r * ldd + c] = src[(size_t)r * lds + c];
+  }
+}
+
+int narrow_scatter(const Launch& Lc, const float* part, const double* bpart,
+                   int splits, const NarrowCat& nc, float* out, const int* skip,
+                   const CgDotFuse* dot) {
+  const int nb = (int)std::min<long long>((nc.n + 255) / 256, CG_MAX_GRID);
+  prof_begin(Lc, "hf_narrow_scatter");
+  hipExtLaunchKernelGGL(hf_narrow_scatter, dim3((unsigned)nb), dim3(256), 0, Lc.stream,
+                        prof_a(Lc), prof_b(Lc), 0, part, bpart, splits, nc, out, skip,
+                        dot ? dot->p : nullptr, dot ? dot->part : nullptr,
+                        dot ? dot->st : nullptr, dot ? dot->j : 0);
+  prof_end(Lc, "hf_narrow_scatter", 0.0, 4.0 * (splits + 1 + (dot ? 1 : 0)) * (double)nc.n);
+  return dot ? nb : 0;
+}
+
+void narrow_gather(const Launch& Lc, const NarrowGather& g) {
+  long long most = 0;
+  for (int k = 0; k < g.nblk; ++k) most = std::max<long long>(most, (long long)g.B * g.cols[k]);
+  const long long nb = std::max<long long>(1, std::min<long long>((most + 255) / 256, 256));
+  prof_begin(Lc, "hf_narrow_gather");
+  hipExtLaunchKernelGGL(hf_narrow_gather, dim3((unsigned)nb, (unsigned)g.nblk), dim3(256), 0,
+                        Lc.stream, prof_a(Lc), prof_b(Lc), 0, g);
+  double by = 0.0;
+  for (int k = 0; k < g.nblk; ++k) by += 8.0 * g.B * g.cols[k];
+  prof_end(Lc, "hf_narrow_gather", 0.0, by);
 }
 
 bool narrow_eligible(int L, const int* d, const float* X, const float* v) {
