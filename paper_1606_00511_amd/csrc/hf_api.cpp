@@ -684,6 +684,7 @@ bool product_narrow(hf_ctx* c, const float* W, const float* X, int B,
   }
   a.X = X;
   a.W = W;
+  a.RZ1 = c->F(c->oRZ[1]);
   a.v = v;
   a.P = c->F(c->oP);
   a.invB = 1.0f / (float)B;
@@ -1254,11 +1255,15 @@ bool cg_graph(hf_ctx* c, const float* W, const float* Xc, int b, const float* g,
   if (hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeRelaxed) != hipSuccess)
     return off();
   c->stream = c->cap_stream;
-  for (int k = 0; k < cg_graph_iters(mode); ++k) {
+  // only the graph's last iteration stores the stop flag in host memory
+  // (its direction kernel stores it whether or not the solve stopped
+  // earlier in the graph); a store there delays the next kernel's start
+  const int K = cg_graph_iters(mode);
+  for (int k = 0; k < K; ++k) {
     const int fb = product_cg(c, W, Xc, b, c->F(c->oPv), mode, c->F(c->oQ), c->Dp(c->oRed), st,
                               -1);
     cg_iteration(c->launch(), step, c->F(c->oR), c->F(c->oPv), c->F(c->oQ), g, neg_dir,
-                 c->n, -1, c->Dp(c->oRed), st, minv, c->hflag_dev, fb);
+                 c->n, -1, c->Dp(c->oRed), st, minv, k == K - 1 ? c->hflag_dev : nullptr, fb);
   }
   c->stream = user;
   hipGraph_t graph = nullptr;

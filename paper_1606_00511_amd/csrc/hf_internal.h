@@ -114,11 +114,12 @@ void gemm_wgrad(const Launch& L, const GemmShape& s, const EpiArgs& e);
 void gemm_wgrad_sq(const Launch& L, const GemmShape& s, const EpiArgs& e);
 
 // ------------------------------------------------- narrow-net product
-// The cached curvature product up to the weight gradients in one launch,
-// for nets with 2 <= L <= NARROW_MAX_LAYERS, at most NARROW_MAX_INPUT inputs,
-// hidden layers at most NARROW_MAX_HIDDEN wide and at most 64 classes
-// (narrow.hip): 16 batch rows
-// per workgroup with every intermediate row in LDS.  Writes Rdelta_l
+// The cached curvature product up to the weight gradients in one launch
+// (or two: layer 1 in tiles, then the row-local rest), for nets with
+// 2 <= L <= NARROW_MAX_LAYERS, at most NARROW_MAX_INPUT inputs, hidden
+// layers at most NARROW_MAX_HIDDEN wide and at most 64 classes
+// (narrow.hip): 16 or 4 batch rows per workgroup with every intermediate
+// row in LDS.  Writes Rdelta_l
 // (l = 1..L, leading dimensions ld[l]) and, for the Hessian, RA_l
 // (l = 1..L-1), which the weight-gradient GEMMs then read.  Pointers per
 // layer index l; the cache (A_l, P, delta_l, E2_l) is that of a solve.
@@ -139,6 +140,8 @@ struct NarrowArgs {
   const float* E2[NARROW_MAX_LAYERS + 1]; // E2_l, l = 1..L-1 (Hessian)
   float* RA[NARROW_MAX_LAYERS + 1];       // out: RA_l (Hessian)
   float* RD[NARROW_MAX_LAYERS + 1];       // out: Rdelta_l
+  float* RZ1;                             // RZ_1 (B x ld[1]): the 4-row form
+                                          // writes it, then reads it
   int ldRA, ldRD;                         // their leading dimensions (0: ld[l])
   float invB;
   const int* skip;

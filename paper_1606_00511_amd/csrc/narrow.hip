@@ -328,6 +328,376 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
   }
 }
 
+// ------------------------------------------------------------------------
+// The same product in two launches, for batches whose 16-row grid would
+// leave most compute units idle: hf_narrow_layer1 (below) forms RZ_1 in
+// tiles that each read only part of V_1, and hf_narrow_product4 does the
+// rest with 4 batch rows per workgroup.  (A workgroup holding all hidden
+// units of its rows must stream all of V_1, which costs a compute unit
+// several microseconds at the 784-input widths.)  The row-local steps use
+// v4x4x1 fp32 MFMAs with the A operand broadcast to all 16 blocks: one
+// instruction multiplies the 4 rows' values at one k by 64 output columns'
+// values at that k, so a wave covers 64 columns and a run of K; the 8 waves
+// split the columns into groups of 64 and K into slices, and their partial
+// sums are added in LDS in a fixed order.
+namespace {
+
+constexpr int R4 = 4;                             // batch rows per workgroup
+constexpr int LR4 = NARROW_MAX_HIDDEN + 16;       // LDS row stride: k + 16 i
+static_assert(NT == R4 * MAXH, "one thread per (row, column) of a layer");
+// acc += sum_a x(a) b[a]: x(a) is the A operand of lanes 4a .. 4a + 3 (row
+// i = lane & 3 at k = a), b[a] this lane's column value at k = a
+#define HF_M4(a) acc = __builtin_amdgcn_mfma_f32_4x4x1f32(xa, b[a], acc, 4, a, 0);
+__device__ __forceinline__ f32x4 mfma4x16(float xa, const float (&b)[16], f32x4 acc) {
+  HF_M4(0) HF_M4(1) HF_M4(2) HF_M4(3) HF_M4(4) HF_M4(5) HF_M4(6) HF_M4(7)
+  HF_M4(8) HF_M4(9) HF_M4(10) HF_M4(11) HF_M4(12) HF_M4(13) HF_M4(14) HF_M4(15)
+  return acc;
+}
+#undef HF_M4
+
+}  // namespace
+
+extern "C" __global__ __launch_bounds__(512) void hf_narrow_product4(NarrowArgs g) {
+  if (g.skip && *g.skip) return;
+  constexpr int ML = MAXL - 1;
+  __shared__ __attribute__((aligned(16))) float sA[ML][R4][LR4];   // A_l
+  __shared__ __attribute__((aligned(16))) float sRA[2][R4][LR4];   // RA_l
+  __shared__ __attribute__((aligned(16))) float sRZ[ML][R4][LR4];  // RZ_l (H)
+  __shared__ __attribute__((aligned(16))) float sRD[2][R4][LR4];   // RZ_L, Rdelta
+  __shared__ __attribute__((aligned(16))) float sD[ML][R4][LR4];   // delta_l (H)
+  __shared__ __attribute__((aligned(16))) float sE2[ML][R4][LR4];  // E2_l (H)
+  __shared__ __attribute__((aligned(16))) float sP[R4][64];        // p
+  __shared__ __attribute__((aligned(16))) float red[NW][R4][64];   // partials
+  // the wave index in a scalar register: the loops and branches on it are
+  // uniform
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int xi = lane & 3, xk = lane >> 2;   // A operand: row, k within 16
+  const int r0 = blockIdx.x * R4;
+  const int L = g.L;
+  const int act = g.act;
+  const bool hess = g.hess != 0;
+
+  // Weight values of layer l for this lane, for the forward step (fw: W_l
+  // and V_l at [c][k], c an output column) or the backward step (W_l and
+  // V_l at [k][c]): wave (column group cg, K slice sl) takes the blocks sl
+  // and sl + nks of 16 k.  Past the layer's widths the loads read the
+  // layer's first weight, unmasked (masking the value would wait for the
+  // load): past d_k they meet the zero K padding of the LDS rows, and a
+  // column past d_n feeds only outputs that are never stored.
+  auto weights = [&](int l, bool fw, float (&bw)[2][16], float (&bv)[2][16]) {
+    const int dk = fw ? g.d[l - 1] : g.d[l], dn = fw ? g.d[l] : g.d[l - 1];
+    const int ncg = (dn + 63) >> 6, nks = NW / ncg;
+    const int cg = wave % ncg, sl = wave / ncg;
+    const int c = 64 * cg + lane;
+    const bool cv = c < dn;
+    const float* w = g.W + g.offW[l];
+    const float* vv = g.v + g.offW[l];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int a = 0; a < 16; ++a) {
+        const int k = 16 * (sl + h * nks) + a;
+        const bool kv = cv && k < dk;
+        const size_t o = kv ? (fw ? (size_t)c * dk + k : (size_t)k * dn + c) : 0;
+        bw[h][a] = w[o];
+        bv[h][a] = vv[o];
+      }
+  };
+  // the first forward and the first backward step's weights, requested
+  // with the rows below
+  float fw2[2][16], fv2[2][16], bwL[2][16], bvL[2][16];
+  weights(2, true, fw2, fv2);
+  weights(L, false, bwL, bvL);
+
+  // the workgroup's rows of the cached operands and of RZ_1, zero past B
+  // and past the layer's width (read as K padding up to the next multiple
+  // of 16); every load issued (an operand the net or the mode does not
+  // have reads X[0] instead, and its value is not used)
+  {
+    const int pr = tid / MAXH, pc = tid - pr * MAXH;   // NT = R4 * MAXH
+    const bool prv = r0 + pr < g.B;
+    const int prow = prv ? r0 + pr : 0;
+    float qa[ML], qe[ML], qd[ML], qp, qz;
+#pragma unroll
+    for (int l = 1; l <= ML; ++l) {
+      const bool has = l < L, hd = hess && l + 1 <= L;
+      const bool ok = prv && has && pc < g.d[l];
+      const bool okd = prv && hd && pc < g.d[hd ? l + 1 : 1];
+      const size_t o = ok ? (size_t)prow * g.ld[l] + pc : 0;
+      qa[l - 1] = (has ? g.A[l] : g.X)[o];
+      qe[l - 1] = (has && hess ? g.E2[l] : g.X)[o];
+      qd[l - 1] = (hd ? g.D[l + 1] : g.X)[okd ? (size_t)prow * g.ld[l + 1] + pc : 0];
+    }
+    {
+      const bool ok = prv && pc < g.d[L] && pc < 64;
+      qp = g.P[ok ? (size_t)prow * g.ld[L] + pc : 0];
+    }
+    const bool okz = prv && pc < g.d[1];
+    qz = g.RZ1[okz ? (size_t)prow * g.ld[1] + pc : 0];
+#pragma unroll
+    for (int l = 1; l <= ML; ++l) {
+      const bool ok = prv && pc < g.d[l];
+      if (l < L) sA[l - 1][pr][pc] = ok ? qa[l - 1] : 0.0f;
+      if (hess && l < L) sE2[l - 1][pr][pc] = ok ? qe[l - 1] : 0.0f;
+      if (hess && l + 1 <= L) sD[l - 1][pr][pc] = (prv && pc < g.d[l + 1]) ? qd[l - 1] : 0.0f;
+    }
+    if (pc < 64) sP[pr][pc] = (prv && pc < g.d[L]) ? qp : 0.0f;
+    // RA_1 = phi'(A_1) RZ_1
+    const float rz = okz ? qz : 0.0f;
+    const float ra = okz ? act_d1(act, qa[0]) * rz : 0.0f;
+    sRA[0][pr][pc] = ra;
+    if (hess) {
+      sRZ[0][pr][pc] = rz;
+      if (okz) g.RA[1][(size_t)prow * (g.ldRA ? g.ldRA : g.ld[1]) + pc] = ra;
+    }
+  }
+  __syncthreads();
+
+  // Cross-wave sum of the partial tiles in red (wave = slice * ncg + cg):
+  // thread (row tid / 128, column tid % 128) gets its column's total.
+  auto total = [&](int ncg, int nks, int i, int c) {
+    float s = 0.0f;
+    for (int k = 0; k < nks; ++k) s += red[k * ncg + (c >> 6)][i][c & 63];
+    return s;
+  };
+
+  // ---- layers 2 .. L: RZ_l = RA_{l-1} W_l^T + A_{l-1} V_l^T + c_l over
+  // K = d_{l-1} <= 128 (at most 8 blocks: a wave takes blocks sl, sl + nks)
+  for (int l = 2; l <= L; ++l) {
+    const int dk = g.d[l - 1], dn = g.d[l];
+    const int ncg = (dn + 63) >> 6, nks = NW / ncg;
+    const int sl = wave / ncg;
+    const int nblk = (dk + 15) >> 4;
+    float bw[2][16], bv[2][16];
+    if (l == 2) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int a = 0; a < 16; ++a) {
+          bw[h][a] = fw2[h][a];
+          bv[h][a] = fv2[h][a];
+        }
+    } else {
+      weights(l, true, bw, bv);
+    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int b = sl + h * nks;
+      if (b < nblk) {
+        acc = mfma4x16(sRA[(l - 2) & 1][xi][16 * b + xk], bw[h], acc);
+        acc = mfma4x16(sA[l - 2][xi][16 * b + xk], bv[h], acc);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc[i];
+    __syncthreads();
+    {
+      const int i = tid >> 7, cc = tid & (MAXH - 1);
+      float rz = 0.0f;
+      if (cc < dn) rz = total(ncg, nks, i, cc) + g.v[g.offB[l] + cc];
+      if (l < L) {
+        const float ra = cc < dn ? act_d1(act, sA[l - 1][i][cc]) * rz : 0.0f;
+        sRA[(l - 1) & 1][i][cc] = ra;
+        if (hess) {
+          sRZ[l - 1][i][cc] = rz;
+          if (cc < dn && r0 + i < g.B)
+            g.RA[l][(size_t)(r0 + i) * (g.ldRA ? g.ldRA : g.ld[l]) + cc] = ra;
+        }
+      } else {
+        sRD[0][i][cc] = rz;
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- output layer: Rdelta_L = p (RZ_L - p.RZ_L) / B, wave i < 4 takes
+  // row i (columns lane < C <= 64)
+  if (wave < R4) {
+    const int i = wave, C = g.d[L];
+    const bool cv = lane < C;
+    const float p = sP[i][lane];
+    const float rz = cv ? sRD[0][i][lane] : 0.0f;
+    const float dot = wave_sum(p * rz);
+    const float rd = cv ? p * (rz - dot) * g.invB : 0.0f;
+    sRD[1][i][lane] = rd;
+    if (cv && r0 + i < g.B)
+      g.RD[L][(size_t)(r0 + i) * (g.ldRD ? g.ldRD : g.ld[L]) + lane] = rd;
+  }
+  __syncthreads();
+
+  // ---- backward, l = L .. 2: Rdelta_{l-1} = (Rdelta_l W_l [+ delta_l V_l])
+  // phi'(A_{l-1}) [+ E2_{l-1} RZ_{l-1}] over K = d_l
+  int cur = 1;
+  for (int l = L; l >= 2; --l) {
+    const int dk = g.d[l], dn = g.d[l - 1];
+    const int ncg = (dn + 63) >> 6, nks = NW / ncg;
+    const int sl = wave / ncg;
+    const int nblk = (dk + 15) >> 4;
+    float bw[2][16], bv[2][16];
+    if (l == L) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int a = 0; a < 16; ++a) {
+          bw[h][a] = bwL[h][a];
+          bv[h][a] = bvL[h][a];
+        }
+    } else {
+      weights(l, false, bw, bv);
+    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int b = sl + h * nks;
+      if (b < nblk) {
+        acc = mfma4x16(sRD[cur][xi][16 * b + xk], bw[h], acc);
+        if (hess) acc = mfma4x16(sD[l - 2][xi][16 * b + xk], bv[h], acc);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc[i];
+    __syncthreads();
+    {
+      const int i = tid >> 7, cc = tid & (MAXH - 1);
+      float rd = 0.0f;
+      if (cc < dn) {
+        rd = total(ncg, nks, i, cc) * act_d1(act, sA[l - 2][i][cc]);
+        if (hess) rd += sE2[l - 2][i][cc] * sRZ[l - 2][i][cc];
+        if (r0 + i < g.B)
+          g.RD[l - 1][(size_t)(r0 + i) * (g.ldRD ? g.ldRD : g.ld[l - 1]) + cc] = rd;
+      }
+      sRD[cur ^ 1][i][cc] = rd;
+    }
+    __syncthreads();
+    cur ^= 1;
+  }
+}
+
+// ------------------------------------------------------------------------
+// Layer 1 of the narrow product on its own: RZ_1 = X V_1^T + c_1 in tiles
+// of 16 batch rows x 32 hidden units, so that a workgroup streams only its
+// 32 rows of V_1 (a workgroup holding all hidden units of its rows would
+// stream all of V_1).  Four waves split K into quarters of whole 16-blocks
+// and add their partial tiles in LDS in a fixed order.  v16x16x4 fp32
+// MFMAs, the K order within a block of 16 permuted identically for both
+// operands; 16-byte loads (the host checks d_0 % 4 == 0 and the 16-byte
+// alignment of X and v).
+namespace {
+constexpr int T1R = 16, T1C = 32;                 // tile: rows x hidden units
+constexpr int NT1 = 256;
+constexpr int U1 = 4;                             // 16-blocks per load stage
+}  // namespace
+
+extern "C" __global__ __launch_bounds__(256) void hf_narrow_layer1(
+    const float* __restrict__ X, const float* __restrict__ v, int B, int d0,
+    int d1, long long offW1, long long offB1, float* __restrict__ rz, int ldrz,
+    const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  __shared__ f32x4 red[4][2][64];                  // per wave, subtile, lane
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int i16 = lane & 15, g16 = lane >> 4;
+  const int r0 = blockIdx.x * T1R, n0 = blockIdx.y * T1C;
+  // a row past B or a hidden unit past d_1 reads row 0: it feeds only
+  // outputs that are never stored
+  const int xr = r0 + i16 < B ? r0 + i16 : 0;
+  const float* xp = X + (size_t)xr * d0 + 4 * g16;
+  const float* vp[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int n = n0 + 16 * s + i16;
+    vp[s] = v + offW1 + (size_t)(n < d1 ? n : 0) * d0 + 4 * g16;
+  }
+  const int nblk = (d0 + 15) >> 4, nfull = d0 >> 4;
+  const int b0 = wave * nblk / 4, b1 = (wave + 1) * nblk / 4;
+  const int fe = b1 < nfull ? b1 : nfull;          // full blocks [b0, fe)
+  f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  auto mma = [&](const f32x4& a, const f32x4& b0v, const f32x4& b1v) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[q], b0v[q], acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[q], b1v[q], acc[1], 0, 0, 0);
+    }
+  };
+  // stages of U1 full blocks: the next stage's loads are issued before the
+  // current stage's MFMAs, with no branch around them
+  const int nst = fe > b0 ? (fe - b0) / U1 : 0;
+  f32x4 xa[U1], va[U1][2];
+  auto load = [&](int bb, f32x4 (&x)[U1], f32x4 (&w)[U1][2]) {
+#pragma unroll
+    for (int u = 0; u < U1; ++u) {
+      x[u] = *(const f32x4*)(xp + 16 * (bb + u));
+      w[u][0] = *(const f32x4*)(vp[0] + 16 * (bb + u));
+      w[u][1] = *(const f32x4*)(vp[1] + 16 * (bb + u));
+    }
+  };
+  if (nst > 0) load(b0, xa, va);
+  for (int st = 0; st < nst; ++st) {
+    // the last stage reloads itself (in bounds, unused)
+    const int nb = b0 + (st + 1 < nst ? st + 1 : st) * U1;
+    f32x4 xn[U1], vn[U1][2];
+    load(nb, xn, vn);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U1; ++u) mma(xa[u], va[u][0], va[u][1]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U1; ++u) {
+      xa[u] = xn[u];
+      va[u][0] = vn[u][0];
+      va[u][1] = vn[u][1];
+    }
+  }
+  // the remaining full blocks (fewer than U1), their loads issued together
+  const int bb = b0 + nst * U1;
+  if (bb < fe) {
+    f32x4 xr2[U1], vr2[U1][2];
+#pragma unroll
+    for (int u = 0; u < U1; ++u) {
+      const int b = bb + u < fe ? bb + u : bb;
+      xr2[u] = *(const f32x4*)(xp + 16 * b);
+      vr2[u][0] = *(const f32x4*)(vp[0] + 16 * b);
+      vr2[u][1] = *(const f32x4*)(vp[1] + 16 * b);
+    }
+#pragma unroll
+    for (int u = 0; u < U1; ++u)
+      if (bb + u < fe) mma(xr2[u], vr2[u][0], vr2[u][1]);
+  }
+  // the ragged last block (d_0 % 16 != 0), in this wave's range: float4s
+  // past d_0 are zero
+  if (nfull < nblk && nfull >= b0 && nfull < b1) {
+    const int k = 16 * nfull + 4 * g16;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    const bool kv = k < d0;
+    const f32x4 a = kv ? *(const f32x4*)(xp + 16 * nfull) : z;
+    const f32x4 w0 = kv ? *(const f32x4*)(vp[0] + 16 * nfull) : z;
+    const f32x4 w1 = kv ? *(const f32x4*)(vp[1] + 16 * nfull) : z;
+    mma(a, w0, w1);
+  }
+  red[wave][0][lane] = acc[0];
+  red[wave][1][lane] = acc[1];
+  __syncthreads();
+  // lane (i16, g16) of a subtile holds rows 4 g16 .. 4 g16 + 3 of column
+  // i16; thread t adds the four waves' values of subtile t / 64 (fixed order)
+  if (tid < 128) {
+    const int s = tid >> 6, l = tid & 63;
+    const int n = n0 + 16 * s + (l & 15);
+    f32x4 t = red[0][s][l];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) t += red[w][s][l];
+    if (n < d1) {
+      const float cb = v[offB1 + n];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = r0 + 4 * (l >> 4) + r;
+        if (row < B) rz[(size_t)row * ldrz + n] = t[r] + cb;
+      }
+    }
+  }
+}
+
 // out[i] for parameter i: a weight of layer l at (m, k) is the diagonal
 // block's element (roff[l] + m, yoff[l - 1] + k), a bias of layer l its row
 // roff[l] + m; both summed over the splits in split order (fp64).  With dpart
@@ -343,17 +713,19 @@ extern "C" __global__ __launch_bounds__(256) void hf_narrow_scatter(
   if (dpart && j < 0 && blockIdx.x == 0 && threadIdx.x == 0)
     st->jc = st->done ? -1 : st->jn;
   if (skip && *skip) return;
+  // (a narrow net has far fewer than 2^31 parameters: 32-bit index
+  // arithmetic)
   const size_t mn = (size_t)nc.M * nc.N;
+  const int n = (int)nc.n;
   double pq = 0.0, pp = 0.0;
-  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < nc.n;
-       i += (long long)gridDim.x * 256) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) {
     int l = 1;
-    while (l < nc.L && i >= nc.offW[l + 1]) ++l;
+    while (l < nc.L && i >= (int)nc.offW[l + 1]) ++l;
     double t = 0.0;
-    if (i < nc.offB[l]) {
-      const long long loc = i - nc.offW[l];
+    if (i < (int)nc.offB[l]) {
+      const int loc = i - (int)nc.offW[l];
       const int dk = nc.d[l - 1];
-      const int m = (int)(loc / dk), k = (int)(loc - (long long)m * dk);
+      const int m = loc / dk, k = loc - m * dk;
       const float* src = part + (size_t)(nc.roff[l] + m) * nc.N + nc.yoff[l - 1] + k;
       for (int z0 = 0; z0 < S; z0 += 8) {
         float v[8];
@@ -364,7 +736,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_narrow_scatter(
           if (z0 + z < S) t += (double)v[z];
       }
     } else {
-      const int m = (int)(i - nc.offB[l]);
+      const int m = i - (int)nc.offB[l];
       for (int z = 0; z < S; ++z) t += bpart[(size_t)z * nc.M + nc.roff[l] + m];
     }
     const float q = (float)t;
@@ -441,15 +813,31 @@ bool narrow_eligible(int L, const int* d, const float* X, const float* v) {
 }
 
 void narrow_product(const Launch& Lc, const NarrowArgs& a) {
-  const int nb = (a.B + RW - 1) / RW;
+  // 16-row workgroups once they alone cover the compute units; below that
+  // the layer-1 tiles and the 4-row workgroups
+  const bool four = (a.B + RW - 1) / RW < 256;
   // algorithmic work: the GEMM flops of the replaced passes
-  double fl = 2.0 * a.B * a.d[0] * a.d[1];
+  const double f1 = 2.0 * a.B * a.d[0] * a.d[1];
+  double fr = 0.0;
   for (int l = 2; l <= a.L; ++l)
-    fl += 2.0 * a.B * a.d[l - 1] * a.d[l] * (a.hess ? 4.0 : 3.0);
-  prof_begin(Lc, "hf_narrow_product");
-  hipExtLaunchKernelGGL(hf_narrow_product, dim3(nb), dim3(NT), 0, Lc.stream,
-                        prof_a(Lc), prof_b(Lc), 0, a);
-  prof_end(Lc, "hf_narrow_product", fl, 4.0 * a.B * (a.d[0] + 4.0 * a.d[1]));
+    fr += 2.0 * a.B * a.d[l - 1] * a.d[l] * (a.hess ? 4.0 : 3.0);
+  if (four) {
+    const dim3 g1((unsigned)((a.B + T1R - 1) / T1R), (unsigned)((a.d[1] + T1C - 1) / T1C));
+    prof_begin(Lc, "hf_narrow_layer1");
+    hipExtLaunchKernelGGL(hf_narrow_layer1, g1, dim3(NT1), 0, Lc.stream, prof_a(Lc),
+                          prof_b(Lc), 0, a.X, a.v, a.B, a.d[0], a.d[1], a.offW[1], a.offB[1],
+                          a.RZ1, a.ld[1], a.skip);
+    prof_end(Lc, "hf_narrow_layer1", f1, 4.0 * a.B * (a.d[0] + a.d[1]));
+    prof_begin(Lc, "hf_narrow_product4");
+    hipExtLaunchKernelGGL(hf_narrow_product4, dim3((unsigned)((a.B + R4 - 1) / R4)), dim3(NT),
+                          0, Lc.stream, prof_a(Lc), prof_b(Lc), 0, a);
+    prof_end(Lc, "hf_narrow_product4", fr, 4.0 * a.B * 5.0 * a.d[1]);
+  } else {
+    prof_begin(Lc, "hf_narrow_product");
+    hipExtLaunchKernelGGL(hf_narrow_product, dim3((unsigned)((a.B + RW - 1) / RW)), dim3(NT), 0,
+                          Lc.stream, prof_a(Lc), prof_b(Lc), 0, a);
+    prof_end(Lc, "hf_narrow_product", f1 + fr, 4.0 * a.B * (a.d[0] + 4.0 * a.d[1]));
+  }
 }
 
 }  // namespace hfk

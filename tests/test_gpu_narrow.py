@@ -1,6 +1,6 @@
 """GPU parity of the narrow-net product (one launch up to the weight
-gradients: 16 batch rows per workgroup, every hidden unit of those rows in
-LDS), through the C ABI, against the fp64 oracle.
+gradients: 4 or 16 batch rows per workgroup, every hidden unit of those rows
+in LDS), through the C ABI, against the fp64 oracle.
 
 The kernel serves nets with 2 to 4 weight layers, hidden layers at most 128
 wide and at most 64 classes, at batches where the first layer's GEMM would
@@ -10,7 +10,8 @@ fp32 products: rel-L2 <= 1e-4 (ReLU with the per-unit bracket), CG counts,
 the detection iteration and the sign of kappa exact.  Shapes: the widest
 admitted layers (128 hidden, 64 classes), widths and batches that are not
 multiples of 16 (the kernel's row and column blocks), one row, and 2, 3 and
-4 weight layers.  The profiler confirms the kernel ran.
+4 weight layers.  Batches below 4,096 rows take the 4-row kernel, larger
+ones the 16-row kernel; the profiler confirms which ran.
 """
 
 import numpy as np
@@ -31,7 +32,13 @@ CASES = [
     ((32, 128, 128, 128, 64), "tanh", 50),
     ((20, 16, 12, 5), "sigmoid", 1),
     ((48, 100, 3), "relu", 130),
+    ((64, 100, 10), "sigmoid", 4100),
 ]
+CG_CASES = CASES[:4] + CASES[-1:]
+
+
+def kernel_for(B):
+    return "hf_narrow_product4" if (B + 15) // 16 < 256 else "hf_narrow_product"
 
 
 def dev(a):
@@ -62,7 +69,7 @@ def test_narrow_product(case, mode):
     out = host(net.hf_hvp(W, X, y, v, mode))
     stats = net.prof_stats()
     net.prof_enable(False)
-    assert "hf_narrow_product" in stats, sorted(stats)
+    assert kernel_for(B) in stats, sorted(stats)
     ref = O.curvature(dims, act, p["theta"], p["X"], p["y"], p["v"], mode)
     err, bound = check(out, ref, act, lambda k: O.curvature(
         dims, act, p["theta"], p["X"], p["y"], p["v"], mode, kink=k),
@@ -72,7 +79,7 @@ def test_narrow_product(case, mode):
 
 
 @pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
-@pytest.mark.parametrize("case", CASES[:4], ids=[sid(c) for c in CASES[:4]])
+@pytest.mark.parametrize("case", CG_CASES, ids=[sid(c) for c in CG_CASES])
 def test_narrow_cg(case, mode):
     """CG on the narrow product: counts, detection and kappa's sign exact;
     the lock-step trace compares every product with the oracle's A p_j."""
@@ -118,6 +125,6 @@ def test_narrow_not_taken_outside_its_shapes():
         out = net.hf_hvp(dev(p["theta"]), dev(p["X"]), dev(p["y"]), dev(p["v"]),
                          "hessian")
         host(out)
-        assert "hf_narrow_product" not in net.prof_stats(), dims
+        assert not any(k.startswith("hf_narrow_product") for k in net.prof_stats()), dims
         net.prof_enable(False)
         net.close()
