@@ -111,7 +111,7 @@ def cpu_model():
     return None
 
 
-def cpu_baseline(w, inp, rows, min_s=12.0, max_pairs=3):
+def cpu_baseline(w, inp, rows, min_s=12.0, max_pairs=1000):
     """The fp64 oracle timed on this host's cores on a bounded sample: pairs
     of one H v and one G v on the first `rows` rows, repeated until at least
     min_s seconds have passed (at most max_pairs pairs), scaled to the full
@@ -147,7 +147,7 @@ def cpu_baseline(w, inp, rows, min_s=12.0, max_pairs=3):
     return {"value": 1.0 / per_product, "unit": "curvature-vector products/s",
             "cores": cores, "kind": "oracle", "cpu_model": cpu_model(),
             "host_cpus": len(os.sched_getaffinity(0)), "blas": blas,
-            "sample": "fp64 NumPy oracle, %d x (one Hv and one Gv) on %s (%.1f s measured)"
+            "sample": "fp64 NumPy oracle, %d x (one Hv and one Gv) on %s (%.2f s measured)"
                       % (pairs, what, elapsed)}
 
 

@@ -62,34 +62,77 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
   __shared__ __attribute__((aligned(16))) float sRZ[MAXL - 1][RW][LDR];  // RZ_l (H)
   __shared__ __attribute__((aligned(16))) float sRD[2][RW][LDR];         // RZ_L, Rdelta
   __shared__ __attribute__((aligned(16))) float sX[RW][LDX];             // X rows
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index in a scalar register: the loops and branches on it are
+  // uniform
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int i16 = lane & 15, g16 = lane >> 4;
   const int r0 = blockIdx.x * RW;
   const int L = g.L;
   const int act = g.act;
   const bool hess = g.hess != 0;
+  const int d0 = g.d[0], d1 = g.d[1];
 
-  // the cached activations of this workgroup's rows, zero past B and past
-  // d_l (columns up to MAXH are read as the next layer's K padding)
-  for (int l = 1; l < L; ++l) {
-    const float* A = g.A[l];
-    const int dl = g.d[l], ldl = g.ld[l];
-    for (int e = tid; e < RW * MAXH; e += NT) {
-      const int r = e / MAXH, c = e - r * MAXH;
-      sA[l - 1][r][c] = (r0 + r < g.B && c < dl) ? A[(size_t)(r0 + r) * ldl + c] : 0.0f;
+  // Layer 1's slots of V_1 (below) are requested first, then the rows of
+  // the cached activations and of X; every load is issued before any is
+  // used (a clamped index where the value is not wanted), so the workgroup
+  // waits on memory once.
+  const int n0 = 16 * wave;
+  const bool l1 = n0 < d1;                       // this wave has layer-1 columns
+  const int nfull = d0 >> 4;
+  // a column past d_1 reads column 0's row: it feeds only outputs that are
+  // never stored
+  const float* vp = g.v + g.offW[1] + (size_t)(n0 + i16 < d1 ? n0 + i16 : 0) * d0 + 4 * g16;
+  constexpr int U = 8;                           // K blocks in flight
+  f32x4 vs[U];
+  auto vload = [&](int b, int u) {
+    vs[u] = *(const f32x4*)(vp + 16 * (b < nfull ? b : nfull - 1));
+  };
+  if (l1 && nfull > 0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      vload(u, u);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
-
-  // the workgroup's rows of X, read once (the waves share them), with
-  // zeros past B and from d_0 to the next multiple of 16
   {
-    const int d0 = g.d[0];
-    const int q4 = (d0 + 15) >> 2 & ~3;    // float4s per row, K padded to 16
-    for (int e = tid; e < RW * q4; e += NT) {
-      const int r = e / q4, c = 4 * (e - r * q4);
-      f32x4 x = {0.f, 0.f, 0.f, 0.f};
-      if (r0 + r < g.B && c < d0) x = *(const f32x4*)(g.X + (size_t)(r0 + r) * d0 + c);
-      *(f32x4*)&sX[r][c] = x;
+    // the cached activations of this workgroup's rows, zero past B and past
+    // d_l (columns up to MAXH are read as the next layer's K padding)
+    constexpr int PE = RW * MAXH / NT;           // elements per thread and layer
+    float qa[MAXL - 1][PE];
+#pragma unroll
+    for (int l = 1; l < MAXL; ++l)
+#pragma unroll
+      for (int j = 0; j < PE; ++j) {
+        const int e = tid + NT * j, r = e / MAXH, c = e - r * MAXH;
+        const bool ok = l < L && r0 + r < g.B && c < g.d[l < L ? l : 1];
+        qa[l - 1][j] = (l < L ? g.A[l] : g.X)[ok ? (size_t)(r0 + r) * g.ld[l] + c : 0];
+      }
+    // the workgroup's rows of X, read once (the waves share them), with
+    // zeros past B and from d_0 to the next multiple of 16: at most
+    // RW * NARROW_MAX_INPUT / 4 = 8 NT float4s
+    constexpr int PX = RW * NARROW_MAX_INPUT / 4 / NT;
+    const int q4 = (d0 + 15) >> 2 & ~3;          // float4s per row, K padded to 16
+    f32x4 qx[PX];
+#pragma unroll
+    for (int j = 0; j < PX; ++j) {
+      const int e = tid + NT * j, r = e / q4, c = 4 * (e - r * q4);
+      const bool ok = e < RW * q4 && r0 + r < g.B && c < d0;
+      qx[j] = *(const f32x4*)(g.X + (ok ? (size_t)(r0 + r) * d0 + c : 0));
+    }
+#pragma unroll
+    for (int l = 1; l < MAXL; ++l)
+#pragma unroll
+      for (int j = 0; j < PE; ++j) {
+        const int e = tid + NT * j, r = e / MAXH, c = e - r * MAXH;
+        const bool ok = l < L && r0 + r < g.B && c < g.d[l < L ? l : 1];
+        if (l < L) sA[l - 1][r][c] = ok ? qa[l - 1][j] : 0.0f;
+      }
+#pragma unroll
+    for (int j = 0; j < PX; ++j) {
+      const int e = tid + NT * j, r = e / q4, c = 4 * (e - r * q4);
+      const bool ok = e < RW * q4 && r0 + r < g.B && c < d0;
+      if (e < RW * q4) *(f32x4*)&sX[r][c] = ok ? qx[j] : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   }
   __syncthreads();
@@ -98,63 +141,29 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
   // host checks d_0 % 4 == 0, d_0 <= NARROW_MAX_INPUT and 16-byte alignment
   // of X and v)
   {
-    const int d0 = g.d[0], d1 = g.d[1];
-    const int n0 = 16 * wave;
     f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
-    if (n0 < d1) {
-      const bool vr = n0 + i16 < d1;
+    if (l1) {
       const float* xs = &sX[i16][4 * g16];
-      const float* vp = g.v + g.offW[1] + (size_t)(vr ? n0 + i16 : 0) * d0 + 4 * g16;
-      // Full K blocks of v in stages of U blocks: the next stage's U loads
-      // are issued before the current stage's 4U MFMAs, with no branch
-      // around them, so that the MFMAs wait only for their own stage.  A
-      // column past d_1 reads column 0's row instead: it feeds only outputs
-      // that are never stored.  X comes from LDS.
-      const int nfull = d0 >> 4;
-      constexpr int U = 8;
-      const int nst = nfull / U;
-      f32x4 va[U];
-      auto load = [&](int b0, f32x4 (&w)[U]) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) w[u] = *(const f32x4*)(vp + 16 * (b0 + u));
-      };
-      if (nst > 0) load(0, va);
-      for (int st = 0; st < nst; ++st) {
-        // the last stage reloads itself (in bounds, unused)
-        const int nb = (st + 1 < nst ? st + 1 : st) * U;
-        f32x4 vn[U];
-        load(nb, vn);
-        // keep the scheduler from sinking these loads to their uses
-        __builtin_amdgcn_sched_barrier(0);
+      // The full K blocks, U in flight: slot u holds block t0 + u and, once
+      // its MFMAs have read it, is reloaded with block t0 + u + U (the last
+      // full block again past the end: in bounds, unused).  No branch
+      // around the loads and no copy between registers (either would make
+      // the compiler wait for loads in flight).  X comes from LDS.
+      for (int t0 = 0; t0 < nfull; t0 += U) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-          const f32x4 xa = *(const f32x4*)(xs + 16 * (st * U + u));
+          if (t0 + u < nfull) {
+            const f32x4 xa = *(const f32x4*)(xs + 16 * (t0 + u));
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if (u & 1) acc1 = mfma16(xa[q], va[u][q], acc1);
-            else acc0 = mfma16(xa[q], va[u][q], acc0);
+            for (int q = 0; q < 4; ++q) {
+              if (u & 1) acc1 = mfma16(xa[q], vs[u][q], acc1);
+              else acc0 = mfma16(xa[q], vs[u][q], acc0);
+            }
           }
+          __builtin_amdgcn_sched_barrier(0);
+          vload(t0 + u + U, u);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int u = 0; u < U; ++u) va[u] = vn[u];
-      }
-      // the remaining full blocks, their loads issued together
-      {
-        const int b0 = nst * U;
-        f32x4 vr2[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int b = b0 + u < nfull ? b0 + u : 0;
-          vr2[u] = *(const f32x4*)(vp + 16 * b);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-          if (b0 + u < nfull) {
-            const f32x4 xa = *(const f32x4*)(xs + 16 * (b0 + u));
-#pragma unroll
-            for (int q = 0; q < 4; ++q) acc0 = mfma16(xa[q], vr2[u][q], acc0);
-          }
       }
       const int k0 = nfull << 4;
       if (k0 < d0) {     // ragged last block: LDS holds zeros past d_0
@@ -199,7 +208,9 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
       const bool nv = n < dn;
       const float* wrow = g.W + g.offW[l] + (size_t)(nv ? n : 0) * dk;
       const float* vrow = g.v + g.offW[l] + (size_t)(nv ? n : 0) * dk;
-      // every weight value this lane feeds, loaded before the first MFMA
+      // every weight value this lane feeds, loaded before the first MFMA;
+      // past d_{l-1} the loads read the row's first weight, unmasked (the A
+      // operands are zero there up to the block's end)
       constexpr int NB = MAXH / 16;
       float bw[NB][4], bv[NB][4];
 #pragma unroll
@@ -207,9 +218,9 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int k = 16 * b + 4 * g16 + q;
-          const bool kv = nv && k < dk;
-          bw[b][q] = kv ? wrow[k] : 0.0f;
-          bv[b][q] = kv ? vrow[k] : 0.0f;
+          const int kc = k < dk ? k : 0;
+          bw[b][q] = wrow[kc];
+          bv[b][q] = vrow[kc];
         }
       f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
 #pragma unroll
@@ -283,18 +294,24 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
       const float* vcol = g.v + g.offW[l] + (nv ? n : 0);
       const bool dr = r0 + i16 < g.B;
       const float* drow = hess ? g.D[l] + (size_t)(dr ? r0 + i16 : 0) * g.ld[l] : nullptr;
-      // every weight (and delta_l) value this lane feeds, loaded first
+      // every weight (and delta_l) value this lane feeds, loaded first;
+      // past d_l the weight loads read the column's first weight, unmasked
+      // (Rdelta_l is zero there up to the block's end), and delta_l is
+      // masked to zero (its partner, V_l, is not)
       constexpr int NB = MAXH / 16;
       float bw[NB][4], bv[NB][4], ad[NB][4];
+      const float* dsrc = hess ? drow : wcol;
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int k = 16 * b + 4 * g16 + q;
           const bool kv = k < dk;
-          bw[b][q] = (kv && nv) ? wcol[(size_t)k * dn] : 0.0f;
-          bv[b][q] = (hess && kv && nv) ? vcol[(size_t)k * dn] : 0.0f;
-          ad[b][q] = (hess && kv && dr) ? drow[k] : 0.0f;
+          const size_t kc = kv ? (size_t)k * dn : 0;
+          bw[b][q] = wcol[kc];
+          bv[b][q] = vcol[kc];
+          const float dv = dsrc[kv && dr ? k : 0];
+          ad[b][q] = hess && kv && dr ? dv : 0.0f;
         }
       f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
 #pragma unroll
@@ -329,8 +346,8 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product(NarrowArgs g
 }
 
 // ------------------------------------------------------------------------
-// The same product in two launches, for batches whose 16-row grid would
-// leave most compute units idle: hf_narrow_layer1 (below) forms RZ_1 in
+// The same product in two launches, for batches whose 16-row grid leaves
+// most compute units idle: hf_narrow_layer1 (below) forms RZ_1 in
 // tiles that each read only part of V_1, and hf_narrow_product4 does the
 // rest with 4 batch rows per workgroup.  (A workgroup holding all hidden
 // units of its rows must stream all of V_1, which costs a compute unit
@@ -621,49 +638,35 @@ extern "C" __global__ __launch_bounds__(256) void hf_narrow_layer1(
       acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[q], b1v[q], acc[1], 0, 0, 0);
     }
   };
-  // stages of U1 full blocks: the next stage's loads are issued before the
-  // current stage's MFMAs, with no branch around them
-  const int nst = fe > b0 ? (fe - b0) / U1 : 0;
-  f32x4 xa[U1], va[U1][2];
-  auto load = [&](int bb, f32x4 (&x)[U1], f32x4 (&w)[U1][2]) {
+  // the full blocks [b0, fe), U1 of them in flight: slot u holds block
+  // t0 + u and, once its MFMAs have read it, is reloaded with block
+  // t0 + u + U1 (the last full block again past the end: in bounds,
+  // unused).  No branch around the loads and no copy between registers
+  // (either would make the compiler wait for loads in flight).
+  if (fe > b0) {
+    f32x4 xs[U1], ws[U1][2];
+    auto load = [&](int b, int u) {
+      const int bb = b < fe ? b : fe - 1;
+      xs[u] = *(const f32x4*)(xp + 16 * bb);
+      ws[u][0] = *(const f32x4*)(vp[0] + 16 * bb);
+      ws[u][1] = *(const f32x4*)(vp[1] + 16 * bb);
+    };
+    // (issued in slot order, as in the loop: the compiler's wait for the
+    // oldest slot then covers both ways into the loop)
 #pragma unroll
     for (int u = 0; u < U1; ++u) {
-      x[u] = *(const f32x4*)(xp + 16 * (bb + u));
-      w[u][0] = *(const f32x4*)(vp[0] + 16 * (bb + u));
-      w[u][1] = *(const f32x4*)(vp[1] + 16 * (bb + u));
+      load(b0 + u, u);
+      __builtin_amdgcn_sched_barrier(0);
     }
-  };
-  if (nst > 0) load(b0, xa, va);
-  for (int st = 0; st < nst; ++st) {
-    // the last stage reloads itself (in bounds, unused)
-    const int nb = b0 + (st + 1 < nst ? st + 1 : st) * U1;
-    f32x4 xn[U1], vn[U1][2];
-    load(nb, xn, vn);
-    __builtin_amdgcn_sched_barrier(0);
+    for (int t0 = b0; t0 < fe; t0 += U1) {
 #pragma unroll
-    for (int u = 0; u < U1; ++u) mma(xa[u], va[u][0], va[u][1]);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int u = 0; u < U1; ++u) {
-      xa[u] = xn[u];
-      va[u][0] = vn[u][0];
-      va[u][1] = vn[u][1];
+      for (int u = 0; u < U1; ++u) {
+        if (t0 + u < fe) mma(xs[u], ws[u][0], ws[u][1]);
+        __builtin_amdgcn_sched_barrier(0);
+        load(t0 + u + U1, u);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-  }
-  // the remaining full blocks (fewer than U1), their loads issued together
-  const int bb = b0 + nst * U1;
-  if (bb < fe) {
-    f32x4 xr2[U1], vr2[U1][2];
-#pragma unroll
-    for (int u = 0; u < U1; ++u) {
-      const int b = bb + u < fe ? bb + u : bb;
-      xr2[u] = *(const f32x4*)(xp + 16 * b);
-      vr2[u][0] = *(const f32x4*)(vp[0] + 16 * b);
-      vr2[u][1] = *(const f32x4*)(vp[1] + 16 * b);
-    }
-#pragma unroll
-    for (int u = 0; u < U1; ++u)
-      if (bb + u < fe) mma(xr2[u], vr2[u][0], vr2[u][1]);
   }
   // the ragged last block (d_0 % 16 != 0), in this wave's range: float4s
   // past d_0 are zero
@@ -813,9 +816,11 @@ bool narrow_eligible(int L, const int* d, const float* X, const float* v) {
 }
 
 void narrow_product(const Launch& Lc, const NarrowArgs& a) {
-  // 16-row workgroups once they alone cover the compute units; below that
-  // the layer-1 tiles and the 4-row workgroups
-  const bool four = (a.B + RW - 1) / RW < 256;
+  // The layer-1 tiles and the 4-row workgroups up to 64 workgroups of 16
+  // rows, the 16-row form above: CG on G measured 10-15% faster on each
+  // side of the switch (nets 784-100-10, 784-128-64 and 256-64-64-10 at
+  // 500 to 8,000 rows; the forms meet between 1,000 and 1,500 rows).
+  const bool four = (a.B + RW - 1) / RW <= 64;
   // algorithmic work: the GEMM flops of the replaced passes
   const double f1 = 2.0 * a.B * a.d[0] * a.d[1];
   double fr = 0.0;

@@ -10,8 +10,9 @@ fp32 products: rel-L2 <= 1e-4 (ReLU with the per-unit bracket), CG counts,
 the detection iteration and the sign of kappa exact.  Shapes: the widest
 admitted layers (128 hidden, 64 classes), widths and batches that are not
 multiples of 16 (the kernel's row and column blocks), one row, and 2, 3 and
-4 weight layers.  Batches below 4,096 rows take the 4-row kernel, larger
-ones the 16-row kernel; the profiler confirms which ran.
+4 weight layers.  Batches up to 1,024 rows take the layer-1 tiles and the
+4-row kernel, larger ones the 16-row kernel; the profiler confirms which
+ran.
 """
 
 import numpy as np
@@ -33,12 +34,13 @@ CASES = [
     ((20, 16, 12, 5), "sigmoid", 1),
     ((48, 100, 3), "relu", 130),
     ((64, 100, 10), "sigmoid", 4100),
+    ((96, 40, 30, 17), "tanh", 1100),
 ]
-CG_CASES = CASES[:4] + CASES[-1:]
+CG_CASES = CASES[:4] + CASES[-2:]
 
 
 def kernel_for(B):
-    return "hf_narrow_product4" if (B + 15) // 16 < 256 else "hf_narrow_product"
+    return "hf_narrow_product4" if (B + 15) // 16 <= 64 else "hf_narrow_product"
 
 
 def dev(a):
