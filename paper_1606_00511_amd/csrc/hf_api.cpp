@@ -1084,14 +1084,65 @@ void narrow_cache(hf_ctx* c, const float* X, int B, bool hess) {
   c->cat_hess = hess;
 }
 
+// Whether the cache of a narrow net is built by the narrow kernels: the
+// products that follow must take the two-launch narrow form (every vector
+// they multiply is aligned: the solvers' own, or v_ext, the caller's x0 or
+// v, which may be null), since the narrow build leaves the transposed weights
+// of the GEMM path unwritten.
+bool narrow_build_ok(const hf_ctx* c, const float* X, const float* v_ext, int B) {
+  return c->narrow_cat && B <= c->Bws && narrow_eligible(c->L, c->d.data(), X, v_ext) &&
+         narrow_eligible(c->L, c->d.data(), nullptr, c->F(c->oPv)) &&
+         gemm_tile(B, c->d[1], c->d[0]) == 64 && (B + 15) / 16 <= 64;
+}
+
+void narrow_build(hf_ctx* c, const float* W, const float* X, int B,
+                  const int32_t* y, bool hess) {
+  const int L = c->L;
+  c->cat_B = -1;
+  NarrowFwdArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.L = L;
+  a.B = B;
+  a.act = c->act;
+  a.hess = hess ? 1 : 0;
+  for (int l = 0; l <= L; ++l) {
+    a.d[l] = c->d[l];
+    a.ld[l] = l == 0 ? c->d[0] : c->ld[l];
+    a.offW[l] = l == 0 ? 0 : (long long)c->offW[l];
+    a.offB[l] = l == 0 ? 0 : (long long)c->offB[l];
+    if (l >= 1 && l < L) {
+      a.A[l] = c->F(c->oA[l]);
+      a.E2[l] = c->F(c->oE2[l]);
+    }
+    if (l >= 2) a.D[l] = c->F(c->oD[l]);
+    a.yoff[l] = c->yoff[l];
+    a.roff[l] = c->roff[l];
+  }
+  a.X = X;
+  a.W = W;
+  a.y = hess ? y : nullptr;
+  a.P = c->F(c->oP);
+  a.Ycat = c->F(c->oYcat);
+  a.ldy = c->ldy_cat;
+  a.Dcat = hess ? c->F(c->oDcat) : nullptr;
+  a.ldr = c->ldr_cat;
+  a.invB = 1.0f / (float)B;
+  a.err = c->errp();
+  narrow_forward(c->launch(), a);
+  c->cat_B = B;
+  c->cat_hess = hess;
+}
+
 // The cache of a solve on the curvature batch: forward pass, p and, for the
 // Hessian, delta_l and (delta_l W_l) phi''(A_{l-1}).
 void build_cache(hf_ctx* c, const float* W, const float* X, int B,
-                 const int32_t* y, bool hess) {
+                 const int32_t* y, bool hess, const float* v_ext = nullptr) {
   if (c->bf16()) {
     forward_plain_h(c, W, X, B, hess ? y : nullptr, hess);
     if (hess)
       for (int l = c->L; l >= 2; --l) backward_data_h(c, l, B, true);
+  } else if (narrow_build_ok(c, X, v_ext, B)) {
+    narrow_build(c, W, X, B, y, hess);
   } else {
     forward_plain(c, W, X, B, hess ? y : nullptr, hess);
     if (hess)
@@ -1303,7 +1354,7 @@ int solve_cg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   float* q = c->F(c->oQ);
 
   // cache of the curvature batch: activations, p, delta_l, E2_l
-  build_cache(c, W, Xc, b, yc, hess);
+  build_cache(c, W, Xc, b, yc, hess, x0);
   // a warm start's residual needs one product on the cache
   const int k0 = x0 ? 1 : 0;
   if (x0) {
@@ -1418,7 +1469,7 @@ int solve_bicg(hf_ctx* c, const float* W, const float* Xc, const int32_t* yc,
   float* ph = minv ? c->F(c->oPh) : p;
   float* sh = minv ? c->F(c->oSh) : sv;
 
-  build_cache(c, W, Xc, b, yc, hess);
+  build_cache(c, W, Xc, b, yc, hess, x0);
   // a warm start's residual needs one product on the cache
   const int k0 = x0 ? 1 : 0;
   if (x0) {
@@ -1499,7 +1550,7 @@ void hvp_any(hf_ctx* c, const float* W, const float* X, const int32_t* y, int b,
   // solve, then its product) takes 64 x 64 tiles and split K there.
   if (c->cached_layout &&
       (long long)((b + 127) / 128) * ((c->d[1] + 127) / 128) < 128) {
-    build_cache(c, W, X, b, y, mode == HF_HESSIAN);
+    build_cache(c, W, X, b, y, mode == HF_HESSIAN, v);
     product_cached(c, W, X, b, v, mode, out, nullptr);
     return;
   }

@@ -193,6 +193,33 @@ void narrow_gather(const Launch& L, const NarrowGather& g);
 // multiple of 4) admit the narrow kernel.
 bool narrow_eligible(int L, const int* d, const float* X, const float* v);
 void narrow_product(const Launch& L, const NarrowArgs& a);
+// The cache of a solve (the activations, p and, for the Hessian, delta_l and
+// E2_l) for the same nets at up to 64 x 16 rows, in two launches: A_1 in
+// tiles, then 4 batch rows per workgroup through the rest; X, A_l and delta_l
+// also into the concatenated columns of the weight-gradient GEMM (Ycat,
+// Dcat; null: not written).  A label outside [0, C) sets *err (Hessian).
+struct NarrowFwdArgs {
+  int L, B, act, hess;
+  int d[NARROW_MAX_LAYERS + 1];
+  int ld[NARROW_MAX_LAYERS + 1];
+  long long offW[NARROW_MAX_LAYERS + 1], offB[NARROW_MAX_LAYERS + 1];
+  const float* X;                         // B x d_0, row-major
+  const float* W;                         // parameters
+  const int32_t* y;                       // labels (Hessian)
+  float* A[NARROW_MAX_LAYERS + 1];        // out: A_l, l = 1..L-1
+  float* P;                               // out: softmax probabilities
+  float* D[NARROW_MAX_LAYERS + 1];        // out: delta_l, l = 2..L (Hessian)
+  float* E2[NARROW_MAX_LAYERS + 1];       // out: E2_l, l = 1..L-1 (Hessian)
+  float* Ycat;                            // out: X, A_l at column yoff[l]
+  int ldy;
+  int yoff[NARROW_MAX_LAYERS + 1];
+  float* Dcat;                            // out: delta_l at column roff[l]
+  int ldr;
+  int roff[NARROW_MAX_LAYERS + 1];
+  float invB;
+  int* err;
+};
+void narrow_forward(const Launch& L, const NarrowFwdArgs& a);
 
 // --------------------------------------------------------- bf16-input GEMM
 // Precision HF_BF16_INPUTS: every GEMM operand is a bf16 copy (stored as

@@ -600,7 +600,8 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_product4(NarrowArgs 
 // and add their partial tiles in LDS in a fixed order.  v16x16x4 fp32
 // MFMAs, the K order within a block of 16 permuted identically for both
 // operands; 16-byte loads (the host checks d_0 % 4 == 0 and the 16-byte
-// alignment of X and v).
+// alignment of X and v).  With act >= 0 (v = W, c = b) it is the forward
+// layer instead: A_1 = phi(X W_1^T + b_1).
 namespace {
 constexpr int T1R = 16, T1C = 32;                 // tile: rows x hidden units
 constexpr int NT1 = 256;
@@ -610,7 +611,7 @@ constexpr int U1 = 4;                             // 16-blocks per load stage
 extern "C" __global__ __launch_bounds__(256) void hf_narrow_layer1(
     const float* __restrict__ X, const float* __restrict__ v, int B, int d0,
     int d1, long long offW1, long long offB1, float* __restrict__ rz, int ldrz,
-    const int* __restrict__ skip) {
+    int act, const int* __restrict__ skip) {
   if (skip && *skip) return;
   __shared__ f32x4 red[4][2][64];                  // per wave, subtile, lane
   const int tid = threadIdx.x, lane = tid & 63;
@@ -695,9 +696,209 @@ extern "C" __global__ __launch_bounds__(256) void hf_narrow_layer1(
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = r0 + 4 * (l >> 4) + r;
-        if (row < B) rz[(size_t)row * ldrz + n] = t[r] + cb;
+        if (row < B) rz[(size_t)row * ldrz + n] = act >= 0 ? act_f(act, t[r] + cb) : t[r] + cb;
       }
     }
+  }
+}
+
+// ------------------------------------------------------------------------
+// The cache of a solve for a narrow net in two launches (Alg. 1 step 1 and
+// the backward pass of Sec. 2.1): hf_narrow_layer1 with the activation
+// forms A_1 = phi(X W_1^T + b_1) in tiles, then this kernel takes 4 batch
+// rows per workgroup through the later layers, the softmax and, for the
+// Hessian, the backward pass of delta and of E2 = (delta_l W_l) phi''.
+// Arithmetic per element is that of the forward and backward epilogues and
+// of the softmax row kernel; the contractions are those of
+// hf_narrow_product4 with W in place of v.
+extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdArgs g) {
+  constexpr int ML = MAXL - 1;
+  __shared__ __attribute__((aligned(16))) float sA[ML][R4][LR4];   // A_l
+  __shared__ __attribute__((aligned(16))) float sD[2][R4][LR4];    // delta_l
+  __shared__ __attribute__((aligned(16))) float sZ[R4][64];        // logits
+  __shared__ __attribute__((aligned(16))) float red[NW][R4][64];   // partials
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int xi = lane & 3, xk = lane >> 2;   // A operand: row, k within 16
+  const int r0 = blockIdx.x * R4;
+  const int L = g.L;
+  const int act = g.act;
+  const bool hess = g.hess != 0;
+
+  // Weight values of W_l for this lane (forward: [c][k]; backward: [k][c]),
+  // blocks sl and sl + nks of 16 k; past the widths the loads read W_l's
+  // first weight, unmasked (the A operands are zero there, and columns past
+  // d_n are never stored)
+  auto weights = [&](int l, bool fw, float (&bw)[2][16]) {
+    const int dk = fw ? g.d[l - 1] : g.d[l], dn = fw ? g.d[l] : g.d[l - 1];
+    const int ncg = (dn + 63) >> 6, nks = NW / ncg;
+    const int c = 64 * (wave % ncg) + lane, sl = wave / ncg;
+    const bool cv = c < dn;
+    const float* w = g.W + g.offW[l];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int a = 0; a < 16; ++a) {
+        const int k = 16 * (sl + h * nks) + a;
+        const bool kv = cv && k < dk;
+        bw[h][a] = w[kv ? (fw ? (size_t)c * dk + k : (size_t)k * dn + c) : 0];
+      }
+  };
+  float fw2[2][16], bwL[2][16];
+  weights(2, true, fw2);
+  weights(L, false, bwL);
+
+  // A_1 rows (zero past B and d_1), also into the concatenated columns;
+  // the workgroup's rows of X into the concatenated columns
+  {
+    const int pr = tid / MAXH, pc = tid - pr * MAXH;   // NT = R4 * MAXH
+    const bool prv = r0 + pr < g.B;
+    const int prow = prv ? r0 + pr : 0;
+    const bool ok = prv && pc < g.d[1];
+    const float a = g.A[1][ok ? (size_t)prow * g.ld[1] + pc : 0];
+    // X: at most R4 * NARROW_MAX_INPUT / 4 = 2 NT float4s
+    const int d0 = g.d[0], q4 = d0 >> 2;
+    f32x4 xv[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int e = tid + NT * h, r = e / (q4 ? q4 : 1), c = 4 * (e - r * q4);
+      const bool xok = g.Ycat && e < R4 * q4 && r0 + r < g.B;
+      xv[h] = *(const f32x4*)(g.X + (xok ? (size_t)(r0 + r) * d0 + c : 0));
+    }
+    sA[0][pr][pc] = ok ? a : 0.0f;
+    if (g.Ycat && ok) g.Ycat[(size_t)prow * g.ldy + g.yoff[1] + pc] = a;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int e = tid + NT * h, r = e / (q4 ? q4 : 1), c = 4 * (e - r * q4);
+      if (g.Ycat && e < R4 * q4 && r0 + r < g.B)
+        *(f32x4*)(g.Ycat + (size_t)(r0 + r) * g.ldy + c) = xv[h];
+    }
+  }
+  __syncthreads();
+
+  auto total = [&](int ncg, int nks, int i, int c) {
+    float s = 0.0f;
+    for (int k = 0; k < nks; ++k) s += red[k * ncg + (c >> 6)][i][c & 63];
+    return s;
+  };
+
+  // ---- layers 2 .. L: Z_l = A_{l-1} W_l^T + b_l; A_l = phi(Z_l) below L
+  for (int l = 2; l <= L; ++l) {
+    const int dk = g.d[l - 1], dn = g.d[l];
+    const int ncg = (dn + 63) >> 6, nks = NW / ncg;
+    const int sl = wave / ncg;
+    const int nblk = (dk + 15) >> 4;
+    float bw[2][16];
+    if (l == 2) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int a = 0; a < 16; ++a) bw[h][a] = fw2[h][a];
+    } else {
+      weights(l, true, bw);
+    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int b = sl + h * nks;
+      if (b < nblk) acc = mfma4x16(sA[l - 2][xi][16 * b + xk], bw[h], acc);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc[i];
+    __syncthreads();
+    {
+      const int i = tid >> 7, cc = tid & (MAXH - 1);
+      const bool cv = cc < dn, rv = r0 + i < g.B;
+      const float z = cv ? total(ncg, nks, i, cc) + g.W[g.offB[l] + cc] : 0.0f;
+      if (l < L) {
+        const float a = cv ? act_f(act, z) : 0.0f;
+        sA[l - 1][i][cc] = a;
+        if (cv && rv) {
+          g.A[l][(size_t)(r0 + i) * g.ld[l] + cc] = a;
+          if (g.Ycat) g.Ycat[(size_t)(r0 + i) * g.ldy + g.yoff[l] + cc] = a;
+        }
+      } else if (cc < 64) {
+        sZ[i][cc] = z;
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- softmax of the logits, wave i < 4 on row i (columns lane < C <= 64);
+  // for the Hessian delta_L = (p - e_y) / B, a label outside [0, C) flagged
+  if (wave < R4) {
+    const int i = wave, C = g.d[L], row = r0 + i;
+    const bool cv = lane < C, rv = row < g.B;
+    const float z = cv ? sZ[i][lane] : -INFINITY;
+    float m = z;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    const float e = cv ? expf(z - m) : 0.0f;
+    const float p = e * (1.0f / wave_sum(e));
+    if (cv && rv) g.P[(size_t)row * g.ld[L] + lane] = p;
+    if (hess) {
+      int yi = rv ? g.y[row] : -1;
+      if (rv && (yi < 0 || yi >= C)) {
+        if (lane == 0) *g.err = 1;
+        yi = -1;
+      }
+      const float dl = cv ? (lane == yi ? p - 1.0f : p) * g.invB : 0.0f;
+      sD[0][i][lane] = dl;
+      if (cv && rv) {
+        g.D[L][(size_t)row * g.ld[L] + lane] = dl;
+        if (g.Dcat) g.Dcat[(size_t)row * g.ldr + g.roff[L] + lane] = dl;
+      }
+    }
+  }
+  __syncthreads();
+  if (!hess) return;
+
+  // ---- backward, l = L .. 2: t = delta_l W_l over K = d_l;
+  // E2_{l-1} = t phi''(A_{l-1}), delta_{l-1} = t phi'(A_{l-1}) (l > 2)
+  int cur = 0;
+  for (int l = L; l >= 2; --l) {
+    const int dk = g.d[l], dn = g.d[l - 1];
+    const int ncg = (dn + 63) >> 6, nks = NW / ncg;
+    const int sl = wave / ncg;
+    const int nblk = (dk + 15) >> 4;
+    float bw[2][16];
+    if (l == L) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int a = 0; a < 16; ++a) bw[h][a] = bwL[h][a];
+    } else {
+      weights(l, false, bw);
+    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int b = sl + h * nks;
+      if (b < nblk) acc = mfma4x16(sD[cur][xi][16 * b + xk], bw[h], acc);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc[i];
+    __syncthreads();
+    {
+      const int i = tid >> 7, cc = tid & (MAXH - 1);
+      const bool cv = cc < dn, rv = r0 + i < g.B;
+      float dl = 0.0f;
+      if (cv) {
+        const float t = total(ncg, nks, i, cc), a = sA[l - 2][i][cc];
+        dl = t * act_d1(act, a);
+        if (rv) {
+          const size_t o = (size_t)(r0 + i) * g.ld[l - 1] + cc;
+          g.E2[l - 1][o] = t * act_d2(act, a);
+          if (l > 2) {
+            g.D[l - 1][o] = dl;
+            if (g.Dcat) g.Dcat[(size_t)(r0 + i) * g.ldr + g.roff[l - 1] + cc] = dl;
+          }
+        }
+      }
+      sD[cur ^ 1][i][cc] = dl;
+    }
+    __syncthreads();
+    cur ^= 1;
   }
 }
 
@@ -831,7 +1032,7 @@ void narrow_product(const Launch& Lc, const NarrowArgs& a) {
     prof_begin(Lc, "hf_narrow_layer1");
     hipExtLaunchKernelGGL(hf_narrow_layer1, g1, dim3(NT1), 0, Lc.stream, prof_a(Lc),
                           prof_b(Lc), 0, a.X, a.v, a.B, a.d[0], a.d[1], a.offW[1], a.offB[1],
-                          a.RZ1, a.ld[1], a.skip);
+                          a.RZ1, a.ld[1], -1, a.skip);
     prof_end(Lc, "hf_narrow_layer1", f1, 4.0 * a.B * (a.d[0] + a.d[1]));
     prof_begin(Lc, "hf_narrow_product4");
     hipExtLaunchKernelGGL(hf_narrow_product4, dim3((unsigned)((a.B + R4 - 1) / R4)), dim3(NT),
@@ -843,6 +1044,21 @@ void narrow_product(const Launch& Lc, const NarrowArgs& a) {
                           Lc.stream, prof_a(Lc), prof_b(Lc), 0, a);
     prof_end(Lc, "hf_narrow_product", f1 + fr, 4.0 * a.B * (a.d[0] + 4.0 * a.d[1]));
   }
+}
+
+void narrow_forward(const Launch& Lc, const NarrowFwdArgs& a) {
+  const dim3 g1((unsigned)((a.B + T1R - 1) / T1R), (unsigned)((a.d[1] + T1C - 1) / T1C));
+  prof_begin(Lc, "hf_narrow_layer1");
+  hipExtLaunchKernelGGL(hf_narrow_layer1, g1, dim3(NT1), 0, Lc.stream, prof_a(Lc), prof_b(Lc),
+                        0, a.X, a.W, a.B, a.d[0], a.d[1], a.offW[1], a.offB[1], a.A[1],
+                        a.ld[1], a.act, nullptr);
+  prof_end(Lc, "hf_narrow_layer1", 2.0 * a.B * a.d[0] * a.d[1], 4.0 * a.B * (a.d[0] + a.d[1]));
+  double fl = 0.0;
+  for (int l = 2; l <= a.L; ++l) fl += 2.0 * a.B * a.d[l - 1] * a.d[l] * (a.hess ? 2.0 : 1.0);
+  prof_begin(Lc, "hf_narrow_forward4");
+  hipExtLaunchKernelGGL(hf_narrow_forward4, dim3((unsigned)((a.B + R4 - 1) / R4)), dim3(NT), 0,
+                        Lc.stream, prof_a(Lc), prof_b(Lc), 0, a);
+  prof_end(Lc, "hf_narrow_forward4", fl, 4.0 * a.B * (a.d[0] + 4.0 * a.d[1]));
 }
 
 }  // namespace hfk
