@@ -72,6 +72,9 @@ def test_narrow_product(case, mode):
     stats = net.prof_stats()
     net.prof_enable(False)
     assert kernel_for(B) in stats, sorted(stats)
+    # up to 64 workgroups of 16 rows the solve's cache is built by the
+    # narrow kernels as well
+    assert ("hf_narrow_forward4" in stats) == ((B + 15) // 16 <= 64), sorted(stats)
     ref = O.curvature(dims, act, p["theta"], p["X"], p["y"], p["v"], mode)
     err, bound = check(out, ref, act, lambda k: O.curvature(
         dims, act, p["theta"], p["X"], p["y"], p["v"], mode, kink=k),
@@ -130,3 +133,34 @@ def test_narrow_not_taken_outside_its_shapes():
         assert not any(k.startswith("hf_narrow_product") for k in net.prof_stats()), dims
         net.prof_enable(False)
         net.close()
+
+
+def test_narrow_bad_label_is_reported():
+    """The narrow cache build checks the labels of a Hessian product or
+    solve as the softmax row kernel does: a label outside [0, C) is
+    reported (HF_ELABEL) and the flag is cleared once read."""
+    from paper_1606_00511_amd.hf import HFNet, HFError, HF_ELABEL
+    dims, act, B = (64, 100, 10), "tanh", 200
+    p = WL.make_small(dims, act, B, seed=6400)
+    y = p["y"].copy()
+    y[7] = 10
+    net = HFNet(dims, act, B)
+    W, X, v = dev(p["theta"]), dev(p["X"]), dev(p["v"])
+    net.prof_enable(True)
+    net.prof_reset()
+    host(net.hf_hvp(W, X, dev(y), v, "hessian"))
+    assert "hf_narrow_forward4" in net.prof_stats()
+    net.prof_enable(False)
+    with pytest.raises(HFError) as ei:
+        net.hf_check()
+    assert ei.value.code == HF_ELABEL
+    net.hf_check()
+    _, g = net.hf_loss_grad(W, X, dev(p["y"]))
+    with pytest.raises(HFError) as ei:
+        net.hf_cg(W, X, dev(y), g, 1e-2, 3, "hessian")
+    assert ei.value.code == HF_ELABEL
+    net.hf_check()
+    # a Gauss-Newton solve reads no labels
+    net.hf_cg(W, X, dev(y), g, 1e-2, 3, "gauss_newton")
+    net.hf_check()
+    net.close()
