@@ -651,6 +651,44 @@ void backward_data(hf_ctx* c, const float* W, int l, int B, bool cache_e2) {
   gemm_bwd(c->launch(), s, e);
 }
 
+// Every layer's weight gradient of a narrow net from one GEMM over the
+// concatenated columns: x0 (width ldr) against Ycat (width ldy), plus x1
+// against y1 when given (the Hessian's second term), over B rows; then the
+// scatter of the diagonal blocks into out (parameter layout).  Returns the
+// scatter's count of CG dot partials (dot: a CG iteration's request).
+int cat_wgrad(hf_ctx* c, int B, const float* x0, const float* x1, const float* y1,
+              float* out, const int* skip, const CgDotFuse* dot) {
+  const int L = c->L;
+  const int M = c->ldr_cat, N = c->ldy_cat;
+  GemmShape s = shape(M, N, B, x0, x1, c->F(c->oYcat), y1, M, N, x1 ? 2 : 1, skip);
+  // always through the partials, so that the scatter has them
+  s.splits = std::max(2, choose_splits(c, M, N, B * s.nseg));
+  EpiArgs e = epi(c, 0);
+  e.out0 = c->F(c->oSplit);
+  e.ldo = N;
+  e.split_stride = (long long)M * N;
+  e.bias_part = c->Dp(c->oBpart);
+  gemm_wgrad(c->launch(), s, e);
+  NarrowCat nc;
+  std::memset(&nc, 0, sizeof nc);
+  nc.L = L;
+  nc.M = M;
+  nc.N = N;
+  for (int l = 0; l <= L; ++l) {
+    nc.d[l] = c->d[l];
+    nc.roff[l] = c->roff[l];
+    nc.yoff[l] = c->yoff[l];
+    if (l >= 1) {
+      nc.offW[l] = c->offW[l];
+      nc.offB[l] = c->offB[l];
+    }
+  }
+  nc.offW[L + 1] = c->n;
+  nc.n = c->n;
+  return narrow_scatter(c->launch(), c->F(c->oSplit), c->Dp(c->oBpart), s.splits, nc, out,
+                        skip, dot);
+}
+
 // One curvature product out = A v on B rows of X with the forward cache
 // (A_l, p, delta_l, E2_l and the transposed weights) already computed;
 // skip = device flag or null.
@@ -701,36 +739,9 @@ bool product_narrow(hf_ctx* c, const float* W, const float* X, int B,
       if (l < L) a.RA[l] = c->F(c->oRAcat) + c->yoff[l];
     }
     narrow_product(c->launch(), a);
-    const int M = c->ldr_cat, N = c->ldy_cat;
-    GemmShape s = shape(M, N, B, c->F(c->oRDcat), hess ? c->F(c->oDcat) : nullptr,
-                        c->F(c->oYcat), hess ? c->F(c->oRAcat) : nullptr, M, N,
-                        hess ? 2 : 1, skip);
-    // always through the partials, so that the scatter has them
-    s.splits = std::max(2, choose_splits(c, M, N, B * s.nseg));
-    EpiArgs e = epi(c, 0);
-    e.out0 = c->F(c->oSplit);
-    e.ldo = N;
-    e.split_stride = (long long)M * N;
-    e.bias_part = c->Dp(c->oBpart);
-    gemm_wgrad(c->launch(), s, e);
-    NarrowCat nc;
-    std::memset(&nc, 0, sizeof nc);
-    nc.L = L;
-    nc.M = M;
-    nc.N = N;
-    for (int l = 0; l <= L; ++l) {
-      nc.d[l] = c->d[l];
-      nc.roff[l] = c->roff[l];
-      nc.yoff[l] = c->yoff[l];
-      if (l >= 1) {
-        nc.offW[l] = c->offW[l];
-        nc.offB[l] = c->offB[l];
-      }
-    }
-    nc.offW[L + 1] = c->n;
-    nc.n = c->n;
-    c->fused_blocks = narrow_scatter(c->launch(), c->F(c->oSplit), c->Dp(c->oBpart), s.splits,
-                                     nc, out, skip, c->fuse.p == v ? &c->fuse : nullptr);
+    c->fused_blocks = cat_wgrad(c, B, c->F(c->oRDcat), hess ? c->F(c->oDcat) : nullptr,
+                                hess ? c->F(c->oRAcat) : nullptr, out, skip,
+                                c->fuse.p == v ? &c->fuse : nullptr);
     return true;
   }
   narrow_product(c->launch(), a);
@@ -1095,8 +1106,11 @@ bool narrow_build_ok(const hf_ctx* c, const float* X, const float* v_ext, int B)
          gemm_tile(B, c->d[1], c->d[0]) == 64 && (B + 15) / 16 <= 64;
 }
 
+// grad: the gradient's pass instead (loss partials into oLoss, delta_1 ..
+// delta_L into the concatenated columns); the columns then hold no solve's
+// cache
 void narrow_build(hf_ctx* c, const float* W, const float* X, int B,
-                  const int32_t* y, bool hess) {
+                  const int32_t* y, bool hess, bool grad = false) {
   const int L = c->L;
   c->cat_B = -1;
   NarrowFwdArgs a;
@@ -1120,17 +1134,21 @@ void narrow_build(hf_ctx* c, const float* W, const float* X, int B,
   }
   a.X = X;
   a.W = W;
-  a.y = hess ? y : nullptr;
+  a.y = hess || grad ? y : nullptr;
   a.P = c->F(c->oP);
   a.Ycat = c->F(c->oYcat);
   a.ldy = c->ldy_cat;
-  a.Dcat = hess ? c->F(c->oDcat) : nullptr;
+  a.Dcat = hess || grad ? c->F(c->oDcat) : nullptr;
   a.ldr = c->ldr_cat;
   a.invB = 1.0f / (float)B;
   a.err = c->errp();
+  a.grad = grad ? 1 : 0;
+  a.loss_part = grad ? c->Dp(c->oLoss) : nullptr;
   narrow_forward(c->launch(), a);
-  c->cat_B = B;
-  c->cat_hess = hess;
+  if (!grad) {
+    c->cat_B = B;
+    c->cat_hess = hess;
+  }
 }
 
 // The cache of a solve on the curvature batch: forward pass, p and, for the
@@ -1215,6 +1233,14 @@ void loss_grad_any(hf_ctx* c, const float* W, const float* X, const int32_t* y,
       if (l > 1) backward_data_h(c, l, b, false);
     }
     if (fisher) waxpy(c->launch(), fisher, nullptr, (double)b, fisher, c->n);
+    return;
+  }
+  if (!fisher && narrow_build_ok(c, X, nullptr, b)) {
+    // narrow nets: the forward and backward pass in two launches, then every
+    // layer's gradient from one GEMM over the concatenated columns
+    narrow_build(c, W, X, b, y, false, true);
+    loss_finalize(c->launch(), c->Dp(c->oLoss), (b + 3) / 4, b, loss, loss64);
+    cat_wgrad(c, b, c->F(c->oDcat), nullptr, nullptr, grad, nullptr, nullptr);
     return;
   }
   forward_plain(c, W, X, b, y, true);

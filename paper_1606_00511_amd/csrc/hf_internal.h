@@ -218,6 +218,11 @@ struct NarrowFwdArgs {
   int roff[NARROW_MAX_LAYERS + 1];
   float invB;
   int* err;
+  // the gradient instead (Alg. 1 step 1): labels checked, the per-row loss
+  // summed into one fp64 partial per 4 rows (loss_part, as the softmax row
+  // kernel does), and delta_1 .. delta_L into Dcat; no E2
+  int grad;
+  double* loss_part;
 };
 void narrow_forward(const Launch& L, const NarrowFwdArgs& a);
 

@@ -723,7 +723,8 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
   const int r0 = blockIdx.x * R4;
   const int L = g.L;
   const int act = g.act;
-  const bool hess = g.hess != 0;
+  const bool hess = g.hess != 0, grad = g.grad != 0;
+  const bool delta = hess || grad;       // the backward pass of delta runs
 
   // Weight values of W_l for this lane (forward: [c][k]; backward: [k][c]),
   // blocks sl and sl + nks of 16 k; past the widths the loads read W_l's
@@ -825,7 +826,9 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
   }
 
   // ---- softmax of the logits, wave i < 4 on row i (columns lane < C <= 64);
-  // for the Hessian delta_L = (p - e_y) / B, a label outside [0, C) flagged
+  // with labels delta_L = (p - e_y) / B, a label outside [0, C) flagged, and
+  // for the gradient the row's loss log(sum exp z) - z_y
+  __shared__ float wl[R4];
   if (wave < R4) {
     const int i = wave, C = g.d[L], row = r0 + i;
     const bool cv = lane < C, rv = row < g.B;
@@ -834,9 +837,10 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
     const float e = cv ? expf(z - m) : 0.0f;
-    const float p = e * (1.0f / wave_sum(e));
+    const float sum = wave_sum(e);
+    const float p = e * (1.0f / sum);
     if (cv && rv) g.P[(size_t)row * g.ld[L] + lane] = p;
-    if (hess) {
+    if (delta) {
       int yi = rv ? g.y[row] : -1;
       if (rv && (yi < 0 || yi >= C)) {
         if (lane == 0) *g.err = 1;
@@ -845,16 +849,23 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
       const float dl = cv ? (lane == yi ? p - 1.0f : p) * g.invB : 0.0f;
       sD[0][i][lane] = dl;
       if (cv && rv) {
-        g.D[L][(size_t)row * g.ld[L] + lane] = dl;
+        if (hess) g.D[L][(size_t)row * g.ld[L] + lane] = dl;
         if (g.Dcat) g.Dcat[(size_t)row * g.ldr + g.roff[L] + lane] = dl;
+      }
+      if (grad && lane == 0) {
+        const float zy = yi >= 0 ? sZ[i][yi] : 0.0f;
+        wl[i] = yi >= 0 ? (m + logf(sum)) - zy : 0.0f;
       }
     }
   }
   __syncthreads();
-  if (!hess) return;
+  if (grad && tid == 0)
+    g.loss_part[blockIdx.x] = ((double)wl[0] + (double)wl[1]) + ((double)wl[2] + (double)wl[3]);
+  if (!delta) return;
 
   // ---- backward, l = L .. 2: t = delta_l W_l over K = d_l;
-  // E2_{l-1} = t phi''(A_{l-1}), delta_{l-1} = t phi'(A_{l-1}) (l > 2)
+  // delta_{l-1} = t phi'(A_{l-1}); for the Hessian E2_{l-1} = t phi''(A_{l-1})
+  // (delta_1 only for the gradient)
   int cur = 0;
   for (int l = L; l >= 2; --l) {
     const int dk = g.d[l], dn = g.d[l - 1];
@@ -888,11 +899,12 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
         dl = t * act_d1(act, a);
         if (rv) {
           const size_t o = (size_t)(r0 + i) * g.ld[l - 1] + cc;
-          g.E2[l - 1][o] = t * act_d2(act, a);
-          if (l > 2) {
-            g.D[l - 1][o] = dl;
-            if (g.Dcat) g.Dcat[(size_t)(r0 + i) * g.ldr + g.roff[l - 1] + cc] = dl;
+          if (hess) {
+            g.E2[l - 1][o] = t * act_d2(act, a);
+            if (l > 2) g.D[l - 1][o] = dl;
           }
+          if (g.Dcat && (grad || l > 2))
+            g.Dcat[(size_t)(r0 + i) * g.ldr + g.roff[l - 1] + cc] = dl;
         }
       }
       sD[cur ^ 1][i][cc] = dl;
@@ -1054,7 +1066,8 @@ void narrow_forward(const Launch& Lc, const NarrowFwdArgs& a) {
                         a.ld[1], a.act, nullptr);
   prof_end(Lc, "hf_narrow_layer1", 2.0 * a.B * a.d[0] * a.d[1], 4.0 * a.B * (a.d[0] + a.d[1]));
   double fl = 0.0;
-  for (int l = 2; l <= a.L; ++l) fl += 2.0 * a.B * a.d[l - 1] * a.d[l] * (a.hess ? 2.0 : 1.0);
+  for (int l = 2; l <= a.L; ++l)
+    fl += 2.0 * a.B * a.d[l - 1] * a.d[l] * (a.hess || a.grad ? 2.0 : 1.0);
   prof_begin(Lc, "hf_narrow_forward4");
   hipExtLaunchKernelGGL(hf_narrow_forward4, dim3((unsigned)((a.B + R4 - 1) / R4)), dim3(NT), 0,
                         Lc.stream, prof_a(Lc), prof_b(Lc), 0, a);

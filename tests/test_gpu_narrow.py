@@ -135,6 +135,32 @@ def test_narrow_not_taken_outside_its_shapes():
         net.close()
 
 
+@pytest.mark.parametrize("case", CASES, ids=[sid(c) for c in CASES])
+def test_narrow_loss_grad(case):
+    """The gradient through the narrow kernels (up to 64 workgroups of 16
+    rows: the forward and backward pass in two launches, then one GEMM over
+    the concatenated columns) against the oracle: loss to 1e-5 relative,
+    gradient rel-L2 <= 1e-4 (ReLU with the bracket)."""
+    from paper_1606_00511_amd.hf import HFNet
+    dims, act, B = case
+    p = WL.make_small(dims, act, B, seed=6500 + B + len(dims))
+    net = HFNet(dims, act, B)
+    net.prof_enable(True)
+    net.prof_reset()
+    f, g = net.hf_loss_grad(dev(p["theta"]), dev(p["X"]), dev(p["y"]))
+    g = host(g)
+    stats = net.prof_stats()
+    net.prof_enable(False)
+    assert ("hf_narrow_forward4" in stats) == ((B + 15) // 16 <= 64), sorted(stats)
+    f_o, g_o = O.loss_grad(dims, act, p["theta"], p["X"], p["y"])
+    assert abs(float(host(f)[0]) - f_o) <= 1e-5 * abs(f_o)
+    err, bound = check(g, g_o, act, lambda k: O.loss_grad(
+        dims, act, p["theta"], p["X"], p["y"], kink=k)[1],
+        margins=relu_margins(dims, act, p["theta"], p["X"]))
+    print("%s gradient: rel %.2e (bound %.2e)" % (sid(case), err, bound))
+    net.close()
+
+
 def test_narrow_bad_label_is_reported():
     """The narrow cache build checks the labels of a Hessian product or
     solve as the softmax row kernel does: a label outside [0, C) is
