@@ -1096,14 +1096,14 @@ void narrow_cache(hf_ctx* c, const float* X, int B, bool hess) {
 }
 
 // Whether the cache of a narrow net is built by the narrow kernels: the
-// products that follow must take the two-launch narrow form (every vector
-// they multiply is aligned: the solvers' own, or v_ext, the caller's x0 or
-// v, which may be null), since the narrow build leaves the transposed weights
-// of the GEMM path unwritten.
+// products that follow must take a narrow form (every vector they multiply
+// is aligned: the solvers' own, or v_ext, the caller's x0 or v, which may be
+// null), since the narrow build leaves the transposed weights of the GEMM
+// path unwritten.
 bool narrow_build_ok(const hf_ctx* c, const float* X, const float* v_ext, int B) {
   return c->narrow_cat && B <= c->Bws && narrow_eligible(c->L, c->d.data(), X, v_ext) &&
          narrow_eligible(c->L, c->d.data(), nullptr, c->F(c->oPv)) &&
-         gemm_tile(B, c->d[1], c->d[0]) == 64 && (B + 15) / 16 <= 64;
+         gemm_tile(B, c->d[1], c->d[0]) == 64;
 }
 
 // grad: the gradient's pass instead (loss partials into oLoss, delta_1 ..
