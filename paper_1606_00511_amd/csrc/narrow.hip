@@ -1,26 +1,34 @@
-// The cached curvature product of a narrow net in one launch (Sec. 2.1:
-// R-forward, the output layer's R-operator, R-backward or the Gauss-Newton
-// backward), for nets whose hidden layers are at most 128 wide and whose
-// output layer is at most 64 wide.
+// The narrow nets' passes (Sec. 2.1 and Alg. 1 step 1), for nets with 2 to 4
+// weight layers whose hidden layers are at most 128 wide and whose output
+// layer is at most 64 wide: the cached curvature product (R-forward, the
+// output layer's R-operator, R-backward or the Gauss-Newton backward), the
+// solve's cache (forward pass, softmax and, for the Hessian, the backward
+// pass of delta and of the phi'' term) and the gradient's passes, each up
+// to the weight gradients; then every layer's weight gradient from one GEMM
+// over concatenated columns, whose diagonal blocks hf_narrow_scatter writes
+// out in the parameter layout.
 //
-// Every step of the product except the weight gradients is row-local: the
-// R-forward of a batch row needs only that row, the softmax R-operator acts
-// on one row of logits, and the backward step to layer l - 1 needs only the
-// row's Rdelta_l.  A workgroup therefore takes 16 batch rows and all of
-// their hidden units, keeps every intermediate row in LDS, and writes out
-// only what the weight-gradient GEMMs that follow read: Rdelta_l for every
-// layer and, for the Hessian, RA_l.  On small batches this replaces the
-// transposes of v, 2L - 1 GEMMs with their split-K passes and the softmax
-// R-operator kernel, whose launch latency, not their work, set the time.
+// Every step except the weight gradients is row-local: the R-forward of a
+// batch row needs only that row, the softmax and its R-operator act on one
+// row of logits, and the backward step to layer l - 1 needs only the row's
+// delta_l or Rdelta_l.  A workgroup therefore takes a few batch rows and all
+// of their hidden units, keeps every intermediate row in LDS, and writes out
+// only what the weight-gradient GEMM reads.  On small batches this replaces
+// chains of GEMMs with their split-K passes and row kernels, whose launch
+// latency, not their work, set the time.  The first layer, whose K is the
+// input width, is a kernel of its own below 1,025 rows (hf_narrow_layer1,
+// in tiles); above, hf_narrow_product holds 16 rows per workgroup and does
+// it inside.
 //
-// Arithmetic per element is that of the epilogues of the separate kernels:
+// The product's arithmetic per element is that of the epilogues of the
+// separate kernels:
 //   RZ_l = RA_{l-1} W_l^T + A_{l-1} V_l^T + c_l  (RZ_1 = X V_1^T + c_1)
 //   RA_l = phi'(A_l) RZ_l
 //   Rdelta_L = p (RZ_L - p.RZ_L) / B
 //   Rdelta_{l-1} = (Rdelta_l W_l [+ delta_l V_l]) phi'(A_{l-1})
 //                  [+ E2_{l-1} RZ_{l-1}]     (bracketed terms: Hessian)
-// with v16x16x4 fp32 MFMAs; the K order within a block of 16 is permuted
-// identically for both operands.
+// The 16-row kernel uses v16x16x4 fp32 MFMAs, the K order within a block of
+// 16 permuted identically for both operands.
 #include "act.h"
 #include "hf_internal.h"
 
