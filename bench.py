@@ -71,11 +71,12 @@ def parse():
     return ap.parse_args()
 
 
-def counter_traffic(kernel):
+def counter_traffic(kernel, workload):
     """HBM bytes per launch of `kernel` from the committed rocprofv3
-    FETCH_SIZE / WRITE_SIZE summary, or None when the summary does not cover
-    the kernel or its GEMM source (gemm.hip, or gemm_bf16.hip for the bf16
-    kernels) has changed since the counters were taken."""
+    FETCH_SIZE / WRITE_SIZE summary, or None when the summary was taken on
+    another workload, does not cover the kernel, or its GEMM source
+    (gemm.hip, or gemm_bf16.hip for the bf16 kernels) has changed since the
+    counters were taken."""
     import hashlib
     bf16 = kernel.startswith("hf_hgemm")
     path = os.path.join(ROOT, "profiles", "speech_b16384_hbm_counters.md")
@@ -94,7 +95,9 @@ def counter_traffic(kernel):
             vals[t[1]] = float(t[2])
         if len(t) == 2 and t[0] == tag:
             vals["sha"] = t[1]
-    if vals.get("sha") != sha:
+        if len(t) == 2 and t[0] == "workload":
+            vals["workload"] = t[1]
+    if vals.get("sha") != sha or vals.get("workload") != workload:
         return None
     return vals.get(kernel)
 
@@ -453,7 +456,7 @@ def main():
             "bound": "mfma", "kernel": s32["dom"],
             "achieved": s32["achieved"], "peak": PEAK_FP32_TFLOPS,
             "unit": "TFLOP/s", "frac": s32["achieved"] / PEAK_FP32_TFLOPS,
-            "traffic": counter_traffic(s32["dom"]),
+            "traffic": counter_traffic(s32["dom"], w.name),
             "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "launches": ds["launches"], "avg_launch_ms": ds["ms"] / ds["launches"],
             "flops_per_launch": ds["flops"] / ds["launches"],
@@ -483,7 +486,7 @@ def main():
                 "bound": "mfma", "kernel": s16["dom"], "achieved": s16["achieved"],
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": s16["achieved"] / PEAK_BF16_TFLOPS,
-                "traffic": counter_traffic(s16["dom"]),
+                "traffic": counter_traffic(s16["dom"], w.name),
                 "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "launches": d16["launches"],
                 "avg_launch_ms": d16["ms"] / d16["launches"],

@@ -1106,11 +1106,15 @@ bool narrow_build_ok(const hf_ctx* c, const float* X, const float* v_ext, int B)
          gemm_tile(B, c->d[1], c->d[0]) == 64;
 }
 
-// grad: the gradient's pass instead (loss partials into oLoss, delta_1 ..
-// delta_L into the concatenated columns); the columns then hold no solve's
-// cache
+// What narrow_build forms: the cache of a solve; the gradient's pass (loss
+// partials into oLoss, delta_1 .. delta_L into the concatenated columns); or
+// the loss alone (partials into oLoss).  After either of the last two no
+// solve's cache is held.
+enum NarrowPass { NARROW_CACHE, NARROW_GRAD, NARROW_LOSS };
+
 void narrow_build(hf_ctx* c, const float* W, const float* X, int B,
-                  const int32_t* y, bool hess, bool grad = false) {
+                  const int32_t* y, bool hess, NarrowPass pass = NARROW_CACHE) {
+  const bool grad = pass == NARROW_GRAD, loss = pass != NARROW_CACHE;
   const int L = c->L;
   c->cat_B = -1;
   NarrowFwdArgs a;
@@ -1134,18 +1138,18 @@ void narrow_build(hf_ctx* c, const float* W, const float* X, int B,
   }
   a.X = X;
   a.W = W;
-  a.y = hess || grad ? y : nullptr;
-  a.P = c->F(c->oP);
-  a.Ycat = c->F(c->oYcat);
+  a.y = hess || loss ? y : nullptr;
+  a.P = loss ? nullptr : c->F(c->oP);
+  a.Ycat = pass == NARROW_LOSS ? nullptr : c->F(c->oYcat);
   a.ldy = c->ldy_cat;
   a.Dcat = hess || grad ? c->F(c->oDcat) : nullptr;
   a.ldr = c->ldr_cat;
   a.invB = 1.0f / (float)B;
   a.err = c->errp();
   a.grad = grad ? 1 : 0;
-  a.loss_part = grad ? c->Dp(c->oLoss) : nullptr;
+  a.loss_part = loss ? c->Dp(c->oLoss) : nullptr;
   narrow_forward(c->launch(), a);
-  if (!grad) {
+  if (!loss) {
     c->cat_B = B;
     c->cat_hess = hess;
   }
@@ -1204,6 +1208,7 @@ namespace {
 void loss_only(hf_ctx* c, const float* W, const float* X, const int32_t* y,
                int B, float* loss, double* loss64) {
   if (c->bf16()) forward_plain_h(c, W, X, B, y, false);
+  else if (narrow_build_ok(c, X, nullptr, B)) narrow_build(c, W, X, B, y, false, NARROW_LOSS);
   else forward_plain(c, W, X, B, y, false);
   loss_finalize(c->launch(), c->Dp(c->oLoss), (B + 3) / 4, B, loss, loss64);
 }
@@ -1238,7 +1243,7 @@ void loss_grad_any(hf_ctx* c, const float* W, const float* X, const int32_t* y,
   if (!fisher && narrow_build_ok(c, X, nullptr, b)) {
     // narrow nets: the forward and backward pass in two launches, then every
     // layer's gradient from one GEMM over the concatenated columns
-    narrow_build(c, W, X, b, y, false, true);
+    narrow_build(c, W, X, b, y, false, NARROW_GRAD);
     loss_finalize(c->launch(), c->Dp(c->oLoss), (b + 3) / 4, b, loss, loss64);
     cat_wgrad(c, b, c->F(c->oDcat), nullptr, nullptr, grad, nullptr, nullptr);
     return;

@@ -206,8 +206,10 @@ struct NarrowFwdArgs {
   const float* X;                         // B x d_0, row-major
   const float* W;                         // parameters
   const int32_t* y;                       // labels (Hessian)
-  float* A[NARROW_MAX_LAYERS + 1];        // out: A_l, l = 1..L-1
-  float* P;                               // out: softmax probabilities
+  float* A[NARROW_MAX_LAYERS + 1];        // out: A_l, l = 1..L-1 (A_1 by
+                                          // the layer-1 kernel, always)
+  float* P;                               // out: softmax probabilities; null:
+                                          // neither P nor A_2 .. A_{L-1} stored
   float* D[NARROW_MAX_LAYERS + 1];        // out: delta_l, l = 2..L (Hessian)
   float* E2[NARROW_MAX_LAYERS + 1];       // out: E2_l, l = 1..L-1 (Hessian)
   float* Ycat;                            // out: X, A_l at column yoff[l]
@@ -218,10 +220,12 @@ struct NarrowFwdArgs {
   int roff[NARROW_MAX_LAYERS + 1];
   float invB;
   int* err;
-  // the gradient instead (Alg. 1 step 1): labels checked, the per-row loss
-  // summed into one fp64 partial per 4 rows (loss_part, as the softmax row
-  // kernel does), and delta_1 .. delta_L into Dcat; no E2
+  // the gradient instead (Alg. 1 step 1): delta_1 .. delta_L into Dcat; no
+  // E2
   int grad;
+  // non-null: labels checked and the per-row loss summed into one fp64
+  // partial per 4 rows, as the softmax row kernel does (the gradient, and
+  // the loss alone with hess = grad = 0)
   double* loss_part;
 };
 void narrow_forward(const Launch& L, const NarrowFwdArgs& a);

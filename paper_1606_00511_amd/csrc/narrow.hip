@@ -718,7 +718,9 @@ extern "C" __global__ __launch_bounds__(256) void hf_narrow_layer1(
 // Hessian, the backward pass of delta and of E2 = (delta_l W_l) phi''.
 // Arithmetic per element is that of the forward and backward epilogues and
 // of the softmax row kernel; the contractions are those of
-// hf_narrow_product4 with W in place of v.
+// hf_narrow_product4 with W in place of v.  With loss_part and no backward
+// pass (hess = grad = 0, P null) it is the loss-only forward of the line
+// search: only the per-row losses leave the workgroup.
 extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdArgs g) {
   constexpr int ML = MAXL - 1;
   __shared__ __attribute__((aligned(16))) float sA[ML][R4][LR4];   // A_l
@@ -733,6 +735,8 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
   const int act = g.act;
   const bool hess = g.hess != 0, grad = g.grad != 0;
   const bool delta = hess || grad;       // the backward pass of delta runs
+  const bool loss = g.loss_part != nullptr;
+  const bool keep = g.P != nullptr;      // A_l and P are stored
 
   // Weight values of W_l for this lane (forward: [c][k]; backward: [k][c]),
   // blocks sl and sl + nks of 16 k; past the widths the loads read W_l's
@@ -823,7 +827,7 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
         const float a = cv ? act_f(act, z) : 0.0f;
         sA[l - 1][i][cc] = a;
         if (cv && rv) {
-          g.A[l][(size_t)(r0 + i) * g.ld[l] + cc] = a;
+          if (keep) g.A[l][(size_t)(r0 + i) * g.ld[l] + cc] = a;
           if (g.Ycat) g.Ycat[(size_t)(r0 + i) * g.ldy + g.yoff[l] + cc] = a;
         }
       } else if (cc < 64) {
@@ -834,8 +838,8 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
   }
 
   // ---- softmax of the logits, wave i < 4 on row i (columns lane < C <= 64);
-  // with labels delta_L = (p - e_y) / B, a label outside [0, C) flagged, and
-  // for the gradient the row's loss log(sum exp z) - z_y
+  // with labels a label outside [0, C) flagged, delta_L = (p - e_y) / B, and
+  // for the loss the row's log(sum exp z) - z_y
   __shared__ float wl[R4];
   if (wave < R4) {
     const int i = wave, C = g.d[L], row = r0 + i;
@@ -847,27 +851,29 @@ extern "C" __global__ __launch_bounds__(512) void hf_narrow_forward4(NarrowFwdAr
     const float e = cv ? expf(z - m) : 0.0f;
     const float sum = wave_sum(e);
     const float p = e * (1.0f / sum);
-    if (cv && rv) g.P[(size_t)row * g.ld[L] + lane] = p;
-    if (delta) {
+    if (keep && cv && rv) g.P[(size_t)row * g.ld[L] + lane] = p;
+    if (delta || loss) {
       int yi = rv ? g.y[row] : -1;
       if (rv && (yi < 0 || yi >= C)) {
         if (lane == 0) *g.err = 1;
         yi = -1;
       }
-      const float dl = cv ? (lane == yi ? p - 1.0f : p) * g.invB : 0.0f;
-      sD[0][i][lane] = dl;
-      if (cv && rv) {
-        if (hess) g.D[L][(size_t)row * g.ld[L] + lane] = dl;
-        if (g.Dcat) g.Dcat[(size_t)row * g.ldr + g.roff[L] + lane] = dl;
+      if (delta) {
+        const float dl = cv ? (lane == yi ? p - 1.0f : p) * g.invB : 0.0f;
+        sD[0][i][lane] = dl;
+        if (cv && rv) {
+          if (hess) g.D[L][(size_t)row * g.ld[L] + lane] = dl;
+          if (g.Dcat) g.Dcat[(size_t)row * g.ldr + g.roff[L] + lane] = dl;
+        }
       }
-      if (grad && lane == 0) {
+      if (loss && lane == 0) {
         const float zy = yi >= 0 ? sZ[i][yi] : 0.0f;
         wl[i] = yi >= 0 ? (m + logf(sum)) - zy : 0.0f;
       }
     }
   }
   __syncthreads();
-  if (grad && tid == 0)
+  if (loss && tid == 0)
     g.loss_part[blockIdx.x] = ((double)wl[0] + (double)wl[1]) + ((double)wl[2] + (double)wl[3]);
   if (!delta) return;
 

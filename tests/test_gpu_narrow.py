@@ -160,6 +160,70 @@ def test_narrow_loss_grad(case):
     net.close()
 
 
+@pytest.mark.parametrize("case", CASES, ids=[sid(c) for c in CASES])
+def test_narrow_loss_only(case):
+    """The loss-only forward of the line search (hf_loss) through the narrow
+    kernels: f within 1e-5 relative of the oracle's, and no forward GEMM."""
+    from paper_1606_00511_amd.hf import HFNet
+    dims, act, B = case
+    p = WL.make_small(dims, act, B, seed=6600 + B + len(dims))
+    net = HFNet(dims, act, B)
+    net.prof_enable(True)
+    net.prof_reset()
+    f = float(host(net.hf_loss(dev(p["theta"]), dev(p["X"]), dev(p["y"])))[0])
+    stats = net.prof_stats()
+    net.prof_enable(False)
+    net.hf_check()
+    assert "hf_narrow_forward4" in stats, sorted(stats)
+    assert not any(k.startswith("hf_gemm") for k in stats), sorted(stats)
+    f_o = O.loss(dims, act, p["theta"], p["X"], p["y"])
+    print("%s loss: rel %.2e" % (sid(case), abs(f - f_o) / abs(f_o)))
+    assert abs(f - f_o) <= 1e-5 * abs(f_o)
+    net.close()
+
+
+@pytest.mark.parametrize("curvature", ["hessian", "gauss_newton"])
+@pytest.mark.parametrize("case", [((64, 100, 10), "sigmoid", 200),
+                                  ((96, 40, 30, 17), "tanh", 77)],
+                         ids=["64x100x10-sigmoid-b200", "96x40x30x17-tanh-b77"])
+def test_narrow_iterate(case, curvature):
+    """One outer iteration (gradient, solve, line search, damping product)
+    on a narrow net against the oracle's, with the bar of the other outer
+    iteration tests; every pass runs in the narrow kernels (no forward GEMM
+    is launched)."""
+    from paper_1606_00511_amd.hf import HFNet
+    from tests.test_gpu_iterate import compare_step
+    dims, act, B = case
+    p = WL.make_small(dims, act, B, seed=6700 + B)
+    th = p["theta"].astype(np.float64)
+    kw = dict(solver="cg", curvature=curvature, damping=1e-2, max_iters=6,
+              adapt_damping=True)
+    o = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver="cg",
+                  curvature_kind=curvature, lam=1e-2, max_iters=6,
+                  damping_adapt=True)
+    net = HFNet(dims, act, B)
+    net.prof_enable(True)
+    net.prof_reset()
+    W = dev(p["theta"].copy())
+    delta = dev(np.zeros_like(p["theta"]))
+    gi, _, _ = compare_step(net, dims, act, p, th, delta, kw, 0, o, W)
+    stats = net.prof_stats()
+    net.prof_enable(False)
+    print("%s %s: dir %d alpha %g evals %d f %.6f -> %.6f (oracle %.6f) rho "
+          "%.4f/%.4f" % (sid(case), curvature, gi["direction"], gi["alpha"],
+                         gi["evals"], gi["f0"], gi["f1"], o["f1"], gi["rho"],
+                         o["rho"]))
+    assert stats["hf_narrow_forward4"]["launches"] >= gi["evals"] + 2, stats
+    assert not any(k.startswith("hf_gemm_fwd") or k.startswith("hf_softmax")
+                   for k in stats), sorted(stats)
+    if gi["accepted"] and o["accepted"] and gi["alpha"] == o["alpha"] and \
+            gi["direction"] == o["direction"]:
+        assert gi["rho"] == pytest.approx(o["rho"], rel=1e-2)
+        if min(abs(o["rho"] - 0.25), abs(o["rho"] - 0.75)) > 1e-2:
+            assert gi["damping_next"] == pytest.approx(o["lam_next"], rel=1e-6)
+    net.close()
+
+
 def test_narrow_bad_label_is_reported():
     """The narrow cache build checks the labels of a Hessian product or
     solve as the softmax row kernel does: a label outside [0, C) is
@@ -187,5 +251,11 @@ def test_narrow_bad_label_is_reported():
     net.hf_check()
     # a Gauss-Newton solve reads no labels
     net.hf_cg(W, X, dev(y), g, 1e-2, 3, "gauss_newton")
+    net.hf_check()
+    # the loss-only forward checks them
+    host(net.hf_loss(W, X, dev(y)))
+    with pytest.raises(HFError) as ei:
+        net.hf_check()
+    assert ei.value.code == HF_ELABEL
     net.hf_check()
     net.close()
