@@ -133,7 +133,7 @@ __device__ __forceinline__ void st_t(const EpiH& e, bf16_t* t, int r0, int c,
 __device__ __forceinline__ void st_ht(const EpiH& e, bf16_t* h, bf16_t* t,
                                       int r0, int c, const Q& q, int M) {
   st_h(e, h, r0, c, q, M);
-  st_t(e, t, r0, c, q, M);
+  if (t) st_t(e, t, r0, c, q, M);
 }
 __device__ __forceinline__ void st_f(const EpiH& e, float* f, int r0, int c,
                                      const Q& q, int M) {
@@ -198,7 +198,7 @@ struct EFwdRFwd {
     Q rz;
 #pragma unroll
     for (int j = 0; j < 4; ++j) rz.v[j] = v1.v[j] + e.rbias[c];
-    st_f(e, e.f1, r0, c, rz, M);
+    if (e.f1) st_f(e, e.f1, r0, c, rz, M);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float a = act_f(e.act, v0.v[j] + e.bias[c]);
@@ -214,7 +214,7 @@ struct EFwdRFwd {
       z.v[j] = v0.v[j] + e.bias[c];
       rz.v[j] = v1.v[j] + e.rbias[c];
     }
-    st_f(e, e.f1, r0, c, rz, M);
+    if (e.f1) st_f(e, e.f1, r0, c, rz, M);
     if (e.hidden) {
       Q a, ra;
 #pragma unroll
@@ -240,7 +240,7 @@ struct ERFwd {
     Q rz;
 #pragma unroll
     for (int j = 0; j < 4; ++j) rz.v[j] = v0.v[j] + e.rbias[c];
-    st_f(e, e.f1, r0, c, rz, M);
+    if (e.f1) st_f(e, e.f1, r0, c, rz, M);
 #pragma unroll
     for (int j = 0; j < 4; ++j) o[0].v[j] = act_d1(e.act, a.v[j]) * rz.v[j];
   }
@@ -249,7 +249,7 @@ struct ERFwd {
     Q rz;
 #pragma unroll
     for (int j = 0; j < 4; ++j) rz.v[j] = v0.v[j] + e.rbias[c];
-    st_f(e, e.f1, r0, c, rz, M);
+    if (e.f1) st_f(e, e.f1, r0, c, rz, M);
     if (e.hidden) {
       const Q a = ld_a0(e, r0, c);
       Q ra;
@@ -388,6 +388,8 @@ struct EGNBwd {
 };
 struct EStore {                      // fp32 only: never staged
   static constexpr int NB = 0;
+  static constexpr bool A0 = false;
+  static __device__ __forceinline__ bool staged(const EpiH&) { return false; }
   static __device__ __forceinline__ void apply(const EpiH& e, int r0, int c, int M, int zs,
                                                const Q& v0, const Q&) {
 #pragma unroll
@@ -566,6 +568,30 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
   const bool do_bias = BIAS && tn == 0 && (e.bias_out || e.bias_part);
   double bsum = 0.0;
 
+  // The staged epilogue's a0 tile ([RM][RN] bf16, 16-byte chunks swizzled
+  // as in the staged output tile, so that each output overwrites its own a0
+  // in place) arrives by direct loads as well: with two stages, the half of
+  // it that covers the stage the last K block leaves free is fetched while
+  // that block's MFMAs run, the other half right after them.  Chunks past
+  // ldo (only in a last column tile, feeding columns that are not stored)
+  // fetch the row's last chunk instead, so that every load stays in the row.
+  constexpr int TA = RM * RN;
+  constexpr bool A0PF = Epi::NB > 0 && Epi::A0 && S == 2 && TA == S * STAGE;
+  const bool a0pf = A0PF && HF_H_STAGE && Epi::staged(e);
+  auto a0_half = [&](int half) {
+    constexpr int CPR = RN / 8;                      // chunks per tile row
+    constexpr int ROWS = RM / 2 / NW;                // rows per wave
+    static_assert(!A0PF || (CPR == 32 && ROWS % 2 == 0), "a0 direct-load layout");
+    const int kmax = (e.ldo - n0) / 8 - 1;
+#pragma unroll
+    for (int j = 0; j < ROWS / 2; ++j) {
+      const int r = half * (RM / 2) + wave * ROWS + 2 * j + (lane >> 5);
+      const int k = min((lane & 31) ^ ((r >> 3) % CPR), kmax);
+      dma16(e.a0 + (size_t)(m0 + r) * e.ldo + n0 + 8 * k,
+            lds + (half * (RM / 2) + wave * ROWS + 2 * j) * RN);
+    }
+  };
+
   // prologue: the first S - 1 blocks in flight
 #pragma unroll
   for (int i = 0; i < S - 1; ++i)
@@ -582,6 +608,7 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
     stage_barrier();     // every wave's loads landed; stage it - 1 is free
     if (it + S - 1 < nblk) issue(vb0 + it + S - 1, (it + S - 1) % S);
     const int st = it % S;
+    if (A0PF && a0pf && it == nblk - 1) a0_half(1 - st);
     compute(st);
     if (BIAS && do_bias && vb0 + it < kbps) {
       const int row = tid % RM, part = tid / RM;
@@ -630,7 +657,18 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
         return r * RN + (((c >> 3) ^ ((r >> 3) % CPR)) << 3) + (c & 7);
       };
       __syncthreads();     // every wave is done with the operand stages
-      if (Epi::A0) {
+      if (A0PF) {
+        // the half the last block's stage covered (all of it if the loop
+        // had no blocks), then every wave's direct loads landed
+        if (nblk > 0) {
+          a0_half((nblk - 1) % S);
+        } else {
+          a0_half(0);
+          a0_half(1);
+        }
+        wait_vm<0>();
+        stage_barrier();
+      } else if (Epi::A0) {
         // a0 rows exist up to M rounded up to 256; columns past ldo read 0
         u32x4 v[PASS];
 #pragma unroll
@@ -701,9 +739,10 @@ __device__ __forceinline__ void hgemm_body(const GemmShapeH& s, const EpiH& e) {
             }
           }
         }
-        // transposed copy: eight consecutive rows of one column per thread,
-        // zeros for rows from M to Mpad; a wave covers 8 columns x 64 rows,
-        // 128 contiguous bytes per column
+        // transposed copy (where one is wanted): eight consecutive rows of
+        // one column per thread, zeros for rows from M to Mpad; a wave
+        // covers 8 columns x 64 rows, 128 contiguous bytes per column
+        if (!tp) continue;
 #pragma unroll
         for (int p = 0; p < PASS; ++p) {
           const int it = tid + p * NT;
@@ -909,16 +948,20 @@ void hgemm_fwd(const Launch& L, const GemmShapeH& s, const EpiH& e) {
          io(s, s.nseg, s.nseg, 4.0));
 }
 void hgemm_fwd_rfwd(const Launch& L, const GemmShapeH& s, const EpiH& e) {
+  // hidden layer: A row-major and transposed, RA row-major, RZ and the
+  // transposed RA where wanted; output layer: logits and RZ
+  const double out = e.hidden ? 6.0 + (e.f1 ? 4.0 : 0.0) + (e.t2 ? 2.0 : 0.0) : 8.0;
   if (s.X[1])
-    launch(L, "hf_hgemm_fwd_rfwd", hf_hgemm_fwd_rfwd, 1, s, e, 3 * mnk(s),
-           io(s, 2, 2, e.hidden ? 12.0 : 8.0));
+    launch(L, "hf_hgemm_fwd_rfwd", hf_hgemm_fwd_rfwd, 1, s, e, 3 * mnk(s), io(s, 2, 2, out));
   else
-    launch(L, "hf_hgemm_fwd_rfwd0", hf_hgemm_fwd_rfwd0, 2, s, e, 2 * mnk(s),
-           io(s, 1, 2, e.hidden ? 12.0 : 8.0));
+    launch(L, "hf_hgemm_fwd_rfwd0", hf_hgemm_fwd_rfwd0, 2, s, e, 2 * mnk(s), io(s, 1, 2, out));
 }
 void hgemm_rfwd(const Launch& L, const GemmShapeH& s, const EpiH& e) {
+  // hidden layer: a0 read, RA stored row-major, RZ and the transposed RA
+  // where wanted; output layer: RZ
+  const double out = e.hidden ? 4.0 + (e.f1 ? 4.0 : 0.0) + (e.t2 ? 2.0 : 0.0) : 4.0;
   launch(L, "hf_hgemm_rfwd", hf_hgemm_rfwd, 0, s, e, mnk(s) * s.nseg,
-         io(s, s.nseg, s.nseg, e.hidden ? 10.0 : 4.0));
+         io(s, s.nseg, s.nseg, out));
 }
 void hgemm_bwd(const Launch& L, const GemmShapeH& s, const EpiH& e) {
   if (e.f2)

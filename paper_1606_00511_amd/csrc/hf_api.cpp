@@ -414,13 +414,13 @@ void plan(hf_ctx* c, int64_t Bplan, bool product_only = false) {
   }
   // Split-K scratch.  A weight gradient (d_l x d_{l-1}, K up to 2 B rows
   // over two segments) takes at most the splits that keep every split within
-  // 2,048 rows at that K, or, if the tile rule asked for more, fewer than
-  // 1,024 tiles of 128 x 128 worth of partials.  A batch-row GEMM splits only
-  // while its grid holds fewer than 512 tiles, so it too stays below 1,024
-  // tiles' worth (and below max_splits x B x the widest layer).  With this
-  // much scratch no split is cut short.  (The bf16 batch-row GEMMs do not
-  // split.)
-  constexpr size_t TILES_1024 = (size_t)1024 * 128 * 128;
+  // 2,048 rows at that K (bf16: fewer), or, if the tile rule asked for
+  // more, fewer than 1,024 tiles of 128 x 128 worth of partials (bf16: 512
+  // tiles of 256 x 256).  A batch-row GEMM splits only while its grid holds
+  // fewer than 512 tiles, so it too stays below 1,024 tiles' worth (and below
+  // max_splits x B x the widest layer).  With this much scratch no split is
+  // cut short.  (The bf16 batch-row GEMMs do not split.)
+  const size_t TILES_1024 = (size_t)1024 * 128 * 128 * (h ? 2 : 1);
   int dmax = 0;
   size_t wg = 0;
   for (int l = 1; l <= L; ++l) {
@@ -528,16 +528,23 @@ void trace_product(hf_ctx* c, int k, const float* v, const float* out,
 // split-K factor for a weight-gradient GEMM with the given tile count and
 // reduction length.  First, no split accumulates more than 2,048 rows in
 // fp32 (the weight gradients are batch means with heavy cancellation, and the
-// splits are combined in fixed order in the reduce kernel); then, enough
-// workgroups to cover the 256 compute units twice while every split keeps
-// at least 64 rows (4 K blocks: enough to fill the load pipeline; a few
-// workgroups with long K chains would leave most of the chip idle).
+// splits are combined in fixed order in the reduce kernel); with bf16
+// operands 8,192 rows, since their rounding (2^-9 relative per operand)
+// outweighs that of fp32 accumulation over 8,192 terms many times over.
+// Then, enough workgroups to cover the 256 compute units twice (fp32: 4
+// workgroups fit a CU), or once (bf16: its 256 x 256 tiles take one CU each,
+// so that each further round of workgroups adds an epilogue and partials
+// without adding MFMA throughput), while every split keeps at least 64 rows
+// (4 K blocks: enough to fill the load pipeline; a few workgroups with long K
+// chains would leave most of the chip idle).
 int choose_splits(const hf_ctx* c, int M, int N, int Ktot) {
-  const int ts = c->bf16() ? 128 : gemm_tile(M, N, Ktot);
+  const bool h = c->bf16();
+  const int ts = h ? 256 : gemm_tile(M, N, Ktot);
   const int tiles = ((M + ts - 1) / ts) * ((N + ts - 1) / ts);
+  const int chain = h ? 8192 : 2048, cover = h ? 256 : 512;
   int s = 1;
-  while (s < c->max_splits && (Ktot + s - 1) / s > 2048) s *= 2;
-  while (s < c->max_splits && tiles * s < 512 && Ktot / (2 * s) >= 64) s *= 2;
+  while (s < c->max_splits && (Ktot + s - 1) / s > chain) s *= 2;
+  while (s < c->max_splits && tiles * s < cover && Ktot / (2 * s) >= 64) s *= 2;
   // the scratch is sized so that this never applies; it keeps the partials
   // in bounds regardless
   while (s > 1 && (size_t)s * M * N > c->split_floats) s /= 2;
@@ -998,11 +1005,15 @@ void product_cached_h(hf_ctx* c, int B, const float* v, int mode, float* out,
                  c->ldh[l - 1], c->ldh[l - 1], 2, skip);
     EpiH e = epih(c, l < L);
     e.rbias = v + c->offB[l];
-    e.f1 = c->F(c->oRZ[l]);
+    // RZ_l is read by the softmax R-op (l = L) and by the Hessian's
+    // R-backward, the transposed RA_l only by the Hessian's weight gradient:
+    // the Gauss-Newton product stores RA_l of a hidden layer row-major only
+    const bool hess = mode == HF_HESSIAN;
+    e.f1 = (l == L || hess) ? c->F(c->oRZ[l]) : nullptr;
     e.ldf = c->ld[l];
     if (l < L) {
       e.h2 = c->H(c->hRA[l]);
-      e.t2 = c->H(c->hRAT[l]);
+      e.t2 = hess ? c->H(c->hRAT[l]) : nullptr;
       e.a0 = c->H(c->hA[l]);
       e.ldo = c->ldh[l];
     }
@@ -1032,13 +1043,15 @@ void hvp_h(hf_ctx* c, const float* W, const float* X, const int32_t* y, int B,
     EpiH e = epih(c, l < L);
     e.bias = W + c->offB[l];
     e.rbias = v + c->offB[l];
-    e.f1 = c->F(c->oRZ[l]);
+    // as in the cached product: RZ_l and the transposed RA_l of a hidden
+    // layer only for the Hessian
+    e.f1 = (l == L || hess) ? c->F(c->oRZ[l]) : nullptr;
     e.ldf = c->ld[l];
     if (l < L) {
       e.h0 = c->H(c->hA[l]);
       e.t0 = c->H(c->hAT[l]);
       e.h2 = c->H(c->hRA[l]);
-      e.t2 = c->H(c->hRAT[l]);
+      e.t2 = hess ? c->H(c->hRAT[l]) : nullptr;
       e.ldo = c->ldh[l];
     } else {
       e.f0 = c->F(c->oZ);

@@ -279,7 +279,9 @@ struct EpiH {
 // the outputs placed as follows:
 //   fwd        hidden: A -> h0/t0; output layer: logits -> f0
 //   fwd_rfwd   RZ -> f1; hidden: A -> h0/t0, RA -> h2/t2; output: logits -> f0
-//   rfwd       RZ -> f1; hidden: RA = phi'(a0) RZ -> h2/t2
+//              (f1 and t2 may be null for a hidden layer, as for rfwd)
+//   rfwd       RZ -> f1; hidden: RA = phi'(a0) RZ -> h2/t2 (f1 and t2 may
+//              be null for a hidden layer: neither is then stored)
 //   bwd        delta -> h0/t0; if f2: E phi''(a0) -> f2
 //   bwd_rbwd   delta -> h0/t0, Rdelta -> h1/t1
 //   rbwd       Rdelta = acc phi'(a0) + a2 a1 -> h1/t1
