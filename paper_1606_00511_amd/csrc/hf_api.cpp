@@ -826,8 +826,9 @@ void product_cached(hf_ctx* c, const float* W, const float* X, int B,
 // The same pass order as above with every GEMM operand a bf16 copy.  The
 // producing epilogues write each bf16 activation or delta twice: row-major
 // (the next forward or backward GEMM's operand) and transposed (the weight
-// gradient's batch-contiguous operand).  Softmax, RZ, the phi'' cache and
-// all reductions stay fp32.
+// gradient's batch-contiguous operand); RA, which only the Hessian's weight
+// gradient reads transposed, is stored once in a Gauss-Newton product.
+// Softmax, RZ, the phi'' cache and all reductions stay fp32.
 
 EpiH epih(const hf_ctx* c, int hidden) {
   EpiH e;

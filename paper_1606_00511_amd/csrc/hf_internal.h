@@ -252,8 +252,8 @@ struct GemmShapeH {
 };
 
 // Epilogue arguments of the bf16-input kernels.  A bf16 result is written
-// twice: row-major to h* (leading dimension ldo) and transposed to t*
-// (t[col * ldt + row]), the batch-contiguous copy the weight gradient
+// row-major to h* (leading dimension ldo) and, where t* is given, transposed
+// to t* (t[col * ldt + row]), the batch-contiguous copy the weight gradient
 // contracts over; t* also gets zeros in rows M .. (M rounded up to 64).
 // fp32 results (logits, RZ, the phi'' cache, weight gradients) go to f*
 // with leading dimension ldf.  Aux buffers must have rows up to M rounded
