@@ -855,11 +855,14 @@ GemmShapeH shapeh(int M, int N, int K, const bf16_t* x0, const bf16_t* x1,
 
 // bf16 copies of the weight blocks of a parameter-layout vector: W_l
 // row-major [d_l][ldh_{l-1}] and transposed [d_{l-1}][ldh_l]
+// (tr null: no transposed copy; a Gauss-Newton product's direction V is
+// read only row-major, by the R-forward)
 void weights_h(hf_ctx* c, const float* v, const std::vector<size_t>& row,
-               const std::vector<size_t>& tr, const int* skip) {
+               const std::vector<size_t>* tr, const int* skip) {
   for (int l = 1; l <= c->L; ++l)
     cvt_bf16(c->launch(), v + c->offW[l], c->d[l], c->d[l - 1], c->d[l - 1],
-             c->H(row[l]), c->ldh[l - 1], c->H(tr[l]), c->ldh[l], c->ldh[l], skip);
+             c->H(row[l]), c->ldh[l - 1], tr ? c->H((*tr)[l]) : nullptr, c->ldh[l],
+             c->ldh[l], skip);
 }
 
 // bf16 copies of the input rows: X [B][ldh_0] and X^T [d_0][ldB]
@@ -911,7 +914,7 @@ void forward_plain_h(hf_ctx* c, const float* W, const float* X, int B,
   const Launch Lc = c->launch();
   const int L = c->L;
   input_h(c, X, B);
-  weights_h(c, W, c->hW, c->hWT, nullptr);
+  weights_h(c, W, c->hW, &c->hWT, nullptr);
   for (int l = 1; l <= L; ++l) {
     GemmShapeH s = shapeh(B, c->d[l], c->d[l - 1], act_h(c, l - 1), nullptr,
                           c->H(c->hW[l]), nullptr, c->ldh[l - 1], c->ldh[l - 1],
@@ -994,7 +997,7 @@ void product_cached_h(hf_ctx* c, int B, const float* v, int mode, float* out,
                       const int* skip) {
   const Launch Lc = c->launch();
   const int L = c->L;
-  weights_h(c, v, c->hV, c->hVT, skip);
+  weights_h(c, v, c->hV, mode == HF_HESSIAN ? &c->hVT : nullptr, skip);
   for (int l = 1; l <= L; ++l) {
     GemmShapeH s;
     if (l == 1)
@@ -1034,8 +1037,8 @@ void hvp_h(hf_ctx* c, const float* W, const float* X, const int32_t* y, int B,
   const int L = c->L;
   const bool hess = mode == HF_HESSIAN;
   input_h(c, X, B);
-  weights_h(c, W, c->hW, c->hWT, nullptr);
-  weights_h(c, v, c->hV, c->hVT, nullptr);
+  weights_h(c, W, c->hW, &c->hWT, nullptr);
+  weights_h(c, v, c->hV, hess ? &c->hVT : nullptr, nullptr);
   for (int l = 1; l <= L; ++l) {
     const int ldk = c->ldh[l - 1];
     GemmShapeH s = shapeh(B, c->d[l], c->d[l - 1], act_h(c, l - 1),
