@@ -867,11 +867,14 @@ HF_HGEMM_KERNEL(hf_hgemm_wgrad, 0, EStore, true, S)
 // = the same value for r < R, zero for R <= r < Rpad (the K padding a later
 // GEMM reads), for c < C; through a padded 32 x 32 LDS tile so that the
 // reads and both writes are coalesced.  Either output may be null.
-extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16(
-    const float* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ out,
-    int ldo, bf16_t* __restrict__ outT, int ldt, int Rpad,
-    const int* __restrict__ skip) {
-  if (skip && *skip) return;
+namespace {
+__device__ __forceinline__ bf16_t to_bf16(float v) { return f2bf(v); }
+__device__ __forceinline__ bf16_t to_bf16(bf16_t v) { return v; }
+
+template <class IN>
+__device__ __forceinline__ void cvt_body(
+    const IN* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ out,
+    int ldo, bf16_t* __restrict__ outT, int ldt, int Rpad) {
   __shared__ bf16_t t[32][34];
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
   const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
@@ -880,7 +883,7 @@ extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16(
     const int r = r0 + ty + 8 * j, c = c0 + tx;
     bf16_t b = 0;
     if (r < R && c < C) {
-      b = f2bf(in[(size_t)r * ldi + c]);
+      b = to_bf16(in[(size_t)r * ldi + c]);
       if (out) out[(size_t)r * ldo + c] = b;
     }
     t[ty + 8 * j][tx] = b;
@@ -892,6 +895,24 @@ extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16(
     const int c = c0 + ty + 8 * j, r = r0 + tx;
     if (r < Rpad && c < C) outT[(size_t)c * ldt + r] = t[tx][ty + 8 * j];
   }
+}
+
+}  // namespace
+
+extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16(
+    const float* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ out,
+    int ldo, bf16_t* __restrict__ outT, int ldt, int Rpad,
+    const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  cvt_body(in, R, C, ldi, out, ldo, outT, ldt, Rpad);
+}
+
+// the transposed copy of a bf16 matrix (with zeros in the padding rows)
+extern "C" __global__ __launch_bounds__(256) void hf_transpose_bf16(
+    const bf16_t* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ outT,
+    int ldt, int Rpad, const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  cvt_body(in, R, C, ldi, (bf16_t*)nullptr, 0, outT, ldt, Rpad);
 }
 
 // p[i] = bf16(p[i]^2) for i < n: squares a bf16 operand in place (the
@@ -994,6 +1015,14 @@ void square_bf16(const Launch& L, bf16_t* p, long long n) {
   hipExtLaunchKernelGGL(hf_square_bf16, dim3((unsigned)nb), dim3(256), 0, L.stream,
                         prof_a(L), prof_b(L), 0, p, n);
   prof_end(L, "hf_square_bf16", 0.0, 4.0 * n);
+}
+void transpose_bf16(const Launch& L, const bf16_t* in, int R, int C, int ldi,
+                    bf16_t* outT, int ldt, int Rpad, const int* skip) {
+  if (Rpad < R) Rpad = R;
+  prof_begin(L, "hf_transpose_bf16");
+  hipExtLaunchKernelGGL(hf_transpose_bf16, dim3(cdiv(C, 32), cdiv(Rpad, 32)), dim3(256), 0,
+                        L.stream, prof_a(L), prof_b(L), 0, in, R, C, ldi, outT, ldt, Rpad, skip);
+  prof_end(L, "hf_transpose_bf16", 0.0, 4.0 * (double)R * C);
 }
 void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
               bf16_t* out, int ldo, bf16_t* outT, int ldt, int Rpad,

@@ -871,6 +871,17 @@ void input_h(hf_ctx* c, const float* X, int B) {
            c->H(c->hXT), c->ldB, round64(B), nullptr);
 }
 
+// Rdelta_L of a bf16-operand product: the softmax R-op writes its bf16
+// row-major copy, then the transposed copy is made from that (the fp32
+// Rdelta_L is not needed)
+void rop_h(hf_ctx* c, int B, const int* skip) {
+  const int L = c->L;
+  softmax_rop_h(c->launch(), c->F(c->oP), c->F(c->oRZ[L]), B, c->d[L], c->ld[L],
+                c->H(c->hRD[L]), c->ldh[L], skip);
+  transpose_bf16(c->launch(), c->H(c->hRD[L]), B, c->d[L], c->ldh[L], c->H(c->hRDT[L]),
+                 c->ldB, round64(B), skip);
+}
+
 // an fp32 output-layer delta (B x d_L, ld_L) to its two bf16 copies
 void delta_h(hf_ctx* c, const float* D, int B, size_t row, size_t tr,
              const int* skip) {
@@ -1023,9 +1034,7 @@ void product_cached_h(hf_ctx* c, int B, const float* v, int mode, float* out,
     }
     hgemm_rfwd(Lc, s, e);
   }
-  softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), B, c->d[L], c->ld[L],
-              c->F(c->oRD[L]), skip);
-  delta_h(c, c->F(c->oRD[L]), B, c->hRD[L], c->hRDT[L], skip);
+  rop_h(c, B, skip);
   for (int l = L; l >= 1; --l) rbackward_h(c, l, B, mode, false, out, skip);
 }
 
@@ -1066,9 +1075,7 @@ void hvp_h(hf_ctx* c, const float* W, const float* X, const int32_t* y, int B,
                c->F(c->oP), hess ? c->F(c->oD[L]) : nullptr, c->Dp(c->oLoss),
                c->errp());
   if (hess) delta_h(c, c->F(c->oD[L]), B, c->hD[L], c->hDT[L], nullptr);
-  softmax_rop(Lc, c->F(c->oP), c->F(c->oRZ[L]), B, c->d[L], c->ld[L],
-              c->F(c->oRD[L]), nullptr);
-  delta_h(c, c->F(c->oRD[L]), B, c->hRD[L], c->hRDT[L], nullptr);
+  rop_h(c, B, nullptr);
   for (int l = L; l >= 1; --l) rbackward_h(c, l, B, mode, true, out, nullptr);
 }
 

@@ -300,6 +300,10 @@ void hgemm_wgrad(const Launch& L, const GemmShapeH& s, const EpiH& e);
 void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
               bf16_t* out, int ldo, bf16_t* outT, int ldt, int Rpad,
               const int* skip);
+// outT[c * ldt + r] = in[r * ldi + c] for r < R, 0 for R <= r < Rpad (bf16
+// R x C in, its transposed copy out)
+void transpose_bf16(const Launch& L, const bf16_t* in, int R, int C, int ldi,
+                    bf16_t* outT, int ldt, int Rpad, const int* skip);
 // p[i] = bf16(p[i]^2), i < n, in place (p 16-byte aligned)
 void square_bf16(const Launch& L, bf16_t* p, long long n);
 
@@ -317,6 +321,10 @@ void loss_finalize(const Launch& L, const double* loss_part, int nparts,
 // Rdelta_L = P * (RZ - rowsum(P * RZ)) / B.
 void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
                  int C, int ld, float* RD, const int* skip);
+// The same written as bf16 (round to nearest even; leading dimension ldo),
+// columns below C only.
+void softmax_rop_h(const Launch& L, const float* P, const float* RZ, int B,
+                   int C, int ld, bf16_t* RD, int ldo, const int* skip);
 // Up to 16 row-major blocks transposed in one launch:
 // out[i][c * ldo[i] + r] = in[i][r * ldi[i] + c] (R[i] x C[i] -> C[i] x R[i]).
 struct TransposeBatch {

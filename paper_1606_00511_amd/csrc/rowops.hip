@@ -14,6 +14,7 @@
 // 64, ...); row reductions use wave shuffles.  Every sum runs in a fixed order, so repeated calls give
 // bit-identical results.
 #include <algorithm>
+#include <type_traits>
 
 #include "hf_internal.h"
 
@@ -138,10 +139,12 @@ extern "C" __global__ __launch_bounds__(256) void hf_loss_finalize(
 // waves in flight to cover the memory latency of this HBM-bound pass.  The
 // row sum runs in the same order as before (each lane's values in column
 // order, then the wave reduction).
-template <int KMAX>
+// OUT: float, or bf16_t (the bf16-operand products' row-major copy, rounded
+// to nearest even once from the same fp32 value)
+template <int KMAX, class OUT>
 __device__ __forceinline__ void softmax_rop_body(
     const float* __restrict__ P, const float* __restrict__ RZ, int B, int C,
-    int ld, float invB, float* __restrict__ RD) {
+    int ld, float invB, OUT* __restrict__ RD, int ldo) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = blockIdx.x * ROWS_PER_BLOCK + wave;
   if (row >= B) return;
@@ -159,11 +162,15 @@ __device__ __forceinline__ void softmax_rop_body(
   for (int k = 0; k < KMAX; ++k)
     if (lane + 64 * k < C) dot += p[k] * r[k];
   dot = wave_sum(dot);
-  float* out = RD + (size_t)row * ld;
+  OUT* out = RD + (size_t)row * ldo;
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) {
     const int c = lane + 64 * k;
-    if (c < C) out[c] = p[k] * (r[k] - dot) * invB;
+    if (c < C) {
+      const float v = p[k] * (r[k] - dot) * invB;
+      if constexpr (std::is_same<OUT, float>::value) out[c] = v;
+      else out[c] = __builtin_bit_cast(uint16_t, (__bf16)v);
+    }
   }
 }
 
@@ -172,7 +179,14 @@ __device__ __forceinline__ void softmax_rop_body(
       const float* __restrict__ P, const float* __restrict__ RZ, int B, int C,  \
       int ld, float invB, float* __restrict__ RD, const int* __restrict__ skip) { \
     if (skip && *skip) return;                                                  \
-    softmax_rop_body<K>(P, RZ, B, C, ld, invB, RD);                             \
+    softmax_rop_body<K, float>(P, RZ, B, C, ld, invB, RD, ld);                  \
+  }                                                                             \
+  extern "C" __global__ __launch_bounds__(256) void hf_softmax_rop_h_k##K(      \
+      const float* __restrict__ P, const float* __restrict__ RZ, int B, int C,  \
+      int ld, float invB, bf16_t* __restrict__ RD, int ldo,                     \
+      const int* __restrict__ skip) {                                           \
+    if (skip && *skip) return;                                                  \
+    softmax_rop_body<K, bf16_t>(P, RZ, B, C, ld, invB, RD, ldo);                \
   }
 HF_SOFTMAX_ROP(4)
 HF_SOFTMAX_ROP(8)
@@ -316,6 +330,20 @@ void softmax_rop(const Launch& L, const float* P, const float* RZ, int B,
   hipExtLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0, P, RZ, B, C, ld,
                      1.0f / (float)B, RD, skip);
   prof_end(L, "hf_softmax_rop", 0.0, 12.0 * B * C);
+}
+
+void softmax_rop_h(const Launch& L, const float* P, const float* RZ, int B,
+                   int C, int ld, bf16_t* RD, int ldo, const int* skip) {
+  const int blocks = (B + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK;
+  typedef void (*K)(const float*, const float*, int, int, int, float, bf16_t*, int,
+                    const int*);
+  const K k = C <= 256 ? hf_softmax_rop_h_k4 : C <= 512 ? hf_softmax_rop_h_k8
+            : C <= 1024 ? hf_softmax_rop_h_k16 : C <= 2048 ? hf_softmax_rop_h_k32
+            : hf_softmax_rop_h_k64;
+  prof_begin(L, "hf_softmax_rop");
+  hipExtLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, L.stream, prof_a(L), prof_b(L), 0, P, RZ, B, C, ld,
+                     1.0f / (float)B, RD, ldo, skip);
+  prof_end(L, "hf_softmax_rop", 0.0, 10.0 * B * C);
 }
 
 void transpose_batch(const Launch& L, const TransposeBatch& b, const int* skip) {
