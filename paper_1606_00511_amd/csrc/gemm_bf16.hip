@@ -907,6 +907,28 @@ extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16(
   cvt_body(in, R, C, ldi, out, ldo, outT, ldt, Rpad);
 }
 
+// Row-major copy only, 8 elements per thread and step (two 16-byte loads,
+// one 16-byte store); C a multiple of 8, in and out 16-byte aligned, ldi a
+// multiple of 4 and ldo of 8.
+extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16_rows(
+    const float* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ out,
+    int ldo, const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  const int cpr = C >> 3;
+  const long long n = (long long)R * cpr;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < n;
+       i += (long long)gridDim.x * 256) {
+    const int r = (int)(i / cpr), c = 8 * (int)(i - (long long)r * cpr);
+    const float4 a = *(const float4*)(in + (size_t)r * ldi + c);
+    const float4 b = *(const float4*)(in + (size_t)r * ldi + c + 4);
+    const uint32_t w0 = (uint32_t)f2bf(a.x) | ((uint32_t)f2bf(a.y) << 16);
+    const uint32_t w1 = (uint32_t)f2bf(a.z) | ((uint32_t)f2bf(a.w) << 16);
+    const uint32_t w2 = (uint32_t)f2bf(b.x) | ((uint32_t)f2bf(b.y) << 16);
+    const uint32_t w3 = (uint32_t)f2bf(b.z) | ((uint32_t)f2bf(b.w) << 16);
+    *(uint4*)(out + (size_t)r * ldo + c) = make_uint4(w0, w1, w2, w3);
+  }
+}
+
 // the transposed copy of a bf16 matrix (with zeros in the padding rows)
 extern "C" __global__ __launch_bounds__(256) void hf_transpose_bf16(
     const bf16_t* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ outT,
@@ -1027,6 +1049,17 @@ void transpose_bf16(const Launch& L, const bf16_t* in, int R, int C, int ldi,
 void cvt_bf16(const Launch& L, const float* in, int R, int C, int ldi,
               bf16_t* out, int ldo, bf16_t* outT, int ldt, int Rpad,
               const int* skip) {
+  if (out && !outT && C % 8 == 0 && ldi % 4 == 0 && ldo % 8 == 0 &&
+      ((uintptr_t)in & 15u) == 0 && ((uintptr_t)out & 15u) == 0) {
+    const long long n = (long long)R * (C / 8);
+    const long long nb = std::min<long long>((n + 255) / 256, 2048);
+    if (nb < 1) return;
+    prof_begin(L, "hf_cvt_bf16");
+    hipExtLaunchKernelGGL(hf_cvt_bf16_rows, dim3((unsigned)nb), dim3(256), 0, L.stream,
+                          prof_a(L), prof_b(L), 0, in, R, C, ldi, out, ldo, skip);
+    prof_end(L, "hf_cvt_bf16", 0.0, 6.0 * (double)R * C);
+    return;
+  }
   if (Rpad < R) Rpad = R;
   prof_begin(L, "hf_cvt_bf16");
   hipExtLaunchKernelGGL(hf_cvt_bf16, dim3(cdiv(C, 32), cdiv(Rpad, 32)), dim3(256), 0,
