@@ -174,13 +174,26 @@ def test_bf16_full_loss_grad(name):
 @pytest.mark.parametrize("mode", ["hessian", "gauss_newton"])
 @pytest.mark.parametrize("name", SPEECH)
 def test_bf16_full_product(name, mode):
+    """The stateless product at full size.  Where 256 x 256 tiles of the
+    first layer cover the 256 CUs (16,384 rows here) it takes the cached
+    route (the forward pass of a solve, then its product); at fewer rows the
+    fused forward / R-forward kernels."""
     st = setup(name)
     w, inp = st["w"], st["inp"]
-    out = st["net"].hf_hvp(st["W"], st["Xc"], st["yc"], st["v"], mode)
+    net = st["net"]
+    net.prof_enable(True)
+    net.prof_reset()
+    out = net.hf_hvp(st["W"], st["Xc"], st["yc"], st["v"], mode)
+    host(out)
+    stats = net.prof_stats()
+    net.prof_enable(False)
+    cached = (w.curv_batch // 256) * (w.dims[1] // 256) >= 256
+    assert ("hf_hgemm_rfwd" in stats) == cached, sorted(stats)
+    assert ("hf_hgemm_fwd_rfwd" in stats) != cached, sorted(stats)
     ref = O.curvature(w.dims, w.act, inp["theta"], inp["X"][:w.curv_batch],
                       inp["y"][:w.curv_batch], inp["v"], mode)
     err = rel(host(out), ref)
-    print("%s %s rel %.2e" % (name, mode, err))
+    print("%s %s rel %.2e (%s route)" % (name, mode, err, "cached" if cached else "fused"))
     assert err <= TOL
 
 

@@ -182,11 +182,12 @@ def test_narrow_loss_only(case):
     net.close()
 
 
+@pytest.mark.parametrize("solver", ["cg", "bicgstab"])
 @pytest.mark.parametrize("curvature", ["hessian", "gauss_newton"])
 @pytest.mark.parametrize("case", [((64, 100, 10), "sigmoid", 200),
                                   ((96, 40, 30, 17), "tanh", 77)],
                          ids=["64x100x10-sigmoid-b200", "96x40x30x17-tanh-b77"])
-def test_narrow_iterate(case, curvature):
+def test_narrow_iterate(case, curvature, solver):
     """One outer iteration (gradient, solve, line search, damping product)
     on a narrow net against the oracle's, with the bar of the other outer
     iteration tests; every pass runs in the narrow kernels (no forward GEMM
@@ -196,9 +197,9 @@ def test_narrow_iterate(case, curvature):
     dims, act, B = case
     p = WL.make_small(dims, act, B, seed=6700 + B)
     th = p["theta"].astype(np.float64)
-    kw = dict(solver="cg", curvature=curvature, damping=1e-2, max_iters=6,
+    kw = dict(solver=solver, curvature=curvature, damping=1e-2, max_iters=6,
               adapt_damping=True)
-    o = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver="cg",
+    o = O.iterate(dims, act, th, p["X"], p["y"], p["X"], p["y"], solver=solver,
                   curvature_kind=curvature, lam=1e-2, max_iters=6,
                   damping_adapt=True)
     net = HFNet(dims, act, B)
@@ -209,15 +210,17 @@ def test_narrow_iterate(case, curvature):
     gi, _, _ = compare_step(net, dims, act, p, th, delta, kw, 0, o, W)
     stats = net.prof_stats()
     net.prof_enable(False)
-    print("%s %s: dir %d alpha %g evals %d f %.6f -> %.6f (oracle %.6f) rho "
-          "%.4f/%.4f" % (sid(case), curvature, gi["direction"], gi["alpha"],
+    print("%s %s %s: dir %d alpha %g evals %d f %.6f -> %.6f (oracle %.6f) rho "
+          "%.4f/%.4f" % (sid(case), curvature, solver, gi["direction"], gi["alpha"],
                          gi["evals"], gi["f0"], gi["f1"], o["f1"], gi["rho"],
                          o["rho"]))
     assert stats["hf_narrow_forward4"]["launches"] >= gi["evals"] + 2, stats
     assert not any(k.startswith("hf_gemm_fwd") or k.startswith("hf_softmax")
                    for k in stats), sorted(stats)
-    if gi["accepted"] and o["accepted"] and gi["alpha"] == o["alpha"] and \
-            gi["direction"] == o["direction"]:
+    # (Bi-CG-STAB's step can move by its rounding sensitivity, which
+    # compare_step allows for; rho is compared for CG)
+    if solver == "cg" and gi["accepted"] and o["accepted"] and \
+            gi["alpha"] == o["alpha"] and gi["direction"] == o["direction"]:
         assert gi["rho"] == pytest.approx(o["rho"], rel=1e-2)
         if min(abs(o["rho"] - 0.25), abs(o["rho"] - 0.75)) > 1e-2:
             assert gi["damping_next"] == pytest.approx(o["lam_next"], rel=1e-6)
