@@ -929,6 +929,51 @@ extern "C" __global__ __launch_bounds__(256) void hf_cvt_bf16_rows(
   }
 }
 
+// The transposed copy of a bf16 matrix (zeros in the padding rows) in
+// 64 x 64 tiles with 16-byte loads and stores: in and outT 16-byte aligned,
+// ldi and ldt multiples of 8, Rpad a multiple of 8.  A thread loads 8
+// consecutive columns of a row (element by element past C) and stores 8
+// consecutive rows of a column.
+extern "C" __global__ __launch_bounds__(256) void hf_transpose_bf16_v(
+    const bf16_t* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ outT,
+    int ldt, int Rpad, const int* __restrict__ skip) {
+  if (skip && *skip) return;
+  __shared__ __attribute__((aligned(16))) bf16_t t[64][72];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int q = threadIdx.x + 256 * h;
+    const int rr = q >> 3, cc = (q & 7) * 8;
+    const int r = r0 + rr, c = c0 + cc;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (r < R) {
+      const bf16_t* src = in + (size_t)r * ldi + c;
+      if (c + 8 <= C) {
+        v = *(const u32x4*)src;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (c + j < C) v[j >> 1] |= (uint32_t)src[j] << (16 * (j & 1));
+      }
+    }
+    *(u32x4*)&t[rr][cc] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int q = threadIdx.x + 256 * h;
+    const int cc = q >> 3, rr = (q & 7) * 8;
+    const int c = c0 + cc, r = r0 + rr;
+    if (c < C && r < Rpad) {
+      u32x4 w;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w[j] = (uint32_t)t[rr + 2 * j][cc] | ((uint32_t)t[rr + 2 * j + 1][cc] << 16);
+      *(u32x4*)(outT + (size_t)c * ldt + r) = w;
+    }
+  }
+}
+
 // the transposed copy of a bf16 matrix (with zeros in the padding rows)
 extern "C" __global__ __launch_bounds__(256) void hf_transpose_bf16(
     const bf16_t* __restrict__ in, int R, int C, int ldi, bf16_t* __restrict__ outT,
@@ -1041,6 +1086,15 @@ void square_bf16(const Launch& L, bf16_t* p, long long n) {
 void transpose_bf16(const Launch& L, const bf16_t* in, int R, int C, int ldi,
                     bf16_t* outT, int ldt, int Rpad, const int* skip) {
   if (Rpad < R) Rpad = R;
+  if (ldi % 8 == 0 && ldt % 8 == 0 && Rpad % 8 == 0 && ((uintptr_t)in & 15u) == 0 &&
+      ((uintptr_t)outT & 15u) == 0) {
+    prof_begin(L, "hf_transpose_bf16");
+    hipExtLaunchKernelGGL(hf_transpose_bf16_v, dim3(cdiv(C, 64), cdiv(Rpad, 64)), dim3(256), 0,
+                          L.stream, prof_a(L), prof_b(L), 0, in, R, C, ldi, outT, ldt, Rpad,
+                          skip);
+    prof_end(L, "hf_transpose_bf16", 0.0, 4.0 * (double)R * C);
+    return;
+  }
   prof_begin(L, "hf_transpose_bf16");
   hipExtLaunchKernelGGL(hf_transpose_bf16, dim3(cdiv(C, 32), cdiv(Rpad, 32)), dim3(256), 0,
                         L.stream, prof_a(L), prof_b(L), 0, in, R, C, ldi, outT, ldt, Rpad, skip);
